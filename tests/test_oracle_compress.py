@@ -1,0 +1,155 @@
+"""Pins for the oracle's Algorithm 1 (Sec. 3.2 Steps 1-4) and the Eq. 3
+error statement (Sec. 3.3, App. A)."""
+
+import os
+
+import numpy as np
+import pytest
+
+from oracle import codebook as cb
+from oracle import compress as cz
+from oracle import rotation as rot
+from paper_2608_08081_amd import synth
+
+LEVELS, THR = cb.isoquant_codebook(128, 3)
+
+
+def _brute_nearest(y):
+    """argmin_k |y - C_k| over the stored levels in exact rational
+    arithmetic, ties to the higher index."""
+    from fractions import Fraction
+    yf = Fraction(float(y))
+    best, best_d = 0, None
+    for k, c in enumerate(LEVELS):
+        dist = abs(yf - Fraction(float(c)))
+        if best_d is None or dist <= best_d:
+            best, best_d = k, dist
+    return best
+
+
+def _enumerated_inputs():
+    pts = [0.0, -0.0, 1.0, -1.0, 0.5, -0.5]
+    for t in THR:
+        x = float(t)
+        pts.append(x)
+        up, dn = x, x
+        for _ in range(2):
+            up = np.nextafter(up, np.inf)
+            dn = np.nextafter(dn, -np.inf)
+            pts += [up, dn]
+    for c in LEVELS:
+        pts.append(float(c))
+    pts += list(np.linspace(-0.3, 0.3, 6001))
+    return pts
+
+
+def test_quantizer_matches_brute_force_nearest_level():
+    pts = _enumerated_inputs()
+    got = cz.quantize(np.array(pts), THR)
+    want = [_brute_nearest(y) for y in pts]
+    assert list(got) == want
+    # -0.0 is treated as 0 (code 4), and the zero coordinate is code 4
+    assert cz.quantize(np.array([-0.0, 0.0]), THR).tolist() == [4, 4]
+
+
+def test_pack_bit_positions_brute_force():
+    """Setting bit b of code i sets exactly bit 3i + b of the record."""
+    for i in range(128):
+        for b in range(3):
+            codes = np.zeros(128, np.uint8)
+            codes[i] = 1 << b
+            rec = cz.pack(codes)
+            assert rec.shape == (48,)
+            bits = [(int(rec[n // 8]) >> (n % 8)) & 1 for n in range(384)]
+            assert sum(bits) == 1 and bits[3 * i + b] == 1
+
+
+def test_pack_round_trip():
+    g = np.random.default_rng(0)
+    codes = g.integers(0, 8, size=(33, 128), dtype=np.uint8)
+    packed = cz.pack(codes)
+    assert packed.shape == (33, 48)
+    assert np.array_equal(cz.unpack(packed), codes)
+
+
+def test_worked_packing_example(golden_dir):
+    """x = e_0 with identity SO(4) parameters (hand derivation in the
+    fixture)."""
+    fixture = {}
+    with open(os.path.join(golden_dir, "pack_e0_identity.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                k, *v = line.split()
+                fixture[k] = v
+    x = np.zeros((1, 128), np.float32)
+    x[0, 0] = 1.0
+    r = rot.rotation_matrix(rot.identity_quaternions(1)[0])
+    packed, norm, codes, y, _ = cz.compress(x, r, THR)
+    assert norm[0] == np.float32(fixture["norm"][0])
+    assert np.all(codes == int(fixture["code"][0]))
+    np.testing.assert_allclose(y, 1 / np.sqrt(128), atol=1e-16)
+    want = bytes(int(b, 16) for b in fixture["bytes"]) * 16
+    assert packed[0].tobytes() == want
+
+
+def test_norm_is_rounded_fp64_norm_and_zero_vector():
+    g = np.random.default_rng(1)
+    x = (g.standard_normal((64, 128)) * 3).astype(np.float16)
+    x[5] = 0
+    r = rot.rotation_matrix(rot.make_quaternions(3, 1)[0])
+    packed, norm, codes, y, s64 = cz.compress(x, r, THR)
+    # fp16 squares are exact in fp64 and so is their sum: compare with an
+    # exact rational computation
+    from fractions import Fraction
+    for i in (0, 7, 33):
+        ss = sum(Fraction(float(v)) ** 2 for v in x[i])
+        assert abs(float(ss) - s64[i] ** 2) <= 2 ** -50 * float(ss)
+    assert norm.dtype == np.float32
+    assert np.array_equal(norm, s64.astype(np.float32))
+    assert norm[5] == 0 and np.all(codes[5] == 4)
+
+
+def test_compress_reconstruction_distortion():
+    """Mean relative squared error of the 3-bit reconstruction: about the
+    codebook's per-coordinate MSE times d (~0.034) for isotropic inputs,
+    similar for anisotropic inputs after the rotation, and far worse without
+    any rotation (the role of the isotropizing rotation, Sec. 3.2)."""
+    g = np.random.default_rng(2)
+    d = 128
+    model = cb.SphereMarginalModel(d)
+    mse_d = d * cb.distortion(model, LEVELS, THR)
+    r = rot.rotation_matrix(rot.make_quaternions(7, 1)[0])
+
+    def rel_err(x, rr):
+        _, norm, codes, _, _ = cz.compress(x, rr, THR)
+        xr = cz.reconstruct(codes, norm, LEVELS, rr)
+        return np.mean(np.sum((xr - x) ** 2, axis=1) / np.sum(x.astype(np.float64) ** 2, axis=1))
+
+    iso = g.standard_normal((4000, d))
+    assert abs(rel_err(iso, r) - mse_d) < 0.002
+    w = synth.WORKLOADS[0]
+    aniso = synth.kv_tensor(11, w, "k", n_tokens=4000)[0, 0].astype(np.float64)
+    e_rot = rel_err(aniso, r)
+    e_none = rel_err(aniso, np.eye(d))
+    assert e_rot < 0.05
+    assert e_none > 5 * e_rot
+
+
+def test_eq3_inner_product_error_statement():
+    """Eq. 3 / App. A: with per-coordinate quantization noise of variance
+    sigma^2, E|q.k - q.k_hat|^2 = sigma^2 ||q||^2 (derived form), which is
+    within the stated bound d sigma^2 ||q||^2.  Checked on unit keys, where
+    sigma^2 is the codebook's per-coordinate MSE."""
+    g = np.random.default_rng(3)
+    d = 128
+    sigma2 = cb.distortion(cb.SphereMarginalModel(d), LEVELS, THR)
+    r = rot.rotation_matrix(rot.make_quaternions(8, 1)[0])
+    k = g.standard_normal((20000, d))
+    k /= np.linalg.norm(k, axis=1, keepdims=True)
+    q = g.standard_normal(d)
+    _, norm, codes, _, _ = cz.compress(k, r, THR)
+    k_hat = cz.reconstruct(codes, norm, LEVELS, r)
+    err2 = np.mean((k @ q - k_hat @ q) ** 2)
+    derived = sigma2 * np.dot(q, q)
+    assert 0.8 * derived < err2 < 1.2 * derived
+    assert err2 <= d * sigma2 * np.dot(q, q)
