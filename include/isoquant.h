@@ -1,0 +1,199 @@
+/*
+ * isoquant.h - C ABI of libisoquant: IsoQuant 3-bit KV-cache compression and
+ * decode attention computed directly on the packed cache, for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * Method: arXiv 2608.08081, "RotaryQuant: Fitting 120B MoE Models on Consumer
+ * Hardware via Fused Compressed-Space Attention".  Citations below name the
+ * paper's sections, equations, algorithms and tables.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - head_dim must be 128 and the code width is 3 bits (the configuration of
+ *   Sec. 3.2 Step 4); anything else returns IQ_ERR_UNSUPPORTED.
+ * - Device pointers are plain HIP device allocations owned by the caller.
+ *   The library never allocates, frees or retains device memory and keeps no
+ *   mutable global state (the codebook is an immutable constant computed once
+ *   per process on first use), so calls are thread-safe.
+ * - Every device entry point is asynchronous on `stream` (0 = the null
+ *   stream) and never synchronizes.  Arguments are validated on the host
+ *   before any HIP call; on a validation error nothing is launched.
+ * - A failed kernel launch returns IQ_ERR_HIP.  Device-side faults surface,
+ *   as usual in HIP, at the caller's next synchronizing call.
+ *
+ * Cache layout (one layer)
+ * ------------------------
+ * codes  : uint8 [batch][n_kv_heads][capacity][48]   one record per token
+ * norms  : fp32  [batch][n_kv_heads][capacity]        per-token scale s
+ * Keys and values use separate, identically laid out arrays.  Record format
+ * (the paper fixes only "48 bytes per 128-dim vector", Sec. 3.2 Step 4): code
+ * i of the vector occupies bits 3i..3i+2 of the record read as a
+ * little-endian bit string (bit n = bit n%8 of byte n/8), LSB first.  Codes
+ * number the codebook levels in ascending order.
+ * Rotation parameters: fp32 [n_kv_heads][32][2][4]: per SO(4) block the pair
+ * (q_L, q_R), each quaternion as (w, x, y, z), 256 floats per head (App. B).
+ */
+#ifndef ISOQUANT_H_
+#define ISOQUANT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define IQ_HEAD_DIM 128
+#define IQ_BITS 3
+#define IQ_LEVELS 8
+#define IQ_RECORD_BYTES 48
+#define IQ_PARAMS_PER_HEAD 256
+
+typedef enum iq_status {
+  IQ_OK = 0,
+  IQ_ERR_INVALID_ARGUMENT = 1,   /* null/misaligned pointer, bad size, range */
+  IQ_ERR_UNSUPPORTED = 2,        /* head_dim != 128, unknown dtype, group > 16 */
+  IQ_ERR_WORKSPACE_TOO_SMALL = 3,
+  IQ_ERR_HIP = 4,                /* a HIP runtime call or launch failed */
+  IQ_ERR_CAPACITY = 5            /* written to status_dev by iq_append_token */
+} iq_status;
+
+typedef enum iq_dtype {
+  IQ_DTYPE_F32 = 0,
+  IQ_DTYPE_F16 = 1
+} iq_dtype;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* iq_status_string(iq_status s);
+
+/* ABI version of this header (major * 100 + minor). */
+int iq_version(void);
+
+/*
+ * iq_codebook - the 3-bit Lloyd-Max codebook C_b (Sec. 3.2 Step 3).
+ * Levels minimize expected squared error for one coordinate of a unit vector
+ * spread uniformly over the sphere S^127 (density proportional to
+ * (1 - t^2)^62.5), each rounded to the nearest fp16 value; thresholds are
+ * the midpoints of adjacent stored levels.  Host memory out:
+ * levels[8] ascending, thresholds[7] ascending.  Either pointer may be NULL.
+ */
+iq_status iq_codebook(float* levels, float* thresholds);
+
+/*
+ * iq_make_rotation - seeded SO(4) parameters for n_kv_heads heads (Sec. 3.3
+ * "SO(4) parameterization", App. B).  Host memory out:
+ * quats_host[n_kv_heads][32][2][4].  Each unit quaternion is drawn from one
+ * SplitMix64 stream seeded with `seed`, in the order head, block, q_L then
+ * q_R: four draws (top 53 bits * 2^-53, mapped to [-1, 1)) rejected unless
+ * the squared norm lies in (1e-6, 1], divided by the norm in fp64, rounded to
+ * fp32.  Pure host function (no HIP call).
+ */
+iq_status iq_make_rotation(uint64_t seed, int64_t n_kv_heads, int64_t head_dim,
+                           float* quats_host);
+
+/*
+ * iq_compress_kv - Algorithm 1 (Sec. 3.2 Steps 1-4) over a block of tokens:
+ * for every vector x: s = ||x||_2 (accumulated in fp64, stored as fp32),
+ * x_tilde = R_SO(4)(H_128 x / s) (Eq. 2), each coordinate replaced by the
+ * index of its nearest codebook level, codes bit-packed into a 48-byte
+ * record.  This is the deferred bulk compression at the prefill-to-decode
+ * boundary (Sec. 3.4 "Deferred prefill", App. C).
+ *
+ * k, v        : device, [batch][n_kv_heads][n_tokens][128] of `dtype`,
+ *               16-byte aligned.  Either side may be NULL together with its
+ *               outputs (compress keys only / values only); not both.
+ * quats       : device fp32 [n_kv_heads][32][2][4] (one rotation per KV head,
+ *               shared by keys, values and the query heads of the group).
+ * k_codes/v_codes : device uint8 [batch][n_kv_heads][capacity][48], 16-byte
+ *               aligned.  k_norms/v_norms: device fp32 [batch][n_kv_heads][capacity].
+ * Token t of the input is written at cache position dst_offset + t.
+ * Requires 0 <= dst_offset and dst_offset + n_tokens <= capacity.
+ * n_tokens == 0 or batch == 0 is a valid no-op.
+ */
+iq_status iq_compress_kv(const void* k, const void* v, iq_dtype dtype,
+                         int64_t batch, int64_t n_kv_heads, int64_t n_tokens,
+                         int64_t head_dim, const float* quats,
+                         uint8_t* k_codes, float* k_norms,
+                         uint8_t* v_codes, float* v_norms,
+                         int64_t capacity, int64_t dst_offset, hipStream_t stream);
+
+/*
+ * iq_append_token - per-step compression of one new token per sequence
+ * (Alg. 1 applied to the decode step's new key and value; the paper's
+ * packed-cache write of App. D, done in place).
+ *
+ * k_new, v_new : device [batch][n_kv_heads][128] of `dtype` (either may be
+ *                NULL with its cache arrays, not both).
+ * seq_lens     : device int32 [batch], read and updated in place: the token of
+ *                sequence b is written at position seq_lens[b], then
+ *                seq_lens[b] is incremented.
+ * status_dev   : optional device int32; if sequence b is already at capacity
+ *                its token is dropped, seq_lens[b] is left unchanged and
+ *                IQ_ERR_CAPACITY is OR-ed into *status_dev.  Never cleared by
+ *                the library.
+ */
+iq_status iq_append_token(const void* k_new, const void* v_new, iq_dtype dtype,
+                          int64_t batch, int64_t n_kv_heads, int64_t head_dim,
+                          const float* quats,
+                          uint8_t* k_codes, float* k_norms,
+                          uint8_t* v_codes, float* v_norms,
+                          int64_t capacity, int32_t* seq_lens, int32_t* status_dev,
+                          hipStream_t stream);
+
+/*
+ * iq_decode_workspace_bytes - size of the device workspace iq_decode_attention
+ * needs for these shapes (split-K partial results and combine tickets).
+ * Returns 0 for invalid shapes.
+ */
+size_t iq_decode_workspace_bytes(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                                 int64_t max_seq_len, int64_t head_dim);
+
+/*
+ * iq_decode_workspace_init - zero-fill a workspace before its first use with
+ * iq_decode_attention (a fill kernel on `stream`, safe under graph capture).
+ * iq_decode_attention leaves the workspace in that state again when it
+ * completes, so one init per allocation suffices.
+ */
+iq_status iq_decode_workspace_init(void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/*
+ * iq_decode_attention - single-token decode attention computed on the packed
+ * cache without materializing keys or values (App. A; Table 2; Fig. 1
+ * bottom): per query head h of KV head g = h / (n_q_heads / n_kv_heads),
+ *   q_tilde = R_g q_h;  score_j = s^K_j (q_tilde . C[codeK_j]) * scale;
+ *   alpha = softmax(score);  o = R_g^T sum_j alpha_j s^V_j C[codeV_j].
+ * The sum over positions is split across workgroups (flash-decoding) and the
+ * partial results are merged before the single inverse rotation.
+ *
+ * q         : device fp32 [batch][n_q_heads][128], original (unrotated) space.
+ * caches    : as written by iq_compress_kv / iq_append_token.
+ * seq_lens  : device int32 [batch]; positions 0 .. seq_lens[b]-1 are attended.
+ *             Values above max_seq_len are treated as max_seq_len; a length of
+ *             0 yields a zero output row.
+ * max_seq_len : host-side upper bound of seq_lens[] (sizes the launch, so no
+ *             device-to-host synchronization is needed); <= capacity.
+ * softmax_scale : <= 0 selects 1/sqrt(128).
+ * out       : device fp32 [batch][n_q_heads][128], original space.
+ * workspace : device, >= iq_decode_workspace_bytes(...) bytes, 256-byte
+ *             aligned, zero-filled once by iq_decode_workspace_init.  Calls
+ *             that share a workspace must not overlap in time.
+ * n_q_heads / n_kv_heads must be an integer <= 16.
+ */
+iq_status iq_decode_attention(const float* q,
+                              const uint8_t* k_codes, const float* k_norms,
+                              const uint8_t* v_codes, const float* v_norms,
+                              const int32_t* seq_lens, int64_t capacity,
+                              int64_t max_seq_len, const float* quats,
+                              int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                              int64_t head_dim, float softmax_scale, float* out,
+                              void* workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+
+#ifdef __cplusplus
+}  /* extern "C" */
+#endif
+
+#endif  /* ISOQUANT_H_ */

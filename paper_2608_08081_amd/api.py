@@ -1,0 +1,207 @@
+"""Thin PyTorch binding of libisoquant (names follow include/isoquant.h).
+
+Argument marshalling only: tensors are checked for device, dtype, shape and
+contiguity (the C library cannot see tensor extents), then their device
+pointers and the current HIP stream are handed to the C ABI.  All
+compression and attention arithmetic runs in the library's HIP kernels.
+"""
+
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+import torch
+
+from . import _lib
+
+HEAD_DIM = 128
+RECORD_BYTES = 48
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _require(t, name, dtype, shape, device=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+def _dtype_code(t):
+    if t.dtype == torch.float16:
+        return _lib.IQ_DTYPE_F16
+    if t.dtype == torch.float32:
+        return _lib.IQ_DTYPE_F32
+    raise TypeError(f"unsupported K/V dtype {t.dtype} (float16 or float32)")
+
+
+# ---------------------------------------------------------------------------
+# host-side entry points
+# ---------------------------------------------------------------------------
+
+def iq_codebook():
+    """(levels[8], thresholds[7]) as float32 numpy arrays."""
+    lv = np.zeros(8, np.float32)
+    th = np.zeros(7, np.float32)
+    _lib.check("iq_codebook", _lib.lib().iq_codebook(lv.ctypes.data_as(ctypes.c_void_p),
+                                                     th.ctypes.data_as(ctypes.c_void_p)))
+    return lv, th
+
+
+def iq_make_rotation(seed: int, n_kv_heads: int) -> torch.Tensor:
+    """Seeded SO(4) parameters, host float32 tensor [n_kv_heads][32][2][4]."""
+    out = np.zeros((n_kv_heads, 32, 2, 4), np.float32)
+    _lib.check("iq_make_rotation", _lib.lib().iq_make_rotation(
+        seed & ((1 << 64) - 1), n_kv_heads, HEAD_DIM, out.ctypes.data_as(ctypes.c_void_p)))
+    return torch.from_numpy(out)
+
+
+def iq_decode_workspace_bytes(batch, n_q_heads, n_kv_heads, max_seq_len) -> int:
+    return int(_lib.lib().iq_decode_workspace_bytes(batch, n_q_heads, n_kv_heads,
+                                                    max_seq_len, HEAD_DIM))
+
+
+# ---------------------------------------------------------------------------
+# device entry points
+# ---------------------------------------------------------------------------
+
+def alloc_cache(batch, n_kv_heads, capacity, device, values=True):
+    """Zero-filled packed cache buffers for one layer: dict with k_codes,
+    k_norms (and v_codes, v_norms), plus seq_lens (int32 zeros)."""
+    c = {
+        "k_codes": torch.zeros((batch, n_kv_heads, capacity, RECORD_BYTES), dtype=torch.uint8,
+                               device=device),
+        "k_norms": torch.zeros((batch, n_kv_heads, capacity), dtype=torch.float32, device=device),
+        "seq_lens": torch.zeros(batch, dtype=torch.int32, device=device),
+    }
+    if values:
+        c["v_codes"] = torch.zeros_like(c["k_codes"])
+        c["v_norms"] = torch.zeros_like(c["k_norms"])
+    return c
+
+
+def iq_compress_kv(k, v, quats, k_codes=None, k_norms=None, v_codes=None, v_norms=None,
+                   dst_offset: int = 0):
+    """Algorithm 1 over a block of tokens: k, v [B][H][T][128] (f16 or f32,
+    either may be None) written into the caches at positions dst_offset.."""
+    src = k if k is not None else v
+    if src is None:
+        raise ValueError("k and v are both None")
+    if src.dim() != 4 or src.shape[-1] != HEAD_DIM:
+        raise ValueError("k/v must be [batch][n_kv_heads][n_tokens][128]")
+    b, h, t, _ = src.shape
+    dev = src.device
+    codes_ref = k_codes if k is not None else v_codes
+    if codes_ref is None:
+        raise ValueError("missing output cache")
+    cap = codes_ref.shape[2]
+    _require(quats, "quats", torch.float32, (h, 32, 2, 4), dev)
+    for name, x, codes, norms in (("k", k, k_codes, k_norms), ("v", v, v_codes, v_norms)):
+        if x is None:
+            continue
+        _require(x, name, src.dtype, (b, h, t, HEAD_DIM), dev)
+        _require(codes, f"{name}_codes", torch.uint8, (b, h, cap, RECORD_BYTES), dev)
+        _require(norms, f"{name}_norms", torch.float32, (b, h, cap), dev)
+    st = _lib.lib().iq_compress_kv(
+        _ptr(k), _ptr(v), _dtype_code(src), b, h, t, HEAD_DIM, _ptr(quats),
+        _ptr(k_codes) if k is not None else None, _ptr(k_norms) if k is not None else None,
+        _ptr(v_codes) if v is not None else None, _ptr(v_norms) if v is not None else None,
+        cap, dst_offset, _stream(dev))
+    _lib.check("iq_compress_kv", st)
+
+
+def iq_append_token(k_new, v_new, quats, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                    status=None):
+    """Compress one new token per sequence (k_new, v_new: [B][H][128]) into
+    position seq_lens[b] and increment seq_lens in place."""
+    src = k_new if k_new is not None else v_new
+    if src is None:
+        raise ValueError("k_new and v_new are both None")
+    b, h, _ = src.shape
+    dev = src.device
+    codes_ref = k_codes if k_new is not None else v_codes
+    cap = codes_ref.shape[2]
+    _require(quats, "quats", torch.float32, (h, 32, 2, 4), dev)
+    _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
+    if status is not None:
+        _require(status, "status", torch.int32, (1,), dev)
+    for name, x, codes, norms in (("k_new", k_new, k_codes, k_norms),
+                                  ("v_new", v_new, v_codes, v_norms)):
+        if x is None:
+            continue
+        _require(x, name, src.dtype, (b, h, HEAD_DIM), dev)
+        _require(codes, f"{name}_codes", torch.uint8, (b, h, cap, RECORD_BYTES), dev)
+        _require(norms, f"{name}_norms", torch.float32, (b, h, cap), dev)
+    st = _lib.lib().iq_append_token(
+        _ptr(k_new), _ptr(v_new), _dtype_code(src), b, h, HEAD_DIM, _ptr(quats),
+        _ptr(k_codes) if k_new is not None else None,
+        _ptr(k_norms) if k_new is not None else None,
+        _ptr(v_codes) if v_new is not None else None,
+        _ptr(v_norms) if v_new is not None else None,
+        cap, _ptr(seq_lens), _ptr(status), _stream(dev))
+    _lib.check("iq_append_token", st)
+
+
+def iq_decode_workspace_init(workspace):
+    st = _lib.lib().iq_decode_workspace_init(_ptr(workspace), workspace.numel() *
+                                             workspace.element_size(), _stream(workspace.device))
+    _lib.check("iq_decode_workspace_init", st)
+
+
+def alloc_workspace(batch, n_q_heads, n_kv_heads, max_seq_len, device):
+    nbytes = iq_decode_workspace_bytes(batch, n_q_heads, n_kv_heads, max_seq_len)
+    if nbytes <= 0:
+        raise ValueError("unsupported decode shape")
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    iq_decode_workspace_init(ws)
+    return ws
+
+
+def iq_decode_attention(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out=None,
+                        workspace=None, max_seq_len=None, softmax_scale: float = 0.0):
+    """Decode attention on the packed cache.  q: [B][H_q][128] fp32 (original
+    space); returns out [B][H_q][128] fp32 (original space)."""
+    if q.dim() != 3 or q.shape[-1] != HEAD_DIM:
+        raise ValueError("q must be [batch][n_q_heads][128]")
+    b, hq, _ = q.shape
+    dev = q.device
+    _require(q, "q", torch.float32, (b, hq, HEAD_DIM), dev)
+    if k_codes.dim() != 4:
+        raise ValueError("k_codes must be [batch][n_kv_heads][capacity][48]")
+    _, hkv, cap, _ = k_codes.shape
+    _require(k_codes, "k_codes", torch.uint8, (b, hkv, cap, RECORD_BYTES), dev)
+    _require(v_codes, "v_codes", torch.uint8, (b, hkv, cap, RECORD_BYTES), dev)
+    _require(k_norms, "k_norms", torch.float32, (b, hkv, cap), dev)
+    _require(v_norms, "v_norms", torch.float32, (b, hkv, cap), dev)
+    _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
+    _require(quats, "quats", torch.float32, (hkv, 32, 2, 4), dev)
+    if max_seq_len is None:
+        max_seq_len = cap
+    if out is None:
+        out = torch.empty((b, hq, HEAD_DIM), dtype=torch.float32, device=dev)
+    _require(out, "out", torch.float32, (b, hq, HEAD_DIM), dev)
+    if workspace is None:
+        workspace = alloc_workspace(b, hq, hkv, max_seq_len, dev)
+    if workspace.dtype != torch.uint8 or workspace.device != dev or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 device tensor")
+    st = _lib.lib().iq_decode_attention(
+        _ptr(q), _ptr(k_codes), _ptr(k_norms), _ptr(v_codes), _ptr(v_norms), _ptr(seq_lens),
+        cap, max_seq_len, _ptr(quats), b, hq, hkv, HEAD_DIM, float(softmax_scale), _ptr(out),
+        _ptr(workspace), workspace.numel(), _stream(dev))
+    _lib.check("iq_decode_attention", st)
+    return out

@@ -1,0 +1,283 @@
+// Host side of libisoquant: the C ABI declared in isoquant.h.
+//
+// Validation happens here, before any HIP call; the kernels live in
+// iq_compress.hip and iq_decode.hip.  The codebook (Sec. 3.2 Step 3) is
+// derived here on first use with a Lloyd-Max iteration in double precision,
+// and the seeded rotation parameters (App. B) with SplitMix64.
+#include <math.h>
+#include <string.h>
+
+#include <mutex>
+
+#include "iq_internal.h"
+
+// IEEE-exact host arithmetic for the parameter generator: no contraction of
+// a*b + c into fused multiply-adds in this translation unit.
+#pragma clang fp contract(off)
+
+namespace iq {
+namespace {
+
+// ---------------------------------------------------------------------------
+// Codebook: Lloyd-Max levels for one coordinate of a uniform point on the
+// sphere S^(d-1), density proportional to (1 - t^2)^k with k = (d - 3) / 2.
+// Level of a cell [a, b] = conditional mean
+//   integral t (1-t^2)^k dt / integral (1-t^2)^k dt,
+// numerator in closed form  ((1-a^2)^(k+1) - (1-b^2)^(k+1)) / (2(k+1)),
+// denominator by composite Simpson quadrature.
+// ---------------------------------------------------------------------------
+double sphere_density(double t, double k) {
+  const double u = 1.0 - t * t;
+  return u > 0.0 ? exp(k * log(u)) : 0.0;
+}
+
+double simpson_mass(double a, double b, double k) {
+  const int n = 4096;  // even
+  const double h = (b - a) / n;
+  double s = sphere_density(a, k) + sphere_density(b, k);
+  for (int i = 1; i < n; ++i) s += sphere_density(a + i * h, k) * ((i & 1) ? 4.0 : 2.0);
+  return s * h / 3.0;
+}
+
+double first_moment(double a, double b, double k) {
+  const double ua = 1.0 - a * a, ub = 1.0 - b * b;
+  const double pa = ua > 0.0 ? exp((k + 1.0) * log(ua)) : 0.0;
+  const double pb = ub > 0.0 ? exp((k + 1.0) * log(ub)) : 0.0;
+  return (pa - pb) / (2.0 * (k + 1.0));
+}
+
+// Round to the nearest IEEE binary16 value (ties to even) for values in the
+// normal binary16 range.
+double round_to_half(double v) {
+  if (v == 0.0) return 0.0;
+  int e = 0;
+  frexp(fabs(v), &e);                   // |v| = f * 2^e, f in [0.5, 1)
+  const double ulp = ldexp(1.0, e - 11);  // 11 significant bits
+  return nearbyint(v / ulp) * ulp;
+}
+
+Codebook build_codebook() {
+  const int d = kDim, n = 8;
+  const double k = (d - 3) / 2.0;
+  double c[n];
+  for (int i = 0; i < n; ++i) c[i] = -2.0 / sqrt(static_cast<double>(d)) + i * (4.0 / sqrt(static_cast<double>(d))) / (n - 1);
+  for (int it = 0; it < 20000; ++it) {
+    double edges[n + 1];
+    edges[0] = -1.0;
+    edges[n] = 1.0;
+    for (int i = 1; i < n; ++i) edges[i] = 0.5 * (c[i - 1] + c[i]);
+    double moved = 0.0;
+    for (int i = 0; i < n; ++i) {
+      const double nc = first_moment(edges[i], edges[i + 1], k) / simpson_mass(edges[i], edges[i + 1], k);
+      moved = fmax(moved, fabs(nc - c[i]));
+      c[i] = nc;
+    }
+    if (moved < 1e-13) break;
+  }
+  Codebook cb{};
+  for (int i = 0; i < n; ++i) cb.level[i] = static_cast<float>(round_to_half(c[i]));
+  // enforce the symmetry of the symmetric density exactly
+  for (int i = 0; i < n / 2; ++i) cb.level[i] = -cb.level[n - 1 - i];
+  for (int i = 0; i < n - 1; ++i)
+    cb.thr[i] = static_cast<float>(0.5 * (static_cast<double>(cb.level[i]) + cb.level[i + 1]));
+  return cb;
+}
+
+// ---------------------------------------------------------------------------
+// SplitMix64 (Steele, Lea & Flood 2014) and the unit-quaternion sampler.
+// ---------------------------------------------------------------------------
+struct SplitMix64 {
+  uint64_t state;
+  uint64_t next() {
+    state += 0x9E3779B97F4A7C15ull;
+    uint64_t z = state;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+  }
+  double uniform_pm1() {
+    const double u = static_cast<double>(next() >> 11) * 0x1.0p-53;
+    return 2.0 * u - 1.0;
+  }
+};
+
+void random_unit_quaternion(SplitMix64& g, float* out) {
+  for (;;) {
+    double u[4];
+    for (int i = 0; i < 4; ++i) u[i] = g.uniform_pm1();
+    double n2 = u[0] * u[0];
+    n2 = n2 + u[1] * u[1];
+    n2 = n2 + u[2] * u[2];
+    n2 = n2 + u[3] * u[3];
+    if (n2 > 1e-6 && n2 <= 1.0) {
+      const double n = sqrt(n2);
+      for (int i = 0; i < 4; ++i) out[i] = static_cast<float>(u[i] / n);
+      return;
+    }
+  }
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Largest element index touched must fit: all sizes here are products of
+// validated non-negative int64 values below 2^62.
+bool mul_ok(int64_t a, int64_t b) { return a == 0 || b <= (int64_t(1) << 62) / a; }
+
+}  // namespace
+
+const Codebook& codebook() {
+  static Codebook cb;
+  static std::once_flag once;
+  std::call_once(once, [] { cb = build_codebook(); });
+  return cb;
+}
+
+}  // namespace iq
+
+using iq::kDim;
+
+extern "C" {
+
+const char* iq_status_string(iq_status s) {
+  switch (s) {
+    case IQ_OK: return "IQ_OK";
+    case IQ_ERR_INVALID_ARGUMENT: return "IQ_ERR_INVALID_ARGUMENT";
+    case IQ_ERR_UNSUPPORTED: return "IQ_ERR_UNSUPPORTED";
+    case IQ_ERR_WORKSPACE_TOO_SMALL: return "IQ_ERR_WORKSPACE_TOO_SMALL";
+    case IQ_ERR_HIP: return "IQ_ERR_HIP";
+    case IQ_ERR_CAPACITY: return "IQ_ERR_CAPACITY";
+  }
+  return "IQ_ERR_UNKNOWN";
+}
+
+int iq_version(void) { return 100; }
+
+iq_status iq_codebook(float* levels, float* thresholds) {
+  const iq::Codebook& cb = iq::codebook();
+  if (levels) memcpy(levels, cb.level, sizeof(cb.level));
+  if (thresholds) memcpy(thresholds, cb.thr, sizeof(cb.thr));
+  return IQ_OK;
+}
+
+iq_status iq_make_rotation(uint64_t seed, int64_t n_kv_heads, int64_t head_dim,
+                           float* quats_host) {
+  if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
+  if (n_kv_heads <= 0 || quats_host == nullptr) return IQ_ERR_INVALID_ARGUMENT;
+  iq::SplitMix64 g{seed};
+  for (int64_t h = 0; h < n_kv_heads; ++h)
+    for (int blk = 0; blk < iq::kNumBlocks; ++blk) {
+      float* dst = quats_host + (h * iq::kNumBlocks + blk) * 8;
+      iq::random_unit_quaternion(g, dst);
+      iq::random_unit_quaternion(g, dst + 4);
+    }
+  return IQ_OK;
+}
+
+iq_status iq_compress_kv(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+                         int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
+                         const float* quats, uint8_t* k_codes, float* k_norms,
+                         uint8_t* v_codes, float* v_norms, int64_t capacity,
+                         int64_t dst_offset, hipStream_t stream) {
+  if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
+  if (dtype != IQ_DTYPE_F32 && dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
+  if (batch < 0 || n_kv_heads <= 0 || n_tokens < 0 || capacity < 0 || dst_offset < 0)
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (dst_offset > capacity || n_tokens > capacity - dst_offset) return IQ_ERR_INVALID_ARGUMENT;
+  if (!iq::mul_ok(batch, n_kv_heads) || !iq::mul_ok(batch * n_kv_heads, capacity + 1) ||
+      !iq::mul_ok(batch * n_kv_heads * (capacity + 1), kDim))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (k == nullptr && v == nullptr) return IQ_ERR_INVALID_ARGUMENT;
+  if (quats == nullptr || !iq::aligned(quats, 4)) return IQ_ERR_INVALID_ARGUMENT;
+  if (k && (!k_codes || !k_norms || !iq::aligned(k, 16) || !iq::aligned(k_codes, 16) ||
+            !iq::aligned(k_norms, 4)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (v && (!v_codes || !v_norms || !iq::aligned(v, 16) || !iq::aligned(v_codes, 16) ||
+            !iq::aligned(v_norms, 4)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (batch == 0 || n_tokens == 0) return IQ_OK;
+  const hipError_t e = iq::launch_compress(k, v, dtype, batch, n_kv_heads, n_tokens, quats,
+                                           k_codes, k_norms, v_codes, v_norms, capacity,
+                                           dst_offset, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+iq_status iq_append_token(const void* k_new, const void* v_new, iq_dtype dtype, int64_t batch,
+                          int64_t n_kv_heads, int64_t head_dim, const float* quats,
+                          uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
+                          int64_t capacity, int32_t* seq_lens, int32_t* status_dev,
+                          hipStream_t stream) {
+  if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
+  if (dtype != IQ_DTYPE_F32 && dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
+  if (batch < 0 || batch > 0x7fffffff || n_kv_heads <= 0 || n_kv_heads > 512 || capacity < 0 ||
+      capacity > 0x7fffffff)
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (!iq::mul_ok(batch, n_kv_heads) || !iq::mul_ok(batch * n_kv_heads, capacity + 1) ||
+      !iq::mul_ok(batch * n_kv_heads * (capacity + 1), kDim))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (k_new == nullptr && v_new == nullptr) return IQ_ERR_INVALID_ARGUMENT;
+  if (quats == nullptr || seq_lens == nullptr || !iq::aligned(seq_lens, 4) ||
+      !iq::aligned(quats, 4) || (status_dev && !iq::aligned(status_dev, 4)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (k_new && (!k_codes || !k_norms || !iq::aligned(k_new, 16) || !iq::aligned(k_codes, 16) ||
+                !iq::aligned(k_norms, 4)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (v_new && (!v_codes || !v_norms || !iq::aligned(v_new, 16) || !iq::aligned(v_codes, 16) ||
+                !iq::aligned(v_norms, 4)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (batch == 0) return IQ_OK;
+  const hipError_t e = iq::launch_append(k_new, v_new, dtype, batch, n_kv_heads, quats, k_codes,
+                                         k_norms, v_codes, v_norms, capacity, seq_lens,
+                                         status_dev, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+size_t iq_decode_workspace_bytes(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                                 int64_t max_seq_len, int64_t head_dim) {
+  if (head_dim != kDim) return 0;
+  iq::DecodePlan plan;
+  if (!iq::plan_decode(batch, n_q_heads, n_kv_heads, max_seq_len, &plan)) return 0;
+  return plan.total_bytes;
+}
+
+iq_status iq_decode_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (workspace == nullptr || !iq::aligned(workspace, 256)) return IQ_ERR_INVALID_ARGUMENT;
+  const hipError_t e = iq::launch_fill_zero(workspace, workspace_bytes, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+iq_status iq_decode_attention(const float* q, const uint8_t* k_codes, const float* k_norms,
+                              const uint8_t* v_codes, const float* v_norms,
+                              const int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                              const float* quats, int64_t batch, int64_t n_q_heads,
+                              int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
+                              float* out, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
+  if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
+  if (batch < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || capacity < 0 || max_seq_len < 0 ||
+      max_seq_len > capacity || capacity > 0x7fffffff || batch > 0xffffff)
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (n_q_heads % n_kv_heads) return IQ_ERR_INVALID_ARGUMENT;
+  if (n_q_heads / n_kv_heads > iq::kMaxGroup) return IQ_ERR_UNSUPPORTED;
+  if (!iq::mul_ok(batch, n_kv_heads) || !iq::mul_ok(batch * n_kv_heads, capacity + 1) ||
+      !iq::mul_ok(batch * n_kv_heads * (capacity + 1), kDim))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (!q || !k_codes || !k_norms || !v_codes || !v_norms || !seq_lens || !quats || !out ||
+      !workspace)
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (!iq::aligned(q, 16) || !iq::aligned(k_codes, 16) || !iq::aligned(v_codes, 16) ||
+      !iq::aligned(k_norms, 4) || !iq::aligned(v_norms, 4) || !iq::aligned(out, 16) ||
+      !iq::aligned(seq_lens, 4) || !iq::aligned(quats, 4) || !iq::aligned(workspace, 256))
+    return IQ_ERR_INVALID_ARGUMENT;
+  iq::DecodePlan plan;
+  if (!iq::plan_decode(batch, n_q_heads, n_kv_heads, max_seq_len, &plan))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < plan.total_bytes) return IQ_ERR_WORKSPACE_TOO_SMALL;
+  if (batch == 0) return IQ_OK;
+  const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf(static_cast<float>(kDim));
+  const hipError_t e = iq::launch_decode(plan, q, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                                         capacity, max_seq_len, quats, batch, n_q_heads,
+                                         n_kv_heads, scale, out, workspace, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,261 @@
+// IsoQuant compression kernels (Algorithm 1; Sec. 3.2 Steps 1-4) for gfx950.
+//
+// One lane compresses one 128-dim vector entirely in registers: there is no
+// cross-lane traffic at all, the 128 values, the fp64 norm accumulators and
+// the 12-word output record all live in VGPRs.  A workgroup is a single
+// wave whose 64 lanes take 64 consecutive tokens of one (K|V, sequence,
+// KV head), so the rotation parameters are wave-uniform and are fetched
+// with scalar loads.
+//
+// Per vector:
+//   s^2  = sum x_i^2 in fp64 (products of fp16/fp32 inputs are exact in fp64),
+//          stored scale = fp32(sqrt(s^2))  (Step 1);
+//   y    = diag(M_i H_4) (H_32 (x) I_4) x   unnormalized, fp32  (Step 2);
+//   code = #{j : y >= t_j * s * sqrt(128)}  (Step 3; comparing the
+//          unnormalized y against scaled thresholds is the same test as
+//          comparing R x / s against t_j, and saves 128 multiplies);
+//   pack = 3-bit codes into 12 words, stored as three 16-byte writes (Step 4).
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include "iq_device.h"
+#include "iq_internal.h"
+
+namespace iq {
+namespace {
+
+__device__ __forceinline__ void load_vector(const __half* src, float (&x)[kDim]) {
+  const uint4* p = reinterpret_cast<const uint4*>(src);
+#pragma unroll
+  for (int i = 0; i < kDim / 8; ++i) {
+    const uint4 u = p[i];
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[8 * i + 2 * j] = __half2float(__ushort_as_half(static_cast<unsigned short>(w[j] & 0xFFFFu)));
+      x[8 * i + 2 * j + 1] = __half2float(__ushort_as_half(static_cast<unsigned short>(w[j] >> 16)));
+    }
+  }
+}
+
+__device__ __forceinline__ void load_vector(const float* src, float (&x)[kDim]) {
+  const float4* p = reinterpret_cast<const float4*>(src);
+#pragma unroll
+  for (int i = 0; i < kDim / 4; ++i) {
+    const float4 f = p[i];
+    x[4 * i] = f.x;
+    x[4 * i + 1] = f.y;
+    x[4 * i + 2] = f.z;
+    x[4 * i + 3] = f.w;
+  }
+}
+
+// Compress one vector (Algorithm 1) and write its record and scale.
+template <typename T>
+__device__ __forceinline__ void compress_one(const T* __restrict__ src,
+                                             const float* __restrict__ quats_head,
+                                             uint8_t* __restrict__ dst_code,
+                                             float* __restrict__ dst_norm,
+                                             const Codebook& cb) {
+  float x[kDim];
+  load_vector(src, x);
+
+  // Step 1: fp64 sum of squares, four independent chains.
+  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+#pragma unroll
+  for (int i = 0; i < kDim; i += 4) {
+    a0 = fma(static_cast<double>(x[i]), static_cast<double>(x[i]), a0);
+    a1 = fma(static_cast<double>(x[i + 1]), static_cast<double>(x[i + 1]), a1);
+    a2 = fma(static_cast<double>(x[i + 2]), static_cast<double>(x[i + 2]), a2);
+    a3 = fma(static_cast<double>(x[i + 3]), static_cast<double>(x[i + 3]), a3);
+  }
+  const double ss = (a0 + a1) + (a2 + a3);
+  const double s = sqrt(ss);
+
+  // Thresholds in the unnormalized domain: t_j * s * sqrt(128).  A zero
+  // vector keeps the plain thresholds, so its all-zero y maps to code 4.
+  float thr[7];
+  if (ss > 0.0) {
+    const double sc = s * 11.313708498984760390;  // sqrt(128)
+#pragma unroll
+    for (int j = 0; j < 7; ++j) thr[j] = static_cast<float>(static_cast<double>(cb.thr[j]) * sc);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 7; ++j) thr[j] = cb.thr[j];
+  }
+
+  // Step 2a: Walsh-Hadamard butterflies on index bits 2..6 (H_32 (x) I_4).
+#pragma unroll
+  for (int st = 4; st < kDim; st <<= 1) {
+#pragma unroll
+    for (int i = 0; i < kDim; ++i) {
+      if (!(i & st)) {
+        const float a = x[i], b = x[i + st];
+        x[i] = a + b;
+        x[i + st] = a - b;
+      }
+    }
+  }
+
+  // Step 2b + 3 + 4: per block, y = (M_i H_4) z, quantize, pack.
+  uint32_t w[kRecordWords];
+#pragma unroll
+  for (int i = 0; i < kRecordWords; ++i) w[i] = 0u;
+#pragma unroll
+  for (int blk = 0; blk < kNumBlocks; ++blk) {
+    float m[4][4];
+    so4_matrix_h4(quats_head + 8 * blk, m);
+    const float z0 = x[4 * blk], z1 = x[4 * blk + 1], z2 = x[4 * blk + 2], z3 = x[4 * blk + 3];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float y = m[r][0] * z0 + m[r][1] * z1 + m[r][2] * z2 + m[r][3] * z3;
+      put_code(w, 4 * blk + r, quantize3(y, thr));
+    }
+  }
+
+  uint4* out = reinterpret_cast<uint4*>(dst_code);
+  out[0] = make_uint4(w[0], w[1], w[2], w[3]);
+  out[1] = make_uint4(w[4], w[5], w[6], w[7]);
+  out[2] = make_uint4(w[8], w[9], w[10], w[11]);
+  *dst_norm = static_cast<float>(s);
+}
+
+// Bulk compression.  1-D grid of single-wave workgroups:
+//   blockIdx.x = (which * (B*H) + bh) * chunks + chunk,  lane = token in chunk.
+template <typename T>
+__global__ __launch_bounds__(64) void compress_kernel(
+    const T* __restrict__ src0, const T* __restrict__ src1, const float* __restrict__ quats,
+    uint8_t* __restrict__ codes0, float* __restrict__ norms0, uint8_t* __restrict__ codes1,
+    float* __restrict__ norms1, int n_heads, int64_t n_bh, int64_t n_tokens, int64_t chunks,
+    int64_t capacity, int64_t dst_offset, Codebook cb) {
+  const int64_t blk = blockIdx.x;
+  const int64_t chunk = blk % chunks;
+  const int64_t rest = blk / chunks;
+  const int64_t bh = rest % n_bh;
+  const int which = static_cast<int>(rest / n_bh);
+  const int h = static_cast<int>(bh % n_heads);
+  const int64_t t = chunk * 64 + threadIdx.x;
+  if (t >= n_tokens) return;
+  const T* src = which ? src1 : src0;
+  uint8_t* codes = which ? codes1 : codes0;
+  float* norms = which ? norms1 : norms0;
+  const int64_t pos = bh * capacity + dst_offset + t;
+  compress_one<T>(src + (bh * n_tokens + t) * kDim, quats + h * kQuatFloats,
+                  codes + pos * kRecordBytes, norms + pos, cb);
+}
+
+// Append one token per sequence: one single-wave workgroup per sequence,
+// lanes loop over the K and V vectors of every KV head.  seq_lens[b] is read
+// before any write and bumped after a barrier, so every vector of the
+// sequence lands at the same position.
+template <typename T>
+__global__ __launch_bounds__(64) void append_kernel(
+    const T* __restrict__ src0, const T* __restrict__ src1, const float* __restrict__ quats,
+    uint8_t* __restrict__ codes0, float* __restrict__ norms0, uint8_t* __restrict__ codes1,
+    float* __restrict__ norms1, int n_heads, int n_vectors, int64_t capacity,
+    int32_t* __restrict__ seq_lens, int32_t* __restrict__ status, Codebook cb) {
+  __shared__ int32_t pos_s;
+  const int b = blockIdx.x;
+  if (threadIdx.x == 0) pos_s = seq_lens[b];
+  __syncthreads();
+  const int64_t pos = pos_s;
+  if (pos < 0 || pos >= capacity) {
+    if (threadIdx.x == 0 && status != nullptr) atomicOr(status, static_cast<int32_t>(IQ_ERR_CAPACITY));
+    return;
+  }
+  for (int idx = threadIdx.x; idx < n_vectors; idx += 64) {
+    const int which = idx / n_heads;
+    const int h = idx % n_heads;
+    const T* src = which ? src1 : src0;
+    uint8_t* codes = which ? codes1 : codes0;
+    float* norms = which ? norms1 : norms0;
+    const int64_t bh = static_cast<int64_t>(b) * n_heads + h;
+    const int64_t p = bh * capacity + pos;
+    compress_one<T>(src + bh * kDim, quats + h * kQuatFloats, codes + p * kRecordBytes,
+                    norms + p, cb);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) seq_lens[b] = static_cast<int32_t>(pos + 1);
+}
+
+__global__ void fill_zero_kernel(uint32_t* __restrict__ p, int64_t n_words) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n_words;
+       i += stride)
+    p[i] = 0u;
+}
+
+}  // namespace
+
+hipError_t launch_compress(const void* k, const void* v, int dtype, int64_t batch,
+                           int64_t n_heads, int64_t n_tokens, const float* quats,
+                           uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
+                           float* v_norms, int64_t capacity, int64_t dst_offset,
+                           hipStream_t stream) {
+  // slot 0 is whichever side is present first, slot 1 the other (if any)
+  const void* s0 = k ? k : v;
+  uint8_t* c0 = k ? k_codes : v_codes;
+  float* n0 = k ? k_norms : v_norms;
+  const void* s1 = (k && v) ? v : nullptr;
+  uint8_t* c1 = (k && v) ? v_codes : nullptr;
+  float* n1 = (k && v) ? v_norms : nullptr;
+  const int nwhich = s1 ? 2 : 1;
+  const int64_t n_bh = batch * n_heads;
+  const int64_t chunks = (n_tokens + 63) / 64;
+  const int64_t blocks = chunks * n_bh * nwhich;
+  if (blocks == 0) return hipSuccess;
+  const Codebook& cb = codebook();
+  const dim3 grid(static_cast<unsigned>(blocks)), block(64);
+  if (dtype == IQ_DTYPE_F16) {
+    hipLaunchKernelGGL(compress_kernel<__half>, grid, block, 0, stream,
+                       static_cast<const __half*>(s0), static_cast<const __half*>(s1), quats, c0,
+                       n0, c1, n1, static_cast<int>(n_heads), n_bh, n_tokens, chunks, capacity,
+                       dst_offset, cb);
+  } else {
+    hipLaunchKernelGGL(compress_kernel<float>, grid, block, 0, stream,
+                       static_cast<const float*>(s0), static_cast<const float*>(s1), quats, c0,
+                       n0, c1, n1, static_cast<int>(n_heads), n_bh, n_tokens, chunks, capacity,
+                       dst_offset, cb);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_append(const void* k, const void* v, int dtype, int64_t batch,
+                         int64_t n_heads, const float* quats, uint8_t* k_codes,
+                         float* k_norms, uint8_t* v_codes, float* v_norms,
+                         int64_t capacity, int32_t* seq_lens, int32_t* status,
+                         hipStream_t stream) {
+  if (batch == 0) return hipSuccess;
+  const void* s0 = k ? k : v;
+  uint8_t* c0 = k ? k_codes : v_codes;
+  float* n0 = k ? k_norms : v_norms;
+  const void* s1 = (k && v) ? v : nullptr;
+  uint8_t* c1 = (k && v) ? v_codes : nullptr;
+  float* n1 = (k && v) ? v_norms : nullptr;
+  const int n_vectors = static_cast<int>(n_heads * (s1 ? 2 : 1));
+  const Codebook& cb = codebook();
+  if (dtype == IQ_DTYPE_F16) {
+    hipLaunchKernelGGL(append_kernel<__half>, dim3(static_cast<unsigned>(batch)), dim3(64), 0,
+                       stream, static_cast<const __half*>(s0), static_cast<const __half*>(s1),
+                       quats, c0, n0, c1, n1, static_cast<int>(n_heads), n_vectors, capacity,
+                       seq_lens, status, cb);
+  } else {
+    hipLaunchKernelGGL(append_kernel<float>, dim3(static_cast<unsigned>(batch)), dim3(64), 0,
+                       stream, static_cast<const float*>(s0), static_cast<const float*>(s1), quats,
+                       c0, n0, c1, n1, static_cast<int>(n_heads), n_vectors, capacity, seq_lens,
+                       status, cb);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream) {
+  const int64_t words = static_cast<int64_t>(bytes / 4);
+  if (words == 0) return hipSuccess;
+  int64_t blocks = (words + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream,
+                     static_cast<uint32_t*>(ptr), words);
+  return hipGetLastError();
+}
+
+}  // namespace iq

@@ -1,0 +1,65 @@
+// Internal declarations of libisoquant shared by the host API and the
+// kernel translation units.  Not installed; the public ABI is isoquant.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "isoquant.h"
+
+namespace iq {
+
+constexpr int kDim = 128;           // head_dim (Sec. 3.2, d = 128)
+constexpr int kRecordBytes = 48;    // 128 codes x 3 bits
+constexpr int kRecordWords = 12;
+constexpr int kNumBlocks = 32;      // SO(4) blocks per head (d / 4)
+constexpr int kQuatFloats = 256;    // stored parameters per head (App. B)
+constexpr int kMaxGroup = 16;       // query heads per KV head supported
+
+// 3-bit codebook, passed to kernels by value.  level[] ascending (fp16-exact
+// values), thr[j] = midpoint of level[j] and level[j+1].
+struct Codebook {
+  float level[8];
+  float thr[7];
+};
+
+// Computed on first use (host), immutable afterwards.
+const Codebook& codebook();
+
+// Split-K plan for one decode call.  Deterministic function of the shapes so
+// that iq_decode_workspace_bytes and iq_decode_attention agree.
+struct DecodePlan {
+  int kernel;             // 0 = generic VALU path, 1 = MFMA path (group 8)
+  int64_t split_len;      // positions per split
+  int64_t n_splits;       // splits per (sequence, KV head)
+  size_t partial_bytes;   // B * H_q * n_splits * 130 floats
+  size_t ticket_bytes;    // one int32 per (sequence, KV head), padded
+  size_t total_bytes;
+};
+bool plan_decode(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                 int64_t max_seq_len, DecodePlan* plan);
+
+// Kernel launchers (return the launch's hipError_t).
+hipError_t launch_compress(const void* k, const void* v, int dtype, int64_t batch,
+                           int64_t n_heads, int64_t n_tokens, const float* quats,
+                           uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
+                           float* v_norms, int64_t capacity, int64_t dst_offset,
+                           hipStream_t stream);
+
+hipError_t launch_append(const void* k, const void* v, int dtype, int64_t batch,
+                         int64_t n_heads, const float* quats, uint8_t* k_codes,
+                         float* k_norms, uint8_t* v_codes, float* v_norms,
+                         int64_t capacity, int32_t* seq_lens, int32_t* status,
+                         hipStream_t stream);
+
+hipError_t launch_decode(const DecodePlan& plan, const float* q, const uint8_t* k_codes,
+                         const float* k_norms, const uint8_t* v_codes,
+                         const float* v_norms, const int32_t* seq_lens,
+                         int64_t capacity, int64_t max_seq_len, const float* quats,
+                         int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                         float scale, float* out, void* workspace, hipStream_t stream);
+
+hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
+
+}  // namespace iq

@@ -118,15 +118,16 @@ def queries(seed: int, w: Workload, n_steps: int = 1) -> np.ndarray:
                              dtype=np.float32)
 
 
-def appended_tokens(seed: int, w: Workload, n_steps: int):
+def appended_tokens(seed: int, w: Workload, n_steps: int, batch: int | None = None):
     """Keys and values appended during decode: two arrays
     [n_steps][B][H_kv][d], same distribution (and channel scales) as the
     cache, drawn from stream 5."""
+    b = w.batch if batch is None else batch
     n_out = 4 if w.kv_dist == "anisotropic" else 0
     sk = channel_scales(rng(seed, w.wid, 0), w.n_kv_heads, n_outliers=n_out)
     sv = channel_scales(rng(seed, w.wid, 1), w.n_kv_heads, n_outliers=n_out)
     g = rng(seed, w.wid, 5)
-    shape = (n_steps, w.batch, w.n_kv_heads, HEAD_DIM)
+    shape = (n_steps, b, w.n_kv_heads, HEAD_DIM)
     k = _draw_entries(g, shape, w.kv_dist) * sk[None, None]
     v = _draw_entries(g, shape, w.kv_dist) * sv[None, None]
     if w.dtype == "f16":

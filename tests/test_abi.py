@@ -1,0 +1,145 @@
+"""CPU tests of the C ABI: the library loads and exports what the header
+declares, its host-side functions agree bit-for-bit with the oracle's
+independent implementations, and argument validation rejects bad calls
+before any HIP call is made (so these run without a GPU)."""
+
+import ctypes
+
+import numpy as np
+import pytest
+
+from oracle import codebook as ocb
+from oracle import rotation as orot
+from paper_2608_08081_amd import _lib
+
+L = None
+
+
+@pytest.fixture(scope="module", autouse=True)
+def loaded():
+    global L
+    L = _lib.lib()
+    return L
+
+
+def test_exports_every_declared_symbol():
+    names = _lib.header_functions()
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings():
+    for code, name in _lib.STATUS_NAMES.items():
+        assert L.iq_status_string(code).decode() == name
+    assert L.iq_version() >= 100
+
+
+def test_codebook_matches_oracle_bit_for_bit():
+    lv = np.zeros(8, np.float32)
+    th = np.zeros(7, np.float32)
+    assert L.iq_codebook(lv.ctypes.data_as(ctypes.c_void_p), th.ctypes.data_as(ctypes.c_void_p)) == 0
+    o_lv, o_th = ocb.isoquant_codebook(128, 3)
+    assert np.array_equal(lv.astype(np.float64), o_lv)
+    assert np.array_equal(th.astype(np.float64), o_th)
+
+
+@pytest.mark.parametrize("seed,heads", [(0, 1), (1000, 1), (1002, 4), (2 ** 63 + 12345, 8)])
+def test_make_rotation_matches_oracle_bit_for_bit(seed, heads):
+    out = np.zeros((heads, 32, 2, 4), np.float32)
+    assert L.iq_make_rotation(seed, heads, 128, out.ctypes.data_as(ctypes.c_void_p)) == 0
+    want = orot.make_quaternions(seed, heads)
+    assert np.array_equal(out.view(np.uint32), want.view(np.uint32))
+
+
+def test_make_rotation_validation():
+    out = np.zeros((1, 32, 2, 4), np.float32)
+    p = out.ctypes.data_as(ctypes.c_void_p)
+    assert L.iq_make_rotation(1, 1, 64, p) == 2
+    assert L.iq_make_rotation(1, 0, 128, p) == 1
+    assert L.iq_make_rotation(1, 1, 128, None) == 1
+
+
+# Fake, aligned, never-dereferenced device addresses: validation must reject
+# every call below before touching them.
+A = ctypes.c_void_p(0x100000)
+B = ctypes.c_void_p(0x200000)
+
+
+def _compress(**kw):
+    args = dict(k=A, v=B, dtype=1, batch=1, heads=2, n=10, hd=128, quats=A, kc=A, kn=A, vc=B,
+                vn=B, cap=16, off=0)
+    args.update(kw)
+    return L.iq_compress_kv(args["k"], args["v"], args["dtype"], args["batch"], args["heads"],
+                            args["n"], args["hd"], args["quats"], args["kc"], args["kn"],
+                            args["vc"], args["vn"], args["cap"], args["off"], None)
+
+
+def test_compress_validation():
+    assert _compress(hd=64) == 2
+    assert _compress(dtype=7) == 2
+    assert _compress(k=None, v=None) == 1
+    assert _compress(quats=None) == 1
+    assert _compress(kc=None) == 1
+    assert _compress(n=17) == 1                 # beyond capacity
+    assert _compress(off=10) == 1               # 10 + 10 > 16
+    assert _compress(off=-1) == 1
+    assert _compress(n=-1) == 1
+    assert _compress(batch=-1) == 1
+    assert _compress(heads=0) == 1
+    assert _compress(kc=ctypes.c_void_p(0x100008)) == 1   # codes not 16-byte aligned
+    assert _compress(k=ctypes.c_void_p(0x100004)) == 1
+    # empty inputs are valid no-ops that launch nothing
+    assert _compress(n=0) == 0
+    assert _compress(batch=0) == 0
+
+
+def _append(**kw):
+    args = dict(k=A, v=B, dtype=1, batch=2, heads=2, hd=128, quats=A, kc=A, kn=A, vc=B, vn=B,
+                cap=16, seq=A, status=None)
+    args.update(kw)
+    return L.iq_append_token(args["k"], args["v"], args["dtype"], args["batch"], args["heads"],
+                             args["hd"], args["quats"], args["kc"], args["kn"], args["vc"],
+                             args["vn"], args["cap"], args["seq"], args["status"], None)
+
+
+def test_append_validation():
+    assert _append(hd=96) == 2
+    assert _append(dtype=3) == 2
+    assert _append(seq=None) == 1
+    assert _append(k=None, v=None) == 1
+    assert _append(vn=None) == 1
+    assert _append(status=ctypes.c_void_p(0x100002)) == 1
+    assert _append(batch=0) == 0
+
+
+def _decode(**kw):
+    args = dict(q=A, kc=A, kn=A, vc=B, vn=B, seq=A, cap=1024, maxlen=1024, quats=A, batch=1,
+                hq=32, hkv=4, hd=128, scale=0.0, out=B, ws=A, wsb=1 << 30)
+    args.update(kw)
+    return L.iq_decode_attention(args["q"], args["kc"], args["kn"], args["vc"], args["vn"],
+                                 args["seq"], args["cap"], args["maxlen"], args["quats"],
+                                 args["batch"], args["hq"], args["hkv"], args["hd"],
+                                 args["scale"], args["out"], args["ws"], args["wsb"], None)
+
+
+def test_decode_validation():
+    assert _decode(hd=256) == 2
+    assert _decode(hq=30) == 1                  # not a multiple of H_kv
+    assert _decode(hq=68) == 2                  # group 17 > 16
+    assert _decode(maxlen=2048) == 1            # beyond capacity
+    assert _decode(q=None) == 1
+    assert _decode(ws=None) == 1
+    assert _decode(ws=ctypes.c_void_p(0x100010)) == 1   # workspace not 256-byte aligned
+    assert _decode(q=ctypes.c_void_p(0x100004)) == 1
+    assert _decode(wsb=16) == 3
+    assert _decode(batch=0) == 0
+
+
+def test_workspace_bytes():
+    n = L.iq_decode_workspace_bytes(1, 32, 4, 32768, 128)
+    assert n > 0 and n % 256 == 0
+    assert L.iq_decode_workspace_bytes(1, 32, 4, 32768, 64) == 0
+    assert L.iq_decode_workspace_bytes(1, 30, 4, 32768, 128) == 0
+    # monotone in context length
+    assert L.iq_decode_workspace_bytes(1, 32, 4, 1024, 128) <= n

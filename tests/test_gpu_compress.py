@@ -1,0 +1,149 @@
+"""GPU parity of iq_compress_kv and iq_append_token against the oracle
+(Algorithm 1), called through the C ABI via the PyTorch binding."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import codebook as ocb
+from oracle import compress as ocz
+from oracle import rotation as orot
+from paper_2608_08081_amd import api, synth
+from tests.parity import check_codes, check_norms
+
+pytestmark = pytest.mark.gpu
+
+LEVELS, THR = ocb.isoquant_codebook(128, 3)
+DEV = torch.device("cuda:0")
+
+
+def _dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def _oracle(x, seed, heads):
+    rots = orot.rotation_matrices(orot.make_quaternions(seed, heads))
+    return ocz.compress_kv(x, rots, THR)
+
+
+def _run_compress(k, v, seed, heads, cap, off):
+    quats = api.iq_make_rotation(seed, heads).to(DEV)
+    b = (k if k is not None else v).shape[0]
+    cache = api.alloc_cache(b, heads, cap, DEV)
+    api.iq_compress_kv(None if k is None else _dev(k), None if v is None else _dev(v), quats,
+                       cache["k_codes"], cache["k_norms"], cache["v_codes"], cache["v_norms"],
+                       dst_offset=off)
+    torch.cuda.synchronize()
+    return {n: t.cpu().numpy() for n, t in cache.items()}
+
+
+@pytest.mark.parametrize("wid,t,off,cap", [(0, 1024, 0, 1024), (1, 777, 5, 800), (1, 1, 0, 1),
+                                           (4, 130, 63, 200)])
+def test_compress_parity(wid, t, off, cap):
+    w = synth.WORKLOADS[wid]
+    k = synth.kv_tensor(21, w, "k", n_tokens=t, batch=1)
+    v = synth.kv_tensor(21, w, "v", n_tokens=t, batch=1)
+    got = _run_compress(k, v, w.rotation_seed, w.n_kv_heads, cap, off)
+    for name, x in (("k", k), ("v", v)):
+        packed, norms, codes, y, s64 = _oracle(x, w.rotation_seed, w.n_kv_heads)
+        gp = got[f"{name}_codes"][:, :, off:off + t]
+        check_codes(gp, codes, y, THR, f"{name} w{wid}")
+        check_norms(got[f"{name}_norms"][:, :, off:off + t], s64, f"{name} w{wid}")
+        # untouched positions stay zero
+        assert not got[f"{name}_codes"][:, :, :off].any()
+        assert not got[f"{name}_codes"][:, :, off + t:].any()
+
+
+def test_compress_keys_only_and_values_only():
+    w = synth.WORKLOADS[1]
+    k = synth.kv_tensor(3, w, "k", n_tokens=100, batch=2)
+    got = _run_compress(k, None, w.rotation_seed, w.n_kv_heads, 128, 0)
+    _, _, codes, y, s64 = _oracle(k, w.rotation_seed, w.n_kv_heads)
+    check_codes(got["k_codes"][:, :, :100], codes, y, THR, "k only")
+    assert not got["v_codes"].any()
+    got = _run_compress(None, k, w.rotation_seed, w.n_kv_heads, 128, 0)
+    check_codes(got["v_codes"][:, :, :100], codes, y, THR, "v only")
+    assert not got["k_codes"].any()
+
+
+def test_compress_special_vectors():
+    """Zero vector -> norm 0 and every code 4; e_0 with identity SO(4)
+    parameters -> the hand-derived record 6D DB B6 x 16."""
+    x = np.zeros((1, 1, 3, 128), np.float32)
+    x[0, 0, 1, 0] = 1.0
+    x[0, 0, 2] = -0.0
+    quats = torch.from_numpy(orot.identity_quaternions(1)).to(DEV)
+    cache = api.alloc_cache(1, 1, 3, DEV, values=False)
+    api.iq_compress_kv(_dev(x), None, quats, cache["k_codes"], cache["k_norms"])
+    torch.cuda.synchronize()
+    rec = cache["k_codes"].cpu().numpy()[0, 0]
+    nrm = cache["k_norms"].cpu().numpy()[0, 0]
+    assert nrm[0] == 0 and nrm[2] == 0 and nrm[1] == 1.0
+    assert np.all(ocz.unpack(rec[0]) == 4) and np.all(ocz.unpack(rec[2]) == 4)
+    assert rec[1].tobytes() == bytes([0x6D, 0xDB, 0xB6]) * 16
+
+
+def test_compress_empty_is_noop():
+    w = synth.WORKLOADS[1]
+    quats = api.iq_make_rotation(w.rotation_seed, w.n_kv_heads).to(DEV)
+    cache = api.alloc_cache(1, w.n_kv_heads, 8, DEV)
+    k = torch.zeros((1, w.n_kv_heads, 0, 128), dtype=torch.float16, device=DEV)
+    api.iq_compress_kv(k, k, quats, cache["k_codes"], cache["k_norms"], cache["v_codes"],
+                       cache["v_norms"])
+    torch.cuda.synchronize()
+    assert not cache["k_codes"].any() and not cache["v_norms"].any()
+
+
+def test_append_parity_and_capacity():
+    """Append one token per sequence at seq_lens[b]; a full sequence is
+    skipped and flagged, its length unchanged."""
+    w = synth.WORKLOADS[1]
+    heads, cap = w.n_kv_heads, 8
+    quats = api.iq_make_rotation(w.rotation_seed, heads).to(DEV)
+    cache = api.alloc_cache(3, heads, cap, DEV)
+    cache["seq_lens"].copy_(torch.tensor([0, 5, 8], dtype=torch.int32))
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    kn, vn = synth.appended_tokens(5, w, 3, batch=3)
+    for step in range(3):
+        api.iq_append_token(_dev(kn[step][:3]), _dev(vn[step][:3]), quats, cache["k_codes"],
+                            cache["k_norms"], cache["v_codes"], cache["v_norms"],
+                            cache["seq_lens"], status)
+    torch.cuda.synchronize()
+    assert cache["seq_lens"].cpu().tolist() == [3, 8, 8]
+    assert int(status.item()) == 5
+    got = {n: t.cpu().numpy() for n, t in cache.items()}
+    for name, x in (("k", kn), ("v", vn)):
+        for b, start, n in ((0, 0, 3), (1, 5, 3)):
+            seq = x[:n, b].transpose(1, 0, 2)[None]            # [1][H][n][128]
+            _, _, codes, y, s64 = _oracle(seq, w.rotation_seed, heads)
+            check_codes(got[f"{name}_codes"][b:b + 1, :, start:start + n], codes, y, THR,
+                        f"append {name} b{b}")
+            check_norms(got[f"{name}_norms"][b:b + 1, :, start:start + n], s64)
+        assert not got[f"{name}_codes"][2].any()               # full: nothing written
+        assert not got[f"{name}_codes"][0, :, 3:].any()
+
+
+@pytest.mark.timeout(300)
+def test_compress_full_size_prefill():
+    """4 x 32768 tokens x 8 KV heads, K and V (heavy-tailed fp16); every
+    vector compressed on the GPU, a seeded sample checked against the
+    oracle, boundary mismatches counted over the sample."""
+    w = synth.WORKLOADS[4]
+    k = synth.kv_tensor(0, w, "k")
+    v = synth.kv_tensor(0, w, "v")
+    got = _run_compress(k, v, w.rotation_seed, w.n_kv_heads, w.context, 0)
+    g = np.random.default_rng(123)
+    idx_b = g.integers(0, w.batch, 2048)
+    idx_h = g.integers(0, w.n_kv_heads, 2048)
+    idx_t = g.integers(0, w.context, 2048)
+    rots = orot.rotation_matrices(orot.make_quaternions(w.rotation_seed, w.n_kv_heads))
+    for name, x in (("k", k), ("v", v)):
+        sample = x[idx_b, idx_h, idx_t]                         # [N][128]
+        ys, codes, s64 = [], [], []
+        for i in range(sample.shape[0]):
+            _, _, c, y, s = ocz.compress(sample[i:i + 1], rots[idx_h[i]], THR)
+            codes.append(c[0]); ys.append(y[0]); s64.append(s[0])
+        check_codes(got[f"{name}_codes"][idx_b, idx_h, idx_t], np.array(codes), np.array(ys),
+                    THR, f"full {name}")
+        check_norms(got[f"{name}_norms"][idx_b, idx_h, idx_t], np.array(s64), f"full {name}")
+    assert np.all(np.isfinite(got["k_norms"])) and np.all(got["k_norms"] > 0)

@@ -1,0 +1,208 @@
+"""GPU parity of iq_decode_attention against the oracle's compressed-space
+decode (App. A), through the C ABI via the PyTorch binding."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as oatt
+from oracle import codebook as ocb
+from oracle import compress as ocz
+from oracle import rotation as orot
+from paper_2608_08081_amd import api, synth
+from tests.parity import check_attention, check_codes
+
+pytestmark = pytest.mark.gpu
+
+LEVELS, THR = ocb.isoquant_codebook(128, 3)
+DEV = torch.device("cuda:0")
+
+
+def _dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def _oracle_cache(w, seed, t, batch, cap):
+    k = synth.kv_tensor(seed, w, "k", n_tokens=cap, batch=batch)
+    v = synth.kv_tensor(seed, w, "v", n_tokens=cap, batch=batch)
+    quats = orot.make_quaternions(w.rotation_seed, w.n_kv_heads)
+    rots = orot.rotation_matrices(quats)
+    kp, kn, *_ = ocz.compress_kv(k, rots, THR)
+    vp, vn, *_ = ocz.compress_kv(v, rots, THR)
+    return k, v, quats, kp, kn, vp, vn
+
+
+def _gpu_decode(q, kp, kn, vp, vn, seq, quats, max_seq_len, scale=0.0, ws=None):
+    out = api.iq_decode_attention(_dev(q), _dev(kp), _dev(kn), _dev(vp), _dev(vn),
+                                  _dev(np.asarray(seq, np.int32)), _dev(quats),
+                                  max_seq_len=max_seq_len, softmax_scale=scale, workspace=ws)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+@pytest.mark.parametrize("hq,hkv,seq", [
+    (1, 1, [1024]),
+    (8, 1, [1, 63, 64, 65]),
+    (32, 4, [777, 0, 513]),
+    (16, 2, [2, 1000]),
+    (6, 2, [300]),
+    (2, 2, [129]),
+])
+def test_decode_parity_on_oracle_cache(hq, hkv, seq):
+    """Decode over caches packed by the oracle (identical packed input on both
+    sides); ragged lengths, an empty sequence, several group sizes."""
+    w = synth.Workload(9, "test", len(seq), hq, hkv, max(seq), "f16", rotation_seed=77)
+    cap = max(max(seq), 1) + 3
+    k, v, quats, kp, kn, vp, vn = _oracle_cache(w, 1, max(seq), len(seq), cap)
+    q = synth.queries(1, w)[0]
+    got = _gpu_decode(q, kp, kn, vp, vn, seq, quats, cap)
+    ref = oatt.decode_fused(q, kp, kn, vp, vn, seq, quats, LEVELS)
+    check_attention(got, ref, f"hq{hq} hkv{hkv}")
+    for b, n in enumerate(seq):
+        if n == 0:
+            assert np.all(got[b] == 0)
+
+
+def test_decode_custom_scale_and_determinism():
+    w = synth.WORKLOADS[1]
+    t = 2000
+    k, v, quats, kp, kn, vp, vn = _oracle_cache(w, 4, t, 1, t)
+    q = synth.queries(4, w)[0]
+    got1 = _gpu_decode(q, kp, kn, vp, vn, [t], quats, t, scale=0.05)
+    got2 = _gpu_decode(q, kp, kn, vp, vn, [t], quats, t, scale=0.05)
+    assert np.array_equal(got1.view(np.uint32), got2.view(np.uint32))
+    ref = oatt.decode_fused(q, kp, kn, vp, vn, [t], quats, LEVELS, scale=0.05)
+    check_attention(got1, ref, "scale 0.05")
+
+
+def test_end_to_end_tiny_config():
+    """Workload 0: fp32 K/V, G = 1, T = 1024: GPU compress then GPU decode,
+    against the oracle's compress + decode."""
+    w = synth.WORKLOADS[0]
+    seed = 0
+    k = synth.kv_tensor(seed, w, "k")
+    v = synth.kv_tensor(seed, w, "v")
+    q = synth.queries(seed, w)[0]
+    quats_t = api.iq_make_rotation(w.rotation_seed, 1).to(DEV)
+    cache = api.alloc_cache(1, 1, w.context, DEV)
+    api.iq_compress_kv(_dev(k), _dev(v), quats_t, cache["k_codes"], cache["k_norms"],
+                       cache["v_codes"], cache["v_norms"])
+    cache["seq_lens"].fill_(w.context)
+    out = api.iq_decode_attention(_dev(q), cache["k_codes"], cache["k_norms"],
+                                  cache["v_codes"], cache["v_norms"], cache["seq_lens"],
+                                  quats_t)
+    torch.cuda.synchronize()
+    quats = orot.make_quaternions(w.rotation_seed, 1)
+    rots = orot.rotation_matrices(quats)
+    kp, kn, kc, ky, _ = ocz.compress_kv(k, rots, THR)
+    vp, vn, *_ = ocz.compress_kv(v, rots, THR)
+    check_codes(cache["k_codes"].cpu().numpy(), kc, ky, THR, "w0 k")
+    ref = oatt.decode_fused(q, kp, kn, vp, vn, [w.context], quats, LEVELS)
+    check_attention(out.cpu().numpy(), ref, "w0")
+
+
+@pytest.mark.timeout(300)
+def test_gqa_append_decode_steps():
+    """Workload 1 shape: bulk-compress 8192 tokens, then (append one token,
+    decode) steps; every decode checked against the oracle on the oracle's
+    own cache of the same tokens."""
+    w = synth.WORKLOADS[1]
+    seed, steps = 2, 6
+    t0 = w.context
+    cap = t0 + steps
+    k = synth.kv_tensor(seed, w, "k")
+    v = synth.kv_tensor(seed, w, "v")
+    kn_new, vn_new = synth.appended_tokens(seed, w, steps)
+    qs = synth.queries(seed, w, steps)
+    quats = orot.make_quaternions(w.rotation_seed, w.n_kv_heads)
+    rots = orot.rotation_matrices(quats)
+    quats_t = _dev(quats)
+    cache = api.alloc_cache(1, w.n_kv_heads, cap, DEV)
+    api.iq_compress_kv(_dev(k), _dev(v), quats_t, cache["k_codes"], cache["k_norms"],
+                       cache["v_codes"], cache["v_norms"])
+    cache["seq_lens"].fill_(t0)
+    ws = api.alloc_workspace(1, w.n_q_heads, w.n_kv_heads, cap, DEV)
+    k_all = np.concatenate([k, kn_new.transpose(1, 2, 0, 3)], axis=2)
+    v_all = np.concatenate([v, vn_new.transpose(1, 2, 0, 3)], axis=2)
+    kp, kn, *_ = ocz.compress_kv(k_all, rots, THR)
+    vp, vn, *_ = ocz.compress_kv(v_all, rots, THR)
+    for s in range(steps):
+        api.iq_append_token(_dev(kn_new[s]), _dev(vn_new[s]), quats_t, cache["k_codes"],
+                            cache["k_norms"], cache["v_codes"], cache["v_norms"],
+                            cache["seq_lens"])
+        out = api.iq_decode_attention(_dev(qs[s]), cache["k_codes"], cache["k_norms"],
+                                      cache["v_codes"], cache["v_norms"], cache["seq_lens"],
+                                      quats_t, workspace=ws, max_seq_len=cap)
+        torch.cuda.synchronize()
+        n = t0 + s + 1
+        ref = oatt.decode_fused(qs[s], kp, kn, vp, vn, [n], quats, LEVELS)
+        check_attention(out.cpu().numpy(), ref, f"step {s}")
+    assert int(cache["seq_lens"].item()) == t0 + steps
+
+
+@pytest.mark.timeout(300)
+def test_long_context_needle():
+    """Workload 2: 32K context, planted key.  GPU compress + decode; every
+    query head checked against the oracle, and the planted head's output
+    equals the planted position's value (softmax argmax kept there)."""
+    w = synth.WORKLOADS[2]
+    seed = 0
+    k = synth.kv_tensor(seed, w, "k")
+    v = synth.kv_tensor(seed, w, "v")
+    q = synth.queries(seed, w)[0]
+    pos = synth.plant_needle(seed, w, k, q)
+    quats = orot.make_quaternions(w.rotation_seed, w.n_kv_heads)
+    rots = orot.rotation_matrices(quats)
+    quats_t = _dev(quats)
+    cache = api.alloc_cache(1, w.n_kv_heads, w.context, DEV)
+    api.iq_compress_kv(_dev(k), _dev(v), quats_t, cache["k_codes"], cache["k_norms"],
+                       cache["v_codes"], cache["v_norms"])
+    cache["seq_lens"].fill_(w.context)
+    out = api.iq_decode_attention(_dev(q), cache["k_codes"], cache["k_norms"],
+                                  cache["v_codes"], cache["v_norms"], cache["seq_lens"],
+                                  quats_t).cpu().numpy()
+    kp, kn, kc, ky, _ = ocz.compress_kv(k, rots, THR)
+    vp, vn, vc, vy, _ = ocz.compress_kv(v, rots, THR)
+    check_codes(cache["k_codes"].cpu().numpy(), kc, ky, THR, "w2 k")
+    check_codes(cache["v_codes"].cpu().numpy(), vc, vy, THR, "w2 v")
+    ref = oatt.decode_fused(q, kp, kn, vp, vn, [w.context], quats, LEVELS)
+    check_attention(out, ref, "w2")
+    for g in range(w.n_kv_heads):
+        h0 = g * w.group
+        s = oatt.fused_scores(q[0, h0:h0 + 1], kp[0, g], kn[0, g], rots[g], LEVELS)[0]
+        assert int(np.argmax(s)) == int(pos[0, g])
+        v_hat = ocz.reconstruct(ocz.unpack(vp[0, g, pos[0, g]]), vn[0, g, pos[0, g]], LEVELS,
+                                rots[g])
+        assert np.max(np.abs(out[0, h0] - v_hat)) <= 2e-3 * np.max(np.abs(v_hat))
+
+
+@pytest.mark.timeout(600)
+def test_varlen_batched_decode_full_size():
+    """Workload 3: 64 sequences, lengths U{2048..32768}, G = 8.  Full GPU
+    compress + decode; a seeded sample of sequences checked against the
+    oracle (all 16 query heads of each)."""
+    w = synth.WORKLOADS[3]
+    seed = 0
+    lens = synth.context_lengths(seed, w)
+    k = synth.kv_tensor(seed, w, "k")
+    v = synth.kv_tensor(seed, w, "v")
+    q = synth.queries(seed, w)[0]
+    quats = orot.make_quaternions(w.rotation_seed, w.n_kv_heads)
+    rots = orot.rotation_matrices(quats)
+    quats_t = _dev(quats)
+    cache = api.alloc_cache(w.batch, w.n_kv_heads, w.context, DEV)
+    kd, vd = _dev(k), _dev(v)
+    api.iq_compress_kv(kd, vd, quats_t, cache["k_codes"], cache["k_norms"], cache["v_codes"],
+                       cache["v_norms"])
+    del kd, vd
+    cache["seq_lens"].copy_(torch.from_numpy(lens))
+    out = api.iq_decode_attention(_dev(q), cache["k_codes"], cache["k_norms"],
+                                  cache["v_codes"], cache["v_norms"], cache["seq_lens"],
+                                  quats_t).cpu().numpy()
+    sample = np.random.default_rng(9).choice(w.batch, 5, replace=False)
+    for b in sample:
+        n = int(lens[b])
+        kp, kn, *_ = ocz.compress_kv(k[b:b + 1, :, :n], rots, THR)
+        vp, vn, *_ = ocz.compress_kv(v[b:b + 1, :, :n], rots, THR)
+        ref = oatt.decode_fused(q[b:b + 1], kp, kn, vp, vn, [n], quats, LEVELS)
+        check_attention(out[b:b + 1], ref, f"w3 b{b} len {n}")
