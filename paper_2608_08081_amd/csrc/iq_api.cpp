@@ -186,6 +186,8 @@ iq_status iq_compress_kv(const void* k, const void* v, iq_dtype dtype, int64_t b
   if (!iq::mul_ok(batch, n_kv_heads) || !iq::mul_ok(batch * n_kv_heads, capacity + 1) ||
       !iq::mul_ok(batch * n_kv_heads * (capacity + 1), kDim))
     return IQ_ERR_INVALID_ARGUMENT;
+  // an empty block is a no-op (empty tensors may carry null data pointers)
+  if (batch == 0 || n_tokens == 0) return IQ_OK;
   if (k == nullptr && v == nullptr) return IQ_ERR_INVALID_ARGUMENT;
   if (quats == nullptr || !iq::aligned(quats, 4)) return IQ_ERR_INVALID_ARGUMENT;
   if (k && (!k_codes || !k_norms || !iq::aligned(k, 16) || !iq::aligned(k_codes, 16) ||
@@ -194,7 +196,6 @@ iq_status iq_compress_kv(const void* k, const void* v, iq_dtype dtype, int64_t b
   if (v && (!v_codes || !v_norms || !iq::aligned(v, 16) || !iq::aligned(v_codes, 16) ||
             !iq::aligned(v_norms, 4)))
     return IQ_ERR_INVALID_ARGUMENT;
-  if (batch == 0 || n_tokens == 0) return IQ_OK;
   const hipError_t e = iq::launch_compress(k, v, dtype, batch, n_kv_heads, n_tokens, quats,
                                            k_codes, k_norms, v_codes, v_norms, capacity,
                                            dst_offset, stream);

@@ -79,6 +79,7 @@ def test_compress_validation():
     assert _compress(hd=64) == 2
     assert _compress(dtype=7) == 2
     assert _compress(k=None, v=None) == 1
+    assert _compress(k=None, v=None, n=0) == 0   # empty: no-op before pointer checks
     assert _compress(quats=None) == 1
     assert _compress(kc=None) == 1
     assert _compress(n=17) == 1                 # beyond capacity
