@@ -44,6 +44,8 @@ def parse():
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
+    p.add_argument("--calibrate-copy-mib", type=int, default=0,
+                   help="also run one plain device copy of this many MiB (counter calibration)")
     return p.parse_args()
 
 
@@ -166,7 +168,7 @@ def main():
     w = synth.WORKLOADS[2]
     nl = args.layers
     total_visits = math.ceil((args.warmup + args.steps) / nl) + 2
-    capacity = args.context + total_visits + 64
+    capacity = (args.context + total_visits + 64 + 63) // 64 * 64
     print(f"# building {nl} layer caches ({args.context} positions each)", file=sys.stderr,
           flush=True)
     quats, layers = make_layers(api, synth, w, nl, args.context, capacity, args.seed, dev)
@@ -181,6 +183,15 @@ def main():
         api.iq_decode_attention(L["q"], c["k_codes"], c["k_norms"], c["v_codes"], c["v_norms"],
                                 c["seq_lens"], quats, out=L["out"], workspace=ws,
                                 max_seq_len=capacity)
+
+    if args.calibrate_copy_mib > 0:
+        # a plain copy kernel of known size, for scaling FETCH_SIZE/WRITE_SIZE
+        src = torch.ones(args.calibrate_copy_mib << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # eager warm-up of every layer once (loads the code object), then capture
     torch.cuda.synchronize()

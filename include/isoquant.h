@@ -31,7 +31,8 @@
  * little-endian bit string (bit n = bit n%8 of byte n/8), LSB first.  Codes
  * number the codebook levels in ascending order.
  * Rotation parameters: fp32 [n_kv_heads][32][2][4]: per SO(4) block the pair
- * (q_L, q_R), each quaternion as (w, x, y, z), 256 floats per head (App. B).
+ * (q_L, q_R), each quaternion as (w, x, y, z), 256 floats per head (App. B);
+ * device copies passed to the kernels must be 16-byte aligned.
  */
 #ifndef ISOQUANT_H_
 #define ISOQUANT_H_
@@ -144,17 +145,16 @@ iq_status iq_append_token(const void* k_new, const void* v_new, iq_dtype dtype,
 
 /*
  * iq_decode_workspace_bytes - size of the device workspace iq_decode_attention
- * needs for these shapes (split-K partial results and combine tickets).
- * Returns 0 for invalid shapes.
+ * needs for these shapes (the split-K partial results).  Returns 0 for
+ * invalid shapes.
  */
 size_t iq_decode_workspace_bytes(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
                                  int64_t max_seq_len, int64_t head_dim);
 
 /*
- * iq_decode_workspace_init - zero-fill a workspace before its first use with
- * iq_decode_attention (a fill kernel on `stream`, safe under graph capture).
- * iq_decode_attention leaves the workspace in that state again when it
- * completes, so one init per allocation suffices.
+ * iq_decode_workspace_init - zero-fill a workspace (a fill kernel on `stream`,
+ * safe under graph capture).  Optional: iq_decode_attention overwrites every
+ * workspace byte it reads within the same call, so it needs no initialization.
  */
 iq_status iq_decode_workspace_init(void* workspace, size_t workspace_bytes,
                                    hipStream_t stream);
@@ -178,8 +178,8 @@ iq_status iq_decode_workspace_init(void* workspace, size_t workspace_bytes,
  * softmax_scale : <= 0 selects 1/sqrt(128).
  * out       : device fp32 [batch][n_q_heads][128], original space.
  * workspace : device, >= iq_decode_workspace_bytes(...) bytes, 256-byte
- *             aligned, zero-filled once by iq_decode_workspace_init.  Calls
- *             that share a workspace must not overlap in time.
+ *             aligned, contents ignored on entry.  Calls that share a
+ *             workspace must not overlap in time.
  * n_q_heads / n_kv_heads must be an integer <= 16.
  */
 iq_status iq_decode_attention(const float* q,

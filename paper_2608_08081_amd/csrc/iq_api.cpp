@@ -189,7 +189,7 @@ iq_status iq_compress_kv(const void* k, const void* v, iq_dtype dtype, int64_t b
   // an empty block is a no-op (empty tensors may carry null data pointers)
   if (batch == 0 || n_tokens == 0) return IQ_OK;
   if (k == nullptr && v == nullptr) return IQ_ERR_INVALID_ARGUMENT;
-  if (quats == nullptr || !iq::aligned(quats, 4)) return IQ_ERR_INVALID_ARGUMENT;
+  if (quats == nullptr || !iq::aligned(quats, 16)) return IQ_ERR_INVALID_ARGUMENT;
   if (k && (!k_codes || !k_norms || !iq::aligned(k, 16) || !iq::aligned(k_codes, 16) ||
             !iq::aligned(k_norms, 4)))
     return IQ_ERR_INVALID_ARGUMENT;
@@ -217,7 +217,7 @@ iq_status iq_append_token(const void* k_new, const void* v_new, iq_dtype dtype, 
     return IQ_ERR_INVALID_ARGUMENT;
   if (k_new == nullptr && v_new == nullptr) return IQ_ERR_INVALID_ARGUMENT;
   if (quats == nullptr || seq_lens == nullptr || !iq::aligned(seq_lens, 4) ||
-      !iq::aligned(quats, 4) || (status_dev && !iq::aligned(status_dev, 4)))
+      !iq::aligned(quats, 16) || (status_dev && !iq::aligned(status_dev, 4)))
     return IQ_ERR_INVALID_ARGUMENT;
   if (k_new && (!k_codes || !k_norms || !iq::aligned(k_new, 16) || !iq::aligned(k_codes, 16) ||
                 !iq::aligned(k_norms, 4)))
@@ -267,7 +267,7 @@ iq_status iq_decode_attention(const float* q, const uint8_t* k_codes, const floa
     return IQ_ERR_INVALID_ARGUMENT;
   if (!iq::aligned(q, 16) || !iq::aligned(k_codes, 16) || !iq::aligned(v_codes, 16) ||
       !iq::aligned(k_norms, 4) || !iq::aligned(v_norms, 4) || !iq::aligned(out, 16) ||
-      !iq::aligned(seq_lens, 4) || !iq::aligned(quats, 4) || !iq::aligned(workspace, 256))
+      !iq::aligned(seq_lens, 4) || !iq::aligned(quats, 16) || !iq::aligned(workspace, 256))
     return IQ_ERR_INVALID_ARGUMENT;
   iq::DecodePlan plan;
   if (!iq::plan_decode(batch, n_q_heads, n_kv_heads, max_seq_len, &plan))

@@ -144,18 +144,55 @@ __global__ __launch_bounds__(64) void compress_kernel(
                   codes + pos * kRecordBytes, norms + pos, cb);
 }
 
-// Append one token per sequence: one single-wave workgroup per sequence,
-// lanes loop over the K and V vectors of every KV head.  seq_lens[b] is read
-// before any write and bumped after a barrier, so every vector of the
-// sequence lands at the same position.
+// Append one token per sequence (latency path): one workgroup per sequence,
+// one wave per vector, lane l holding dims 2l and 2l+1, so the whole
+// Algorithm 1 for a vector is a few dozen instructions deep instead of the
+// ~2.7K-instruction serial chain of the one-lane-per-vector bulk kernel.
+//   Step 1: fp64 sum of squares, wave reduction.
+//   Step 2: H_128 as 7 butterfly stages (stage 1 in-lane, stages 2..7 with
+//           the partner lane l ^ (st/2)), then the SO(4) block of the lane
+//           pair (2 blk, 2 blk + 1).
+//   Step 3: codes against the thresholds scaled by s sqrt(128).
+//   Step 4: lane l's 6-bit field (codes of dims 2l, 2l+1) goes to LDS and
+//           lanes 0..11 assemble the 12 record words.
+// seq_lens[b] is read once before any write and bumped after a barrier.
+constexpr int kAppendMaxWaves = 16;
+
+__device__ __forceinline__ double shfl_xor_f64(double v, int m) {
+  const int2 p = __builtin_bit_cast(int2, v);
+  int2 r;
+  r.x = __shfl_xor(p.x, m);
+  r.y = __shfl_xor(p.y, m);
+  return __builtin_bit_cast(double, r);
+}
+
 template <typename T>
-__global__ __launch_bounds__(64) void append_kernel(
+__device__ __forceinline__ void load_pair(const T* src, int lane, float& a, float& b);
+template <>
+__device__ __forceinline__ void load_pair<__half>(const __half* src, int lane, float& a, float& b) {
+  const uint32_t w = reinterpret_cast<const uint32_t*>(src)[lane];
+  a = __half2float(__ushort_as_half(static_cast<unsigned short>(w & 0xFFFFu)));
+  b = __half2float(__ushort_as_half(static_cast<unsigned short>(w >> 16)));
+}
+template <>
+__device__ __forceinline__ void load_pair<float>(const float* src, int lane, float& a, float& b) {
+  const float2 f = reinterpret_cast<const float2*>(src)[lane];
+  a = f.x;
+  b = f.y;
+}
+
+template <typename T>
+__global__ __launch_bounds__(64 * kAppendMaxWaves) void append_kernel(
     const T* __restrict__ src0, const T* __restrict__ src1, const float* __restrict__ quats,
     uint8_t* __restrict__ codes0, float* __restrict__ norms0, uint8_t* __restrict__ codes1,
     float* __restrict__ norms1, int n_heads, int n_vectors, int64_t capacity,
     int32_t* __restrict__ seq_lens, int32_t* __restrict__ status, Codebook cb) {
   __shared__ int32_t pos_s;
+  __shared__ float qp[kAppendMaxWaves][kQuatFloats];
+  __shared__ uint32_t fld[kAppendMaxWaves][64];
   const int b = blockIdx.x;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int n_waves = blockDim.x >> 6;
   if (threadIdx.x == 0) pos_s = seq_lens[b];
   __syncthreads();
   const int64_t pos = pos_s;
@@ -163,18 +200,77 @@ __global__ __launch_bounds__(64) void append_kernel(
     if (threadIdx.x == 0 && status != nullptr) atomicOr(status, static_cast<int32_t>(IQ_ERR_CAPACITY));
     return;
   }
-  for (int idx = threadIdx.x; idx < n_vectors; idx += 64) {
-    const int which = idx / n_heads;
-    const int h = idx % n_heads;
+  const int rounds = (n_vectors + n_waves - 1) / n_waves;
+  for (int round = 0; round < rounds; ++round) {
+    const int idx = round * n_waves + wave;
+    const bool active = idx < n_vectors;
+    const int which = active ? idx / n_heads : 0;
+    const int h = active ? idx % n_heads : 0;
     const T* src = which ? src1 : src0;
-    uint8_t* codes = which ? codes1 : codes0;
-    float* norms = which ? norms1 : norms0;
     const int64_t bh = static_cast<int64_t>(b) * n_heads + h;
-    const int64_t p = bh * capacity + pos;
-    compress_one<T>(src + bh * kDim, quats + h * kQuatFloats, codes + p * kRecordBytes,
-                    norms + p, cb);
+    float x0 = 0.f, x1 = 0.f;
+    if (active) {
+      load_pair<T>(src + bh * kDim, lane, x0, x1);
+      const float4 qv = reinterpret_cast<const float4*>(quats + static_cast<int64_t>(h) * kQuatFloats)[lane];
+      qp[wave][4 * lane] = qv.x;
+      qp[wave][4 * lane + 1] = qv.y;
+      qp[wave][4 * lane + 2] = qv.z;
+      qp[wave][4 * lane + 3] = qv.w;
+    }
+    // Step 1
+    double ss = static_cast<double>(x0) * static_cast<double>(x0) +
+                static_cast<double>(x1) * static_cast<double>(x1);
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) ss += shfl_xor_f64(ss, m);
+    const double s = sqrt(ss);
+    // Step 2: unnormalized WHT
+    float a = x0 + x1, c = x0 - x1;            // stage 1 (dims 2l, 2l+1)
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) {         // stages 2..7: partner lane l ^ m
+      const float pa = __shfl_xor(a, m), pc = __shfl_xor(c, m);
+      const bool upper = (lane & m) != 0;
+      a = upper ? pa - a : a + pa;
+      c = upper ? pc - c : c + pc;
+    }
+    // SO(4) block blk = lane / 2 covers dims 4 blk .. 4 blk + 3 = (a, c) of
+    // lanes 2 blk and 2 blk + 1
+    const float oa = __shfl_xor(a, 1), oc = __shfl_xor(c, 1);
+    const bool odd = lane & 1;
+    const float z0 = odd ? oa : a, z1 = odd ? oc : c, z2 = odd ? a : oa, z3 = odd ? c : oc;
+    __syncthreads();                          // qp visible
+    float m[4][4];
+    so4_matrix(&qp[wave][8 * (lane >> 1)], m);
+    const int r0 = odd ? 2 : 0;
+    const float y0 = m[r0][0] * z0 + m[r0][1] * z1 + m[r0][2] * z2 + m[r0][3] * z3;
+    const float y1 = m[r0 + 1][0] * z0 + m[r0 + 1][1] * z1 + m[r0 + 1][2] * z2 + m[r0 + 1][3] * z3;
+    // Step 3
+    float thr[7];
+    if (ss > 0.0) {
+      const double sc = s * 11.313708498984760390;
+#pragma unroll
+      for (int j = 0; j < 7; ++j) thr[j] = static_cast<float>(static_cast<double>(cb.thr[j]) * sc);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 7; ++j) thr[j] = cb.thr[j];
+    }
+    fld[wave][lane] = quantize3(y0, thr) | (quantize3(y1, thr) << 3);
+    __syncthreads();                          // fields visible
+    // Step 4: lanes 0..11 build record word w = bits 32w .. 32w+31
+    if (active && lane < kRecordWords) {
+      const int w = lane;
+      uint32_t word = 0u;
+      const int f_lo = (32 * w) / 6, f_hi = (32 * w + 31) / 6;
+      for (int f = f_lo; f <= f_hi && f < 64; ++f) {
+        const int sh = 6 * f - 32 * w;
+        const uint32_t v = fld[wave][f];
+        word |= sh >= 0 ? (v << sh) : (v >> (-sh));
+      }
+      uint8_t* codes = which ? codes1 : codes0;
+      reinterpret_cast<uint32_t*>(codes + (bh * capacity + pos) * kRecordBytes)[w] = word;
+      if (w == 0) (which ? norms1 : norms0)[bh * capacity + pos] = static_cast<float>(s);
+    }
+    __syncthreads();                          // before the next round reuses qp / fld
   }
-  __syncthreads();
   if (threadIdx.x == 0) seq_lens[b] = static_cast<int32_t>(pos + 1);
 }
 
@@ -233,14 +329,16 @@ hipError_t launch_append(const void* k, const void* v, int dtype, int64_t batch,
   uint8_t* c1 = (k && v) ? v_codes : nullptr;
   float* n1 = (k && v) ? v_norms : nullptr;
   const int n_vectors = static_cast<int>(n_heads * (s1 ? 2 : 1));
+  const int waves = n_vectors < kAppendMaxWaves ? n_vectors : kAppendMaxWaves;
+  const dim3 block(static_cast<unsigned>(64 * waves));
   const Codebook& cb = codebook();
   if (dtype == IQ_DTYPE_F16) {
-    hipLaunchKernelGGL(append_kernel<__half>, dim3(static_cast<unsigned>(batch)), dim3(64), 0,
+    hipLaunchKernelGGL(append_kernel<__half>, dim3(static_cast<unsigned>(batch)), block, 0,
                        stream, static_cast<const __half*>(s0), static_cast<const __half*>(s1),
                        quats, c0, n0, c1, n1, static_cast<int>(n_heads), n_vectors, capacity,
                        seq_lens, status, cb);
   } else {
-    hipLaunchKernelGGL(append_kernel<float>, dim3(static_cast<unsigned>(batch)), dim3(64), 0,
+    hipLaunchKernelGGL(append_kernel<float>, dim3(static_cast<unsigned>(batch)), block, 0,
                        stream, static_cast<const float*>(s0), static_cast<const float*>(s1), quats,
                        c0, n0, c1, n1, static_cast<int>(n_heads), n_vectors, capacity, seq_lens,
                        status, cb);

@@ -244,6 +244,20 @@ __global__ __launch_bounds__(kDim) void decode_combine_kernel(
 
 }  // namespace
 
+// Splits of the generic path: aim at >= 1024 workgroups; 64..512 positions.
+static void plan_generic(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len,
+                         int64_t* split_len, int64_t* n_splits) {
+  const int64_t work = batch * n_kv_heads * (max_seq_len > 0 ? max_seq_len : 1);
+  int64_t len = (work + 1023) / 1024;
+  len = ((len + 63) / 64) * 64;
+  if (len < 64) len = 64;
+  if (len > kMaxSplitLen) len = kMaxSplitLen;
+  *split_len = len;
+  *n_splits = max_seq_len > 0 ? (max_seq_len + len - 1) / len : 1;
+}
+
+static size_t round256(size_t x) { return (x + 255) / 256 * 256; }
+
 bool plan_decode(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads, int64_t max_seq_len,
                  DecodePlan* plan) {
   if (batch < 0 || n_kv_heads <= 0 || n_q_heads <= 0 || max_seq_len < 0) return false;
@@ -252,19 +266,25 @@ bool plan_decode(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads, int64_t m
   if (group > kMaxGroup) return false;
   DecodePlan p{};
   p.kernel = 0;
-  // Aim at >= 1024 workgroups over the 256 CUs; splits hold 64..512 positions.
-  const int64_t work = batch * n_kv_heads * (max_seq_len > 0 ? max_seq_len : 1);
-  int64_t len = (work + 1023) / 1024;
-  len = ((len + 63) / 64) * 64;
-  if (len < 64) len = 64;
-  if (len > kMaxSplitLen) len = kMaxSplitLen;
-  p.split_len = len;
-  p.n_splits = max_seq_len > 0 ? (max_seq_len + len - 1) / len : 1;
-  p.partial_bytes = static_cast<size_t>(batch) * n_q_heads * p.n_splits * kPartialFloats * 4;
-  p.partial_bytes = (p.partial_bytes + 255) / 256 * 256;
+  plan_generic(batch, n_kv_heads, max_seq_len, &p.split_len, &p.n_splits);
+  // workspace = split partials of whichever path runs (no other state)
   p.ticket_bytes = 0;
-  p.total_bytes = p.partial_bytes + p.ticket_bytes;
-  if (p.total_bytes == 0) p.total_bytes = 256;
+  p.partial_bytes =
+      round256(static_cast<size_t>(batch) * n_q_heads * p.n_splits * kPartialFloats * 4);
+  size_t need = p.partial_bytes;
+  if (group == 8) {
+    int nb = 0;
+    int64_t splits = 0, len = 0;
+    g8_plan(batch, n_kv_heads, max_seq_len, &nb, &splits, &len);
+    p.g8_batches = nb;
+    p.g8_splits = splits;
+    p.g8_split_len = len;
+    p.g8_partial_bytes = round256(static_cast<size_t>(batch) * n_kv_heads * splits * 8 *
+                                  kPartialFloats * 4);
+    if (p.g8_partial_bytes > need) need = p.g8_partial_bytes;
+  }
+  size_t generic_bytes = p.ticket_bytes + need;
+  p.total_bytes = generic_bytes > 0 ? generic_bytes : 256;
   *plan = p;
   return true;
 }
@@ -277,7 +297,16 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, const uint8_t* 
                          float scale, float* out, void* workspace, hipStream_t stream) {
   if (batch == 0) return hipSuccess;
   const int group = static_cast<int>(n_q_heads / n_kv_heads);
-  float* partials = static_cast<float*>(workspace);
+  const bool aligned16 = (reinterpret_cast<uintptr_t>(k_norms) % 16 == 0) &&
+                         (reinterpret_cast<uintptr_t>(v_norms) % 16 == 0);
+  if (group == 8 && plan.g8_batches > 0 && capacity % 4 == 0 && aligned16) {
+    float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
+    return launch_decode_g8(plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes,
+                            k_norms, v_codes,
+                            v_norms, seq_lens, capacity, max_seq_len, quats, batch, n_kv_heads,
+                            scale, out, parts, stream);
+  }
+  float* partials = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
   const int64_t split_blocks = batch * n_kv_heads * plan.n_splits;
   hipLaunchKernelGGL(decode_split_kernel, dim3(static_cast<unsigned>(split_blocks)),
                      dim3(kSplitThreads), 0, stream, q, k_codes, k_norms, v_codes, v_norms,

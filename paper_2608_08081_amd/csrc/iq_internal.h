@@ -30,12 +30,16 @@ const Codebook& codebook();
 // Split-K plan for one decode call.  Deterministic function of the shapes so
 // that iq_decode_workspace_bytes and iq_decode_attention agree.
 struct DecodePlan {
-  int kernel;             // 0 = generic VALU path, 1 = MFMA path (group 8)
-  int64_t split_len;      // positions per split
-  int64_t n_splits;       // splits per (sequence, KV head)
-  size_t partial_bytes;   // B * H_q * n_splits * 130 floats
-  size_t ticket_bytes;    // one int32 per (sequence, KV head), padded
-  size_t total_bytes;
+  int kernel;               // reserved
+  int64_t split_len;        // generic path: positions per split
+  int64_t n_splits;         // generic path: splits per (sequence, KV head)
+  size_t partial_bytes;     // generic path: B * H_q * n_splits * 130 floats
+  int g8_batches;           // group-8 path: 16-position batches per wave (0 = n/a)
+  int64_t g8_splits;        // group-8 path: splits per (sequence, KV head)
+  int64_t g8_split_len;     // group-8 path: positions per split
+  size_t ticket_bytes;      // reserved (0)
+  size_t g8_partial_bytes;  // group-8 path: B * H_kv * splits * 8 * 130 floats
+  size_t total_bytes;       // max over both paths
 };
 bool plan_decode(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
                  int64_t max_seq_len, DecodePlan* plan);
@@ -61,5 +65,14 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, const uint8_t* 
                          float scale, float* out, void* workspace, hipStream_t stream);
 
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
+
+void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
+             int64_t* n_splits, int64_t* split_len);
+hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const float* q,
+                            const uint8_t* k_codes,
+                            const float* k_norms, const uint8_t* v_codes, const float* v_norms,
+                            const int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                            const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
+                            float* out, float* partials, hipStream_t stream);
 
 }  // namespace iq

@@ -72,5 +72,6 @@ def row_rel_err(got, ref):
 def check_attention(got, ref, label=""):
     err = row_rel_err(got, ref)
     assert np.all(np.isfinite(got)), f"{label}: non-finite output"
+    print(f"[attn] {label}: max row rel err {err.max():.3e}")
     assert np.all(err <= ATTN_RTOL), f"{label}: max row rel err {err.max():.3e}"
     return float(err.max())

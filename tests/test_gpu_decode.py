@@ -109,7 +109,7 @@ def test_gqa_append_decode_steps():
     w = synth.WORKLOADS[1]
     seed, steps = 2, 6
     t0 = w.context
-    cap = t0 + steps
+    cap = t0 + 8
     k = synth.kv_tensor(seed, w, "k")
     v = synth.kv_tensor(seed, w, "v")
     kn_new, vn_new = synth.appended_tokens(seed, w, steps)
@@ -206,3 +206,93 @@ def test_varlen_batched_decode_full_size():
         vp, vn, *_ = ocz.compress_kv(v[b:b + 1, :, :n], rots, THR)
         ref = oatt.decode_fused(q[b:b + 1], kp, kn, vp, vn, [n], quats, LEVELS)
         check_attention(out[b:b + 1], ref, f"w3 b{b} len {n}")
+
+
+@pytest.mark.parametrize("seq", [
+    [1], [15, 16, 17], [63, 64, 65], [255, 256, 257], [511, 512, 513], [1000, 0, 2049],
+    [4095], [4096], [4097],
+])
+def test_group8_matrix_core_path(seq):
+    """Group-8 decode (matrix-core path: capacity a multiple of 4, 16-byte
+    aligned scales) at lengths around every batch/wave/split boundary,
+    several sequences per call, one of them empty."""
+    w = synth.Workload(8, "g8", len(seq), 8 * 2, 2, max(seq), "f16", rotation_seed=5)
+    cap = ((max(max(seq), 1) + 3) // 4) * 4 + 4
+    k, v, quats, kp, kn, vp, vn = _oracle_cache(w, 3, max(seq), len(seq), cap)
+    q = synth.queries(3, w)[0]
+    got = _gpu_decode(q, kp, kn, vp, vn, seq, quats, cap)
+    ref = oatt.decode_fused(q, kp, kn, vp, vn, seq, quats, LEVELS)
+    check_attention(got, ref, f"g8 {seq}")
+    for b, n in enumerate(seq):
+        if n == 0:
+            assert np.all(got[b] == 0)
+
+
+def test_group8_workspace_reuse_and_determinism():
+    """The split tickets are reset by the call that uses them: repeated calls
+    on one workspace, with different shapes, stay correct and bit-identical."""
+    w = synth.Workload(8, "g8", 2, 32, 4, 3000, "f16", rotation_seed=6)
+    cap = 3008
+    k, v, quats, kp, kn, vp, vn = _oracle_cache(w, 5, 3000, 2, cap)
+    q = synth.queries(5, w)[0]
+    ws = api.alloc_workspace(2, 32, 4, cap, DEV)
+    ref = oatt.decode_fused(q, kp, kn, vp, vn, [3000, 1500], quats, LEVELS)
+    outs = [_gpu_decode(q, kp, kn, vp, vn, [3000, 1500], quats, cap, ws=ws) for _ in range(3)]
+    for o in outs:
+        check_attention(o, ref, "reuse")
+        assert np.array_equal(o.view(np.uint32), outs[0].view(np.uint32))
+    # smaller max_seq_len on the same workspace
+    ref2 = oatt.decode_fused(q, kp, kn, vp, vn, [700, 64], quats, LEVELS)
+    got2 = _gpu_decode(q, kp, kn, vp, vn, [700, 64], quats, cap, ws=ws)
+    check_attention(got2, ref2, "reuse small")
+
+
+def test_graph_replay_matches_eager():
+    """Append + decode captured in a HIP graph: every replay (with eager work
+    and synchronizations in between) equals the eager computation on the
+    same cache state."""
+    w = synth.WORKLOADS[1]
+    t0, cap = 1000, 1024
+    k = synth.kv_tensor(7, w, "k", n_tokens=t0)
+    v = synth.kv_tensor(7, w, "v", n_tokens=t0)
+    kn_new, vn_new = synth.appended_tokens(7, w, 1)
+    q = _dev(synth.queries(7, w)[0])
+    quats = _dev(orot.make_quaternions(w.rotation_seed, w.n_kv_heads))
+    caches = []
+    for _ in range(2):
+        c = api.alloc_cache(1, w.n_kv_heads, cap, DEV)
+        api.iq_compress_kv(_dev(k), _dev(v), quats, c["k_codes"], c["k_norms"], c["v_codes"],
+                           c["v_norms"])
+        c["seq_lens"].fill_(t0)
+        caches.append(c)
+    ws_g = api.alloc_workspace(1, w.n_q_heads, w.n_kv_heads, cap, DEV)
+    ws_e = api.alloc_workspace(1, w.n_q_heads, w.n_kv_heads, cap, DEV)
+    kd, vd = _dev(kn_new[0]), _dev(vn_new[0])
+    out_g = torch.empty((1, w.n_q_heads, 128), device=DEV)
+
+    def step(c, out, ws):
+        api.iq_append_token(kd, vd, quats, c["k_codes"], c["k_norms"], c["v_codes"],
+                            c["v_norms"], c["seq_lens"])
+        api.iq_decode_attention(q, c["k_codes"], c["k_norms"], c["v_codes"], c["v_norms"],
+                                c["seq_lens"], quats, out=out, workspace=ws, max_seq_len=cap)
+
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step(caches[0], out_g, ws_g)           # warm-up (eager) on the graph cache
+    torch.cuda.current_stream().wait_stream(s)
+    step(caches[1], torch.empty_like(out_g), ws_e)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(caches[0], out_g, ws_g)
+    for rep in range(4):
+        g.replay()
+        torch.cuda.synchronize()
+        out_e = torch.empty_like(out_g)
+        step(caches[1], out_e, ws_e)
+        torch.cuda.synchronize()
+        assert int(caches[0]["seq_lens"].item()) == int(caches[1]["seq_lens"].item())
+        assert torch.equal(out_g, out_e), f"replay {rep}"
+        assert torch.equal(caches[0]["k_codes"], caches[1]["k_codes"])
