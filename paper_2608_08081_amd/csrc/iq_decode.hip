@@ -299,7 +299,10 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, const uint8_t* 
   const int group = static_cast<int>(n_q_heads / n_kv_heads);
   const bool aligned16 = (reinterpret_cast<uintptr_t>(k_norms) % 16 == 0) &&
                          (reinterpret_cast<uintptr_t>(v_norms) % 16 == 0);
-  if (group == 8 && plan.g8_batches > 0 && capacity % 4 == 0 && aligned16) {
+  // the group-8 kernel addresses one (sequence, KV head) row with 32-bit
+  // byte offsets
+  const bool row32 = capacity * kRecordBytes <= 0x7fffffff;
+  if (group == 8 && plan.g8_batches > 0 && capacity % 4 == 0 && aligned16 && row32) {
     float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
     return launch_decode_g8(plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes,
                             k_norms, v_codes,

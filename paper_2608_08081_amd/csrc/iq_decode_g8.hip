@@ -56,6 +56,7 @@ constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 constexpr int kHeads = 8;                 // query heads per KV head
 constexpr int kPart = 2 + kDim;           // m, l, o[128] per head
+constexpr int kLutStride = 64;            // words between entries of the lane-private tables
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kInvSqrtDim = 0.08838834764831845f;
 
@@ -64,17 +65,14 @@ __device__ __forceinline__ f32x4_t mfma(u32x4_t a, u32x4_t b, f32x4_t c) {
                                                 __builtin_bit_cast(half8_t, b), c, 0, 0, 0);
 }
 
-// 6-bit field F (codes of dims 2F', 2F'+1) of a 96-bit slice w0:w1:w2 at bit 6F.
-template <int F>
-__device__ __forceinline__ uint32_t slice_field(uint32_t w0, uint32_t w1, uint32_t w2) {
-  constexpr int bit = 6 * F, word = bit / 32, off = bit % 32;
+// 6-bit field F (codes of dims 2F', 2F'+1) of a 96-bit slice w0:w1:w2 at bit
+// 6F; F must be a compile-time constant after unrolling.
+__device__ __forceinline__ uint32_t slice_field(int F, uint32_t w0, uint32_t w1, uint32_t w2) {
+  const int bit = 6 * F, word = bit / 32, off = bit % 32;
   const uint32_t lo = word == 0 ? w0 : (word == 1 ? w1 : w2);
-  if constexpr (off <= 26) {
-    return __builtin_amdgcn_ubfe(lo, off, 6);
-  } else {
-    const uint32_t hi = word == 0 ? w1 : w2;
-    return __builtin_amdgcn_alignbit(hi, lo, off) & 63u;
-  }
+  if (off <= 26) return __builtin_amdgcn_ubfe(lo, off, 6);
+  const uint32_t hi = word == 0 ? w1 : w2;
+  return __builtin_amdgcn_alignbit(hi, lo, off) & 63u;
 }
 
 // Workgroup barrier that orders LDS only.  __syncthreads() also fences
@@ -97,42 +95,235 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// Inverse rotation of 8 heads in LDS (buf[h][128], already divided by l):
-// per block z = M^T o_blk, then the normalized WHT, written to dst.
-__device__ void inverse_rotate_store(float* buf, const float* qparam, float* __restrict__ dst,
-                                     int tid) {
-  // 8 heads x 32 blocks = 256 (head, block) tasks, one per thread; qparam
-  // holds the parameters of block tid % 32
-  {
-    const int h = tid >> 5, blk = tid & 31;
-    float m[4][4];
-    so4_matrix(qparam, m);
-    float* o = buf + h * kDim + 4 * blk;
-    const float o0 = o[0], o1 = o[1], o2 = o[2], o3 = o[3];
-    float z[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) z[r] = m[0][r] * o0 + m[1][r] * o1 + m[2][r] * o2 + m[3][r] * o3;
-    o[0] = z[0];
-    o[1] = z[1];
-    o[2] = z[2];
-    o[3] = z[3];
+// Value of lane (lane ^ kM) within the lane's group of 32 lanes (kM < 32):
+// quad permutations through DPP for 1 and 2, the swizzle unit otherwise.
+template <int kM>
+__device__ __forceinline__ float xor_lane(float v) {
+  const int x = __builtin_bit_cast(int, v);
+  if constexpr (kM == 1) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false));
+  } else if constexpr (kM == 2) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false));
+  } else {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(x, (kM << 10) | 0x1F));
   }
-  lds_barrier();
-  for (int st = 1; st < kDim; st <<= 1) {
-    // 8 heads x 64 butterflies per stage, 2 per thread
+}
+
+// One Walsh-Hadamard stage across lanes: the pair (i, i ^ kM) becomes
+// (x_i + x_(i^kM), x_i - x_(i^kM)); blk = this lane's index in its 32-group.
+template <int kM>
+__device__ __forceinline__ void lane_butterfly(f32x4_t& x, int blk) {
+  const float sg = (blk & kM) ? -1.0f : 1.0f;
 #pragma unroll
-    for (int rep = 0; rep < 2; ++rep) {
-      const int e = tid + rep * kThreads;          // 0..511
-      const int h = e >> 6, p = e & 63;
-      const int i = ((p & ~(st - 1)) << 1) | (p & (st - 1));   // lower index of the pair
-      float* v = buf + h * kDim;
-      const float a = v[i], b = v[i + st];
-      v[i] = a + b;
-      v[i + st] = a - b;
+  for (int r = 0; r < 4; ++r) x[r] = __builtin_fmaf(sg, x[r], xor_lane<kM>(x[r]));
+}
+
+// Unnormalized H_32 over the block index held by 32 consecutive lanes (each
+// lane holds its block's 4 entries).  With the in-block H_4 this is H_128:
+// the transform factors over index bits (bits 0..1 inside the block, bits
+// 2..6 = block index).
+__device__ __forceinline__ void lane_wht32(f32x4_t& x, int blk) {
+  lane_butterfly<1>(x, blk);
+  lane_butterfly<2>(x, blk);
+  lane_butterfly<4>(x, blk);
+  lane_butterfly<8>(x, blk);
+  lane_butterfly<16>(x, blk);
+}
+
+// Largest value over the lane's group of 32 lanes.
+__device__ __forceinline__ float group32_max(float v) {
+  v = fmaxf(v, xor_lane<1>(v));
+  v = fmaxf(v, xor_lane<2>(v));
+  v = fmaxf(v, xor_lane<4>(v));
+  v = fmaxf(v, xor_lane<8>(v));
+  v = fmaxf(v, xor_lane<16>(v));
+  return v;
+}
+
+// Forward rotation (App. A) of one head held by 32 lanes, 4 dims per lane:
+// y_blk = M_blk H_4 (H_32 x)_blk, times `scale` (1/sqrt(128) and any score
+// scale).  qparam: this lane's block parameters (q_L, q_R).
+__device__ __forceinline__ f32x4_t rotate_forward(f32x4_t x, const float* qparam, int blk,
+                                                  float scale) {
+  lane_wht32(x, blk);
+  float a = x[0], b = x[1], c = x[2], d = x[3];
+  wht4(a, b, c, d);
+  float m[4][4];
+  so4_matrix(qparam, m);
+  f32x4_t y;
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+    y[r] = (m[r][0] * a + m[r][1] * b + m[r][2] * c + m[r][3] * d) * scale;
+  return y;
+}
+
+// Inverse rotation R^T = H_128 diag(M^T) / sqrt(128) (Table 2 D) of one head
+// held by 32 lanes, 4 dims per lane.
+__device__ __forceinline__ f32x4_t rotate_inverse(f32x4_t o, const float* qparam, int blk) {
+  float m[4][4];
+  so4_matrix(qparam, m);
+  float z[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+    z[r] = m[0][r] * o[0] + m[1][r] * o[1] + m[2][r] * o[2] + m[3][r] * o[3];
+  wht4(z[0], z[1], z[2], z[3]);
+  f32x4_t x = f32x4_t{z[0], z[1], z[2], z[3]};
+  lane_wht32(x, blk);
+  return x * kInvSqrtDim;
+}
+
+// Issues every cache load of one wave: keys, values and both scale arrays
+// of its NB batches of 16 positions, all before any arithmetic.
+//  keys:   lane (t = col, gk = grp) takes dwords 3gk..3gk+2 of position t;
+//  values: lane (u = col, grp) takes 8 bytes covering bytes 3u..3u+2 of
+//          positions 4 grp + r, r = 0..3 (dword vdw = min(3u/4, 10));
+//  scales: one 16-byte load per array (positions 4 grp .. 4 grp + 3).
+// kMasked (the wave reaches past the last position `last` of its split):
+// key positions are clamped to `last`, and value and scale groups to the
+// 4-aligned group holding `last`, which lies inside the row because the
+// capacity is a multiple of 4; the positions past `last` are masked later.
+// Otherwise every address is the lane's base offset plus a constant.
+template <int NB, bool kMasked>
+__device__ __forceinline__ void load_wave(const uint8_t* kc, const float* kn, const uint8_t* vc,
+                                          const float* vn, int wbase, int last, int col, int grp,
+                                          int vdw, uint32_t (&kw)[NB][3],
+                                          uint32_t (&vw)[NB][4][2], f32x4_t (&ks)[NB],
+                                          f32x4_t (&vs)[NB]) {
+  const uint8_t* kn8 = reinterpret_cast<const uint8_t*>(kn);
+  const uint8_t* vn8 = reinterpret_cast<const uint8_t*>(vn);
+  const uint32_t koff = static_cast<uint32_t>((wbase + col) * kRecordBytes + 12 * grp);
+  const uint32_t voff = static_cast<uint32_t>((wbase + 4 * grp) * kRecordBytes + 4 * vdw);
+  const uint32_t soff = static_cast<uint32_t>(4 * (wbase + 4 * grp));
+  const int last4 = last & ~3;
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const uint32_t* p;
+    const uint8_t* sk;
+    if constexpr (kMasked) {
+      const int t = wbase + 16 * i + col < last ? wbase + 16 * i + col : last;
+      p = reinterpret_cast<const uint32_t*>(kc +
+                                            static_cast<uint32_t>(t * kRecordBytes + 12 * grp));
+      const int t4 = wbase + 16 * i + 4 * grp < last4 ? wbase + 16 * i + 4 * grp : last4;
+      sk = kn8 + static_cast<uint32_t>(4 * t4);
+    } else {
+      p = reinterpret_cast<const uint32_t*>(kc + koff + 16 * kRecordBytes * i);
+      sk = kn8 + soff + 64 * i;
     }
-    lds_barrier();
+    kw[i][0] = p[0];
+    kw[i][1] = p[1];
+    kw[i][2] = p[2];
+    ks[i] = *reinterpret_cast<const f32x4_t*>(sk);
   }
-  for (int e = tid; e < kHeads * kDim; e += kThreads) dst[e] = buf[e] * kInvSqrtDim;
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const uint8_t* pv;
+    const uint8_t* sv;
+    if constexpr (kMasked) {
+      const int t4 = wbase + 16 * i + 4 * grp < last4 ? wbase + 16 * i + 4 * grp : last4;
+      pv = vc + static_cast<uint32_t>(t4 * kRecordBytes + 4 * vdw);
+      sv = vn8 + static_cast<uint32_t>(4 * t4);
+    } else {
+      pv = vc + voff + 16 * kRecordBytes * i;
+      sv = vn8 + soff + 64 * i;
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const u32x2_a4_t d = *reinterpret_cast<const u32x2_a4_t*>(pv + kRecordBytes * r);
+      vw[i][r][0] = d[0];
+      vw[i][r][1] = d[1];
+    }
+    vs[i] = *reinterpret_cast<const f32x4_t*>(sv);
+  }
+}
+
+// Scores, softmax and value accumulation of one wave over its NB batches
+// (kMasked: some positions of the wave lie past the end of the split).
+template <int NB, bool kMasked>
+__device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
+                                            const uint32_t (&vw)[NB][4][2],
+                                            const f32x4_t (&ks)[NB], const f32x4_t (&vs)[NB],
+                                            const u32x4_t (&qhi)[4], const u32x4_t (&qlo)[4],
+                                            const uint32_t* lutl, int col, int grp, int nvalid,
+                                            uint32_t vshift, float qdown, float& m_run,
+                                            float& l_run, float& vmax, f32x4_t (&o_acc)[4]) {
+  // ---- phase 1: scores (Table 2 A) -----------------------------------------
+  f32x4_t sc[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const uint32_t w0 = kw[i][0], w1 = kw[i][1], w2 = kw[i][2];
+    u32x4_t a[4];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      a[kb] = u32x4_t{lutl[kLutStride * slice_field(kb * 4 + 0, w0, w1, w2)],
+                      lutl[kLutStride * slice_field(kb * 4 + 1, w0, w1, w2)],
+                      lutl[kLutStride * slice_field(kb * 4 + 2, w0, w1, w2)],
+                      lutl[kLutStride * slice_field(kb * 4 + 3, w0, w1, w2)]};
+    }
+    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      acc = mfma(a[kb], qhi[kb], acc);
+      acc = mfma(a[kb], qlo[kb], acc);
+    }
+    // lane (col, grp) holds positions 16 i + 4 grp + r of head col % 8
+    const f32x4_t kq = ks[i] * qdown;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float s = acc[r] * kq[r];
+      if constexpr (kMasked) {
+        const bool ok = 16 * i + 4 * grp + r < nvalid;
+        s = ok ? s : -INFINITY;
+        vmax = fmaxf(vmax, ok ? vs[i][r] : 0.f);
+      } else {
+        vmax = fmaxf(vmax, vs[i][r]);
+      }
+      sc[i][r] = s;
+      m_run = fmaxf(m_run, s);
+    }
+  }
+  m_run = wave_max(m_run);
+  vmax = wave_max(vmax);
+  // weights scaled by 2^15 / vmax: in [0, 2^15], fp16-normal down to ~2e-9 of
+  // the largest weight; split into fp16 hi + lo parts
+  const float vinv = vmax > 0.f ? 32768.0f * __builtin_amdgcn_rcpf(vmax) : 0.f;
+  const uint32_t slot_shift = (col >= 8) ? 16u : 0u;
+
+  // ---- phase 2: weights (Table 2 B) and values (Table 2 C) -----------------
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    f32x4_t wv = vs[i] * vinv;
+    if constexpr (kMasked) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) wv[r] = (16 * i + 4 * grp + r < nvalid) ? wv[r] : 0.f;
+    }
+    u32x4_t pw_hi, pw_lo;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float e = __builtin_amdgcn_exp2f(sc[i][r] - m_run);
+      l_run += e;
+      const float pf = e * wv[r];
+      const _Float16 ph = static_cast<_Float16>(pf);
+      const _Float16 pl = static_cast<_Float16>(pf - static_cast<float>(ph));
+      pw_hi[r] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, ph)) << slot_shift;
+      pw_lo[r] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, pl)) << slot_shift;
+    }
+    u32x4_t vb[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const uint32_t lo = col == 15 ? vw[i][r][1] : vw[i][r][0];
+      const uint32_t win = __builtin_amdgcn_alignbit(vw[i][r][1], lo, vshift);
+      vb[0][r] = lutl[kLutStride * (win & 63u)];
+      vb[1][r] = lutl[kLutStride * __builtin_amdgcn_ubfe(win, 6, 6)];
+      vb[2][r] = lutl[kLutStride * __builtin_amdgcn_ubfe(win, 12, 6)];
+      vb[3][r] = lutl[kLutStride * __builtin_amdgcn_ubfe(win, 18, 6)];
+    }
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+      o_acc[nb] = mfma(pw_hi, vb[nb], o_acc[nb]);
+      o_acc[nb] = mfma(pw_lo, vb[nb], o_acc[nb]);
+    }
+  }
+  l_run = wave_sum(l_run);
 }
 
 template <int NB>
@@ -141,13 +332,20 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     const float* __restrict__ k_norms, const uint8_t* __restrict__ v_codes,
     const float* __restrict__ v_norms, const int32_t* __restrict__ seq_lens,
     const float* __restrict__ quats, float* __restrict__ partials, float* __restrict__ out,
-    int64_t capacity, int64_t max_seq_len, int n_kv_heads, int n_splits, int split_len,
+    int64_t capacity, int max_seq_len, int n_kv_heads, int n_splits, int split_len,
     float qscale, Codebook cb) {
-  __shared__ uint32_t lut[64];
-  __shared__ float qbuf[kHeads * kDim];
-  __shared__ float wave_o[kWaves][kHeads * kDim];
+  constexpr int kQRow = kDim / 2 + 4;   // fp16-pair row of one head, padded (68 words)
+  __shared__ uint32_t lut64[64];
+  // 64 copies of the 64-entry table: entry e of copy l at word 64 e + l, so
+  // lane l always reads bank l (random codes make shared-table lookups
+  // conflict); after the last lookup the same memory holds the per-wave
+  // outputs
+  static_assert(kWaves * kHeads * kDim == kLutStride * 64, "table / output aliasing");
+  __shared__ __attribute__((aligned(16))) uint32_t big[kLutStride * 64];
+  __shared__ __attribute__((aligned(16))) uint32_t qop[2][kHeads][kQRow];
+  __shared__ int qexp_s[kHeads];
+  float(*wave_o)[kHeads * kDim] = reinterpret_cast<float(*)[kHeads * kDim]>(big);
   __shared__ float wave_ml[kWaves][2][kHeads];
-  __shared__ float qmax_s[kWaves];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -159,22 +357,26 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   const int b = bg / n_kv_heads;
   const int n_q_heads = n_kv_heads * kHeads;
 
-  int64_t seq = seq_lens[b];
-  if (seq > max_seq_len) seq = max_seq_len;
-  if (seq < 0) seq = 0;
-  const int used = static_cast<int>((seq + split_len - 1) / split_len);
-  float* out_bg = out + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * kHeads) * kDim;
+  int seq = seq_lens[b];
+  seq = seq > max_seq_len ? max_seq_len : (seq < 0 ? 0 : seq);
+  const int used = (seq + split_len - 1) / split_len;
+  float* out_bg =
+      out + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * kHeads) * kDim;
   if (split >= used) {
     if (seq == 0 && split == 0)
       for (int e = tid; e < kHeads * kDim; e += kThreads) out_bg[e] = 0.f;
     return;
   }
-  const int64_t start = static_cast<int64_t>(split) * split_len;
-  const int64_t end = seq < start + split_len ? seq : start + split_len;
-  const int64_t wbase = start + static_cast<int64_t>(wave) * NB * 16;   // first position of the wave
-  const int64_t last = end - 1;                                           // last position of the split
-  const int64_t last4 = last & ~static_cast<int64_t>(3);
-  const int64_t row = (static_cast<int64_t>(b) * n_kv_heads + g) * capacity;
+  const int start = split * split_len;
+  const int end = seq < start + split_len ? seq : start + split_len;
+  const int wbase = start + wave * NB * 16;   // first position of the wave
+  const int last = end - 1;                   // last position of the split
+  // (b, g) row bases (wave-uniform); lane offsets in 32 bits (capacity * 48 < 2^31)
+  const int64_t row = static_cast<int64_t>(bg) * capacity;
+  const uint8_t* kc = k_codes + row * kRecordBytes;
+  const uint8_t* vc = v_codes + row * kRecordBytes;
+  const float* kn = k_norms + row;
+  const float* vn = v_norms + row;
 
   // ---- issue every load of the wave -------------------------------------
   // the group's 8 query heads first (one float4 per thread), then the cache
@@ -190,217 +392,101 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     qparam[0] = p0[0]; qparam[1] = p0[1]; qparam[2] = p0[2]; qparam[3] = p0[3];
     qparam[4] = p1[0]; qparam[5] = p1[1]; qparam[6] = p1[2]; qparam[7] = p1[3];
   }
-  // keys: lane (t = col, gk = grp) takes dwords 3gk..3gk+2 of position t
   uint32_t kw[NB][3];
-  // values: lane (u = col, grp) takes 8 bytes covering bytes 3u..3u+2 of
-  // positions 4 grp + r, r = 0..3
   uint32_t vw[NB][4][2];
   f32x4_t ks[NB], vs[NB];
   const int vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
-  const uint32_t vshift = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));   // 0..40
-  // keys and key scales of every batch first: the score phase can start on
-  // the first batch while the values are still arriving
-#pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    const int64_t base = wbase + 16 * i;
-    int64_t t = base + col;
-    t = t < last ? t : last;
-    const uint32_t* p = reinterpret_cast<const uint32_t*>(k_codes + (row + t) * kRecordBytes) + 3 * grp;
-    kw[i][0] = p[0];
-    kw[i][1] = p[1];
-    kw[i][2] = p[2];
-    // one 16-byte load of scales; the 4-aligned group holding the last valid
-    // position is the furthest one read (capacity % 4 == 0); positions past
-    // the end are masked below
-    int64_t t4 = base + 4 * grp;
-    t4 = t4 < last4 ? t4 : last4;
-    ks[i] = *reinterpret_cast<const f32x4_t*>(k_norms + row + t4);
-  }
-#pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    const int64_t base = wbase + 16 * i;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      int64_t t = base + 4 * grp + r;
-      t = t < last ? t : last;
-      const u32x2_a4_t d =
-          *reinterpret_cast<const u32x2_a4_t*>(v_codes + (row + t) * kRecordBytes + 4 * vdw);
-      vw[i][r][0] = d[0];
-      vw[i][r][1] = d[1];
-    }
-    int64_t t4 = base + 4 * grp;
-    t4 = t4 < last4 ? t4 : last4;
-    vs[i] = *reinterpret_cast<const f32x4_t*>(v_norms + row + t4);
-  }
+  const uint32_t vshift = static_cast<uint32_t>(8 * (3 * col - 4 * vdw)) & 31u;   // col 15: 40 -> 8
+  const int nvalid = end - wbase;   // valid positions of this wave (may be <= 0)
+  if (nvalid >= NB * 16)
+    load_wave<NB, false>(kc, kn, vc, vn, wbase, last, col, grp, vdw, kw, vw, ks, vs);
+  else
+    load_wave<NB, true>(kc, kn, vc, vn, wbase, last, col, grp, vdw, kw, vw, ks, vs);
 
   // ---- while the loads fly: LUT and the rotated query --------------------
   if (tid < 64) {
     const uint32_t lo = __builtin_bit_cast(uint16_t, static_cast<_Float16>(cb.level[tid & 7]));
     const uint32_t hi = __builtin_bit_cast(uint16_t, static_cast<_Float16>(cb.level[tid >> 3]));
-    lut[tid] = lo | (hi << 16);
+    lut64[tid] = lo | (hi << 16);
   }
-  qbuf[4 * tid] = qv[0];
-  qbuf[4 * tid + 1] = qv[1];
-  qbuf[4 * tid + 2] = qv[2];
-  qbuf[4 * tid + 3] = qv[3];
-  lds_barrier();
-  // forward rotation q_tilde = diag(M) H q (App. A), scaled by qscale
-  for (int st = 1; st < kDim; st <<= 1) {
-#pragma unroll
-    for (int rep = 0; rep < 2; ++rep) {
-      const int e = tid + rep * kThreads;
-      const int h = e >> 6, p = e & 63;
-      const int i = ((p & ~(st - 1)) << 1) | (p & (st - 1));
-      float* v = qbuf + h * kDim;
-      const float a = v[i], bb = v[i + st];
-      v[i] = a + bb;
-      v[i + st] = a - bb;
-    }
-    lds_barrier();
-  }
-  {
-    const int h = tid >> 5, blk = tid & 31;
-    float m[4][4];
-    so4_matrix(qparam, m);
-    float* z = qbuf + h * kDim + 4 * blk;
-    const float s = kInvSqrtDim * qscale;
-    const float z0 = z[0] * s, z1 = z[1] * s, z2 = z[2] * s, z3 = z[3] * s;
-    float y[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) y[r] = m[r][0] * z0 + m[r][1] * z1 + m[r][2] * z2 + m[r][3] * z3;
-    z[0] = y[0];
-    z[1] = y[1];
-    z[2] = y[2];
-    z[3] = y[3];
-    float am = fmaxf(fmaxf(fabsf(y[0]), fabsf(y[1])), fmaxf(fabsf(y[2]), fabsf(y[3])));
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) am = fmaxf(am, __shfl_xor(am, o));
-    if (lane == 0) qmax_s[wave] = am;
-  }
-  lds_barrier();
-  // fp16 operands are kept in the normal range by exact power-of-two
-  // scaling: the rotated queries so that the largest entry is below 2^14
-  // (hi and lo parts both normal), undone on the scores.
+  // thread = (head qh, SO(4) block qblk); the 32 blocks of a head are 32
+  // consecutive lanes of one wave, so the rotation needs no barrier
+  const int qh = tid >> 5, qblk = tid & 31;
+  const f32x4_t y = rotate_forward(qv, qparam, qblk, kInvSqrtDim * qscale);
+  // fp16 operands are kept in the normal range by an exact power-of-two
+  // scale per head: the largest rotated entry is brought below 2^14 (hi and
+  // lo parts both normal) and the scale is undone on the scores
   int qexp = 0;
   {
-    const float am = fmaxf(fmaxf(qmax_s[0], qmax_s[1]), fmaxf(qmax_s[2], qmax_s[3]));
+    const float am = group32_max(
+        fmaxf(fmaxf(fabsf(y[0]), fabsf(y[1])), fmaxf(fabsf(y[2]), fabsf(y[3]))));
     if (am > 0.f) {
       int e = 0;
-      frexpf(am, &e);                      // am < 2^e
+      frexpf(am, &e);   // am < 2^e
       qexp = 14 - e;
       qexp = qexp > 100 ? 100 : (qexp < -100 ? -100 : qexp);
     }
   }
-  const float qup = ldexpf(1.0f, qexp), qdown = ldexpf(1.0f, -qexp);
-  // QK B operands: column col -> head col % 8; MFMA kb, lane group grp ->
-  // dims 32 grp + 8 kb + 0..7; hi and lo fp16 parts.
-  u32x4_t qhi[4], qlo[4];
   {
-    const float* qh = qbuf + (col & 7) * kDim + 32 * grp;
+    // fp16 hi and lo pairs of this thread's 4 dims, stored once per workgroup
+    const float qup = ldexpf(1.0f, qexp);
+    uint32_t hw[2], lw[2];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float x0 = qh[8 * kb + 2 * j] * qup, x1 = qh[8 * kb + 2 * j + 1] * qup;
-        const _Float16 h0 = static_cast<_Float16>(x0), h1 = static_cast<_Float16>(x1);
-        const _Float16 l0 = static_cast<_Float16>(x0 - static_cast<float>(h0));
-        const _Float16 l1 = static_cast<_Float16>(x1 - static_cast<float>(h1));
-        qhi[kb][j] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h0)) |
-                     (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h1)) << 16);
-        qlo[kb][j] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, l0)) |
-                     (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, l1)) << 16);
-      }
+    for (int j = 0; j < 2; ++j) {
+      const float x0 = y[2 * j] * qup, x1 = y[2 * j + 1] * qup;
+      const _Float16 h0 = static_cast<_Float16>(x0), h1 = static_cast<_Float16>(x1);
+      const _Float16 l0 = static_cast<_Float16>(x0 - static_cast<float>(h0));
+      const _Float16 l1 = static_cast<_Float16>(x1 - static_cast<float>(h1));
+      hw[j] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h0)) |
+              (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h1)) << 16);
+      lw[j] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, l0)) |
+              (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, l1)) << 16);
     }
+    qop[0][qh][2 * qblk] = hw[0];
+    qop[0][qh][2 * qblk + 1] = hw[1];
+    qop[1][qh][2 * qblk] = lw[0];
+    qop[1][qh][2 * qblk + 1] = lw[1];
+    if (qblk == 0) qexp_s[qh] = qexp;
   }
+  lds_barrier();   // lut64, qop, qexp_s
+#pragma unroll
+  for (int j = 0; j < 64 / kWaves; ++j) {
+    const int e = wave + kWaves * j;
+    big[kLutStride * e + lane] = lut64[e];
+  }
+  // QK B operands: column col -> head col % 8; MFMA kb, lane group grp ->
+  // dims 32 grp + 8 kb + 0..7 (fp16 pair words 16 grp + 4 kb .. +3)
+  u32x4_t qhi[4], qlo[4];
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) {
+    qhi[kb] = *reinterpret_cast<const u32x4_t*>(&qop[0][col & 7][16 * grp + 4 * kb]);
+    qlo[kb] = *reinterpret_cast<const u32x4_t*>(&qop[1][col & 7][16 * grp + 4 * kb]);
+  }
+  const float qdown = ldexpf(1.0f, -qexp_s[col & 7]);
+  lds_barrier();   // lane-private tables
 
-  const int64_t nvalid = end - wbase;   // valid positions of this wave (may be <= 0)
   float m_run = -INFINITY, l_run = 0.f, vmax = 0.f;
   f32x4_t o_acc[4];
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  if (nvalid > 0) {
-    // ---- phase 1: scores ---------------------------------------------------
-    f32x4_t sc[NB];
-#pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const uint32_t w0 = kw[i][0], w1 = kw[i][1], w2 = kw[i][2];
-      u32x4_t a[4];
-      a[0] = u32x4_t{lut[slice_field<0>(w0, w1, w2)], lut[slice_field<1>(w0, w1, w2)],
-                     lut[slice_field<2>(w0, w1, w2)], lut[slice_field<3>(w0, w1, w2)]};
-      a[1] = u32x4_t{lut[slice_field<4>(w0, w1, w2)], lut[slice_field<5>(w0, w1, w2)],
-                     lut[slice_field<6>(w0, w1, w2)], lut[slice_field<7>(w0, w1, w2)]};
-      a[2] = u32x4_t{lut[slice_field<8>(w0, w1, w2)], lut[slice_field<9>(w0, w1, w2)],
-                     lut[slice_field<10>(w0, w1, w2)], lut[slice_field<11>(w0, w1, w2)]};
-      a[3] = u32x4_t{lut[slice_field<12>(w0, w1, w2)], lut[slice_field<13>(w0, w1, w2)],
-                     lut[slice_field<14>(w0, w1, w2)], lut[slice_field<15>(w0, w1, w2)]};
-      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        acc = mfma(a[kb], qhi[kb], acc);
-        acc = mfma(a[kb], qlo[kb], acc);
-      }
-      // lane (col, grp) now holds positions 16 i + 4 grp + r of head col % 8
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t p = 16 * i + 4 * grp + r;
-        float s = acc[r] * (ks[i][r] * qdown);
-        if (p >= nvalid) s = -INFINITY;
-        sc[i][r] = s;
-        m_run = fmaxf(m_run, s);
-        if (p < nvalid) vmax = fmaxf(vmax, vs[i][r]);
-      }
-    }
-    m_run = wave_max(m_run);
-    vmax = wave_max(vmax);
-    // weights scaled by 2^15 / vmax: in [0, 2^15], fp16-normal down to
-    // ~2e-9 of the largest weight; split into fp16 hi + lo parts
-    const float vinv = vmax > 0.f ? 32768.0f / vmax : 0.f;
-
-    // ---- phase 2: weights and values ---------------------------------------
-    const uint32_t slot_shift = (col >= 8) ? 16u : 0u;
-#pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      u32x4_t pw_hi, pw_lo;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float e = __builtin_amdgcn_exp2f(sc[i][r] - m_run);
-        l_run += e;
-        const float sv = (16 * i + 4 * grp + r < nvalid) ? vs[i][r] : 0.f;
-        const float pf = e * (sv * vinv);
-        const _Float16 ph = static_cast<_Float16>(pf);
-        const _Float16 pl = static_cast<_Float16>(pf - static_cast<float>(ph));
-        pw_hi[r] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, ph)) << slot_shift;
-        pw_lo[r] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, pl)) << slot_shift;
-      }
-      u32x4_t vb[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const uint32_t lo = col == 15 ? vw[i][r][1] : vw[i][r][0];
-        const uint32_t win = __builtin_amdgcn_alignbit(vw[i][r][1], lo, vshift & 31u);
-        vb[0][r] = lut[win & 63u];
-        vb[1][r] = lut[__builtin_amdgcn_ubfe(win, 6, 6)];
-        vb[2][r] = lut[__builtin_amdgcn_ubfe(win, 12, 6)];
-        vb[3][r] = lut[__builtin_amdgcn_ubfe(win, 18, 6)];
-      }
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        o_acc[nb] = mfma(pw_hi, vb[nb], o_acc[nb]);
-        o_acc[nb] = mfma(pw_lo, vb[nb], o_acc[nb]);
-      }
-    }
-    l_run = wave_sum(l_run);
-  }
+  if (nvalid >= NB * 16)
+    attend_wave<NB, false>(kw, vw, ks, vs, qhi, qlo, big + lane, col, grp, nvalid, vshift,
+                           qdown, m_run, l_run, vmax, o_acc);
+  else if (nvalid > 0)
+    attend_wave<NB, true>(kw, vw, ks, vs, qhi, qlo, big + lane, col, grp, nvalid, vshift,
+                          qdown, m_run, l_run, vmax, o_acc);
 
   // ---- merge the 4 waves in LDS ---------------------------------------------
+  lds_barrier();   // every wave is done with the tables
   // lane (u = col, grp) holds rows 4 grp + r = (head (4 grp + r) % 8, slot
   // grp / 2) of MFMA nb, i.e. dim 2 (4 u + nb) + slot.
+  const float oscale = vmax * (1.0f / 32768.0f);
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int h = (4 * grp + r) & 7, s = grp >> 1;
-      wave_o[wave][h * kDim + 8 * col + 2 * nb + s] = o_acc[nb][r] * (vmax * (1.0f / 32768.0f));
+      const int h = (4 * grp + r) & 7, sl = grp >> 1;
+      wave_o[wave][h * kDim + 8 * col + 2 * nb + sl] = o_acc[nb][r] * oscale;
     }
   if (lane < kHeads) {
     wave_ml[wave][0][lane] = m_run;     // lanes 0..7 hold heads 0..7
@@ -413,31 +499,22 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   float M = -INFINITY;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wave_ml[w][0][mh]);
-  float L = 0.f, O0 = 0.f, O1 = 0.f, O2 = 0.f, O3 = 0.f;
+  float L = 0.f;
+  f32x4_t O = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) {
     const float mw = wave_ml[w][0][mh];
     const float c = (mw == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mw - M);
     L += c * wave_ml[w][1][mh];
-    const float* ow = wave_o[w] + mh * kDim + md;
-    O0 += c * ow[0];
-    O1 += c * ow[1];
-    O2 += c * ow[2];
-    O3 += c * ow[3];
+    O += c * *reinterpret_cast<const f32x4_t*>(wave_o[w] + mh * kDim + md);
   }
 
   if (used == 1) {
-    const float il = 1.0f / L;
-    float* ob = qbuf + mh * kDim + md;
-    ob[0] = O0 * il;
-    ob[1] = O1 * il;
-    ob[2] = O2 * il;
-    ob[3] = O3 * il;
-    lds_barrier();
-    inverse_rotate_store(qbuf, qparam, out_bg, tid);
+    // thread (mh, md / 4) holds block md / 4 of head mh: rotate back in place
+    const f32x4_t o = rotate_inverse(O * (1.0f / L), qparam, tid & 31);
+    *reinterpret_cast<f32x4_t*>(out_bg + mh * kDim + md) = o;
     return;
   }
-
   // ---- partial result of this split ------------------------------------------
   float* pp = partials + (static_cast<int64_t>(bg) * n_splits + split) * (kHeads * kPart) +
               mh * kPart;
@@ -445,7 +522,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     pp[0] = M;
     pp[1] = L;
   }
-  *reinterpret_cast<f32x4_t*>(pp + 2 + md) = f32x4_t{O0, O1, O2, O3};
+  *reinterpret_cast<f32x4_t*>(pp + 2 + md) = O;
 }
 
 // Merge of the split partials of one (sequence b, query head h): one
@@ -458,9 +535,8 @@ __global__ __launch_bounds__(kThreads) void merge_g8_kernel(
     const float* __restrict__ quats, float* __restrict__ out, int64_t max_seq_len,
     int n_kv_heads, int n_splits, int split_len) {
   constexpr int kUnroll = 16;
-  __shared__ float red_o[8][kDim];
+  __shared__ __attribute__((aligned(16))) float red_o[8][kDim];
   __shared__ float red_m[8], red_l[8];
-  __shared__ float obuf[kDim];
   const int tid = threadIdx.x;
   const int n_q_heads = n_kv_heads * kHeads;
   const int h = blockIdx.x % n_q_heads;
@@ -472,7 +548,8 @@ __global__ __launch_bounds__(kThreads) void merge_g8_kernel(
   const int used = static_cast<int>((seq + split_len - 1) / split_len);
   if (used <= 1) return;   // empty sequence or a single split: written by the split kernel
   const int sg = tid >> 5, dq = tid & 31;
-  const float* base = partials + static_cast<int64_t>(b * n_kv_heads + g) * n_splits * (kHeads * kPart) +
+  const float* base = partials +
+                      static_cast<int64_t>(b * n_kv_heads + g) * n_splits * (kHeads * kPart) +
                       hh * kPart;
   // block parameters for the inverse rotation (threads 0..31: block tid)
   float qparam[8];
@@ -524,42 +601,19 @@ __global__ __launch_bounds__(kThreads) void merge_g8_kernel(
   red_o[sg][4 * dq + 3] = c * O[3];
   if (dq == 0) red_l[sg] = c * L;
   lds_barrier();
-  if (tid < kDim) {
-    float o = 0.f, l = 0.f;
+  // lanes 0..31 of wave 0: block tid of the head, divided by the sum, then
+  // the inverse rotation in registers
+  if (tid < 32) {
+    f32x4_t o = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float l = 0.f;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      o += red_o[j][tid];
+      o += *reinterpret_cast<const f32x4_t*>(&red_o[j][4 * tid]);
       l += red_l[j];
     }
-    obuf[tid] = o / l;
+    *reinterpret_cast<f32x4_t*>(out + (static_cast<int64_t>(b) * n_q_heads + h) * kDim + 4 * tid) =
+        rotate_inverse(o * (1.0f / l), qparam, tid);
   }
-  lds_barrier();
-  // inverse rotation: z = M^T o per block, then the normalized WHT
-  if (tid < 32) {
-    float m[4][4];
-    so4_matrix(qparam, m);
-    float* ob = obuf + 4 * tid;
-    const float o0 = ob[0], o1 = ob[1], o2 = ob[2], o3 = ob[3];
-    float z[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) z[r] = m[0][r] * o0 + m[1][r] * o1 + m[2][r] * o2 + m[3][r] * o3;
-    ob[0] = z[0];
-    ob[1] = z[1];
-    ob[2] = z[2];
-    ob[3] = z[3];
-  }
-  lds_barrier();
-  for (int st = 1; st < kDim; st <<= 1) {
-    if (tid < 64) {
-      const int i = ((tid & ~(st - 1)) << 1) | (tid & (st - 1));
-      const float a = obuf[i], bb = obuf[i + st];
-      obuf[i] = a + bb;
-      obuf[i + st] = a - bb;
-    }
-    lds_barrier();
-  }
-  if (tid < kDim)
-    out[(static_cast<int64_t>(b) * n_q_heads + h) * kDim + tid] = obuf[tid] * kInvSqrtDim;
 }
 
 }  // namespace
@@ -599,7 +653,8 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   const Codebook& cb = codebook();
 #define IQ_LAUNCH_G8(NB_)                                                                        \
   hipLaunchKernelGGL(decode_g8_kernel<NB_>, grid, block, 0, stream, q, k_codes, k_norms,       \
-                     v_codes, v_norms, seq_lens, quats, partials, out, capacity, max_seq_len,  \
+                     v_codes, v_norms, seq_lens, quats, partials, out, capacity,               \
+                     static_cast<int>(max_seq_len),                                              \
                      static_cast<int>(n_kv_heads), static_cast<int>(n_splits),                \
                      static_cast<int>(split_len), qscale, cb)
   switch (nb) {
