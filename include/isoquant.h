@@ -192,6 +192,38 @@ iq_status iq_decode_attention(const float* q,
                               void* workspace, size_t workspace_bytes,
                               hipStream_t stream);
 
+/*
+ * iq_decode_step - one fused decode step: iq_append_token of (k_new, v_new)
+ * followed by iq_decode_attention of q over the advanced lengths (Alg. 1 on
+ * the step's new key and value, then App. A / Table 2 on the packed cache;
+ * the per-step cache write of App. D), issued as one launch sequence.  The
+ * new record is written at position seq_lens[b] by the workgroup that owns
+ * that position, which uses it directly for its own part of the attention.
+ *
+ * Results are those of the two separate calls:
+ *   - if 0 <= seq_lens[b] < capacity, the token is written at seq_lens[b],
+ *     positions 0 .. seq_lens[b] are attended and seq_lens[b] is incremented;
+ *   - otherwise the token is dropped, IQ_ERR_CAPACITY is OR-ed into
+ *     *status_dev (if not NULL), seq_lens[b] is unchanged and positions
+ *     0 .. seq_lens[b]-1 are attended.
+ * Attended lengths above max_seq_len are treated as max_seq_len (the token is
+ * still written); max_seq_len bounds the lengths after the append and must
+ * be >= 1.
+ *
+ * k_new, v_new : device [batch][n_kv_heads][128] of `dtype`, 16-byte aligned,
+ *                both required.
+ * Every other argument is as for iq_decode_attention (same workspace size,
+ * iq_decode_workspace_bytes) and iq_append_token; seq_lens is read and
+ * updated in place.
+ */
+iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, iq_dtype dtype,
+                         uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
+                         int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                         const float* quats, int64_t batch, int64_t n_q_heads,
+                         int64_t n_kv_heads, int64_t head_dim, float softmax_scale, float* out,
+                         void* workspace, size_t workspace_bytes, int32_t* status_dev,
+                         hipStream_t stream);
+
 #ifdef __cplusplus
 }  /* extern "C" */
 #endif

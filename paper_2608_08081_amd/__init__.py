@@ -2,7 +2,7 @@
 
 * ``paper_2608_08081_amd.api``   - PyTorch binding of the C ABI
   (include/isoquant.h): iq_make_rotation, iq_compress_kv, iq_append_token,
-  iq_decode_attention, ...
+  iq_decode_attention, iq_decode_step, ...
 * ``paper_2608_08081_amd.synth`` - seeded synthetic workloads.
 * ``paper_2608_08081_amd.build`` - builds libisoquant.so for gfx950.
 

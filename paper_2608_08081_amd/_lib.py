@@ -47,6 +47,9 @@ _SIGNATURES = {
     "iq_decode_attention": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp,
                                      _c_i64, _c_i64, _c_i64, _c_i64, _c_float, _vp, _vp,
                                      _c_size, _vp]),
+    "iq_decode_step": (_c_int, [_vp, _vp, _vp, _c_int, _vp, _vp, _vp, _vp, _vp, _c_i64,
+                                _c_i64, _vp, _c_i64, _c_i64, _c_i64, _c_i64, _c_float, _vp,
+                                _vp, _c_size, _vp, _vp]),
 }
 
 _lib = None

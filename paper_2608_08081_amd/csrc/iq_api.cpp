@@ -150,7 +150,7 @@ const char* iq_status_string(iq_status s) {
   return "IQ_ERR_UNKNOWN";
 }
 
-int iq_version(void) { return 100; }
+int iq_version(void) { return 101; }
 
 iq_status iq_codebook(float* levels, float* thresholds) {
   const iq::Codebook& cb = iq::codebook();
@@ -246,13 +246,16 @@ iq_status iq_decode_workspace_init(void* workspace, size_t workspace_bytes, hipS
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 
-iq_status iq_decode_attention(const float* q, const uint8_t* k_codes, const float* k_norms,
-                              const uint8_t* v_codes, const float* v_norms,
-                              const int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
-                              const float* quats, int64_t batch, int64_t n_q_heads,
-                              int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
-                              float* out, void* workspace, size_t workspace_bytes,
-                              hipStream_t stream) {
+namespace {
+
+// Shared argument checks of iq_decode_attention and iq_decode_step; fills
+// the split plan.
+iq_status check_decode_args(const float* q, const void* k_codes, const float* k_norms,
+                            const void* v_codes, const float* v_norms, const int32_t* seq_lens,
+                            int64_t capacity, int64_t max_seq_len, const float* quats,
+                            int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                            int64_t head_dim, const float* out, const void* workspace,
+                            size_t workspace_bytes, iq::DecodePlan* plan) {
   if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
   if (batch < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || capacity < 0 || max_seq_len < 0 ||
       max_seq_len > capacity || capacity > 0x7fffffff || batch > 0xffffff)
@@ -269,15 +272,65 @@ iq_status iq_decode_attention(const float* q, const uint8_t* k_codes, const floa
       !iq::aligned(k_norms, 4) || !iq::aligned(v_norms, 4) || !iq::aligned(out, 16) ||
       !iq::aligned(seq_lens, 4) || !iq::aligned(quats, 16) || !iq::aligned(workspace, 256))
     return IQ_ERR_INVALID_ARGUMENT;
-  iq::DecodePlan plan;
-  if (!iq::plan_decode(batch, n_q_heads, n_kv_heads, max_seq_len, &plan))
+  if (!iq::plan_decode(batch, n_q_heads, n_kv_heads, max_seq_len, plan))
     return IQ_ERR_INVALID_ARGUMENT;
-  if (workspace_bytes < plan.total_bytes) return IQ_ERR_WORKSPACE_TOO_SMALL;
+  if (workspace_bytes < plan->total_bytes) return IQ_ERR_WORKSPACE_TOO_SMALL;
+  return IQ_OK;
+}
+
+float resolve_scale(float softmax_scale) {
+  return softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf(static_cast<float>(kDim));
+}
+
+}  // namespace
+
+iq_status iq_decode_attention(const float* q, const uint8_t* k_codes, const float* k_norms,
+                              const uint8_t* v_codes, const float* v_norms,
+                              const int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                              const float* quats, int64_t batch, int64_t n_q_heads,
+                              int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
+                              float* out, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
+  iq::DecodePlan plan;
+  const iq_status st = check_decode_args(q, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                                         capacity, max_seq_len, quats, batch, n_q_heads,
+                                         n_kv_heads, head_dim, out, workspace, workspace_bytes,
+                                         &plan);
+  if (st != IQ_OK) return st;
   if (batch == 0) return IQ_OK;
-  const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf(static_cast<float>(kDim));
+  // without an append the launch only reads the cache and the lengths
+  const hipError_t e = iq::launch_decode(
+      plan, q, const_cast<uint8_t*>(k_codes), const_cast<float*>(k_norms),
+      const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms), const_cast<int32_t*>(seq_lens),
+      capacity, max_seq_len, quats, batch, n_q_heads, n_kv_heads, resolve_scale(softmax_scale),
+      out, workspace, nullptr, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, iq_dtype dtype,
+                         uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
+                         int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                         const float* quats, int64_t batch, int64_t n_q_heads,
+                         int64_t n_kv_heads, int64_t head_dim, float softmax_scale, float* out,
+                         void* workspace, size_t workspace_bytes, int32_t* status_dev,
+                         hipStream_t stream) {
+  if (dtype != IQ_DTYPE_F32 && dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
+  iq::DecodePlan plan;
+  const iq_status st = check_decode_args(q, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                                         capacity, max_seq_len, quats, batch, n_q_heads,
+                                         n_kv_heads, head_dim, out, workspace, workspace_bytes,
+                                         &plan);
+  if (st != IQ_OK) return st;
+  if (max_seq_len < 1 || n_kv_heads > 512) return IQ_ERR_INVALID_ARGUMENT;
+  if (!k_new || !v_new || !iq::aligned(k_new, 16) || !iq::aligned(v_new, 16) ||
+      (status_dev && !iq::aligned(status_dev, 4)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (batch == 0) return IQ_OK;
+  const iq::StepAppend append{k_new, v_new, dtype == IQ_DTYPE_F16 ? 1 : 0, status_dev};
   const hipError_t e = iq::launch_decode(plan, q, k_codes, k_norms, v_codes, v_norms, seq_lens,
                                          capacity, max_seq_len, quats, batch, n_q_heads,
-                                         n_kv_heads, scale, out, workspace, stream);
+                                         n_kv_heads, resolve_scale(softmax_scale), out, workspace,
+                                         &append, stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 

@@ -144,42 +144,12 @@ __global__ __launch_bounds__(64) void compress_kernel(
                   codes + pos * kRecordBytes, norms + pos, cb);
 }
 
-// Append one token per sequence (latency path): one workgroup per sequence,
-// one wave per vector, lane l holding dims 2l and 2l+1, so the whole
-// Algorithm 1 for a vector is a few dozen instructions deep instead of the
-// ~2.7K-instruction serial chain of the one-lane-per-vector bulk kernel.
-//   Step 1: fp64 sum of squares, wave reduction.
-//   Step 2: H_128 as 7 butterfly stages (stage 1 in-lane, stages 2..7 with
-//           the partner lane l ^ (st/2)), then the SO(4) block of the lane
-//           pair (2 blk, 2 blk + 1).
-//   Step 3: codes against the thresholds scaled by s sqrt(128).
-//   Step 4: lane l's 6-bit field (codes of dims 2l, 2l+1) goes to LDS and
-//           lanes 0..11 assemble the 12 record words.
-// seq_lens[b] is read once before any write and bumped after a barrier.
+// Per-step append: one workgroup per sequence, one wave per vector (keys and
+// values of every KV head), each vector compressed by compress_vector_wave,
+// which keeps the serial chain short (a lane-per-vector kernel would run a
+// ~2.7K-instruction chain for a handful of vectors).  seq_lens[b] is read
+// once, before any write, and bumped by thread 0 after its own vectors.
 constexpr int kAppendMaxWaves = 16;
-
-__device__ __forceinline__ double shfl_xor_f64(double v, int m) {
-  const int2 p = __builtin_bit_cast(int2, v);
-  int2 r;
-  r.x = __shfl_xor(p.x, m);
-  r.y = __shfl_xor(p.y, m);
-  return __builtin_bit_cast(double, r);
-}
-
-template <typename T>
-__device__ __forceinline__ void load_pair(const T* src, int lane, float& a, float& b);
-template <>
-__device__ __forceinline__ void load_pair<__half>(const __half* src, int lane, float& a, float& b) {
-  const uint32_t w = reinterpret_cast<const uint32_t*>(src)[lane];
-  a = __half2float(__ushort_as_half(static_cast<unsigned short>(w & 0xFFFFu)));
-  b = __half2float(__ushort_as_half(static_cast<unsigned short>(w >> 16)));
-}
-template <>
-__device__ __forceinline__ void load_pair<float>(const float* src, int lane, float& a, float& b) {
-  const float2 f = reinterpret_cast<const float2*>(src)[lane];
-  a = f.x;
-  b = f.y;
-}
 
 template <typename T>
 __global__ __launch_bounds__(64 * kAppendMaxWaves) void append_kernel(
@@ -188,8 +158,6 @@ __global__ __launch_bounds__(64 * kAppendMaxWaves) void append_kernel(
     float* __restrict__ norms1, int n_heads, int n_vectors, int64_t capacity,
     int32_t* __restrict__ seq_lens, int32_t* __restrict__ status, Codebook cb) {
   __shared__ int32_t pos_s;
-  __shared__ float qp[kAppendMaxWaves][kQuatFloats];
-  __shared__ uint32_t fld[kAppendMaxWaves][64];
   const int b = blockIdx.x;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int n_waves = blockDim.x >> 6;
@@ -197,79 +165,30 @@ __global__ __launch_bounds__(64 * kAppendMaxWaves) void append_kernel(
   __syncthreads();
   const int64_t pos = pos_s;
   if (pos < 0 || pos >= capacity) {
-    if (threadIdx.x == 0 && status != nullptr) atomicOr(status, static_cast<int32_t>(IQ_ERR_CAPACITY));
+    if (threadIdx.x == 0 && status != nullptr)
+      atomicOr(status, static_cast<int32_t>(IQ_ERR_CAPACITY));
     return;
   }
-  const int rounds = (n_vectors + n_waves - 1) / n_waves;
-  for (int round = 0; round < rounds; ++round) {
-    const int idx = round * n_waves + wave;
-    const bool active = idx < n_vectors;
-    const int which = active ? idx / n_heads : 0;
-    const int h = active ? idx % n_heads : 0;
-    const T* src = which ? src1 : src0;
+  for (int idx = wave; idx < n_vectors; idx += n_waves) {
+    const int which = idx / n_heads;
+    const int h = idx % n_heads;
     const int64_t bh = static_cast<int64_t>(b) * n_heads + h;
-    float x0 = 0.f, x1 = 0.f;
-    if (active) {
-      load_pair<T>(src + bh * kDim, lane, x0, x1);
-      const float4 qv = reinterpret_cast<const float4*>(quats + static_cast<int64_t>(h) * kQuatFloats)[lane];
-      qp[wave][4 * lane] = qv.x;
-      qp[wave][4 * lane + 1] = qv.y;
-      qp[wave][4 * lane + 2] = qv.z;
-      qp[wave][4 * lane + 3] = qv.w;
+    float x0, x1;
+    load_pair((which ? src1 : src0) + bh * kDim, lane, x0, x1);
+    float qp[8];
+    {
+      const float4* qs = reinterpret_cast<const float4*>(
+          quats + static_cast<int64_t>(h) * kQuatFloats + 8 * (lane >> 1));
+      const float4 p0 = qs[0], p1 = qs[1];
+      qp[0] = p0.x; qp[1] = p0.y; qp[2] = p0.z; qp[3] = p0.w;
+      qp[4] = p1.x; qp[5] = p1.y; qp[6] = p1.z; qp[7] = p1.w;
     }
-    // Step 1
-    double ss = static_cast<double>(x0) * static_cast<double>(x0) +
-                static_cast<double>(x1) * static_cast<double>(x1);
-#pragma unroll
-    for (int m = 1; m < 64; m <<= 1) ss += shfl_xor_f64(ss, m);
-    const double s = sqrt(ss);
-    // Step 2: unnormalized WHT
-    float a = x0 + x1, c = x0 - x1;            // stage 1 (dims 2l, 2l+1)
-#pragma unroll
-    for (int m = 1; m < 64; m <<= 1) {         // stages 2..7: partner lane l ^ m
-      const float pa = __shfl_xor(a, m), pc = __shfl_xor(c, m);
-      const bool upper = (lane & m) != 0;
-      a = upper ? pa - a : a + pa;
-      c = upper ? pc - c : c + pc;
-    }
-    // SO(4) block blk = lane / 2 covers dims 4 blk .. 4 blk + 3 = (a, c) of
-    // lanes 2 blk and 2 blk + 1
-    const float oa = __shfl_xor(a, 1), oc = __shfl_xor(c, 1);
-    const bool odd = lane & 1;
-    const float z0 = odd ? oa : a, z1 = odd ? oc : c, z2 = odd ? a : oa, z3 = odd ? c : oc;
-    __syncthreads();                          // qp visible
-    float m[4][4];
-    so4_matrix(&qp[wave][8 * (lane >> 1)], m);
-    const int r0 = odd ? 2 : 0;
-    const float y0 = m[r0][0] * z0 + m[r0][1] * z1 + m[r0][2] * z2 + m[r0][3] * z3;
-    const float y1 = m[r0 + 1][0] * z0 + m[r0 + 1][1] * z1 + m[r0 + 1][2] * z2 + m[r0 + 1][3] * z3;
-    // Step 3
-    float thr[7];
-    if (ss > 0.0) {
-      const double sc = s * 11.313708498984760390;
-#pragma unroll
-      for (int j = 0; j < 7; ++j) thr[j] = static_cast<float>(static_cast<double>(cb.thr[j]) * sc);
-    } else {
-#pragma unroll
-      for (int j = 0; j < 7; ++j) thr[j] = cb.thr[j];
-    }
-    fld[wave][lane] = quantize3(y0, thr) | (quantize3(y1, thr) << 3);
-    __syncthreads();                          // fields visible
-    // Step 4: lanes 0..11 build record word w = bits 32w .. 32w+31
-    if (active && lane < kRecordWords) {
-      const int w = lane;
-      uint32_t word = 0u;
-      const int f_lo = (32 * w) / 6, f_hi = (32 * w + 31) / 6;
-      for (int f = f_lo; f <= f_hi && f < 64; ++f) {
-        const int sh = 6 * f - 32 * w;
-        const uint32_t v = fld[wave][f];
-        word |= sh >= 0 ? (v << sh) : (v >> (-sh));
-      }
+    const WaveCode wc = compress_vector_wave(x0, x1, qp, cb, lane);
+    if (lane < kRecordWords) {
       uint8_t* codes = which ? codes1 : codes0;
-      reinterpret_cast<uint32_t*>(codes + (bh * capacity + pos) * kRecordBytes)[w] = word;
-      if (w == 0) (which ? norms1 : norms0)[bh * capacity + pos] = static_cast<float>(s);
+      reinterpret_cast<uint32_t*>(codes + (bh * capacity + pos) * kRecordBytes)[lane] = wc.word;
+      if (lane == 0) (which ? norms1 : norms0)[bh * capacity + pos] = wc.scale;
     }
-    __syncthreads();                          // before the next round reuses qp / fld
   }
   if (threadIdx.x == 0) seq_lens[b] = static_cast<int32_t>(pos + 1);
 }

@@ -289,12 +289,12 @@ bool plan_decode(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads, int64_t m
   return true;
 }
 
-hipError_t launch_decode(const DecodePlan& plan, const float* q, const uint8_t* k_codes,
-                         const float* k_norms, const uint8_t* v_codes,
-                         const float* v_norms, const int32_t* seq_lens,
-                         int64_t capacity, int64_t max_seq_len, const float* quats,
-                         int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
-                         float scale, float* out, void* workspace, hipStream_t stream) {
+hipError_t launch_decode(const DecodePlan& plan, const float* q, uint8_t* k_codes,
+                         float* k_norms, uint8_t* v_codes, float* v_norms,
+                         int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                         const float* quats, int64_t batch, int64_t n_q_heads,
+                         int64_t n_kv_heads, float scale, float* out, void* workspace,
+                         const StepAppend* append, hipStream_t stream) {
   if (batch == 0) return hipSuccess;
   const int group = static_cast<int>(n_q_heads / n_kv_heads);
   const bool aligned16 = (reinterpret_cast<uintptr_t>(k_norms) % 16 == 0) &&
@@ -305,9 +305,17 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, const uint8_t* 
   if (group == 8 && plan.g8_batches > 0 && capacity % 4 == 0 && aligned16 && row32) {
     float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
     return launch_decode_g8(plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes,
-                            k_norms, v_codes,
-                            v_norms, seq_lens, capacity, max_seq_len, quats, batch, n_kv_heads,
-                            scale, out, parts, stream);
+                            k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len, quats,
+                            batch, n_kv_heads, scale, out, parts, append, stream);
+  }
+  if (append) {
+    // generic path of the fused step: the append kernel, then attention
+    // over the advanced lengths
+    const hipError_t e =
+        launch_append(append->k_new, append->v_new, append->f16 ? IQ_DTYPE_F16 : IQ_DTYPE_F32,
+                      batch, n_kv_heads, quats, k_codes, k_norms, v_codes, v_norms, capacity,
+                      seq_lens, append->status, stream);
+    if (e != hipSuccess) return e;
   }
   float* partials = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
   const int64_t split_blocks = batch * n_kv_heads * plan.n_splits;

@@ -95,20 +95,6 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// Value of lane (lane ^ kM) within the lane's group of 32 lanes (kM < 32):
-// quad permutations through DPP for 1 and 2, the swizzle unit otherwise.
-template <int kM>
-__device__ __forceinline__ float xor_lane(float v) {
-  const int x = __builtin_bit_cast(int, v);
-  if constexpr (kM == 1) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false));
-  } else if constexpr (kM == 2) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false));
-  } else {
-    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(x, (kM << 10) | 0x1F));
-  }
-}
-
 // One Walsh-Hadamard stage across lanes: the pair (i, i ^ kM) becomes
 // (x_i + x_(i^kM), x_i - x_(i^kM)); blk = this lane's index in its 32-group.
 template <int kM>
@@ -170,6 +156,22 @@ __device__ __forceinline__ f32x4_t rotate_inverse(f32x4_t o, const float* qparam
   f32x4_t x = f32x4_t{z[0], z[1], z[2], z[3]};
   lane_wht32(x, blk);
   return x * kInvSqrtDim;
+}
+
+// Codebook values of dims d..d+3 (d % 4 == 0) of a packed record held in
+// LDS (12 words): codes at bits 3d .. 3d+11, two 6-bit fields looked up in
+// the fp16 pair table.
+__device__ __forceinline__ f32x4_t decode_record_dims(const uint32_t* rec, const uint32_t* lut64,
+                                                      int d) {
+  const int bit = 3 * d, w = bit >> 5, off = bit & 31;
+  const uint32_t lo = rec[w];
+  const uint32_t hi = w + 1 < kRecordWords ? rec[w + 1] : 0u;
+  const uint32_t bits = __builtin_amdgcn_alignbit(hi, lo, off);
+  const uint32_t p0 = lut64[bits & 63u], p1 = lut64[(bits >> 6) & 63u];
+  return f32x4_t{static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p0))),
+                 static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p0 >> 16))),
+                 static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p1))),
+                 static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p1 >> 16)))};
 }
 
 // Issues every cache load of one wave: keys, values and both scale arrays
@@ -326,14 +328,22 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
   l_run = wave_sum(l_run);
 }
 
-template <int NB>
+// kAppend: the fused decode step.  The new key and value of every (sequence
+// b, KV head g) are compressed (Alg. 1) and written at position seq_lens[b]
+// by the workgroup whose split holds that position; that workgroup's waves
+// attend the positions before it, and the new token's score and value, taken
+// from the fresh record, join in the workgroup merge.  seq_lens is advanced
+// by the merge kernel (or by advance_lengths_kernel for a single split),
+// after every workgroup has read it.
+template <int NB, bool kAppend>
 __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
-    const float* __restrict__ q, const uint8_t* __restrict__ k_codes,
-    const float* __restrict__ k_norms, const uint8_t* __restrict__ v_codes,
-    const float* __restrict__ v_norms, const int32_t* __restrict__ seq_lens,
-    const float* __restrict__ quats, float* __restrict__ partials, float* __restrict__ out,
-    int64_t capacity, int max_seq_len, int n_kv_heads, int n_splits, int split_len,
-    float qscale, Codebook cb) {
+    const float* __restrict__ q, uint8_t* __restrict__ k_codes, float* __restrict__ k_norms,
+    uint8_t* __restrict__ v_codes, float* __restrict__ v_norms,
+    const int32_t* __restrict__ seq_lens, const float* __restrict__ quats,
+    float* __restrict__ partials, float* __restrict__ out, int64_t capacity, int max_seq_len,
+    int n_kv_heads, int n_splits, int split_len, float qscale, Codebook cb,
+    const void* __restrict__ k_new, const void* __restrict__ v_new, int new_f16,
+    int32_t* __restrict__ status) {
   constexpr int kQRow = kDim / 2 + 4;   // fp16-pair row of one head, padded (68 words)
   __shared__ uint32_t lut64[64];
   // 64 copies of the 64-entry table: entry e of copy l at word 64 e + l, so
@@ -346,6 +356,8 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   __shared__ int qexp_s[kHeads];
   float(*wave_o)[kHeads * kDim] = reinterpret_cast<float(*)[kHeads * kDim]>(big);
   __shared__ float wave_ml[kWaves][2][kHeads];
+  __shared__ uint32_t new_rec[2][kRecordWords];   // kAppend: the new key / value record
+  __shared__ float new_scale[2];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -357,26 +369,73 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   const int b = bg / n_kv_heads;
   const int n_q_heads = n_kv_heads * kHeads;
 
-  int seq = seq_lens[b];
+  const int seq0 = seq_lens[b];
+  int seq = seq0;
+  bool appended = false;   // kAppend: the new token goes to position seq0
+  if constexpr (kAppend) {
+    appended = seq0 >= 0 && seq0 < capacity;
+    if (appended) seq = seq0 + 1;
+    if (!appended && status != nullptr && g == 0 && split == 0 && tid == 0)
+      atomicOr(status, static_cast<int32_t>(IQ_ERR_CAPACITY));
+  }
   seq = seq > max_seq_len ? max_seq_len : (seq < 0 ? 0 : seq);
   const int used = (seq + split_len - 1) / split_len;
   float* out_bg =
       out + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * kHeads) * kDim;
+  float* part_bg = partials + static_cast<int64_t>(bg) * n_splits * (kHeads * kPart);
   if (split >= used) {
-    if (seq == 0 && split == 0)
+    // nothing to attend: with several splits, an empty partial (m = -inf)
+    // for the merge; with one, a zero output row for an empty sequence
+    if (n_splits > 1) {
+      if (tid < kHeads)
+        part_bg[static_cast<int64_t>(split) * (kHeads * kPart) + tid * kPart] = -INFINITY;
+    } else {
       for (int e = tid; e < kHeads * kDim; e += kThreads) out_bg[e] = 0.f;
+    }
     return;
   }
+  // the workgroup writing the new record: the split holding position seq0
+  // (or, if seq0 lies beyond max_seq_len, the last attended split)
+  const bool writer =
+      kAppend && appended && split == (seq0 < max_seq_len ? seq0 : max_seq_len - 1) / split_len;
   const int start = split * split_len;
-  const int end = seq < start + split_len ? seq : start + split_len;
+  // the appended token (position seq0 = the split's last attended position)
+  // is not read back from the cache: its score and value come from the new
+  // record directly, merged with the waves' results below
+  const bool new_attended = writer && seq0 < max_seq_len;
+  int end = seq < start + split_len ? seq : start + split_len;
+  if (new_attended) end = seq0;
   const int wbase = start + wave * NB * 16;   // first position of the wave
-  const int last = end - 1;                   // last position of the split
+  const int last = end > 0 ? end - 1 : 0;     // last position read (clamp target)
   // (b, g) row bases (wave-uniform); lane offsets in 32 bits (capacity * 48 < 2^31)
   const int64_t row = static_cast<int64_t>(bg) * capacity;
-  const uint8_t* kc = k_codes + row * kRecordBytes;
-  const uint8_t* vc = v_codes + row * kRecordBytes;
+  uint8_t* kc = k_codes + row * kRecordBytes;
+  uint8_t* vc = v_codes + row * kRecordBytes;
   const float* kn = k_norms + row;
   const float* vn = v_norms + row;
+
+  // kAppend, writer workgroup: the last wave, which holds the fewest
+  // positions of the split, compresses the new key and value after its own
+  // positions (they are needed only in the workgroup merge)
+  constexpr int kCompressWave = kWaves - 1;
+  float nk0 = 0.f, nk1 = 0.f, nv0 = 0.f, nv1 = 0.f;
+  float nqp[8];
+  const bool compressing = writer && wave == kCompressWave;
+  if (compressing) {
+    const int64_t off = (static_cast<int64_t>(b) * n_kv_heads + g) * kDim;
+    if (new_f16) {
+      load_pair(static_cast<const __half*>(k_new) + off, lane, nk0, nk1);
+      load_pair(static_cast<const __half*>(v_new) + off, lane, nv0, nv1);
+    } else {
+      load_pair(static_cast<const float*>(k_new) + off, lane, nk0, nk1);
+      load_pair(static_cast<const float*>(v_new) + off, lane, nv0, nv1);
+    }
+    const f32x4_t* qs = reinterpret_cast<const f32x4_t*>(
+        quats + static_cast<int64_t>(g) * kQuatFloats + 8 * (lane >> 1));
+    const f32x4_t p0 = qs[0], p1 = qs[1];
+    nqp[0] = p0[0]; nqp[1] = p0[1]; nqp[2] = p0[2]; nqp[3] = p0[3];
+    nqp[4] = p1[0]; nqp[5] = p1[1]; nqp[6] = p1[2]; nqp[7] = p1[3];
+  }
 
   // ---- issue every load of the wave -------------------------------------
   // the group's 8 query heads first (one float4 per thread), then the cache
@@ -476,8 +535,26 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     attend_wave<NB, true>(kw, vw, ks, vs, qhi, qlo, big + lane, col, grp, nvalid, vshift,
                           qdown, m_run, l_run, vmax, o_acc);
 
+  if (compressing) {
+    // the two chains are independent and interleave
+    const WaveCode wk = compress_vector_wave(nk0, nk1, nqp, cb, lane);
+    const WaveCode wv = compress_vector_wave(nv0, nv1, nqp, cb, lane);
+    if (lane < kRecordWords) {
+      reinterpret_cast<uint32_t*>(kc + static_cast<int64_t>(seq0) * kRecordBytes)[lane] = wk.word;
+      reinterpret_cast<uint32_t*>(vc + static_cast<int64_t>(seq0) * kRecordBytes)[lane] = wv.word;
+      new_rec[0][lane] = wk.word;
+      new_rec[1][lane] = wv.word;
+    }
+    if (lane == 0) {
+      k_norms[row + seq0] = wk.scale;
+      v_norms[row + seq0] = wv.scale;
+      new_scale[0] = wk.scale;
+      new_scale[1] = wv.scale;
+    }
+  }
+
   // ---- merge the 4 waves in LDS ---------------------------------------------
-  lds_barrier();   // every wave is done with the tables
+  lds_barrier();   // every wave is done with the tables; new_rec, new_scale
   // lane (u = col, grp) holds rows 4 grp + r = (head (4 grp + r) % 8, slot
   // grp / 2) of MFMA nb, i.e. dim 2 (4 u + nb) + slot.
   const float oscale = vmax * (1.0f / 32768.0f);
@@ -494,11 +571,29 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   }
   lds_barrier();
 
-  // thread -> (head h = tid / 32, dims 4 (tid % 32) .. +3)
+  // thread -> (head h = tid / 32, dims 4 (tid % 32) .. +3), the same
+  // (head, block) as in the query rotation
   const int mh = tid >> 5, md = (tid & 31) * 4;
   float M = -INFINITY;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wave_ml[w][0][mh]);
+  float s_new = -INFINITY;
+  f32x4_t v_new4;
+  if (new_attended) {
+    // score of the appended key: s^K (q_tilde . C[code]) over this thread's
+    // 4 dims (codes of dims md..md+3 = bits 3 md .. 3 md + 11 of the record),
+    // summed over the head's 32 lanes; y already carries the score scale
+    const f32x4_t k4 = decode_record_dims(new_rec[0], lut64, md);
+    v_new4 = decode_record_dims(new_rec[1], lut64, md);
+    float dot = y[0] * k4[0] + y[1] * k4[1] + y[2] * k4[2] + y[3] * k4[3];
+    dot += xor_lane<1>(dot);
+    dot += xor_lane<2>(dot);
+    dot += xor_lane<4>(dot);
+    dot += xor_lane<8>(dot);
+    dot += xor_lane<16>(dot);
+    s_new = dot * new_scale[0];
+    M = fmaxf(M, s_new);
+  }
   float L = 0.f;
   f32x4_t O = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -508,16 +603,20 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     L += c * wave_ml[w][1][mh];
     O += c * *reinterpret_cast<const f32x4_t*>(wave_o[w] + mh * kDim + md);
   }
+  if (new_attended) {
+    const float c = __builtin_amdgcn_exp2f(s_new - M);
+    L += c;
+    O += (c * new_scale[1]) * v_new4;
+  }
 
-  if (used == 1) {
+  if (n_splits == 1) {
     // thread (mh, md / 4) holds block md / 4 of head mh: rotate back in place
     const f32x4_t o = rotate_inverse(O * (1.0f / L), qparam, tid & 31);
     *reinterpret_cast<f32x4_t*>(out_bg + mh * kDim + md) = o;
     return;
   }
   // ---- partial result of this split ------------------------------------------
-  float* pp = partials + (static_cast<int64_t>(bg) * n_splits + split) * (kHeads * kPart) +
-              mh * kPart;
+  float* pp = part_bg + static_cast<int64_t>(split) * (kHeads * kPart) + mh * kPart;
   if ((tid & 31) == 0) {
     pp[0] = M;
     pp[1] = L;
@@ -529,11 +628,14 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
 // 256-thread workgroup; thread (sg, dq) takes splits sg, sg + 8, ... and dims
 // 4 dq .. 4 dq + 3, with up to 16 splits' loads in flight per thread.  Then
 // o = sum_s c_s O_s / sum_s c_s l_s with c_s = 2^(m_s - max m), and the single
-// inverse rotation.
+// inverse rotation.  Splits with nothing to attend carry m = -inf (their
+// other entries are never read), so the merge needs no sequence length.
+// kAppend: workgroup (b, head 0) then advances seq_lens[b] past the token the
+// decode kernel appended.
+template <bool kAppend>
 __global__ __launch_bounds__(kThreads) void merge_g8_kernel(
-    const float* __restrict__ partials, const int32_t* __restrict__ seq_lens,
-    const float* __restrict__ quats, float* __restrict__ out, int64_t max_seq_len,
-    int n_kv_heads, int n_splits, int split_len) {
+    const float* __restrict__ partials, const float* __restrict__ quats, float* __restrict__ out,
+    int n_kv_heads, int n_splits, int32_t* __restrict__ seq_lens, int64_t capacity) {
   constexpr int kUnroll = 16;
   __shared__ __attribute__((aligned(16))) float red_o[8][kDim];
   __shared__ float red_m[8], red_l[8];
@@ -542,11 +644,8 @@ __global__ __launch_bounds__(kThreads) void merge_g8_kernel(
   const int h = blockIdx.x % n_q_heads;
   const int b = blockIdx.x / n_q_heads;
   const int g = h / kHeads, hh = h % kHeads;
-  int64_t seq = seq_lens[b];
-  if (seq > max_seq_len) seq = max_seq_len;
-  if (seq < 0) seq = 0;
-  const int used = static_cast<int>((seq + split_len - 1) / split_len);
-  if (used <= 1) return;   // empty sequence or a single split: written by the split kernel
+  int seq0 = 0;
+  if (kAppend && h == 0 && tid == 0) seq0 = seq_lens[b];
   const int sg = tid >> 5, dq = tid & 31;
   const float* base = partials +
                       static_cast<int64_t>(b * n_kv_heads + g) * n_splits * (kHeads * kPart) +
@@ -562,15 +661,15 @@ __global__ __launch_bounds__(kThreads) void merge_g8_kernel(
   }
   float M = -INFINITY, L = 0.f;
   f32x4_t O = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  for (int s0 = sg; s0 < used; s0 += 8 * kUnroll) {
+  for (int s0 = sg; s0 < n_splits; s0 += 8 * kUnroll) {
     float mv[kUnroll], lv[kUnroll];
     f32x4_t ov[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int s = s0 + 8 * u;
-      const int sc = s < used ? s : s0;
+      const int sc = s < n_splits ? s : s0;
       const float* p = base + static_cast<int64_t>(sc) * (kHeads * kPart);
-      mv[u] = s < used ? p[0] : -INFINITY;
+      mv[u] = s < n_splits ? p[0] : -INFINITY;
       lv[u] = p[1];
       ov[u] = *reinterpret_cast<const f32x4_t*>(p + 2 + 4 * dq);
     }
@@ -582,9 +681,14 @@ __global__ __launch_bounds__(kThreads) void merge_g8_kernel(
     O *= cM;
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const float c = (mv[u] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mv[u] - Mn);
-      L += c * lv[u];
-      O += c * ov[u];
+      // an empty split's l and O were never written: select, do not scale
+      const bool live = mv[u] != -INFINITY;
+      const float c = live ? __builtin_amdgcn_exp2f(mv[u] - Mn) : 0.f;
+      L += live ? c * lv[u] : 0.f;
+      O[0] += live ? c * ov[u][0] : 0.f;
+      O[1] += live ? c * ov[u][1] : 0.f;
+      O[2] += live ? c * ov[u][2] : 0.f;
+      O[3] += live ? c * ov[u][3] : 0.f;
     }
     M = Mn;
   }
@@ -611,8 +715,23 @@ __global__ __launch_bounds__(kThreads) void merge_g8_kernel(
       o += *reinterpret_cast<const f32x4_t*>(&red_o[j][4 * tid]);
       l += red_l[j];
     }
-    *reinterpret_cast<f32x4_t*>(out + (static_cast<int64_t>(b) * n_q_heads + h) * kDim + 4 * tid) =
-        rotate_inverse(o * (1.0f / l), qparam, tid);
+    // an empty sequence (every split empty) gives a zero row
+    const f32x4_t r = l > 0.f ? rotate_inverse(o * (1.0f / l), qparam, tid)
+                              : f32x4_t{0.f, 0.f, 0.f, 0.f};
+    *reinterpret_cast<f32x4_t*>(out + (static_cast<int64_t>(b) * n_q_heads + h) * kDim +
+                                4 * tid) = r;
+  }
+  if (kAppend && h == 0 && tid == 0 && seq0 >= 0 && seq0 < capacity) seq_lens[b] = seq0 + 1;
+}
+
+// Fused decode step with a single split: advances seq_lens after the decode
+// kernel (which read it in every workgroup) has finished.
+__global__ void advance_lengths_kernel(int32_t* __restrict__ seq_lens, int64_t capacity,
+                                       int batch) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < batch) {
+    const int s = seq_lens[b];
+    if (s >= 0 && s < capacity) seq_lens[b] = s + 1;
   }
 }
 
@@ -643,39 +762,60 @@ void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
 }
 
 hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const float* q,
-                            const uint8_t* k_codes,
-                            const float* k_norms, const uint8_t* v_codes, const float* v_norms,
-                            const int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                            uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
+                            int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                             const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
-                            float* out, float* partials, hipStream_t stream) {
+                            float* out, float* partials, const StepAppend* append,
+                            hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>(batch * n_kv_heads * n_splits)), block(kThreads);
   const float qscale = scale * kLog2e;
   const Codebook& cb = codebook();
-#define IQ_LAUNCH_G8(NB_)                                                                        \
-  hipLaunchKernelGGL(decode_g8_kernel<NB_>, grid, block, 0, stream, q, k_codes, k_norms,       \
+  const void* k_new = append ? append->k_new : nullptr;
+  const void* v_new = append ? append->v_new : nullptr;
+  const int new_f16 = append ? append->f16 : 0;
+  int32_t* status = append ? append->status : nullptr;
+#define IQ_LAUNCH_G8(NB_, APP_)                                                                  \
+  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_>), grid, block, 0, stream, q, k_codes, k_norms, \
                      v_codes, v_norms, seq_lens, quats, partials, out, capacity,               \
-                     static_cast<int>(max_seq_len),                                              \
-                     static_cast<int>(n_kv_heads), static_cast<int>(n_splits),                \
-                     static_cast<int>(split_len), qscale, cb)
-  switch (nb) {
-    case 1: IQ_LAUNCH_G8(1); break;
-    case 2: IQ_LAUNCH_G8(2); break;
-    case 3: IQ_LAUNCH_G8(3); break;
-    case 4: IQ_LAUNCH_G8(4); break;
-    case 5: IQ_LAUNCH_G8(5); break;
-    case 6: IQ_LAUNCH_G8(6); break;
-    case 7: IQ_LAUNCH_G8(7); break;
-    default: IQ_LAUNCH_G8(8); break;
+                     static_cast<int>(max_seq_len), static_cast<int>(n_kv_heads),              \
+                     static_cast<int>(n_splits), static_cast<int>(split_len), qscale, cb,      \
+                     k_new, v_new, new_f16, status)
+#define IQ_LAUNCH_G8_NB(APP_)            \
+  switch (nb) {                          \
+    case 1: IQ_LAUNCH_G8(1, APP_); break; \
+    case 2: IQ_LAUNCH_G8(2, APP_); break; \
+    case 3: IQ_LAUNCH_G8(3, APP_); break; \
+    case 4: IQ_LAUNCH_G8(4, APP_); break; \
+    case 5: IQ_LAUNCH_G8(5, APP_); break; \
+    case 6: IQ_LAUNCH_G8(6, APP_); break; \
+    case 7: IQ_LAUNCH_G8(7, APP_); break; \
+    default: IQ_LAUNCH_G8(8, APP_); break; \
   }
+  if (append) {
+    IQ_LAUNCH_G8_NB(true)
+  } else {
+    IQ_LAUNCH_G8_NB(false)
+  }
+#undef IQ_LAUNCH_G8_NB
 #undef IQ_LAUNCH_G8
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // splits of every (sequence, query head) merged by a second launch
+  // splits of every (sequence, query head) merged by a second launch; the
+  // fused step advances the lengths there (or separately, for one split)
   if (n_splits > 1) {
-    hipLaunchKernelGGL(merge_g8_kernel, dim3(static_cast<unsigned>(batch * n_kv_heads * kHeads)),
-                       dim3(kThreads), 0, stream, partials, seq_lens, quats, out, max_seq_len,
-                       static_cast<int>(n_kv_heads), static_cast<int>(n_splits),
-                       static_cast<int>(split_len));
+    const dim3 mgrid(static_cast<unsigned>(batch * n_kv_heads * kHeads));
+    if (append)
+      hipLaunchKernelGGL(merge_g8_kernel<true>, mgrid, dim3(kThreads), 0, stream, partials, quats,
+                         out, static_cast<int>(n_kv_heads), static_cast<int>(n_splits), seq_lens,
+                         capacity);
+    else
+      hipLaunchKernelGGL(merge_g8_kernel<false>, mgrid, dim3(kThreads), 0, stream, partials, quats,
+                         out, static_cast<int>(n_kv_heads), static_cast<int>(n_splits), seq_lens,
+                         capacity);
+    e = hipGetLastError();
+  } else if (append) {
+    hipLaunchKernelGGL(advance_lengths_kernel, dim3(static_cast<unsigned>((batch + 255) / 256)),
+                       dim3(256), 0, stream, seq_lens, capacity, static_cast<int>(batch));
     e = hipGetLastError();
   }
   return e;

@@ -2,7 +2,9 @@
 // (Sec. 3.2 Steps 2-4, Sec. 3.3, App. B), shared by the kernels of libisoquant.
 #pragma once
 
+#include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdint.h>
 
 #include "iq_internal.h"
@@ -70,6 +72,129 @@ __device__ __forceinline__ void put_code(uint32_t (&w)[kRecordWords], int i, uin
   const int word = bit >> 5, off = bit & 31;
   w[word] |= code << off;
   if (off > 29) w[word + 1] |= code >> (32 - off);
+}
+
+// Value of lane (lane ^ kM) within the lane's group of 32 lanes (kM < 32):
+// quad permutations through DPP for 1 and 2, the swizzle unit otherwise.
+template <int kM>
+__device__ __forceinline__ float xor_lane(float v) {
+  const int x = __builtin_bit_cast(int, v);
+  if constexpr (kM == 1) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false));
+  } else if constexpr (kM == 2) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false));
+  } else {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(x, (kM << 10) | 0x1F));
+  }
+}
+
+// Value of lane (lane ^ m) for any m < 64 (xor 32 through the permute unit).
+template <int kM>
+__device__ __forceinline__ float xor_lane64(float v) {
+  if constexpr (kM < 32) {
+    return xor_lane<kM>(v);
+  } else {
+    return __shfl_xor(v, kM);
+  }
+}
+
+// ---- one vector per wave -------------------------------------------------
+// Used where only a few vectors are compressed at once (the per-step append):
+// the 128 dims are spread over the 64 lanes (lane l holds dims 2l, 2l+1), so
+// the serial chain is short.
+
+template <int kM>
+__device__ __forceinline__ double xor_lane64_f64(double v) {
+  const float2 p = __builtin_bit_cast(float2, v);
+  return __builtin_bit_cast(double, float2{xor_lane64<kM>(p.x), xor_lane64<kM>(p.y)});
+}
+
+// One butterfly stage of the cross-lane Walsh-Hadamard transform (partner
+// lane l ^ kM), on the lane's two partial sums.
+template <int kM>
+__device__ __forceinline__ void wave_butterfly(float& a, float& c, int lane) {
+  const float pa = xor_lane64<kM>(a), pc = xor_lane64<kM>(c);
+  const bool upper = (lane & kM) != 0;
+  a = upper ? pa - a : a + pa;
+  c = upper ? pc - c : c + pc;
+}
+
+// dims 2 lane, 2 lane + 1 of a 128-dim vector of fp32 or fp16
+__device__ __forceinline__ void load_pair(const float* src, int lane, float& a, float& b) {
+  const float2 f = reinterpret_cast<const float2*>(src)[lane];
+  a = f.x;
+  b = f.y;
+}
+__device__ __forceinline__ void load_pair(const __half* src, int lane, float& a, float& b) {
+  const uint32_t w = reinterpret_cast<const uint32_t*>(src)[lane];
+  a = __half2float(__ushort_as_half(static_cast<unsigned short>(w & 0xFFFFu)));
+  b = __half2float(__ushort_as_half(static_cast<unsigned short>(w >> 16)));
+}
+
+struct WaveCode {
+  uint32_t word;   // record word `lane` (meaningful in lanes 0..11)
+  float scale;     // s = ||x||_2
+};
+
+// Algorithm 1 for one vector held by one wave (lane l: x0 = x[2l],
+// x1 = x[2l+1]); qp holds (q_L, q_R) of SO(4) block l / 2 of the vector's
+// head.  Every lane of the wave must take part.
+//   Step 1: fp64 sum of squares, wave reduction.
+//   Step 2: H_128 as 7 butterfly stages (stage 1 in-lane, stages 2..7 with
+//           the partner lane l ^ (st/2)), then the SO(4) block of the lane
+//           pair (2 blk, 2 blk + 1).
+//   Step 3: codes against the thresholds scaled by s sqrt(128).
+//   Step 4: lane w < 12 gathers the (at most 7) 6-bit fields overlapping
+//           record word w.
+__device__ __forceinline__ WaveCode compress_vector_wave(float x0, float x1, const float* qp,
+                                                        const Codebook& cb, int lane) {
+  double ss = static_cast<double>(x0) * static_cast<double>(x0) +
+              static_cast<double>(x1) * static_cast<double>(x1);
+  ss += xor_lane64_f64<1>(ss);
+  ss += xor_lane64_f64<2>(ss);
+  ss += xor_lane64_f64<4>(ss);
+  ss += xor_lane64_f64<8>(ss);
+  ss += xor_lane64_f64<16>(ss);
+  ss += xor_lane64_f64<32>(ss);
+  const double s = sqrt(ss);
+  float a = x0 + x1, c = x0 - x1;   // stage 1 (dims 2l, 2l+1)
+  wave_butterfly<1>(a, c, lane);
+  wave_butterfly<2>(a, c, lane);
+  wave_butterfly<4>(a, c, lane);
+  wave_butterfly<8>(a, c, lane);
+  wave_butterfly<16>(a, c, lane);
+  wave_butterfly<32>(a, c, lane);
+  // block blk = lane / 2 covers dims 4 blk .. 4 blk + 3 = (a, c) of lanes
+  // 2 blk and 2 blk + 1
+  const float oa = xor_lane<1>(a), oc = xor_lane<1>(c);
+  const bool odd = lane & 1;
+  const float z0 = odd ? oa : a, z1 = odd ? oc : c, z2 = odd ? a : oa, z3 = odd ? c : oc;
+  float m[4][4];
+  so4_matrix(qp, m);
+  const int r0 = odd ? 2 : 0;
+  const float y0 = m[r0][0] * z0 + m[r0][1] * z1 + m[r0][2] * z2 + m[r0][3] * z3;
+  const float y1 = m[r0 + 1][0] * z0 + m[r0 + 1][1] * z1 + m[r0 + 1][2] * z2 + m[r0 + 1][3] * z3;
+  float thr[7];
+  if (ss > 0.0) {
+    const double sc = s * 11.313708498984760390;   // s sqrt(128)
+#pragma unroll
+    for (int j = 0; j < 7; ++j) thr[j] = static_cast<float>(static_cast<double>(cb.thr[j]) * sc);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 7; ++j) thr[j] = cb.thr[j];
+  }
+  const uint32_t fld = quantize3(y0, thr) | (quantize3(y1, thr) << 3);
+  const int w = lane < kRecordWords ? lane : 0;
+  const int f_lo = (32 * w) / 6;
+  uint32_t word = 0u;
+#pragma unroll
+  for (int k = 0; k < 7; ++k) {
+    const int f = f_lo + k;
+    const uint32_t v = static_cast<uint32_t>(__shfl(static_cast<int>(fld), f & 63));
+    const int sh = 6 * f - 32 * w;
+    if (f < 64 && sh < 32) word |= sh >= 0 ? (v << sh) : (v >> (-sh));
+  }
+  return WaveCode{word, static_cast<float>(s)};
 }
 
 }  // namespace iq

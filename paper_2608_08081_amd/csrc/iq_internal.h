@@ -57,22 +57,32 @@ hipError_t launch_append(const void* k, const void* v, int dtype, int64_t batch,
                          int64_t capacity, int32_t* seq_lens, int32_t* status,
                          hipStream_t stream);
 
-hipError_t launch_decode(const DecodePlan& plan, const float* q, const uint8_t* k_codes,
-                         const float* k_norms, const uint8_t* v_codes,
-                         const float* v_norms, const int32_t* seq_lens,
-                         int64_t capacity, int64_t max_seq_len, const float* quats,
-                         int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
-                         float scale, float* out, void* workspace, hipStream_t stream);
+// The new token of a fused decode step (keys and values of every KV head).
+struct StepAppend {
+  const void* k_new;
+  const void* v_new;
+  int f16;            // 1: fp16 inputs, 0: fp32
+  int32_t* status;    // optional IQ_ERR_CAPACITY flag
+};
+
+// Decode attention; with `append`, the fused step: append the new token at
+// seq_lens[b], attend over seq_lens[b] + 1 positions, advance seq_lens.
+hipError_t launch_decode(const DecodePlan& plan, const float* q, uint8_t* k_codes,
+                         float* k_norms, uint8_t* v_codes, float* v_norms,
+                         int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                         const float* quats, int64_t batch, int64_t n_q_heads,
+                         int64_t n_kv_heads, float scale, float* out, void* workspace,
+                         const StepAppend* append, hipStream_t stream);
 
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 
 void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
              int64_t* n_splits, int64_t* split_len);
 hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const float* q,
-                            const uint8_t* k_codes,
-                            const float* k_norms, const uint8_t* v_codes, const float* v_norms,
-                            const int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                            uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
+                            int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                             const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
-                            float* out, float* partials, hipStream_t stream);
+                            float* out, float* partials, const StepAppend* append,
+                            hipStream_t stream);
 
 }  // namespace iq

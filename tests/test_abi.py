@@ -144,3 +144,30 @@ def test_workspace_bytes():
     assert L.iq_decode_workspace_bytes(1, 30, 4, 32768, 128) == 0
     # monotone in context length
     assert L.iq_decode_workspace_bytes(1, 32, 4, 1024, 128) <= n
+
+
+def _step(**kw):
+    args = dict(q=A, k=A, v=B, dtype=1, kc=A, kn=A, vc=B, vn=B, seq=A, cap=1024, maxlen=1024,
+                quats=A, batch=1, hq=32, hkv=4, hd=128, scale=0.0, out=B, ws=A, wsb=1 << 30,
+                status=None)
+    args.update(kw)
+    return L.iq_decode_step(args["q"], args["k"], args["v"], args["dtype"], args["kc"],
+                            args["kn"], args["vc"], args["vn"], args["seq"], args["cap"],
+                            args["maxlen"], args["quats"], args["batch"], args["hq"],
+                            args["hkv"], args["hd"], args["scale"], args["out"], args["ws"],
+                            args["wsb"], args["status"], None)
+
+
+def test_step_validation():
+    assert _step(hd=96) == 2
+    assert _step(dtype=3) == 2
+    assert _step(hq=68) == 2                    # group 17 > 16
+    assert _step(k=None) == 1                   # both new vectors are required
+    assert _step(v=None) == 1
+    assert _step(k=ctypes.c_void_p(0x100004)) == 1   # k_new not 16-byte aligned
+    assert _step(maxlen=0) == 1                 # the step always attends the new token
+    assert _step(maxlen=2048) == 1              # beyond capacity
+    assert _step(seq=None) == 1
+    assert _step(status=ctypes.c_void_p(0x100002)) == 1
+    assert _step(wsb=16) == 3
+    assert _step(batch=0) == 0
