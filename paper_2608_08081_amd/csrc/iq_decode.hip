@@ -110,7 +110,7 @@ __global__ __launch_bounds__(kSplitThreads) void decode_split_kernel(
     return;
   }
 
-  if (tid < 8) lut[tid] = cb.level[tid];
+  if (tid < 8) lut[tid] = codebook_level(cb, tid);
   const float* qsrc = q + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * group) * kDim;
   for (int e = tid; e < group * kDim; e += kSplitThreads) qt[e] = qsrc[e];
   __syncthreads();
@@ -302,7 +302,7 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, uint8_t* k_code
   // the group-8 kernel addresses one (sequence, KV head) row with 32-bit
   // byte offsets
   const bool row32 = capacity * kRecordBytes <= 0x7fffffff;
-  if (group == 8 && plan.g8_batches > 0 && capacity % 4 == 0 && aligned16 && row32) {
+  if (group == 8 && plan.g8_batches > 0 && capacity % 16 == 0 && aligned16 && row32) {
     float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
     return launch_decode_g8(plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes,
                             k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len, quats,

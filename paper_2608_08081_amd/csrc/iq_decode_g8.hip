@@ -1,11 +1,15 @@
 // Decode attention on the packed 3-bit cache for groups of 8 query heads per
-// KV head (App. A; Table 2 A-D; Sec. 3.4), gfx950, one launch per call.
+// KV head (App. A; Table 2 A-D; Sec. 3.4), gfx950.
 //
-// Work decomposition: one 256-thread workgroup per (sequence b, KV head g,
-// split of 64*NB positions); each of its 4 waves owns NB consecutive batches
-// of 16 positions.  Every load of the wave (packed keys, packed values and
-// both scale arrays for all its batches) is issued before any arithmetic, so
-// the whole cache is in flight at once.
+// Work decomposition: one 512-thread workgroup (8 waves, two per SIMD) per
+// (sequence b, KV head g, split of 16 * nbat positions); the split's nbat
+// batches of 16 positions are dealt to the 8 waves in contiguous runs of
+// nbat / 8 or nbat / 8 + 1 batches.  With one workgroup per CU the SIMDs
+// carry equal work.  Every load of a wave (query, rotation parameters, then
+// keys, value scales and values of all its batches, in the order they are
+// used) is issued before any arithmetic from one straight-line sequence, so
+// each later wait covers only the data it needs and the waves compute while
+// the rest of the cache is still arriving.
 //
 // The two contractions of a batch are dense 8-head x 128-dim x 16-position
 // products and run on the matrix cores (v_mfma_f32_16x16x32_f16):
@@ -32,12 +36,12 @@
 // weights and the PV products; scores are in log2 units (the rotated query
 // is pre-scaled by scale * log2 e) so exp2 is a single instruction.  The
 // value scales s^V are divided by the wave's largest value scale before the
-// fp16 conversion, keeping the weights in [0, 1].
+// fp16 conversion, keeping the weights in [0, 2^15].
 //
-// Merge: the 4 waves merge in LDS; workgroups of one (b, g) then merge
-// through the workspace, the last workgroup to finish (an atomic ticket per
-// (b, g), reset by that workgroup) merges all splits, divides by the sum and
-// applies the single inverse rotation R^T = H_128 M^T (Table 2 D).
+// Merge: the 8 waves merge in LDS; with several splits per (b, g) each
+// workgroup writes its partial (m, l, O) per head and a second kernel merges
+// them, divides by the sum and applies the single inverse rotation
+// R^T = H_128 M^T (Table 2 D); with one split the workgroup does it itself.
 #include <hip/hip_runtime.h>
 #include <math.h>
 
@@ -52,11 +56,13 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_a4_t __attribute__((ext_vector_type(2), aligned(4)));
 
-constexpr int kThreads = 256;
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;                 // waves of a decode workgroup
+constexpr int kThreads = 64 * kWaves;
+constexpr int kRotThreads = 256;          // (head, SO(4) block) tasks: waves 0..3
+constexpr int kMaxBatches = 5;            // 16-position batches per wave (register budget)
+constexpr int kMergeThreads = 256;
 constexpr int kHeads = 8;                 // query heads per KV head
 constexpr int kPart = 2 + kDim;           // m, l, o[128] per head
-constexpr int kLutStride = 64;            // words between entries of the lane-private tables
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kInvSqrtDim = 0.08838834764831845f;
 
@@ -126,34 +132,38 @@ __device__ __forceinline__ float group32_max(float v) {
   return v;
 }
 
+// Hamilton product a b of quaternions (w, x, y, z).
+__device__ __forceinline__ f32x4_t quat_mul(f32x4_t a, f32x4_t b) {
+  return f32x4_t{a[0] * b[0] - a[1] * b[1] - a[2] * b[2] - a[3] * b[3],
+                 a[0] * b[1] + a[1] * b[0] + a[2] * b[3] - a[3] * b[2],
+                 a[0] * b[2] - a[1] * b[3] + a[2] * b[0] + a[3] * b[1],
+                 a[0] * b[3] + a[1] * b[2] - a[2] * b[1] + a[3] * b[0]};
+}
+__device__ __forceinline__ f32x4_t quat_conj(f32x4_t a) {
+  return f32x4_t{a[0], -a[1], -a[2], -a[3]};
+}
+
 // Forward rotation (App. A) of one head held by 32 lanes, 4 dims per lane:
-// y_blk = M_blk H_4 (H_32 x)_blk, times `scale` (1/sqrt(128) and any score
-// scale).  qparam: this lane's block parameters (q_L, q_R).
-__device__ __forceinline__ f32x4_t rotate_forward(f32x4_t x, const float* qparam, int blk,
+// the block map v -> q_L v conj(q_R) (Sec. 3.3) applied to (H_4 (H_32 x))_blk,
+// times `scale` (1/sqrt(128) and any score scale).  ql, qr: this lane's block
+// parameters.
+__device__ __forceinline__ f32x4_t rotate_forward(f32x4_t x, f32x4_t ql, f32x4_t qr, int blk,
                                                   float scale) {
   lane_wht32(x, blk);
   float a = x[0], b = x[1], c = x[2], d = x[3];
   wht4(a, b, c, d);
-  float m[4][4];
-  so4_matrix(qparam, m);
-  f32x4_t y;
-#pragma unroll
-  for (int r = 0; r < 4; ++r)
-    y[r] = (m[r][0] * a + m[r][1] * b + m[r][2] * c + m[r][3] * d) * scale;
-  return y;
+  return quat_mul(quat_mul(ql, f32x4_t{a, b, c, d}), quat_conj(qr)) * scale;
 }
 
 // Inverse rotation R^T = H_128 diag(M^T) / sqrt(128) (Table 2 D) of one head
-// held by 32 lanes, 4 dims per lane.
-__device__ __forceinline__ f32x4_t rotate_inverse(f32x4_t o, const float* qparam, int blk) {
-  float m[4][4];
-  so4_matrix(qparam, m);
-  float z[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r)
-    z[r] = m[0][r] * o[0] + m[1][r] * o[1] + m[2][r] * o[2] + m[3][r] * o[3];
-  wht4(z[0], z[1], z[2], z[3]);
-  f32x4_t x = f32x4_t{z[0], z[1], z[2], z[3]};
+// held by 32 lanes, 4 dims per lane.  M^T z = conj(q_L) z q_R: the matrices
+// of left and right multiplication by a quaternion transpose to those of its
+// conjugate.
+__device__ __forceinline__ f32x4_t rotate_inverse(f32x4_t o, f32x4_t ql, f32x4_t qr, int blk) {
+  f32x4_t x = quat_mul(quat_mul(quat_conj(ql), o), qr);
+  float a = x[0], b = x[1], c = x[2], d = x[3];
+  wht4(a, b, c, d);
+  x = f32x4_t{a, b, c, d};
   lane_wht32(x, blk);
   return x * kInvSqrtDim;
 }
@@ -174,92 +184,86 @@ __device__ __forceinline__ f32x4_t decode_record_dims(const uint32_t* rec, const
                  static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p1 >> 16)))};
 }
 
-// Issues every cache load of one wave: keys, values and both scale arrays
-// of its NB batches of 16 positions, all before any arithmetic.
+// Issues every cache load of one wave: keys, value scales and values of its
+// NB batches of 16 positions, in the order they are used, before any
+// arithmetic.
 //  keys:   lane (t = col, gk = grp) takes dwords 3gk..3gk+2 of position t;
 //  values: lane (u = col, grp) takes 8 bytes covering bytes 3u..3u+2 of
 //          positions 4 grp + r, r = 0..3 (dword vdw = min(3u/4, 10));
 //  scales: one 16-byte load per array (positions 4 grp .. 4 grp + 3).
-// kMasked (the wave reaches past the last position `last` of its split):
-// key positions are clamped to `last`, and value and scale groups to the
-// 4-aligned group holding `last`, which lies inside the row because the
-// capacity is a multiple of 4; the positions past `last` are masked later.
-// Otherwise every address is the lane's base offset plus a constant.
-template <int NB, bool kMasked>
+// Batch starts are multiples of 16 and the capacity is a multiple of 16, so a
+// batch holding any position before the end of the split lies inside the
+// row.  Batch starts are clamped to `clamp16`, the wave's last batch holding
+// positions (a batch past it re-reads the same lines and is skipped).  Per
+// batch the start is a scalar and the lane offsets are constants: one
+// straight-line sequence for every wave, so the compiler keeps exact counts
+// of the loads in flight.
+template <int NB>
 __device__ __forceinline__ void load_wave(const uint8_t* kc, const float* kn, const uint8_t* vc,
-                                          const float* vn, int wbase, int last, int col, int grp,
-                                          int vdw, uint32_t (&kw)[NB][3],
+                                          const float* vn, int wbase, int clamp16, int col,
+                                          int grp, int vdw, uint32_t (&kw)[NB][3],
                                           uint32_t (&vw)[NB][4][2], f32x4_t (&ks)[NB],
                                           f32x4_t (&vs)[NB]) {
-  const uint8_t* kn8 = reinterpret_cast<const uint8_t*>(kn);
-  const uint8_t* vn8 = reinterpret_cast<const uint8_t*>(vn);
-  const uint32_t koff = static_cast<uint32_t>((wbase + col) * kRecordBytes + 12 * grp);
-  const uint32_t voff = static_cast<uint32_t>((wbase + 4 * grp) * kRecordBytes + 4 * vdw);
-  const uint32_t soff = static_cast<uint32_t>(4 * (wbase + 4 * grp));
-  const int last4 = last & ~3;
+  const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
+  const uint32_t voff = static_cast<uint32_t>(4 * grp * kRecordBytes + 4 * vdw);
+  const uint32_t soff = static_cast<uint32_t>(16 * grp);
+  int tb[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) tb[i] = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
-    const uint32_t* p;
-    const uint8_t* sk;
-    if constexpr (kMasked) {
-      const int t = wbase + 16 * i + col < last ? wbase + 16 * i + col : last;
-      p = reinterpret_cast<const uint32_t*>(kc +
-                                            static_cast<uint32_t>(t * kRecordBytes + 12 * grp));
-      const int t4 = wbase + 16 * i + 4 * grp < last4 ? wbase + 16 * i + 4 * grp : last4;
-      sk = kn8 + static_cast<uint32_t>(4 * t4);
-    } else {
-      p = reinterpret_cast<const uint32_t*>(kc + koff + 16 * kRecordBytes * i);
-      sk = kn8 + soff + 64 * i;
-    }
+    const uint8_t* kb = kc + static_cast<uint32_t>(tb[i] * kRecordBytes);
+    const uint32_t* p = reinterpret_cast<const uint32_t*>(kb + koff);
     kw[i][0] = p[0];
     kw[i][1] = p[1];
     kw[i][2] = p[2];
-    ks[i] = *reinterpret_cast<const f32x4_t*>(sk);
+    ks[i] = *reinterpret_cast<const f32x4_t*>(reinterpret_cast<const uint8_t*>(kn + tb[i]) +
+                                              soff);
   }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+    vs[i] = *reinterpret_cast<const f32x4_t*>(reinterpret_cast<const uint8_t*>(vn + tb[i]) +
+                                              soff);
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
-    const uint8_t* pv;
-    const uint8_t* sv;
-    if constexpr (kMasked) {
-      const int t4 = wbase + 16 * i + 4 * grp < last4 ? wbase + 16 * i + 4 * grp : last4;
-      pv = vc + static_cast<uint32_t>(t4 * kRecordBytes + 4 * vdw);
-      sv = vn8 + static_cast<uint32_t>(4 * t4);
-    } else {
-      pv = vc + voff + 16 * kRecordBytes * i;
-      sv = vn8 + soff + 64 * i;
-    }
+    const uint8_t* pv = vc + static_cast<uint32_t>(tb[i] * kRecordBytes) + voff;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const u32x2_a4_t d = *reinterpret_cast<const u32x2_a4_t*>(pv + kRecordBytes * r);
       vw[i][r][0] = d[0];
       vw[i][r][1] = d[1];
     }
-    vs[i] = *reinterpret_cast<const f32x4_t*>(sv);
   }
 }
 
-// Scores, softmax and value accumulation of one wave over its NB batches
-// (kMasked: some positions of the wave lie past the end of the split).
-template <int NB, bool kMasked>
+// Scores, softmax and value accumulation of one wave over the batches that
+// hold its nvalid (> 0) positions; only the last of them can be partial.
+// Scores are kept in the per-head scaled domain (x = acc * s^K, the query
+// operand carried 2^qexp); qdown = 2^-qexp turns them into log2 units inside
+// the exponent.  On return m_run is in log2 units.
+template <int NB>
 __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
                                             const uint32_t (&vw)[NB][4][2],
                                             const f32x4_t (&ks)[NB], const f32x4_t (&vs)[NB],
                                             const u32x4_t (&qhi)[4], const u32x4_t (&qlo)[4],
-                                            const uint32_t* lutl, int col, int grp, int nvalid,
-                                            uint32_t vshift, float qdown, float& m_run,
+                                            const uint32_t* lut, int col, int grp, int nvalid,
+                                            uint32_t vsh, float qdown, float& m_run,
                                             float& l_run, float& vmax, f32x4_t (&o_acc)[4]) {
   // ---- phase 1: scores (Table 2 A) -----------------------------------------
   f32x4_t sc[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
+    if (16 * i >= nvalid) break;
     const uint32_t w0 = kw[i][0], w1 = kw[i][1], w2 = kw[i][2];
     u32x4_t a[4];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      a[kb] = u32x4_t{lutl[kLutStride * slice_field(kb * 4 + 0, w0, w1, w2)],
-                      lutl[kLutStride * slice_field(kb * 4 + 1, w0, w1, w2)],
-                      lutl[kLutStride * slice_field(kb * 4 + 2, w0, w1, w2)],
-                      lutl[kLutStride * slice_field(kb * 4 + 3, w0, w1, w2)]};
+      a[kb] = u32x4_t{lut[slice_field(kb * 4 + 0, w0, w1, w2)],
+                      lut[slice_field(kb * 4 + 1, w0, w1, w2)],
+                      lut[slice_field(kb * 4 + 2, w0, w1, w2)],
+                      lut[slice_field(kb * 4 + 3, w0, w1, w2)]};
     }
     f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -268,20 +272,24 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
       acc = mfma(a[kb], qlo[kb], acc);
     }
     // lane (col, grp) holds positions 16 i + 4 grp + r of head col % 8
-    const f32x4_t kq = ks[i] * qdown;
+    f32x4_t x = acc * ks[i];
+    if (16 * i + 16 > nvalid) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      float s = acc[r] * kq[r];
-      if constexpr (kMasked) {
-        const bool ok = 16 * i + 4 * grp + r < nvalid;
-        s = ok ? s : -INFINITY;
-        vmax = fmaxf(vmax, ok ? vs[i][r] : 0.f);
-      } else {
-        vmax = fmaxf(vmax, vs[i][r]);
-      }
-      sc[i][r] = s;
-      m_run = fmaxf(m_run, s);
+      for (int r = 0; r < 4; ++r) x[r] = (16 * i + 4 * grp + r < nvalid) ? x[r] : -INFINITY;
     }
+    sc[i] = x;
+    m_run = fmaxf(fmaxf(m_run, fmaxf(x[0], x[1])), fmaxf(x[2], x[3]));
+  }
+  // largest value scale of the wave (its loads were issued after the keys)
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    if (16 * i >= nvalid) break;
+    f32x4_t v = vs[i];
+    if (16 * i + 16 > nvalid) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v[r] = (16 * i + 4 * grp + r < nvalid) ? v[r] : 0.f;
+    }
+    vmax = fmaxf(fmaxf(vmax, fmaxf(v[0], v[1])), fmaxf(v[2], v[3]));
   }
   m_run = wave_max(m_run);
   vmax = wave_max(vmax);
@@ -289,19 +297,21 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
   // the largest weight; split into fp16 hi + lo parts
   const float vinv = vmax > 0.f ? 32768.0f * __builtin_amdgcn_rcpf(vmax) : 0.f;
   const uint32_t slot_shift = (col >= 8) ? 16u : 0u;
+  const float mq = -m_run * qdown;
 
   // ---- phase 2: weights (Table 2 B) and values (Table 2 C) -----------------
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
+    if (16 * i >= nvalid) break;
     f32x4_t wv = vs[i] * vinv;
-    if constexpr (kMasked) {
+    if (16 * i + 16 > nvalid) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) wv[r] = (16 * i + 4 * grp + r < nvalid) ? wv[r] : 0.f;
     }
     u32x4_t pw_hi, pw_lo;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float e = __builtin_amdgcn_exp2f(sc[i][r] - m_run);
+      const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[i][r], qdown, mq));
       l_run += e;
       const float pf = e * wv[r];
       const _Float16 ph = static_cast<_Float16>(pf);
@@ -312,12 +322,14 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
     u32x4_t vb[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const uint32_t lo = col == 15 ? vw[i][r][1] : vw[i][r][0];
-      const uint32_t win = __builtin_amdgcn_alignbit(vw[i][r][1], lo, vshift);
-      vb[0][r] = lutl[kLutStride * (win & 63u)];
-      vb[1][r] = lutl[kLutStride * __builtin_amdgcn_ubfe(win, 6, 6)];
-      vb[2][r] = lutl[kLutStride * __builtin_amdgcn_ubfe(win, 12, 6)];
-      vb[3][r] = lutl[kLutStride * __builtin_amdgcn_ubfe(win, 18, 6)];
+      // bytes 3u .. 3u+2 of the 8-byte window (a 64-bit shift: lane 15's
+      // bytes start 5 bytes in)
+      const uint64_t w64 = (static_cast<uint64_t>(vw[i][r][1]) << 32) | vw[i][r][0];
+      const uint32_t win = static_cast<uint32_t>(w64 >> vsh);
+      vb[0][r] = lut[win & 63u];
+      vb[1][r] = lut[__builtin_amdgcn_ubfe(win, 6, 6)];
+      vb[2][r] = lut[__builtin_amdgcn_ubfe(win, 12, 6)];
+      vb[3][r] = lut[__builtin_amdgcn_ubfe(win, 18, 6)];
     }
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
@@ -326,6 +338,7 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
     }
   }
   l_run = wave_sum(l_run);
+  m_run *= qdown;
 }
 
 // kAppend: the fused decode step.  The new key and value of every (sequence
@@ -346,21 +359,18 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     int32_t* __restrict__ status) {
   constexpr int kQRow = kDim / 2 + 4;   // fp16-pair row of one head, padded (68 words)
   __shared__ uint32_t lut64[64];
-  // 64 copies of the 64-entry table: entry e of copy l at word 64 e + l, so
-  // lane l always reads bank l (random codes make shared-table lookups
-  // conflict); after the last lookup the same memory holds the per-wave
-  // outputs
-  static_assert(kWaves * kHeads * kDim == kLutStride * 64, "table / output aliasing");
-  __shared__ __attribute__((aligned(16))) uint32_t big[kLutStride * 64];
   __shared__ __attribute__((aligned(16))) uint32_t qop[2][kHeads][kQRow];
   __shared__ int qexp_s[kHeads];
-  float(*wave_o)[kHeads * kDim] = reinterpret_cast<float(*)[kHeads * kDim]>(big);
+  __shared__ __attribute__((aligned(16))) float wave_o[kWaves][kHeads * kDim];
   __shared__ float wave_ml[kWaves][2][kHeads];
   __shared__ uint32_t new_rec[2][kRecordWords];   // kAppend: the new key / value record
   __shared__ float new_scale[2];
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  // the wave index as a scalar: every per-wave branch is then a scalar
+  // branch, and per-wave positions are scalars
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
 
   const int split = blockIdx.x % n_splits;
@@ -405,9 +415,19 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   const bool new_attended = writer && seq0 < max_seq_len;
   int end = seq < start + split_len ? seq : start + split_len;
   if (new_attended) end = seq0;
-  const int wbase = start + wave * NB * 16;   // first position of the wave
-  const int last = end > 0 ? end - 1 : 0;     // last position read (clamp target)
-  // (b, g) row bases (wave-uniform); lane offsets in 32 bits (capacity * 48 < 2^31)
+  // this wave's run of batches: nbat / 8 each, one more for the first
+  // nbat % 8 waves
+  const int nbat = split_len >> 4;
+  const int nb_base = nbat / kWaves, nb_rem = nbat % kWaves;
+  const int nb_w = nb_base + (wave < nb_rem ? 1 : 0);
+  const int wbase = start + 16 * (wave * nb_base + (wave < nb_rem ? wave : nb_rem));
+  int nvalid = end - wbase;   // this wave's positions (may be <= 0)
+  nvalid = nvalid < 16 * nb_w ? nvalid : 16 * nb_w;
+  // start of the wave's last batch holding positions (clamp of the loads)
+  int clamp16 = ((end > 0 ? end - 1 : 0) & ~15);
+  clamp16 = clamp16 < wbase + 16 * (nb_w - 1) ? clamp16 : wbase + 16 * (nb_w - 1);
+  clamp16 = clamp16 > 0 ? clamp16 : 0;
+  // (b, g) row bases (scalars); lane offsets in 32 bits (capacity * 48 < 2^31)
   const int64_t row = static_cast<int64_t>(bg) * capacity;
   uint8_t* kc = k_codes + row * kRecordBytes;
   uint8_t* vc = v_codes + row * kRecordBytes;
@@ -438,45 +458,42 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   }
 
   // ---- issue every load of the wave -------------------------------------
-  // the group's 8 query heads first (one float4 per thread), then the cache
+  // thread (head qh, SO(4) block qblk) for tid < 256; the other waves load
+  // the same query and parameters (no branch around loads)
+  const int qh = (tid >> 5) & 7, qblk = tid & 31;
   const f32x4_t qv = *reinterpret_cast<const f32x4_t*>(
-      q + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * kHeads) * kDim +
-      4 * tid);
-  // this thread's SO(4) block parameters (block tid % 32 of KV head g)
-  const float* quats_g = quats + static_cast<int64_t>(g) * kQuatFloats;
-  float qparam[8];
-  {
-    const f32x4_t p0 = *reinterpret_cast<const f32x4_t*>(quats_g + 8 * (tid & 31));
-    const f32x4_t p1 = *reinterpret_cast<const f32x4_t*>(quats_g + 8 * (tid & 31) + 4);
-    qparam[0] = p0[0]; qparam[1] = p0[1]; qparam[2] = p0[2]; qparam[3] = p0[3];
-    qparam[4] = p1[0]; qparam[5] = p1[1]; qparam[6] = p1[2]; qparam[7] = p1[3];
-  }
+      q + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * kHeads + qh) * kDim +
+      4 * qblk);
+  const f32x4_t* qpar = reinterpret_cast<const f32x4_t*>(
+      quats + static_cast<int64_t>(g) * kQuatFloats + 8 * qblk);
+  const f32x4_t ql = qpar[0], qr = qpar[1];
+  // the query and rotation loads go out before the cache loads: loads
+  // complete in issue order, so waiting for them must not wait for the cache
+  __builtin_amdgcn_sched_barrier(0);
   uint32_t kw[NB][3];
   uint32_t vw[NB][4][2];
   f32x4_t ks[NB], vs[NB];
   const int vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
-  const uint32_t vshift = static_cast<uint32_t>(8 * (3 * col - 4 * vdw)) & 31u;   // col 15: 40 -> 8
-  const int nvalid = end - wbase;   // valid positions of this wave (may be <= 0)
-  if (nvalid >= NB * 16)
-    load_wave<NB, false>(kc, kn, vc, vn, wbase, last, col, grp, vdw, kw, vw, ks, vs);
-  else
-    load_wave<NB, true>(kc, kn, vc, vn, wbase, last, col, grp, vdw, kw, vw, ks, vs);
+  const uint32_t vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));   // 0..40
+  load_wave<NB>(kc, kn, vc, vn, wbase, clamp16, col, grp, vdw, kw, vw, ks, vs);
 
   // ---- while the loads fly: LUT and the rotated query --------------------
   if (tid < 64) {
-    const uint32_t lo = __builtin_bit_cast(uint16_t, static_cast<_Float16>(cb.level[tid & 7]));
-    const uint32_t hi = __builtin_bit_cast(uint16_t, static_cast<_Float16>(cb.level[tid >> 3]));
+    const uint32_t lo =
+        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & 7)));
+    const uint32_t hi =
+        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> 3)));
     lut64[tid] = lo | (hi << 16);
   }
-  // thread = (head qh, SO(4) block qblk); the 32 blocks of a head are 32
-  // consecutive lanes of one wave, so the rotation needs no barrier
-  const int qh = tid >> 5, qblk = tid & 31;
-  const f32x4_t y = rotate_forward(qv, qparam, qblk, kInvSqrtDim * qscale);
-  // fp16 operands are kept in the normal range by an exact power-of-two
-  // scale per head: the largest rotated entry is brought below 2^14 (hi and
-  // lo parts both normal) and the scale is undone on the scores
-  int qexp = 0;
-  {
+  // the 32 blocks of a head are 32 consecutive lanes of one wave, so the
+  // rotation needs no barrier
+  f32x4_t y = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  if (tid < kRotThreads) {
+    y = rotate_forward(qv, ql, qr, qblk, kInvSqrtDim * qscale);
+    // fp16 operands are kept in the normal range by an exact power-of-two
+    // scale per head: the largest rotated entry is brought below 2^14 (hi
+    // and lo parts both normal) and the scale is undone on the scores
+    int qexp = 0;
     const float am = group32_max(
         fmaxf(fmaxf(fabsf(y[0]), fabsf(y[1])), fmaxf(fabsf(y[2]), fabsf(y[3]))));
     if (am > 0.f) {
@@ -485,8 +502,6 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
       qexp = 14 - e;
       qexp = qexp > 100 ? 100 : (qexp < -100 ? -100 : qexp);
     }
-  }
-  {
     // fp16 hi and lo pairs of this thread's 4 dims, stored once per workgroup
     const float qup = ldexpf(1.0f, qexp);
     uint32_t hw[2], lw[2];
@@ -508,11 +523,6 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     if (qblk == 0) qexp_s[qh] = qexp;
   }
   lds_barrier();   // lut64, qop, qexp_s
-#pragma unroll
-  for (int j = 0; j < 64 / kWaves; ++j) {
-    const int e = wave + kWaves * j;
-    big[kLutStride * e + lane] = lut64[e];
-  }
   // QK B operands: column col -> head col % 8; MFMA kb, lane group grp ->
   // dims 32 grp + 8 kb + 0..7 (fp16 pair words 16 grp + 4 kb .. +3)
   u32x4_t qhi[4], qlo[4];
@@ -522,23 +532,20 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     qlo[kb] = *reinterpret_cast<const u32x4_t*>(&qop[1][col & 7][16 * grp + 4 * kb]);
   }
   const float qdown = ldexpf(1.0f, -qexp_s[col & 7]);
-  lds_barrier();   // lane-private tables
 
   float m_run = -INFINITY, l_run = 0.f, vmax = 0.f;
   f32x4_t o_acc[4];
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  if (nvalid >= NB * 16)
-    attend_wave<NB, false>(kw, vw, ks, vs, qhi, qlo, big + lane, col, grp, nvalid, vshift,
-                           qdown, m_run, l_run, vmax, o_acc);
-  else if (nvalid > 0)
-    attend_wave<NB, true>(kw, vw, ks, vs, qhi, qlo, big + lane, col, grp, nvalid, vshift,
-                          qdown, m_run, l_run, vmax, o_acc);
+  if (nvalid > 0)
+    attend_wave<NB>(kw, vw, ks, vs, qhi, qlo, lut64, col, grp, nvalid, vsh, qdown, m_run,
+                    l_run, vmax, o_acc);
 
   if (compressing) {
     // the two chains are independent and interleave
-    const WaveCode wk = compress_vector_wave(nk0, nk1, nqp, cb, lane);
-    const WaveCode wv = compress_vector_wave(nv0, nv1, nqp, cb, lane);
+    const float* qp0 = nqp;
+    const WaveCode wk = compress_vector_wave(nk0, nk1, qp0, cb, lane);
+    const WaveCode wv = compress_vector_wave(nv0, nv1, qp0, cb, lane);
     if (lane < kRecordWords) {
       reinterpret_cast<uint32_t*>(kc + static_cast<int64_t>(seq0) * kRecordBytes)[lane] = wk.word;
       reinterpret_cast<uint32_t*>(vc + static_cast<int64_t>(seq0) * kRecordBytes)[lane] = wv.word;
@@ -553,8 +560,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     }
   }
 
-  // ---- merge the 4 waves in LDS ---------------------------------------------
-  lds_barrier();   // every wave is done with the tables; new_rec, new_scale
+  // ---- merge the 8 waves in LDS ---------------------------------------------
   // lane (u = col, grp) holds rows 4 grp + r = (head (4 grp + r) % 8, slot
   // grp / 2) of MFMA nb, i.e. dim 2 (4 u + nb) + slot.
   const float oscale = vmax * (1.0f / 32768.0f);
@@ -569,16 +575,17 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     wave_ml[wave][0][lane] = m_run;     // lanes 0..7 hold heads 0..7
     wave_ml[wave][1][lane] = l_run;
   }
-  lds_barrier();
+  lds_barrier();   // wave_o, wave_ml, new_rec, new_scale
+  if (tid >= kRotThreads) return;
 
   // thread -> (head h = tid / 32, dims 4 (tid % 32) .. +3), the same
   // (head, block) as in the query rotation
-  const int mh = tid >> 5, md = (tid & 31) * 4;
+  const int mh = qh, md = 4 * qblk;
   float M = -INFINITY;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wave_ml[w][0][mh]);
   float s_new = -INFINITY;
-  f32x4_t v_new4;
+  f32x4_t v_new4 = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if (new_attended) {
     // score of the appended key: s^K (q_tilde . C[code]) over this thread's
     // 4 dims (codes of dims md..md+3 = bits 3 md .. 3 md + 11 of the record),
@@ -611,13 +618,13 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
 
   if (n_splits == 1) {
     // thread (mh, md / 4) holds block md / 4 of head mh: rotate back in place
-    const f32x4_t o = rotate_inverse(O * (1.0f / L), qparam, tid & 31);
+    const f32x4_t o = rotate_inverse(O * (1.0f / L), ql, qr, qblk);
     *reinterpret_cast<f32x4_t*>(out_bg + mh * kDim + md) = o;
     return;
   }
   // ---- partial result of this split ------------------------------------------
   float* pp = part_bg + static_cast<int64_t>(split) * (kHeads * kPart) + mh * kPart;
-  if ((tid & 31) == 0) {
+  if (qblk == 0) {
     pp[0] = M;
     pp[1] = L;
   }
@@ -633,7 +640,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
 // kAppend: workgroup (b, head 0) then advances seq_lens[b] past the token the
 // decode kernel appended.
 template <bool kAppend>
-__global__ __launch_bounds__(kThreads) void merge_g8_kernel(
+__global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     const float* __restrict__ partials, const float* __restrict__ quats, float* __restrict__ out,
     int n_kv_heads, int n_splits, int32_t* __restrict__ seq_lens, int64_t capacity) {
   constexpr int kUnroll = 16;
@@ -651,14 +658,9 @@ __global__ __launch_bounds__(kThreads) void merge_g8_kernel(
                       static_cast<int64_t>(b * n_kv_heads + g) * n_splits * (kHeads * kPart) +
                       hh * kPart;
   // block parameters for the inverse rotation (threads 0..31: block tid)
-  float qparam[8];
-  {
-    const float* qg = quats + static_cast<int64_t>(g) * kQuatFloats + 8 * dq;
-    const f32x4_t p0 = *reinterpret_cast<const f32x4_t*>(qg);
-    const f32x4_t p1 = *reinterpret_cast<const f32x4_t*>(qg + 4);
-    qparam[0] = p0[0]; qparam[1] = p0[1]; qparam[2] = p0[2]; qparam[3] = p0[3];
-    qparam[4] = p1[0]; qparam[5] = p1[1]; qparam[6] = p1[2]; qparam[7] = p1[3];
-  }
+  const f32x4_t* qg =
+      reinterpret_cast<const f32x4_t*>(quats + static_cast<int64_t>(g) * kQuatFloats + 8 * dq);
+  const f32x4_t ql = qg[0], qr = qg[1];
   float M = -INFINITY, L = 0.f;
   f32x4_t O = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int s0 = sg; s0 < n_splits; s0 += 8 * kUnroll) {
@@ -716,7 +718,7 @@ __global__ __launch_bounds__(kThreads) void merge_g8_kernel(
       l += red_l[j];
     }
     // an empty sequence (every split empty) gives a zero row
-    const f32x4_t r = l > 0.f ? rotate_inverse(o * (1.0f / l), qparam, tid)
+    const f32x4_t r = l > 0.f ? rotate_inverse(o * (1.0f / l), ql, qr, tid)
                               : f32x4_t{0.f, 0.f, 0.f, 0.f};
     *reinterpret_cast<f32x4_t*>(out + (static_cast<int64_t>(b) * n_q_heads + h) * kDim +
                                 4 * tid) = r;
@@ -738,27 +740,32 @@ __global__ void advance_lengths_kernel(int32_t* __restrict__ seq_lens, int64_t c
 }  // namespace
 
 // Split plan of the group-8 path: splits per (sequence, KV head) and their
-// length.  At least ceil(T / 512) splits (a wave handles at most 8 batches of
-// 16 positions); while the grid is small (<= 4 rounds of 256 workgroups) the
-// split count is raised so that the grid fills whole rounds of the 256 CUs.
+// length (a multiple of 16).  A workgroup covers at most 8 waves x 5 batches
+// x 16 = 640 positions; while the grid is small (<= 4 rounds of one
+// workgroup per CU) the split count is raised so that the grid fills whole
+// rounds, but a split keeps at least one batch per wave.
 void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
              int64_t* n_splits, int64_t* split_len) {
+  constexpr int64_t kCus = 256;
+  constexpr int64_t kMaxLen = 16 * kWaves * kMaxBatches;
   const int64_t t = max_seq_len > 0 ? max_seq_len : 1;
   const int64_t bg = batch * n_kv_heads > 0 ? batch * n_kv_heads : 1;
-  int64_t s = (t + 511) / 512;
+  int64_t s = (t + kMaxLen - 1) / kMaxLen;
   const int64_t wgs = bg * s;
-  if (wgs <= 4 * 256) {
-    const int64_t rounds = (wgs + 255) / 256;
-    const int64_t s_fill = (rounds * 256) / bg;
+  if (wgs <= 4 * kCus) {
+    const int64_t rounds = (wgs + kCus - 1) / kCus;
+    int64_t s_fill = (rounds * kCus) / bg;
+    const int64_t s_min_len = (t + 16 * kWaves - 1) / (16 * kWaves);   // >= 1 batch per wave
+    if (s_fill > s_min_len) s_fill = s_min_len;
     if (s_fill > s) s = s_fill;
   }
-  if (s > t) s = t;
   int64_t len = (t + s - 1) / s;
   len = (len + 15) / 16 * 16;
   s = (t + len - 1) / len;
   *split_len = len;
   *n_splits = s;
-  *nb = static_cast<int>((len + kWaves * 16 - 1) / (kWaves * 16));
+  const int64_t nbat = len / 16;
+  *nb = static_cast<int>((nbat + kWaves - 1) / kWaves);
 }
 
 hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const float* q,
@@ -786,10 +793,7 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
     case 2: IQ_LAUNCH_G8(2, APP_); break; \
     case 3: IQ_LAUNCH_G8(3, APP_); break; \
     case 4: IQ_LAUNCH_G8(4, APP_); break; \
-    case 5: IQ_LAUNCH_G8(5, APP_); break; \
-    case 6: IQ_LAUNCH_G8(6, APP_); break; \
-    case 7: IQ_LAUNCH_G8(7, APP_); break; \
-    default: IQ_LAUNCH_G8(8, APP_); break; \
+    default: IQ_LAUNCH_G8(5, APP_); break; \
   }
   if (append) {
     IQ_LAUNCH_G8_NB(true)
@@ -805,13 +809,13 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   if (n_splits > 1) {
     const dim3 mgrid(static_cast<unsigned>(batch * n_kv_heads * kHeads));
     if (append)
-      hipLaunchKernelGGL(merge_g8_kernel<true>, mgrid, dim3(kThreads), 0, stream, partials, quats,
-                         out, static_cast<int>(n_kv_heads), static_cast<int>(n_splits), seq_lens,
-                         capacity);
+      hipLaunchKernelGGL(merge_g8_kernel<true>, mgrid, dim3(kMergeThreads), 0, stream, partials,
+                         quats, out, static_cast<int>(n_kv_heads), static_cast<int>(n_splits),
+                         seq_lens, capacity);
     else
-      hipLaunchKernelGGL(merge_g8_kernel<false>, mgrid, dim3(kThreads), 0, stream, partials, quats,
-                         out, static_cast<int>(n_kv_heads), static_cast<int>(n_splits), seq_lens,
-                         capacity);
+      hipLaunchKernelGGL(merge_g8_kernel<false>, mgrid, dim3(kMergeThreads), 0, stream, partials,
+                         quats, out, static_cast<int>(n_kv_heads), static_cast<int>(n_splits),
+                         seq_lens, capacity);
     e = hipGetLastError();
   } else if (append) {
     hipLaunchKernelGGL(advance_lengths_kernel, dim3(static_cast<unsigned>((batch + 255) / 256)),

@@ -213,11 +213,11 @@ def test_varlen_batched_decode_full_size():
     [4095], [4096], [4097],
 ])
 def test_group8_matrix_core_path(seq):
-    """Group-8 decode (matrix-core path: capacity a multiple of 4, 16-byte
+    """Group-8 decode (matrix-core path: capacity a multiple of 16, 16-byte
     aligned scales) at lengths around every batch/wave/split boundary,
     several sequences per call, one of them empty."""
     w = synth.Workload(8, "g8", len(seq), 8 * 2, 2, max(seq), "f16", rotation_seed=5)
-    cap = ((max(max(seq), 1) + 3) // 4) * 4 + 4
+    cap = ((max(max(seq), 1) + 15) // 16) * 16 + 16
     k, v, quats, kp, kn, vp, vn = _oracle_cache(w, 3, max(seq), len(seq), cap)
     q = synth.queries(3, w)[0]
     got = _gpu_decode(q, kp, kn, vp, vn, seq, quats, cap)

@@ -78,7 +78,8 @@ def _check_new_records(cache, ora, seq0, cap, label):
     (16, 2, [0, 1, 15, 16, 17, 31, 32, 33, 63, 64, 65, 127, 128, 129, 500], 512),
     (32, 4, [2999, 1500], 3008),
     (8, 1, [4095], 4096),
-    (8, 1, [4096], 4100),
+    (8, 1, [4096], 4112),
+    (8, 1, [4096], 4100),       # capacity not a multiple of 16: generic path
     # other group sizes: append kernel, then the generic decode
     (16, 4, [0, 700, 1023], 1024),
     (6, 2, [300], 301),
@@ -99,7 +100,7 @@ def test_step_matches_oracle(hq, hkv, seq0, cap):
 
 def test_step_f32_inputs_and_custom_scale():
     w = synth.Workload(0, "step32", 2, 16, 2, 777, "f32", rotation_seed=3)
-    seq0, cap = [776, 100], 780
+    seq0, cap = [776, 100], 784
     cache, quats, k_new, v_new, ora = _setup(w, 6, seq0, cap)
     q = synth.queries(6, w)[0]
     out = api.iq_decode_step(_dev(q), _dev(k_new), _dev(v_new), cache["k_codes"],
@@ -149,8 +150,9 @@ def test_step_beyond_max_seq_len():
 
 
 @pytest.mark.parametrize("hq,hkv,seq0,cap", [
-    (32, 4, [8191], 8200),
+    (32, 4, [8191], 8208),
     (16, 2, [17, 0, 1000], 1024),
+    (32, 4, [8191], 8200),      # capacity not a multiple of 16: generic path
 ])
 def test_step_equals_append_then_decode(hq, hkv, seq0, cap):
     """Fused step and the two separate calls on identical caches: identical
