@@ -53,6 +53,7 @@ namespace {
 
 typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_a4_t __attribute__((ext_vector_type(2), aligned(4)));
 
@@ -88,6 +89,16 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Orders this wave's LDS accesses across lanes: a value one lane wrote is
+// read by another lane of the same wave after this point.  The wave's LDS
+// operations execute in order, so no hardware wait is needed; this keeps the
+// compiler from moving the accesses across it.
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront", "local");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront", "local");
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -184,13 +195,20 @@ __device__ __forceinline__ f32x4_t decode_record_dims(const uint32_t* rec, const
                  static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p1 >> 16)))};
 }
 
-// Issues every cache load of one wave: keys, value scales and values of its
-// NB batches of 16 positions, in the order they are used, before any
-// arithmetic.
-//  keys:   lane (t = col, gk = grp) takes dwords 3gk..3gk+2 of position t;
-//  values: lane (u = col, grp) takes 8 bytes covering bytes 3u..3u+2 of
-//          positions 4 grp + r, r = 0..3 (dword vdw = min(3u/4, 10));
-//  scales: one 16-byte load per array (positions 4 grp .. 4 grp + 3).
+// Per-wave LDS staging: the two scale arrays of the wave (a 16-byte group
+// per lane, 64 groups) and a double buffer of one batch of value records.
+struct WaveStage {
+  f32x4_t ks[64];
+  f32x4_t vs[64];
+  uint32_t rec[2][16 * kRecordWords];
+};
+
+// Issues every cache load of one wave, in the order the data is used and
+// before any arithmetic: both scale arrays (one 16-byte load per lane: lane
+// j takes positions 4j .. 4j+3 of the wave), then per batch of 16 positions
+// the keys, then the values.  Keys and values are loaded the same way: lane
+// (t = col, gk = grp) takes dwords 3gk .. 3gk+2 of position t, one coalesced
+// 768-byte load per batch.
 // Batch starts are multiples of 16 and the capacity is a multiple of 16, so a
 // batch holding any position before the end of the split lies inside the
 // row.  Batch starts are clamped to `clamp16`, the wave's last batch holding
@@ -200,41 +218,37 @@ __device__ __forceinline__ f32x4_t decode_record_dims(const uint32_t* rec, const
 // of the loads in flight.
 template <int NB>
 __device__ __forceinline__ void load_wave(const uint8_t* kc, const float* kn, const uint8_t* vc,
-                                          const float* vn, int wbase, int clamp16, int col,
-                                          int grp, int vdw, uint32_t (&kw)[NB][3],
-                                          uint32_t (&vw)[NB][4][2], f32x4_t (&ks)[NB],
-                                          f32x4_t (&vs)[NB]) {
+                                          const float* vn, int wbase, int clamp16, int lane,
+                                          int col, int grp, uint32_t (&kw)[NB][3],
+                                          uint32_t (&vw)[NB][3], f32x4_t& ksl, f32x4_t& vsl) {
   const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
-  const uint32_t voff = static_cast<uint32_t>(4 * grp * kRecordBytes + 4 * vdw);
-  const uint32_t soff = static_cast<uint32_t>(16 * grp);
+  // scales: lane j -> batch j / 4 (clamped like the batches), group j % 4
+  {
+    const int jb = lane >> 2 < NB ? lane >> 2 : NB - 1;
+    const int tj = (wbase + 16 * jb < clamp16 ? wbase + 16 * jb : clamp16) + 4 * (lane & 3);
+    ksl = *reinterpret_cast<const f32x4_t*>(kn + tj);
+    vsl = *reinterpret_cast<const f32x4_t*>(vn + tj);
+  }
   int tb[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) tb[i] = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
-    const uint8_t* kb = kc + static_cast<uint32_t>(tb[i] * kRecordBytes);
-    const uint32_t* p = reinterpret_cast<const uint32_t*>(kb + koff);
+    const uint32_t* p =
+        reinterpret_cast<const uint32_t*>(kc + static_cast<uint32_t>(tb[i] * kRecordBytes) + koff);
     kw[i][0] = p[0];
     kw[i][1] = p[1];
     kw[i][2] = p[2];
-    ks[i] = *reinterpret_cast<const f32x4_t*>(reinterpret_cast<const uint8_t*>(kn + tb[i]) +
-                                              soff);
   }
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-  for (int i = 0; i < NB; ++i)
-    vs[i] = *reinterpret_cast<const f32x4_t*>(reinterpret_cast<const uint8_t*>(vn + tb[i]) +
-                                              soff);
-  __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
   for (int i = 0; i < NB; ++i) {
-    const uint8_t* pv = vc + static_cast<uint32_t>(tb[i] * kRecordBytes) + voff;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const u32x2_a4_t d = *reinterpret_cast<const u32x2_a4_t*>(pv + kRecordBytes * r);
-      vw[i][r][0] = d[0];
-      vw[i][r][1] = d[1];
-    }
+    const uint32_t* p =
+        reinterpret_cast<const uint32_t*>(vc + static_cast<uint32_t>(tb[i] * kRecordBytes) + koff);
+    vw[i][0] = p[0];
+    vw[i][1] = p[1];
+    vw[i][2] = p[2];
   }
 }
 
@@ -243,13 +257,16 @@ __device__ __forceinline__ void load_wave(const uint8_t* kc, const float* kn, co
 // Scores are kept in the per-head scaled domain (x = acc * s^K, the query
 // operand carried 2^qexp); qdown = 2^-qexp turns them into log2 units inside
 // the exponent.  On return m_run is in log2 units.
+// Scale group g of batch i (positions 16 i + 4 g ..) is st.ks[4 i + g].  Each
+// batch's value records go through st.rec (lane (t, gk) writes its 12 bytes
+// of record t, lane (u, grp) reads the 8-byte window holding bytes 3u..3u+2
+// of records 4 grp + r); the wave's own LDS operations complete in order.
 template <int NB>
 __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
-                                            const uint32_t (&vw)[NB][4][2],
-                                            const f32x4_t (&ks)[NB], const f32x4_t (&vs)[NB],
+                                            const uint32_t (&vw)[NB][3], WaveStage& st,
                                             const u32x4_t (&qhi)[4], const u32x4_t (&qlo)[4],
                                             const uint32_t* lut, int col, int grp, int nvalid,
-                                            uint32_t vsh, float qdown, float& m_run,
+                                            int vdw, uint32_t vsh, float qdown, float& m_run,
                                             float& l_run, float& vmax, f32x4_t (&o_acc)[4]) {
   // ---- phase 1: scores (Table 2 A) -----------------------------------------
   f32x4_t sc[NB];
@@ -272,7 +289,7 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
       acc = mfma(a[kb], qlo[kb], acc);
     }
     // lane (col, grp) holds positions 16 i + 4 grp + r of head col % 8
-    f32x4_t x = acc * ks[i];
+    f32x4_t x = acc * st.ks[4 * i + grp];
     if (16 * i + 16 > nvalid) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) x[r] = (16 * i + 4 * grp + r < nvalid) ? x[r] : -INFINITY;
@@ -280,15 +297,17 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
     sc[i] = x;
     m_run = fmaxf(fmaxf(m_run, fmaxf(x[0], x[1])), fmaxf(x[2], x[3]));
   }
-  // largest value scale of the wave (its loads were issued after the keys)
+  // largest value scale of the wave
+  f32x4_t vsv[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
     if (16 * i >= nvalid) break;
-    f32x4_t v = vs[i];
+    f32x4_t v = st.vs[4 * i + grp];
     if (16 * i + 16 > nvalid) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) v[r] = (16 * i + 4 * grp + r < nvalid) ? v[r] : 0.f;
     }
+    vsv[i] = v;
     vmax = fmaxf(fmaxf(vmax, fmaxf(v[0], v[1])), fmaxf(v[2], v[3]));
   }
   m_run = wave_max(m_run);
@@ -303,11 +322,13 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
     if (16 * i >= nvalid) break;
-    f32x4_t wv = vs[i] * vinv;
-    if (16 * i + 16 > nvalid) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) wv[r] = (16 * i + 4 * grp + r < nvalid) ? wv[r] : 0.f;
-    }
+    uint32_t* rec = st.rec[i & 1];
+    wave_lds_fence();   // reads of this buffer two batches ago come first
+    rec[col * kRecordWords + 3 * grp] = vw[i][0];
+    rec[col * kRecordWords + 3 * grp + 1] = vw[i][1];
+    rec[col * kRecordWords + 3 * grp + 2] = vw[i][2];
+    wave_lds_fence();
+    const f32x4_t wv = vsv[i] * vinv;
     u32x4_t pw_hi, pw_lo;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -324,7 +345,8 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
     for (int r = 0; r < 4; ++r) {
       // bytes 3u .. 3u+2 of the 8-byte window (a 64-bit shift: lane 15's
       // bytes start 5 bytes in)
-      const uint64_t w64 = (static_cast<uint64_t>(vw[i][r][1]) << 32) | vw[i][r][0];
+      const uint32_t* wp = rec + (4 * grp + r) * kRecordWords + vdw;
+      const uint64_t w64 = (static_cast<uint64_t>(wp[1]) << 32) | wp[0];
       const uint32_t win = static_cast<uint32_t>(w64 >> vsh);
       vb[0][r] = lut[win & 63u];
       vb[1][r] = lut[__builtin_amdgcn_ubfe(win, 6, 6)];
@@ -365,6 +387,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   __shared__ float wave_ml[kWaves][2][kHeads];
   __shared__ uint32_t new_rec[2][kRecordWords];   // kAppend: the new key / value record
   __shared__ float new_scale[2];
+  __shared__ WaveStage stage[kWaves];
 
   const int tid = threadIdx.x;
   // the wave index as a scalar: every per-wave branch is then a scalar
@@ -470,12 +493,11 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   // the query and rotation loads go out before the cache loads: loads
   // complete in issue order, so waiting for them must not wait for the cache
   __builtin_amdgcn_sched_barrier(0);
-  uint32_t kw[NB][3];
-  uint32_t vw[NB][4][2];
-  f32x4_t ks[NB], vs[NB];
+  uint32_t kw[NB][3], vw[NB][3];
+  f32x4_t ksl, vsl;
+  load_wave<NB>(kc, kn, vc, vn, wbase, clamp16, lane, col, grp, kw, vw, ksl, vsl);
   const int vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
   const uint32_t vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));   // 0..40
-  load_wave<NB>(kc, kn, vc, vn, wbase, clamp16, col, grp, vdw, kw, vw, ks, vs);
 
   // ---- while the loads fly: LUT and the rotated query --------------------
   if (tid < 64) {
@@ -532,14 +554,18 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     qlo[kb] = *reinterpret_cast<const u32x4_t*>(&qop[1][col & 7][16 * grp + 4 * kb]);
   }
   const float qdown = ldexpf(1.0f, -qexp_s[col & 7]);
+  // this wave's scales to its LDS stage (read back per batch)
+  stage[wave].ks[lane] = ksl;
+  stage[wave].vs[lane] = vsl;
+  wave_lds_fence();
 
   float m_run = -INFINITY, l_run = 0.f, vmax = 0.f;
   f32x4_t o_acc[4];
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if (nvalid > 0)
-    attend_wave<NB>(kw, vw, ks, vs, qhi, qlo, lut64, col, grp, nvalid, vsh, qdown, m_run,
-                    l_run, vmax, o_acc);
+    attend_wave<NB>(kw, vw, stage[wave], qhi, qlo, lut64, col, grp, nvalid, vdw, vsh, qdown,
+                    m_run, l_run, vmax, o_acc);
 
   if (compressing) {
     // the two chains are independent and interleave
@@ -633,7 +659,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
 
 // Merge of the split partials of one (sequence b, query head h): one
 // 256-thread workgroup; thread (sg, dq) takes splits sg, sg + 8, ... and dims
-// 4 dq .. 4 dq + 3, with up to 16 splits' loads in flight per thread.  Then
+// 4 dq .. 4 dq + 3, with up to 8 splits' loads in flight per thread.  Then
 // o = sum_s c_s O_s / sum_s c_s l_s with c_s = 2^(m_s - max m), and the single
 // inverse rotation.  Splits with nothing to attend carry m = -inf (their
 // other entries are never read), so the merge needs no sequence length.
@@ -643,7 +669,7 @@ template <bool kAppend>
 __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     const float* __restrict__ partials, const float* __restrict__ quats, float* __restrict__ out,
     int n_kv_heads, int n_splits, int32_t* __restrict__ seq_lens, int64_t capacity) {
-  constexpr int kUnroll = 16;
+  constexpr int kUnroll = 8;   // 8 x 8 = 64 splits per pass, all loads in flight
   __shared__ __attribute__((aligned(16))) float red_o[8][kDim];
   __shared__ float red_m[8], red_l[8];
   const int tid = threadIdx.x;
@@ -665,15 +691,22 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
   f32x4_t O = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int s0 = sg; s0 < n_splits; s0 += 8 * kUnroll) {
     float mv[kUnroll], lv[kUnroll];
+    f32x2_t mlv[kUnroll];
     f32x4_t ov[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int s = s0 + 8 * u;
       const int sc = s < n_splits ? s : s0;
       const float* p = base + static_cast<int64_t>(sc) * (kHeads * kPart);
-      mv[u] = s < n_splits ? p[0] : -INFINITY;
-      lv[u] = p[1];
+      mlv[u] = *reinterpret_cast<const f32x2_t*>(p);   // (m, l)
       ov[u] = *reinterpret_cast<const f32x4_t*>(p + 2 + 4 * dq);
+    }
+    // every load of the pass is issued before the first use
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      mv[u] = s0 + 8 * u < n_splits ? mlv[u][0] : -INFINITY;
+      lv[u] = mlv[u][1];
     }
     float Mn = M;
 #pragma unroll
