@@ -62,6 +62,8 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kRotThreads = 256;          // (head, SO(4) block) tasks: waves 0..3
 constexpr int kMaxBatches = 5;            // 16-position batches per wave (register budget)
 constexpr int kMergeThreads = 256;
+constexpr int kRecStride = kRecordWords + 1;   // staged record stride (words): spreads banks
+constexpr int kQRowWords = kDim / 2 + 4;  // fp16-pair row of one head, padded (68 words)
 constexpr int kHeads = 8;                 // query heads per KV head
 constexpr int kPart = 2 + kDim;           // m, l, o[128] per head
 constexpr float kLog2e = 1.4426950408889634f;
@@ -182,13 +184,13 @@ __device__ __forceinline__ f32x4_t rotate_inverse(f32x4_t o, f32x4_t ql, f32x4_t
 // Codebook values of dims d..d+3 (d % 4 == 0) of a packed record held in
 // LDS (12 words): codes at bits 3d .. 3d+11, two 6-bit fields looked up in
 // the fp16 pair table.
-__device__ __forceinline__ f32x4_t decode_record_dims(const uint32_t* rec, const uint32_t* lut64,
+__device__ __forceinline__ f32x4_t decode_record_dims(const uint32_t* rec, const uint32_t* lut,
                                                       int d) {
   const int bit = 3 * d, w = bit >> 5, off = bit & 31;
   const uint32_t lo = rec[w];
   const uint32_t hi = w + 1 < kRecordWords ? rec[w + 1] : 0u;
   const uint32_t bits = __builtin_amdgcn_alignbit(hi, lo, off);
-  const uint32_t p0 = lut64[bits & 63u], p1 = lut64[(bits >> 6) & 63u];
+  const uint32_t p0 = lut[bits & 63u], p1 = lut[(bits >> 6) & 63u];
   return f32x4_t{static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p0))),
                  static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p0 >> 16))),
                  static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p1))),
@@ -200,7 +202,7 @@ __device__ __forceinline__ f32x4_t decode_record_dims(const uint32_t* rec, const
 struct WaveStage {
   f32x4_t ks[64];
   f32x4_t vs[64];
-  uint32_t rec[2][16 * kRecordWords];
+  uint32_t rec[2][16 * kRecStride];
 };
 
 // Issues every cache load of one wave, in the order the data is used and
@@ -254,14 +256,17 @@ __device__ __forceinline__ void load_wave(const uint8_t* kc, const float* kn, co
 
 // Scores, softmax and value accumulation of one wave over the batches that
 // hold its nvalid (> 0) positions; only the last of them can be partial.
+// kFull: exactly NBX full batches, straight-line code (the scheduler can
+// overlap batches); otherwise up to NBX batches with per-batch checks.
 // Scores are kept in the per-head scaled domain (x = acc * s^K, the query
 // operand carried 2^qexp); qdown = 2^-qexp turns them into log2 units inside
 // the exponent.  On return m_run is in log2 units.
-// Scale group g of batch i (positions 16 i + 4 g ..) is st.ks[4 i + g].  Each
+// Scale group g of batch i (positions 16 i + 4 g ..) is st.ks[4 i + g].
+// lut: this lane's copy of the pair table (entry e at lut[32 e]).  Each
 // batch's value records go through st.rec (lane (t, gk) writes its 12 bytes
 // of record t, lane (u, grp) reads the 8-byte window holding bytes 3u..3u+2
 // of records 4 grp + r); the wave's own LDS operations complete in order.
-template <int NB>
+template <int NB, int NBX, bool kFull>
 __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
                                             const uint32_t (&vw)[NB][3], WaveStage& st,
                                             const u32x4_t (&qhi)[4], const u32x4_t (&qlo)[4],
@@ -269,10 +274,10 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
                                             int vdw, uint32_t vsh, float qdown, float& m_run,
                                             float& l_run, float& vmax, f32x4_t (&o_acc)[4]) {
   // ---- phase 1: scores (Table 2 A) -----------------------------------------
-  f32x4_t sc[NB];
+  f32x4_t sc[NBX];
 #pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    if (16 * i >= nvalid) break;
+  for (int i = 0; i < NBX; ++i) {
+    if (!kFull && 16 * i >= nvalid) break;
     const uint32_t w0 = kw[i][0], w1 = kw[i][1], w2 = kw[i][2];
     u32x4_t a[4];
 #pragma unroll
@@ -282,15 +287,17 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
                       lut[slice_field(kb * 4 + 2, w0, w1, w2)],
                       lut[slice_field(kb * 4 + 3, w0, w1, w2)]};
     }
-    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // hi and lo query parts in two independent accumulation chains
+    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f}, acc_lo = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       acc = mfma(a[kb], qhi[kb], acc);
-      acc = mfma(a[kb], qlo[kb], acc);
+      acc_lo = mfma(a[kb], qlo[kb], acc_lo);
     }
+    acc += acc_lo;
     // lane (col, grp) holds positions 16 i + 4 grp + r of head col % 8
     f32x4_t x = acc * st.ks[4 * i + grp];
-    if (16 * i + 16 > nvalid) {
+    if (!kFull && 16 * i + 16 > nvalid) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) x[r] = (16 * i + 4 * grp + r < nvalid) ? x[r] : -INFINITY;
     }
@@ -298,12 +305,12 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
     m_run = fmaxf(fmaxf(m_run, fmaxf(x[0], x[1])), fmaxf(x[2], x[3]));
   }
   // largest value scale of the wave
-  f32x4_t vsv[NB];
+  f32x4_t vsv[NBX];
 #pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    if (16 * i >= nvalid) break;
+  for (int i = 0; i < NBX; ++i) {
+    if (!kFull && 16 * i >= nvalid) break;
     f32x4_t v = st.vs[4 * i + grp];
-    if (16 * i + 16 > nvalid) {
+    if (!kFull && 16 * i + 16 > nvalid) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) v[r] = (16 * i + 4 * grp + r < nvalid) ? v[r] : 0.f;
     }
@@ -320,13 +327,13 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
 
   // ---- phase 2: weights (Table 2 B) and values (Table 2 C) -----------------
 #pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    if (16 * i >= nvalid) break;
+  for (int i = 0; i < NBX; ++i) {
+    if (!kFull && 16 * i >= nvalid) break;
     uint32_t* rec = st.rec[i & 1];
     wave_lds_fence();   // reads of this buffer two batches ago come first
-    rec[col * kRecordWords + 3 * grp] = vw[i][0];
-    rec[col * kRecordWords + 3 * grp + 1] = vw[i][1];
-    rec[col * kRecordWords + 3 * grp + 2] = vw[i][2];
+    rec[col * kRecStride + 3 * grp] = vw[i][0];
+    rec[col * kRecStride + 3 * grp + 1] = vw[i][1];
+    rec[col * kRecStride + 3 * grp + 2] = vw[i][2];
     wave_lds_fence();
     const f32x4_t wv = vsv[i] * vinv;
     u32x4_t pw_hi, pw_lo;
@@ -345,7 +352,7 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
     for (int r = 0; r < 4; ++r) {
       // bytes 3u .. 3u+2 of the 8-byte window (a 64-bit shift: lane 15's
       // bytes start 5 bytes in)
-      const uint32_t* wp = rec + (4 * grp + r) * kRecordWords + vdw;
+      const uint32_t* wp = rec + (4 * grp + r) * kRecStride + vdw;
       const uint64_t w64 = (static_cast<uint64_t>(wp[1]) << 32) | wp[0];
       const uint32_t win = static_cast<uint32_t>(w64 >> vsh);
       vb[0][r] = lut[win & 63u];
@@ -379,15 +386,30 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     int n_kv_heads, int n_splits, int split_len, float qscale, Codebook cb,
     const void* __restrict__ k_new, const void* __restrict__ v_new, int new_f16,
     int32_t* __restrict__ status) {
-  constexpr int kQRow = kDim / 2 + 4;   // fp16-pair row of one head, padded (68 words)
-  __shared__ uint32_t lut64[64];
-  __shared__ __attribute__((aligned(16))) uint32_t qop[2][kHeads][kQRow];
-  __shared__ int qexp_s[kHeads];
-  __shared__ __attribute__((aligned(16))) float wave_o[kWaves][kHeads * kDim];
-  __shared__ float wave_ml[kWaves][2][kHeads];
-  __shared__ uint32_t new_rec[2][kRecordWords];   // kAppend: the new key / value record
-  __shared__ float new_scale[2];
-  __shared__ WaveStage stage[kWaves];
+  // All LDS of the kernel in one object, the pair table first (address 0:
+  // a lookup address is just field * 4).
+  struct Smem {
+    uint32_t lut[64];   // fp16 pair table: entry f = (C[f % 8], C[f / 8])
+    uint32_t qop[2][kHeads][kQRowWords];
+    int qexp[kHeads];
+    float wave_ml[kWaves][2][kHeads];
+    uint32_t new_rec[2][kRecordWords];   // kAppend: the new key / value record
+    float new_scale[2];
+    // the waves' staging areas while attending, their outputs afterwards
+    union {
+      WaveStage stage[kWaves];
+      float wave_o[kWaves][kHeads * kDim];
+    };
+  };
+  __shared__ __attribute__((aligned(16))) Smem sm;
+  uint32_t* lut = sm.lut;
+  uint32_t(*qop)[kHeads][kQRowWords] = sm.qop;
+  int* qexp_s = sm.qexp;
+  float(*wave_ml)[2][kHeads] = sm.wave_ml;
+  uint32_t(*new_rec)[kRecordWords] = sm.new_rec;
+  float* new_scale = sm.new_scale;
+  WaveStage* stage = sm.stage;
+  float(*wave_o)[kHeads * kDim] = sm.wave_o;
 
   const int tid = threadIdx.x;
   // the wave index as a scalar: every per-wave branch is then a scalar
@@ -505,7 +527,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
         __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & 7)));
     const uint32_t hi =
         __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> 3)));
-    lut64[tid] = lo | (hi << 16);
+    lut[tid] = lo | (hi << 16);
   }
   // the 32 blocks of a head are 32 consecutive lanes of one wave, so the
   // rotation needs no barrier
@@ -544,7 +566,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     qop[1][qh][2 * qblk + 1] = lw[1];
     if (qblk == 0) qexp_s[qh] = qexp;
   }
-  lds_barrier();   // lut64, qop, qexp_s
+  lds_barrier();   // lut, qop, qexp_s
   // QK B operands: column col -> head col % 8; MFMA kb, lane group grp ->
   // dims 32 grp + 8 kb + 0..7 (fp16 pair words 16 grp + 4 kb .. +3)
   u32x4_t qhi[4], qlo[4];
@@ -563,9 +585,16 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   f32x4_t o_acc[4];
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  if (nvalid > 0)
-    attend_wave<NB>(kw, vw, stage[wave], qhi, qlo, lut64, col, grp, nvalid, vdw, vsh, qdown,
-                    m_run, l_run, vmax, o_acc);
+  if (nvalid == 16 * NB)
+    attend_wave<NB, NB, true>(kw, vw, stage[wave], qhi, qlo, lut, col, grp, nvalid, vdw, vsh,
+                              qdown, m_run, l_run, vmax, o_acc);
+  else if (NB > 1 && nvalid == 16 * (NB - 1))
+    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true>(kw, vw, stage[wave], qhi, qlo, lut, col, grp,
+                                                nvalid, vdw, vsh, qdown, m_run, l_run, vmax,
+                                                o_acc);
+  else if (nvalid > 0)
+    attend_wave<NB, NB, false>(kw, vw, stage[wave], qhi, qlo, lut, col, grp, nvalid, vdw, vsh,
+                               qdown, m_run, l_run, vmax, o_acc);
 
   if (compressing) {
     // the two chains are independent and interleave
@@ -587,6 +616,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   }
 
   // ---- merge the 8 waves in LDS ---------------------------------------------
+  lds_barrier();   // every wave is done with its staging area
   // lane (u = col, grp) holds rows 4 grp + r = (head (4 grp + r) % 8, slot
   // grp / 2) of MFMA nb, i.e. dim 2 (4 u + nb) + slot.
   const float oscale = vmax * (1.0f / 32768.0f);
@@ -616,8 +646,8 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     // score of the appended key: s^K (q_tilde . C[code]) over this thread's
     // 4 dims (codes of dims md..md+3 = bits 3 md .. 3 md + 11 of the record),
     // summed over the head's 32 lanes; y already carries the score scale
-    const f32x4_t k4 = decode_record_dims(new_rec[0], lut64, md);
-    v_new4 = decode_record_dims(new_rec[1], lut64, md);
+    const f32x4_t k4 = decode_record_dims(new_rec[0], lut, md);
+    v_new4 = decode_record_dims(new_rec[1], lut, md);
     float dot = y[0] * k4[0] + y[1] * k4[1] + y[2] * k4[2] + y[3] * k4[3];
     dot += xor_lane<1>(dot);
     dot += xor_lane<2>(dot);
