@@ -205,10 +205,10 @@ struct WaveStage {
   uint32_t rec[2][16 * kRecStride];
 };
 
-// Issues every cache load of one wave, in the order the data is used and
-// before any arithmetic: both scale arrays (one 16-byte load per lane: lane
-// j takes positions 4j .. 4j+3 of the wave), then per batch of 16 positions
-// the keys, then the values.  Keys and values are loaded the same way: lane
+// Cache loads of one wave, in the order the data is used: both scale arrays
+// (one 16-byte load per lane: lane j takes positions 4j .. 4j+3 of the
+// wave), then per batch of 16 positions the keys (load_keys), and later the
+// values (load_values).  Keys and values are loaded the same way: lane
 // (t = col, gk = grp) takes dwords 3gk .. 3gk+2 of position t, one coalesced
 // 768-byte load per batch.
 // Batch starts are multiples of 16 and the capacity is a multiple of 16, so a
@@ -219,10 +219,9 @@ struct WaveStage {
 // straight-line sequence for every wave, so the compiler keeps exact counts
 // of the loads in flight.
 template <int NB>
-__device__ __forceinline__ void load_wave(const uint8_t* kc, const float* kn, const uint8_t* vc,
-                                          const float* vn, int wbase, int clamp16, int lane,
-                                          int col, int grp, uint32_t (&kw)[NB][3],
-                                          uint32_t (&vw)[NB][3], f32x4_t& ksl, f32x4_t& vsl) {
+__device__ __forceinline__ void load_keys(const uint8_t* kc, const float* kn, const float* vn,
+                                          int wbase, int clamp16, int lane, int col, int grp,
+                                          uint32_t (&kw)[NB][3], f32x4_t& ksl, f32x4_t& vsl) {
   const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
   // scales: lane j -> batch j / 4 (clamped like the batches), group j % 4
   {
@@ -231,27 +230,34 @@ __device__ __forceinline__ void load_wave(const uint8_t* kc, const float* kn, co
     ksl = *reinterpret_cast<const f32x4_t*>(kn + tj);
     vsl = *reinterpret_cast<const f32x4_t*>(vn + tj);
   }
-  int tb[NB];
-#pragma unroll
-  for (int i = 0; i < NB; ++i) tb[i] = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
+    const int tb = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
     const uint32_t* p =
-        reinterpret_cast<const uint32_t*>(kc + static_cast<uint32_t>(tb[i] * kRecordBytes) + koff);
+        reinterpret_cast<const uint32_t*>(kc + static_cast<uint32_t>(tb * kRecordBytes) + koff);
     kw[i][0] = p[0];
     kw[i][1] = p[1];
     kw[i][2] = p[2];
   }
   __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int NB>
+__device__ __forceinline__ void load_values(const uint8_t* vc, int wbase, int clamp16, int col,
+                                            int grp, uint32_t (&vw)[NB][3]) {
+  const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
+    const int tb = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
     const uint32_t* p =
-        reinterpret_cast<const uint32_t*>(vc + static_cast<uint32_t>(tb[i] * kRecordBytes) + koff);
+        reinterpret_cast<const uint32_t*>(vc + static_cast<uint32_t>(tb * kRecordBytes) + koff);
     vw[i][0] = p[0];
     vw[i][1] = p[1];
     vw[i][2] = p[2];
   }
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 // Scores, softmax and value accumulation of one wave over the batches that
@@ -396,9 +402,11 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     uint32_t new_rec[2][kRecordWords];   // kAppend: the new key / value record
     float new_scale[2];
     // the waves' staging areas while attending, their outputs afterwards
+    // (wave_o[w][r][lane] = the lane's accumulator entries r of the four
+    // PV products, as written by the matrix cores)
     union {
       WaveStage stage[kWaves];
-      float wave_o[kWaves][kHeads * kDim];
+      f32x4_t wave_o[kWaves][4][64];
     };
   };
   __shared__ __attribute__((aligned(16))) Smem sm;
@@ -409,7 +417,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   uint32_t(*new_rec)[kRecordWords] = sm.new_rec;
   float* new_scale = sm.new_scale;
   WaveStage* stage = sm.stage;
-  float(*wave_o)[kHeads * kDim] = sm.wave_o;
+  f32x4_t(*wave_o)[4][64] = sm.wave_o;
 
   const int tid = threadIdx.x;
   // the wave index as a scalar: every per-wave branch is then a scalar
@@ -517,7 +525,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   __builtin_amdgcn_sched_barrier(0);
   uint32_t kw[NB][3], vw[NB][3];
   f32x4_t ksl, vsl;
-  load_wave<NB>(kc, kn, vc, vn, wbase, clamp16, lane, col, grp, kw, vw, ksl, vsl);
+  load_keys<NB>(kc, kn, vn, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
   const int vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
   const uint32_t vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));   // 0..40
 
@@ -567,6 +575,9 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     if (qblk == 0) qexp_s[qh] = qexp;
   }
   lds_barrier();   // lut, qop, qexp_s
+  // the values go out after the barrier: a wave reaches it once its keys are
+  // issued, and the values stream in while the scores are computed
+  load_values<NB>(vc, wbase, clamp16, col, grp, vw);
   // QK B operands: column col -> head col % 8; MFMA kb, lane group grp ->
   // dims 32 grp + 8 kb + 0..7 (fp16 pair words 16 grp + 4 kb .. +3)
   u32x4_t qhi[4], qlo[4];
@@ -618,15 +629,12 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   // ---- merge the 8 waves in LDS ---------------------------------------------
   lds_barrier();   // every wave is done with its staging area
   // lane (u = col, grp) holds rows 4 grp + r = (head (4 grp + r) % 8, slot
-  // grp / 2) of MFMA nb, i.e. dim 2 (4 u + nb) + slot.
+  // grp / 2) of MFMA nb, i.e. dim 8 u + 2 nb + slot; stored as one 16-byte
+  // vector per (r, lane) over nb (consecutive lanes: no bank conflicts)
   const float oscale = vmax * (1.0f / 32768.0f);
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int h = (4 * grp + r) & 7, sl = grp >> 1;
-      wave_o[wave][h * kDim + 8 * col + 2 * nb + sl] = o_acc[nb][r] * oscale;
-    }
+  for (int r = 0; r < 4; ++r)
+    wave_o[wave][r][lane] = f32x4_t{o_acc[0][r], o_acc[1][r], o_acc[2][r], o_acc[3][r]} * oscale;
   if (lane < kHeads) {
     wave_ml[wave][0][lane] = m_run;     // lanes 0..7 hold heads 0..7
     wave_ml[wave][1][lane] = l_run;
@@ -657,6 +665,10 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     s_new = dot * new_scale[0];
     M = fmaxf(M, s_new);
   }
+  // dims md + j, j = 0..3: column u = md / 8, MFMA nb = (md % 8) / 2 + j / 2,
+  // slot j % 2, row r = mh % 4 of lane u + 16 grp with grp = (mh / 4) % 2 +
+  // 2 slot; entries (nb, nb + 1) of a lane are one aligned 8-byte pair
+  const int o_r = mh & 3, o_lane = (md >> 3) + 16 * ((mh >> 2) & 1), o_nb = (md & 7) >> 1;
   float L = 0.f;
   f32x4_t O = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -664,7 +676,11 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     const float mw = wave_ml[w][0][mh];
     const float c = (mw == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mw - M);
     L += c * wave_ml[w][1][mh];
-    O += c * *reinterpret_cast<const f32x4_t*>(wave_o[w] + mh * kDim + md);
+    const f32x2_t s0 = *reinterpret_cast<const f32x2_t*>(   // slot 0
+        reinterpret_cast<const float*>(&wave_o[w][o_r][o_lane]) + o_nb);
+    const f32x2_t s1 = *reinterpret_cast<const f32x2_t*>(   // slot 1
+        reinterpret_cast<const float*>(&wave_o[w][o_r][o_lane + 32]) + o_nb);
+    O += c * f32x4_t{s0[0], s1[0], s0[1], s1[1]};
   }
   if (new_attended) {
     const float c = __builtin_amdgcn_exp2f(s_new - M);
