@@ -432,6 +432,20 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   const int b = bg / n_kv_heads;
   const int n_q_heads = n_kv_heads * kHeads;
 
+  // The query and rotation loads go out first: they do not depend on the
+  // sequence length, so they are issued while it is read, and loads complete
+  // in issue order, so waiting for them never waits for the cache loads.
+  // Thread (head qh, SO(4) block qblk) for tid < 256; the other waves load
+  // the same query and parameters (no branch around loads).
+  const int qh = (tid >> 5) & 7, qblk = tid & 31;
+  const f32x4_t qv = *reinterpret_cast<const f32x4_t*>(
+      q + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * kHeads + qh) * kDim +
+      4 * qblk);
+  const f32x4_t* qpar = reinterpret_cast<const f32x4_t*>(
+      quats + static_cast<int64_t>(g) * kQuatFloats + 8 * qblk);
+  const f32x4_t ql = qpar[0], qr = qpar[1];
+  __builtin_amdgcn_sched_barrier(0);
+
   const int seq0 = seq_lens[b];
   int seq = seq0;
   bool appended = false;   // kAppend: the new token goes to position seq0
@@ -491,17 +505,24 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   // positions of the split, compresses the new key and value after its own
   // positions (they are needed only in the workgroup merge)
   constexpr int kCompressWave = kWaves - 1;
-  float nk0 = 0.f, nk1 = 0.f, nv0 = 0.f, nv1 = 0.f;
+  // the new key and value stay raw (dims 2 lane, 2 lane + 1: one fp16 pair
+  // word, or two fp32 words) until they are compressed, so that no wait for
+  // them is placed before the cache loads
+  uint32_t nkr[2] = {0u, 0u}, nvr[2] = {0u, 0u};
   float nqp[8];
   const bool compressing = writer && wave == kCompressWave;
   if (compressing) {
     const int64_t off = (static_cast<int64_t>(b) * n_kv_heads + g) * kDim;
     if (new_f16) {
-      load_pair(static_cast<const __half*>(k_new) + off, lane, nk0, nk1);
-      load_pair(static_cast<const __half*>(v_new) + off, lane, nv0, nv1);
+      nkr[0] = reinterpret_cast<const uint32_t*>(static_cast<const __half*>(k_new) + off)[lane];
+      nvr[0] = reinterpret_cast<const uint32_t*>(static_cast<const __half*>(v_new) + off)[lane];
     } else {
-      load_pair(static_cast<const float*>(k_new) + off, lane, nk0, nk1);
-      load_pair(static_cast<const float*>(v_new) + off, lane, nv0, nv1);
+      const u32x2_a4_t kr =
+          reinterpret_cast<const u32x2_a4_t*>(static_cast<const float*>(k_new) + off)[lane];
+      const u32x2_a4_t vr =
+          reinterpret_cast<const u32x2_a4_t*>(static_cast<const float*>(v_new) + off)[lane];
+      nkr[0] = kr[0]; nkr[1] = kr[1];
+      nvr[0] = vr[0]; nvr[1] = vr[1];
     }
     const f32x4_t* qs = reinterpret_cast<const f32x4_t*>(
         quats + static_cast<int64_t>(g) * kQuatFloats + 8 * (lane >> 1));
@@ -510,19 +531,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     nqp[4] = p1[0]; nqp[5] = p1[1]; nqp[6] = p1[2]; nqp[7] = p1[3];
   }
 
-  // ---- issue every load of the wave -------------------------------------
-  // thread (head qh, SO(4) block qblk) for tid < 256; the other waves load
-  // the same query and parameters (no branch around loads)
-  const int qh = (tid >> 5) & 7, qblk = tid & 31;
-  const f32x4_t qv = *reinterpret_cast<const f32x4_t*>(
-      q + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * kHeads + qh) * kDim +
-      4 * qblk);
-  const f32x4_t* qpar = reinterpret_cast<const f32x4_t*>(
-      quats + static_cast<int64_t>(g) * kQuatFloats + 8 * qblk);
-  const f32x4_t ql = qpar[0], qr = qpar[1];
-  // the query and rotation loads go out before the cache loads: loads
-  // complete in issue order, so waiting for them must not wait for the cache
-  __builtin_amdgcn_sched_barrier(0);
+  // ---- the cache loads (keys now, values after the barrier below) ----------
   uint32_t kw[NB][3], vw[NB][3];
   f32x4_t ksl, vsl;
   load_keys<NB>(kc, kn, vn, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
@@ -608,6 +617,18 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
                                qdown, m_run, l_run, vmax, o_acc);
 
   if (compressing) {
+    float nk0, nk1, nv0, nv1;
+    if (new_f16) {
+      nk0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(nkr[0])));
+      nk1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(nkr[0] >> 16)));
+      nv0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(nvr[0])));
+      nv1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(nvr[0] >> 16)));
+    } else {
+      nk0 = __builtin_bit_cast(float, nkr[0]);
+      nk1 = __builtin_bit_cast(float, nkr[1]);
+      nv0 = __builtin_bit_cast(float, nvr[0]);
+      nv1 = __builtin_bit_cast(float, nvr[1]);
+    }
     // the two chains are independent and interleave
     const float* qp0 = nqp;
     const WaveCode wk = compress_vector_wave(nk0, nk1, qp0, cb, lane);
