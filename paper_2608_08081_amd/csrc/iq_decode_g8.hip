@@ -15,9 +15,10 @@
 // products and run on the matrix cores (v_mfma_f32_16x16x32_f16):
 //
 //  QK (Table 2 A): S[t][n] = sum_k Khat[t][k] Qt[k][n], rows t = 16 positions,
-//    columns n = 16 = the group's 8 heads twice, k = 32 dims per instruction.
-//    The fp32 rotated query is split into fp16 hi + lo parts and both are
-//    multiplied into the same accumulator, so the scores carry ~22 bits.
+//    columns n = 16, k = 32 dims per instruction.  The fp32 rotated query is
+//    split into fp16 hi + lo parts: columns 0..7 hold the 8 heads' hi parts,
+//    columns 8..15 their lo parts, and lanes n and n ^ 8 add their products,
+//    so the scores carry ~22 bits.
 //    A lane (t, gk) supplies 8 dims 32gk+8kb..+7 of position t, i.e. 4
 //    consecutive 6-bit fields (2 codes each) of its 12-byte slice of the
 //    record; each field indexes a 64-entry LDS table holding the pair of
@@ -198,11 +199,11 @@ __device__ __forceinline__ f32x4_t decode_record_dims(const uint32_t* rec, const
 }
 
 // Per-wave LDS staging: the two scale arrays of the wave (a 16-byte group
-// per lane, 64 groups) and a double buffer of one batch of value records.
+// per lane, 64 groups) and the value records of all its batches.
 struct WaveStage {
   f32x4_t ks[64];
   f32x4_t vs[64];
-  uint32_t rec[2][16 * kRecStride];
+  uint32_t rec[kMaxBatches][16 * kRecStride];
 };
 
 // Cache loads of one wave, in the order the data is used: both scale arrays
@@ -268,14 +269,14 @@ __device__ __forceinline__ void load_values(const uint8_t* vc, int wbase, int cl
 // operand carried 2^qexp); qdown = 2^-qexp turns them into log2 units inside
 // the exponent.  On return m_run is in log2 units.
 // Scale group g of batch i (positions 16 i + 4 g ..) is st.ks[4 i + g].
-// lut: this lane's copy of the pair table (entry e at lut[32 e]).  Each
-// batch's value records go through st.rec (lane (t, gk) writes its 12 bytes
-// of record t, lane (u, grp) reads the 8-byte window holding bytes 3u..3u+2
-// of records 4 grp + r); the wave's own LDS operations complete in order.
+// lut: the pair table.  Each batch's value records go through st.rec[i]
+// (lane (t, gk) writes its 12 bytes of record t, lane (u, grp) reads the
+// 8-byte window holding bytes 3u..3u+2 of records 4 grp + r); the wave's own
+// LDS operations complete in order.
 template <int NB, int NBX, bool kFull>
 __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
                                             const uint32_t (&vw)[NB][3], WaveStage& st,
-                                            const u32x4_t (&qhi)[4], const u32x4_t (&qlo)[4],
+                                            const u32x4_t (&qb)[4],
                                             const uint32_t* lut, int col, int grp, int nvalid,
                                             int vdw, uint32_t vsh, float qdown, float& m_run,
                                             float& l_run, float& vmax, f32x4_t (&o_acc)[4]) {
@@ -293,14 +294,13 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
                       lut[slice_field(kb * 4 + 2, w0, w1, w2)],
                       lut[slice_field(kb * 4 + 3, w0, w1, w2)]};
     }
-    // hi and lo query parts in two independent accumulation chains
-    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f}, acc_lo = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      acc = mfma(a[kb], qhi[kb], acc);
-      acc_lo = mfma(a[kb], qlo[kb], acc_lo);
-    }
-    acc += acc_lo;
+    for (int kb = 0; kb < 4; ++kb) acc = mfma(a[kb], qb[kb], acc);
+    // column col holds the hi (col < 8) or lo (col >= 8) product of head
+    // col % 8: both lanes of the pair get the sum
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r] += xor_lane<8>(acc[r]);
     // lane (col, grp) holds positions 16 i + 4 grp + r of head col % 8
     f32x4_t x = acc * st.ks[4 * i + grp];
     if (!kFull && 16 * i + 16 > nvalid) {
@@ -332,15 +332,20 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
   const float mq = -m_run * qdown;
 
   // ---- phase 2: weights (Table 2 B) and values (Table 2 C) -----------------
+  // every batch's value records go to their own staging rows first, so the
+  // reads of all batches may be scheduled freely after one fence
 #pragma unroll
   for (int i = 0; i < NBX; ++i) {
     if (!kFull && 16 * i >= nvalid) break;
-    uint32_t* rec = st.rec[i & 1];
-    wave_lds_fence();   // reads of this buffer two batches ago come first
-    rec[col * kRecStride + 3 * grp] = vw[i][0];
-    rec[col * kRecStride + 3 * grp + 1] = vw[i][1];
-    rec[col * kRecStride + 3 * grp + 2] = vw[i][2];
-    wave_lds_fence();
+    st.rec[i][col * kRecStride + 3 * grp] = vw[i][0];
+    st.rec[i][col * kRecStride + 3 * grp + 1] = vw[i][1];
+    st.rec[i][col * kRecStride + 3 * grp + 2] = vw[i][2];
+  }
+  wave_lds_fence();
+#pragma unroll
+  for (int i = 0; i < NBX; ++i) {
+    if (!kFull && 16 * i >= nvalid) break;
+    const uint32_t* rec = st.rec[i];
     const f32x4_t wv = vsv[i] * vinv;
     u32x4_t pw_hi, pw_lo;
 #pragma unroll
@@ -587,14 +592,13 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   // the values go out after the barrier: a wave reaches it once its keys are
   // issued, and the values stream in while the scores are computed
   load_values<NB>(vc, wbase, clamp16, col, grp, vw);
-  // QK B operands: column col -> head col % 8; MFMA kb, lane group grp ->
-  // dims 32 grp + 8 kb + 0..7 (fp16 pair words 16 grp + 4 kb .. +3)
-  u32x4_t qhi[4], qlo[4];
+  // QK B operands: column col -> head col % 8, hi part for col < 8, lo part
+  // for col >= 8; MFMA kb, lane group grp -> dims 32 grp + 8 kb + 0..7 (fp16
+  // pair words 16 grp + 4 kb .. +3)
+  u32x4_t qb[4];
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
-    qhi[kb] = *reinterpret_cast<const u32x4_t*>(&qop[0][col & 7][16 * grp + 4 * kb]);
-    qlo[kb] = *reinterpret_cast<const u32x4_t*>(&qop[1][col & 7][16 * grp + 4 * kb]);
-  }
+  for (int kb = 0; kb < 4; ++kb)
+    qb[kb] = *reinterpret_cast<const u32x4_t*>(&qop[col >> 3][col & 7][16 * grp + 4 * kb]);
   const float qdown = ldexpf(1.0f, -qexp_s[col & 7]);
   // this wave's scales to its LDS stage (read back per batch)
   stage[wave].ks[lane] = ksl;
@@ -606,14 +610,14 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if (nvalid == 16 * NB)
-    attend_wave<NB, NB, true>(kw, vw, stage[wave], qhi, qlo, lut, col, grp, nvalid, vdw, vsh,
+    attend_wave<NB, NB, true>(kw, vw, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
                               qdown, m_run, l_run, vmax, o_acc);
   else if (NB > 1 && nvalid == 16 * (NB - 1))
-    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true>(kw, vw, stage[wave], qhi, qlo, lut, col, grp,
+    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true>(kw, vw, stage[wave], qb, lut, col, grp,
                                                 nvalid, vdw, vsh, qdown, m_run, l_run, vmax,
                                                 o_acc);
   else if (nvalid > 0)
-    attend_wave<NB, NB, false>(kw, vw, stage[wave], qhi, qlo, lut, col, grp, nvalid, vdw, vsh,
+    attend_wave<NB, NB, false>(kw, vw, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
                                qdown, m_run, l_run, vmax, o_acc);
 
   if (compressing) {

@@ -101,6 +101,9 @@ __device__ __forceinline__ float xor_lane(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false));
   } else if constexpr (kM == 2) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false));
+  } else if constexpr (kM == 8) {
+    // rotation by 8 inside each row of 16 lanes (row_ror:8) is xor 8
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0x128, 0xF, 0xF, false));
   } else {
     return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(x, (kM << 10) | 0x1F));
   }
