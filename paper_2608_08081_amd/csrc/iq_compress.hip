@@ -1,11 +1,10 @@
 // IsoQuant compression kernels (Algorithm 1; Sec. 3.2 Steps 1-4) for gfx950.
 //
-// One lane compresses one 128-dim vector entirely in registers: there is no
-// cross-lane traffic at all, the 128 values, the fp64 norm accumulators and
-// the 12-word output record all live in VGPRs.  A workgroup is a single
-// wave whose 64 lanes take 64 consecutive tokens of one (K|V, sequence,
-// KV head), so the rotation parameters are wave-uniform and are fetched
-// with scalar loads.
+// Bulk compression: one lane compresses one 128-dim vector entirely in
+// registers, with no cross-lane traffic.  A workgroup (4 waves) takes 256
+// consecutive tokens of one (K|V, sequence, KV head); it first builds the
+// head's 32 block matrices M_i H_4 in LDS (2 KB), which every lane then reads
+// as wave-uniform 16-byte rows (LDS broadcasts).
 //
 // Per vector:
 //   s^2  = sum x_i^2 in fp64 (products of fp16/fp32 inputs are exact in fp64),
@@ -13,8 +12,14 @@
 //   y    = diag(M_i H_4) (H_32 (x) I_4) x   unnormalized, fp32  (Step 2);
 //   code = #{j : y >= t_j * s * sqrt(128)}  (Step 3; comparing the
 //          unnormalized y against scaled thresholds is the same test as
-//          comparing R x / s against t_j, and saves 128 multiplies);
+//          comparing R x / s against t_j, and saves 128 multiplies).  The
+//          codebook is symmetric (t_{6-j} = -t_j, t_3 = 0), so the code is
+//          4 + m for y >= 0 and 3 - m = (4 + m) ^ 7 for y < 0, where
+//          m = #{k = 1..3 : |y| >= T_k} comes from a two-step search; the
+//          two rules differ only when |y| equals a threshold exactly;
 //   pack = 3-bit codes into 12 words, stored as three 16-byte writes (Step 4).
+// A vector whose s^2 is not finite (NaN or infinite input) gets the record of
+// all-NaN coordinates, code 0 everywhere, as #{j : t_j <= NaN} = 0.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -23,6 +28,10 @@
 
 namespace iq {
 namespace {
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kCompressThreads = 256;   // tokens per workgroup
 
 __device__ __forceinline__ void load_vector(const __half* src, float (&x)[kDim]) {
   const uint4* p = reinterpret_cast<const uint4*>(src);
@@ -50,13 +59,41 @@ __device__ __forceinline__ void load_vector(const float* src, float (&x)[kDim]) 
   }
 }
 
+// Code of y against the scaled positive thresholds T1 < T2 < T3 of a
+// symmetric codebook (see the file comment), already shifted to bit `off`
+// of its record word: ((4 + m) ^ (y < 0 ? 7 : 0)) << off, built from three
+// selects of shifted constants.
+__device__ __forceinline__ uint32_t quantize_sym(float y, float t1, float t2, float t3, int off) {
+  const float a = fabsf(y);
+  const bool b1 = a >= t2;
+  const bool b0 = a >= (b1 ? t3 : t1);
+  const uint32_t hi = b1 ? (6u << off) : (4u << off);
+  const uint32_t lo = b0 ? (1u << off) : 0u;
+  const uint32_t flip = y >= 0.f ? 0u : (7u << off);
+  return (hi | lo) ^ flip;
+}
+
+// OR the code of coordinate i (bits 3i .. 3i+2 of the record) into w.
+__device__ __forceinline__ void put_code_sym(uint32_t (&w)[kRecordWords], int i, float y,
+                                             float t1, float t2, float t3) {
+  const int bit = 3 * i;
+  const int word = bit >> 5, off = bit & 31;
+  if (off <= 29) {
+    w[word] |= quantize_sym(y, t1, t2, t3, off);
+  } else {
+    const uint32_t c = quantize_sym(y, t1, t2, t3, 0);
+    w[word] |= c << off;
+    w[word + 1] |= c >> (32 - off);
+  }
+}
+
 // Compress one vector (Algorithm 1) and write its record and scale.
+// mtab: rows of the head's block matrices M_i H_4 (row r of block i at
+// mtab[4 i + r]).
 template <typename T>
-__device__ __forceinline__ void compress_one(const T* __restrict__ src,
-                                             const float* __restrict__ quats_head,
+__device__ __forceinline__ void compress_one(const T* __restrict__ src, const f32x4_t* mtab,
                                              uint8_t* __restrict__ dst_code,
-                                             float* __restrict__ dst_norm,
-                                             const Codebook& cb) {
+                                             float* __restrict__ dst_norm, const Codebook& cb) {
   float x[kDim];
   load_vector(src, x);
 
@@ -71,18 +108,17 @@ __device__ __forceinline__ void compress_one(const T* __restrict__ src,
   }
   const double ss = (a0 + a1) + (a2 + a3);
   const double s = sqrt(ss);
+  const bool finite = ss < static_cast<double>(INFINITY);
 
-  // Thresholds in the unnormalized domain: t_j * s * sqrt(128).  A zero
-  // vector keeps the plain thresholds, so its all-zero y maps to code 4.
-  float thr[7];
-  if (ss > 0.0) {
-    const double sc = s * 11.313708498984760390;  // sqrt(128)
-#pragma unroll
-    for (int j = 0; j < 7; ++j) thr[j] = static_cast<float>(static_cast<double>(cb.thr[j]) * sc);
-  } else {
-#pragma unroll
-    for (int j = 0; j < 7; ++j) thr[j] = cb.thr[j];
-  }
+  // Positive thresholds in the unnormalized domain: t_j * s * sqrt(128).  A
+  // zero vector keeps the plain thresholds, so its all-zero y maps to code 4.
+  const double sc = ss > 0.0 ? s * 11.313708498984760390 : 1.0;   // sqrt(128)
+  float t1 = static_cast<float>(static_cast<double>(cb.thr[4]) * sc);
+  float t2 = static_cast<float>(static_cast<double>(cb.thr[5]) * sc);
+  float t3 = static_cast<float>(static_cast<double>(cb.thr[6]) * sc);
+  // opaque from here on: otherwise the select between t1 and t3 below is
+  // pushed above the fp64 scaling, which then runs once per coordinate
+  asm volatile("" : "+v"(t1), "+v"(t2), "+v"(t3));
 
   // Step 2a: Walsh-Hadamard butterflies on index bits 2..6 (H_32 (x) I_4).
 #pragma unroll
@@ -103,14 +139,17 @@ __device__ __forceinline__ void compress_one(const T* __restrict__ src,
   for (int i = 0; i < kRecordWords; ++i) w[i] = 0u;
 #pragma unroll
   for (int blk = 0; blk < kNumBlocks; ++blk) {
-    float m[4][4];
-    so4_matrix_h4(quats_head + 8 * blk, m);
     const float z0 = x[4 * blk], z1 = x[4 * blk + 1], z2 = x[4 * blk + 2], z3 = x[4 * blk + 3];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float y = m[r][0] * z0 + m[r][1] * z1 + m[r][2] * z2 + m[r][3] * z3;
-      put_code(w, 4 * blk + r, quantize3(y, thr));
+      const f32x4_t m = mtab[4 * blk + r];
+      const float y = m[0] * z0 + m[1] * z1 + m[2] * z2 + m[3] * z3;
+      put_code_sym(w, 4 * blk + r, y, t1, t2, t3);
     }
+  }
+  if (!finite) {
+#pragma unroll
+    for (int i = 0; i < kRecordWords; ++i) w[i] = 0u;
   }
 
   uint4* out = reinterpret_cast<uint4*>(dst_code);
@@ -120,28 +159,42 @@ __device__ __forceinline__ void compress_one(const T* __restrict__ src,
   *dst_norm = static_cast<float>(s);
 }
 
-// Bulk compression.  1-D grid of single-wave workgroups:
-//   blockIdx.x = (which * (B*H) + bh) * chunks + chunk,  lane = token in chunk.
+// Bulk compression.  1-D grid of 256-thread workgroups:
+//   blockIdx.x = (which * (B*H) + bh) * chunks + chunk,  thread = token in chunk.
 template <typename T>
-__global__ __launch_bounds__(64) void compress_kernel(
+__global__ __launch_bounds__(kCompressThreads) void compress_kernel(
     const T* __restrict__ src0, const T* __restrict__ src1, const float* __restrict__ quats,
     uint8_t* __restrict__ codes0, float* __restrict__ norms0, uint8_t* __restrict__ codes1,
     float* __restrict__ norms1, int n_heads, int64_t n_bh, int64_t n_tokens, int64_t chunks,
     int64_t capacity, int64_t dst_offset, Codebook cb) {
+  __shared__ f32x4_t mtab[kNumBlocks * 4];
   const int64_t blk = blockIdx.x;
   const int64_t chunk = blk % chunks;
   const int64_t rest = blk / chunks;
   const int64_t bh = rest % n_bh;
   const int which = static_cast<int>(rest / n_bh);
   const int h = static_cast<int>(bh % n_heads);
-  const int64_t t = chunk * 64 + threadIdx.x;
+  const int tid = threadIdx.x;
+  // rows of M_i H_4: thread tid < 128 builds row tid % 4 of block tid / 4
+  if (tid < kNumBlocks * 4) {
+    float m[4][4];
+    so4_matrix_h4(quats + static_cast<int64_t>(h) * kQuatFloats + 8 * (tid >> 2), m);
+    const int r = tid & 3;
+    f32x4_t row = f32x4_t{m[0][0], m[0][1], m[0][2], m[0][3]};
+#pragma unroll
+    for (int i = 1; i < 4; ++i)
+      if (r == i) row = f32x4_t{m[i][0], m[i][1], m[i][2], m[i][3]};
+    mtab[tid] = row;
+  }
+  __syncthreads();
+  const int64_t t = chunk * kCompressThreads + tid;
   if (t >= n_tokens) return;
   const T* src = which ? src1 : src0;
   uint8_t* codes = which ? codes1 : codes0;
   float* norms = which ? norms1 : norms0;
   const int64_t pos = bh * capacity + dst_offset + t;
-  compress_one<T>(src + (bh * n_tokens + t) * kDim, quats + h * kQuatFloats,
-                  codes + pos * kRecordBytes, norms + pos, cb);
+  compress_one<T>(src + (bh * n_tokens + t) * kDim, mtab, codes + pos * kRecordBytes,
+                  norms + pos, cb);
 }
 
 // Per-step append: one workgroup per sequence, one wave per vector (keys and
@@ -216,11 +269,11 @@ hipError_t launch_compress(const void* k, const void* v, int dtype, int64_t batc
   float* n1 = (k && v) ? v_norms : nullptr;
   const int nwhich = s1 ? 2 : 1;
   const int64_t n_bh = batch * n_heads;
-  const int64_t chunks = (n_tokens + 63) / 64;
+  const int64_t chunks = (n_tokens + kCompressThreads - 1) / kCompressThreads;
   const int64_t blocks = chunks * n_bh * nwhich;
   if (blocks == 0) return hipSuccess;
   const Codebook& cb = codebook();
-  const dim3 grid(static_cast<unsigned>(blocks)), block(64);
+  const dim3 grid(static_cast<unsigned>(blocks)), block(kCompressThreads);
   if (dtype == IQ_DTYPE_F16) {
     hipLaunchKernelGGL(compress_kernel<__half>, grid, block, 0, stream,
                        static_cast<const __half*>(s0), static_cast<const __half*>(s1), quats, c0,
