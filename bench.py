@@ -13,6 +13,15 @@ sweep over the layers).
 Prints one JSON line.  ``value`` is the achieved algorithmic HBM bandwidth of
 a step (bytes the method must move / step time); ``us_per_step`` is the
 decode-attention step time.
+
+``--workload`` selects the other measured shapes (each prints its own line;
+the default is the one above):
+  varlen    batch 64, 16 query heads, 2 KV heads, per-sequence contexts drawn
+            uniform in [2048, 32768]: one fused decode step per sequence;
+  compress  iq_compress_kv over 4 sequences x 32768 tokens x 8 KV heads, K and
+            V, fp16 Student-t(4) entries times log-normal channel scales;
+  append8k  batch 1, 32 query heads, 4 KV heads, 8192 compressed tokens, then
+            fused steps that each append one token (48 layer caches cycled).
 """
 
 from __future__ import annotations
@@ -38,16 +47,30 @@ BYTES_PER_TOKEN_HEAD = 2 * (RECORD + 4)      # K and V: 48-byte record + fp32 sc
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=4800)
-    p.add_argument("--warmup", type=int, default=480)
-    p.add_argument("--layers", type=int, default=48)
+    p.add_argument("--workload", choices=("step32k", "varlen", "compress", "append8k"),
+                   default="step32k")
+    p.add_argument("--steps", type=int, default=None,
+                   help="timed steps (default: 4800; varlen 240; compress 20; append8k 1000)")
+    p.add_argument("--warmup", type=int, default=None,
+                   help="untimed steps (default: steps / 10)")
+    p.add_argument("--layers", type=int, default=None,
+                   help="distinct layer caches cycled (default: 48; varlen 3)")
     p.add_argument("--context", type=int, default=32768)
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--calibrate-copy-mib", type=int, default=0,
                    help="also run one plain device copy of this many MiB (counter calibration)")
-    return p.parse_args()
+    a = p.parse_args()
+    defaults = {"step32k": (4800, 48), "varlen": (240, 3), "compress": (20, 1),
+                "append8k": (1000, 48)}[a.workload]
+    if a.steps is None:
+        a.steps = defaults[0]
+    if a.warmup is None:
+        a.warmup = max(1, a.steps // 10)
+    if a.layers is None:
+        a.layers = defaults[1]
+    return a
 
 
 def source_digest() -> str:
@@ -152,28 +175,53 @@ def read_traffic(digest: str):
     return t.get("hbm_bytes_per_launch")
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
-                          "n_gpus": args.gpus}))
-        sys.exit(2)
-
+def make_varlen_layers(api, synth, w, n_layers, lengths, capacity, seed, dev, slice_b=8):
+    """Per layer: batch caches where sequence b holds lengths[b] compressed
+    tokens (compressed in slices of `slice_b` sequences, each slice up to its
+    longest sequence; positions past a sequence's length are never read)."""
     import torch
 
-    from paper_2608_08081_amd import api, synth
+    layers = []
+    quats = api.iq_make_rotation(w.rotation_seed, w.n_kv_heads).to(dev)
+    for li in range(n_layers):
+        g = torch.Generator(device=dev)
+        g.manual_seed(seed * 100003 + 7919 * li + 1)
+        cache = api.alloc_cache(w.batch, w.n_kv_heads, capacity, dev)
+        scales = []
+        for stream in (0, 1):
+            sc = synth.channel_scales(synth.rng(seed + li, w.wid, stream), w.n_kv_heads)
+            scales.append(torch.from_numpy(sc).to(dev))
+        for b0 in range(0, w.batch, slice_b):
+            b1 = min(w.batch, b0 + slice_b)
+            t = int(lengths[b0:b1].max())
+            kv = []
+            for which in (0, 1):
+                x = torch.randn((b1 - b0, w.n_kv_heads, t, 128), generator=g, device=dev)
+                kv.append((x * scales[which][None, :, None, :]).half())
+            api.iq_compress_kv(kv[0], kv[1], quats, cache["k_codes"][b0:b1],
+                               cache["k_norms"][b0:b1], cache["v_codes"][b0:b1],
+                               cache["v_norms"][b0:b1])
+            del kv
+        cache["seq_lens"].copy_(torch.from_numpy(lengths).to(dev))
+        k_new = (torch.randn((w.batch, w.n_kv_heads, 128), generator=g, device=dev)
+                 * scales[0][None]).half()
+        v_new = (torch.randn((w.batch, w.n_kv_heads, 128), generator=g, device=dev)
+                 * scales[1][None]).half()
+        q = torch.randn((w.batch, w.n_q_heads, 128), generator=g, device=dev)
+        out = torch.empty((w.batch, w.n_q_heads, 128), device=dev)
+        layers.append(dict(cache=cache, k_new=k_new, v_new=v_new, q=q, out=out))
+    torch.cuda.synchronize()
+    return quats, layers
 
-    if not torch.cuda.is_available():
-        raise RuntimeError("bench.py needs a GPU")
-    dev = torch.device("cuda:0")
-    w = synth.WORKLOADS[2]
-    nl = args.layers
-    total_visits = math.ceil((args.warmup + args.steps) / nl) + 2
-    capacity = (args.context + total_visits + 64 + 63) // 64 * 64
-    print(f"# building {nl} layer caches ({args.context} positions each)", file=sys.stderr,
-          flush=True)
-    quats, layers = make_layers(api, synth, w, nl, args.context, capacity, args.seed, dev)
-    ws = api.alloc_workspace(w.batch, w.n_q_heads, w.n_kv_heads, capacity, dev)
+
+def time_steps(api, layers, quats, ws, capacity, args):
+    """Warm-up, then `args.steps` fused steps (append + attention) cycling the
+    layers, replayed from HIP graphs and timed with HIP events on the replay
+    stream; then the attention alone (iq_decode_attention) the same way.
+    Returns (us per fused step, us per decode-only call, wall seconds)."""
+    import torch
+
+    nl = len(layers)
 
     def step(li, append=True):
         L = layers[li]
@@ -186,15 +234,6 @@ def main():
             api.iq_decode_attention(L["q"], c["k_codes"], c["k_norms"], c["v_codes"],
                                     c["v_norms"], c["seq_lens"], quats, out=L["out"],
                                     workspace=ws, max_seq_len=capacity)
-
-    if args.calibrate_copy_mib > 0:
-        # a plain copy kernel of known size, for scaling FETCH_SIZE/WRITE_SIZE
-        src = torch.ones(args.calibrate_copy_mib << 18, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
 
     # eager warm-up of every layer once (loads the code object), then capture
     torch.cuda.synchronize()
@@ -239,12 +278,11 @@ def main():
     ev1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_total = ev0.elapsed_time(ev1)
-    us_per_step = ms_total * 1e3 / args.steps
+    us_per_step = ev0.elapsed_time(ev1) * 1e3 / args.steps
 
     # decode-only: HIP events around graph replays of decode launches on the
     # replay stream (the graph launches onto torch's current stream)
-    reps = max(1, 2400 // nl)
+    reps = max(1, min(2400, args.steps) // nl)
     d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     d0.record()
@@ -253,16 +291,25 @@ def main():
     d1.record()
     torch.cuda.synchronize()
     decode_us = d0.elapsed_time(d1) * 1e3 / (reps * nl)
+    return us_per_step, decode_us, wall
 
-    seq_now = float(sum(int(L["cache"]["seq_lens"][0]) for L in layers)) / nl
-    decode_bytes = w.batch * w.n_kv_heads * seq_now * BYTES_PER_TOKEN_HEAD
+
+def step_result(metric, workload, w, layers, nl, us_per_step, decode_us, wall, args, kernel,
+                extra_config=None):
+    """JSON line of a fused-step workload: algorithmic bytes of the attended
+    positions (per KV head and position: K and V records + scales) plus the
+    appended tokens' inputs and records, over the measured step time."""
+    seq_sum = sum(float(L["cache"]["seq_lens"].sum()) for L in layers) / nl
+    decode_bytes = w.n_kv_heads * seq_sum * BYTES_PER_TOKEN_HEAD
     append_bytes = w.batch * w.n_kv_heads * 2 * (128 * 2 + RECORD + 4)
     step_bytes = decode_bytes + append_bytes
     value = step_bytes / (us_per_step * 1e-6) / 1e9
-    digest = source_digest()
-
-    result = {
-        "metric": METRIC,
+    config = {"workload": workload, "batch": w.batch, "n_q_heads": w.n_q_heads,
+              "n_kv_heads": w.n_kv_heads, "mean_context": int(round(seq_sum / w.batch)),
+              "layers_cycled": nl, "step": "iq_decode_step (fused append + attention), one layer"}
+    config.update(extra_config or {})
+    return {
+        "metric": metric,
         "value": round(value, 2),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -276,35 +323,219 @@ def main():
         "vs_baseline": None,
         "dtype": "u3 codes, f32 accumulate",
         "data": "synthetic (seeded anisotropic fp16 K/V, compressed on device)",
-        "config": {
-            "workload": f"32K-context GQA decode step (append + attention), batch 1, 32 query "
-                        f"heads, 4 KV heads, head_dim 128, 3-bit packed KV; {nl} distinct layer "
-                        f"caches cycled (cold HBM)",
-            "batch": w.batch, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads,
-            "context": int(round(seq_now)), "layers_cycled": nl,
-            "step": "iq_decode_step (fused append + attention), one layer",
-        },
+        "config": config,
         "roofline": {
             "bound": "hbm",
             "achieved": round(value, 2),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(value / HBM_PEAK_GBS, 4),
-            "traffic": read_traffic(digest),
-            "kernel": "iq_decode_step per call = decode_g8_kernel<NB, append> + "
-                      "merge_g8_kernel<append>, back to back in one graph; algorithmic bytes = "
-                      f"{BYTES_PER_TOKEN_HEAD} B x positions x KV heads + the appended token's "
-                      "inputs and records",
+            "traffic": None,
+            "kernel": kernel,
             "bytes_per_launch": int(step_bytes),
             "launch_us": round(us_per_step, 3),
             "decode_only_us": round(decode_us, 3),
         },
         "wall_s": round(wall, 3),
-        "source_digest": digest,
     }
+
+
+def run_step32k(args, torch, api, synth, dev):
+    w = synth.WORKLOADS[2]
+    nl = args.layers
+    total_visits = math.ceil((args.warmup + args.steps) / nl) + 2
+    capacity = (args.context + total_visits + 64 + 63) // 64 * 64
+    print(f"# building {nl} layer caches ({args.context} positions each)", file=sys.stderr,
+          flush=True)
+    quats, layers = make_layers(api, synth, w, nl, args.context, capacity, args.seed, dev)
+    ws = api.alloc_workspace(w.batch, w.n_q_heads, w.n_kv_heads, capacity, dev)
+    if args.calibrate_copy_mib > 0:
+        # a plain copy kernel of known size, for scaling FETCH_SIZE/WRITE_SIZE
+        src = torch.ones(args.calibrate_copy_mib << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    us_per_step, decode_us, wall = time_steps(api, layers, quats, ws, capacity, args)
+    digest = source_digest()
+    result = step_result(
+        METRIC,
+        f"32K-context GQA decode step (append + attention), batch 1, 32 query heads, 4 KV "
+        f"heads, head_dim 128, 3-bit packed KV; {nl} distinct layer caches cycled (cold HBM)",
+        w, layers, nl, us_per_step, decode_us, wall, args,
+        "iq_decode_step per call = decode_g8_kernel<NB, append> + merge_g8_kernel<append>, back "
+        f"to back in one graph; algorithmic bytes = {BYTES_PER_TOKEN_HEAD} B x positions x KV "
+        "heads + the appended token's inputs and records")
+    result["config"]["context"] = result["config"].pop("mean_context")
+    result["roofline"]["traffic"] = read_traffic(digest)
+    result["source_digest"] = digest
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.context, args.cpu_seconds)
-    print(json.dumps(result), flush=True)
+    return result
+
+
+def run_varlen(args, torch, api, synth, dev):
+    w = synth.WORKLOADS[3]
+    nl = args.layers
+    lengths = synth.context_lengths(args.seed, w)
+    total_visits = math.ceil((args.warmup + args.steps) / nl) + 2
+    capacity = (int(lengths.max()) + total_visits + 64 + 63) // 64 * 64
+    print(f"# building {nl} varlen layer caches (batch {w.batch}, mean context "
+          f"{lengths.mean():.0f})", file=sys.stderr, flush=True)
+    quats, layers = make_varlen_layers(api, synth, w, nl, lengths, capacity, args.seed, dev)
+    ws = api.alloc_workspace(w.batch, w.n_q_heads, w.n_kv_heads, capacity, dev)
+    us_per_step, decode_us, wall = time_steps(api, layers, quats, ws, capacity, args)
+    return step_result(
+        "batched varlen decode µs/step + achieved HBM GB/s on packed 3-bit KV",
+        f"batched serving decode step (append + attention), batch {w.batch}, {w.n_q_heads} "
+        f"query heads, {w.n_kv_heads} KV heads, head_dim 128, contexts uniform in "
+        f"[{w.varlen[0]}, {w.varlen[1]}] (seeded); {nl} distinct layer caches cycled",
+        w, layers, nl, us_per_step, decode_us, wall, args,
+        "iq_decode_step per call = decode_g8_kernel<NB, append> + merge_g8_kernel<append>; "
+        f"algorithmic bytes = {BYTES_PER_TOKEN_HEAD} B x attended positions x KV heads + the "
+        "appended tokens' inputs and records",
+        {"lengths_min": int(lengths.min()), "lengths_max": int(lengths.max())})
+
+
+def run_append8k(args, torch, api, synth, dev):
+    w = synth.WORKLOADS[1]
+    nl = args.layers
+    total_visits = math.ceil((args.warmup + args.steps) / nl) + 2
+    capacity = (w.context + total_visits + 64 + 63) // 64 * 64
+    print(f"# building {nl} layer caches ({w.context} positions each)", file=sys.stderr,
+          flush=True)
+    quats, layers = make_layers(api, synth, w, nl, w.context, capacity, args.seed, dev)
+    ws = api.alloc_workspace(w.batch, w.n_q_heads, w.n_kv_heads, capacity, dev)
+    us_per_step, decode_us, wall = time_steps(api, layers, quats, ws, capacity, args)
+    return step_result(
+        "8K-context decode step (append one token + attention) µs/step + achieved HBM GB/s",
+        f"GQA decode steps that each append one token, batch 1, 32 query heads, 4 KV heads, "
+        f"head_dim 128, {w.context} compressed tokens to start; {nl} distinct layer caches "
+        "cycled",
+        w, layers, nl, us_per_step, decode_us, wall, args,
+        "iq_decode_step per call = decode_g8_kernel<NB, append> + merge_g8_kernel<append>; "
+        f"algorithmic bytes = {BYTES_PER_TOKEN_HEAD} B x attended positions x KV heads + the "
+        "appended tokens' inputs and records")
+
+
+def cpu_compress_baseline(seconds):
+    """The oracle's fp64 compression on a bounded sample of vectors."""
+    import numpy as np
+
+    from oracle import codebook as ocb
+    from oracle import compress as ocz
+    from oracle import rotation as orot
+    from paper_2608_08081_amd import synth
+
+    _, thr = ocb.isoquant_codebook()
+    w = synth.WORKLOADS[4]
+    k = synth.kv_tensor(3, w, "k", n_tokens=1024, batch=1)[:, :1]
+    rots = orot.rotation_matrices(orot.make_quaternions(w.rotation_seed, 1))
+    n_vec = k.shape[2]
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        ocz.compress_kv(k, rots, thr)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or reps >= 1000:
+            break
+    per = el / reps
+    return {"value": n_vec * (256 + 52) / per / 1e9, "unit": "GB/s", "cores": os.cpu_count(),
+            "kind": "oracle",
+            "sample": f"oracle fp64 compress_kv of {n_vec} fp16 vectors, {reps} reps in "
+                      f"{el:.1f}s ({per * 1e3:.1f} ms each); algorithmic bytes / time"}
+
+
+def run_compress(args, torch, api, synth, dev):
+    w = synth.WORKLOADS[4]
+    g = torch.Generator(device=dev)
+    g.manual_seed(args.seed * 100003 + 4)
+    quats = api.iq_make_rotation(w.rotation_seed, w.n_kv_heads).to(dev)
+    kv = []
+    for stream in (0, 1):
+        sc = torch.from_numpy(synth.channel_scales(synth.rng(args.seed, w.wid, stream),
+                                                   w.n_kv_heads, n_outliers=0)).to(dev)
+        shape = (w.batch, w.n_kv_heads, w.context, 128)
+        # Student-t(4) = N(0,1) / sqrt(chi2_4 / 4)
+        z = torch.randn(shape, generator=g, device=dev)
+        chi = sum(torch.randn(shape, generator=g, device=dev) ** 2 for _ in range(4))
+        kv.append((z * torch.rsqrt(chi / 4.0) * sc[None, :, None, :]).half())
+        del z, chi
+    cache = api.alloc_cache(w.batch, w.n_kv_heads, w.context, dev)
+
+    def call():
+        api.iq_compress_kv(kv[0], kv[1], quats, cache["k_codes"], cache["k_norms"],
+                           cache["v_codes"], cache["v_norms"])
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(args.steps):
+        call()
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    us = ev0.elapsed_time(ev1) * 1e3 / args.steps
+    n_vec = 2 * w.batch * w.n_kv_heads * w.context
+    byts = n_vec * (128 * 2 + RECORD + 4)
+    value = byts / (us * 1e-6) / 1e9
+    result = {
+        "metric": "compression GB/s (read + written) and vectors/s, prefill-scale",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(us / 1e3, 6),
+        "us_per_call": round(us, 3),
+        "vectors_per_s": round(n_vec / (us * 1e-6), 1),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16 in, u3 codes + f32 scales out, f32/f64 arithmetic",
+        "data": "synthetic (seeded Student-t(4) x log-normal channel scales, fp16)",
+        "config": {"workload": f"iq_compress_kv of K and V, {w.batch} sequences x {w.context} "
+                               f"tokens x {w.n_kv_heads} KV heads, head_dim 128",
+                   "vectors": n_vec},
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(value, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(value / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "kernel": "compress_kernel<__half>: 256 B read + 52 B written per vector",
+            "bytes_per_launch": int(byts),
+            "launch_us": round(us, 3),
+        },
+        "wall_s": round(wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_compress_baseline(min(args.cpu_seconds, 10.0))
+    return result
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+
+    from paper_2608_08081_amd import api, synth
+
+    if not torch.cuda.is_available():
+        raise RuntimeError("bench.py needs a GPU")
+    dev = torch.device("cuda:0")
+    run = {"step32k": run_step32k, "varlen": run_varlen, "compress": run_compress,
+           "append8k": run_append8k}[args.workload]
+    print(json.dumps(run(args, torch, api, synth, dev)), flush=True)
 
 
 if __name__ == "__main__":

@@ -61,7 +61,7 @@ typedef uint32_t u32x2_a4_t __attribute__((ext_vector_type(2), aligned(4)));
 constexpr int kWaves = 8;                 // waves of a decode workgroup
 constexpr int kThreads = 64 * kWaves;
 constexpr int kRotThreads = 256;          // (head, SO(4) block) tasks: waves 0..3
-constexpr int kMaxBatches = 5;            // 16-position batches per wave (register budget)
+constexpr int kMaxBatches = 6;            // 16-position batches per wave (register budget)
 constexpr int kMergeThreads = 256;
 constexpr int kRecStride = kRecordWords + 1;   // staged record stride (words): spreads banks
 constexpr int kQRowWords = kDim / 2 + 4;  // fp16-pair row of one head, padded (68 words)
@@ -487,12 +487,18 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   const bool new_attended = writer && seq0 < max_seq_len;
   int end = seq < start + split_len ? seq : start + split_len;
   if (new_attended) end = seq0;
-  // this wave's run of batches: nbat / 8 each, one more for the first
-  // nbat % 8 waves
+  // this wave's run of batches: nbat / n_att each, one more for the first
+  // nbat % n_att waves, over the n_att attending waves (all 8, or in the
+  // writer workgroup the 7 that do not compress the new token, so that the
+  // compression runs beside the attention rather than before it)
+  constexpr int kCompressWave = kWaves - 1;
   const int nbat = split_len >> 4;
-  const int nb_base = nbat / kWaves, nb_rem = nbat % kWaves;
-  const int nb_w = nb_base + (wave < nb_rem ? 1 : 0);
-  const int wbase = start + 16 * (wave * nb_base + (wave < nb_rem ? wave : nb_rem));
+  const int n_att = (kAppend && writer) ? kWaves - 1 : kWaves;
+  const bool att_wave = wave < n_att;
+  const int nb_base = nbat / n_att, nb_rem = nbat % n_att;
+  const int nb_w = att_wave ? nb_base + (wave < nb_rem ? 1 : 0) : 0;
+  const int wbase =
+      start + (att_wave ? 16 * (wave * nb_base + (wave < nb_rem ? wave : nb_rem)) : 0);
   int nvalid = end - wbase;   // this wave's positions (may be <= 0)
   nvalid = nvalid < 16 * nb_w ? nvalid : 16 * nb_w;
   // start of the wave's last batch holding positions (clamp of the loads)
@@ -506,10 +512,9 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   const float* kn = k_norms + row;
   const float* vn = v_norms + row;
 
-  // kAppend, writer workgroup: the last wave, which holds the fewest
-  // positions of the split, compresses the new key and value after its own
-  // positions (they are needed only in the workgroup merge)
-  constexpr int kCompressWave = kWaves - 1;
+  // kAppend, writer workgroup: the last wave, which attends no positions,
+  // compresses the new key and value (the records are needed only in the
+  // workgroup merge)
   // the new key and value stay raw (dims 2 lane, 2 lane + 1: one fp16 pair
   // word, or two fp32 words) until they are compressed, so that no wait for
   // them is placed before the cache loads
@@ -605,21 +610,6 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   stage[wave].vs[lane] = vsl;
   wave_lds_fence();
 
-  float m_run = -INFINITY, l_run = 0.f, vmax = 0.f;
-  f32x4_t o_acc[4];
-#pragma unroll
-  for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  if (nvalid == 16 * NB)
-    attend_wave<NB, NB, true>(kw, vw, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
-                              qdown, m_run, l_run, vmax, o_acc);
-  else if (NB > 1 && nvalid == 16 * (NB - 1))
-    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true>(kw, vw, stage[wave], qb, lut, col, grp,
-                                                nvalid, vdw, vsh, qdown, m_run, l_run, vmax,
-                                                o_acc);
-  else if (nvalid > 0)
-    attend_wave<NB, NB, false>(kw, vw, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
-                               qdown, m_run, l_run, vmax, o_acc);
-
   if (compressing) {
     float nk0, nk1, nv0, nv1;
     if (new_f16) {
@@ -650,6 +640,21 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
       new_scale[1] = wv.scale;
     }
   }
+
+  float m_run = -INFINITY, l_run = 0.f, vmax = 0.f;
+  f32x4_t o_acc[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  if (nvalid == 16 * NB)
+    attend_wave<NB, NB, true>(kw, vw, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
+                              qdown, m_run, l_run, vmax, o_acc);
+  else if (NB > 1 && nvalid == 16 * (NB - 1))
+    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true>(kw, vw, stage[wave], qb, lut, col, grp,
+                                                nvalid, vdw, vsh, qdown, m_run, l_run, vmax,
+                                                o_acc);
+  else if (nvalid > 0)
+    attend_wave<NB, NB, false>(kw, vw, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
+                               qdown, m_run, l_run, vmax, o_acc);
 
   // ---- merge the 8 waves in LDS ---------------------------------------------
   lds_barrier();   // every wave is done with its staging area
@@ -851,7 +856,9 @@ __global__ void advance_lengths_kernel(int32_t* __restrict__ seq_lens, int64_t c
 void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
              int64_t* n_splits, int64_t* split_len) {
   constexpr int64_t kCus = 256;
-  constexpr int64_t kMaxLen = 16 * kWaves * kMaxBatches;
+  // at most 5 batches per wave over 8 waves; the fused step's writer
+  // workgroup deals them over 7 waves, at most 6 each
+  constexpr int64_t kMaxLen = 16 * kWaves * 5;
   const int64_t t = max_seq_len > 0 ? max_seq_len : 1;
   const int64_t bg = batch * n_kv_heads > 0 ? batch * n_kv_heads : 1;
   int64_t s = (t + kMaxLen - 1) / kMaxLen;
@@ -879,6 +886,8 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                             float* out, float* partials, const StepAppend* append,
                             hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>(batch * n_kv_heads * n_splits)), block(kThreads);
+  // the fused step's writer workgroup deals the split's batches over 7 waves
+  if (append) nb = static_cast<int>((split_len / 16 + kWaves - 2) / (kWaves - 1));
   const float qscale = scale * kLog2e;
   const Codebook& cb = codebook();
   const void* k_new = append ? append->k_new : nullptr;
@@ -897,7 +906,8 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
     case 2: IQ_LAUNCH_G8(2, APP_); break; \
     case 3: IQ_LAUNCH_G8(3, APP_); break; \
     case 4: IQ_LAUNCH_G8(4, APP_); break; \
-    default: IQ_LAUNCH_G8(5, APP_); break; \
+    case 5: IQ_LAUNCH_G8(5, APP_); break; \
+    default: IQ_LAUNCH_G8(6, APP_); break; \
   }
   if (append) {
     IQ_LAUNCH_G8_NB(true)
