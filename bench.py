@@ -349,14 +349,6 @@ def run_step32k(args, torch, api, synth, dev):
           flush=True)
     quats, layers = make_layers(api, synth, w, nl, args.context, capacity, args.seed, dev)
     ws = api.alloc_workspace(w.batch, w.n_q_heads, w.n_kv_heads, capacity, dev)
-    if args.calibrate_copy_mib > 0:
-        # a plain copy kernel of known size, for scaling FETCH_SIZE/WRITE_SIZE
-        src = torch.ones(args.calibrate_copy_mib << 18, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
     us_per_step, decode_us, wall = time_steps(api, layers, quats, ws, capacity, args)
     digest = source_digest()
     result = step_result(
@@ -533,6 +525,14 @@ def main():
     if not torch.cuda.is_available():
         raise RuntimeError("bench.py needs a GPU")
     dev = torch.device("cuda:0")
+    if args.calibrate_copy_mib > 0:
+        # a plain copy kernel of known size, for scaling FETCH_SIZE/WRITE_SIZE
+        src = torch.ones(args.calibrate_copy_mib << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     run = {"step32k": run_step32k, "varlen": run_varlen, "compress": run_compress,
            "append8k": run_append8k}[args.workload]
     print(json.dumps(run(args, torch, api, synth, dev)), flush=True)
