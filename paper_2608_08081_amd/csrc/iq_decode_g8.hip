@@ -209,7 +209,7 @@ struct WaveStage {
 // Cache loads of one wave, in the order the data is used: both scale arrays
 // (one 16-byte load per lane: lane j takes positions 4j .. 4j+3 of the
 // wave), then per batch of 16 positions the keys (load_keys), and later the
-// values (load_values).  Keys and values are loaded the same way: lane
+// values (load_value_batch, one batch at a time as the scores proceed).  Keys and values are loaded the same way: lane
 // (t = col, gk = grp) takes dwords 3gk .. 3gk+2 of position t, one coalesced
 // 768-byte load per batch.
 // Batch starts are multiples of 16 and the capacity is a multiple of 16, so a
@@ -244,21 +244,19 @@ __device__ __forceinline__ void load_keys(const uint8_t* kc, const float* kn, co
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int NB>
-__device__ __forceinline__ void load_values(const uint8_t* vc, int wbase, int clamp16, int col,
-                                            int grp, uint32_t (&vw)[NB][3]) {
-  const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
-  __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    const int tb = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
-    const uint32_t* p =
-        reinterpret_cast<const uint32_t*>(vc + static_cast<uint32_t>(tb * kRecordBytes) + koff);
-    vw[i][0] = p[0];
-    vw[i][1] = p[1];
-    vw[i][2] = p[2];
-  }
-  __builtin_amdgcn_sched_barrier(0);
+// Scheduling-barrier mask: every instruction type may move across except
+// vector-memory ones (keeps the value loads in their place and order).
+constexpr int kNoVmemAcross = 0x1 | 0x2 | 0x4 | 0x8 | 0x80 | 0x100 | 0x200 | 0x400;
+
+// Value slice of one batch: lane (t = col, gk = grp) takes dwords 3gk ..
+// 3gk+2 of position tb + t (one coalesced 768-byte load).
+__device__ __forceinline__ void load_value_batch(const uint8_t* vc, int tb, uint32_t koff,
+                                                 uint32_t (&v)[3]) {
+  const uint32_t* p =
+      reinterpret_cast<const uint32_t*>(vc + static_cast<uint32_t>(tb * kRecordBytes) + koff);
+  v[0] = p[0];
+  v[1] = p[1];
+  v[2] = p[2];
 }
 
 // Scores, softmax and value accumulation of one wave over the batches that
@@ -275,16 +273,22 @@ __device__ __forceinline__ void load_values(const uint8_t* vc, int wbase, int cl
 // LDS operations complete in order.
 template <int NB, int NBX, bool kFull>
 __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
-                                            const uint32_t (&vw)[NB][3], WaveStage& st,
+                                            uint32_t (&vw)[NB][3], const uint8_t* vc,
+                                            uint32_t koff, const int (&tb)[NB], WaveStage& st,
                                             const u32x4_t (&qb)[4],
                                             const uint32_t* lut, int col, int grp, int nvalid,
                                             int vdw, uint32_t vsh, float qdown, float& m_run,
                                             float& l_run, float& vmax, f32x4_t (&o_acc)[4]) {
   // ---- phase 1: scores (Table 2 A) -----------------------------------------
+  // the value load of batch i goes out as batch i's scores start, so that
+  // phase 1 begins without waiting to issue every value load first
   f32x4_t sc[NBX];
 #pragma unroll
   for (int i = 0; i < NBX; ++i) {
     if (!kFull && 16 * i >= nvalid) break;
+    __builtin_amdgcn_sched_barrier(kNoVmemAcross);
+    load_value_batch(vc, tb[i], koff, vw[i]);
+    __builtin_amdgcn_sched_barrier(kNoVmemAcross);
     const uint32_t w0 = kw[i][0], w1 = kw[i][1], w2 = kw[i][2];
     u32x4_t a[4];
 #pragma unroll
@@ -594,9 +598,13 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     if (qblk == 0) qexp_s[qh] = qexp;
   }
   lds_barrier();   // lut, qop, qexp_s
-  // the values go out after the barrier: a wave reaches it once its keys are
-  // issued, and the values stream in while the scores are computed
-  load_values<NB>(vc, wbase, clamp16, col, grp, vw);
+  // the values go out after the barrier, one batch per batch of scores: a
+  // wave reaches the barrier once its keys are issued, and the values stream
+  // in while the scores are computed
+  const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
+  int tb[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) tb[i] = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
   // QK B operands: column col -> head col % 8, hi part for col < 8, lo part
   // for col >= 8; MFMA kb, lane group grp -> dims 32 grp + 8 kb + 0..7 (fp16
   // pair words 16 grp + 4 kb .. +3)
@@ -646,14 +654,14 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if (nvalid == 16 * NB)
-    attend_wave<NB, NB, true>(kw, vw, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
+    attend_wave<NB, NB, true>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
                               qdown, m_run, l_run, vmax, o_acc);
   else if (NB > 1 && nvalid == 16 * (NB - 1))
-    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true>(kw, vw, stage[wave], qb, lut, col, grp,
+    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp,
                                                 nvalid, vdw, vsh, qdown, m_run, l_run, vmax,
                                                 o_acc);
   else if (nvalid > 0)
-    attend_wave<NB, NB, false>(kw, vw, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
+    attend_wave<NB, NB, false>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
                                qdown, m_run, l_run, vmax, o_acc);
 
   // ---- merge the 8 waves in LDS ---------------------------------------------
