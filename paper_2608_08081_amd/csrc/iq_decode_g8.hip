@@ -61,8 +61,11 @@ typedef uint32_t u32x2_a4_t __attribute__((ext_vector_type(2), aligned(4)));
 constexpr int kWaves = 8;                 // waves of a decode workgroup
 constexpr int kThreads = 64 * kWaves;
 constexpr int kRotThreads = 256;          // (head, SO(4) block) tasks: waves 0..3
-constexpr int kMaxBatches = 6;            // 16-position batches per wave (register budget)
+constexpr int kMaxBatches = 5;            // 16-position batches per wave (register budget)
 constexpr int kMergeThreads = 256;
+// dynamic LDS that, added to the kernel's own, leaves room for one
+// workgroup per CU (160 KB of LDS per CU)
+constexpr size_t kOneWorkgroupPadBytes = 48 * 1024;
 constexpr int kRecStride = kRecordWords + 1;   // staged record stride (words): spreads banks
 constexpr int kQRowWords = kDim / 2 + 4;  // fp16-pair row of one head, padded (68 words)
 constexpr int kHeads = 8;                 // query heads per KV head
@@ -134,6 +137,25 @@ __device__ __forceinline__ void lane_wht32(f32x4_t& x, int blk) {
   lane_butterfly<4>(x, blk);
   lane_butterfly<8>(x, blk);
   lane_butterfly<16>(x, blk);
+}
+
+// Largest value over all 64 lanes, returned wave-uniform: quad and row
+// rotations (DPP) give every 16-lane row its maximum, the row broadcasts
+// (row_bcast:15 into rows 1 and 3, row_bcast:31 into rows 2 and 3) carry
+// the lower rows into row 3, and its last lane is read out.
+__device__ __forceinline__ float wave64_max(float x) {
+  x = fmaxf(x, xor_lane<1>(x));
+  x = fmaxf(x, xor_lane<2>(x));
+  x = fmaxf(x, __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x),
+                                                                  0x124, 0xF, 0xF, true)));
+  x = fmaxf(x, xor_lane<8>(x));
+  int xi = __builtin_bit_cast(int, x);
+  x = fmaxf(x, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(xi, xi, 0x142, 0xA, 0xF,
+                                                                     false)));
+  xi = __builtin_bit_cast(int, x);
+  x = fmaxf(x, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(xi, xi, 0x143, 0xC, 0xF,
+                                                                     false)));
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 63));
 }
 
 // Largest value over the lane's group of 32 lanes.
@@ -266,12 +288,16 @@ __device__ __forceinline__ void load_value_batch(const uint8_t* vc, int tb, uint
 // Scores are kept in the per-head scaled domain (x = acc * s^K, the query
 // operand carried 2^qexp); qdown = 2^-qexp turns them into log2 units inside
 // the exponent.  On return m_run is in log2 units.
-// Scale group g of batch i (positions 16 i + 4 g ..) is st.ks[4 i + g].
+// Scale group g of batch i (positions 16 i + 4 g ..) is st.ks[4 i + g].  The
+// value scales st.vs[4 i + g]: kWide, staged already multiplied by 2^15 /
+// vmax (vmax = the wave's largest attended value scale, computed by the
+// caller) and 0 past nvalid; otherwise staged as loaded, and vmax (in: 0) is
+// computed here.
 // lut: the pair table.  Each batch's value records go through st.rec[i]
 // (lane (t, gk) writes its 12 bytes of record t, lane (u, grp) reads the
 // 8-byte window holding bytes 3u..3u+2 of records 4 grp + r); the wave's own
 // LDS operations complete in order.
-template <int NB, int NBX, bool kFull>
+template <int NB, int NBX, bool kFull, bool kWide>
 __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
                                             uint32_t (&vw)[NB][3], const uint8_t* vc,
                                             uint32_t koff, const int (&tb)[NB], WaveStage& st,
@@ -312,26 +338,34 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
       for (int r = 0; r < 4; ++r) x[r] = (16 * i + 4 * grp + r < nvalid) ? x[r] : -INFINITY;
     }
     sc[i] = x;
-    m_run = fmaxf(fmaxf(m_run, fmaxf(x[0], x[1])), fmaxf(x[2], x[3]));
-  }
-  // largest value scale of the wave
-  f32x4_t vsv[NBX];
-#pragma unroll
-  for (int i = 0; i < NBX; ++i) {
-    if (!kFull && 16 * i >= nvalid) break;
-    f32x4_t v = st.vs[4 * i + grp];
-    if (!kFull && 16 * i + 16 > nvalid) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = (16 * i + 4 * grp + r < nvalid) ? v[r] : 0.f;
-    }
-    vsv[i] = v;
-    vmax = fmaxf(fmaxf(vmax, fmaxf(v[0], v[1])), fmaxf(v[2], v[3]));
+    m_run = fmaxf(fmaxf(m_run, x[0]), x[1]);
+    m_run = fmaxf(fmaxf(m_run, x[2]), x[3]);
   }
   m_run = wave_max(m_run);
-  vmax = wave_max(vmax);
-  // weights scaled by 2^15 / vmax: in [0, 2^15], fp16-normal down to ~2e-9 of
-  // the largest weight; split into fp16 hi + lo parts
-  const float vinv = vmax > 0.f ? 32768.0f * __builtin_amdgcn_rcpf(vmax) : 0.f;
+  // weight scales s^V * 2^15 / vmax.  Wide grids: staged that way in the
+  // prologue and read per batch, so the kernel stays within 128 VGPRs.
+  // Otherwise: the batches' value scales are read into registers here,
+  // before the fence below (which would hold the reads back), with vmax
+  // taken over them (off the prologue's critical path).
+  f32x4_t wvv[NBX];
+  if constexpr (!kWide) {
+#pragma unroll
+    for (int i = 0; i < NBX; ++i) {
+      if (!kFull && 16 * i >= nvalid) break;
+      f32x4_t v = st.vs[4 * i + grp];
+      if (!kFull && 16 * i + 16 > nvalid) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = (16 * i + 4 * grp + r < nvalid) ? v[r] : 0.f;
+      }
+      wvv[i] = v;
+      vmax = fmaxf(fmaxf(vmax, v[0]), v[1]);
+      vmax = fmaxf(fmaxf(vmax, v[2]), v[3]);
+    }
+    vmax = wave_max(vmax);
+    const float vinv = vmax > 0.f ? 32768.0f * __builtin_amdgcn_rcpf(vmax) : 0.f;
+#pragma unroll
+    for (int i = 0; i < NBX; ++i) wvv[i] *= vinv;
+  }
   const uint32_t slot_shift = (col >= 8) ? 16u : 0u;
   const float mq = -m_run * qdown;
 
@@ -350,7 +384,7 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
   for (int i = 0; i < NBX; ++i) {
     if (!kFull && 16 * i >= nvalid) break;
     const uint32_t* rec = st.rec[i];
-    const f32x4_t wv = vsv[i] * vinv;
+    const f32x4_t wv = kWide ? st.vs[4 * i + grp] : wvv[i];   // 0 past nvalid
     u32x4_t pw_hi, pw_lo;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -392,7 +426,7 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
 // from the fresh record, join in the workgroup merge.  seq_lens is advanced
 // by the merge kernel (or by advance_lengths_kernel for a single split),
 // after every workgroup has read it.
-template <int NB, bool kAppend>
+template <int NB, bool kAppend, bool kWide>
 __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     const float* __restrict__ q, uint8_t* __restrict__ k_codes, float* __restrict__ k_norms,
     uint8_t* __restrict__ v_codes, float* __restrict__ v_norms,
@@ -613,9 +647,24 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   for (int kb = 0; kb < 4; ++kb)
     qb[kb] = *reinterpret_cast<const u32x4_t*>(&qop[col >> 3][col & 7][16 * grp + 4 * kb]);
   const float qdown = ldexpf(1.0f, -qexp_s[col & 7]);
-  // this wave's scales to its LDS stage (read back per batch)
+  // this wave's scales to its LDS stage (read back per batch).  Lane j
+  // holds positions 4j .. 4j+3 of the wave; the value scales of positions at
+  // or past nvalid count as 0.  The largest of the rest, vmax, sets the
+  // weight scale 2^15 / vmax: weights in [0, 2^15], fp16-normal down to ~2e-9
+  // of the largest weight (they are split into fp16 hi + lo parts).  Wide
+  // grids apply it here; otherwise attend_wave does, after the scores.
+  float vmax = 0.f;
+  if constexpr (kWide) {
+    f32x4_t v = vsl;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[r] = (4 * lane + r < nvalid) ? v[r] : 0.f;
+    vmax = wave64_max(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+    const float vinv = vmax > 0.f ? 32768.0f * __builtin_amdgcn_rcpf(vmax) : 0.f;
+    stage[wave].vs[lane] = v * vinv;
+  } else {
+    stage[wave].vs[lane] = vsl;   // scaled in attend_wave
+  }
   stage[wave].ks[lane] = ksl;
-  stage[wave].vs[lane] = vsl;
   wave_lds_fence();
 
   if (compressing) {
@@ -649,19 +698,19 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     }
   }
 
-  float m_run = -INFINITY, l_run = 0.f, vmax = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
   f32x4_t o_acc[4];
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if (nvalid == 16 * NB)
-    attend_wave<NB, NB, true>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
+    attend_wave<NB, NB, true, kWide>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
                               qdown, m_run, l_run, vmax, o_acc);
   else if (NB > 1 && nvalid == 16 * (NB - 1))
-    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp,
+    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true, kWide>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp,
                                                 nvalid, vdw, vsh, qdown, m_run, l_run, vmax,
                                                 o_acc);
   else if (nvalid > 0)
-    attend_wave<NB, NB, false>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
+    attend_wave<NB, NB, false, kWide>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
                                qdown, m_run, l_run, vmax, o_acc);
 
   // ---- merge the 8 waves in LDS ---------------------------------------------
@@ -857,16 +906,16 @@ __global__ void advance_lengths_kernel(int32_t* __restrict__ seq_lens, int64_t c
 }  // namespace
 
 // Split plan of the group-8 path: splits per (sequence, KV head) and their
-// length (a multiple of 16).  A workgroup covers at most 8 waves x 5 batches
-// x 16 = 640 positions; while the grid is small (<= 4 rounds of one
+// length (a multiple of 16).  A workgroup covers at most 7 x 5 batches x 16 =
+// 560 positions; while the grid is small (<= 4 rounds of one
 // workgroup per CU) the split count is raised so that the grid fills whole
 // rounds, but a split keeps at least one batch per wave.
 void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
              int64_t* n_splits, int64_t* split_len) {
   constexpr int64_t kCus = 256;
-  // at most 5 batches per wave over 8 waves; the fused step's writer
-  // workgroup deals them over 7 waves, at most 6 each
-  constexpr int64_t kMaxLen = 16 * kWaves * 5;
+  // at most 7 x 5 batches: the fused step's writer workgroup deals them over
+  // 7 waves, the others over 8, at most 5 each
+  constexpr int64_t kMaxLen = 16 * (kWaves - 1) * kMaxBatches;
   const int64_t t = max_seq_len > 0 ? max_seq_len : 1;
   const int64_t bg = batch * n_kv_heads > 0 ? batch * n_kv_heads : 1;
   int64_t s = (t + kMaxLen - 1) / kMaxLen;
@@ -894,6 +943,14 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                             float* out, float* partials, const StepAppend* append,
                             hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>(batch * n_kv_heads * n_splits)), block(kThreads);
+  // Up to 5 batches per wave the kernel needs at most 128 VGPRs and ~55 KB of
+  // LDS, so two workgroups fit on a CU: a grid of several rounds then runs
+  // one workgroup's prologue and merge beside another's attention.  A grid
+  // of at most one round would instead pile two workgroups on some CUs and
+  // leave others idle; padding its LDS request keeps one workgroup per CU.
+  constexpr int64_t kCus = 256;
+  const bool wide = grid.x > kCus;
+  const size_t lds_pad = wide ? 0 : kOneWorkgroupPadBytes;
   // the fused step's writer workgroup deals the split's batches over 7 waves
   if (append) nb = static_cast<int>((split_len / 16 + kWaves - 2) / (kWaves - 1));
   const float qscale = scale * kLog2e;
@@ -902,20 +959,25 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   const void* v_new = append ? append->v_new : nullptr;
   const int new_f16 = append ? append->f16 : 0;
   int32_t* status = append ? append->status : nullptr;
-#define IQ_LAUNCH_G8(NB_, APP_)                                                                  \
-  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_>), grid, block, 0, stream, q, k_codes, k_norms, \
-                     v_codes, v_norms, seq_lens, quats, partials, out, capacity,               \
-                     static_cast<int>(max_seq_len), static_cast<int>(n_kv_heads),              \
+#define IQ_LAUNCH_G8_W(NB_, APP_, WIDE_)                                                         \
+  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_>), grid, block, lds_pad, stream, q,      \
+                     k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials, out,        \
+                     capacity, static_cast<int>(max_seq_len), static_cast<int>(n_kv_heads),     \
                      static_cast<int>(n_splits), static_cast<int>(split_len), qscale, cb,      \
                      k_new, v_new, new_f16, status)
+#define IQ_LAUNCH_G8(NB_, APP_)          \
+  if (wide) {                            \
+    IQ_LAUNCH_G8_W(NB_, APP_, true);     \
+  } else {                               \
+    IQ_LAUNCH_G8_W(NB_, APP_, false);    \
+  }
 #define IQ_LAUNCH_G8_NB(APP_)            \
   switch (nb) {                          \
     case 1: IQ_LAUNCH_G8(1, APP_); break; \
     case 2: IQ_LAUNCH_G8(2, APP_); break; \
     case 3: IQ_LAUNCH_G8(3, APP_); break; \
     case 4: IQ_LAUNCH_G8(4, APP_); break; \
-    case 5: IQ_LAUNCH_G8(5, APP_); break; \
-    default: IQ_LAUNCH_G8(6, APP_); break; \
+    default: IQ_LAUNCH_G8(5, APP_); break; \
   }
   if (append) {
     IQ_LAUNCH_G8_NB(true)
@@ -924,6 +986,7 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   }
 #undef IQ_LAUNCH_G8_NB
 #undef IQ_LAUNCH_G8
+#undef IQ_LAUNCH_G8_W
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // splits of every (sequence, query head) merged by a second launch; the

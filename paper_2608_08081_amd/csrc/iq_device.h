@@ -97,13 +97,15 @@ __device__ __forceinline__ void put_code(uint32_t (&w)[kRecordWords], int i, uin
 template <int kM>
 __device__ __forceinline__ float xor_lane(float v) {
   const int x = __builtin_bit_cast(int, v);
+  // every lane reads a lane inside its own row, so bound_ctrl never applies;
+  // setting it lets the compiler fold the move into the instruction using it
   if constexpr (kM == 1) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false));
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, true));
   } else if constexpr (kM == 2) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false));
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, true));
   } else if constexpr (kM == 8) {
     // rotation by 8 inside each row of 16 lanes (row_ror:8) is xor 8
-    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0x128, 0xF, 0xF, false));
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0x128, 0xF, 0xF, true));
   } else {
     return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(x, (kM << 10) | 0x1F));
   }
