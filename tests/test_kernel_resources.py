@@ -1,0 +1,72 @@
+"""CPU checks of the decode kernel's resource budget (compiled for gfx950
+here, no GPU needed): the instances launched on grids of several rounds
+must let two 512-thread workgroups share a CU (at most 128 VGPRs, at most
+80 KB of LDS), every instance must fit two waves per SIMD with no scratch,
+and the dynamic LDS the launcher adds to one-round grids must leave room for
+only one workgroup per CU (160 KB of LDS per CU)."""
+
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+from paper_2608_08081_amd import build as B
+
+LDS_PER_CU = 160 * 1024
+
+
+def _device_asm(src, tmp_path):
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available")
+    out = tmp_path / (src + ".s")
+    flags = [f for f in B.COMMON_FLAGS if f not in ("-fPIC",)]
+    cmd = [hipcc, "-x", "hip", *flags, "-I", B.INCLUDE, "-I", B.CSRC, "-S",
+           "--cuda-device-only", os.path.join(B.CSRC, src), "-o", str(out)]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    return out.read_text()
+
+
+def _kernels(asm):
+    """name -> (vgprs, lds bytes, scratch bytes) from the AMDGPU metadata."""
+    res = {}
+    for m in re.finditer(r"^\s+\.group_segment_fixed_size:\s+(\d+)\n(.*?)^\s+\.vgpr_spill_count",
+                         asm, re.S | re.M):
+        block = m.group(0)
+        name = re.search(r"\.name:\s+(\S+)", block).group(1)
+        vg = int(re.search(r"\.vgpr_count:\s+(\d+)", block).group(1))
+        priv = int(re.search(r"\.private_segment_fixed_size:\s+(\d+)", block).group(1))
+        res[name] = (vg, int(m.group(1)), priv)
+    return res
+
+
+def test_decode_g8_occupancy_budget(tmp_path):
+    asm = _device_asm("iq_decode_g8.hip", tmp_path)
+    src = open(os.path.join(B.CSRC, "iq_decode_g8.hip")).read()
+    pad = eval(re.search(r"kOneWorkgroupPadBytes\s*=\s*([^;]+);", src).group(1))
+    ks = _kernels(asm)
+    dec = {n: v for n, v in ks.items() if "decode_g8_kernel" in n}
+    assert len(dec) == 20, sorted(dec)
+    for name, (vg, lds, priv) in dec.items():
+        m = re.search(r"decode_g8_kernelILi(\d)ELb(\d)ELb(\d)EE", name)
+        nb, wide = int(m.group(1)), m.group(3) == "1"
+        assert priv == 0, f"{name}: scratch {priv}"
+        assert vg <= 256, f"{name}: {vg} VGPRs"
+        if wide:
+            assert vg <= 128, f"wide NB={nb}: {vg} VGPRs, two workgroups no longer fit a CU"
+            assert 2 * lds <= LDS_PER_CU, f"wide NB={nb}: {lds} B LDS"
+        else:
+            assert 2 * (lds + pad) > LDS_PER_CU, f"narrow NB={nb}: padding too small"
+            assert lds + pad <= LDS_PER_CU
+
+
+def test_compress_kernel_has_no_scratch(tmp_path):
+    ks = _kernels(_device_asm("iq_compress.hip", tmp_path))
+    comp = {n: v for n, v in ks.items() if "compress_kernel" in n}
+    assert len(comp) == 2
+    for name, (vg, lds, priv) in comp.items():
+        assert priv == 0, f"{name}: scratch {priv}"
+        assert vg <= 256, f"{name}: {vg} VGPRs"
