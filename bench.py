@@ -21,7 +21,12 @@ the default is the one above):
   compress  iq_compress_kv over 4 sequences x 32768 tokens x 8 KV heads, K and
             V, fp16 Student-t(4) entries times log-normal channel scales;
   append8k  batch 1, 32 query heads, 4 KV heads, 8192 compressed tokens, then
-            fused steps that each append one token (48 layer caches cycled).
+            fused steps that each append one token (48 layer caches cycled);
+  baseline32k  the 32K shape above through the reconstruct-then-compute
+            pipeline the packed path replaces (Fig. 1 top): decode attention
+            on an fp16 cache, materialization of the packed cache as fp16
+            (iq_dequantize_kv) and the two chained, next to the packed decode
+            attention on the same caches (48 layers cycled).
 """
 
 from __future__ import annotations
@@ -47,7 +52,8 @@ BYTES_PER_TOKEN_HEAD = 2 * (RECORD + 4)      # K and V: 48-byte record + fp32 sc
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--workload", choices=("step32k", "varlen", "compress", "append8k"),
+    p.add_argument("--workload", choices=("step32k", "varlen", "compress", "append8k",
+                                          "baseline32k"),
                    default="step32k")
     p.add_argument("--steps", type=int, default=None,
                    help="timed steps (default: 4800; varlen 240; compress 20; append8k 1000)")
@@ -63,7 +69,7 @@ def parse():
                    help="also run one plain device copy of this many MiB (counter calibration)")
     a = p.parse_args()
     defaults = {"step32k": (4800, 48), "varlen": (240, 3), "compress": (20, 1),
-                "append8k": (1000, 48)}[a.workload]
+                "append8k": (1000, 48), "baseline32k": (960, 48)}[a.workload]
     if a.steps is None:
         a.steps = defaults[0]
     if a.warmup is None:
@@ -411,6 +417,154 @@ def run_append8k(args, torch, api, synth, dev):
         "appended tokens' inputs and records")
 
 
+def time_graph_sweeps(torch, fn, n_layers, steps, warmup):
+    """fn(li) issues one call for layer li.  Captures one sweep over the layers
+    as a HIP graph, replays it for warm-up, then times replays covering at
+    least `steps` calls with HIP events on the replay stream.  Returns us per
+    call."""
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        for li in range(n_layers):
+            fn(li)
+    torch.cuda.current_stream().wait_stream(stream)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for li in range(n_layers):
+            fn(li)
+    torch.cuda.synchronize()
+    for _ in range(max(1, warmup // n_layers)):
+        g.replay()
+    reps = max(1, -(-steps // n_layers))
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(reps):
+        g.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    return ev0.elapsed_time(ev1) * 1e3 / (reps * n_layers)
+
+
+def run_baseline32k(args, torch, api, synth, dev):
+    """Reconstruct-then-compute (Fig. 1 top) against compressed-space decode
+    (Fig. 1 bottom) at the 32K shape.  Per layer the same seeded fp16 K/V
+    are kept as an fp16 cache and compressed into a packed cache.  Paths:
+      packed       iq_decode_attention on the packed cache;
+      fp16         iq_decode_attention_f16 on the fp16 cache;
+      dequantize   iq_dequantize_kv of the packed cache into one fp16
+                   scratch cache shared by all layers (as a pipeline that
+                   materializes per layer would);
+      reconstruct  dequantize, then iq_decode_attention_f16 on the scratch."""
+    w = synth.WORKLOADS[2]
+    nl = args.layers
+    t = args.context
+    capacity = t
+    print(f"# building {nl} layer caches, packed and fp16 ({t} positions each)",
+          file=sys.stderr, flush=True)
+    quats = api.iq_make_rotation(w.rotation_seed, w.n_kv_heads).to(dev)
+    layers = []
+    for li in range(nl):
+        g = torch.Generator(device=dev)
+        g.manual_seed(args.seed * 100003 + li)
+        scales = [torch.from_numpy(synth.channel_scales(synth.rng(args.seed + li, w.wid, st),
+                                                        w.n_kv_heads)).to(dev)
+                  for st in (0, 1)]
+        k = (torch.randn((w.batch, w.n_kv_heads, t, 128), generator=g, device=dev)
+             * scales[0][None, :, None, :]).half()
+        v = (torch.randn((w.batch, w.n_kv_heads, t, 128), generator=g, device=dev)
+             * scales[1][None, :, None, :]).half()
+        cache = api.alloc_cache(w.batch, w.n_kv_heads, capacity, dev)
+        api.iq_compress_kv(k, v, quats, cache["k_codes"], cache["k_norms"], cache["v_codes"],
+                           cache["v_norms"])
+        cache["seq_lens"].fill_(t)
+        q = torch.randn((w.batch, w.n_q_heads, 128), generator=g, device=dev)
+        layers.append(dict(cache=cache, k=k, v=v, q=q,
+                           out=torch.empty((w.batch, w.n_q_heads, 128), device=dev)))
+    torch.cuda.synchronize()
+    ws = api.alloc_workspace(w.batch, w.n_q_heads, w.n_kv_heads, capacity, dev)
+    ws16 = api.alloc_f16_workspace(w.batch, w.n_q_heads, w.n_kv_heads, capacity, dev)
+    k_s = torch.empty((w.batch, w.n_kv_heads, t, 128), dtype=torch.float16, device=dev)
+    v_s = torch.empty_like(k_s)
+
+    def packed(li):
+        L = layers[li]
+        c = L["cache"]
+        api.iq_decode_attention(L["q"], c["k_codes"], c["k_norms"], c["v_codes"], c["v_norms"],
+                                c["seq_lens"], quats, out=L["out"], workspace=ws,
+                                max_seq_len=capacity)
+
+    def fp16(li):
+        L = layers[li]
+        api.iq_decode_attention_f16(L["q"], L["k"], L["v"], L["cache"]["seq_lens"],
+                                    out=L["out"], workspace=ws16, max_seq_len=capacity)
+
+    def dequantize(li):
+        c = layers[li]["cache"]
+        api.iq_dequantize_kv(c["k_codes"], c["k_norms"], c["v_codes"], c["v_norms"], quats,
+                             n_tokens=t, seq_lens=c["seq_lens"], out_dtype=torch.float16,
+                             k_out=k_s, v_out=v_s)
+
+    def reconstruct(li):
+        dequantize(li)
+        L = layers[li]
+        api.iq_decode_attention_f16(L["q"], k_s, v_s, L["cache"]["seq_lens"], out=L["out"],
+                                    workspace=ws16, max_seq_len=capacity)
+
+    t0 = time.perf_counter()
+    us = {name: time_graph_sweeps(torch, fn, nl, args.steps, args.warmup)
+          for name, fn in (("packed", packed), ("fp16", fp16), ("dequantize", dequantize),
+                           ("reconstruct", reconstruct))}
+    wall = time.perf_counter() - t0
+    pos = w.n_kv_heads * t
+    fp16_bytes = pos * 2 * 128 * 2
+    byts = {"packed": pos * BYTES_PER_TOKEN_HEAD,
+            "fp16": fp16_bytes,
+            "dequantize": pos * BYTES_PER_TOKEN_HEAD + fp16_bytes,
+            "reconstruct": pos * BYTES_PER_TOKEN_HEAD + 2 * fp16_bytes}
+    paths = {}
+    for name in us:
+        gbs = byts[name] / (us[name] * 1e-6) / 1e9
+        paths[name] = {"us_per_call": round(us[name], 3), "algorithmic_bytes": int(byts[name]),
+                       "GB/s": round(gbs, 2), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+    f16_gbs = paths["fp16"]["GB/s"]
+    return {
+        "metric": "32K decode attention µs/call: packed 3-bit (compressed-space) vs fp16 cache "
+                  "vs reconstruct-then-compute",
+        "value": round(us["packed"], 3),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(us["packed"] / 1e3, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u3 codes / f16 cache, f32 accumulate",
+        "data": "synthetic (seeded anisotropic fp16 K/V; packed caches compressed on device)",
+        "config": {"workload": f"decode attention, batch 1, 32 query heads, 4 KV heads, "
+                               f"head_dim 128, context {t}; {nl} distinct layer caches cycled",
+                   "context": t, "layers_cycled": nl},
+        "paths": paths,
+        "speedup_vs_fp16": round(us["fp16"] / us["packed"], 3),
+        "speedup_vs_reconstruct": round(us["reconstruct"] / us["packed"], 3),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": f16_gbs,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(f16_gbs / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "kernel": "iq_decode_attention_f16 = decode_f16_kernel<4> + merge_f16_kernel; "
+                      "algorithmic bytes = 512 B (fp16 K + V) x positions x KV heads",
+            "bytes_per_launch": int(fp16_bytes),
+            "launch_us": round(us["fp16"], 3),
+        },
+        "wall_s": round(wall, 3),
+    }
+
 def cpu_compress_baseline(seconds):
     """The oracle's fp64 compression on a bounded sample of vectors."""
     import numpy as np
@@ -534,7 +688,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     run = {"step32k": run_step32k, "varlen": run_varlen, "compress": run_compress,
-           "append8k": run_append8k}[args.workload]
+           "append8k": run_append8k, "baseline32k": run_baseline32k}[args.workload]
     print(json.dumps(run(args, torch, api, synth, dev)), flush=True)
 
 

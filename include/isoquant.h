@@ -224,6 +224,77 @@ iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, i
                          void* workspace, size_t workspace_bytes, int32_t* status_dev,
                          hipStream_t stream);
 
+/*
+ * Reconstruct-then-compute baseline (Sec. 1, Fig. 1 top)
+ * ------------------------------------------------------
+ * The pipeline the compressed-space path replaces: dequantize the packed
+ * cache and apply R^-1 to every token, materializing fp16 tensors, then run
+ * ordinary attention on them.  These entry points exist so that the two
+ * pipelines can be compared on the same shapes; iq_decode_attention_f16 is
+ * also plain decode attention on an uncompressed fp16 cache.
+ */
+
+/*
+ * iq_dequantize_kv - materialize cache records as original-space vectors
+ * (the "Dequant R^-1" stage of Fig. 1 top): x_hat = s R_g^T C[code] for
+ * every token, with R_g = diag(M_i) H_128 / sqrt(128) the rotation of Eq. 2
+ * and C the codebook of iq_codebook.  Computed in fp32 and rounded once to
+ * the output type.
+ *
+ * k_codes/k_norms, v_codes/v_norms : device, a cache as written by
+ *               iq_compress_kv ([batch][n_kv_heads][capacity][48] uint8 and
+ *               [batch][n_kv_heads][capacity] fp32).  Either side may be NULL
+ *               together with its output; not both.
+ * quats       : device fp32 [n_kv_heads][32][2][4], 16-byte aligned.
+ * seq_lens    : optional device int32 [batch]; when given, output token t of
+ *               sequence b is written only if src_offset + t < seq_lens[b].
+ * k_out/v_out : device [batch][n_kv_heads][n_tokens][128] of `out_dtype`
+ *               (IQ_DTYPE_F16 or IQ_DTYPE_F32), 16-byte aligned; token t
+ *               comes from cache position src_offset + t.  Tokens not written
+ *               keep their contents.
+ * Requires 0 <= src_offset and src_offset + n_tokens <= capacity.
+ * n_tokens == 0 or batch == 0 is a valid no-op.
+ */
+iq_status iq_dequantize_kv(const uint8_t* k_codes, const float* k_norms,
+                           const uint8_t* v_codes, const float* v_norms,
+                           const float* quats, const int32_t* seq_lens,
+                           int64_t batch, int64_t n_kv_heads, int64_t n_tokens,
+                           int64_t head_dim, int64_t capacity, int64_t src_offset,
+                           iq_dtype out_dtype, void* k_out, void* v_out,
+                           hipStream_t stream);
+
+/*
+ * iq_decode_f16_workspace_bytes - device workspace iq_decode_attention_f16
+ * needs for these shapes (split partial results).  0 for invalid shapes.
+ */
+size_t iq_decode_f16_workspace_bytes(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                                     int64_t max_seq_len, int64_t head_dim);
+
+/*
+ * iq_decode_attention_f16 - single-token decode attention on an fp16 cache
+ * (the "GEMM Q K^T, softmax, . V" stages of Fig. 1 top): per query head h of
+ * KV head g = h / (n_q_heads / n_kv_heads),
+ *   o = sum_j softmax_j(scale * q_h . k_j) v_j,   j < seq_lens[b],
+ * split over workgroups (flash-decoding) and merged; fp32 accumulation.
+ *
+ * q        : device fp32 [batch][n_q_heads][128], 16-byte aligned;
+ *            |q_i| * scale must stay below 4e4 (the query is carried as fp16
+ *            hi + lo parts).
+ * k, v     : device fp16 [batch][n_kv_heads][capacity][128], 16-byte aligned
+ *            (e.g. the output of iq_dequantize_kv with n_tokens = capacity).
+ * seq_lens, capacity, max_seq_len, softmax_scale, out : as for
+ *            iq_decode_attention.
+ * workspace : device, >= iq_decode_f16_workspace_bytes(...) bytes, 256-byte
+ *            aligned, contents ignored; calls sharing it must not overlap.
+ * n_q_heads / n_kv_heads must be an integer <= 8 (IQ_ERR_UNSUPPORTED above).
+ */
+iq_status iq_decode_attention_f16(const float* q, const void* k, const void* v,
+                                  const int32_t* seq_lens, int64_t capacity,
+                                  int64_t max_seq_len, int64_t batch, int64_t n_q_heads,
+                                  int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
+                                  float* out, void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream);
+
 #ifdef __cplusplus
 }  /* extern "C" */
 #endif

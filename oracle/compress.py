@@ -117,3 +117,16 @@ def reconstruct(codes, scale, levels, r):
     """Original-space reconstruction x_hat' = s * R^T C[code] (what the
     reconstruct-then-compute path materializes)."""
     return dequantize_rotated(codes, scale, levels) @ np.asarray(r, dtype=np.float64)
+
+
+def reconstruct_kv(packed, norms, rots, levels, d: int = 128):
+    """Materialize a packed cache [B][H_kv][T][d*3/8] with scales [B][H_kv][T]
+    as original-space vectors [B][H_kv][T][d] (fp64): the dequantization and
+    R^T of the reconstruct-then-compute pipeline (Fig. 1 top), one rotation
+    per KV head."""
+    packed = np.asarray(packed)
+    b, h, t, _ = packed.shape
+    out = np.empty((b, h, t, d), dtype=np.float64)
+    for hh in range(h):
+        out[:, hh] = reconstruct(unpack(packed[:, hh], d), norms[:, hh], levels, rots[hh])
+    return out

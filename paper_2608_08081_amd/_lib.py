@@ -50,6 +50,11 @@ _SIGNATURES = {
     "iq_decode_step": (_c_int, [_vp, _vp, _vp, _c_int, _vp, _vp, _vp, _vp, _vp, _c_i64,
                                 _c_i64, _vp, _c_i64, _c_i64, _c_i64, _c_i64, _c_float, _vp,
                                 _vp, _c_size, _vp, _vp]),
+    "iq_dequantize_kv": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _c_i64,
+                                  _c_i64, _c_i64, _c_i64, _c_int, _vp, _vp, _vp]),
+    "iq_decode_f16_workspace_bytes": (_c_size, [_c_i64, _c_i64, _c_i64, _c_i64, _c_i64]),
+    "iq_decode_attention_f16": (_c_int, [_vp, _vp, _vp, _vp, _c_i64, _c_i64, _c_i64, _c_i64,
+                                         _c_i64, _c_i64, _c_float, _vp, _vp, _c_size, _vp]),
 }
 
 _lib = None

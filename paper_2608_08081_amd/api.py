@@ -247,3 +247,90 @@ def iq_decode_step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens
         _ptr(status), _stream(dev))
     _lib.check("iq_decode_step", st)
     return out
+
+
+# ---------------------------------------------------------------------------
+# reconstruct-then-compute baseline (materialized fp16 cache)
+# ---------------------------------------------------------------------------
+
+def iq_dequantize_kv(k_codes, k_norms, v_codes, v_norms, quats, n_tokens=None,
+                     src_offset: int = 0, seq_lens=None, out_dtype=torch.float16,
+                     k_out=None, v_out=None):
+    """Materialize cache positions src_offset .. src_offset + n_tokens - 1 as
+    original-space vectors [B][H_kv][n_tokens][128] of out_dtype (fp16 or
+    fp32).  Either side may be None.  With seq_lens, tokens at or past a
+    sequence's length are not written.  Returns (k_out, v_out)."""
+    ref = k_codes if k_codes is not None else v_codes
+    if ref is None or ref.dim() != 4:
+        raise ValueError("codes must be [batch][n_kv_heads][capacity][48]")
+    b, hkv, cap, _ = ref.shape
+    dev = ref.device
+    if n_tokens is None:
+        n_tokens = cap - src_offset
+    if out_dtype not in (torch.float16, torch.float32):
+        raise TypeError("out_dtype must be torch.float16 or torch.float32")
+    shape = (b, hkv, n_tokens, HEAD_DIM)
+    outs = []
+    for codes, norms, out, name in ((k_codes, k_norms, k_out, "k"), (v_codes, v_norms, v_out, "v")):
+        if codes is None:
+            outs.append(None)
+            continue
+        _require(codes, f"{name}_codes", torch.uint8, (b, hkv, cap, RECORD_BYTES), dev)
+        _require(norms, f"{name}_norms", torch.float32, (b, hkv, cap), dev)
+        if out is None:
+            out = torch.empty(shape, dtype=out_dtype, device=dev)
+        _require(out, f"{name}_out", out_dtype, shape, dev)
+        outs.append(out)
+    _require(quats, "quats", torch.float32, (hkv, 32, 2, 4), dev)
+    if seq_lens is not None:
+        _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
+    code = _lib.IQ_DTYPE_F16 if out_dtype == torch.float16 else _lib.IQ_DTYPE_F32
+    st = _lib.lib().iq_dequantize_kv(
+        _ptr(k_codes), _ptr(k_norms), _ptr(v_codes), _ptr(v_norms), _ptr(quats), _ptr(seq_lens),
+        b, hkv, n_tokens, HEAD_DIM, cap, src_offset, code, _ptr(outs[0]), _ptr(outs[1]),
+        _stream(dev))
+    _lib.check("iq_dequantize_kv", st)
+    return outs[0], outs[1]
+
+
+def iq_decode_f16_workspace_bytes(batch, n_q_heads, n_kv_heads, max_seq_len) -> int:
+    return int(_lib.lib().iq_decode_f16_workspace_bytes(batch, n_q_heads, n_kv_heads,
+                                                        max_seq_len, HEAD_DIM))
+
+
+def alloc_f16_workspace(batch, n_q_heads, n_kv_heads, max_seq_len, device):
+    nbytes = iq_decode_f16_workspace_bytes(batch, n_q_heads, n_kv_heads, max_seq_len)
+    if nbytes <= 0:
+        raise ValueError("unsupported decode shape")
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def iq_decode_attention_f16(q, k, v, seq_lens, out=None, workspace=None, max_seq_len=None,
+                            softmax_scale: float = 0.0):
+    """Decode attention on an fp16 cache k, v [B][H_kv][capacity][128]; q
+    [B][H_q][128] fp32.  Returns out [B][H_q][128] fp32."""
+    if q.dim() != 3 or q.shape[-1] != HEAD_DIM:
+        raise ValueError("q must be [batch][n_q_heads][128]")
+    b, hq, _ = q.shape
+    dev = q.device
+    _require(q, "q", torch.float32, (b, hq, HEAD_DIM), dev)
+    if k.dim() != 4:
+        raise ValueError("k must be [batch][n_kv_heads][capacity][128]")
+    _, hkv, cap, _ = k.shape
+    _require(k, "k", torch.float16, (b, hkv, cap, HEAD_DIM), dev)
+    _require(v, "v", torch.float16, (b, hkv, cap, HEAD_DIM), dev)
+    _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
+    if max_seq_len is None:
+        max_seq_len = cap
+    if out is None:
+        out = torch.empty((b, hq, HEAD_DIM), dtype=torch.float32, device=dev)
+    _require(out, "out", torch.float32, (b, hq, HEAD_DIM), dev)
+    if workspace is None:
+        workspace = alloc_f16_workspace(b, hq, hkv, max_seq_len, dev)
+    if workspace.dtype != torch.uint8 or workspace.device != dev or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 device tensor")
+    st = _lib.lib().iq_decode_attention_f16(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(seq_lens), cap, max_seq_len, b, hq, hkv, HEAD_DIM,
+        float(softmax_scale), _ptr(out), _ptr(workspace), workspace.numel(), _stream(dev))
+    _lib.check("iq_decode_attention_f16", st)
+    return out

@@ -150,7 +150,7 @@ const char* iq_status_string(iq_status s) {
   return "IQ_ERR_UNKNOWN";
 }
 
-int iq_version(void) { return 101; }
+int iq_version(void) { return 102; }
 
 iq_status iq_codebook(float* levels, float* thresholds) {
   const iq::Codebook& cb = iq::codebook();
@@ -331,6 +331,74 @@ iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, i
                                          capacity, max_seq_len, quats, batch, n_q_heads,
                                          n_kv_heads, resolve_scale(softmax_scale), out, workspace,
                                          &append, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+iq_status iq_dequantize_kv(const uint8_t* k_codes, const float* k_norms,
+                           const uint8_t* v_codes, const float* v_norms, const float* quats,
+                           const int32_t* seq_lens, int64_t batch, int64_t n_kv_heads,
+                           int64_t n_tokens, int64_t head_dim, int64_t capacity,
+                           int64_t src_offset, iq_dtype out_dtype, void* k_out, void* v_out,
+                           hipStream_t stream) {
+  if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
+  if (out_dtype != IQ_DTYPE_F32 && out_dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
+  if (batch < 0 || n_kv_heads <= 0 || n_tokens < 0 || capacity < 0 || src_offset < 0)
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (src_offset > capacity || n_tokens > capacity - src_offset) return IQ_ERR_INVALID_ARGUMENT;
+  if (!iq::mul_ok(batch, n_kv_heads) || !iq::mul_ok(batch * n_kv_heads, capacity + 1) ||
+      !iq::mul_ok(batch * n_kv_heads * (capacity + 1), kDim))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (batch == 0 || n_tokens == 0) return IQ_OK;
+  if (k_codes == nullptr && v_codes == nullptr) return IQ_ERR_INVALID_ARGUMENT;
+  if (quats == nullptr || !iq::aligned(quats, 16)) return IQ_ERR_INVALID_ARGUMENT;
+  if (seq_lens && !iq::aligned(seq_lens, 4)) return IQ_ERR_INVALID_ARGUMENT;
+  if (k_codes && (!k_norms || !k_out || !iq::aligned(k_codes, 4) || !iq::aligned(k_norms, 4) ||
+                  !iq::aligned(k_out, 16)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (v_codes && (!v_norms || !v_out || !iq::aligned(v_codes, 4) || !iq::aligned(v_norms, 4) ||
+                  !iq::aligned(v_out, 16)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  const hipError_t e = iq::launch_dequant(k_codes, k_norms, v_codes, v_norms, quats, seq_lens,
+                                          batch, n_kv_heads, n_tokens, capacity, src_offset,
+                                          out_dtype == IQ_DTYPE_F16 ? 1 : 0, k_out, v_out,
+                                          stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+size_t iq_decode_f16_workspace_bytes(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                                     int64_t max_seq_len, int64_t head_dim) {
+  if (head_dim != kDim || batch < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || max_seq_len < 0)
+    return 0;
+  if (n_q_heads % n_kv_heads || n_q_heads / n_kv_heads > 8) return 0;
+  return iq::f16_workspace_bytes(batch, n_kv_heads, max_seq_len);
+}
+
+iq_status iq_decode_attention_f16(const float* q, const void* k, const void* v,
+                                  const int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                                  int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                                  int64_t head_dim, float softmax_scale, float* out,
+                                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
+  if (batch < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || capacity < 0 || max_seq_len < 0 ||
+      max_seq_len > capacity || capacity > 0x7fffffff || batch > 0xffffff)
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (n_q_heads % n_kv_heads) return IQ_ERR_INVALID_ARGUMENT;
+  if (n_q_heads / n_kv_heads > 8) return IQ_ERR_UNSUPPORTED;
+  if (!iq::mul_ok(batch, n_kv_heads) || !iq::mul_ok(batch * n_kv_heads, capacity + 1) ||
+      !iq::mul_ok(batch * n_kv_heads * (capacity + 1), kDim) ||
+      !iq::mul_ok(batch, n_q_heads) || batch * n_q_heads > 0x7fffffff)
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (!q || !k || !v || !seq_lens || !out || !workspace) return IQ_ERR_INVALID_ARGUMENT;
+  if (!iq::aligned(q, 16) || !iq::aligned(k, 16) || !iq::aligned(v, 16) ||
+      !iq::aligned(out, 16) || !iq::aligned(seq_lens, 4) || !iq::aligned(workspace, 256))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < iq::f16_workspace_bytes(batch, n_kv_heads, max_seq_len))
+    return IQ_ERR_WORKSPACE_TOO_SMALL;
+  if (batch == 0) return IQ_OK;
+  const hipError_t e = iq::launch_decode_f16(
+      q, static_cast<const __half*>(k), static_cast<const __half*>(v), seq_lens, capacity,
+      max_seq_len, batch, n_kv_heads, n_q_heads / n_kv_heads, resolve_scale(softmax_scale), out,
+      static_cast<float*>(workspace), stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 

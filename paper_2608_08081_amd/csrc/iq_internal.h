@@ -2,6 +2,7 @@
 // kernel translation units.  Not installed; the public ABI is isoquant.h.
 #pragma once
 
+#include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -84,5 +85,21 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                             const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
                             float* out, float* partials, const StepAppend* append,
                             hipStream_t stream);
+
+// Reconstruct-then-compute baseline (Fig. 1 top): materialize the packed
+// cache as fp16 or fp32 vectors, and decode attention on an fp16 cache.
+hipError_t launch_dequant(const uint8_t* k_codes, const float* k_norms, const uint8_t* v_codes,
+                          const float* v_norms, const float* quats, const int32_t* seq_lens,
+                          int64_t batch, int64_t n_heads, int64_t n_tokens, int64_t capacity,
+                          int64_t src_offset, int out_f16, void* k_out, void* v_out,
+                          hipStream_t stream);
+
+void f16_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
+              int64_t* n_splits, int64_t* split_len);
+size_t f16_workspace_bytes(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len);
+hipError_t launch_decode_f16(const float* q, const __half* k, const __half* v,
+                             const int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                             int64_t batch, int64_t n_kv_heads, int64_t group, float scale,
+                             float* out, float* partials, hipStream_t stream);
 
 }  // namespace iq

@@ -171,3 +171,56 @@ def test_step_validation():
     assert _step(status=ctypes.c_void_p(0x100002)) == 1
     assert _step(wsb=16) == 3
     assert _step(batch=0) == 0
+
+
+def _dequant(**kw):
+    args = dict(kc=A, kn=A, vc=B, vn=B, quats=A, seq=None, batch=1, heads=2, n=10, hd=128,
+                cap=16, off=0, dtype=1, ko=A, vo=B)
+    args.update(kw)
+    return L.iq_dequantize_kv(args["kc"], args["kn"], args["vc"], args["vn"], args["quats"],
+                              args["seq"], args["batch"], args["heads"], args["n"], args["hd"],
+                              args["cap"], args["off"], args["dtype"], args["ko"], args["vo"],
+                              None)
+
+
+def test_dequantize_validation():
+    assert _dequant(hd=64) == 2
+    assert _dequant(dtype=5) == 2
+    assert _dequant(kc=None, vc=None) == 1
+    assert _dequant(quats=None) == 1
+    assert _dequant(ko=None) == 1
+    assert _dequant(vn=None) == 1
+    assert _dequant(n=17) == 1                  # beyond capacity
+    assert _dequant(off=7) == 1                 # 7 + 10 > 16
+    assert _dequant(off=-1) == 1
+    assert _dequant(heads=0) == 1
+    assert _dequant(ko=ctypes.c_void_p(0x100008)) == 1   # output not 16-byte aligned
+    assert _dequant(seq=ctypes.c_void_p(0x100002)) == 1
+    assert _dequant(n=0) == 0
+    assert _dequant(batch=0) == 0
+
+
+def _decode_f16(**kw):
+    args = dict(q=A, k=A, v=B, seq=A, cap=1024, maxlen=1024, batch=1, hq=32, hkv=4, hd=128,
+                scale=0.0, out=B, ws=A, wsb=1 << 30)
+    args.update(kw)
+    return L.iq_decode_attention_f16(args["q"], args["k"], args["v"], args["seq"], args["cap"],
+                                     args["maxlen"], args["batch"], args["hq"], args["hkv"],
+                                     args["hd"], args["scale"], args["out"], args["ws"],
+                                     args["wsb"], None)
+
+
+def test_decode_f16_validation():
+    assert _decode_f16(hd=64) == 2
+    assert _decode_f16(hq=36) == 2              # group 9 > 8
+    assert _decode_f16(hq=30) == 1
+    assert _decode_f16(maxlen=2048) == 1
+    assert _decode_f16(k=None) == 1
+    assert _decode_f16(out=ctypes.c_void_p(0x100004)) == 1
+    assert _decode_f16(ws=ctypes.c_void_p(0x100040)) == 1
+    assert _decode_f16(wsb=16) == 3
+    assert _decode_f16(batch=0) == 0
+    n = L.iq_decode_f16_workspace_bytes(1, 32, 4, 32768, 128)
+    assert n > 0 and n % 256 == 0
+    assert L.iq_decode_f16_workspace_bytes(1, 36, 4, 32768, 128) == 0
+    assert L.iq_decode_f16_workspace_bytes(1, 32, 4, 32768, 64) == 0

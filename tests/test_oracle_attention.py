@@ -144,3 +144,30 @@ def test_needle_argmax_survives_compression():
         assert int(np.argmax(s)) == int(pos[0, g])
         exact = k[0, g].astype(np.float64) @ q[0, h0].astype(np.float64)
         assert int(np.argmax(exact)) == int(pos[0, g])
+
+
+def test_exact_attention_matches_library_attention():
+    """The unquantized-cache attention (the fp16 baseline's reference, Fig. 1
+    top after materialization) against PyTorch's CPU scaled-dot-product
+    attention in fp64, grouped query heads expanded per KV head, ragged
+    lengths, one empty sequence and a non-default scale."""
+    torch = pytest.importorskip("torch")
+    g = np.random.default_rng(9)
+    b, hkv, grp, cap = 3, 2, 4, 40
+    k = g.standard_normal((b, hkv, cap, 128)) * 3.0
+    v = g.standard_normal((b, hkv, cap, 128))
+    q = g.standard_normal((b, hkv * grp, 128))
+    lens = [40, 17, 0]
+    for scale in (None, 0.2):
+        got = att.attention_exact(q, k, v, lens, hkv, scale)
+        for bb in range(b):
+            n = lens[bb]
+            if n == 0:
+                assert np.all(got[bb] == 0)
+                continue
+            kt = torch.from_numpy(k[bb, :, :n]).repeat_interleave(grp, dim=0)
+            vt = torch.from_numpy(v[bb, :, :n]).repeat_interleave(grp, dim=0)
+            qt = torch.from_numpy(q[bb])[:, None, :]
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                qt, kt, vt, scale=scale)[:, 0, :].numpy()
+            np.testing.assert_allclose(got[bb], ref, rtol=0, atol=1e-12)

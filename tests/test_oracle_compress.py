@@ -153,3 +153,30 @@ def test_eq3_inner_product_error_statement():
     derived = sigma2 * np.dot(q, q)
     assert 0.8 * derived < err2 < 1.2 * derived
     assert err2 <= d * sigma2 * np.dot(q, q)
+
+
+def test_reconstruct_inverts_the_forward_rotation():
+    """The materialized vector is s R^T C[code]: rotating it forward with the
+    compression's own Step 2 gives back s C[code] (so a transposed R in the
+    reconstruction fails), and its norm is s ||C[code]|| (R orthogonal)."""
+    g = np.random.default_rng(5)
+    d = 128
+    quats = rot.make_quaternions(21, 2)
+    rots = rot.rotation_matrices(quats)
+    codes = g.integers(0, 8, size=(1, 2, 6, d)).astype(np.uint8)
+    norms = g.uniform(0.5, 40.0, size=(1, 2, 6)).astype(np.float32)
+    packed = cz.pack(codes)
+    x = cz.reconstruct_kv(packed, norms, rots, LEVELS)
+    for hh in range(2):
+        back = cz.rotate(x[0, hh], rots[hh])
+        want = norms[0, hh].astype(np.float64)[:, None] * np.asarray(LEVELS)[codes[0, hh]]
+        np.testing.assert_allclose(back, want, rtol=0, atol=1e-12 * np.max(np.abs(want)))
+        np.testing.assert_allclose(np.linalg.norm(x[0, hh], axis=1),
+                                   np.linalg.norm(want, axis=1), rtol=1e-13)
+    # compressing the reconstruction again: Step 2 of the unit vector gives
+    # C[code] / ||C[code]||, and Step 3 quantizes exactly that
+    _, n2, c2, y2, _ = cz.compress(x[0, 0], rots[0], THR)
+    lv = np.asarray(LEVELS)[codes[0, 0]] / np.linalg.norm(np.asarray(LEVELS)[codes[0, 0]],
+                                                          axis=1, keepdims=True)
+    np.testing.assert_allclose(y2, lv, rtol=0, atol=1e-13)
+    assert np.array_equal(c2, cz.quantize(lv, THR))
