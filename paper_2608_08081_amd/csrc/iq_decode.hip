@@ -279,7 +279,8 @@ bool plan_decode(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads, int64_t m
     p.g8_batches = nb;
     p.g8_splits = splits;
     p.g8_split_len = len;
-    p.g8_partial_bytes = round256(static_cast<size_t>(batch) * n_kv_heads * splits * 8 *
+    // one partial per split, and one for the fused step's new token
+    p.g8_partial_bytes = round256(static_cast<size_t>(batch) * n_kv_heads * (splits + 1) * 8 *
                                   kPartialFloats * 4);
     if (p.g8_partial_bytes > need) need = p.g8_partial_bytes;
   }
@@ -300,9 +301,13 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, uint8_t* k_code
   const bool aligned16 = (reinterpret_cast<uintptr_t>(k_norms) % 16 == 0) &&
                          (reinterpret_cast<uintptr_t>(v_norms) % 16 == 0);
   // the group-8 kernel addresses one (sequence, KV head) row with 32-bit
-  // byte offsets
+  // byte offsets, loads whole batches of 16 positions below max_seq_len
+  // (clamped to the row: capacity a multiple of 16, at least 16), and takes
+  // KV heads and sequences as grid dimensions (at most 65535 each)
   const bool row32 = capacity * kRecordBytes <= 0x7fffffff;
-  if (group == 8 && plan.g8_batches > 0 && capacity % 16 == 0 && aligned16 && row32) {
+  const bool grid_ok = batch <= 65535 && n_kv_heads <= 65535;
+  if (group == 8 && plan.g8_batches > 0 && capacity % 16 == 0 && capacity >= 16 && aligned16 &&
+      row32 && grid_ok) {
     float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
     return launch_decode_g8(plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes,
                             k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len, quats,

@@ -2,14 +2,16 @@
 // KV head (App. A; Table 2 A-D; Sec. 3.4), gfx950.
 //
 // Work decomposition: one 512-thread workgroup (8 waves, two per SIMD) per
-// (sequence b, KV head g, split of 16 * nbat positions); the split's nbat
-// batches of 16 positions are dealt to the 8 waves in contiguous runs of
-// nbat / 8 or nbat / 8 + 1 batches.  With one workgroup per CU the SIMDs
-// carry equal work.  Every load of a wave (query, rotation parameters, then
-// keys, value scales and values of all its batches, in the order they are
-// used) is issued before any arithmetic from one straight-line sequence, so
-// each later wait covers only the data it needs and the waves compute while
-// the rest of the cache is still arriving.
+// (split of 16 * nbat positions, KV head g, sequence b), the grid's three
+// dimensions; the split's nbat batches of 16 positions are dealt to the 8
+// waves in contiguous runs of nbat / 8 or nbat / 8 + 1 batches.  With one
+// workgroup per CU the SIMDs carry equal work.  A wave's loads (query,
+// rotation parameters, both scale arrays and the keys of all its batches,
+// then each batch's values as its scores start) are issued in the order the
+// data is used, so each wait covers only the data it needs and the waves
+// compute while the rest of the cache is still arriving.  In grids of one
+// round the loads do not wait for the sequence length (see the kernel).
+// The fused step adds one workgroup per (b, g) for the new token.
 //
 // The two contractions of a batch are dense 8-head x 128-dim x 16-position
 // products and run on the matrix cores (v_mfma_f32_16x16x32_f16):
@@ -419,13 +421,21 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
   m_run *= qdown;
 }
 
-// kAppend: the fused decode step.  The new key and value of every (sequence
-// b, KV head g) are compressed (Alg. 1) and written at position seq_lens[b]
-// by the workgroup whose split holds that position; that workgroup's waves
-// attend the positions before it, and the new token's score and value, taken
-// from the fresh record, join in the workgroup merge.  seq_lens is advanced
-// by the merge kernel (or by advance_lengths_kernel for a single split),
-// after every workgroup has read it.
+// Grid (split, KV head g, sequence b).  The attention workgroups attend the
+// positions before min(seq_lens[b], max_seq_len); their work split does not
+// depend on the length, so every cache load is addressed from the split
+// range alone (clamped to max_seq_len, hence inside the capacity) and issued
+// before the length is read; positions at or past the length are masked.
+// With several splits each workgroup writes its partial (m, l, O) per head;
+// with one it writes the output row itself.
+//
+// kAppend, the fused decode step: one more workgroup per (b, g), split index
+// n_splits, compresses the new key and value (Alg. 1), writes their records
+// at position seq_lens[b] and publishes the new token's score and value as
+// the partial of that extra split (m = -inf when the token is not attended:
+// at capacity, or at or past max_seq_len).  No attention workgroup reads the
+// records being written, and seq_lens is advanced by the merge kernel after
+// every workgroup has read it.
 template <int NB, bool kAppend, bool kWide>
 __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     const float* __restrict__ q, uint8_t* __restrict__ k_codes, float* __restrict__ k_norms,
@@ -442,7 +452,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     uint32_t qop[2][kHeads][kQRowWords];
     int qexp[kHeads];
     float wave_ml[kWaves][2][kHeads];
-    uint32_t new_rec[2][kRecordWords];   // kAppend: the new key / value record
+    uint32_t new_rec[2][kRecordWords];   // append workgroup: the new key / value record
     float new_scale[2];
     // the waves' staging areas while attending, their outputs afterwards
     // (wave_o[w][r][lane] = the lane's accumulator entries r of the four
@@ -457,8 +467,6 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   uint32_t(*qop)[kHeads][kQRowWords] = sm.qop;
   int* qexp_s = sm.qexp;
   float(*wave_ml)[2][kHeads] = sm.wave_ml;
-  uint32_t(*new_rec)[kRecordWords] = sm.new_rec;
-  float* new_scale = sm.new_scale;
   WaveStage* stage = sm.stage;
   f32x4_t(*wave_o)[4][64] = sm.wave_o;
 
@@ -469,17 +477,15 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   const int lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
 
-  const int split = blockIdx.x % n_splits;
-  const int bg = blockIdx.x / n_splits;
-  const int g = bg % n_kv_heads;
-  const int b = bg / n_kv_heads;
+  const int split = blockIdx.x;
+  const int g = blockIdx.y;
+  const int b = blockIdx.z;
+  const int bg = b * n_kv_heads + g;
   const int n_q_heads = n_kv_heads * kHeads;
+  const int n_parts = kAppend ? n_splits + 1 : n_splits;
 
-  // The query and rotation loads go out first: they do not depend on the
-  // sequence length, so they are issued while it is read, and loads complete
-  // in issue order, so waiting for them never waits for the cache loads.
-  // Thread (head qh, SO(4) block qblk) for tid < 256; the other waves load
-  // the same query and parameters (no branch around loads).
+  // The query and rotation loads go out first (thread (head qh, SO(4) block
+  // qblk) for tid < 256; the other waves load the same values).
   const int qh = (tid >> 5) & 7, qblk = tid & 31;
   const f32x4_t qv = *reinterpret_cast<const f32x4_t*>(
       q + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * kHeads + qh) * kDim +
@@ -487,104 +493,139 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   const f32x4_t* qpar = reinterpret_cast<const f32x4_t*>(
       quats + static_cast<int64_t>(g) * kQuatFloats + 8 * qblk);
   const f32x4_t ql = qpar[0], qr = qpar[1];
-  __builtin_amdgcn_sched_barrier(0);
-
-  const int seq0 = seq_lens[b];
-  int seq = seq0;
-  bool appended = false;   // kAppend: the new token goes to position seq0
-  if constexpr (kAppend) {
-    appended = seq0 >= 0 && seq0 < capacity;
-    if (appended) seq = seq0 + 1;
-    if (!appended && status != nullptr && g == 0 && split == 0 && tid == 0)
-      atomicOr(status, static_cast<int32_t>(IQ_ERR_CAPACITY));
-  }
-  seq = seq > max_seq_len ? max_seq_len : (seq < 0 ? 0 : seq);
-  const int used = (seq + split_len - 1) / split_len;
   float* out_bg =
       out + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * kHeads) * kDim;
-  float* part_bg = partials + static_cast<int64_t>(bg) * n_splits * (kHeads * kPart);
-  if (split >= used) {
-    // nothing to attend: with several splits, an empty partial (m = -inf)
-    // for the merge; with one, a zero output row for an empty sequence
-    if (n_splits > 1) {
-      if (tid < kHeads)
-        part_bg[static_cast<int64_t>(split) * (kHeads * kPart) + tid * kPart] = -INFINITY;
-    } else {
-      for (int e = tid; e < kHeads * kDim; e += kThreads) out_bg[e] = 0.f;
-    }
-    return;
-  }
-  // the workgroup writing the new record: the split holding position seq0
-  // (or, if seq0 lies beyond max_seq_len, the last attended split)
-  const bool writer =
-      kAppend && appended && split == (seq0 < max_seq_len ? seq0 : max_seq_len - 1) / split_len;
-  const int start = split * split_len;
-  // the appended token (position seq0 = the split's last attended position)
-  // is not read back from the cache: its score and value come from the new
-  // record directly, merged with the waves' results below
-  const bool new_attended = writer && seq0 < max_seq_len;
-  int end = seq < start + split_len ? seq : start + split_len;
-  if (new_attended) end = seq0;
-  // this wave's run of batches: nbat / n_att each, one more for the first
-  // nbat % n_att waves, over the n_att attending waves (all 8, or in the
-  // writer workgroup the 7 that do not compress the new token, so that the
-  // compression runs beside the attention rather than before it)
-  constexpr int kCompressWave = kWaves - 1;
-  const int nbat = split_len >> 4;
-  const int n_att = (kAppend && writer) ? kWaves - 1 : kWaves;
-  const bool att_wave = wave < n_att;
-  const int nb_base = nbat / n_att, nb_rem = nbat % n_att;
-  const int nb_w = att_wave ? nb_base + (wave < nb_rem ? 1 : 0) : 0;
-  const int wbase =
-      start + (att_wave ? 16 * (wave * nb_base + (wave < nb_rem ? wave : nb_rem)) : 0);
-  int nvalid = end - wbase;   // this wave's positions (may be <= 0)
-  nvalid = nvalid < 16 * nb_w ? nvalid : 16 * nb_w;
-  // start of the wave's last batch holding positions (clamp of the loads)
-  int clamp16 = ((end > 0 ? end - 1 : 0) & ~15);
-  clamp16 = clamp16 < wbase + 16 * (nb_w - 1) ? clamp16 : wbase + 16 * (nb_w - 1);
-  clamp16 = clamp16 > 0 ? clamp16 : 0;
-  // (b, g) row bases (scalars); lane offsets in 32 bits (capacity * 48 < 2^31)
+  float* part_bg = partials + static_cast<int64_t>(bg) * n_parts * (kHeads * kPart);
   const int64_t row = static_cast<int64_t>(bg) * capacity;
   uint8_t* kc = k_codes + row * kRecordBytes;
   uint8_t* vc = v_codes + row * kRecordBytes;
+
+  if (kAppend && split == n_splits) {
+    // ---- the append workgroup ------------------------------------------------
+    const int seq0 = seq_lens[b];
+    const bool appended = seq0 >= 0 && seq0 < capacity;
+    const bool attend_new = appended && seq0 < max_seq_len;
+    if (!appended && status != nullptr && g == 0 && tid == 0)
+      atomicOr(status, static_cast<int32_t>(IQ_ERR_CAPACITY));
+    // waves 4 and 5 compress the new key and value: lane l holds dims 2l,
+    // 2l + 1 and the parameters of SO(4) block l / 2
+    if (wave == 4 || wave == 5) {
+      const void* src = wave == 4 ? k_new : v_new;
+      const int64_t off = (static_cast<int64_t>(b) * n_kv_heads + g) * kDim;
+      float x0, x1;
+      if (new_f16) {
+        const uint32_t w = reinterpret_cast<const uint32_t*>(static_cast<const __half*>(src) +
+                                                             off)[lane];
+        x0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w)));
+        x1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16)));
+      } else {
+        const f32x2_t w =
+            reinterpret_cast<const f32x2_t*>(static_cast<const float*>(src) + off)[lane];
+        x0 = w[0];
+        x1 = w[1];
+      }
+      const f32x4_t* qs = reinterpret_cast<const f32x4_t*>(
+          quats + static_cast<int64_t>(g) * kQuatFloats + 8 * (lane >> 1));
+      const f32x4_t p0 = qs[0], p1 = qs[1];
+      const float qp[8] = {p0[0], p0[1], p0[2], p0[3], p1[0], p1[1], p1[2], p1[3]};
+      const WaveCode wc = compress_vector_wave(x0, x1, qp, cb, lane);
+      const int which = wave - 4;
+      if (lane < kRecordWords) sm.new_rec[which][lane] = wc.word;
+      if (lane == 0) sm.new_scale[which] = wc.scale;
+      if (appended) {
+        uint8_t* codes = which == 0 ? kc : vc;
+        float* norms = (which == 0 ? k_norms : v_norms) + row;
+        if (lane < kRecordWords)
+          reinterpret_cast<uint32_t*>(codes + static_cast<int64_t>(seq0) * kRecordBytes)[lane] =
+              wc.word;
+        if (lane == 0) norms[seq0] = wc.scale;
+      }
+    }
+    if (tid < 64) {
+      const uint32_t lo =
+          __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & 7)));
+      const uint32_t hi =
+          __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> 3)));
+      lut[tid] = lo | (hi << 16);
+    }
+    f32x4_t y = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (tid < kRotThreads) y = rotate_forward(qv, ql, qr, qblk, kInvSqrtDim * qscale);
+    lds_barrier();   // new_rec, new_scale, lut
+    if (tid >= kRotThreads) return;
+    // score of the new key for head qh: s^K (q_tilde . C[code]) over this
+    // thread's dims 4 qblk .. +3, summed over the head's 32 lanes (y already
+    // carries the score scale, in log2 units)
+    const int md = 4 * qblk;
+    const f32x4_t k4 = decode_record_dims(sm.new_rec[0], lut, md);
+    const f32x4_t v4 = decode_record_dims(sm.new_rec[1], lut, md);
+    float dot = y[0] * k4[0] + y[1] * k4[1] + y[2] * k4[2] + y[3] * k4[3];
+    dot += xor_lane<1>(dot);
+    dot += xor_lane<2>(dot);
+    dot += xor_lane<4>(dot);
+    dot += xor_lane<8>(dot);
+    dot += xor_lane<16>(dot);
+    float* pp = part_bg + static_cast<int64_t>(n_splits) * (kHeads * kPart) + qh * kPart;
+    if (qblk == 0) {
+      pp[0] = attend_new ? dot * sm.new_scale[0] : -INFINITY;
+      pp[1] = 1.0f;
+    }
+    *reinterpret_cast<f32x4_t*>(pp + 2 + md) = sm.new_scale[1] * v4;
+    return;
+  }
+
+  // ---- attention workgroups -------------------------------------------------
+  // this wave's run of batches: nbat / 8 each, one more for the first
+  // nbat % 8 waves
+  const int start = split * split_len;
+  const int nbat = split_len >> 4;
+  const int nb_base = nbat / kWaves, nb_rem = nbat % kWaves;
+  const int nb_w = nb_base + (wave < nb_rem ? 1 : 0);
+  const int wbase = start + 16 * (wave * nb_base + (wave < nb_rem ? wave : nb_rem));
+  // Grids of one round (at most one workgroup per CU) are bound by latency:
+  // their loads are addressed from the split range clamped to max_seq_len
+  // and go out before the length is read.  Grids of several rounds read the
+  // length first and skip splits past it, whose loads would take bandwidth
+  // from the other workgroups.
+  int seq0 = 0;
+  int lim = start + split_len < max_seq_len ? start + split_len : max_seq_len;
+  if constexpr (kWide) {
+    seq0 = seq_lens[b];
+    const int seq_w = seq0 < 0 ? 0 : (seq0 > max_seq_len ? max_seq_len : seq0);
+    if (start >= seq_w) {
+      // nothing to attend: an empty partial (m = -inf) for the merge, or a
+      // zero output row for an empty sequence
+      if (n_parts > 1) {
+        if (tid < kHeads)
+          part_bg[static_cast<int64_t>(split) * (kHeads * kPart) + tid * kPart] = -INFINITY;
+      } else {
+        for (int e = tid; e < kHeads * kDim; e += kThreads) out_bg[e] = 0.f;
+      }
+      return;
+    }
+    lim = lim < seq_w ? lim : seq_w;
+  }
+  // start of the wave's last batch before lim (the clamp of the loads):
+  // lim <= max_seq_len <= capacity, a multiple of 16, so every loaded batch
+  // lies in the row
+  int clamp16 = (lim > 0 ? lim - 1 : 0) & ~15;
+  clamp16 = clamp16 < wbase + 16 * (nb_w - 1) ? clamp16 : wbase + 16 * (nb_w - 1);
+  clamp16 = clamp16 > 0 ? clamp16 : 0;
   const float* kn = k_norms + row;
   const float* vn = v_norms + row;
 
-  // kAppend, writer workgroup: the last wave, which attends no positions,
-  // compresses the new key and value (the records are needed only in the
-  // workgroup merge)
-  // the new key and value stay raw (dims 2 lane, 2 lane + 1: one fp16 pair
-  // word, or two fp32 words) until they are compressed, so that no wait for
-  // them is placed before the cache loads
-  uint32_t nkr[2] = {0u, 0u}, nvr[2] = {0u, 0u};
-  float nqp[8];
-  const bool compressing = writer && wave == kCompressWave;
-  if (compressing) {
-    const int64_t off = (static_cast<int64_t>(b) * n_kv_heads + g) * kDim;
-    if (new_f16) {
-      nkr[0] = reinterpret_cast<const uint32_t*>(static_cast<const __half*>(k_new) + off)[lane];
-      nvr[0] = reinterpret_cast<const uint32_t*>(static_cast<const __half*>(v_new) + off)[lane];
-    } else {
-      const u32x2_a4_t kr =
-          reinterpret_cast<const u32x2_a4_t*>(static_cast<const float*>(k_new) + off)[lane];
-      const u32x2_a4_t vr =
-          reinterpret_cast<const u32x2_a4_t*>(static_cast<const float*>(v_new) + off)[lane];
-      nkr[0] = kr[0]; nkr[1] = kr[1];
-      nvr[0] = vr[0]; nvr[1] = vr[1];
-    }
-    const f32x4_t* qs = reinterpret_cast<const f32x4_t*>(
-        quats + static_cast<int64_t>(g) * kQuatFloats + 8 * (lane >> 1));
-    const f32x4_t p0 = qs[0], p1 = qs[1];
-    nqp[0] = p0[0]; nqp[1] = p0[1]; nqp[2] = p0[2]; nqp[3] = p0[3];
-    nqp[4] = p1[0]; nqp[5] = p1[1]; nqp[6] = p1[2]; nqp[7] = p1[3];
-  }
-
-  // ---- the cache loads (keys now, values after the barrier below) ----------
+  // ---- the cache loads (keys and scales now, values as the scores proceed)
   uint32_t kw[NB][3], vw[NB][3];
   f32x4_t ksl, vsl;
   load_keys<NB>(kc, kn, vn, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
   const int vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
   const uint32_t vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));   // 0..40
+
+  // one-round grids: the length, read once the loads are in flight
+  if constexpr (!kWide) seq0 = seq_lens[b];
+  const int seq = seq0 < 0 ? 0 : (seq0 > max_seq_len ? max_seq_len : seq0);
+  const int end = seq < start + split_len ? seq : start + split_len;
+  int nvalid = end - wbase;   // this wave's positions (may be <= 0)
+  nvalid = nvalid < 16 * nb_w ? nvalid : 16 * nb_w;
 
   // ---- while the loads fly: LUT and the rotated query --------------------
   if (tid < 64) {
@@ -596,9 +637,8 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   }
   // the 32 blocks of a head are 32 consecutive lanes of one wave, so the
   // rotation needs no barrier
-  f32x4_t y = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if (tid < kRotThreads) {
-    y = rotate_forward(qv, ql, qr, qblk, kInvSqrtDim * qscale);
+    const f32x4_t y = rotate_forward(qv, ql, qr, qblk, kInvSqrtDim * qscale);
     // fp16 operands are kept in the normal range by an exact power-of-two
     // scale per head: the largest rotated entry is brought below 2^14 (hi
     // and lo parts both normal) and the scale is undone on the scores
@@ -632,9 +672,6 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     if (qblk == 0) qexp_s[qh] = qexp;
   }
   lds_barrier();   // lut, qop, qexp_s
-  // the values go out after the barrier, one batch per batch of scores: a
-  // wave reaches the barrier once its keys are issued, and the values stream
-  // in while the scores are computed
   const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
   int tb[NB];
 #pragma unroll
@@ -667,51 +704,20 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   stage[wave].ks[lane] = ksl;
   wave_lds_fence();
 
-  if (compressing) {
-    float nk0, nk1, nv0, nv1;
-    if (new_f16) {
-      nk0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(nkr[0])));
-      nk1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(nkr[0] >> 16)));
-      nv0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(nvr[0])));
-      nv1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(nvr[0] >> 16)));
-    } else {
-      nk0 = __builtin_bit_cast(float, nkr[0]);
-      nk1 = __builtin_bit_cast(float, nkr[1]);
-      nv0 = __builtin_bit_cast(float, nvr[0]);
-      nv1 = __builtin_bit_cast(float, nvr[1]);
-    }
-    // the two chains are independent and interleave
-    const float* qp0 = nqp;
-    const WaveCode wk = compress_vector_wave(nk0, nk1, qp0, cb, lane);
-    const WaveCode wv = compress_vector_wave(nv0, nv1, qp0, cb, lane);
-    if (lane < kRecordWords) {
-      reinterpret_cast<uint32_t*>(kc + static_cast<int64_t>(seq0) * kRecordBytes)[lane] = wk.word;
-      reinterpret_cast<uint32_t*>(vc + static_cast<int64_t>(seq0) * kRecordBytes)[lane] = wv.word;
-      new_rec[0][lane] = wk.word;
-      new_rec[1][lane] = wv.word;
-    }
-    if (lane == 0) {
-      k_norms[row + seq0] = wk.scale;
-      v_norms[row + seq0] = wv.scale;
-      new_scale[0] = wk.scale;
-      new_scale[1] = wv.scale;
-    }
-  }
-
   float m_run = -INFINITY, l_run = 0.f;
   f32x4_t o_acc[4];
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if (nvalid == 16 * NB)
-    attend_wave<NB, NB, true, kWide>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
-                              qdown, m_run, l_run, vmax, o_acc);
+    attend_wave<NB, NB, true, kWide>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp,
+                                     nvalid, vdw, vsh, qdown, m_run, l_run, vmax, o_acc);
   else if (NB > 1 && nvalid == 16 * (NB - 1))
-    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true, kWide>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp,
-                                                nvalid, vdw, vsh, qdown, m_run, l_run, vmax,
-                                                o_acc);
+    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true, kWide>(kw, vw, vc, koff, tb, stage[wave], qb,
+                                                        lut, col, grp, nvalid, vdw, vsh, qdown,
+                                                        m_run, l_run, vmax, o_acc);
   else if (nvalid > 0)
-    attend_wave<NB, NB, false, kWide>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh,
-                               qdown, m_run, l_run, vmax, o_acc);
+    attend_wave<NB, NB, false, kWide>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp,
+                                      nvalid, vdw, vsh, qdown, m_run, l_run, vmax, o_acc);
 
   // ---- merge the 8 waves in LDS ---------------------------------------------
   lds_barrier();   // every wave is done with its staging area
@@ -726,32 +732,16 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     wave_ml[wave][0][lane] = m_run;     // lanes 0..7 hold heads 0..7
     wave_ml[wave][1][lane] = l_run;
   }
-  lds_barrier();   // wave_o, wave_ml, new_rec, new_scale
+  lds_barrier();   // wave_o, wave_ml
   if (tid >= kRotThreads) return;
 
   // thread -> (head h = tid / 32, dims 4 (tid % 32) .. +3), the same
-  // (head, block) as in the query rotation
+  // (head, block) as in the query rotation.  A workgroup with nothing to
+  // attend (split at or past the length) ends with M = -inf, L = 0, O = 0.
   const int mh = qh, md = 4 * qblk;
   float M = -INFINITY;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wave_ml[w][0][mh]);
-  float s_new = -INFINITY;
-  f32x4_t v_new4 = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  if (new_attended) {
-    // score of the appended key: s^K (q_tilde . C[code]) over this thread's
-    // 4 dims (codes of dims md..md+3 = bits 3 md .. 3 md + 11 of the record),
-    // summed over the head's 32 lanes; y already carries the score scale
-    const f32x4_t k4 = decode_record_dims(new_rec[0], lut, md);
-    v_new4 = decode_record_dims(new_rec[1], lut, md);
-    float dot = y[0] * k4[0] + y[1] * k4[1] + y[2] * k4[2] + y[3] * k4[3];
-    dot += xor_lane<1>(dot);
-    dot += xor_lane<2>(dot);
-    dot += xor_lane<4>(dot);
-    dot += xor_lane<8>(dot);
-    dot += xor_lane<16>(dot);
-    s_new = dot * new_scale[0];
-    M = fmaxf(M, s_new);
-  }
   // dims md + j, j = 0..3: column u = md / 8, MFMA nb = (md % 8) / 2 + j / 2,
   // slot j % 2, row r = mh % 4 of lane u + 16 grp with grp = (mh / 4) % 2 +
   // 2 slot; entries (nb, nb + 1) of a lane are one aligned 8-byte pair
@@ -769,15 +759,12 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
         reinterpret_cast<const float*>(&wave_o[w][o_r][o_lane + 32]) + o_nb);
     O += c * f32x4_t{s0[0], s1[0], s0[1], s1[1]};
   }
-  if (new_attended) {
-    const float c = __builtin_amdgcn_exp2f(s_new - M);
-    L += c;
-    O += (c * new_scale[1]) * v_new4;
-  }
 
-  if (n_splits == 1) {
-    // thread (mh, md / 4) holds block md / 4 of head mh: rotate back in place
-    const f32x4_t o = rotate_inverse(O * (1.0f / L), ql, qr, qblk);
+  if (n_parts == 1) {
+    // thread (mh, md / 4) holds block md / 4 of head mh: rotate back in
+    // place (an empty sequence gives a zero row)
+    const f32x4_t o = L > 0.f ? rotate_inverse(O * (1.0f / L), ql, qr, qblk)
+                              : f32x4_t{0.f, 0.f, 0.f, 0.f};
     *reinterpret_cast<f32x4_t*>(out_bg + mh * kDim + md) = o;
     return;
   }
@@ -790,31 +777,32 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   *reinterpret_cast<f32x4_t*>(pp + 2 + md) = O;
 }
 
-// Merge of the split partials of one (sequence b, query head h): one
-// 256-thread workgroup; thread (sg, dq) takes splits sg, sg + 8, ... and dims
-// 4 dq .. 4 dq + 3, with up to 8 splits' loads in flight per thread.  Then
-// o = sum_s c_s O_s / sum_s c_s l_s with c_s = 2^(m_s - max m), and the single
-// inverse rotation.  Splits with nothing to attend carry m = -inf (their
-// other entries are never read), so the merge needs no sequence length.
-// kAppend: workgroup (b, head 0) then advances seq_lens[b] past the token the
-// decode kernel appended.
+// Merge of the split partials of one (sequence b, query head h): grid
+// (query head, sequence), one 256-thread workgroup each; thread (sg, dq)
+// takes partials sg, sg + 8, ... and dims 4 dq .. 4 dq + 3, with up to 8
+// partials' loads in flight per thread.  Then o = sum_s c_s O_s / sum_s c_s
+// l_s with c_s = 2^(m_s - max m), and the single inverse rotation.  Splits
+// with nothing to attend carry m = -inf (their other entries are never read),
+// so the merge needs no sequence length.  kAppend: the last of the n_parts
+// partials is the new token's, and workgroup (b, head 0) then advances
+// seq_lens[b] past the token the decode kernel appended.
 template <bool kAppend>
 __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     const float* __restrict__ partials, const float* __restrict__ quats, float* __restrict__ out,
-    int n_kv_heads, int n_splits, int32_t* __restrict__ seq_lens, int64_t capacity) {
+    int n_kv_heads, int n_parts, int32_t* __restrict__ seq_lens, int64_t capacity) {
   constexpr int kUnroll = 8;   // 8 x 8 = 64 splits per pass, all loads in flight
   __shared__ __attribute__((aligned(16))) float red_o[8][kDim];
   __shared__ float red_m[8], red_l[8];
   const int tid = threadIdx.x;
   const int n_q_heads = n_kv_heads * kHeads;
-  const int h = blockIdx.x % n_q_heads;
-  const int b = blockIdx.x / n_q_heads;
+  const int h = blockIdx.x;
+  const int b = blockIdx.y;
   const int g = h / kHeads, hh = h % kHeads;
   int seq0 = 0;
   if (kAppend && h == 0 && tid == 0) seq0 = seq_lens[b];
   const int sg = tid >> 5, dq = tid & 31;
   const float* base = partials +
-                      static_cast<int64_t>(b * n_kv_heads + g) * n_splits * (kHeads * kPart) +
+                      static_cast<int64_t>(b * n_kv_heads + g) * n_parts * (kHeads * kPart) +
                       hh * kPart;
   // block parameters for the inverse rotation (threads 0..31: block tid)
   const f32x4_t* qg =
@@ -822,14 +810,14 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
   const f32x4_t ql = qg[0], qr = qg[1];
   float M = -INFINITY, L = 0.f;
   f32x4_t O = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  for (int s0 = sg; s0 < n_splits; s0 += 8 * kUnroll) {
+  for (int s0 = sg; s0 < n_parts; s0 += 8 * kUnroll) {
     float mv[kUnroll], lv[kUnroll];
     f32x2_t mlv[kUnroll];
     f32x4_t ov[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int s = s0 + 8 * u;
-      const int sc = s < n_splits ? s : s0;
+      const int sc = s < n_parts ? s : s0;
       const float* p = base + static_cast<int64_t>(sc) * (kHeads * kPart);
       mlv[u] = *reinterpret_cast<const f32x2_t*>(p);   // (m, l)
       ov[u] = *reinterpret_cast<const f32x4_t*>(p + 2 + 4 * dq);
@@ -838,7 +826,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      mv[u] = s0 + 8 * u < n_splits ? mlv[u][0] : -INFINITY;
+      mv[u] = s0 + 8 * u < n_parts ? mlv[u][0] : -INFINITY;
       lv[u] = mlv[u][1];
     }
     float Mn = M;
@@ -892,37 +880,26 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
   if (kAppend && h == 0 && tid == 0 && seq0 >= 0 && seq0 < capacity) seq_lens[b] = seq0 + 1;
 }
 
-// Fused decode step with a single split: advances seq_lens after the decode
-// kernel (which read it in every workgroup) has finished.
-__global__ void advance_lengths_kernel(int32_t* __restrict__ seq_lens, int64_t capacity,
-                                       int batch) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b < batch) {
-    const int s = seq_lens[b];
-    if (s >= 0 && s < capacity) seq_lens[b] = s + 1;
-  }
-}
-
 }  // namespace
 
 // Split plan of the group-8 path: splits per (sequence, KV head) and their
-// length (a multiple of 16).  A workgroup covers at most 7 x 5 batches x 16 =
-// 560 positions; while the grid is small (<= 4 rounds of one
-// workgroup per CU) the split count is raised so that the grid fills whole
-// rounds, but a split keeps at least one batch per wave.
+// length (a multiple of 16).  A workgroup covers at most 8 waves x 5 batches
+// x 16 = 640 positions, capped at 560 so that long contexts keep more
+// splits; while the grid is small (<= 4 rounds of one workgroup per CU) the
+// split count is raised so that the grid, with the fused step's append
+// workgroup per (sequence, KV head), fills whole rounds, but a split keeps at
+// least one batch per wave.
 void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
              int64_t* n_splits, int64_t* split_len) {
   constexpr int64_t kCus = 256;
-  // at most 7 x 5 batches: the fused step's writer workgroup deals them over
-  // 7 waves, the others over 8, at most 5 each
-  constexpr int64_t kMaxLen = 16 * (kWaves - 1) * kMaxBatches;
+  constexpr int64_t kMaxLen = 560;
   const int64_t t = max_seq_len > 0 ? max_seq_len : 1;
   const int64_t bg = batch * n_kv_heads > 0 ? batch * n_kv_heads : 1;
   int64_t s = (t + kMaxLen - 1) / kMaxLen;
-  const int64_t wgs = bg * s;
+  const int64_t wgs = bg * (s + 1);
   if (wgs <= 4 * kCus) {
     const int64_t rounds = (wgs + kCus - 1) / kCus;
-    int64_t s_fill = (rounds * kCus) / bg;
+    int64_t s_fill = (rounds * kCus) / bg - 1;
     const int64_t s_min_len = (t + 16 * kWaves - 1) / (16 * kWaves);   // >= 1 batch per wave
     if (s_fill > s_min_len) s_fill = s_min_len;
     if (s_fill > s) s = s_fill;
@@ -942,17 +919,20 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                             const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
                             float* out, float* partials, const StepAppend* append,
                             hipStream_t stream) {
-  const dim3 grid(static_cast<unsigned>(batch * n_kv_heads * n_splits)), block(kThreads);
+  // partials per (sequence, KV head): the splits, and the fused step's new
+  // token
+  const int64_t n_parts = append ? n_splits + 1 : n_splits;
+  const dim3 grid(static_cast<unsigned>(n_parts), static_cast<unsigned>(n_kv_heads),
+                  static_cast<unsigned>(batch)),
+      block(kThreads);
   // Up to 5 batches per wave the kernel needs at most 128 VGPRs and ~55 KB of
   // LDS, so two workgroups fit on a CU: a grid of several rounds then runs
   // one workgroup's prologue and merge beside another's attention.  A grid
   // of at most one round would instead pile two workgroups on some CUs and
   // leave others idle; padding its LDS request keeps one workgroup per CU.
   constexpr int64_t kCus = 256;
-  const bool wide = grid.x > kCus;
+  const bool wide = n_parts * n_kv_heads * batch > kCus;
   const size_t lds_pad = wide ? 0 : kOneWorkgroupPadBytes;
-  // the fused step's writer workgroup deals the split's batches over 7 waves
-  if (append) nb = static_cast<int>((split_len / 16 + kWaves - 2) / (kWaves - 1));
   const float qscale = scale * kLog2e;
   const Codebook& cb = codebook();
   const void* k_new = append ? append->k_new : nullptr;
@@ -989,22 +969,18 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
 #undef IQ_LAUNCH_G8_W
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // splits of every (sequence, query head) merged by a second launch; the
-  // fused step advances the lengths there (or separately, for one split)
-  if (n_splits > 1) {
-    const dim3 mgrid(static_cast<unsigned>(batch * n_kv_heads * kHeads));
+  // the partials of every (sequence, query head) merged by a second launch,
+  // which in the fused step also advances the lengths
+  if (n_parts > 1) {
+    const dim3 mgrid(static_cast<unsigned>(n_kv_heads * kHeads), static_cast<unsigned>(batch));
     if (append)
       hipLaunchKernelGGL(merge_g8_kernel<true>, mgrid, dim3(kMergeThreads), 0, stream, partials,
-                         quats, out, static_cast<int>(n_kv_heads), static_cast<int>(n_splits),
+                         quats, out, static_cast<int>(n_kv_heads), static_cast<int>(n_parts),
                          seq_lens, capacity);
     else
       hipLaunchKernelGGL(merge_g8_kernel<false>, mgrid, dim3(kMergeThreads), 0, stream, partials,
-                         quats, out, static_cast<int>(n_kv_heads), static_cast<int>(n_splits),
+                         quats, out, static_cast<int>(n_kv_heads), static_cast<int>(n_parts),
                          seq_lens, capacity);
-    e = hipGetLastError();
-  } else if (append) {
-    hipLaunchKernelGGL(advance_lengths_kernel, dim3(static_cast<unsigned>((batch + 255) / 256)),
-                       dim3(256), 0, stream, seq_lens, capacity, static_cast<int>(batch));
     e = hipGetLastError();
   }
   return e;

@@ -39,7 +39,7 @@ struct DecodePlan {
   int64_t g8_splits;        // group-8 path: splits per (sequence, KV head)
   int64_t g8_split_len;     // group-8 path: positions per split
   size_t ticket_bytes;      // reserved (0)
-  size_t g8_partial_bytes;  // group-8 path: B * H_kv * splits * 8 * 130 floats
+  size_t g8_partial_bytes;  // group-8 path: B * H_kv * (splits + 1) * 8 * 130 floats
   size_t total_bytes;       // max over both paths
 };
 bool plan_decode(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
