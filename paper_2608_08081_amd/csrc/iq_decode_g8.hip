@@ -80,14 +80,50 @@ __device__ __forceinline__ f32x4_t mfma(u32x4_t a, u32x4_t b, f32x4_t c) {
                                                 __builtin_bit_cast(half8_t, b), c, 0, 0, 0);
 }
 
-// 6-bit field F (codes of dims 2F', 2F'+1) of a 96-bit slice w0:w1:w2 at bit
-// 6F; F must be a compile-time constant after unrolling.
-__device__ __forceinline__ uint32_t slice_field(int F, uint32_t w0, uint32_t w1, uint32_t w2) {
-  const int bit = 6 * F, word = bit / 32, off = bit % 32;
-  const uint32_t lo = word == 0 ? w0 : (word == 1 ? w1 : w2);
-  if (off <= 26) return __builtin_amdgcn_ubfe(lo, off, 6);
-  const uint32_t hi = word == 0 ? w1 : w2;
-  return __builtin_amdgcn_alignbit(hi, lo, off) & 63u;
+// Pair-table byte offsets (4 * field) of 6-bit fields that lie inside one
+// byte of a word, one instruction each through the byte selects of SDWA:
+// top6x4<K>(w) = 4 * bits 8K+2 .. 8K+7 (a field at bit 8K + 2),
+// low6x4<K>(w) = 4 * bits 8K .. 8K+5 (a field at bit 8K; the shifted byte is
+// truncated to 8 bits, dropping the byte's top two bits).
+template <int K>
+__device__ __forceinline__ uint32_t top6x4(uint32_t w) {
+  static_assert(K >= 0 && K < 4, "byte index");
+  uint32_t r;
+  if constexpr (K == 0)
+    asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_0 "
+        "src1_sel:DWORD" : "=v"(r) : "v"(w), "s"(0xFCu));
+  else if constexpr (K == 1)
+    asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 "
+        "src1_sel:DWORD" : "=v"(r) : "v"(w), "s"(0xFCu));
+  else if constexpr (K == 2)
+    asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_2 "
+        "src1_sel:DWORD" : "=v"(r) : "v"(w), "s"(0xFCu));
+  else
+    asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3 "
+        "src1_sel:DWORD" : "=v"(r) : "v"(w), "s"(0xFCu));
+  return r;
+}
+template <int K>
+__device__ __forceinline__ uint32_t low6x4(uint32_t w) {
+  static_assert(K >= 0 && K < 4, "byte index");
+  uint32_t r;
+  if constexpr (K == 0)
+    asm("v_lshlrev_b32_sdwa %0, 2, %1 dst_sel:BYTE_0 dst_unused:UNUSED_PAD src0_sel:DWORD "
+        "src1_sel:BYTE_0" : "=v"(r) : "v"(w));
+  else if constexpr (K == 1)
+    asm("v_lshlrev_b32_sdwa %0, 2, %1 dst_sel:BYTE_0 dst_unused:UNUSED_PAD src0_sel:DWORD "
+        "src1_sel:BYTE_1" : "=v"(r) : "v"(w));
+  else if constexpr (K == 2)
+    asm("v_lshlrev_b32_sdwa %0, 2, %1 dst_sel:BYTE_0 dst_unused:UNUSED_PAD src0_sel:DWORD "
+        "src1_sel:BYTE_2" : "=v"(r) : "v"(w));
+  else
+    asm("v_lshlrev_b32_sdwa %0, 2, %1 dst_sel:BYTE_0 dst_unused:UNUSED_PAD src0_sel:DWORD "
+        "src1_sel:BYTE_3" : "=v"(r) : "v"(w));
+  return r;
+}
+// Pair-table entry at byte offset a4 (the table sits at LDS address 0).
+__device__ __forceinline__ uint32_t lut_at(const uint32_t* lut, uint32_t a4) {
+  return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(lut) + a4);
 }
 
 // Workgroup barrier that orders LDS only.  __syncthreads() also fences
@@ -318,14 +354,21 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
     load_value_batch(vc, tb[i], koff, vw[i]);
     __builtin_amdgcn_sched_barrier(kNoVmemAcross);
     const uint32_t w0 = kw[i][0], w1 = kw[i][1], w2 = kw[i][2];
-    u32x4_t a[4];
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      a[kb] = u32x4_t{lut[slice_field(kb * 4 + 0, w0, w1, w2)],
-                      lut[slice_field(kb * 4 + 1, w0, w1, w2)],
-                      lut[slice_field(kb * 4 + 2, w0, w1, w2)],
-                      lut[slice_field(kb * 4 + 3, w0, w1, w2)]};
-    }
+    // fields F = 0..15 at bit 6F of the 96-bit slice w0:w1:w2: those at
+    // bits 0 or 2 mod 8 are byte selects of w0..w2, the others byte selects
+    // of the slice shifted right by 4 (u0..u2)
+    const uint32_t u0 = __builtin_amdgcn_alignbit(w1, w0, 4);
+    const uint32_t u1 = __builtin_amdgcn_alignbit(w2, w1, 4);
+    const uint32_t u2 = w2 >> 4;
+    const u32x4_t a[4] = {
+        u32x4_t{lut_at(lut, low6x4<0>(w0)), lut_at(lut, top6x4<0>(u0)),
+                lut_at(lut, low6x4<1>(u0)), lut_at(lut, top6x4<2>(w0))},
+        u32x4_t{lut_at(lut, low6x4<3>(w0)), lut_at(lut, top6x4<3>(u0)),
+                lut_at(lut, low6x4<0>(u1)), lut_at(lut, top6x4<1>(w1))},
+        u32x4_t{lut_at(lut, low6x4<2>(w1)), lut_at(lut, top6x4<2>(u1)),
+                lut_at(lut, low6x4<3>(u1)), lut_at(lut, top6x4<0>(w2))},
+        u32x4_t{lut_at(lut, low6x4<1>(w2)), lut_at(lut, top6x4<1>(u2)),
+                lut_at(lut, low6x4<2>(u2)), lut_at(lut, top6x4<3>(w2))}};
     f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) acc = mfma(a[kb], qb[kb], acc);
@@ -405,11 +448,14 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
       // bytes start 5 bytes in)
       const uint32_t* wp = rec + (4 * grp + r) * kRecStride + vdw;
       const uint64_t w64 = (static_cast<uint64_t>(wp[1]) << 32) | wp[0];
+      // fields at bits 0, 6, 12, 18 of the window: bits 0 and 18 are byte
+      // selects of it, bits 6 and 12 of the window shifted right by 4
       const uint32_t win = static_cast<uint32_t>(w64 >> vsh);
-      vb[0][r] = lut[win & 63u];
-      vb[1][r] = lut[__builtin_amdgcn_ubfe(win, 6, 6)];
-      vb[2][r] = lut[__builtin_amdgcn_ubfe(win, 12, 6)];
-      vb[3][r] = lut[__builtin_amdgcn_ubfe(win, 18, 6)];
+      const uint32_t wu = static_cast<uint32_t>(w64 >> (vsh + 4));
+      vb[0][r] = lut_at(lut, low6x4<0>(win));
+      vb[1][r] = lut_at(lut, top6x4<0>(wu));
+      vb[2][r] = lut_at(lut, low6x4<1>(wu));
+      vb[3][r] = lut_at(lut, top6x4<2>(win));
     }
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
