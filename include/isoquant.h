@@ -94,6 +94,28 @@ iq_status iq_codebook(float* levels, float* thresholds);
 iq_status iq_make_rotation(uint64_t seed, int64_t n_kv_heads, int64_t head_dim,
                            float* quats_host);
 
+/* Designs of the rotation ablation (Sec. 4.6, "Rotation Design Ablation")
+ * that keep the structure R = R_blocks H_128, so every kernel runs them
+ * unchanged. */
+typedef enum iq_rotation_variant {
+  IQ_ROTATION_SO4 = 0,        /* v3, the method: paired (q_L, q_R) SO(4) blocks after H */
+  IQ_ROTATION_SO3 = 1,        /* H, then single-quaternion blocks v -> q v conj(q) (SO(3)) */
+  IQ_ROTATION_WHT_ONLY = 2    /* H alone: identity quaternions */
+} iq_rotation_variant;
+
+/*
+ * iq_make_rotation_variant - parameters of one rotation design, same layout
+ * as iq_make_rotation (host quats_host[n_kv_heads][32][2][4]).
+ * IQ_ROTATION_SO4 equals iq_make_rotation; IQ_ROTATION_SO3 takes the same
+ * draws and sets q_R = q_L in every block, so each block acts as SO(3) and
+ * fixes its real axis (App. B); IQ_ROTATION_WHT_ONLY writes (1, 0, 0, 0)
+ * everywhere.  The ablation's v1 and v2 (blocks without H) are not of this
+ * form and exist only in the CPU oracle.  IQ_ERR_UNSUPPORTED for another
+ * variant or head_dim != 128.  Pure host function (no HIP call).
+ */
+iq_status iq_make_rotation_variant(uint64_t seed, int64_t n_kv_heads, int64_t head_dim,
+                                   int32_t variant, float* quats_host);
+
 /*
  * iq_compress_kv - Algorithm 1 (Sec. 3.2 Steps 1-4) over a block of tokens:
  * for every vector x: s = ||x||_2 (accumulated in fp64, stored as fp32),

@@ -19,6 +19,8 @@ Modules (each function cites the passage of the paper it follows):
 * ``compress``  - Algorithm 1: normalize, rotate, quantize, bit-pack.
 * ``attention`` - decode attention in the compressed space (App. A, Table 2)
   and the reconstruct-then-compute path it replaces (Sec. 1, Fig. 1 top).
+* ``rotation_study`` - distortion, coordinate energy and attention error of
+  the rotation designs of the ablation (Sec. 4.6) on seeded synthetic K/V.
 
 Parity status: every function is pinned by tests under ``tests/`` against
 closed forms, textbook tables, invariants or brute force, except where a

@@ -59,13 +59,22 @@ def decode_fused(q, k_packed, k_norms, v_packed, v_norms, seq_lens, quats,
     [H_kv][d/4][2][4].  Returns out [B][H_q][d] fp64 in the original space.
     ``skip_inverse`` returns o_tilde without R^T (the negative control of
     Sec. 5, "Inverse rotation is mandatory")."""
+    rots = _rot.rotation_matrices(np.asarray(quats))
+    return decode_fused_rotations(q, k_packed, k_norms, v_packed, v_norms, seq_lens, rots,
+                                  levels, scale, skip_inverse)
+
+
+def decode_fused_rotations(q, k_packed, k_norms, v_packed, v_norms, seq_lens, rots, levels,
+                           scale=None, skip_inverse=False):
+    """decode_fused with the rotation of each KV head given as a d x d
+    orthogonal matrix ([H_kv][d][d]): App. A holds for any orthogonal R, so
+    the designs of the rotation ablation run through the same steps."""
     q = np.asarray(q, dtype=np.float64)
     bsz, hq, d = q.shape
     hkv = k_packed.shape[1]
     if hq % hkv:
         raise ValueError("H_q must be a multiple of H_kv")
     group = hq // hkv
-    rots = _rot.rotation_matrices(np.asarray(quats))
     out = np.zeros((bsz, hq, d))
     for b in range(bsz):
         n = int(seq_lens[b])

@@ -160,3 +160,79 @@ def rotation_matrix(quats_head) -> np.ndarray:
 def rotation_matrices(quats) -> np.ndarray:
     """Stack of R for every head: [n_heads][d][d]."""
     return np.stack([rotation_matrix(quats[h]) for h in range(quats.shape[0])])
+
+
+# --------------------------------------------------------------------------
+# Designs of the rotation ablation (Sec. 4.6, "Rotation Design Ablation", and
+# its table of designs; the rotation comparison table of Sec. 2)
+# --------------------------------------------------------------------------
+
+# v1: one quaternion per block, v -> q v conj(q) (an SO(3) action), no WHT;
+# v2: the paired SO(4) blocks without the WHT pre-mix;
+# v3: the method, R_SO(4) H_d (Eq. 2);
+# wht: H_d alone (the Hadamard row of the comparison table);
+# wht_so3: H_d followed by v1's single-quaternion blocks (the variant of v1
+#   that the GPU kernels can run unchanged: q_R = q_L);
+# dense: a Haar-random dense orthogonal matrix (the dense-random row);
+# none: no rotation.
+VARIANTS = ("v1_so3", "v2_so4", "v3_wht_so4", "wht", "wht_so3", "dense", "none")
+
+
+def dense_orthogonal(gaussian) -> np.ndarray:
+    """Haar-distributed orthogonal matrix from a d x d matrix of independent
+    standard normal entries: the Q factor of its QR factorization with the
+    column signs chosen so that the triangular factor has a positive
+    diagonal (the sign fix that makes Q Haar distributed; Mezzadri, Notices
+    of the AMS 54(5), 2007).  The entries are passed in (drawn by the seeded
+    input generator)."""
+    g = np.asarray(gaussian, dtype=np.float64)
+    q, r = np.linalg.qr(g)
+    return q * np.sign(np.diag(r))[None, :]
+
+
+def block_diag_so3(quats_head) -> np.ndarray:
+    """d x d block diagonal of v -> q v conj(q) with q = each block's q_L."""
+    nb = quats_head.shape[0]
+    r = np.zeros((4 * nb, 4 * nb))
+    for i in range(nb):
+        r[4 * i:4 * i + 4, 4 * i:4 * i + 4] = so3_block(quats_head[i, 0])
+    return r
+
+
+def variant_rotation(variant: str, quats_head, gaussian=None) -> np.ndarray:
+    """d x d orthogonal rotation of one head for a design of the ablation
+    (names in VARIANTS).  quats_head: [d/4][2][4]; ``gaussian`` (d x d
+    standard normal entries) only for "dense"."""
+    d = 4 * quats_head.shape[0]
+    if variant == "v1_so3":
+        return block_diag_so3(quats_head)
+    if variant == "v2_so4":
+        return block_diag_so4(quats_head)
+    if variant == "v3_wht_so4":
+        return rotation_matrix(quats_head)
+    if variant == "wht":
+        return hadamard(d)
+    if variant == "wht_so3":
+        return block_diag_so3(quats_head) @ hadamard(d)
+    if variant == "dense":
+        if gaussian is None:
+            raise ValueError("the dense design needs its Gaussian entries")
+        return dense_orthogonal(gaussian)
+    if variant == "none":
+        return np.eye(d)
+    raise ValueError(f"unknown rotation design {variant!r}")
+
+
+def variant_quaternions(variant: str, seed: int, n_heads: int, d: int = 128) -> np.ndarray:
+    """Stored parameters of the designs the structured kernels run as they
+    are (R = R_blocks H_d): "v3_wht_so4" the seeded pairs, "wht_so3" the
+    same draws with q_R replaced by q_L, "wht" identity quaternions."""
+    if variant == "v3_wht_so4":
+        return make_quaternions(seed, n_heads, d)
+    if variant == "wht_so3":
+        q = make_quaternions(seed, n_heads, d)
+        q[:, :, 1] = q[:, :, 0]
+        return q
+    if variant == "wht":
+        return identity_quaternions(n_heads, d)
+    raise ValueError(f"design {variant!r} is not of the form R_blocks H_d")

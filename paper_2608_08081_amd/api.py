@@ -71,6 +71,20 @@ def iq_make_rotation(seed: int, n_kv_heads: int) -> torch.Tensor:
     return torch.from_numpy(out)
 
 
+ROTATION_VARIANTS = {"so4": 0, "so3": 1, "wht_only": 2}
+
+
+def iq_make_rotation_variant(seed: int, n_kv_heads: int, variant: str) -> torch.Tensor:
+    """Parameters of one rotation design of the ablation that keeps the
+    R_blocks H_128 form ("so4" = the method, "so3" = single-quaternion
+    blocks, "wht_only" = identity blocks), host float32 [n_kv_heads][32][2][4]."""
+    out = np.zeros((n_kv_heads, 32, 2, 4), np.float32)
+    _lib.check("iq_make_rotation_variant", _lib.lib().iq_make_rotation_variant(
+        seed & ((1 << 64) - 1), n_kv_heads, HEAD_DIM, ROTATION_VARIANTS[variant],
+        out.ctypes.data_as(ctypes.c_void_p)))
+    return torch.from_numpy(out)
+
+
 def iq_decode_workspace_bytes(batch, n_q_heads, n_kv_heads, max_seq_len) -> int:
     return int(_lib.lib().iq_decode_workspace_bytes(batch, n_q_heads, n_kv_heads,
                                                     max_seq_len, HEAD_DIM))

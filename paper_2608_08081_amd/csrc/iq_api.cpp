@@ -150,7 +150,7 @@ const char* iq_status_string(iq_status s) {
   return "IQ_ERR_UNKNOWN";
 }
 
-int iq_version(void) { return 102; }
+int iq_version(void) { return 103; }
 
 iq_status iq_codebook(float* levels, float* thresholds) {
   const iq::Codebook& cb = iq::codebook();
@@ -170,6 +170,29 @@ iq_status iq_make_rotation(uint64_t seed, int64_t n_kv_heads, int64_t head_dim,
       iq::random_unit_quaternion(g, dst);
       iq::random_unit_quaternion(g, dst + 4);
     }
+  return IQ_OK;
+}
+
+iq_status iq_make_rotation_variant(uint64_t seed, int64_t n_kv_heads, int64_t head_dim,
+                                   int32_t variant, float* quats_host) {
+  if (variant != IQ_ROTATION_SO4 && variant != IQ_ROTATION_SO3 &&
+      variant != IQ_ROTATION_WHT_ONLY)
+    return IQ_ERR_UNSUPPORTED;
+  if (variant == IQ_ROTATION_WHT_ONLY) {
+    if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
+    if (n_kv_heads <= 0 || quats_host == nullptr) return IQ_ERR_INVALID_ARGUMENT;
+    for (int64_t i = 0; i < n_kv_heads * iq::kNumBlocks * 2; ++i) {
+      float* q = quats_host + 4 * i;
+      q[0] = 1.0f;
+      q[1] = q[2] = q[3] = 0.0f;
+    }
+    return IQ_OK;
+  }
+  const iq_status st = iq_make_rotation(seed, n_kv_heads, head_dim, quats_host);
+  if (st != IQ_OK || variant == IQ_ROTATION_SO4) return st;
+  // single quaternion per block: q_R = q_L
+  for (int64_t i = 0; i < n_kv_heads * iq::kNumBlocks; ++i)
+    for (int c = 0; c < 4; ++c) quats_host[8 * i + 4 + c] = quats_host[8 * i + c];
   return IQ_OK;
 }
 

@@ -22,7 +22,8 @@ evaluates, which are not available; head_dim 128 as in App. C):
 
 Streams: numpy ``default_rng([seed, workload_id, stream])`` with stream
 0 = key channel scales, 1 = value channel scales, 2 = keys, 3 = values,
-4 = queries, 5 = needle positions / appended tokens, 6 = context lengths.
+4 = queries, 5 = needle positions / appended tokens, 6 = context lengths,
+7 = the standard normal matrices of the dense-random rotation design.
 """
 
 from __future__ import annotations
@@ -157,3 +158,10 @@ def plant_needle(seed: int, w: Workload, k: np.ndarray, q: np.ndarray,
             u = qv / np.sqrt(np.dot(qv, qv))
             k[b, h, pos[b, h]] = (factor * np.sqrt(d) * u).astype(k.dtype)
     return pos
+
+
+def gaussian_matrices(seed: int, n: int, d: int = HEAD_DIM) -> np.ndarray:
+    """[n][d][d] independent standard normal entries (fp64): the input of the
+    dense-random rotation design of the rotation study (one matrix per KV
+    head)."""
+    return rng(seed, 90, 7).standard_normal((n, d, d))

@@ -52,6 +52,26 @@ def test_make_rotation_matches_oracle_bit_for_bit(seed, heads):
     assert np.array_equal(out.view(np.uint32), want.view(np.uint32))
 
 
+@pytest.mark.parametrize("variant,name", [(0, "v3_wht_so4"), (1, "wht_so3"), (2, "wht")])
+def test_make_rotation_variant_matches_oracle_bit_for_bit(variant, name):
+    out = np.zeros((3, 32, 2, 4), np.float32)
+    assert L.iq_make_rotation_variant(1002, 3, 128, variant,
+                                      out.ctypes.data_as(ctypes.c_void_p)) == 0
+    want = orot.variant_quaternions(name, 1002, 3)
+    assert np.array_equal(out.view(np.uint32), want.view(np.uint32))
+
+
+def test_make_rotation_variant_validation():
+    out = np.zeros((1, 32, 2, 4), np.float32)
+    p = out.ctypes.data_as(ctypes.c_void_p)
+    assert L.iq_make_rotation_variant(1, 1, 128, 3, p) == 2
+    assert L.iq_make_rotation_variant(1, 1, 128, -1, p) == 2
+    for v in (0, 1, 2):
+        assert L.iq_make_rotation_variant(1, 1, 64, v, p) == 2
+        assert L.iq_make_rotation_variant(1, 0, 128, v, p) == 1
+        assert L.iq_make_rotation_variant(1, 1, 128, v, None) == 1
+
+
 def test_make_rotation_validation():
     out = np.zeros((1, 32, 2, 4), np.float32)
     p = out.ctypes.data_as(ctypes.c_void_p)
