@@ -22,6 +22,11 @@ the default is the one above):
             V, fp16 Student-t(4) entries times log-normal channel scales;
   append8k  batch 1, 32 query heads, 4 KV heads, 8192 compressed tokens, then
             fused steps that each append one token (48 layer caches cycled);
+  rotation_fit  SO(4) block parameters fitted on the host (iq_fit_rotation)
+            to 4 x 4096 anisotropic calibration keys, then the 3-bit distortion
+            of 4 x 32768 held-out keys with the same channel scales, compressed
+            and materialized by the library's kernels, for the fitted, random,
+            single-quaternion and Hadamard-only parameters;
   baseline32k  the 32K shape above through the reconstruct-then-compute
             pipeline the packed path replaces (Fig. 1 top): decode attention
             on an fp16 cache, materialization of the packed cache as fp16
@@ -53,7 +58,7 @@ def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--workload", choices=("step32k", "varlen", "compress", "append8k",
-                                          "baseline32k"),
+                                          "baseline32k", "rotation_fit"),
                    default="step32k")
     p.add_argument("--steps", type=int, default=None,
                    help="timed steps (default: 4800; varlen 240; compress 20; append8k 1000)")
@@ -69,7 +74,8 @@ def parse():
                    help="also run one plain device copy of this many MiB (counter calibration)")
     a = p.parse_args()
     defaults = {"step32k": (4800, 48), "varlen": (240, 3), "compress": (20, 1),
-                "append8k": (1000, 48), "baseline32k": (960, 48)}[a.workload]
+                "append8k": (1000, 48), "baseline32k": (960, 48),
+                "rotation_fit": (1, 1)}[a.workload]
     if a.steps is None:
         a.steps = defaults[0]
     if a.warmup is None:
@@ -671,6 +677,54 @@ def run_compress(args, torch, api, synth, dev):
     return result
 
 
+def run_rotation_fit(args, torch, api, synth, dev):
+    """Fit the SO(4) blocks on calibration keys (host), then measure the
+    held-out relative squared error ||x - x_hat||^2 / ||x||^2 of keys
+    compressed (iq_compress_kv) and materialized (iq_dequantize_kv) on the
+    GPU with each parameter set.  A quality figure, not a throughput."""
+    n_heads, n_cal, n_held = 4, 4096, 32768
+    w = synth.Workload(96, "rotation_fit", 1, 8 * n_heads, n_heads, n_cal + n_held, "f16")
+    k = synth.kv_tensor(args.seed, w, "k")                      # [1][H][T][d] fp16
+    cal = k[0, :, :n_cal].astype("float32")
+    t0 = time.perf_counter()
+    fitted = api.iq_fit_rotation(cal, sweeps=4)
+    fit_s = time.perf_counter() - t0
+    held = torch.from_numpy(k[:, :, n_cal:].copy()).to(dev)
+    params = {"fitted": fitted,
+              "random_so4": api.iq_make_rotation(w.rotation_seed, n_heads),
+              "single_quaternion": api.iq_make_rotation_variant(w.rotation_seed, n_heads, "so3"),
+              "wht_only": api.iq_make_rotation_variant(w.rotation_seed, n_heads, "wht_only")}
+    x = held.float()
+    x2 = (x * x).sum(-1)
+    res = {}
+    for name, q in params.items():
+        qd = q.to(dev)
+        cache = api.alloc_cache(1, n_heads, n_held, dev, values=False)
+        api.iq_compress_kv(held, None, qd, cache["k_codes"], cache["k_norms"], None, None)
+        xh, _ = api.iq_dequantize_kv(cache["k_codes"], cache["k_norms"], None, None, qd,
+                                     out_dtype=torch.float32)
+        err = ((x - xh) ** 2).sum(-1) / x2
+        res[name] = round(float(err.mean()), 6)
+    torch.cuda.synchronize()
+    return {
+        "metric": "held-out 3-bit relative squared error of keys, fitted vs random SO(4) blocks",
+        "value": res["fitted"],
+        "unit": "mean ||x - x_hat||^2 / ||x||^2",
+        "n_gpus": 1,
+        "steps": 1,
+        "warmup": 0,
+        "higher_is_better": False,
+        "vs_baseline": None,
+        "dtype": "f16 in, u3 codes, f32 out",
+        "data": "synthetic (seeded anisotropic fp16 keys: N(0,1) x log-normal channel scales, "
+                "4 outlier channels x20)",
+        "config": {"workload": f"{n_heads} KV heads, {n_cal} calibration + {n_held} held-out "
+                               f"keys per head, head_dim 128, 4 fitting sweeps"},
+        "distortion": res,
+        "fit_seconds_host": round(fit_s, 3),
+    }
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -694,7 +748,8 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     run = {"step32k": run_step32k, "varlen": run_varlen, "compress": run_compress,
-           "append8k": run_append8k, "baseline32k": run_baseline32k}[args.workload]
+           "append8k": run_append8k, "baseline32k": run_baseline32k,
+           "rotation_fit": run_rotation_fit}[args.workload]
     print(json.dumps(run(args, torch, api, synth, dev)), flush=True)
 
 

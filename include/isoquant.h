@@ -117,6 +117,36 @@ iq_status iq_make_rotation_variant(uint64_t seed, int64_t n_kv_heads, int64_t he
                                    int32_t variant, float* quats_host);
 
 /*
+ * iq_fit_rotation - fitted SO(4) block parameters (Sec. 3.2: the blocks
+ * fine-tune the rotation after H_128, 6 degrees of freedom each, 192
+ * "learnable" parameters per head; the paper gives no procedure).  Reading:
+ * per KV head and block, the rotation of the block's four post-WHT
+ * coordinates that minimizes their mean squared quantization error (the
+ * objective Step 3 states for the quantizer) on the calibration vectors,
+ * found by `sweeps` Jacobi sweeps over the six coordinate planes from the
+ * identity (a grid of 24 angles, then golden-section refinement; a plane
+ * rotation is kept only if it lowers the error), so the fitted error never
+ * exceeds that of H_128 alone on the calibration set.  Host memory:
+ * calib[n_kv_heads][n_vectors][128] fp32 in (zero and non-finite vectors
+ * are skipped), quats_host[n_kv_heads][32][2][4] out, the layout of
+ * iq_make_rotation.  1 <= n_vectors <= 2^24, sweeps >= 0 (0 gives identity
+ * quaternions).  Pure host function (no HIP call); runs the 32 blocks of a
+ * head on up to 8 host threads.
+ */
+iq_status iq_fit_rotation(const float* calib, int64_t n_vectors, int64_t n_kv_heads,
+                          int64_t head_dim, int32_t sweeps, float* quats_host);
+
+/*
+ * iq_so4_to_quaternions - the pair (q_L, q_R) with m v = q_L v conj(q_R)
+ * for a rotation m of R^4 (App. B: SO(4) is covered by S^3 x S^3), block
+ * component 0 the real part.  m: host fp64 4 x 4, row-major; q_pair: host
+ * fp32 out (q_L.w, q_L.x, q_L.y, q_L.z, q_R.w, ..., q_R.z), unit, defined
+ * up to the common sign (q_L, q_R) -> (-q_L, -q_R).  IQ_ERR_INVALID_ARGUMENT
+ * if m is not orthogonal to 1e-6 or has determinant -1.  Pure host function.
+ */
+iq_status iq_so4_to_quaternions(const double* m, float* q_pair);
+
+/*
  * iq_compress_kv - Algorithm 1 (Sec. 3.2 Steps 1-4) over a block of tokens:
  * for every vector x: s = ||x||_2 (accumulated in fp64, stored as fp32),
  * x_tilde = R_SO(4)(H_128 x / s) (Eq. 2), each coordinate replaced by the

@@ -39,6 +39,8 @@ _SIGNATURES = {
     "iq_codebook": (_c_int, [_vp, _vp]),
     "iq_make_rotation": (_c_int, [_c_u64, _c_i64, _c_i64, _vp]),
     "iq_make_rotation_variant": (_c_int, [_c_u64, _c_i64, _c_i64, _c_int, _vp]),
+    "iq_fit_rotation": (_c_int, [_vp, _c_i64, _c_i64, _c_i64, _c_int, _vp]),
+    "iq_so4_to_quaternions": (_c_int, [_vp, _vp]),
     "iq_compress_kv": (_c_int, [_vp, _vp, _c_int, _c_i64, _c_i64, _c_i64, _c_i64, _vp,
                                 _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp]),
     "iq_append_token": (_c_int, [_vp, _vp, _c_int, _c_i64, _c_i64, _c_i64, _vp,

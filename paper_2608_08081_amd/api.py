@@ -85,6 +85,32 @@ def iq_make_rotation_variant(seed: int, n_kv_heads: int, variant: str) -> torch.
     return torch.from_numpy(out)
 
 
+def iq_fit_rotation(calib, sweeps: int = 4) -> torch.Tensor:
+    """Fitted SO(4) block parameters from calibration vectors (host fp32
+    [n_kv_heads][n_vectors][128], a tensor or array): host float32
+    [n_kv_heads][32][2][4] in the layout of iq_make_rotation."""
+    x = np.ascontiguousarray(np.asarray(calib.cpu() if hasattr(calib, "cpu") else calib,
+                                        dtype=np.float32))
+    if x.ndim != 3 or x.shape[2] != HEAD_DIM:
+        raise ValueError("calib must be [n_kv_heads][n_vectors][128]")
+    out = np.zeros((x.shape[0], 32, 2, 4), np.float32)
+    _lib.check("iq_fit_rotation", _lib.lib().iq_fit_rotation(
+        x.ctypes.data_as(ctypes.c_void_p), x.shape[1], x.shape[0], HEAD_DIM, sweeps,
+        out.ctypes.data_as(ctypes.c_void_p)))
+    return torch.from_numpy(out)
+
+
+def iq_so4_to_quaternions(m) -> np.ndarray:
+    """(q_L, q_R) of a 4 x 4 rotation (fp64): float32 [2][4]."""
+    a = np.ascontiguousarray(np.asarray(m, dtype=np.float64))
+    if a.shape != (4, 4):
+        raise ValueError("m must be 4 x 4")
+    out = np.zeros((2, 4), np.float32)
+    _lib.check("iq_so4_to_quaternions", _lib.lib().iq_so4_to_quaternions(
+        a.ctypes.data_as(ctypes.c_void_p), out.ctypes.data_as(ctypes.c_void_p)))
+    return out
+
+
 def iq_decode_workspace_bytes(batch, n_q_heads, n_kv_heads, max_seq_len) -> int:
     return int(_lib.lib().iq_decode_workspace_bytes(batch, n_q_heads, n_kv_heads,
                                                     max_seq_len, HEAD_DIM))
