@@ -249,8 +249,9 @@ iq_status iq_decode_attention(const float* q,
  * followed by iq_decode_attention of q over the advanced lengths (Alg. 1 on
  * the step's new key and value, then App. A / Table 2 on the packed cache;
  * the per-step cache write of App. D), issued as one launch sequence.  The
- * new record is written at position seq_lens[b] by the workgroup that owns
- * that position, which uses it directly for its own part of the attention.
+ * new record is written at position seq_lens[b] by an extra workgroup per
+ * (sequence, KV head) of the attention launch, which also contributes the
+ * new token to the attention from its fresh record.
  *
  * Results are those of the two separate calls:
  *   - if 0 <= seq_lens[b] < capacity, the token is written at seq_lens[b],
@@ -275,6 +276,65 @@ iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, i
                          int64_t n_kv_heads, int64_t head_dim, float softmax_scale, float* out,
                          void* workspace, size_t workspace_bytes, int32_t* status_dev,
                          hipStream_t stream);
+
+/*
+ * Paged cache (serving with page pools)
+ * -------------------------------------
+ * The same records (48-byte codes + fp32 scale per vector, Sec. 3.2 Step 4)
+ * in a pool of pages shared by all sequences, located through per-sequence
+ * page tables instead of one contiguous row per (sequence, KV head):
+ *   k_codes / v_codes : device uint8 [n_pages][n_kv_heads][page_size][48],
+ *                       16-byte aligned;
+ *   k_norms / v_norms : device fp32 [n_pages][n_kv_heads][page_size],
+ *                       16-byte aligned (iq_compress_kv_paged: 4);
+ *   block_tables      : device int32 [batch][max_pages]: logical position t of
+ *                       sequence b lives in page block_tables[b][t / page_size],
+ *                       slot t % page_size;
+ *   page_size         : positions per page, a multiple of 16, >= 16;
+ *   capacity          : max_pages * page_size (logical positions per
+ *                       sequence), with capacity * 48 < 2^31.
+ * A page index outside [0, n_pages) is a caller error: reads then use page 0
+ * and writes are skipped, so no access leaves the pools.  The decode entry
+ * points run the group-8 matrix-core path only (IQ_ERR_UNSUPPORTED unless
+ * n_q_heads == 8 * n_kv_heads); batch and n_kv_heads <= 65535.  Results
+ * equal those of the contiguous entry points on a cache holding the same
+ * records; the workspace is sized by iq_decode_workspace_bytes.
+ */
+
+/* iq_compress_kv_paged - iq_compress_kv into a paged cache: tokens
+ * [0, n_tokens) of every sequence to logical positions dst_offset ..
+ * dst_offset + n_tokens - 1 (<= capacity). */
+iq_status iq_compress_kv_paged(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+                               int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
+                               const float* quats, uint8_t* k_codes, float* k_norms,
+                               uint8_t* v_codes, float* v_norms, int64_t page_size,
+                               int64_t n_pages, const int32_t* block_tables, int64_t max_pages,
+                               int64_t dst_offset, hipStream_t stream);
+
+/* iq_decode_attention_paged - iq_decode_attention on a paged cache
+ * (max_seq_len <= capacity). */
+iq_status iq_decode_attention_paged(const float* q, const uint8_t* k_codes,
+                                    const float* k_norms, const uint8_t* v_codes,
+                                    const float* v_norms, int64_t page_size, int64_t n_pages,
+                                    const int32_t* block_tables, int64_t max_pages,
+                                    const int32_t* seq_lens, int64_t max_seq_len,
+                                    const float* quats, int64_t batch, int64_t n_q_heads,
+                                    int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
+                                    float* out, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream);
+
+/* iq_decode_step_paged - iq_decode_step on a paged cache: the new token goes
+ * to logical position seq_lens[b] (the caller has mapped its page), if
+ * below capacity. */
+iq_status iq_decode_step_paged(const float* q, const void* k_new, const void* v_new,
+                               iq_dtype dtype, uint8_t* k_codes, float* k_norms,
+                               uint8_t* v_codes, float* v_norms, int64_t page_size,
+                               int64_t n_pages, const int32_t* block_tables, int64_t max_pages,
+                               int32_t* seq_lens, int64_t max_seq_len, const float* quats,
+                               int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                               int64_t head_dim, float softmax_scale, float* out,
+                               void* workspace, size_t workspace_bytes, int32_t* status_dev,
+                               hipStream_t stream);
 
 /*
  * Reconstruct-then-compute baseline (Sec. 1, Fig. 1 top)

@@ -40,6 +40,15 @@ _SIGNATURES = {
     "iq_make_rotation": (_c_int, [_c_u64, _c_i64, _c_i64, _vp]),
     "iq_make_rotation_variant": (_c_int, [_c_u64, _c_i64, _c_i64, _c_int, _vp]),
     "iq_fit_rotation": (_c_int, [_vp, _c_i64, _c_i64, _c_i64, _c_int, _vp]),
+    "iq_compress_kv_paged": (_c_int, [_vp, _vp, _c_int, _c_i64, _c_i64, _c_i64, _c_i64, _vp,
+                                      _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp, _c_i64,
+                                      _c_i64, _vp]),
+    "iq_decode_attention_paged": (_c_int, [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp,
+                                           _c_i64, _vp, _c_i64, _vp, _c_i64, _c_i64, _c_i64,
+                                           _c_i64, _c_float, _vp, _vp, _c_size, _vp]),
+    "iq_decode_step_paged": (_c_int, [_vp, _vp, _vp, _c_int, _vp, _vp, _vp, _vp, _c_i64,
+                                      _c_i64, _vp, _c_i64, _vp, _c_i64, _vp, _c_i64, _c_i64,
+                                      _c_i64, _c_i64, _c_float, _vp, _vp, _c_size, _vp, _vp]),
     "iq_so4_to_quaternions": (_c_int, [_vp, _vp]),
     "iq_compress_kv": (_c_int, [_vp, _vp, _c_int, _c_i64, _c_i64, _c_i64, _c_i64, _vp,
                                 _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp]),

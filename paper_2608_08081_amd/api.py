@@ -290,6 +290,123 @@ def iq_decode_step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens
 
 
 # ---------------------------------------------------------------------------
+# paged cache (page pools shared by all sequences + per-sequence page tables)
+# ---------------------------------------------------------------------------
+
+def alloc_paged_cache(n_pages, n_kv_heads, page_size, device):
+    """Zero-filled page pools: dict with k_codes / v_codes
+    [n_pages][n_kv_heads][page_size][48] uint8 and k_norms / v_norms
+    [n_pages][n_kv_heads][page_size] fp32."""
+    c = {}
+    for side in ("k", "v"):
+        c[f"{side}_codes"] = torch.zeros((n_pages, n_kv_heads, page_size, RECORD_BYTES),
+                                         dtype=torch.uint8, device=device)
+        c[f"{side}_norms"] = torch.zeros((n_pages, n_kv_heads, page_size), dtype=torch.float32,
+                                         device=device)
+    return c
+
+
+def _paged_pools(pool, block_tables, dev):
+    if pool["k_codes"].dim() != 4:
+        raise ValueError("k_codes must be [n_pages][n_kv_heads][page_size][48]")
+    n_pages, hkv, page, _ = pool["k_codes"].shape
+    for side in ("k", "v"):
+        if pool.get(f"{side}_codes") is None:
+            continue
+        _require(pool[f"{side}_codes"], f"{side}_codes", torch.uint8,
+                 (n_pages, hkv, page, RECORD_BYTES), dev)
+        _require(pool[f"{side}_norms"], f"{side}_norms", torch.float32, (n_pages, hkv, page),
+                 dev)
+    if block_tables.dim() != 2:
+        raise ValueError("block_tables must be [batch][max_pages]")
+    _require(block_tables, "block_tables", torch.int32, tuple(block_tables.shape), dev)
+    return n_pages, hkv, page, block_tables.shape[1]
+
+
+def iq_compress_kv_paged(k, v, quats, pool, block_tables, dst_offset: int = 0):
+    """iq_compress_kv into page pools (dict from alloc_paged_cache): k / v
+    [B][H_kv][T][128] (fp16 or fp32; either may be None) to logical positions
+    dst_offset .. dst_offset + T - 1 of every sequence."""
+    src = k if k is not None else v
+    if src is None:
+        raise ValueError("k and v are both None")
+    b, hkv, t, _ = src.shape
+    dev = src.device
+    n_pages, phkv, page, max_pages = _paged_pools(pool, block_tables, dev)
+    if phkv != hkv or block_tables.shape[0] != b:
+        raise ValueError("pools / block_tables do not match the inputs")
+    for x, name in ((k, "k"), (v, "v")):
+        if x is not None:
+            _require(x, name, src.dtype, (b, hkv, t, HEAD_DIM), dev)
+    _require(quats, "quats", torch.float32, (hkv, 32, 2, 4), dev)
+    st = _lib.lib().iq_compress_kv_paged(
+        _ptr(k), _ptr(v), _dtype_code(src), b, hkv, t, HEAD_DIM, _ptr(quats),
+        _ptr(pool["k_codes"]) if k is not None else None,
+        _ptr(pool["k_norms"]) if k is not None else None,
+        _ptr(pool["v_codes"]) if v is not None else None,
+        _ptr(pool["v_norms"]) if v is not None else None,
+        page, n_pages, _ptr(block_tables), max_pages, dst_offset, _stream(dev))
+    _lib.check("iq_compress_kv_paged", st)
+
+
+def iq_decode_attention_paged(q, pool, block_tables, seq_lens, quats, out=None,
+                              workspace=None, max_seq_len=None, softmax_scale: float = 0.0):
+    """iq_decode_attention on page pools; q [B][8 H_kv][128]."""
+    b, hq, _ = q.shape
+    dev = q.device
+    _require(q, "q", torch.float32, (b, hq, HEAD_DIM), dev)
+    n_pages, hkv, page, max_pages = _paged_pools(pool, block_tables, dev)
+    _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
+    _require(quats, "quats", torch.float32, (hkv, 32, 2, 4), dev)
+    if max_seq_len is None:
+        max_seq_len = max_pages * page
+    if out is None:
+        out = torch.empty((b, hq, HEAD_DIM), dtype=torch.float32, device=dev)
+    _require(out, "out", torch.float32, (b, hq, HEAD_DIM), dev)
+    if workspace is None:
+        workspace = alloc_workspace(b, hq, hkv, max_seq_len, dev)
+    st = _lib.lib().iq_decode_attention_paged(
+        _ptr(q), _ptr(pool["k_codes"]), _ptr(pool["k_norms"]), _ptr(pool["v_codes"]),
+        _ptr(pool["v_norms"]), page, n_pages, _ptr(block_tables), max_pages, _ptr(seq_lens),
+        max_seq_len, _ptr(quats), b, hq, hkv, HEAD_DIM, float(softmax_scale), _ptr(out),
+        _ptr(workspace), workspace.numel(), _stream(dev))
+    _lib.check("iq_decode_attention_paged", st)
+    return out
+
+
+def iq_decode_step_paged(q, k_new, v_new, pool, block_tables, seq_lens, quats, out=None,
+                         workspace=None, max_seq_len=None, softmax_scale: float = 0.0,
+                         status=None):
+    """iq_decode_step on page pools: the new token goes to logical position
+    seq_lens[b] (its page must be mapped in block_tables)."""
+    b, hq, _ = q.shape
+    dev = q.device
+    _require(q, "q", torch.float32, (b, hq, HEAD_DIM), dev)
+    n_pages, hkv, page, max_pages = _paged_pools(pool, block_tables, dev)
+    _require(k_new, "k_new", k_new.dtype, (b, hkv, HEAD_DIM), dev)
+    _require(v_new, "v_new", k_new.dtype, (b, hkv, HEAD_DIM), dev)
+    _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
+    _require(quats, "quats", torch.float32, (hkv, 32, 2, 4), dev)
+    if status is not None:
+        _require(status, "status", torch.int32, (1,), dev)
+    if max_seq_len is None:
+        max_seq_len = max_pages * page
+    if out is None:
+        out = torch.empty((b, hq, HEAD_DIM), dtype=torch.float32, device=dev)
+    _require(out, "out", torch.float32, (b, hq, HEAD_DIM), dev)
+    if workspace is None:
+        workspace = alloc_workspace(b, hq, hkv, max_seq_len, dev)
+    st = _lib.lib().iq_decode_step_paged(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _dtype_code(k_new), _ptr(pool["k_codes"]),
+        _ptr(pool["k_norms"]), _ptr(pool["v_codes"]), _ptr(pool["v_norms"]), page, n_pages,
+        _ptr(block_tables), max_pages, _ptr(seq_lens), max_seq_len, _ptr(quats), b, hq, hkv,
+        HEAD_DIM, float(softmax_scale), _ptr(out), _ptr(workspace), workspace.numel(),
+        _ptr(status), _stream(dev))
+    _lib.check("iq_decode_step_paged", st)
+    return out
+
+
+# ---------------------------------------------------------------------------
 # reconstruct-then-compute baseline (materialized fp16 cache)
 # ---------------------------------------------------------------------------
 

@@ -357,6 +357,150 @@ iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, i
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 
+// ---------------------------------------------------------------------------
+// Paged cache (page pools + per-sequence page tables)
+// ---------------------------------------------------------------------------
+namespace {
+
+// Checks shared by the paged entry points; fills the page table.
+iq_status check_pages(int64_t n_kv_heads, int64_t page_size, int64_t n_pages,
+                      const int32_t* block_tables, int64_t max_pages, iq::PageTable* pt) {
+  if (page_size < 16 || page_size % 16 || page_size > (int64_t(1) << 20))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (n_pages < 1 || n_pages > 0x7fffffff || max_pages < 1 || block_tables == nullptr ||
+      !iq::aligned(block_tables, 4))
+    return IQ_ERR_INVALID_ARGUMENT;
+  // the decode kernel addresses positions with 32-bit byte offsets
+  if (!iq::mul_ok(max_pages, page_size) || max_pages * page_size * iq::kRecordBytes > 0x7fffffff)
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (!iq::mul_ok(n_pages, n_kv_heads) || !iq::mul_ok(n_pages * n_kv_heads, page_size) ||
+      !iq::mul_ok(n_pages * n_kv_heads * page_size, iq::kRecordBytes))
+    return IQ_ERR_INVALID_ARGUMENT;
+  *pt = iq::PageTable{block_tables, max_pages, static_cast<int32_t>(page_size),
+                      static_cast<int32_t>(n_pages)};
+  return IQ_OK;
+}
+
+iq_status check_paged_decode(const float* q, const void* k_codes, const float* k_norms,
+                             const void* v_codes, const float* v_norms,
+                             const int32_t* seq_lens, int64_t max_seq_len, const float* quats,
+                             int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                             int64_t head_dim, const float* out, const void* workspace,
+                             size_t workspace_bytes, const iq::PageTable& pt,
+                             iq::DecodePlan* plan) {
+  if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
+  if (batch < 0 || n_kv_heads <= 0 || n_q_heads <= 0 || max_seq_len < 0 ||
+      max_seq_len > pt.max_pages * pt.page_size || batch > 65535 || n_kv_heads > 65535)
+    return IQ_ERR_INVALID_ARGUMENT;
+  // paged caches run on the matrix-core path: 8 query heads per KV head
+  if (n_q_heads != 8 * n_kv_heads) return IQ_ERR_UNSUPPORTED;
+  if (!q || !k_codes || !k_norms || !v_codes || !v_norms || !seq_lens || !quats || !out ||
+      !workspace)
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (!iq::aligned(q, 16) || !iq::aligned(k_codes, 16) || !iq::aligned(v_codes, 16) ||
+      !iq::aligned(k_norms, 16) || !iq::aligned(v_norms, 16) || !iq::aligned(out, 16) ||
+      !iq::aligned(seq_lens, 4) || !iq::aligned(quats, 16) || !iq::aligned(workspace, 256))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (!iq::plan_decode(batch, n_q_heads, n_kv_heads, max_seq_len, plan))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < plan->total_bytes) return IQ_ERR_WORKSPACE_TOO_SMALL;
+  return IQ_OK;
+}
+
+}  // namespace
+
+iq_status iq_compress_kv_paged(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+                               int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
+                               const float* quats, uint8_t* k_codes, float* k_norms,
+                               uint8_t* v_codes, float* v_norms, int64_t page_size,
+                               int64_t n_pages, const int32_t* block_tables, int64_t max_pages,
+                               int64_t dst_offset, hipStream_t stream) {
+  if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
+  if (dtype != IQ_DTYPE_F32 && dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
+  if (batch < 0 || n_kv_heads <= 0 || n_tokens < 0 || dst_offset < 0)
+    return IQ_ERR_INVALID_ARGUMENT;
+  iq::PageTable pt;
+  const iq_status ps = check_pages(n_kv_heads, page_size, n_pages, block_tables, max_pages, &pt);
+  if (ps != IQ_OK) return ps;
+  const int64_t capacity = max_pages * page_size;
+  if (dst_offset > capacity || n_tokens > capacity - dst_offset) return IQ_ERR_INVALID_ARGUMENT;
+  if (!iq::mul_ok(batch, n_kv_heads) || !iq::mul_ok(batch * n_kv_heads, n_tokens + 1) ||
+      !iq::mul_ok(batch * n_kv_heads * (n_tokens + 1), kDim))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (batch == 0 || n_tokens == 0) return IQ_OK;
+  if (k == nullptr && v == nullptr) return IQ_ERR_INVALID_ARGUMENT;
+  if (quats == nullptr || !iq::aligned(quats, 16)) return IQ_ERR_INVALID_ARGUMENT;
+  if (k && (!k_codes || !k_norms || !iq::aligned(k, 16) || !iq::aligned(k_codes, 16) ||
+            !iq::aligned(k_norms, 4)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (v && (!v_codes || !v_norms || !iq::aligned(v, 16) || !iq::aligned(v_codes, 16) ||
+            !iq::aligned(v_norms, 4)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  const hipError_t e = iq::launch_compress_paged(k, v, dtype, batch, n_kv_heads, n_tokens, quats,
+                                                 k_codes, k_norms, v_codes, v_norms, pt,
+                                                 dst_offset, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+iq_status iq_decode_attention_paged(const float* q, const uint8_t* k_codes,
+                                    const float* k_norms, const uint8_t* v_codes,
+                                    const float* v_norms, int64_t page_size, int64_t n_pages,
+                                    const int32_t* block_tables, int64_t max_pages,
+                                    const int32_t* seq_lens, int64_t max_seq_len,
+                                    const float* quats, int64_t batch, int64_t n_q_heads,
+                                    int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
+                                    float* out, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream) {
+  iq::PageTable pt;
+  iq_status st = check_pages(n_kv_heads, page_size, n_pages, block_tables, max_pages, &pt);
+  if (st != IQ_OK) return st;
+  iq::DecodePlan plan;
+  st = check_paged_decode(q, k_codes, k_norms, v_codes, v_norms, seq_lens, max_seq_len, quats,
+                          batch, n_q_heads, n_kv_heads, head_dim, out, workspace,
+                          workspace_bytes, pt, &plan);
+  if (st != IQ_OK) return st;
+  if (batch == 0) return IQ_OK;
+  float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
+  const hipError_t e = iq::launch_decode_g8(
+      plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, const_cast<uint8_t*>(k_codes),
+      const_cast<float*>(k_norms), const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms),
+      const_cast<int32_t*>(seq_lens), max_pages * page_size, max_seq_len, quats, batch,
+      n_kv_heads, resolve_scale(softmax_scale), out, parts, nullptr, &pt, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+iq_status iq_decode_step_paged(const float* q, const void* k_new, const void* v_new,
+                               iq_dtype dtype, uint8_t* k_codes, float* k_norms,
+                               uint8_t* v_codes, float* v_norms, int64_t page_size,
+                               int64_t n_pages, const int32_t* block_tables, int64_t max_pages,
+                               int32_t* seq_lens, int64_t max_seq_len, const float* quats,
+                               int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                               int64_t head_dim, float softmax_scale, float* out,
+                               void* workspace, size_t workspace_bytes, int32_t* status_dev,
+                               hipStream_t stream) {
+  if (dtype != IQ_DTYPE_F32 && dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
+  iq::PageTable pt;
+  iq_status st = check_pages(n_kv_heads, page_size, n_pages, block_tables, max_pages, &pt);
+  if (st != IQ_OK) return st;
+  iq::DecodePlan plan;
+  st = check_paged_decode(q, k_codes, k_norms, v_codes, v_norms, seq_lens, max_seq_len, quats,
+                          batch, n_q_heads, n_kv_heads, head_dim, out, workspace,
+                          workspace_bytes, pt, &plan);
+  if (st != IQ_OK) return st;
+  if (max_seq_len < 1) return IQ_ERR_INVALID_ARGUMENT;
+  if (!k_new || !v_new || !iq::aligned(k_new, 16) || !iq::aligned(v_new, 16) ||
+      (status_dev && !iq::aligned(status_dev, 4)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (batch == 0) return IQ_OK;
+  const iq::StepAppend append{k_new, v_new, dtype == IQ_DTYPE_F16 ? 1 : 0, status_dev};
+  float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
+  const hipError_t e = iq::launch_decode_g8(
+      plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes, k_norms, v_codes, v_norms,
+      seq_lens, max_pages * page_size, max_seq_len, quats, batch, n_kv_heads,
+      resolve_scale(softmax_scale), out, parts, &append, &pt, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
 iq_status iq_dequantize_kv(const uint8_t* k_codes, const float* k_norms,
                            const uint8_t* v_codes, const float* v_norms, const float* quats,
                            const int32_t* seq_lens, int64_t batch, int64_t n_kv_heads,

@@ -161,12 +161,14 @@ __device__ __forceinline__ void compress_one(const T* __restrict__ src, const f3
 
 // Bulk compression.  1-D grid of 256-thread workgroups:
 //   blockIdx.x = (which * (B*H) + bh) * chunks + chunk,  thread = token in chunk.
-template <typename T>
+// kPaged: the destination is a page pool; a token whose page index is
+// invalid is not written.
+template <typename T, bool kPaged>
 __global__ __launch_bounds__(kCompressThreads) void compress_kernel(
     const T* __restrict__ src0, const T* __restrict__ src1, const float* __restrict__ quats,
     uint8_t* __restrict__ codes0, float* __restrict__ norms0, uint8_t* __restrict__ codes1,
     float* __restrict__ norms1, int n_heads, int64_t n_bh, int64_t n_tokens, int64_t chunks,
-    int64_t capacity, int64_t dst_offset, Codebook cb) {
+    int64_t capacity, int64_t dst_offset, Codebook cb, PageTable pages) {
   __shared__ f32x4_t mtab[kNumBlocks * 4];
   const int64_t blk = blockIdx.x;
   const int64_t chunk = blk % chunks;
@@ -192,7 +194,11 @@ __global__ __launch_bounds__(kCompressThreads) void compress_kernel(
   const T* src = which ? src1 : src0;
   uint8_t* codes = which ? codes1 : codes0;
   float* norms = which ? norms1 : norms0;
-  const int64_t pos = bh * capacity + dst_offset + t;
+  int64_t pos = bh * capacity + dst_offset + t;
+  if constexpr (kPaged) {
+    pos = paged_record(pages, n_heads, static_cast<int>(bh / n_heads), h, dst_offset + t);
+    if (pos < 0) return;
+  }
   compress_one<T>(src + (bh * n_tokens + t) * kDim, mtab, codes + pos * kRecordBytes,
                   norms + pos, cb);
 }
@@ -255,11 +261,13 @@ __global__ void fill_zero_kernel(uint32_t* __restrict__ p, int64_t n_words) {
 
 }  // namespace
 
-hipError_t launch_compress(const void* k, const void* v, int dtype, int64_t batch,
-                           int64_t n_heads, int64_t n_tokens, const float* quats,
-                           uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
-                           float* v_norms, int64_t capacity, int64_t dst_offset,
-                           hipStream_t stream) {
+namespace {
+
+hipError_t launch_compress_any(const void* k, const void* v, int dtype, int64_t batch,
+                               int64_t n_heads, int64_t n_tokens, const float* quats,
+                               uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
+                               float* v_norms, int64_t capacity, int64_t dst_offset,
+                               const PageTable* pages, hipStream_t stream) {
   // slot 0 is whichever side is present first, slot 1 the other (if any)
   const void* s0 = k ? k : v;
   uint8_t* c0 = k ? k_codes : v_codes;
@@ -274,18 +282,42 @@ hipError_t launch_compress(const void* k, const void* v, int dtype, int64_t batc
   if (blocks == 0) return hipSuccess;
   const Codebook& cb = codebook();
   const dim3 grid(static_cast<unsigned>(blocks)), block(kCompressThreads);
+  const PageTable pt = pages ? *pages : PageTable{nullptr, 0, 16, 1};
+#define IQ_LAUNCH_COMPRESS(T_, P_)                                                             \
+  hipLaunchKernelGGL((compress_kernel<T_, P_>), grid, block, 0, stream,                         \
+                     static_cast<const T_*>(s0), static_cast<const T_*>(s1), quats, c0, n0, c1, \
+                     n1, static_cast<int>(n_heads), n_bh, n_tokens, chunks, capacity,           \
+                     dst_offset, cb, pt)
   if (dtype == IQ_DTYPE_F16) {
-    hipLaunchKernelGGL(compress_kernel<__half>, grid, block, 0, stream,
-                       static_cast<const __half*>(s0), static_cast<const __half*>(s1), quats, c0,
-                       n0, c1, n1, static_cast<int>(n_heads), n_bh, n_tokens, chunks, capacity,
-                       dst_offset, cb);
+    if (pages) IQ_LAUNCH_COMPRESS(__half, true);
+    else IQ_LAUNCH_COMPRESS(__half, false);
   } else {
-    hipLaunchKernelGGL(compress_kernel<float>, grid, block, 0, stream,
-                       static_cast<const float*>(s0), static_cast<const float*>(s1), quats, c0,
-                       n0, c1, n1, static_cast<int>(n_heads), n_bh, n_tokens, chunks, capacity,
-                       dst_offset, cb);
+    if (pages) IQ_LAUNCH_COMPRESS(float, true);
+    else IQ_LAUNCH_COMPRESS(float, false);
   }
+#undef IQ_LAUNCH_COMPRESS
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_compress(const void* k, const void* v, int dtype, int64_t batch,
+                           int64_t n_heads, int64_t n_tokens, const float* quats,
+                           uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
+                           float* v_norms, int64_t capacity, int64_t dst_offset,
+                           hipStream_t stream) {
+  return launch_compress_any(k, v, dtype, batch, n_heads, n_tokens, quats, k_codes, k_norms,
+                             v_codes, v_norms, capacity, dst_offset, nullptr, stream);
+}
+
+hipError_t launch_compress_paged(const void* k, const void* v, int dtype, int64_t batch,
+                                 int64_t n_heads, int64_t n_tokens, const float* quats,
+                                 uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
+                                 float* v_norms, const PageTable& pages, int64_t dst_offset,
+                                 hipStream_t stream) {
+  return launch_compress_any(k, v, dtype, batch, n_heads, n_tokens, quats, k_codes, k_norms,
+                             v_codes, v_norms, pages.max_pages * pages.page_size, dst_offset,
+                             &pages, stream);
 }
 
 hipError_t launch_append(const void* k, const void* v, int dtype, int64_t batch,

@@ -279,24 +279,35 @@ struct WaveStage {
 // batch the start is a scalar and the lane offsets are constants: one
 // straight-line sequence for every wave, so the compiler keeps exact counts
 // of the loads in flight.
-template <int NB>
+// kPaged: batch i of the wave lies at record index dlt[i] + (its position)
+// of the pools (dlt[i] = the batch page's record base minus the page's first
+// logical position); contiguous caches use the row pointers as they are.
+template <int NB, bool kPaged>
 __device__ __forceinline__ void load_keys(const uint8_t* kc, const float* kn, const float* vn,
-                                          int wbase, int clamp16, int lane, int col, int grp,
-                                          uint32_t (&kw)[NB][3], f32x4_t& ksl, f32x4_t& vsl) {
+                                          const int64_t (&dlt)[NB], int wbase, int clamp16,
+                                          int lane, int col, int grp, uint32_t (&kw)[NB][3],
+                                          f32x4_t& ksl, f32x4_t& vsl) {
   const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
   // scales: lane j -> batch j / 4 (clamped like the batches), group j % 4
   {
     const int jb = lane >> 2 < NB ? lane >> 2 : NB - 1;
     const int tj = (wbase + 16 * jb < clamp16 ? wbase + 16 * jb : clamp16) + 4 * (lane & 3);
-    ksl = *reinterpret_cast<const f32x4_t*>(kn + tj);
-    vsl = *reinterpret_cast<const f32x4_t*>(vn + tj);
+    int64_t d = 0;
+    if constexpr (kPaged) {
+      d = dlt[0];
+#pragma unroll
+      for (int i = 1; i < NB; ++i) d = jb == i ? dlt[i] : d;
+    }
+    ksl = *reinterpret_cast<const f32x4_t*>(kn + d + tj);
+    vsl = *reinterpret_cast<const f32x4_t*>(vn + d + tj);
   }
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
     const int tb = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
+    const uint8_t* kb = kPaged ? kc + dlt[i] * kRecordBytes : kc;
     const uint32_t* p =
-        reinterpret_cast<const uint32_t*>(kc + static_cast<uint32_t>(tb * kRecordBytes) + koff);
+        reinterpret_cast<const uint32_t*>(kb + static_cast<uint32_t>(tb * kRecordBytes) + koff);
     kw[i][0] = p[0];
     kw[i][1] = p[1];
     kw[i][2] = p[2];
@@ -335,10 +346,11 @@ __device__ __forceinline__ void load_value_batch(const uint8_t* vc, int tb, uint
 // (lane (t, gk) writes its 12 bytes of record t, lane (u, grp) reads the
 // 8-byte window holding bytes 3u..3u+2 of records 4 grp + r); the wave's own
 // LDS operations complete in order.
-template <int NB, int NBX, bool kFull, bool kWide>
+template <int NB, int NBX, bool kFull, bool kWide, bool kPaged>
 __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
                                             uint32_t (&vw)[NB][3], const uint8_t* vc,
-                                            uint32_t koff, const int (&tb)[NB], WaveStage& st,
+                                            uint32_t koff, const int (&tb)[NB],
+                                            const int64_t (&dlt)[NB], WaveStage& st,
                                             const u32x4_t (&qb)[4],
                                             const uint32_t* lut, int col, int grp, int nvalid,
                                             int vdw, uint32_t vsh, float qdown, float& m_run,
@@ -351,7 +363,7 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
   for (int i = 0; i < NBX; ++i) {
     if (!kFull && 16 * i >= nvalid) break;
     __builtin_amdgcn_sched_barrier(kNoVmemAcross);
-    load_value_batch(vc, tb[i], koff, vw[i]);
+    load_value_batch(kPaged ? vc + dlt[i] * kRecordBytes : vc, tb[i], koff, vw[i]);
     __builtin_amdgcn_sched_barrier(kNoVmemAcross);
     const uint32_t w0 = kw[i][0], w1 = kw[i][1], w2 = kw[i][2];
     // fields F = 0..15 at bit 6F of the 96-bit slice w0:w1:w2: those at
@@ -482,7 +494,11 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
 // at capacity, or at or past max_seq_len).  No attention workgroup reads the
 // records being written, and seq_lens is advanced by the merge kernel after
 // every workgroup has read it.
-template <int NB, bool kAppend, bool kWide>
+//
+// kPaged: the cache is a page pool (PageTable); capacity is then the logical
+// capacity max_pages * page_size, and every batch of 16 positions and the
+// new token's slot are located through the page table.
+template <int NB, bool kAppend, bool kWide, bool kPaged>
 __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     const float* __restrict__ q, uint8_t* __restrict__ k_codes, float* __restrict__ k_norms,
     uint8_t* __restrict__ v_codes, float* __restrict__ v_norms,
@@ -490,7 +506,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     float* __restrict__ partials, float* __restrict__ out, int64_t capacity, int max_seq_len,
     int n_kv_heads, int n_splits, int split_len, float qscale, Codebook cb,
     const void* __restrict__ k_new, const void* __restrict__ v_new, int new_f16,
-    int32_t* __restrict__ status) {
+    int32_t* __restrict__ status, PageTable pages) {
   // All LDS of the kernel in one object, the pair table first (address 0:
   // a lookup address is just field * 4).
   struct Smem {
@@ -542,7 +558,9 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   float* out_bg =
       out + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * kHeads) * kDim;
   float* part_bg = partials + static_cast<int64_t>(bg) * n_parts * (kHeads * kPart);
-  const int64_t row = static_cast<int64_t>(bg) * capacity;
+  // contiguous: the (b, g) row; paged: the pools (positions are placed by
+  // the per-batch deltas)
+  const int64_t row = kPaged ? 0 : static_cast<int64_t>(bg) * capacity;
   uint8_t* kc = k_codes + row * kRecordBytes;
   uint8_t* vc = v_codes + row * kRecordBytes;
 
@@ -578,13 +596,15 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
       const int which = wave - 4;
       if (lane < kRecordWords) sm.new_rec[which][lane] = wc.word;
       if (lane == 0) sm.new_scale[which] = wc.scale;
-      if (appended) {
-        uint8_t* codes = which == 0 ? kc : vc;
-        float* norms = (which == 0 ? k_norms : v_norms) + row;
+      // record index of the new token (its page's slot, or the row position)
+      const int64_t rec =
+          !appended ? -1 : (kPaged ? paged_record(pages, n_kv_heads, b, g, seq0) : row + seq0);
+      if (rec >= 0) {
+        uint8_t* codes = which == 0 ? k_codes : v_codes;
+        float* norms = which == 0 ? k_norms : v_norms;
         if (lane < kRecordWords)
-          reinterpret_cast<uint32_t*>(codes + static_cast<int64_t>(seq0) * kRecordBytes)[lane] =
-              wc.word;
-        if (lane == 0) norms[seq0] = wc.scale;
+          reinterpret_cast<uint32_t*>(codes + rec * kRecordBytes)[lane] = wc.word;
+        if (lane == 0) norms[rec] = wc.scale;
       }
     }
     if (tid < 64) {
@@ -658,11 +678,24 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   clamp16 = clamp16 > 0 ? clamp16 : 0;
   const float* kn = k_norms + row;
   const float* vn = v_norms + row;
+  // paged: each batch's record delta (its page's record base minus the
+  // page's first logical position; page 0 for an invalid page index)
+  int64_t dlt[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    dlt[i] = 0;
+    if constexpr (kPaged) {
+      const int t = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
+      const int64_t rec = paged_record(pages, n_kv_heads, b, g, t);
+      const int slot = t % pages.page_size;
+      dlt[i] = (rec >= 0 ? rec : static_cast<int64_t>(g) * pages.page_size + slot) - t;
+    }
+  }
 
   // ---- the cache loads (keys and scales now, values as the scores proceed)
   uint32_t kw[NB][3], vw[NB][3];
   f32x4_t ksl, vsl;
-  load_keys<NB>(kc, kn, vn, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
+  load_keys<NB, kPaged>(kc, kn, vn, dlt, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
   const int vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
   const uint32_t vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));   // 0..40
 
@@ -755,14 +788,14 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if (nvalid == 16 * NB)
-    attend_wave<NB, NB, true, kWide>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp,
+    attend_wave<NB, NB, true, kWide, kPaged>(kw, vw, vc, koff, tb, dlt, stage[wave], qb, lut, col, grp,
                                      nvalid, vdw, vsh, qdown, m_run, l_run, vmax, o_acc);
   else if (NB > 1 && nvalid == 16 * (NB - 1))
-    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true, kWide>(kw, vw, vc, koff, tb, stage[wave], qb,
+    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true, kWide, kPaged>(kw, vw, vc, koff, tb, dlt, stage[wave], qb,
                                                         lut, col, grp, nvalid, vdw, vsh, qdown,
                                                         m_run, l_run, vmax, o_acc);
   else if (nvalid > 0)
-    attend_wave<NB, NB, false, kWide>(kw, vw, vc, koff, tb, stage[wave], qb, lut, col, grp,
+    attend_wave<NB, NB, false, kWide, kPaged>(kw, vw, vc, koff, tb, dlt, stage[wave], qb, lut, col, grp,
                                       nvalid, vdw, vsh, qdown, m_run, l_run, vmax, o_acc);
 
   // ---- merge the 8 waves in LDS ---------------------------------------------
@@ -964,7 +997,7 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                             int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                             const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
                             float* out, float* partials, const StepAppend* append,
-                            hipStream_t stream) {
+                            const PageTable* pages, hipStream_t stream) {
   // partials per (sequence, KV head): the splits, and the fused step's new
   // token
   const int64_t n_parts = append ? n_splits + 1 : n_splits;
@@ -985,17 +1018,24 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   const void* v_new = append ? append->v_new : nullptr;
   const int new_f16 = append ? append->f16 : 0;
   int32_t* status = append ? append->status : nullptr;
-#define IQ_LAUNCH_G8_W(NB_, APP_, WIDE_)                                                         \
-  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_>), grid, block, lds_pad, stream, q,      \
-                     k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials, out,        \
+  const PageTable pt = pages ? *pages : PageTable{nullptr, 0, 16, 1};
+#define IQ_LAUNCH_G8_WP(NB_, APP_, WIDE_, PAGED_)                                                \
+  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_, PAGED_>), grid, block, lds_pad, stream, \
+                     q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials, out,     \
                      capacity, static_cast<int>(max_seq_len), static_cast<int>(n_kv_heads),     \
                      static_cast<int>(n_splits), static_cast<int>(split_len), qscale, cb,      \
-                     k_new, v_new, new_f16, status)
+                     k_new, v_new, new_f16, status, pt)
+#define IQ_LAUNCH_G8_W(NB_, APP_, WIDE_)        \
+  if (pages) {                                  \
+    IQ_LAUNCH_G8_WP(NB_, APP_, WIDE_, true);    \
+  } else {                                      \
+    IQ_LAUNCH_G8_WP(NB_, APP_, WIDE_, false);   \
+  }
 #define IQ_LAUNCH_G8(NB_, APP_)          \
   if (wide) {                            \
-    IQ_LAUNCH_G8_W(NB_, APP_, true);     \
+    IQ_LAUNCH_G8_W(NB_, APP_, true)      \
   } else {                               \
-    IQ_LAUNCH_G8_W(NB_, APP_, false);    \
+    IQ_LAUNCH_G8_W(NB_, APP_, false)     \
   }
 #define IQ_LAUNCH_G8_NB(APP_)            \
   switch (nb) {                          \
@@ -1013,6 +1053,7 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
 #undef IQ_LAUNCH_G8_NB
 #undef IQ_LAUNCH_G8
 #undef IQ_LAUNCH_G8_W
+#undef IQ_LAUNCH_G8_WP
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // the partials of every (sequence, query head) merged by a second launch,

@@ -28,6 +28,29 @@ struct Codebook {
 // Computed on first use (host), immutable afterwards.
 const Codebook& codebook();
 
+// A paged cache: records of logical position t of (sequence b, KV head g)
+// live in page tables[b * max_pages + t / page_size], slot t % page_size, of
+// pools laid out [n_pages][n_kv_heads][page_size][48] (codes) and
+// [n_pages][n_kv_heads][page_size] (scales).  page_size is a multiple of 16,
+// so a batch of 16 positions never straddles a page.  A page index outside
+// [0, n_pages) is a caller error: reads then use page 0 and writes are
+// skipped, so no access leaves the pools.
+struct PageTable {
+  const int32_t* tables;   // [batch][max_pages]
+  int64_t max_pages;
+  int32_t page_size;
+  int32_t n_pages;
+};
+
+// Record index (into the pools viewed as [n_pages * n_kv_heads * page_size]
+// records) of logical position t, or -1 if its page index is invalid.
+__device__ __forceinline__ int64_t paged_record(const PageTable& pt, int n_kv_heads, int b,
+                                                int g, int64_t t) {
+  const int32_t page = pt.tables[static_cast<int64_t>(b) * pt.max_pages + t / pt.page_size];
+  if (page < 0 || page >= pt.n_pages) return -1;
+  return (static_cast<int64_t>(page) * n_kv_heads + g) * pt.page_size + t % pt.page_size;
+}
+
 // Split-K plan for one decode call.  Deterministic function of the shapes so
 // that iq_decode_workspace_bytes and iq_decode_attention agree.
 struct DecodePlan {
@@ -51,6 +74,14 @@ hipError_t launch_compress(const void* k, const void* v, int dtype, int64_t batc
                            uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
                            float* v_norms, int64_t capacity, int64_t dst_offset,
                            hipStream_t stream);
+
+// Bulk compression into a paged cache: tokens [0, n_tokens) of every
+// sequence to logical positions dst_offset ..
+hipError_t launch_compress_paged(const void* k, const void* v, int dtype, int64_t batch,
+                                 int64_t n_heads, int64_t n_tokens, const float* quats,
+                                 uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
+                                 float* v_norms, const PageTable& pages, int64_t dst_offset,
+                                 hipStream_t stream);
 
 hipError_t launch_append(const void* k, const void* v, int dtype, int64_t batch,
                          int64_t n_heads, const float* quats, uint8_t* k_codes,
@@ -79,12 +110,14 @@ hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 
 void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
              int64_t* n_splits, int64_t* split_len);
+// pages: null for a contiguous cache ([B][H_kv][capacity] records), else
+// the page table (capacity is then max_pages * page_size).
 hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const float* q,
                             uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
                             int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                             const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
                             float* out, float* partials, const StepAppend* append,
-                            hipStream_t stream);
+                            const PageTable* pages, hipStream_t stream);
 
 // Reconstruct-then-compute baseline (Fig. 1 top): materialize the packed
 // cache as fp16 or fp32 vectors, and decode attention on an fp16 cache.

@@ -244,3 +244,45 @@ def test_decode_f16_validation():
     assert n > 0 and n % 256 == 0
     assert L.iq_decode_f16_workspace_bytes(1, 36, 4, 32768, 128) == 0
     assert L.iq_decode_f16_workspace_bytes(1, 32, 4, 32768, 64) == 0
+
+
+def _paged_decode(**kw):
+    args = dict(q=A, kc=A, kn=A, vc=B, vn=B, page=64, n_pages=8, bt=A, max_pages=4, seq=A,
+                msl=256, quats=A, batch=1, hq=16, hkv=2, hd=128, scale=0.0, out=A, ws=A,
+                wsb=1 << 30)
+    args.update(kw)
+    return L.iq_decode_attention_paged(args["q"], args["kc"], args["kn"], args["vc"],
+                                       args["vn"], args["page"], args["n_pages"], args["bt"],
+                                       args["max_pages"], args["seq"], args["msl"],
+                                       args["quats"], args["batch"], args["hq"], args["hkv"],
+                                       args["hd"], args["scale"], args["out"], args["ws"],
+                                       args["wsb"], None)
+
+
+def test_paged_decode_validation():
+    assert _paged_decode(page=48) == 1           # not a multiple of 16
+    assert _paged_decode(page=0) == 1
+    assert _paged_decode(n_pages=0) == 1
+    assert _paged_decode(max_pages=0) == 1
+    assert _paged_decode(bt=None) == 1
+    assert _paged_decode(msl=257) == 1           # beyond max_pages * page_size
+    assert _paged_decode(hq=8) == 2              # group 4: not the matrix-core path
+    assert _paged_decode(hd=64) == 2
+    assert _paged_decode(batch=70000) == 1
+    assert _paged_decode(max_pages=1 << 40) == 1
+    assert _paged_decode(wsb=16) == 3
+    assert _paged_decode(batch=0) == 0           # empty batch: nothing launched
+
+
+def test_paged_compress_validation():
+    def call(**kw):
+        a = dict(k=A, v=B, dtype=1, batch=1, hkv=2, n=10, hd=128, quats=A, page=64,
+                 n_pages=4, bt=A, max_pages=2, off=0)
+        a.update(kw)
+        return L.iq_compress_kv_paged(a["k"], a["v"], a["dtype"], a["batch"], a["hkv"], a["n"],
+                                      a["hd"], a["quats"], A, A, B, B, a["page"], a["n_pages"],
+                                      a["bt"], a["max_pages"], a["off"], None)
+    assert call(off=120) == 1                    # 120 + 10 > 2 * 64
+    assert call(page=40) == 1
+    assert call(dtype=7) == 2
+    assert call(n=0) == 0

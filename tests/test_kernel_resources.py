@@ -49,9 +49,9 @@ def test_decode_g8_occupancy_budget(tmp_path):
     pad = eval(re.search(r"kOneWorkgroupPadBytes\s*=\s*([^;]+);", src).group(1))
     ks = _kernels(asm)
     dec = {n: v for n, v in ks.items() if "decode_g8_kernel" in n}
-    assert len(dec) == 20, sorted(dec)
+    assert len(dec) == 40, sorted(dec)
     for name, (vg, lds, priv) in dec.items():
-        m = re.search(r"decode_g8_kernelILi(\d)ELb(\d)ELb(\d)EE", name)
+        m = re.search(r"decode_g8_kernelILi(\d)ELb(\d)ELb(\d)ELb(\d)EE", name)
         nb, wide = int(m.group(1)), m.group(3) == "1"
         assert priv == 0, f"{name}: scratch {priv}"
         assert vg <= 256, f"{name}: {vg} VGPRs"
@@ -66,7 +66,7 @@ def test_decode_g8_occupancy_budget(tmp_path):
 def test_compress_kernel_has_no_scratch(tmp_path):
     ks = _kernels(_device_asm("iq_compress.hip", tmp_path))
     comp = {n: v for n, v in ks.items() if "compress_kernel" in n}
-    assert len(comp) == 2
+    assert len(comp) == 4
     for name, (vg, lds, priv) in comp.items():
         assert priv == 0, f"{name}: scratch {priv}"
         assert vg <= 256, f"{name}: {vg} VGPRs"
