@@ -27,6 +27,9 @@ the default is the one above):
             of 4 x 32768 held-out keys with the same channel scales, compressed
             and materialized by the library's kernels, for the fitted, random,
             single-quaternion and Hadamard-only parameters;
+  paged     the varlen shape on a paged cache (iq_decode_step_paged; pages of
+            --page-size positions, physical pages randomly permuted), then
+            on contiguous caches with the same lengths for comparison;
   baseline32k  the 32K shape above through the reconstruct-then-compute
             pipeline the packed path replaces (Fig. 1 top): decode attention
             on an fp16 cache, materialization of the packed cache as fp16
@@ -58,7 +61,7 @@ def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--workload", choices=("step32k", "varlen", "compress", "append8k",
-                                          "baseline32k", "rotation_fit"),
+                                          "baseline32k", "rotation_fit", "paged"),
                    default="step32k")
     p.add_argument("--steps", type=int, default=None,
                    help="timed steps (default: 4800; varlen 240; compress 20; append8k 1000)")
@@ -67,6 +70,8 @@ def parse():
     p.add_argument("--layers", type=int, default=None,
                    help="distinct layer caches cycled (default: 48; varlen 3)")
     p.add_argument("--context", type=int, default=32768)
+    p.add_argument("--page-size", type=int, default=16,
+                   help="positions per page of the paged workload (a power of two, >= 16)")
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -75,13 +80,15 @@ def parse():
     a = p.parse_args()
     defaults = {"step32k": (4800, 48), "varlen": (240, 3), "compress": (20, 1),
                 "append8k": (1000, 48), "baseline32k": (960, 48),
-                "rotation_fit": (1, 1)}[a.workload]
+                "rotation_fit": (1, 1), "paged": (240, 3)}[a.workload]
     if a.steps is None:
         a.steps = defaults[0]
     if a.warmup is None:
         a.warmup = max(1, a.steps // 10)
     if a.layers is None:
         a.layers = defaults[1]
+    if a.page_size < 16 or a.page_size & (a.page_size - 1):
+        p.error("--page-size must be a power of two, at least 16")
     return a
 
 
@@ -232,6 +239,60 @@ def make_varlen_layers(api, synth, w, n_layers, lengths, capacity, seed, dev, sl
     return quats, layers
 
 
+def make_paged_layers(api, synth, w, n_layers, lengths, capacity, page, seed, dev,
+                      slice_b=8):
+    """Per layer: page pools for the varlen shape, located through one page
+    table shared by all layers (as a serving engine keeps one page list per
+    sequence).  Sequence b maps ceil((its length + growth) / page) logical
+    pages; the physical pages of all sequences are one random permutation of
+    the pool (no two neighbours in a sequence are adjacent in memory, as in
+    a long-running server).  Tokens are compressed straight into the pages
+    (iq_compress_kv_paged)."""
+    import numpy as np
+    import torch
+
+    layers = []
+    quats = api.iq_make_rotation(w.rotation_seed, w.n_kv_heads).to(dev)
+    max_pages = capacity // page
+    need = [min(max_pages, -(-(int(n) + capacity - int(lengths.max())) // page))
+            for n in lengths]
+    n_pages = int(sum(need))
+    perm = np.random.default_rng([seed, 11]).permutation(n_pages).astype(np.int32)
+    tables = np.full((w.batch, max_pages), -1, np.int32)
+    k0 = 0
+    for b, m in enumerate(need):
+        tables[b, :m] = perm[k0:k0 + m]
+        k0 += m
+    bt = torch.from_numpy(tables).to(dev)
+    for li in range(n_layers):
+        g = torch.Generator(device=dev)
+        g.manual_seed(seed * 100003 + 7919 * li + 1)
+        pool = api.alloc_paged_cache(n_pages, w.n_kv_heads, page, dev)
+        scales = []
+        for stream in (0, 1):
+            sc = synth.channel_scales(synth.rng(seed + li, w.wid, stream), w.n_kv_heads)
+            scales.append(torch.from_numpy(sc).to(dev))
+        for b0 in range(0, w.batch, slice_b):
+            b1 = min(w.batch, b0 + slice_b)
+            t = int(lengths[b0:b1].max())
+            kv = []
+            for which in (0, 1):
+                x = torch.randn((b1 - b0, w.n_kv_heads, t, 128), generator=g, device=dev)
+                kv.append((x * scales[which][None, :, None, :]).half())
+            api.iq_compress_kv_paged(kv[0], kv[1], quats, pool, bt[b0:b1])
+            del kv
+        pool["seq_lens"] = torch.from_numpy(lengths).to(dev)
+        k_new = (torch.randn((w.batch, w.n_kv_heads, 128), generator=g, device=dev)
+                 * scales[0][None]).half()
+        v_new = (torch.randn((w.batch, w.n_kv_heads, 128), generator=g, device=dev)
+                 * scales[1][None]).half()
+        q = torch.randn((w.batch, w.n_q_heads, 128), generator=g, device=dev)
+        out = torch.empty((w.batch, w.n_q_heads, 128), device=dev)
+        layers.append(dict(cache=pool, tables=bt, k_new=k_new, v_new=v_new, q=q, out=out))
+    torch.cuda.synchronize()
+    return quats, layers
+
+
 def time_steps(api, layers, quats, ws, capacity, args):
     """Warm-up, then `args.steps` fused steps (append + attention) cycling the
     layers, replayed from HIP graphs and timed with HIP events on the replay
@@ -244,7 +305,15 @@ def time_steps(api, layers, quats, ws, capacity, args):
     def step(li, append=True):
         L = layers[li]
         c = L["cache"]
-        if append:
+        if "tables" in L:
+            if append:
+                api.iq_decode_step_paged(L["q"], L["k_new"], L["v_new"], c, L["tables"],
+                                         c["seq_lens"], quats, out=L["out"], workspace=ws,
+                                         max_seq_len=capacity)
+            else:
+                api.iq_decode_attention_paged(L["q"], c, L["tables"], c["seq_lens"], quats,
+                                              out=L["out"], workspace=ws, max_seq_len=capacity)
+        elif append:
             api.iq_decode_step(L["q"], L["k_new"], L["v_new"], c["k_codes"], c["k_norms"],
                                c["v_codes"], c["v_norms"], c["seq_lens"], quats, out=L["out"],
                                workspace=ws, max_seq_len=capacity)
@@ -406,6 +475,44 @@ def run_varlen(args, torch, api, synth, dev):
         f"algorithmic bytes = {BYTES_PER_TOKEN_HEAD} B x attended positions x KV heads + the "
         "appended tokens' inputs and records",
         {"lengths_min": int(lengths.min()), "lengths_max": int(lengths.max())})
+
+
+def run_paged(args, torch, api, synth, dev):
+    """The varlen shape on page pools (iq_decode_step_paged), then the same
+    lengths on contiguous caches (iq_decode_step) for comparison."""
+    w = synth.WORKLOADS[3]
+    nl = args.layers
+    page = args.page_size
+    lengths = synth.context_lengths(args.seed, w)
+    total_visits = math.ceil((args.warmup + args.steps) / nl) + 2
+    capacity = (int(lengths.max()) + total_visits + page + page - 1) // page * page
+    print(f"# building {nl} paged layer caches (batch {w.batch}, page {page})",
+          file=sys.stderr, flush=True)
+    quats, layers = make_paged_layers(api, synth, w, nl, lengths, capacity, page, args.seed,
+                                      dev)
+    ws = api.alloc_workspace(w.batch, w.n_q_heads, w.n_kv_heads, capacity, dev)
+    us_per_step, decode_us, wall = time_steps(api, layers, quats, ws, capacity, args)
+    result = step_result(
+        "paged batched varlen decode µs/step + achieved HBM GB/s on packed 3-bit KV",
+        f"batched serving decode step (append + attention) on a paged cache ({page}-position "
+        f"pages, randomly permuted pool, one page table for all layers), batch {w.batch}, {w.n_q_heads} query heads, "
+        f"{w.n_kv_heads} KV heads, head_dim 128, contexts uniform in [{w.varlen[0]}, "
+        f"{w.varlen[1]}] (seeded); {nl} distinct layer pools cycled",
+        w, layers, nl, us_per_step, decode_us, wall, args,
+        "iq_decode_step_paged per call = decode_g8_kernel<NB, append, wide, paged> + "
+        f"merge_g8_kernel; algorithmic bytes = {BYTES_PER_TOKEN_HEAD} B x attended positions x "
+        "KV heads + the appended tokens' inputs and records",
+        {"page_size": page, "lengths_min": int(lengths.min()),
+         "lengths_max": int(lengths.max())})
+    del layers, ws
+    torch.cuda.empty_cache()
+    print("# contiguous caches, same lengths", file=sys.stderr, flush=True)
+    quats, layers = make_varlen_layers(api, synth, w, nl, lengths, capacity, args.seed, dev)
+    ws = api.alloc_workspace(w.batch, w.n_q_heads, w.n_kv_heads, capacity, dev)
+    c_us, c_dec, _ = time_steps(api, layers, quats, ws, capacity, args)
+    result["contiguous"] = {"us_per_step": round(c_us, 3), "decode_us": round(c_dec, 3),
+                            "paged_over_contiguous": round(us_per_step / c_us, 4)}
+    return result
 
 
 def run_append8k(args, torch, api, synth, dev):
@@ -749,7 +856,7 @@ def main():
         del src, dst
     run = {"step32k": run_step32k, "varlen": run_varlen, "compress": run_compress,
            "append8k": run_append8k, "baseline32k": run_baseline32k,
-           "rotation_fit": run_rotation_fit}[args.workload]
+           "rotation_fit": run_rotation_fit, "paged": run_paged}[args.workload]
     print(json.dumps(run(args, torch, api, synth, dev)), flush=True)
 
 

@@ -290,7 +290,7 @@ iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, i
  *   block_tables      : device int32 [batch][max_pages]: logical position t of
  *                       sequence b lives in page block_tables[b][t / page_size],
  *                       slot t % page_size;
- *   page_size         : positions per page, a multiple of 16, >= 16;
+ *   page_size         : positions per page, a power of two, 16 .. 2^20;
  *   capacity          : max_pages * page_size (logical positions per
  *                       sequence), with capacity * 48 < 2^31.
  * A page index outside [0, n_pages) is a caller error: reads then use page 0

@@ -365,8 +365,10 @@ namespace {
 // Checks shared by the paged entry points; fills the page table.
 iq_status check_pages(int64_t n_kv_heads, int64_t page_size, int64_t n_pages,
                       const int32_t* block_tables, int64_t max_pages, iq::PageTable* pt) {
-  if (page_size < 16 || page_size % 16 || page_size > (int64_t(1) << 20))
+  if (page_size < 16 || page_size > (int64_t(1) << 20) || (page_size & (page_size - 1)))
     return IQ_ERR_INVALID_ARGUMENT;
+  int32_t shift = 0;
+  while ((int64_t(1) << shift) < page_size) ++shift;
   if (n_pages < 1 || n_pages > 0x7fffffff || max_pages < 1 || block_tables == nullptr ||
       !iq::aligned(block_tables, 4))
     return IQ_ERR_INVALID_ARGUMENT;
@@ -376,8 +378,7 @@ iq_status check_pages(int64_t n_kv_heads, int64_t page_size, int64_t n_pages,
   if (!iq::mul_ok(n_pages, n_kv_heads) || !iq::mul_ok(n_pages * n_kv_heads, page_size) ||
       !iq::mul_ok(n_pages * n_kv_heads * page_size, iq::kRecordBytes))
     return IQ_ERR_INVALID_ARGUMENT;
-  *pt = iq::PageTable{block_tables, max_pages, static_cast<int32_t>(page_size),
-                      static_cast<int32_t>(n_pages)};
+  *pt = iq::PageTable{block_tables, max_pages, shift, static_cast<int32_t>(n_pages)};
   return IQ_OK;
 }
 
@@ -390,7 +391,7 @@ iq_status check_paged_decode(const float* q, const void* k_codes, const float* k
                              iq::DecodePlan* plan) {
   if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
   if (batch < 0 || n_kv_heads <= 0 || n_q_heads <= 0 || max_seq_len < 0 ||
-      max_seq_len > pt.max_pages * pt.page_size || batch > 65535 || n_kv_heads > 65535)
+      max_seq_len > (pt.max_pages << pt.page_shift) || batch > 65535 || n_kv_heads > 65535)
     return IQ_ERR_INVALID_ARGUMENT;
   // paged caches run on the matrix-core path: 8 query heads per KV head
   if (n_q_heads != 8 * n_kv_heads) return IQ_ERR_UNSUPPORTED;

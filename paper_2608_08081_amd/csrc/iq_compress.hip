@@ -282,7 +282,7 @@ hipError_t launch_compress_any(const void* k, const void* v, int dtype, int64_t 
   if (blocks == 0) return hipSuccess;
   const Codebook& cb = codebook();
   const dim3 grid(static_cast<unsigned>(blocks)), block(kCompressThreads);
-  const PageTable pt = pages ? *pages : PageTable{nullptr, 0, 16, 1};
+  const PageTable pt = pages ? *pages : PageTable{nullptr, 0, 4, 1};
 #define IQ_LAUNCH_COMPRESS(T_, P_)                                                             \
   hipLaunchKernelGGL((compress_kernel<T_, P_>), grid, block, 0, stream,                         \
                      static_cast<const T_*>(s0), static_cast<const T_*>(s1), quats, c0, n0, c1, \
@@ -316,7 +316,7 @@ hipError_t launch_compress_paged(const void* k, const void* v, int dtype, int64_
                                  float* v_norms, const PageTable& pages, int64_t dst_offset,
                                  hipStream_t stream) {
   return launch_compress_any(k, v, dtype, batch, n_heads, n_tokens, quats, k_codes, k_norms,
-                             v_codes, v_norms, pages.max_pages * pages.page_size, dst_offset,
+                             v_codes, v_norms, (pages.max_pages << pages.page_shift), dst_offset,
                              &pages, stream);
 }
 

@@ -654,6 +654,15 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   // from the other workgroups.
   int seq0 = 0;
   int lim = start + split_len < max_seq_len ? start + split_len : max_seq_len;
+  // start of the wave's last batch before lim (the clamp of the loads):
+  // lim <= max_seq_len <= capacity, a multiple of 16, so every loaded batch
+  // lies in the row (in a mapped or the fallback page when paged)
+  auto last_batch = [&](int l) {
+    int c = (l > 0 ? l - 1 : 0) & ~15;
+    c = c < wbase + 16 * (nb_w - 1) ? c : wbase + 16 * (nb_w - 1);
+    return c > 0 ? c : 0;
+  };
+  int clamp16 = last_batch(lim);
   if constexpr (kWide) {
     seq0 = seq_lens[b];
     const int seq_w = seq0 < 0 ? 0 : (seq0 > max_seq_len ? max_seq_len : seq0);
@@ -669,28 +678,36 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
       return;
     }
     lim = lim < seq_w ? lim : seq_w;
+    clamp16 = last_batch(lim);
   }
-  // start of the wave's last batch before lim (the clamp of the loads):
-  // lim <= max_seq_len <= capacity, a multiple of 16, so every loaded batch
-  // lies in the row
-  int clamp16 = (lim > 0 ? lim - 1 : 0) & ~15;
-  clamp16 = clamp16 < wbase + 16 * (nb_w - 1) ? clamp16 : wbase + 16 * (nb_w - 1);
-  clamp16 = clamp16 > 0 ? clamp16 : 0;
-  const float* kn = k_norms + row;
-  const float* vn = v_norms + row;
   // paged: each batch's record delta (its page's record base minus the
-  // page's first logical position; page 0 for an invalid page index)
+  // page's first logical position; page 0 for an invalid page index).  All
+  // NB table entries are read before any is used, and an invalid entry is
+  // replaced by a select, so the reads go out together (one round trip).
+  // In grids of several rounds they follow the length read: issued beside
+  // it, they would hold every empty split until they return.
   int64_t dlt[NB];
 #pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    dlt[i] = 0;
-    if constexpr (kPaged) {
+  for (int i = 0; i < NB; ++i) dlt[i] = 0;
+  if constexpr (kPaged) {
+    const int32_t* trow = pages.tables + static_cast<int64_t>(b) * pages.max_pages;
+    int32_t pg[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
       const int t = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
-      const int64_t rec = paged_record(pages, n_kv_heads, b, g, t);
-      const int slot = t % pages.page_size;
-      dlt[i] = (rec >= 0 ? rec : static_cast<int64_t>(g) * pages.page_size + slot) - t;
+      pg[i] = trow[t >> pages.page_shift];
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int t = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
+      const int64_t page =
+          static_cast<uint32_t>(pg[i]) < static_cast<uint32_t>(pages.n_pages) ? pg[i] : 0;
+      dlt[i] = ((page * n_kv_heads + g) << pages.page_shift) -
+               static_cast<int64_t>((t >> pages.page_shift) << pages.page_shift);
     }
   }
+  const float* kn = k_norms + row;
+  const float* vn = v_norms + row;
 
   // ---- the cache loads (keys and scales now, values as the scores proceed)
   uint32_t kw[NB][3], vw[NB][3];
@@ -1018,7 +1035,7 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   const void* v_new = append ? append->v_new : nullptr;
   const int new_f16 = append ? append->f16 : 0;
   int32_t* status = append ? append->status : nullptr;
-  const PageTable pt = pages ? *pages : PageTable{nullptr, 0, 16, 1};
+  const PageTable pt = pages ? *pages : PageTable{nullptr, 0, 4, 1};
 #define IQ_LAUNCH_G8_WP(NB_, APP_, WIDE_, PAGED_)                                                \
   hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_, PAGED_>), grid, block, lds_pad, stream, \
                      q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials, out,     \

@@ -31,14 +31,15 @@ const Codebook& codebook();
 // A paged cache: records of logical position t of (sequence b, KV head g)
 // live in page tables[b * max_pages + t / page_size], slot t % page_size, of
 // pools laid out [n_pages][n_kv_heads][page_size][48] (codes) and
-// [n_pages][n_kv_heads][page_size] (scales).  page_size is a multiple of 16,
-// so a batch of 16 positions never straddles a page.  A page index outside
-// [0, n_pages) is a caller error: reads then use page 0 and writes are
-// skipped, so no access leaves the pools.
+// [n_pages][n_kv_heads][page_size] (scales).  page_size is a power of two
+// (page_shift its log2), at least 16, so a batch of 16 positions never
+// straddles a page.  A page index outside [0, n_pages) is a caller error:
+// reads then use page 0 and writes are skipped, so no access leaves the
+// pools.
 struct PageTable {
   const int32_t* tables;   // [batch][max_pages]
   int64_t max_pages;
-  int32_t page_size;
+  int32_t page_shift;
   int32_t n_pages;
 };
 
@@ -46,9 +47,10 @@ struct PageTable {
 // records) of logical position t, or -1 if its page index is invalid.
 __device__ __forceinline__ int64_t paged_record(const PageTable& pt, int n_kv_heads, int b,
                                                 int g, int64_t t) {
-  const int32_t page = pt.tables[static_cast<int64_t>(b) * pt.max_pages + t / pt.page_size];
-  if (page < 0 || page >= pt.n_pages) return -1;
-  return (static_cast<int64_t>(page) * n_kv_heads + g) * pt.page_size + t % pt.page_size;
+  const int32_t page = pt.tables[static_cast<int64_t>(b) * pt.max_pages + (t >> pt.page_shift)];
+  if (static_cast<uint32_t>(page) >= static_cast<uint32_t>(pt.n_pages)) return -1;
+  const int64_t slot = t & ((int64_t(1) << pt.page_shift) - 1);
+  return ((static_cast<int64_t>(page) * n_kv_heads + g) << pt.page_shift) + slot;
 }
 
 // Split-K plan for one decode call.  Deterministic function of the shapes so

@@ -260,7 +260,8 @@ def _paged_decode(**kw):
 
 
 def test_paged_decode_validation():
-    assert _paged_decode(page=48) == 1           # not a multiple of 16
+    assert _paged_decode(page=48) == 1           # not a power of two
+    assert _paged_decode(page=8) == 1
     assert _paged_decode(page=0) == 1
     assert _paged_decode(n_pages=0) == 1
     assert _paged_decode(max_pages=0) == 1
@@ -284,5 +285,6 @@ def test_paged_compress_validation():
                                       a["bt"], a["max_pages"], a["off"], None)
     assert call(off=120) == 1                    # 120 + 10 > 2 * 64
     assert call(page=40) == 1
+    assert call(page=96) == 1                    # multiple of 16, not a power of two
     assert call(dtype=7) == 2
     assert call(n=0) == 0
