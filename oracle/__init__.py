@@ -16,7 +16,9 @@ Modules (each function cites the passage of the paper it follows):
 * ``rotation``  - seeded unit quaternions, the normalized Walsh-Hadamard
   matrix H_d, the SO(4) block maps v -> q_L v conj(q_R) and the composed
   rotation R = R_SO(4) H_d (Sec. 3.2 Step 2, Eq. 2; Sec. 3.3; App. B).
-* ``compress``  - Algorithm 1: normalize, rotate, quantize, bit-pack.
+* ``compress``  - Algorithm 1: normalize, rotate, quantize, bit-pack, at the
+  bit width b of the codebook given (b = 3 in the paper's experiments; 2
+  and 4 through the same steps with C_2, C_4).
 * ``attention`` - decode attention in the compressed space (App. A, Table 2)
   and the reconstruct-then-compute path it replaces (Sec. 1, Fig. 1 top).
 * ``rotation_study`` - distortion, coordinate energy and attention error of

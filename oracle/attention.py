@@ -42,11 +42,12 @@ def _default_scale(d, scale):
 
 def fused_scores(q, k_packed, k_norms, r, levels, scale=None):
     """Compressed-space scores for one KV head: q [G][d] (original space),
-    k_packed [T][48], k_norms [T] -> scores [G][T] (fp64)."""
+    k_packed [T][d*b/8], k_norms [T] -> scores [G][T] (fp64)."""
     q = np.asarray(q, dtype=np.float64)
     d = q.shape[-1]
     qt = q @ np.asarray(r).T                                   # R q per head
-    kt = _cz.dequantize_rotated(_cz.unpack(k_packed, d), k_norms, levels)
+    bits = _cz.bits_of(levels)
+    kt = _cz.dequantize_rotated(_cz.unpack(k_packed, d, bits), k_norms, levels)
     return (qt @ kt.T) * _default_scale(d, scale)
 
 
@@ -54,7 +55,8 @@ def decode_fused(q, k_packed, k_norms, v_packed, v_norms, seq_lens, quats,
                  levels, scale=None, skip_inverse=False):
     """Compressed-space decode attention for a batch (App. A).
 
-    q: [B][H_q][d]; k_packed/v_packed: [B][H_kv][cap][48] uint8;
+    q: [B][H_q][d]; k_packed/v_packed: [B][H_kv][cap][d*b/8] uint8 (b from
+    the codebook: 48 bytes at b = 3);
     k_norms/v_norms: [B][H_kv][cap] fp32; seq_lens: [B]; quats:
     [H_kv][d/4][2][4].  Returns out [B][H_q][d] fp64 in the original space.
     ``skip_inverse`` returns o_tilde without R^T (the negative control of
@@ -76,6 +78,7 @@ def decode_fused_rotations(q, k_packed, k_norms, v_packed, v_norms, seq_lens, ro
         raise ValueError("H_q must be a multiple of H_kv")
     group = hq // hkv
     out = np.zeros((bsz, hq, d))
+    bits = _cz.bits_of(levels)
     for b in range(bsz):
         n = int(seq_lens[b])
         if n == 0:
@@ -85,7 +88,7 @@ def decode_fused_rotations(q, k_packed, k_norms, v_packed, v_norms, seq_lens, ro
             scores = fused_scores(q[b, heads], k_packed[b, g, :n], k_norms[b, g, :n],
                                   rots[g], levels, scale)
             alpha = softmax(scores)                                   # [G][n]
-            vt = _cz.dequantize_rotated(_cz.unpack(v_packed[b, g, :n], d),
+            vt = _cz.dequantize_rotated(_cz.unpack(v_packed[b, g, :n], d, bits),
                                         v_norms[b, g, :n], levels)     # [n][d]
             o_tilde = alpha @ vt                                      # [G][d]
             out[b, heads] = o_tilde if skip_inverse else o_tilde @ rots[g]
@@ -103,14 +106,15 @@ def decode_reconstruct(q, k_packed, k_norms, v_packed, v_norms, seq_lens, quats,
     rots = _rot.rotation_matrices(np.asarray(quats))
     sc = _default_scale(d, scale)
     out = np.zeros((bsz, hq, d))
+    bits = _cz.bits_of(levels)
     for b in range(bsz):
         n = int(seq_lens[b])
         if n == 0:
             continue
         for g in range(hkv):
-            k_hat = _cz.reconstruct(_cz.unpack(k_packed[b, g, :n], d), k_norms[b, g, :n],
+            k_hat = _cz.reconstruct(_cz.unpack(k_packed[b, g, :n], d, bits), k_norms[b, g, :n],
                                     levels, rots[g])
-            v_hat = _cz.reconstruct(_cz.unpack(v_packed[b, g, :n], d), v_norms[b, g, :n],
+            v_hat = _cz.reconstruct(_cz.unpack(v_packed[b, g, :n], d, bits), v_norms[b, g, :n],
                                     levels, rots[g])
             for h in range(g * group, (g + 1) * group):
                 alpha = softmax((k_hat @ q[b, h]) * sc)

@@ -8,7 +8,9 @@ For one key or value vector x in R^d:
 2. Rotate (Step 2, Eq. 2): x_tilde = R_SO(4)(H_d x_hat) = R x_hat.
 3. Quantize (Step 3): each coordinate to the nearest codebook level.
 4. Bit-pack (Step 4): d codes of b bits into d*b/8 bytes (48 bytes at
-   d = 128, b = 3).
+   d = 128, b = 3; 32 at b = 2, 64 at b = 4).  Algorithm 1 is stated for a
+   general b with its codebook C_b; the bit width is read off the codebook
+   (2^b levels, 2^b - 1 thresholds).
 
 Readings of what the paper leaves open:
 
@@ -19,11 +21,11 @@ Readings of what the paper leaves open:
   levels are numbered in ascending order and a value exactly on a threshold
   goes to the upper level (-0.0 counts as 0).  With thresholds at the level
   midpoints this is the nearest level, ties upward.
-* Packed layout: code i occupies bits 3i .. 3i+2 of a little-endian bit
+* Packed layout: code i occupies bits b*i .. b*i+b-1 of a little-endian bit
   string (bit n is bit n % 8 of byte n // 8), least significant bit first;
-  so dims 8g .. 8g+7 fill bytes 3g .. 3g+2.  Keys and values use the same
-  record format, one 48-byte record per token, records of consecutive tokens
-  contiguous, scales stored in a separate fp32 array.
+  at b = 3 dims 8g .. 8g+7 fill bytes 3g .. 3g+2.  Keys and values use the
+  same record format, one d*b/8-byte record per token, records of
+  consecutive tokens contiguous, scales stored in a separate fp32 array.
 """
 
 from __future__ import annotations
@@ -31,6 +33,17 @@ from __future__ import annotations
 import numpy as np
 
 BITS = 3
+
+
+def bits_of(codebook) -> int:
+    """Bit width b of a codebook given by its levels (2^b) or thresholds
+    (2^b - 1)."""
+    n = len(codebook)
+    n = n + 1 if n % 2 else n
+    b = int(n).bit_length() - 1
+    if n != 1 << b or b < 1:
+        raise ValueError(f"codebook of {len(codebook)} entries is not 2^b levels")
+    return b
 
 
 def normalize(x):
@@ -79,24 +92,24 @@ def unpack(packed, d: int = 128, bits: int = BITS):
 def compress(x, r, thresholds):
     """Algorithm 1 for a batch of vectors that share one rotation.
 
-    x: [..., d] (any float dtype, taken exactly); r: [d, d].
-    Returns (packed [..., d*3/8] uint8, scale fp32 [...], codes [..., d],
-    x_tilde fp64 [..., d], scale fp64 [...]).  The last three are for
-    analysis (boundary distances, reconstruction).
+    x: [..., d] (any float dtype, taken exactly); r: [d, d]; thresholds of
+    C_b (2^b - 1 of them).  Returns (packed [..., d*b/8] uint8, scale fp32
+    [...], codes [..., d], x_tilde fp64 [..., d], scale fp64 [...]).  The
+    last three are for analysis (boundary distances, reconstruction).
     """
     s, xhat = normalize(x)
     y = rotate(xhat, r)
     codes = quantize(y, thresholds)
-    return pack(codes), s.astype(np.float32), codes, y, s
+    return pack(codes, bits_of(thresholds)), s.astype(np.float32), codes, y, s
 
 
 def compress_kv(x, rots, thresholds):
     """Compress a cache tensor x: [B][H_kv][T][d] with one rotation per KV
-    head (rots: [H_kv][d][d]).  Returns (packed [B][H][T][48], scale fp32
-    [B][H][T], codes, x_tilde, scale64)."""
+    head (rots: [H_kv][d][d]).  Returns (packed [B][H][T][d*b/8], scale
+    fp32 [B][H][T], codes, x_tilde, scale64)."""
     x = np.asarray(x)
     b, h, t, d = x.shape
-    packed = np.empty((b, h, t, d * BITS // 8), dtype=np.uint8)
+    packed = np.empty((b, h, t, d * bits_of(thresholds) // 8), dtype=np.uint8)
     norms = np.empty((b, h, t), dtype=np.float32)
     codes = np.empty((b, h, t, d), dtype=np.uint8)
     ys = np.empty((b, h, t, d), dtype=np.float64)
@@ -120,7 +133,7 @@ def reconstruct(codes, scale, levels, r):
 
 
 def reconstruct_kv(packed, norms, rots, levels, d: int = 128):
-    """Materialize a packed cache [B][H_kv][T][d*3/8] with scales [B][H_kv][T]
+    """Materialize a packed cache [B][H_kv][T][d*b/8] with scales [B][H_kv][T]
     as original-space vectors [B][H_kv][T][d] (fp64): the dequantization and
     R^T of the reconstruct-then-compute pipeline (Fig. 1 top), one rotation
     per KV head."""
@@ -128,5 +141,6 @@ def reconstruct_kv(packed, norms, rots, levels, d: int = 128):
     b, h, t, _ = packed.shape
     out = np.empty((b, h, t, d), dtype=np.float64)
     for hh in range(h):
-        out[:, hh] = reconstruct(unpack(packed[:, hh], d), norms[:, hh], levels, rots[hh])
+        out[:, hh] = reconstruct(unpack(packed[:, hh], d, bits_of(levels)), norms[:, hh], levels,
+                                 rots[hh])
     return out
