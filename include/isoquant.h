@@ -407,6 +407,48 @@ iq_status iq_decode_attention_f16(const float* q, const void* k, const void* v,
                                   float* out, void* workspace, size_t workspace_bytes,
                                   hipStream_t stream);
 
+/*
+ * Other code widths (Algorithm 1 at b = 2 and b = 4)
+ * ---------------------------------------------------
+ * Algorithm 1 quantizes to b bits per coordinate with the Lloyd-Max codebook
+ * C_b of the same sphere marginal and packs the codes into d*b/8 bytes
+ * (Sec. 3.2 Steps 3-4); the paper's cache uses b = 3.  These entry points
+ * take b explicitly: records are 16*b bytes (32 at b = 2, 48 at b = 3, 64 at
+ * b = 4), code i at bits b*i .. b*i+b-1 of the little-endian bit string,
+ * scales and every other layout and argument as for the 3-bit entry points.
+ * b = 3 gives exactly the results of iq_codebook / iq_compress_kv /
+ * iq_decode_attention.  Any other b returns IQ_ERR_UNSUPPORTED.
+ */
+
+/* C_b: levels[2^b] and thresholds[2^b - 1] (host memory, either may be
+ * NULL), built as for iq_codebook. */
+iq_status iq_codebook_bits(int bits, float* levels, float* thresholds);
+
+/* iq_compress_kv writing b-bit records: k_codes / v_codes are
+ * [batch][n_kv_heads][capacity][16*bits] uint8, 16-byte aligned. */
+iq_status iq_compress_kv_bits(const void* k, const void* v, iq_dtype dtype,
+                              int64_t batch, int64_t n_kv_heads, int64_t n_tokens,
+                              int64_t head_dim, const float* quats,
+                              uint8_t* k_codes, float* k_norms,
+                              uint8_t* v_codes, float* v_norms,
+                              int64_t capacity, int64_t dst_offset, int bits,
+                              hipStream_t stream);
+
+/* iq_decode_attention on b-bit records (workspace as sized by
+ * iq_decode_workspace_bytes).  b = 2 and b = 4 run on the matrix-core path
+ * only: n_q_heads == 8 * n_kv_heads, capacity a multiple of 16 (>= 16) with
+ * capacity * 16 * bits < 2^31, 16-byte aligned scale arrays, batch and
+ * n_kv_heads <= 65535; otherwise IQ_ERR_UNSUPPORTED. */
+iq_status iq_decode_attention_bits(const float* q,
+                                   const uint8_t* k_codes, const float* k_norms,
+                                   const uint8_t* v_codes, const float* v_norms,
+                                   const int32_t* seq_lens, int64_t capacity,
+                                   int64_t max_seq_len, const float* quats,
+                                   int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                                   int64_t head_dim, float softmax_scale, float* out,
+                                   void* workspace, size_t workspace_bytes, int bits,
+                                   hipStream_t stream);
+
 #ifdef __cplusplus
 }  /* extern "C" */
 #endif

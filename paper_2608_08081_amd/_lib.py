@@ -50,6 +50,12 @@ _SIGNATURES = {
                                       _c_i64, _vp, _c_i64, _vp, _c_i64, _vp, _c_i64, _c_i64,
                                       _c_i64, _c_i64, _c_float, _vp, _vp, _c_size, _vp, _vp]),
     "iq_so4_to_quaternions": (_c_int, [_vp, _vp]),
+    "iq_codebook_bits": (_c_int, [_c_int, _vp, _vp]),
+    "iq_compress_kv_bits": (_c_int, [_vp, _vp, _c_int, _c_i64, _c_i64, _c_i64, _c_i64, _vp,
+                                     _vp, _vp, _vp, _vp, _c_i64, _c_i64, _c_int, _vp]),
+    "iq_decode_attention_bits": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp,
+                                          _c_i64, _c_i64, _c_i64, _c_i64, _c_float, _vp, _vp,
+                                          _c_size, _c_int, _vp]),
     "iq_compress_kv": (_c_int, [_vp, _vp, _c_int, _c_i64, _c_i64, _c_i64, _c_i64, _vp,
                                 _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp]),
     "iq_append_token": (_c_int, [_vp, _vp, _c_int, _c_i64, _c_i64, _c_i64, _vp,

@@ -63,6 +63,22 @@ def iq_codebook():
     return lv, th
 
 
+def iq_codebook_bits(bits: int):
+    """C_b: (levels[2^b], thresholds[2^b - 1]) as float32 numpy arrays."""
+    n = 1 << bits
+    lv = np.zeros(n, np.float32)
+    th = np.zeros(n - 1, np.float32)
+    _lib.check("iq_codebook_bits",
+               _lib.lib().iq_codebook_bits(bits, lv.ctypes.data_as(ctypes.c_void_p),
+                                           th.ctypes.data_as(ctypes.c_void_p)))
+    return lv, th
+
+
+def record_bytes(bits: int = 3) -> int:
+    """Bytes of one packed record of 128 b-bit codes."""
+    return HEAD_DIM * bits // 8
+
+
 def iq_make_rotation(seed: int, n_kv_heads: int) -> torch.Tensor:
     """Seeded SO(4) parameters, host float32 tensor [n_kv_heads][32][2][4]."""
     out = np.zeros((n_kv_heads, 32, 2, 4), np.float32)
@@ -120,12 +136,13 @@ def iq_decode_workspace_bytes(batch, n_q_heads, n_kv_heads, max_seq_len) -> int:
 # device entry points
 # ---------------------------------------------------------------------------
 
-def alloc_cache(batch, n_kv_heads, capacity, device, values=True):
+def alloc_cache(batch, n_kv_heads, capacity, device, values=True, bits: int = 3):
     """Zero-filled packed cache buffers for one layer: dict with k_codes,
-    k_norms (and v_codes, v_norms), plus seq_lens (int32 zeros)."""
+    k_norms (and v_codes, v_norms), plus seq_lens (int32 zeros); records of
+    16 * bits bytes."""
     c = {
-        "k_codes": torch.zeros((batch, n_kv_heads, capacity, RECORD_BYTES), dtype=torch.uint8,
-                               device=device),
+        "k_codes": torch.zeros((batch, n_kv_heads, capacity, record_bytes(bits)),
+                               dtype=torch.uint8, device=device),
         "k_norms": torch.zeros((batch, n_kv_heads, capacity), dtype=torch.float32, device=device),
         "seq_lens": torch.zeros(batch, dtype=torch.int32, device=device),
     }
@@ -139,6 +156,16 @@ def iq_compress_kv(k, v, quats, k_codes=None, k_norms=None, v_codes=None, v_norm
                    dst_offset: int = 0):
     """Algorithm 1 over a block of tokens: k, v [B][H][T][128] (f16 or f32,
     either may be None) written into the caches at positions dst_offset.."""
+    _compress(k, v, quats, k_codes, k_norms, v_codes, v_norms, dst_offset, 3)
+
+
+def iq_compress_kv_bits(k, v, quats, k_codes=None, k_norms=None, v_codes=None, v_norms=None,
+                        dst_offset: int = 0, bits: int = 3):
+    """iq_compress_kv to b-bit records (k_codes / v_codes [B][H][cap][16 b])."""
+    _compress(k, v, quats, k_codes, k_norms, v_codes, v_norms, dst_offset, bits)
+
+
+def _compress(k, v, quats, k_codes, k_norms, v_codes, v_norms, dst_offset, bits):
     src = k if k is not None else v
     if src is None:
         raise ValueError("k and v are both None")
@@ -155,14 +182,17 @@ def iq_compress_kv(k, v, quats, k_codes=None, k_norms=None, v_codes=None, v_norm
         if x is None:
             continue
         _require(x, name, src.dtype, (b, h, t, HEAD_DIM), dev)
-        _require(codes, f"{name}_codes", torch.uint8, (b, h, cap, RECORD_BYTES), dev)
+        _require(codes, f"{name}_codes", torch.uint8, (b, h, cap, record_bytes(bits)), dev)
         _require(norms, f"{name}_norms", torch.float32, (b, h, cap), dev)
-    st = _lib.lib().iq_compress_kv(
-        _ptr(k), _ptr(v), _dtype_code(src), b, h, t, HEAD_DIM, _ptr(quats),
-        _ptr(k_codes) if k is not None else None, _ptr(k_norms) if k is not None else None,
-        _ptr(v_codes) if v is not None else None, _ptr(v_norms) if v is not None else None,
-        cap, dst_offset, _stream(dev))
-    _lib.check("iq_compress_kv", st)
+    args = (_ptr(k), _ptr(v), _dtype_code(src), b, h, t, HEAD_DIM, _ptr(quats),
+            _ptr(k_codes) if k is not None else None, _ptr(k_norms) if k is not None else None,
+            _ptr(v_codes) if v is not None else None, _ptr(v_norms) if v is not None else None,
+            cap, dst_offset)
+    if bits == 3:
+        _lib.check("iq_compress_kv", _lib.lib().iq_compress_kv(*args, _stream(dev)))
+    else:
+        _lib.check("iq_compress_kv_bits",
+                   _lib.lib().iq_compress_kv_bits(*args, bits, _stream(dev)))
 
 
 def iq_append_token(k_new, v_new, quats, k_codes, k_norms, v_codes, v_norms, seq_lens,
@@ -216,16 +246,30 @@ def iq_decode_attention(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, 
                         workspace=None, max_seq_len=None, softmax_scale: float = 0.0):
     """Decode attention on the packed cache.  q: [B][H_q][128] fp32 (original
     space); returns out [B][H_q][128] fp32 (original space)."""
+    return _decode(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out, workspace,
+                   max_seq_len, softmax_scale, 3)
+
+
+def iq_decode_attention_bits(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out=None,
+                             workspace=None, max_seq_len=None, softmax_scale: float = 0.0,
+                             bits: int = 3):
+    """iq_decode_attention on b-bit records ([B][H_kv][cap][16 b])."""
+    return _decode(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out, workspace,
+                   max_seq_len, softmax_scale, bits)
+
+
+def _decode(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out, workspace,
+            max_seq_len, softmax_scale, bits):
     if q.dim() != 3 or q.shape[-1] != HEAD_DIM:
         raise ValueError("q must be [batch][n_q_heads][128]")
     b, hq, _ = q.shape
     dev = q.device
     _require(q, "q", torch.float32, (b, hq, HEAD_DIM), dev)
     if k_codes.dim() != 4:
-        raise ValueError("k_codes must be [batch][n_kv_heads][capacity][48]")
+        raise ValueError("k_codes must be [batch][n_kv_heads][capacity][16 * bits]")
     _, hkv, cap, _ = k_codes.shape
-    _require(k_codes, "k_codes", torch.uint8, (b, hkv, cap, RECORD_BYTES), dev)
-    _require(v_codes, "v_codes", torch.uint8, (b, hkv, cap, RECORD_BYTES), dev)
+    _require(k_codes, "k_codes", torch.uint8, (b, hkv, cap, record_bytes(bits)), dev)
+    _require(v_codes, "v_codes", torch.uint8, (b, hkv, cap, record_bytes(bits)), dev)
     _require(k_norms, "k_norms", torch.float32, (b, hkv, cap), dev)
     _require(v_norms, "v_norms", torch.float32, (b, hkv, cap), dev)
     _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
@@ -239,11 +283,14 @@ def iq_decode_attention(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, 
         workspace = alloc_workspace(b, hq, hkv, max_seq_len, dev)
     if workspace.dtype != torch.uint8 or workspace.device != dev or not workspace.is_contiguous():
         raise ValueError("workspace must be a contiguous uint8 device tensor")
-    st = _lib.lib().iq_decode_attention(
-        _ptr(q), _ptr(k_codes), _ptr(k_norms), _ptr(v_codes), _ptr(v_norms), _ptr(seq_lens),
-        cap, max_seq_len, _ptr(quats), b, hq, hkv, HEAD_DIM, float(softmax_scale), _ptr(out),
-        _ptr(workspace), workspace.numel(), _stream(dev))
-    _lib.check("iq_decode_attention", st)
+    args = (_ptr(q), _ptr(k_codes), _ptr(k_norms), _ptr(v_codes), _ptr(v_norms), _ptr(seq_lens),
+            cap, max_seq_len, _ptr(quats), b, hq, hkv, HEAD_DIM, float(softmax_scale), _ptr(out),
+            _ptr(workspace), workspace.numel())
+    if bits == 3:
+        _lib.check("iq_decode_attention", _lib.lib().iq_decode_attention(*args, _stream(dev)))
+    else:
+        _lib.check("iq_decode_attention_bits",
+                   _lib.lib().iq_decode_attention_bits(*args, bits, _stream(dev)))
     return out
 
 

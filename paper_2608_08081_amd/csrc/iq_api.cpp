@@ -56,8 +56,9 @@ double round_to_half(double v) {
   return nearbyint(v / ulp) * ulp;
 }
 
-Codebook build_codebook() {
-  const int d = kDim, n = 8;
+template <int kBits>
+CodebookB<kBits> build_codebook() {
+  constexpr int d = kDim, n = 1 << kBits;
   const double k = (d - 3) / 2.0;
   double c[n];
   for (int i = 0; i < n; ++i) c[i] = -2.0 / sqrt(static_cast<double>(d)) + i * (4.0 / sqrt(static_cast<double>(d))) / (n - 1);
@@ -74,7 +75,7 @@ Codebook build_codebook() {
     }
     if (moved < 1e-13) break;
   }
-  Codebook cb{};
+  CodebookB<kBits> cb{};
   for (int i = 0; i < n; ++i) cb.level[i] = static_cast<float>(round_to_half(c[i]));
   // enforce the symmetry of the symmetric density exactly
   for (int i = 0; i < n / 2; ++i) cb.level[i] = -cb.level[n - 1 - i];
@@ -125,12 +126,18 @@ bool mul_ok(int64_t a, int64_t b) { return a == 0 || b <= (int64_t(1) << 62) / a
 
 }  // namespace
 
-const Codebook& codebook() {
-  static Codebook cb;
+template <int kBits>
+const CodebookB<kBits>& codebook_b() {
+  static CodebookB<kBits> cb;
   static std::once_flag once;
-  std::call_once(once, [] { cb = build_codebook(); });
+  std::call_once(once, [] { cb = build_codebook<kBits>(); });
   return cb;
 }
+template const CodebookB<2>& codebook_b<2>();
+template const CodebookB<3>& codebook_b<3>();
+template const CodebookB<4>& codebook_b<4>();
+
+const Codebook& codebook() { return codebook_b<3>(); }
 
 }  // namespace iq
 
@@ -150,13 +157,22 @@ const char* iq_status_string(iq_status s) {
   return "IQ_ERR_UNKNOWN";
 }
 
-int iq_version(void) { return 103; }
+int iq_version(void) { return 104; }
 
-iq_status iq_codebook(float* levels, float* thresholds) {
-  const iq::Codebook& cb = iq::codebook();
-  if (levels) memcpy(levels, cb.level, sizeof(cb.level));
-  if (thresholds) memcpy(thresholds, cb.thr, sizeof(cb.thr));
-  return IQ_OK;
+iq_status iq_codebook(float* levels, float* thresholds) { return iq_codebook_bits(3, levels, thresholds); }
+
+iq_status iq_codebook_bits(int bits, float* levels, float* thresholds) {
+  auto copy = [&](const auto& cb) {
+    if (levels) memcpy(levels, cb.level, sizeof(cb.level));
+    if (thresholds) memcpy(thresholds, cb.thr, sizeof(cb.thr));
+    return IQ_OK;
+  };
+  switch (bits) {
+    case 2: return copy(iq::codebook_b<2>());
+    case 3: return copy(iq::codebook_b<3>());
+    case 4: return copy(iq::codebook_b<4>());
+    default: return IQ_ERR_UNSUPPORTED;
+  }
 }
 
 iq_status iq_make_rotation(uint64_t seed, int64_t n_kv_heads, int64_t head_dim,
@@ -201,7 +217,17 @@ iq_status iq_compress_kv(const void* k, const void* v, iq_dtype dtype, int64_t b
                          const float* quats, uint8_t* k_codes, float* k_norms,
                          uint8_t* v_codes, float* v_norms, int64_t capacity,
                          int64_t dst_offset, hipStream_t stream) {
+  return iq_compress_kv_bits(k, v, dtype, batch, n_kv_heads, n_tokens, head_dim, quats, k_codes,
+                             k_norms, v_codes, v_norms, capacity, dst_offset, 3, stream);
+}
+
+iq_status iq_compress_kv_bits(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+                              int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
+                              const float* quats, uint8_t* k_codes, float* k_norms,
+                              uint8_t* v_codes, float* v_norms, int64_t capacity,
+                              int64_t dst_offset, int bits, hipStream_t stream) {
   if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
+  if (bits < 2 || bits > 4) return IQ_ERR_UNSUPPORTED;
   if (dtype != IQ_DTYPE_F32 && dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
   if (batch < 0 || n_kv_heads <= 0 || n_tokens < 0 || capacity < 0 || dst_offset < 0)
     return IQ_ERR_INVALID_ARGUMENT;
@@ -221,7 +247,7 @@ iq_status iq_compress_kv(const void* k, const void* v, iq_dtype dtype, int64_t b
     return IQ_ERR_INVALID_ARGUMENT;
   const hipError_t e = iq::launch_compress(k, v, dtype, batch, n_kv_heads, n_tokens, quats,
                                            k_codes, k_norms, v_codes, v_norms, capacity,
-                                           dst_offset, stream);
+                                           dst_offset, bits, stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 
@@ -327,6 +353,42 @@ iq_status iq_decode_attention(const float* q, const uint8_t* k_codes, const floa
       const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms), const_cast<int32_t*>(seq_lens),
       capacity, max_seq_len, quats, batch, n_q_heads, n_kv_heads, resolve_scale(softmax_scale),
       out, workspace, nullptr, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+iq_status iq_decode_attention_bits(const float* q, const uint8_t* k_codes, const float* k_norms,
+                                   const uint8_t* v_codes, const float* v_norms,
+                                   const int32_t* seq_lens, int64_t capacity,
+                                   int64_t max_seq_len, const float* quats, int64_t batch,
+                                   int64_t n_q_heads, int64_t n_kv_heads, int64_t head_dim,
+                                   float softmax_scale, float* out, void* workspace,
+                                   size_t workspace_bytes, int bits, hipStream_t stream) {
+  if (bits == 3)
+    return iq_decode_attention(q, k_codes, k_norms, v_codes, v_norms, seq_lens, capacity,
+                               max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
+                               softmax_scale, out, workspace, workspace_bytes, stream);
+  if (bits != 2 && bits != 4) return IQ_ERR_UNSUPPORTED;
+  iq::DecodePlan plan;
+  const iq_status st = check_decode_args(q, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                                         capacity, max_seq_len, quats, batch, n_q_heads,
+                                         n_kv_heads, head_dim, out, workspace, workspace_bytes,
+                                         &plan);
+  if (st != IQ_OK) return st;
+  // 2- and 4-bit records run on the group-8 matrix-core path only: rows of
+  // whole 16-position batches addressed with 32-bit byte offsets, KV heads
+  // and sequences as grid dimensions
+  if (n_q_heads != 8 * n_kv_heads || plan.g8_batches <= 0) return IQ_ERR_UNSUPPORTED;
+  if (capacity % 16 || capacity < 16 || capacity * 16 * bits > 0x7fffffff ||
+      !iq::aligned(k_norms, 16) || !iq::aligned(v_norms, 16) || batch > 65535 ||
+      n_kv_heads > 65535)
+    return IQ_ERR_UNSUPPORTED;
+  if (batch == 0) return IQ_OK;
+  float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
+  const hipError_t e = iq::launch_decode_g8(
+      plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, const_cast<uint8_t*>(k_codes),
+      const_cast<float*>(k_norms), const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms),
+      const_cast<int32_t*>(seq_lens), capacity, max_seq_len, quats, batch, n_kv_heads,
+      resolve_scale(softmax_scale), out, parts, nullptr, nullptr, bits, stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 
@@ -466,7 +528,7 @@ iq_status iq_decode_attention_paged(const float* q, const uint8_t* k_codes,
       plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, const_cast<uint8_t*>(k_codes),
       const_cast<float*>(k_norms), const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms),
       const_cast<int32_t*>(seq_lens), max_pages * page_size, max_seq_len, quats, batch,
-      n_kv_heads, resolve_scale(softmax_scale), out, parts, nullptr, &pt, stream);
+      n_kv_heads, resolve_scale(softmax_scale), out, parts, nullptr, &pt, 3, stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 
@@ -498,7 +560,7 @@ iq_status iq_decode_step_paged(const float* q, const void* k_new, const void* v_
   const hipError_t e = iq::launch_decode_g8(
       plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes, k_norms, v_codes, v_norms,
       seq_lens, max_pages * page_size, max_seq_len, quats, batch, n_kv_heads,
-      resolve_scale(softmax_scale), out, parts, &append, &pt, stream);
+      resolve_scale(softmax_scale), out, parts, &append, &pt, 3, stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 

@@ -18,6 +18,8 @@
 //          m = #{k = 1..3 : |y| >= T_k} comes from a two-step search; the
 //          two rules differ only when |y| equals a threshold exactly;
 //   pack = 3-bit codes into 12 words, stored as three 16-byte writes (Step 4).
+// The same kernel compresses to b = 2 or b = 4 bit codes (Algorithm 1 with
+// C_2 or C_4: 2^(b-1) - 1 positive thresholds, records of 4b words).
 // A vector whose s^2 is not finite (NaN or infinite input) gets the record of
 // all-NaN coordinates, code 0 everywhere, as #{j : t_j <= NaN} = 0.
 #include <hip/hip_fp16.h>
@@ -73,6 +75,30 @@ __device__ __forceinline__ uint32_t quantize_sym(float y, float t1, float t2, fl
   return (hi | lo) ^ flip;
 }
 
+// The same rule for b = 2 and b = 4 (h = 2^(b-1) levels per sign, positive
+// thresholds t[0] < ... < t[h-2]): code (h + m) ^ (y < 0 ? 2h - 1 : 0) with
+// m = #{k : |y| >= t[k]}.  Codes of 2 and 4 bits never
+// straddle a 32-bit word.
+template <int kBits>
+__device__ __forceinline__ uint32_t quantize_sym_b(float y, const float (&t)[(1 << (kBits - 1)) - 1],
+                                                   int off) {
+  constexpr uint32_t h = 1u << (kBits - 1);
+  const float a = fabsf(y);
+  uint32_t m;
+  if constexpr (kBits == 2) {
+    m = a >= t[0] ? 1u : 0u;
+  } else {
+    static_assert(kBits == 4, "2 or 4 bits");
+    // a plain count: a select tree over 7 thresholds, interleaved across
+    // coordinates, more than doubles the register footprint
+    m = 0u;
+#pragma unroll
+    for (int k = 0; k < 7; ++k) m += a >= t[k] ? 1u : 0u;
+  }
+  const uint32_t flip = y >= 0.f ? 0u : (2 * h - 1);
+  return ((h + m) ^ flip) << off;
+}
+
 // OR the code of coordinate i (bits 3i .. 3i+2 of the record) into w.
 __device__ __forceinline__ void put_code_sym(uint32_t (&w)[kRecordWords], int i, float y,
                                              float t1, float t2, float t3) {
@@ -89,11 +115,14 @@ __device__ __forceinline__ void put_code_sym(uint32_t (&w)[kRecordWords], int i,
 
 // Compress one vector (Algorithm 1) and write its record and scale.
 // mtab: rows of the head's block matrices M_i H_4 (row r of block i at
-// mtab[4 i + r]).
-template <typename T>
+// mtab[4 i + r]).  The record has 4 kBits words.
+template <typename T, int kBits>
 __device__ __forceinline__ void compress_one(const T* __restrict__ src, const f32x4_t* mtab,
                                              uint8_t* __restrict__ dst_code,
-                                             float* __restrict__ dst_norm, const Codebook& cb) {
+                                             float* __restrict__ dst_norm,
+                                             const CodebookB<kBits>& cb) {
+  constexpr int kWords = 4 * kBits;
+  constexpr int kHalf = 1 << (kBits - 1);
   float x[kDim];
   load_vector(src, x);
 
@@ -111,14 +140,17 @@ __device__ __forceinline__ void compress_one(const T* __restrict__ src, const f3
   const bool finite = ss < static_cast<double>(INFINITY);
 
   // Positive thresholds in the unnormalized domain: t_j * s * sqrt(128).  A
-  // zero vector keeps the plain thresholds, so its all-zero y maps to code 4.
+  // zero vector keeps the plain thresholds, so its all-zero y maps to the
+  // first non-negative level.
   const double sc = ss > 0.0 ? s * 11.313708498984760390 : 1.0;   // sqrt(128)
-  float t1 = static_cast<float>(static_cast<double>(cb.thr[4]) * sc);
-  float t2 = static_cast<float>(static_cast<double>(cb.thr[5]) * sc);
-  float t3 = static_cast<float>(static_cast<double>(cb.thr[6]) * sc);
-  // opaque from here on: otherwise the select between t1 and t3 below is
-  // pushed above the fp64 scaling, which then runs once per coordinate
-  asm volatile("" : "+v"(t1), "+v"(t2), "+v"(t3));
+  float tp[kHalf - 1];
+#pragma unroll
+  for (int j = 0; j < kHalf - 1; ++j) {
+    tp[j] = static_cast<float>(static_cast<double>(cb.thr[kHalf + j]) * sc);
+    // opaque from here on: otherwise the threshold selects of the search
+    // are pushed above the fp64 scaling, which then runs once per coordinate
+    asm volatile("" : "+v"(tp[j]));
+  }
 
   // Step 2a: Walsh-Hadamard butterflies on index bits 2..6 (H_32 (x) I_4).
 #pragma unroll
@@ -134,9 +166,9 @@ __device__ __forceinline__ void compress_one(const T* __restrict__ src, const f3
   }
 
   // Step 2b + 3 + 4: per block, y = (M_i H_4) z, quantize, pack.
-  uint32_t w[kRecordWords];
+  uint32_t w[kWords];
 #pragma unroll
-  for (int i = 0; i < kRecordWords; ++i) w[i] = 0u;
+  for (int i = 0; i < kWords; ++i) w[i] = 0u;
 #pragma unroll
   for (int blk = 0; blk < kNumBlocks; ++blk) {
     const float z0 = x[4 * blk], z1 = x[4 * blk + 1], z2 = x[4 * blk + 2], z3 = x[4 * blk + 3];
@@ -144,18 +176,24 @@ __device__ __forceinline__ void compress_one(const T* __restrict__ src, const f3
     for (int r = 0; r < 4; ++r) {
       const f32x4_t m = mtab[4 * blk + r];
       const float y = m[0] * z0 + m[1] * z1 + m[2] * z2 + m[3] * z3;
-      put_code_sym(w, 4 * blk + r, y, t1, t2, t3);
+      const int i = 4 * blk + r;
+      if constexpr (kBits == 3) {
+        put_code_sym(w, i, y, tp[0], tp[1], tp[2]);
+      } else {
+        const int bit = kBits * i;
+        w[bit >> 5] |= quantize_sym_b<kBits>(y, tp, bit & 31);
+      }
     }
   }
   if (!finite) {
 #pragma unroll
-    for (int i = 0; i < kRecordWords; ++i) w[i] = 0u;
+    for (int i = 0; i < kWords; ++i) w[i] = 0u;
   }
 
   uint4* out = reinterpret_cast<uint4*>(dst_code);
-  out[0] = make_uint4(w[0], w[1], w[2], w[3]);
-  out[1] = make_uint4(w[4], w[5], w[6], w[7]);
-  out[2] = make_uint4(w[8], w[9], w[10], w[11]);
+#pragma unroll
+  for (int j = 0; j < kBits; ++j)
+    out[j] = make_uint4(w[4 * j], w[4 * j + 1], w[4 * j + 2], w[4 * j + 3]);
   *dst_norm = static_cast<float>(s);
 }
 
@@ -163,12 +201,12 @@ __device__ __forceinline__ void compress_one(const T* __restrict__ src, const f3
 //   blockIdx.x = (which * (B*H) + bh) * chunks + chunk,  thread = token in chunk.
 // kPaged: the destination is a page pool; a token whose page index is
 // invalid is not written.
-template <typename T, bool kPaged>
+template <typename T, bool kPaged, int kBits>
 __global__ __launch_bounds__(kCompressThreads) void compress_kernel(
     const T* __restrict__ src0, const T* __restrict__ src1, const float* __restrict__ quats,
     uint8_t* __restrict__ codes0, float* __restrict__ norms0, uint8_t* __restrict__ codes1,
     float* __restrict__ norms1, int n_heads, int64_t n_bh, int64_t n_tokens, int64_t chunks,
-    int64_t capacity, int64_t dst_offset, Codebook cb, PageTable pages) {
+    int64_t capacity, int64_t dst_offset, CodebookB<kBits> cb, PageTable pages) {
   __shared__ f32x4_t mtab[kNumBlocks * 4];
   const int64_t blk = blockIdx.x;
   const int64_t chunk = blk % chunks;
@@ -199,8 +237,8 @@ __global__ __launch_bounds__(kCompressThreads) void compress_kernel(
     pos = paged_record(pages, n_heads, static_cast<int>(bh / n_heads), h, dst_offset + t);
     if (pos < 0) return;
   }
-  compress_one<T>(src + (bh * n_tokens + t) * kDim, mtab, codes + pos * kRecordBytes,
-                  norms + pos, cb);
+  compress_one<T, kBits>(src + (bh * n_tokens + t) * kDim, mtab,
+                         codes + pos * record_bytes<kBits>(), norms + pos, cb);
 }
 
 // Per-step append: one workgroup per sequence, one wave per vector (keys and
@@ -267,7 +305,7 @@ hipError_t launch_compress_any(const void* k, const void* v, int dtype, int64_t 
                                int64_t n_heads, int64_t n_tokens, const float* quats,
                                uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
                                float* v_norms, int64_t capacity, int64_t dst_offset,
-                               const PageTable* pages, hipStream_t stream) {
+                               const PageTable* pages, int bits, hipStream_t stream) {
   // slot 0 is whichever side is present first, slot 1 the other (if any)
   const void* s0 = k ? k : v;
   uint8_t* c0 = k ? k_codes : v_codes;
@@ -280,21 +318,26 @@ hipError_t launch_compress_any(const void* k, const void* v, int dtype, int64_t 
   const int64_t chunks = (n_tokens + kCompressThreads - 1) / kCompressThreads;
   const int64_t blocks = chunks * n_bh * nwhich;
   if (blocks == 0) return hipSuccess;
-  const Codebook& cb = codebook();
   const dim3 grid(static_cast<unsigned>(blocks)), block(kCompressThreads);
   const PageTable pt = pages ? *pages : PageTable{nullptr, 0, 4, 1};
-#define IQ_LAUNCH_COMPRESS(T_, P_)                                                             \
-  hipLaunchKernelGGL((compress_kernel<T_, P_>), grid, block, 0, stream,                         \
+  // paged pools hold the paper's 3-bit records only
+  if (pages && bits != 3) return hipErrorInvalidValue;
+#define IQ_LAUNCH_COMPRESS(T_, P_, B_)                                                         \
+  hipLaunchKernelGGL((compress_kernel<T_, P_, B_>), grid, block, 0, stream,                     \
                      static_cast<const T_*>(s0), static_cast<const T_*>(s1), quats, c0, n0, c1, \
                      n1, static_cast<int>(n_heads), n_bh, n_tokens, chunks, capacity,           \
-                     dst_offset, cb, pt)
+                     dst_offset, codebook_b<B_>(), pt)
+#define IQ_LAUNCH_COMPRESS_T(T_)                   \
+  if (pages) IQ_LAUNCH_COMPRESS(T_, true, 3);      \
+  else if (bits == 2) IQ_LAUNCH_COMPRESS(T_, false, 2); \
+  else if (bits == 4) IQ_LAUNCH_COMPRESS(T_, false, 4); \
+  else IQ_LAUNCH_COMPRESS(T_, false, 3);
   if (dtype == IQ_DTYPE_F16) {
-    if (pages) IQ_LAUNCH_COMPRESS(__half, true);
-    else IQ_LAUNCH_COMPRESS(__half, false);
+    IQ_LAUNCH_COMPRESS_T(__half)
   } else {
-    if (pages) IQ_LAUNCH_COMPRESS(float, true);
-    else IQ_LAUNCH_COMPRESS(float, false);
+    IQ_LAUNCH_COMPRESS_T(float)
   }
+#undef IQ_LAUNCH_COMPRESS_T
 #undef IQ_LAUNCH_COMPRESS
   return hipGetLastError();
 }
@@ -304,10 +347,10 @@ hipError_t launch_compress_any(const void* k, const void* v, int dtype, int64_t 
 hipError_t launch_compress(const void* k, const void* v, int dtype, int64_t batch,
                            int64_t n_heads, int64_t n_tokens, const float* quats,
                            uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
-                           float* v_norms, int64_t capacity, int64_t dst_offset,
+                           float* v_norms, int64_t capacity, int64_t dst_offset, int bits,
                            hipStream_t stream) {
   return launch_compress_any(k, v, dtype, batch, n_heads, n_tokens, quats, k_codes, k_norms,
-                             v_codes, v_norms, capacity, dst_offset, nullptr, stream);
+                             v_codes, v_norms, capacity, dst_offset, nullptr, bits, stream);
 }
 
 hipError_t launch_compress_paged(const void* k, const void* v, int dtype, int64_t batch,
@@ -317,7 +360,7 @@ hipError_t launch_compress_paged(const void* k, const void* v, int dtype, int64_
                                  hipStream_t stream) {
   return launch_compress_any(k, v, dtype, batch, n_heads, n_tokens, quats, k_codes, k_norms,
                              v_codes, v_norms, (pages.max_pages << pages.page_shift), dst_offset,
-                             &pages, stream);
+                             &pages, 3, stream);
 }
 
 hipError_t launch_append(const void* k, const void* v, int dtype, int64_t batch,

@@ -311,7 +311,7 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, uint8_t* k_code
     float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
     return launch_decode_g8(plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes,
                             k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len, quats,
-                            batch, n_kv_heads, scale, out, parts, append, nullptr, stream);
+                            batch, n_kv_heads, scale, out, parts, append, nullptr, 3, stream);
   }
   if (append) {
     // generic path of the fused step: the append kernel, then attention

@@ -1,5 +1,8 @@
 // Decode attention on the packed 3-bit cache for groups of 8 query heads per
-// KV head (App. A; Table 2 A-D; Sec. 3.4), gfx950.
+// KV head (App. A; Table 2 A-D; Sec. 3.4), gfx950.  The same kernel runs on
+// 2- and 4-bit records (Algorithm 1 at b = 2, 4); the notes below describe
+// the 3-bit case, the others differ only in how a lane's slice of a record
+// splits into code pairs.
 //
 // Work decomposition: one 512-thread workgroup (8 waves, two per SIMD) per
 // (split of 16 * nbat positions, KV head g, sequence b), the grid's three
@@ -119,6 +122,46 @@ __device__ __forceinline__ uint32_t low6x4(uint32_t w) {
   else
     asm("v_lshlrev_b32_sdwa %0, 2, %1 dst_sel:BYTE_0 dst_unused:UNUSED_PAD src0_sel:DWORD "
         "src1_sel:BYTE_3" : "=v"(r) : "v"(w));
+  return r;
+}
+// 4 * byte K of w (a 4-bit code pair, 256-entry table), one SDWA shift.
+template <int K>
+__device__ __forceinline__ uint32_t byte4x4(uint32_t w) {
+  static_assert(K >= 0 && K < 4, "byte index");
+  uint32_t r;
+  if constexpr (K == 0)
+    asm("v_lshlrev_b32_sdwa %0, 2, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD "
+        "src1_sel:BYTE_0" : "=v"(r) : "v"(w));
+  else if constexpr (K == 1)
+    asm("v_lshlrev_b32_sdwa %0, 2, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD "
+        "src1_sel:BYTE_1" : "=v"(r) : "v"(w));
+  else if constexpr (K == 2)
+    asm("v_lshlrev_b32_sdwa %0, 2, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD "
+        "src1_sel:BYTE_2" : "=v"(r) : "v"(w));
+  else
+    asm("v_lshlrev_b32_sdwa %0, 2, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD "
+        "src1_sel:BYTE_3" : "=v"(r) : "v"(w));
+  return r;
+}
+// 4 * a nibble (a 2-bit code pair, 16-entry table): byte K of u masked with
+// 0x3C, one SDWA AND.  With u = w << 2 that is the low nibble of byte K of
+// w, with u = w >> 2 its high nibble.
+template <int K>
+__device__ __forceinline__ uint32_t nib4x4(uint32_t u) {
+  static_assert(K >= 0 && K < 4, "byte index");
+  uint32_t r;
+  if constexpr (K == 0)
+    asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_0 "
+        "src1_sel:DWORD" : "=v"(r) : "v"(u), "s"(0x3Cu));
+  else if constexpr (K == 1)
+    asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 "
+        "src1_sel:DWORD" : "=v"(r) : "v"(u), "s"(0x3Cu));
+  else if constexpr (K == 2)
+    asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_2 "
+        "src1_sel:DWORD" : "=v"(r) : "v"(u), "s"(0x3Cu));
+  else
+    asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3 "
+        "src1_sel:DWORD" : "=v"(r) : "v"(u), "s"(0x3Cu));
   return r;
 }
 // Pair-table entry at byte offset a4 (the table sits at LDS address 0).
@@ -258,13 +301,23 @@ __device__ __forceinline__ f32x4_t decode_record_dims(const uint32_t* rec, const
                  static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p1 >> 16)))};
 }
 
+// Staged record stride (words) for b-bit records of 4b words: 13 for the
+// 3-bit records; 10 and 20 put the four lane groups of the value reads
+// (record 4 gk + r, word u or u / 2) on disjoint banks.
+template <int kBits>
+constexpr int rec_stride() {
+  return kBits == 3 ? kRecStride : (kBits == 2 ? 10 : 20);
+}
+
 // Per-wave LDS staging: the two scale arrays of the wave (a 16-byte group
 // per lane, 64 groups) and the value records of all its batches.
-struct WaveStage {
+template <int kBits>
+struct WaveStageB {
   f32x4_t ks[64];
   f32x4_t vs[64];
-  uint32_t rec[kMaxBatches][16 * kRecStride];
+  uint32_t rec[kMaxBatches][16 * rec_stride<kBits>()];
 };
+using WaveStage = WaveStageB<3>;
 
 // Cache loads of one wave, in the order the data is used: both scale arrays
 // (one 16-byte load per lane: lane j takes positions 4j .. 4j+3 of the
@@ -282,12 +335,13 @@ struct WaveStage {
 // kPaged: batch i of the wave lies at record index dlt[i] + (its position)
 // of the pools (dlt[i] = the batch page's record base minus the page's first
 // logical position); contiguous caches use the row pointers as they are.
-template <int NB, bool kPaged>
+template <int NB, bool kPaged, int kBits>
 __device__ __forceinline__ void load_keys(const uint8_t* kc, const float* kn, const float* vn,
                                           const int64_t (&dlt)[NB], int wbase, int clamp16,
-                                          int lane, int col, int grp, uint32_t (&kw)[NB][3],
+                                          int lane, int col, int grp, uint32_t (&kw)[NB][kBits],
                                           f32x4_t& ksl, f32x4_t& vsl) {
-  const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
+  constexpr int kRB = record_bytes<kBits>();
+  const uint32_t koff = static_cast<uint32_t>(col * kRB + 4 * kBits * grp);
   // scales: lane j -> batch j / 4 (clamped like the batches), group j % 4
   {
     const int jb = lane >> 2 < NB ? lane >> 2 : NB - 1;
@@ -305,12 +359,11 @@ __device__ __forceinline__ void load_keys(const uint8_t* kc, const float* kn, co
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
     const int tb = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
-    const uint8_t* kb = kPaged ? kc + dlt[i] * kRecordBytes : kc;
+    const uint8_t* kb = kPaged ? kc + dlt[i] * kRB : kc;
     const uint32_t* p =
-        reinterpret_cast<const uint32_t*>(kb + static_cast<uint32_t>(tb * kRecordBytes) + koff);
-    kw[i][0] = p[0];
-    kw[i][1] = p[1];
-    kw[i][2] = p[2];
+        reinterpret_cast<const uint32_t*>(kb + static_cast<uint32_t>(tb * kRB) + koff);
+#pragma unroll
+    for (int j = 0; j < kBits; ++j) kw[i][j] = p[j];
   }
   __builtin_amdgcn_sched_barrier(0);
 }
@@ -319,15 +372,99 @@ __device__ __forceinline__ void load_keys(const uint8_t* kc, const float* kn, co
 // vector-memory ones (keeps the value loads in their place and order).
 constexpr int kNoVmemAcross = 0x1 | 0x2 | 0x4 | 0x8 | 0x80 | 0x100 | 0x200 | 0x400;
 
-// Value slice of one batch: lane (t = col, gk = grp) takes dwords 3gk ..
-// 3gk+2 of position tb + t (one coalesced 768-byte load).
+// Value slice of one batch: lane (t = col, gk = grp) takes dwords b gk ..
+// b gk + b - 1 of position tb + t (one coalesced 16 x 8b-byte load; 768
+// bytes at b = 3).
+template <int kBits>
 __device__ __forceinline__ void load_value_batch(const uint8_t* vc, int tb, uint32_t koff,
-                                                 uint32_t (&v)[3]) {
-  const uint32_t* p =
-      reinterpret_cast<const uint32_t*>(vc + static_cast<uint32_t>(tb * kRecordBytes) + koff);
-  v[0] = p[0];
-  v[1] = p[1];
-  v[2] = p[2];
+                                                 uint32_t (&v)[kBits]) {
+  const uint32_t* p = reinterpret_cast<const uint32_t*>(
+      vc + static_cast<uint32_t>(tb * record_bytes<kBits>()) + koff);
+#pragma unroll
+  for (int j = 0; j < kBits; ++j) v[j] = p[j];
+}
+
+// QK operand dwords of one lane: pairs F = 4 kb + e (e = 0..3) of its slice
+// w (the lane's 32 dims), each a byte offset into the pair table.
+template <int kBits>
+__device__ __forceinline__ void key_pairs(const uint32_t* lut, const uint32_t (&w)[kBits],
+                                          u32x4_t (&a)[4]) {
+  if constexpr (kBits == 3) {
+    // fields F = 0..15 at bit 6F of the 96-bit slice w0:w1:w2: those at
+    // bits 0 or 2 mod 8 are byte selects of w0..w2, the others byte selects
+    // of the slice shifted right by 4 (u0..u2)
+    const uint32_t w0 = w[0], w1 = w[1], w2 = w[2];
+    const uint32_t u0 = __builtin_amdgcn_alignbit(w1, w0, 4);
+    const uint32_t u1 = __builtin_amdgcn_alignbit(w2, w1, 4);
+    const uint32_t u2 = w2 >> 4;
+    a[0] = u32x4_t{lut_at(lut, low6x4<0>(w0)), lut_at(lut, top6x4<0>(u0)),
+                   lut_at(lut, low6x4<1>(u0)), lut_at(lut, top6x4<2>(w0))};
+    a[1] = u32x4_t{lut_at(lut, low6x4<3>(w0)), lut_at(lut, top6x4<3>(u0)),
+                   lut_at(lut, low6x4<0>(u1)), lut_at(lut, top6x4<1>(w1))};
+    a[2] = u32x4_t{lut_at(lut, low6x4<2>(w1)), lut_at(lut, top6x4<2>(u1)),
+                   lut_at(lut, low6x4<3>(u1)), lut_at(lut, top6x4<0>(w2))};
+    a[3] = u32x4_t{lut_at(lut, low6x4<1>(w2)), lut_at(lut, top6x4<1>(u2)),
+                   lut_at(lut, low6x4<2>(u2)), lut_at(lut, top6x4<3>(w2))};
+  } else if constexpr (kBits == 4) {
+    // pair F = byte F of the 16-byte slice: byte e of word kb
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+      a[kb] = u32x4_t{lut_at(lut, byte4x4<0>(w[kb])), lut_at(lut, byte4x4<1>(w[kb])),
+                      lut_at(lut, byte4x4<2>(w[kb])), lut_at(lut, byte4x4<3>(w[kb]))};
+  } else {
+    static_assert(kBits == 2, "2, 3 or 4 bits");
+    // pair F = nibble F of the 8-byte slice: nibbles 0..3 of bytes 2 (kb % 2)
+    // and 2 (kb % 2) + 1 of word kb / 2
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t lo = w[h] << 2, hi = w[h] >> 2;
+      a[2 * h] = u32x4_t{lut_at(lut, nib4x4<0>(lo)), lut_at(lut, nib4x4<0>(hi)),
+                         lut_at(lut, nib4x4<1>(lo)), lut_at(lut, nib4x4<1>(hi))};
+      a[2 * h + 1] = u32x4_t{lut_at(lut, nib4x4<2>(lo)), lut_at(lut, nib4x4<2>(hi)),
+                             lut_at(lut, nib4x4<3>(lo)), lut_at(lut, nib4x4<3>(hi))};
+    }
+  }
+}
+
+// PV operand dwords of lane u = col for the position rows 4 gk + r of a
+// staged batch: pairs F = 4u + nb (nb = 0..3), i.e. dims 8u .. 8u + 7.
+// 3 bits: bytes 3u .. 3u + 2 of the record, found in the 8-byte window at
+// word vdw shifted right by vsh; 4 bits: word u (vdw = u); 2 bits: the half
+// of word u / 2 (vdw) at bit vsh = 16 (u % 2).
+template <int kBits>
+__device__ __forceinline__ void value_pairs(const uint32_t* lut, const uint32_t* rec, int grp,
+                                            int vdw, uint32_t vsh, u32x4_t (&vb)[4]) {
+  constexpr int kStride = rec_stride<kBits>();
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const uint32_t* wp = rec + (4 * grp + r) * kStride + vdw;
+    if constexpr (kBits == 3) {
+      // bytes 3u .. 3u+2 of the 8-byte window (a 64-bit shift: lane 15's
+      // bytes start 5 bytes in)
+      const uint64_t w64 = (static_cast<uint64_t>(wp[1]) << 32) | wp[0];
+      // fields at bits 0, 6, 12, 18 of the window: bits 0 and 18 are byte
+      // selects of it, bits 6 and 12 of the window shifted right by 4
+      const uint32_t win = static_cast<uint32_t>(w64 >> vsh);
+      const uint32_t wu = static_cast<uint32_t>(w64 >> (vsh + 4));
+      vb[0][r] = lut_at(lut, low6x4<0>(win));
+      vb[1][r] = lut_at(lut, top6x4<0>(wu));
+      vb[2][r] = lut_at(lut, low6x4<1>(wu));
+      vb[3][r] = lut_at(lut, top6x4<2>(win));
+    } else if constexpr (kBits == 4) {
+      const uint32_t x = wp[0];
+      vb[0][r] = lut_at(lut, byte4x4<0>(x));
+      vb[1][r] = lut_at(lut, byte4x4<1>(x));
+      vb[2][r] = lut_at(lut, byte4x4<2>(x));
+      vb[3][r] = lut_at(lut, byte4x4<3>(x));
+    } else {
+      const uint32_t x = wp[0] >> vsh;
+      const uint32_t lo = x << 2, hi = x >> 2;
+      vb[0][r] = lut_at(lut, nib4x4<0>(lo));
+      vb[1][r] = lut_at(lut, nib4x4<0>(hi));
+      vb[2][r] = lut_at(lut, nib4x4<1>(lo));
+      vb[3][r] = lut_at(lut, nib4x4<1>(hi));
+    }
+  }
 }
 
 // Scores, softmax and value accumulation of one wave over the batches that
@@ -346,11 +483,11 @@ __device__ __forceinline__ void load_value_batch(const uint8_t* vc, int tb, uint
 // (lane (t, gk) writes its 12 bytes of record t, lane (u, grp) reads the
 // 8-byte window holding bytes 3u..3u+2 of records 4 grp + r); the wave's own
 // LDS operations complete in order.
-template <int NB, int NBX, bool kFull, bool kWide, bool kPaged>
-__device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
-                                            uint32_t (&vw)[NB][3], const uint8_t* vc,
+template <int NB, int NBX, bool kFull, bool kWide, bool kPaged, int kBits>
+__device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][kBits],
+                                            uint32_t (&vw)[NB][kBits], const uint8_t* vc,
                                             uint32_t koff, const int (&tb)[NB],
-                                            const int64_t (&dlt)[NB], WaveStage& st,
+                                            const int64_t (&dlt)[NB], WaveStageB<kBits>& st,
                                             const u32x4_t (&qb)[4],
                                             const uint32_t* lut, int col, int grp, int nvalid,
                                             int vdw, uint32_t vsh, float qdown, float& m_run,
@@ -363,24 +500,11 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
   for (int i = 0; i < NBX; ++i) {
     if (!kFull && 16 * i >= nvalid) break;
     __builtin_amdgcn_sched_barrier(kNoVmemAcross);
-    load_value_batch(kPaged ? vc + dlt[i] * kRecordBytes : vc, tb[i], koff, vw[i]);
+    load_value_batch<kBits>(kPaged ? vc + dlt[i] * record_bytes<kBits>() : vc, tb[i], koff,
+                            vw[i]);
     __builtin_amdgcn_sched_barrier(kNoVmemAcross);
-    const uint32_t w0 = kw[i][0], w1 = kw[i][1], w2 = kw[i][2];
-    // fields F = 0..15 at bit 6F of the 96-bit slice w0:w1:w2: those at
-    // bits 0 or 2 mod 8 are byte selects of w0..w2, the others byte selects
-    // of the slice shifted right by 4 (u0..u2)
-    const uint32_t u0 = __builtin_amdgcn_alignbit(w1, w0, 4);
-    const uint32_t u1 = __builtin_amdgcn_alignbit(w2, w1, 4);
-    const uint32_t u2 = w2 >> 4;
-    const u32x4_t a[4] = {
-        u32x4_t{lut_at(lut, low6x4<0>(w0)), lut_at(lut, top6x4<0>(u0)),
-                lut_at(lut, low6x4<1>(u0)), lut_at(lut, top6x4<2>(w0))},
-        u32x4_t{lut_at(lut, low6x4<3>(w0)), lut_at(lut, top6x4<3>(u0)),
-                lut_at(lut, low6x4<0>(u1)), lut_at(lut, top6x4<1>(w1))},
-        u32x4_t{lut_at(lut, low6x4<2>(w1)), lut_at(lut, top6x4<2>(u1)),
-                lut_at(lut, low6x4<3>(u1)), lut_at(lut, top6x4<0>(w2))},
-        u32x4_t{lut_at(lut, low6x4<1>(w2)), lut_at(lut, top6x4<1>(u2)),
-                lut_at(lut, low6x4<2>(u2)), lut_at(lut, top6x4<3>(w2))}};
+    u32x4_t a[4];
+    key_pairs<kBits>(lut, kw[i], a);
     f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) acc = mfma(a[kb], qb[kb], acc);
@@ -432,9 +556,9 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
 #pragma unroll
   for (int i = 0; i < NBX; ++i) {
     if (!kFull && 16 * i >= nvalid) break;
-    st.rec[i][col * kRecStride + 3 * grp] = vw[i][0];
-    st.rec[i][col * kRecStride + 3 * grp + 1] = vw[i][1];
-    st.rec[i][col * kRecStride + 3 * grp + 2] = vw[i][2];
+#pragma unroll
+    for (int j = 0; j < kBits; ++j)
+      st.rec[i][col * rec_stride<kBits>() + kBits * grp + j] = vw[i][j];
   }
   wave_lds_fence();
 #pragma unroll
@@ -454,21 +578,7 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
       pw_lo[r] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, pl)) << slot_shift;
     }
     u32x4_t vb[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      // bytes 3u .. 3u+2 of the 8-byte window (a 64-bit shift: lane 15's
-      // bytes start 5 bytes in)
-      const uint32_t* wp = rec + (4 * grp + r) * kRecStride + vdw;
-      const uint64_t w64 = (static_cast<uint64_t>(wp[1]) << 32) | wp[0];
-      // fields at bits 0, 6, 12, 18 of the window: bits 0 and 18 are byte
-      // selects of it, bits 6 and 12 of the window shifted right by 4
-      const uint32_t win = static_cast<uint32_t>(w64 >> vsh);
-      const uint32_t wu = static_cast<uint32_t>(w64 >> (vsh + 4));
-      vb[0][r] = lut_at(lut, low6x4<0>(win));
-      vb[1][r] = lut_at(lut, top6x4<0>(wu));
-      vb[2][r] = lut_at(lut, low6x4<1>(wu));
-      vb[3][r] = lut_at(lut, top6x4<2>(win));
-    }
+    value_pairs<kBits>(lut, rec, grp, vdw, vsh, vb);
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
       o_acc[nb] = mfma(pw_hi, vb[nb], o_acc[nb]);
@@ -498,19 +608,26 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][3],
 // kPaged: the cache is a page pool (PageTable); capacity is then the logical
 // capacity max_pages * page_size, and every batch of 16 positions and the
 // new token's slot are located through the page table.
-template <int NB, bool kAppend, bool kWide, bool kPaged>
+//
+// kBits: the records' code width, 3 (the paper's cache) or 2 / 4 (Algorithm
+// 1 with C_2 / C_4: records of 32 / 64 bytes).  The fused step and paged
+// pools run on 3-bit records only.
+template <int NB, bool kAppend, bool kWide, bool kPaged, int kBits>
 __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     const float* __restrict__ q, uint8_t* __restrict__ k_codes, float* __restrict__ k_norms,
     uint8_t* __restrict__ v_codes, float* __restrict__ v_norms,
     const int32_t* __restrict__ seq_lens, const float* __restrict__ quats,
     float* __restrict__ partials, float* __restrict__ out, int64_t capacity, int max_seq_len,
-    int n_kv_heads, int n_splits, int split_len, float qscale, Codebook cb,
+    int n_kv_heads, int n_splits, int split_len, float qscale, CodebookB<kBits> cb,
     const void* __restrict__ k_new, const void* __restrict__ v_new, int new_f16,
     int32_t* __restrict__ status, PageTable pages) {
+  static_assert(kBits == 3 || (!kAppend && !kPaged), "fused step and pages: 3-bit records");
+  constexpr int kRB = record_bytes<kBits>();
+  constexpr int kLut = 1 << (2 * kBits);   // pairs of codes
   // All LDS of the kernel in one object, the pair table first (address 0:
   // a lookup address is just field * 4).
   struct Smem {
-    uint32_t lut[64];   // fp16 pair table: entry f = (C[f % 8], C[f / 8])
+    uint32_t lut[kLut];   // fp16 pair table: entry f = (C[f % 2^b], C[f / 2^b])
     uint32_t qop[2][kHeads][kQRowWords];
     int qexp[kHeads];
     float wave_ml[kWaves][2][kHeads];
@@ -520,7 +637,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     // (wave_o[w][r][lane] = the lane's accumulator entries r of the four
     // PV products, as written by the matrix cores)
     union {
-      WaveStage stage[kWaves];
+      WaveStageB<kBits> stage[kWaves];
       f32x4_t wave_o[kWaves][4][64];
     };
   };
@@ -529,7 +646,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   uint32_t(*qop)[kHeads][kQRowWords] = sm.qop;
   int* qexp_s = sm.qexp;
   float(*wave_ml)[2][kHeads] = sm.wave_ml;
-  WaveStage* stage = sm.stage;
+  WaveStageB<kBits>* stage = sm.stage;
   f32x4_t(*wave_o)[4][64] = sm.wave_o;
 
   const int tid = threadIdx.x;
@@ -561,10 +678,10 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   // contiguous: the (b, g) row; paged: the pools (positions are placed by
   // the per-batch deltas)
   const int64_t row = kPaged ? 0 : static_cast<int64_t>(bg) * capacity;
-  uint8_t* kc = k_codes + row * kRecordBytes;
-  uint8_t* vc = v_codes + row * kRecordBytes;
+  uint8_t* kc = k_codes + row * kRB;
+  uint8_t* vc = v_codes + row * kRB;
 
-  if (kAppend && split == n_splits) {
+  if constexpr (kAppend) if (split == n_splits) {
     // ---- the append workgroup ------------------------------------------------
     const int seq0 = seq_lens[b];
     const bool appended = seq0 >= 0 && seq0 < capacity;
@@ -710,11 +827,22 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   const float* vn = v_norms + row;
 
   // ---- the cache loads (keys and scales now, values as the scores proceed)
-  uint32_t kw[NB][3], vw[NB][3];
+  uint32_t kw[NB][kBits], vw[NB][kBits];
   f32x4_t ksl, vsl;
-  load_keys<NB, kPaged>(kc, kn, vn, dlt, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
-  const int vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
-  const uint32_t vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));   // 0..40
+  load_keys<NB, kPaged, kBits>(kc, kn, vn, dlt, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
+  // the word of the value window of lane u = col (see value_pairs)
+  int vdw;
+  uint32_t vsh;
+  if constexpr (kBits == 3) {
+    vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
+    vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));   // 0..40
+  } else if constexpr (kBits == 4) {
+    vdw = col;
+    vsh = 0;
+  } else {
+    vdw = col >> 1;
+    vsh = static_cast<uint32_t>(16 * (col & 1));
+  }
 
   // one-round grids: the length, read once the loads are in flight
   if constexpr (!kWide) seq0 = seq_lens[b];
@@ -724,11 +852,12 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   nvalid = nvalid < 16 * nb_w ? nvalid : 16 * nb_w;
 
   // ---- while the loads fly: LUT and the rotated query --------------------
-  if (tid < 64) {
+  if (tid < kLut) {
+    constexpr int kMask = (1 << kBits) - 1;
     const uint32_t lo =
-        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & 7)));
+        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & kMask)));
     const uint32_t hi =
-        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> 3)));
+        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> kBits)));
     lut[tid] = lo | (hi << 16);
   }
   // the 32 blocks of a head are 32 consecutive lanes of one wave, so the
@@ -768,7 +897,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     if (qblk == 0) qexp_s[qh] = qexp;
   }
   lds_barrier();   // lut, qop, qexp_s
-  const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
+  const uint32_t koff = static_cast<uint32_t>(col * kRB + 4 * kBits * grp);
   int tb[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) tb[i] = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
@@ -805,15 +934,17 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if (nvalid == 16 * NB)
-    attend_wave<NB, NB, true, kWide, kPaged>(kw, vw, vc, koff, tb, dlt, stage[wave], qb, lut, col, grp,
-                                     nvalid, vdw, vsh, qdown, m_run, l_run, vmax, o_acc);
+    attend_wave<NB, NB, true, kWide, kPaged, kBits>(kw, vw, vc, koff, tb, dlt, stage[wave], qb,
+                                                    lut, col, grp, nvalid, vdw, vsh, qdown,
+                                                    m_run, l_run, vmax, o_acc);
   else if (NB > 1 && nvalid == 16 * (NB - 1))
-    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true, kWide, kPaged>(kw, vw, vc, koff, tb, dlt, stage[wave], qb,
-                                                        lut, col, grp, nvalid, vdw, vsh, qdown,
-                                                        m_run, l_run, vmax, o_acc);
+    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true, kWide, kPaged, kBits>(
+        kw, vw, vc, koff, tb, dlt, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh, qdown,
+        m_run, l_run, vmax, o_acc);
   else if (nvalid > 0)
-    attend_wave<NB, NB, false, kWide, kPaged>(kw, vw, vc, koff, tb, dlt, stage[wave], qb, lut, col, grp,
-                                      nvalid, vdw, vsh, qdown, m_run, l_run, vmax, o_acc);
+    attend_wave<NB, NB, false, kWide, kPaged, kBits>(kw, vw, vc, koff, tb, dlt, stage[wave], qb,
+                                                     lut, col, grp, nvalid, vdw, vsh, qdown,
+                                                     m_run, l_run, vmax, o_acc);
 
   // ---- merge the 8 waves in LDS ---------------------------------------------
   lds_barrier();   // every wave is done with its staging area
@@ -1014,7 +1145,8 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                             int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                             const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
                             float* out, float* partials, const StepAppend* append,
-                            const PageTable* pages, hipStream_t stream) {
+                            const PageTable* pages, int bits, hipStream_t stream) {
+  if (bits != 3 && (append || pages)) return hipErrorInvalidValue;
   // partials per (sequence, KV head): the splits, and the fused step's new
   // token
   const int64_t n_parts = append ? n_splits + 1 : n_splits;
@@ -1030,23 +1162,27 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   const bool wide = n_parts * n_kv_heads * batch > kCus;
   const size_t lds_pad = wide ? 0 : kOneWorkgroupPadBytes;
   const float qscale = scale * kLog2e;
-  const Codebook& cb = codebook();
   const void* k_new = append ? append->k_new : nullptr;
   const void* v_new = append ? append->v_new : nullptr;
   const int new_f16 = append ? append->f16 : 0;
   int32_t* status = append ? append->status : nullptr;
   const PageTable pt = pages ? *pages : PageTable{nullptr, 0, 4, 1};
-#define IQ_LAUNCH_G8_WP(NB_, APP_, WIDE_, PAGED_)                                                \
-  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_, PAGED_>), grid, block, lds_pad, stream, \
-                     q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials, out,     \
-                     capacity, static_cast<int>(max_seq_len), static_cast<int>(n_kv_heads),     \
-                     static_cast<int>(n_splits), static_cast<int>(split_len), qscale, cb,      \
-                     k_new, v_new, new_f16, status, pt)
-#define IQ_LAUNCH_G8_W(NB_, APP_, WIDE_)        \
-  if (pages) {                                  \
-    IQ_LAUNCH_G8_WP(NB_, APP_, WIDE_, true);    \
-  } else {                                      \
-    IQ_LAUNCH_G8_WP(NB_, APP_, WIDE_, false);   \
+#define IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, PAGED_, BITS_)                                     \
+  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_, PAGED_, BITS_>), grid, block, lds_pad, \
+                     stream, q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials,  \
+                     out, capacity, static_cast<int>(max_seq_len),                              \
+                     static_cast<int>(n_kv_heads), static_cast<int>(n_splits),                  \
+                     static_cast<int>(split_len), qscale, codebook_b<BITS_>(), k_new, v_new,    \
+                     new_f16, status, pt)
+#define IQ_LAUNCH_G8_W(NB_, APP_, WIDE_)                \
+  if (pages) {                                          \
+    IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, true, 3);        \
+  } else if (APP_ || bits == 3) {                       \
+    IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, false, 3);       \
+  } else if (bits == 2) {                               \
+    IQ_LAUNCH_G8_WPB(NB_, false, WIDE_, false, 2);      \
+  } else {                                              \
+    IQ_LAUNCH_G8_WPB(NB_, false, WIDE_, false, 4);      \
   }
 #define IQ_LAUNCH_G8(NB_, APP_)          \
   if (wide) {                            \
@@ -1070,7 +1206,7 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
 #undef IQ_LAUNCH_G8_NB
 #undef IQ_LAUNCH_G8
 #undef IQ_LAUNCH_G8_W
-#undef IQ_LAUNCH_G8_WP
+#undef IQ_LAUNCH_G8_WPB
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // the partials of every (sequence, query head) merged by a second launch,

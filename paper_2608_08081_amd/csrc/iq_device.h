@@ -53,21 +53,23 @@ __device__ __forceinline__ void so4_matrix_h4(const float* qv, float (&m)[4][4])
   for (int i = 0; i < 4; ++i) wht4(m[i][0], m[i][1], m[i][2], m[i][3]);
 }
 
-// Level i (0..7) of a codebook held in kernel arguments.  A select chain
+// Level i (0 .. 2^b - 1) of a codebook held in kernel arguments.  A select chain
 // over compile-time indices: indexing the argument struct with a lane value
 // would turn into a memory load, whose wait would also wait for every load
 // issued before it.
-__device__ __forceinline__ float codebook_level(const Codebook& cb, int i) {
+template <int kBits>
+__device__ __forceinline__ float codebook_level(const CodebookB<kBits>& cb, int i) {
   // readfirstlane pins each level to a register value, so that the selects
   // are not folded back into an address computation
-  float lv[8];
+  constexpr int n = 1 << kBits;
+  float lv[n];
 #pragma unroll
-  for (int j = 0; j < 8; ++j)
+  for (int j = 0; j < n; ++j)
     lv[j] = __builtin_bit_cast(
         float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, cb.level[j])));
   float v = lv[0];
 #pragma unroll
-  for (int j = 1; j < 8; ++j) v = (i == j) ? lv[j] : v;
+  for (int j = 1; j < n; ++j) v = (i == j) ? lv[j] : v;
   return v;
 }
 

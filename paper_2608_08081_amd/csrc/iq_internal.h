@@ -18,14 +18,27 @@ constexpr int kNumBlocks = 32;      // SO(4) blocks per head (d / 4)
 constexpr int kQuatFloats = 256;    // stored parameters per head (App. B)
 constexpr int kMaxGroup = 16;       // query heads per KV head supported
 
-// 3-bit codebook, passed to kernels by value.  level[] ascending (fp16-exact
-// values), thr[j] = midpoint of level[j] and level[j+1].
-struct Codebook {
-  float level[8];
-  float thr[7];
+// Codebook C_b of b-bit codes, passed to kernels by value.  level[]
+// ascending (fp16-exact values), thr[j] = midpoint of level[j] and
+// level[j+1].  The cache format of the paper is b = 3 (Codebook); b = 2 and
+// b = 4 run through the same steps with 2^b levels.
+template <int kBits>
+struct CodebookB {
+  float level[1 << kBits];
+  float thr[(1 << kBits) - 1];
 };
+using Codebook = CodebookB<3>;
 
-// Computed on first use (host), immutable afterwards.
+// Bytes of one packed record of 128 b-bit codes.
+template <int kBits>
+constexpr int record_bytes() {
+  return kDim * kBits / 8;
+}
+
+// Computed on first use (host), immutable afterwards.  codebook_b<b>() for
+// b = 2, 3, 4; codebook() is codebook_b<3>().
+template <int kBits>
+const CodebookB<kBits>& codebook_b();
 const Codebook& codebook();
 
 // A paged cache: records of logical position t of (sequence b, KV head g)
@@ -71,10 +84,11 @@ bool plan_decode(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
                  int64_t max_seq_len, DecodePlan* plan);
 
 // Kernel launchers (return the launch's hipError_t).
+// bits: 3 (the cache format), or 2 / 4 (records of 16 * bits bytes).
 hipError_t launch_compress(const void* k, const void* v, int dtype, int64_t batch,
                            int64_t n_heads, int64_t n_tokens, const float* quats,
                            uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
-                           float* v_norms, int64_t capacity, int64_t dst_offset,
+                           float* v_norms, int64_t capacity, int64_t dst_offset, int bits,
                            hipStream_t stream);
 
 // Bulk compression into a paged cache: tokens [0, n_tokens) of every
@@ -113,13 +127,14 @@ hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
              int64_t* n_splits, int64_t* split_len);
 // pages: null for a contiguous cache ([B][H_kv][capacity] records), else
-// the page table (capacity is then max_pages * page_size).
+// the page table (capacity is then max_pages * page_size).  bits: the
+// records' code width (2, 3 or 4; the fused step and pages need 3).
 hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const float* q,
                             uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
                             int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                             const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
                             float* out, float* partials, const StepAppend* append,
-                            const PageTable* pages, hipStream_t stream);
+                            const PageTable* pages, int bits, hipStream_t stream);
 
 // Reconstruct-then-compute baseline (Fig. 1 top): materialize the packed
 // cache as fp16 or fp32 vectors, and decode attention on an fp16 cache.

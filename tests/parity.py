@@ -19,9 +19,10 @@ ATTN_RTOL = 2e-3
 
 
 def check_codes(gpu_packed, oracle_codes, oracle_y, thresholds, label=""):
-    """Compare GPU records with the oracle's codes.  Returns the number of
-    (allowed) boundary mismatches."""
-    g = ocz.unpack(np.asarray(gpu_packed))
+    """Compare GPU records with the oracle's codes (code width b read off the
+    thresholds of C_b).  Returns the number of (allowed) boundary
+    mismatches."""
+    g = ocz.unpack(np.asarray(gpu_packed), 128, ocz.bits_of(thresholds))
     o = np.asarray(oracle_codes)
     assert g.shape == o.shape, (g.shape, o.shape)
     bad = g != o

@@ -288,3 +288,39 @@ def test_paged_compress_validation():
     assert call(page=96) == 1                    # multiple of 16, not a power of two
     assert call(dtype=7) == 2
     assert call(n=0) == 0
+
+
+def test_codebook_bits_equal_oracle():
+    """iq_codebook_bits equals the oracle's stored C_b exactly (b = 2, 3, 4)
+    and iq_codebook is C_3; other widths are refused."""
+    import numpy as np
+    from oracle import codebook as ocb
+    for bits in (2, 3, 4):
+        n = 1 << bits
+        lv = np.zeros(n, np.float32)
+        th = np.zeros(n - 1, np.float32)
+        assert L.iq_codebook_bits(bits, lv.ctypes.data_as(ctypes.c_void_p),
+                                  th.ctypes.data_as(ctypes.c_void_p)) == 0
+        s, t = ocb.isoquant_codebook(128, bits)
+        assert np.array_equal(lv.astype(np.float64), s)
+        assert np.array_equal(th.astype(np.float64), t)
+    assert L.iq_codebook_bits(5, None, None) == 2
+    assert L.iq_codebook_bits(1, None, None) == 2
+
+
+def test_bits_entry_point_validation():
+    def dec(**kw):
+        a = dict(hq=16, hkv=2, cap=256, msl=256, bits=4, b=1)
+        a.update(kw)
+        return L.iq_decode_attention_bits(A, A, A, B, B, A, a["cap"], a["msl"], A, a["b"],
+                                          a["hq"], a["hkv"], 128, 0.0, A, A, 1 << 30, a["bits"],
+                                          None)
+    assert dec(bits=5) == 2
+    assert dec(bits=1) == 2
+    assert dec(hq=8) == 2                        # group 4: matrix-core path only
+    assert dec(cap=250, msl=250) == 2            # capacity not a multiple of 16
+    assert dec(msl=300) == 1                     # max_seq_len beyond capacity
+    assert dec(b=0) == 0
+    assert L.iq_compress_kv_bits(A, B, 1, 1, 2, 10, 128, A, A, A, B, B, 16, 0, 5, None) == 2
+    assert L.iq_compress_kv_bits(A, B, 1, 1, 2, 10, 128, A, A, A, B, B, 16, 10, 4, None) == 1
+    assert L.iq_compress_kv_bits(A, B, 1, 1, 2, 0, 128, A, A, A, B, B, 16, 0, 2, None) == 0
