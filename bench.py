@@ -30,6 +30,8 @@ the default is the one above):
   paged     the varlen shape on a paged cache (iq_decode_step_paged; pages of
             --page-size positions, physical pages randomly permuted), then
             on contiguous caches with the same lengths for comparison;
+  bits32k   decode attention at the 32K shape on 2-, 3- and 4-bit records
+            (Algorithm 1 with C_b; --bits picks the one reported as value);
   baseline32k  the 32K shape above through the reconstruct-then-compute
             pipeline the packed path replaces (Fig. 1 top): decode attention
             on an fp16 cache, materialization of the packed cache as fp16
@@ -61,7 +63,7 @@ def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--workload", choices=("step32k", "varlen", "compress", "append8k",
-                                          "baseline32k", "rotation_fit", "paged"),
+                                          "baseline32k", "rotation_fit", "paged", "bits32k"),
                    default="step32k")
     p.add_argument("--steps", type=int, default=None,
                    help="timed steps (default: 4800; varlen 240; compress 20; append8k 1000)")
@@ -70,6 +72,8 @@ def parse():
     p.add_argument("--layers", type=int, default=None,
                    help="distinct layer caches cycled (default: 48; varlen 3)")
     p.add_argument("--context", type=int, default=32768)
+    p.add_argument("--bits", type=int, choices=(2, 3, 4), default=4,
+                   help="code width reported as value by the bits32k workload")
     p.add_argument("--page-size", type=int, default=16,
                    help="positions per page of the paged workload (a power of two, >= 16)")
     p.add_argument("--seed", type=int, default=0)
@@ -80,7 +84,7 @@ def parse():
     a = p.parse_args()
     defaults = {"step32k": (4800, 48), "varlen": (240, 3), "compress": (20, 1),
                 "append8k": (1000, 48), "baseline32k": (960, 48),
-                "rotation_fit": (1, 1), "paged": (240, 3)}[a.workload]
+                "rotation_fit": (1, 1), "paged": (240, 3), "bits32k": (960, 48)}[a.workload]
     if a.steps is None:
         a.steps = defaults[0]
     if a.warmup is None:
@@ -108,7 +112,7 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def make_layers(api, synth, w, n_layers, context, capacity, seed, dev):
+def make_layers(api, synth, w, n_layers, context, capacity, seed, dev, bits=3):
     """Per layer: packed caches filled with `context` compressed tokens of
     fresh synthetic keys/values (seeded, drawn on the device with the same
     recipe as synth.kv_tensor), the token to append, and the query."""
@@ -120,7 +124,7 @@ def make_layers(api, synth, w, n_layers, context, capacity, seed, dev):
     for li in range(n_layers):
         g = torch.Generator(device=dev)
         g.manual_seed(seed * 100003 + li)
-        cache = api.alloc_cache(w.batch, w.n_kv_heads, capacity, dev)
+        cache = api.alloc_cache(w.batch, w.n_kv_heads, capacity, dev, bits=bits)
         scales = []
         for which, stream in (("k", 0), ("v", 1)):
             sc = synth.channel_scales(synth.rng(seed + li, w.wid, stream), w.n_kv_heads)
@@ -129,8 +133,8 @@ def make_layers(api, synth, w, n_layers, context, capacity, seed, dev):
         k = (k * scales[0][None, :, None, :]).half()
         v = torch.randn((w.batch, w.n_kv_heads, context, 128), generator=g, device=dev)
         v = (v * scales[1][None, :, None, :]).half()
-        api.iq_compress_kv(k, v, quats, cache["k_codes"], cache["k_norms"], cache["v_codes"],
-                           cache["v_norms"])
+        api.iq_compress_kv_bits(k, v, quats, cache["k_codes"], cache["k_norms"],
+                                cache["v_codes"], cache["v_norms"], bits=bits)
         del k, v
         cache["seq_lens"].fill_(context)
         k_new = (torch.randn((w.batch, w.n_kv_heads, 128), generator=g, device=dev)
@@ -567,6 +571,62 @@ def time_graph_sweeps(torch, fn, n_layers, steps, warmup):
     return ev0.elapsed_time(ev1) * 1e3 / (reps * n_layers)
 
 
+def run_bits32k(args, torch, api, synth, dev):
+    """Decode attention at the 32K shape on caches of b-bit records (Algorithm
+    1 with C_b; b = 2, 3, 4, each its own set of layer caches compressed from
+    the same seeded fp16 K/V recipe), iq_decode_attention_bits replayed from
+    HIP graphs over the cycled layers.  Algorithmic bytes per position and
+    KV head: K and V records of 16 b bytes plus their fp32 scales."""
+    w = synth.WORKLOADS[2]
+    nl = args.layers
+    cap = args.context
+    per = {}
+    for bits in (2, 3, 4):
+        print(f"# building {nl} layer caches of {bits}-bit records", file=sys.stderr, flush=True)
+        quats, layers = make_layers(api, synth, w, nl, cap, cap, args.seed, dev, bits=bits)
+        ws = api.alloc_workspace(w.batch, w.n_q_heads, w.n_kv_heads, cap, dev)
+
+        def call(li, layers=layers, quats=quats, ws=ws, bits=bits):
+            L = layers[li]
+            c = L["cache"]
+            api.iq_decode_attention_bits(L["q"], c["k_codes"], c["k_norms"], c["v_codes"],
+                                         c["v_norms"], c["seq_lens"], quats, out=L["out"],
+                                         workspace=ws, max_seq_len=cap, bits=bits)
+
+        us = time_graph_sweeps(torch, call, nl, args.steps, args.warmup)
+        nbytes = w.batch * w.n_kv_heads * cap * 2 * (16 * bits + 4)
+        per[bits] = {"us_per_call": round(us, 3), "bytes": int(nbytes),
+                     "gbs": round(nbytes / (us * 1e-6) / 1e9, 2)}
+        del layers, ws
+        torch.cuda.empty_cache()
+    b = args.bits
+    value = per[b]["gbs"]
+    return {
+        "metric": f"{b}-bit decode-attention µs/call + achieved HBM GB/s, 32K ctx",
+        "value": value,
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(per[b]["us_per_call"] / 1e3, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": f"u{b} codes, f32 accumulate",
+        "data": "synthetic (seeded anisotropic fp16 K/V, compressed on device)",
+        "config": {"workload": f"32K-context GQA decode attention on {b}-bit records, batch 1, "
+                               f"32 query heads, 4 KV heads, head_dim 128; {nl} distinct layer "
+                               "caches cycled (cold HBM)",
+                   "context": cap, "bits": b},
+        "roofline": {"bound": "hbm", "achieved": value, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(value / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": f"decode_g8_kernel<NB, false, false, false, {b}> + "
+                               "merge_g8_kernel<false>",
+                     "bytes_per_launch": per[b]["bytes"], "launch_us": per[b]["us_per_call"]},
+        "per_bits": {str(k): v for k, v in per.items()},
+    }
+
+
 def run_baseline32k(args, torch, api, synth, dev):
     """Reconstruct-then-compute (Fig. 1 top) against compressed-space decode
     (Fig. 1 bottom) at the 32K shape.  Per layer the same seeded fp16 K/V
@@ -856,7 +916,8 @@ def main():
         del src, dst
     run = {"step32k": run_step32k, "varlen": run_varlen, "compress": run_compress,
            "append8k": run_append8k, "baseline32k": run_baseline32k,
-           "rotation_fit": run_rotation_fit, "paged": run_paged}[args.workload]
+           "rotation_fit": run_rotation_fit, "paged": run_paged,
+           "bits32k": run_bits32k}[args.workload]
     print(json.dumps(run(args, torch, api, synth, dev)), flush=True)
 
 
