@@ -95,6 +95,26 @@ def decode_fused_rotations(q, k_packed, k_norms, v_packed, v_norms, seq_lens, ro
     return out
 
 
+def decode_multi(q, k_packed, k_norms, v_packed, v_norms, seq_lens, quats, levels,
+                 scale=None):
+    """Decode of T query tokens per sequence over one cache (the verification
+    step of speculative decoding; App. A applied per token): the T tokens
+    occupy the last T of the seq_lens[b] cached positions, and token t
+    attends positions 0 .. seq_lens[b] - T + t (causal among the new tokens),
+    i.e. it is single-token decode with length max(seq_lens[b] - T + 1 + t, 0).
+
+    q: [B][T][H_q][d]; caches and quats as for decode_fused.  Returns
+    [B][T][H_q][d] fp64."""
+    q = np.asarray(q, dtype=np.float64)
+    bsz, t_new, hq, d = q.shape
+    out = np.zeros((bsz, t_new, hq, d))
+    for t in range(t_new):
+        lens = [max(int(n) - t_new + 1 + t, 0) for n in seq_lens]
+        out[:, t] = decode_fused(q[:, t], k_packed, k_norms, v_packed, v_norms, lens, quats,
+                                 levels, scale)
+    return out
+
+
 def decode_reconstruct(q, k_packed, k_norms, v_packed, v_norms, seq_lens, quats,
                        levels, scale=None):
     """Reconstruct-then-compute decode: dequantize, apply R^T per token, then

@@ -171,3 +171,49 @@ def test_exact_attention_matches_library_attention():
             ref = torch.nn.functional.scaled_dot_product_attention(
                 qt, kt, vt, scale=scale)[:, 0, :].numpy()
             np.testing.assert_allclose(got[bb], ref, rtol=0, atol=1e-12)
+
+
+def test_decode_multi_brute_force_causal():
+    """Multi-token decode recomputed in explicit loops: token t attends the
+    cached positions before seq - T + 1 + t, so the last token sees every
+    position and the first sees all but the T - 1 newer ones."""
+    q1, kp, kn, vp, vn, quats, rots, *_ = _make_cache(4, 1, 1, 6, 2)
+    g = np.random.default_rng(9)
+    t_new, seq = 3, 6
+    q = g.standard_normal((1, t_new, 2, 128)).astype(np.float32)
+    got = att.decode_multi(q, kp, kn, vp, vn, [seq], quats, LEVELS)
+    d = 128
+    r = rots[0]
+    kc = cz.unpack(kp[0, 0])
+    vc = cz.unpack(vp[0, 0])
+    for t in range(t_new):
+        n = seq - t_new + 1 + t
+        for h in range(2):
+            qt = [sum(r[i][j] * float(q[0, t, h, j]) for j in range(d)) for i in range(d)]
+            scores = [float(kn[0, 0, p]) * sum(qt[i] * float(LEVELS[kc[p, i]]) for i in range(d))
+                      / math.sqrt(d) for p in range(n)]
+            m = max(scores)
+            e = [math.exp(s - m) for s in scores]
+            z = sum(e)
+            ot = [sum(e[p] / z * float(vn[0, 0, p]) * float(LEVELS[vc[p, i]]) for p in range(n))
+                  for i in range(d)]
+            o = [sum(r[i][j] * ot[i] for i in range(d)) for j in range(d)]
+            np.testing.assert_allclose(got[0, t, h], o, rtol=0, atol=1e-12 * max(map(abs, o)))
+
+
+def test_decode_multi_special_cases():
+    """T = 1 is single-token decode; a token whose causal length is 0 (seq < T)
+    gives a zero row; a token sees nothing past its own position (changing
+    the last cached record moves only the last token's output)."""
+    q, kp, kn, vp, vn, quats, *_ = _make_cache(6, 2, 2, 12, 4)
+    one = att.decode_multi(q[:, None], kp, kn, vp, vn, [12, 5], quats, LEVELS)
+    ref = att.decode_fused(q, kp, kn, vp, vn, [12, 5], quats, LEVELS)
+    assert np.array_equal(one[:, 0], ref)
+    g = np.random.default_rng(3)
+    qm = g.standard_normal((2, 3, 4, 128))
+    out = att.decode_multi(qm, kp, kn, vp, vn, [12, 2], quats, LEVELS)
+    assert np.all(out[1, 0] == 0) and np.any(out[1, 1] != 0)
+    kp2 = kp.copy()
+    kp2[0, :, 11] ^= 0xFF
+    out2 = att.decode_multi(qm, kp2, kn, vp, vn, [12, 2], quats, LEVELS)
+    assert np.array_equal(out2[0, :2], out[0, :2]) and not np.array_equal(out2[0, 2], out[0, 2])
