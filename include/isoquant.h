@@ -449,6 +449,39 @@ iq_status iq_decode_attention_bits(const float* q,
                                    void* workspace, size_t workspace_bytes, int bits,
                                    hipStream_t stream);
 
+/*
+ * Multi-token decode (the verification step of speculative decoding)
+ * ------------------------------------------------------------------
+ * n_tokens query tokens per sequence attend one packed 3-bit cache that
+ * already holds them at its last n_tokens positions: token t of sequence b
+ * attends positions 0 .. L_b - n_tokens + t, with L_b = min(seq_lens[b],
+ * max_seq_len) (causal among the new tokens; a token with no position gives
+ * a zero row).  Each token is App. A decode attention with that length; the
+ * cache is read once for all tokens.
+ *   q, out    : device fp32 [batch][n_tokens][n_q_heads][128], 16-byte
+ *               aligned (original space).
+ *   n_tokens  : 1 .. 4 (1 is iq_decode_attention);
+ *   workspace : >= iq_decode_multi_workspace_bytes(...) bytes, 256-byte
+ *               aligned, contents ignored on entry.
+ * Other arguments as for iq_decode_attention.  n_tokens >= 2 runs on the
+ * matrix-core path only (n_q_heads == 8 * n_kv_heads, capacity a multiple
+ * of 16 and >= 16, 16-byte aligned scale arrays, batch and n_kv_heads <=
+ * 65535); otherwise IQ_ERR_UNSUPPORTED.
+ */
+size_t iq_decode_multi_workspace_bytes(int64_t batch, int64_t n_tokens, int64_t n_q_heads,
+                                       int64_t n_kv_heads, int64_t max_seq_len,
+                                       int64_t head_dim);
+
+iq_status iq_decode_attention_multi(const float* q,
+                                    const uint8_t* k_codes, const float* k_norms,
+                                    const uint8_t* v_codes, const float* v_norms,
+                                    const int32_t* seq_lens, int64_t capacity,
+                                    int64_t max_seq_len, const float* quats,
+                                    int64_t batch, int64_t n_tokens, int64_t n_q_heads,
+                                    int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
+                                    float* out, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream);
+
 #ifdef __cplusplus
 }  /* extern "C" */
 #endif

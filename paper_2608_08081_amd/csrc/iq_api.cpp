@@ -5,6 +5,7 @@
 // derived here on first use with a Lloyd-Max iteration in double precision,
 // and the seeded rotation parameters (App. B) with SplitMix64.
 #include <math.h>
+#include <stdint.h>
 #include <string.h>
 
 #include <mutex>
@@ -389,6 +390,61 @@ iq_status iq_decode_attention_bits(const float* q, const uint8_t* k_codes, const
       const_cast<float*>(k_norms), const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms),
       const_cast<int32_t*>(seq_lens), capacity, max_seq_len, quats, batch, n_kv_heads,
       resolve_scale(softmax_scale), out, parts, nullptr, nullptr, bits, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+size_t iq_decode_multi_workspace_bytes(int64_t batch, int64_t n_tokens, int64_t n_q_heads,
+                                       int64_t n_kv_heads, int64_t max_seq_len,
+                                       int64_t head_dim) {
+  if (n_tokens == 1)
+    return iq_decode_workspace_bytes(batch, n_q_heads, n_kv_heads, max_seq_len, head_dim);
+  if (head_dim != kDim || batch < 0 || n_tokens < 2 || n_tokens > 4 || n_kv_heads <= 0 ||
+      n_q_heads != 8 * n_kv_heads || max_seq_len < 0 || batch > 65535 || n_kv_heads > 65535)
+    return 0;
+  int nb = 0;
+  int64_t splits = 0, len = 0;
+  iq::g8_plan(batch, n_kv_heads, max_seq_len, &nb, &splits, &len);
+  const size_t bytes = static_cast<size_t>(batch) * n_kv_heads * splits * n_tokens * 8 *
+                       (2 + kDim) * sizeof(float);
+  return bytes > 0 ? (bytes + 255) / 256 * 256 : 256;
+}
+
+iq_status iq_decode_attention_multi(const float* q, const uint8_t* k_codes,
+                                    const float* k_norms, const uint8_t* v_codes,
+                                    const float* v_norms, const int32_t* seq_lens,
+                                    int64_t capacity, int64_t max_seq_len, const float* quats,
+                                    int64_t batch, int64_t n_tokens, int64_t n_q_heads,
+                                    int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
+                                    float* out, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream) {
+  if (n_tokens == 1)
+    return iq_decode_attention(q, k_codes, k_norms, v_codes, v_norms, seq_lens, capacity,
+                               max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
+                               softmax_scale, out, workspace, workspace_bytes, stream);
+  if (n_tokens < 2 || n_tokens > 4) return IQ_ERR_UNSUPPORTED;
+  iq::DecodePlan plan;
+  // the single-token checks cover the cache, pointers and alignment; the
+  // workspace is checked against the multi-token size below
+  const iq_status st = check_decode_args(q, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                                         capacity, max_seq_len, quats, batch, n_q_heads,
+                                         n_kv_heads, head_dim, out, workspace, SIZE_MAX, &plan);
+  if (st != IQ_OK) return st;
+  if (n_q_heads != 8 * n_kv_heads || plan.g8_batches <= 0) return IQ_ERR_UNSUPPORTED;
+  if (capacity % 16 || capacity < 16 || capacity * iq::kRecordBytes > 0x7fffffff ||
+      !iq::aligned(k_norms, 16) || !iq::aligned(v_norms, 16) || batch > 65535 ||
+      n_kv_heads > 65535)
+    return IQ_ERR_UNSUPPORTED;
+  if (!iq::mul_ok(batch, n_tokens) || !iq::mul_ok(batch * n_tokens, n_q_heads))
+    return IQ_ERR_INVALID_ARGUMENT;
+  const size_t need = iq_decode_multi_workspace_bytes(batch, n_tokens, n_q_heads, n_kv_heads,
+                                                      max_seq_len, head_dim);
+  if (need == 0) return IQ_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < need) return IQ_ERR_WORKSPACE_TOO_SMALL;
+  if (batch == 0) return IQ_OK;
+  const hipError_t e = iq::launch_decode_g8_multi(
+      plan.g8_batches, plan.g8_splits, plan.g8_split_len, static_cast<int>(n_tokens), q,
+      k_codes, k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len, quats, batch,
+      n_kv_heads, resolve_scale(softmax_scale), out, static_cast<float*>(workspace), stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 

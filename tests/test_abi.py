@@ -324,3 +324,26 @@ def test_bits_entry_point_validation():
     assert L.iq_compress_kv_bits(A, B, 1, 1, 2, 10, 128, A, A, A, B, B, 16, 0, 5, None) == 2
     assert L.iq_compress_kv_bits(A, B, 1, 1, 2, 10, 128, A, A, A, B, B, 16, 10, 4, None) == 1
     assert L.iq_compress_kv_bits(A, B, 1, 1, 2, 0, 128, A, A, A, B, B, 16, 0, 2, None) == 0
+
+
+def test_multi_token_validation():
+    def call(**kw):
+        a = dict(b=1, t=2, hq=16, hkv=2, cap=256, msl=256, wsb=1 << 30)
+        a.update(kw)
+        return L.iq_decode_attention_multi(A, A, A, B, B, A, a["cap"], a["msl"], A, a["b"],
+                                           a["t"], a["hq"], a["hkv"], 128, 0.0, A, A, a["wsb"],
+                                           None)
+    assert call(t=5) == 2
+    assert call(t=0) == 2
+    assert call(hq=8) == 2                       # group 4: matrix-core path only
+    assert call(cap=250, msl=250) == 2
+    assert call(msl=300) == 1
+    assert call(wsb=16) == 3
+    assert call(b=0) == 0
+    ws1 = L.iq_decode_multi_workspace_bytes(1, 1, 16, 2, 256, 128)
+    assert ws1 == L.iq_decode_workspace_bytes(1, 16, 2, 256, 128)
+    w2 = L.iq_decode_multi_workspace_bytes(1, 2, 16, 2, 256, 128)
+    w4 = L.iq_decode_multi_workspace_bytes(1, 4, 16, 2, 256, 128)
+    assert w2 > 0 and w4 >= 2 * w2 - 256
+    assert L.iq_decode_multi_workspace_bytes(1, 5, 16, 2, 256, 128) == 0
+    assert L.iq_decode_multi_workspace_bytes(1, 2, 8, 2, 256, 128) == 0
