@@ -32,6 +32,9 @@ the default is the one above):
             on contiguous caches with the same lengths for comparison;
   bits32k   decode attention at the 32K shape on 2-, 3- and 4-bit records
             (Algorithm 1 with C_b; --bits picks the one reported as value);
+  multi32k  decode of 1-4 query tokens per call at the 32K shape
+            (iq_decode_attention_multi, speculative verification; --tokens picks
+            the one reported as value), against single-token calls;
   baseline32k  the 32K shape above through the reconstruct-then-compute
             pipeline the packed path replaces (Fig. 1 top): decode attention
             on an fp16 cache, materialization of the packed cache as fp16
@@ -63,7 +66,8 @@ def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--workload", choices=("step32k", "varlen", "compress", "append8k",
-                                          "baseline32k", "rotation_fit", "paged", "bits32k"),
+                                          "baseline32k", "rotation_fit", "paged", "bits32k",
+                                          "multi32k"),
                    default="step32k")
     p.add_argument("--steps", type=int, default=None,
                    help="timed steps (default: 4800; varlen 240; compress 20; append8k 1000)")
@@ -74,6 +78,8 @@ def parse():
     p.add_argument("--context", type=int, default=32768)
     p.add_argument("--bits", type=int, choices=(2, 3, 4), default=4,
                    help="code width reported as value by the bits32k workload")
+    p.add_argument("--tokens", type=int, choices=(1, 2, 3, 4), default=4,
+                   help="query tokens per call reported as value by the multi32k workload")
     p.add_argument("--page-size", type=int, default=16,
                    help="positions per page of the paged workload (a power of two, >= 16)")
     p.add_argument("--seed", type=int, default=0)
@@ -84,7 +90,8 @@ def parse():
     a = p.parse_args()
     defaults = {"step32k": (4800, 48), "varlen": (240, 3), "compress": (20, 1),
                 "append8k": (1000, 48), "baseline32k": (960, 48),
-                "rotation_fit": (1, 1), "paged": (240, 3), "bits32k": (960, 48)}[a.workload]
+                "rotation_fit": (1, 1), "paged": (240, 3), "bits32k": (960, 48),
+                "multi32k": (960, 48)}[a.workload]
     if a.steps is None:
         a.steps = defaults[0]
     if a.warmup is None:
@@ -627,6 +634,73 @@ def run_bits32k(args, torch, api, synth, dev):
     }
 
 
+def run_multi32k(args, torch, api, synth, dev):
+    """Multi-token decode at the 32K shape: T = 1..4 query tokens per call
+    over the same 48 cycled layer caches (iq_decode_attention_multi), against
+    T single-token calls.  Algorithmic bytes per call: the cache read once
+    (104 B per position and KV head) plus the T tokens' queries and outputs."""
+    import numpy as np
+
+    w = synth.WORKLOADS[2]
+    nl = args.layers
+    cap = args.context
+    print(f"# building {nl} layer caches", file=sys.stderr, flush=True)
+    quats, layers = make_layers(api, synth, w, nl, cap, cap, args.seed, dev)
+    per = {}
+    for n_tok in (1, 2, 3, 4):
+        g = torch.Generator(device=dev)
+        g.manual_seed(args.seed * 7 + n_tok)
+        qs = [torch.randn((w.batch, n_tok, w.n_q_heads, 128), generator=g, device=dev)
+              for _ in range(nl)]
+        outs = [torch.empty_like(x) for x in qs]
+        ws = torch.empty(api.iq_decode_multi_workspace_bytes(w.batch, n_tok, w.n_q_heads,
+                                                             w.n_kv_heads, cap),
+                         dtype=torch.uint8, device=dev)
+
+        def call(li, n_tok=n_tok, qs=qs, outs=outs, ws=ws):
+            c = layers[li]["cache"]
+            api.iq_decode_attention_multi(qs[li], c["k_codes"], c["k_norms"], c["v_codes"],
+                                          c["v_norms"], c["seq_lens"], quats, out=outs[li],
+                                          workspace=ws, max_seq_len=cap)
+
+        us = time_graph_sweeps(torch, call, nl, args.steps, args.warmup)
+        nbytes = w.n_kv_heads * cap * BYTES_PER_TOKEN_HEAD + 2 * n_tok * w.n_q_heads * 128 * 4
+        per[n_tok] = {"us_per_call": round(us, 3), "bytes": int(nbytes),
+                      "gbs": round(nbytes / (us * 1e-6) / 1e9, 2),
+                      "tokens_per_s": round(n_tok / (us * 1e-6), 1)}
+        del qs, outs, ws
+    t = args.tokens
+    single = per[1]["us_per_call"]
+    for n_tok, d in per.items():
+        d["vs_single_calls"] = round(n_tok * single / d["us_per_call"], 3)
+    value = per[t]["gbs"]
+    return {
+        "metric": f"{t}-token decode-attention µs/call + achieved HBM GB/s, 32K ctx",
+        "value": value,
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(per[t]["us_per_call"] / 1e3, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u3 codes, f32 accumulate",
+        "data": "synthetic (seeded anisotropic fp16 K/V, compressed on device)",
+        "config": {"workload": f"32K-context GQA decode of {t} query tokens per sequence "
+                               "(speculative verification, causal among them), batch 1, 32 query "
+                               f"heads, 4 KV heads, head_dim 128; {nl} distinct layer caches "
+                               "cycled (cold HBM)",
+                   "context": cap, "tokens": t},
+        "roofline": {"bound": "hbm", "achieved": value, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(value / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": f"decode_g8_multi_kernel<NB, false, {t}> + merge_g8_kernel<false, "
+                               f"{t}>" if t > 1 else "decode_g8_kernel + merge_g8_kernel",
+                     "bytes_per_launch": per[t]["bytes"], "launch_us": per[t]["us_per_call"]},
+        "per_tokens": {str(k): v for k, v in per.items()},
+    }
+
+
 def run_baseline32k(args, torch, api, synth, dev):
     """Reconstruct-then-compute (Fig. 1 top) against compressed-space decode
     (Fig. 1 bottom) at the 32K shape.  Per layer the same seeded fp16 K/V
@@ -917,7 +991,7 @@ def main():
     run = {"step32k": run_step32k, "varlen": run_varlen, "compress": run_compress,
            "append8k": run_append8k, "baseline32k": run_baseline32k,
            "rotation_fit": run_rotation_fit, "paged": run_paged,
-           "bits32k": run_bits32k}[args.workload]
+           "bits32k": run_bits32k, "multi32k": run_multi32k}[args.workload]
     print(json.dumps(run(args, torch, api, synth, dev)), flush=True)
 
 

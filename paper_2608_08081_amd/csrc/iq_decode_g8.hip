@@ -1011,9 +1011,10 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
 // loads and record decoding as decode_g8_kernel on 3-bit records: every
 // batch of keys and values is decoded once and feeds kT sets of matrix
 // instructions (the QK B operand of token t is read from LDS per batch).  The
-// softmax is online per batch (running max per token and head, rescaling the
-// accumulators), so only one batch of scores per token is live.  Partials
-// per (split, token, head); the merge kernel takes the token axis.
+// softmax is two-phase as in decode_g8_kernel: all scores of every token
+// first (kept in registers), one max per token and head, then the weights
+// and values.  Partials per (split, token, head); the merge kernel takes the
+// token axis.
 template <int NB, bool kWide, int kT>
 __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
     const float* __restrict__ q, const uint8_t* __restrict__ k_codes,
@@ -1109,8 +1110,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
   int tb[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) tb[i] = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
-  // every value batch goes out behind the keys: the online softmax consumes
-  // each batch's values right after its scores
+  // every value batch goes out behind the keys
 #pragma unroll
   for (int i = 0; i < NB; ++i) load_value_batch<3>(vc, tb[i], koff, vw[i]);
   const int vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
@@ -1187,28 +1187,18 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
   st.ks[lane] = ksl;
   wave_lds_fence();
 
+  // phase 1 (Table 2 A): every batch's keys decoded once, the scores of all
+  // kT tokens kept in registers; one max per token and head afterwards
   float m_run[kT], l_run[kT];
-  f32x4_t o_acc[kT][4];
+  f32x4_t sc[kT][NB];
 #pragma unroll
-  for (int t = 0; t < kT; ++t) {
-    m_run[t] = -INFINITY;
-    l_run[t] = 0.f;
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb) o_acc[t][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  }
-  const uint32_t slot_shift = (col >= 8) ? 16u : 0u;
+  for (int t = 0; t < kT; ++t) m_run[t] = -INFINITY;
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
     if (16 * i >= nvalid) break;
-    // this batch's value records to the stage, regrouped for the PV operand
-#pragma unroll
-    for (int j = 0; j < 3; ++j) st.rec[i][col * kRecStride + 3 * grp + j] = vw[i][j];
-    wave_lds_fence();
-    u32x4_t a[4], vb[4];
+    u32x4_t a[4];
     key_pairs<3>(lut, kw[i], a);
-    value_pairs<3>(lut, st.rec[i], grp, vdw, vsh, vb);
     const f32x4_t ks = st.ks[4 * i + grp];
-    const f32x4_t wv = st.vs[4 * i + grp];   // 0 past the last token's length
 #pragma unroll
     for (int t = 0; t < kT; ++t) {
       f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -1223,32 +1213,46 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
       f32x4_t x = acc * ks;
 #pragma unroll
       for (int r = 0; r < 4; ++r) x[r] = (16 * i + 4 * grp + r < nv[t]) ? x[r] : -INFINITY;
-      const float bm = wave_max(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
-      const float mnew = fmaxf(m_run[t], bm);
-      // rescale what this token accumulated so far to the new running max.
-      // c is the factor of this lane's head col % 8 (its sum l_run), but
-      // accumulator entry r of lane (u, gk) is a row of head (4 gk + r) % 8:
-      // the eight factors come from lanes 0..7 (head = lane there)
-      const float c = (m_run[t] == -INFINITY)
-                          ? 0.f
-                          : __builtin_amdgcn_exp2f((m_run[t] - mnew) * qdown[t]);
-      l_run[t] *= c;
-      float ch[kHeads];
+      sc[t][i] = x;
+      m_run[t] = fmaxf(fmaxf(m_run[t], fmaxf(x[0], x[1])), fmaxf(x[2], x[3]));
+    }
+  }
 #pragma unroll
-      for (int h = 0; h < kHeads; ++h)
-        ch[h] = __builtin_bit_cast(
-            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c), h));
-      f32x4_t crow;
+  for (int t = 0; t < kT; ++t) m_run[t] = wave_max(m_run[t]);
+
+  // phase 2 (Table 2 B, C): value records of all batches to the stage behind
+  // one fence, then per batch the decoded values feed every token's weights
 #pragma unroll
-      for (int r = 0; r < 4; ++r) crow[r] = (grp & 1) ? ch[4 + r] : ch[r];
+  for (int i = 0; i < NB; ++i) {
+    if (16 * i >= nvalid) break;
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) o_acc[t][nb] *= crow;
-      m_run[t] = mnew;
-      const float mq = (mnew == -INFINITY) ? 0.f : -mnew * qdown[t];
+    for (int j = 0; j < 3; ++j) st.rec[i][col * kRecStride + 3 * grp + j] = vw[i][j];
+  }
+  wave_lds_fence();
+  f32x4_t o_acc[kT][4];
+  float mq[kT];
+#pragma unroll
+  for (int t = 0; t < kT; ++t) {
+    l_run[t] = 0.f;
+    // a token with nothing to attend in this wave keeps m = -inf: its
+    // weights are exp2(-inf) = 0
+    mq[t] = (m_run[t] == -INFINITY) ? 0.f : -m_run[t] * qdown[t];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) o_acc[t][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
+  const uint32_t slot_shift = (col >= 8) ? 16u : 0u;
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    if (16 * i >= nvalid) break;
+    u32x4_t vb[4];
+    value_pairs<3>(lut, st.rec[i], grp, vdw, vsh, vb);
+    const f32x4_t wv = st.vs[4 * i + grp];   // 0 past the last token's length
+#pragma unroll
+    for (int t = 0; t < kT; ++t) {
       u32x4_t pw_hi, pw_lo;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(x[r], qdown[t], mq));
+        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][i][r], qdown[t], mq[t]));
         l_run[t] += e;
         const float pf = e * wv[r];
         const _Float16 ph = static_cast<_Float16>(pf);
