@@ -105,8 +105,8 @@ def parse():
 
 # sources of the decode step's kernels and their launch path: the counter
 # figures in profiles/ hold only while these are unchanged
-DECODE_SOURCES = ("iq_api.cpp", "iq_decode.hip", "iq_decode_g8.hip", "iq_device.h",
-                  "iq_internal.h")
+DECODE_SOURCES = ("iq_api.cpp", "iq_decode.hip", "iq_decode_g8.hip", "iq_g8_device.h",
+                  "iq_device.h", "iq_internal.h")
 
 
 def source_digest() -> str:

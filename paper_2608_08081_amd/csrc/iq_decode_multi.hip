@@ -1,0 +1,397 @@
+// Multi-token decode on the packed 3-bit cache for groups of 8 query heads
+// per KV head (App. A applied to each of 2-4 query tokens; Table 2 A-D),
+// gfx950: the verification step of speculative decoding, the tokens causal
+// among themselves.  Same split grid, loads, record decoding and merge as
+// the single-token kernel (iq_decode_g8.hip); see the kernel comment.
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include "iq_g8_device.h"
+
+namespace iq {
+namespace {
+
+// Multi-token decode (speculative verification): kT query tokens per
+// sequence over the same cache, token t attending positions before
+// seq - kT + 1 + t (causal among the new tokens, which the caller has
+// already compressed into the last kT positions).  Same grid, split plan,
+// loads and record decoding as decode_g8_kernel on 3-bit records: every
+// batch of keys and values is decoded once and feeds kT sets of matrix
+// instructions (the QK B operand of token t is read from LDS per batch).  The
+// softmax is two-phase as in decode_g8_kernel: all scores of every token
+// first (kept in registers), one max per token and head, then the weights
+// and values.  Partials per (split, token, head); the merge kernel takes the
+// token axis.
+template <int NB, bool kWide, int kT>
+__global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
+    const float* __restrict__ q, const uint8_t* __restrict__ k_codes,
+    const float* __restrict__ k_norms, const uint8_t* __restrict__ v_codes,
+    const float* __restrict__ v_norms, const int32_t* __restrict__ seq_lens,
+    const float* __restrict__ quats, float* __restrict__ partials, float* __restrict__ out,
+    int64_t capacity, int max_seq_len, int n_kv_heads, int n_splits, int split_len, float qscale,
+    Codebook cb) {
+  static_assert(kT >= 2 && kT <= 4, "2 to 4 tokens");
+  struct Smem {
+    uint32_t lut[64];
+    uint32_t qop[kT][2][kHeads][kQRowWords];
+    int qexp[kT][kHeads];
+    float wave_ml[kWaves][2][kHeads];
+    union {
+      WaveStage stage[kWaves];
+      f32x4_t wave_o[kWaves][4][64];
+    };
+  };
+  __shared__ __attribute__((aligned(16))) Smem sm;
+  uint32_t* lut = sm.lut;
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int split = blockIdx.x;
+  const int g = blockIdx.y;
+  const int b = blockIdx.z;
+  const int bg = b * n_kv_heads + g;
+  const int n_q_heads = n_kv_heads * kHeads;
+
+  // queries of the kT tokens (thread (head qh, block qblk) for tid < 256)
+  const int qh = (tid >> 5) & 7, qblk = tid & 31;
+  f32x4_t qv[kT];
+#pragma unroll
+  for (int t = 0; t < kT; ++t)
+    qv[t] = *reinterpret_cast<const f32x4_t*>(
+        q + ((static_cast<int64_t>(b) * kT + t) * n_q_heads + static_cast<int64_t>(g) * kHeads +
+             qh) * kDim + 4 * qblk);
+  const f32x4_t* qpar = reinterpret_cast<const f32x4_t*>(
+      quats + static_cast<int64_t>(g) * kQuatFloats + 8 * qblk);
+  const f32x4_t ql = qpar[0], qr = qpar[1];
+  float* part_bg = partials + static_cast<int64_t>(bg) * n_splits * kT * (kHeads * kPart);
+  const int64_t row = static_cast<int64_t>(bg) * capacity;
+  const uint8_t* kc = k_codes + row * kRecordBytes;
+  const uint8_t* vc = v_codes + row * kRecordBytes;
+
+  // this wave's run of batches (as in decode_g8_kernel)
+  const int start = split * split_len;
+  const int nbat = split_len >> 4;
+  const int nb_base = nbat / kWaves, nb_rem = nbat % kWaves;
+  const int nb_w = nb_base + (wave < nb_rem ? 1 : 0);
+  const int wbase = start + 16 * (wave * nb_base + (wave < nb_rem ? wave : nb_rem));
+  int seq0 = 0;
+  int lim = start + split_len < max_seq_len ? start + split_len : max_seq_len;
+  auto last_batch = [&](int l) {
+    int c = (l > 0 ? l - 1 : 0) & ~15;
+    c = c < wbase + 16 * (nb_w - 1) ? c : wbase + 16 * (nb_w - 1);
+    return c > 0 ? c : 0;
+  };
+  int clamp16 = last_batch(lim);
+  if constexpr (kWide) {
+    seq0 = seq_lens[b];
+    const int seq_w = seq0 < 0 ? 0 : (seq0 > max_seq_len ? max_seq_len : seq0);
+    if (start >= seq_w) {
+      // nothing to attend for any token
+      if (n_splits > 1) {
+        if (tid < kT * kHeads)
+          part_bg[(static_cast<int64_t>(split) * kT + tid / kHeads) * (kHeads * kPart) +
+                  (tid % kHeads) * kPart] = -INFINITY;
+      } else {
+        for (int e = tid; e < kT * kHeads * kDim; e += kThreads) {
+          const int t = e / (kHeads * kDim), r = e % (kHeads * kDim);
+          out[((static_cast<int64_t>(b) * kT + t) * n_q_heads +
+               static_cast<int64_t>(g) * kHeads) * kDim + r] = 0.f;
+        }
+      }
+      return;
+    }
+    lim = lim < seq_w ? lim : seq_w;
+    clamp16 = last_batch(lim);
+  }
+  const float* kn = k_norms + row;
+  const float* vn = v_norms + row;
+  int64_t dlt[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) dlt[i] = 0;
+  uint32_t kw[NB][3], vw[NB][3];
+  f32x4_t ksl, vsl;
+  load_keys<NB, false, 3>(kc, kn, vn, dlt, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
+  const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
+  int tb[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) tb[i] = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
+  // every value batch goes out behind the keys
+#pragma unroll
+  for (int i = 0; i < NB; ++i) load_value_batch<3>(vc, tb[i], koff, vw[i]);
+  const int vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
+  const uint32_t vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));
+
+  if constexpr (!kWide) seq0 = seq_lens[b];
+  const int seq = seq0 < 0 ? 0 : (seq0 > max_seq_len ? max_seq_len : seq0);
+  // positions of this wave each token attends (may be <= 0)
+  int nv[kT];
+#pragma unroll
+  for (int t = 0; t < kT; ++t) {
+    int st = seq - (kT - 1 - t);
+    st = st > 0 ? st : 0;
+    const int end = st < start + split_len ? st : start + split_len;
+    int n = end - wbase;
+    nv[t] = n < 16 * nb_w ? n : 16 * nb_w;
+  }
+  const int nvalid = nv[kT - 1];
+
+  // ---- while the loads fly: LUT and the rotated queries --------------------
+  if (tid < 64) {
+    const uint32_t lo =
+        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & 7)));
+    const uint32_t hi =
+        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> 3)));
+    lut[tid] = lo | (hi << 16);
+  }
+  if (tid < kRotThreads) {
+#pragma unroll
+    for (int t = 0; t < kT; ++t) {
+      const f32x4_t y = rotate_forward(qv[t], ql, qr, qblk, kInvSqrtDim * qscale);
+      int qexp = 0;
+      const float am = group32_max(
+          fmaxf(fmaxf(fabsf(y[0]), fabsf(y[1])), fmaxf(fabsf(y[2]), fabsf(y[3]))));
+      if (am > 0.f) {
+        int e = 0;
+        frexpf(am, &e);
+        qexp = 14 - e;
+        qexp = qexp > 100 ? 100 : (qexp < -100 ? -100 : qexp);
+      }
+      const float qup = ldexpf(1.0f, qexp);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const float x0 = y[2 * j] * qup, x1 = y[2 * j + 1] * qup;
+        const _Float16 h0 = static_cast<_Float16>(x0), h1 = static_cast<_Float16>(x1);
+        const _Float16 l0 = static_cast<_Float16>(x0 - static_cast<float>(h0));
+        const _Float16 l1 = static_cast<_Float16>(x1 - static_cast<float>(h1));
+        sm.qop[t][0][qh][2 * qblk + j] =
+            static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h0)) |
+            (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h1)) << 16);
+        sm.qop[t][1][qh][2 * qblk + j] =
+            static_cast<uint32_t>(__builtin_bit_cast(uint16_t, l0)) |
+            (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, l1)) << 16);
+      }
+      if (qblk == 0) sm.qexp[t][qh] = qexp;
+    }
+  }
+  lds_barrier();   // lut, qop, qexp
+  float qdown[kT];
+#pragma unroll
+  for (int t = 0; t < kT; ++t) qdown[t] = ldexpf(1.0f, -sm.qexp[t][col & 7]);
+  // scales to the wave's stage; value scales past the last token's length
+  // are 0 and the rest are brought to [0, 2^15] by the wave's largest
+  WaveStage& st = sm.stage[wave];
+  float vmax;
+  {
+    f32x4_t v = vsl;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[r] = (4 * lane + r < nvalid) ? v[r] : 0.f;
+    vmax = wave64_max(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+    const float vinv = vmax > 0.f ? 32768.0f * __builtin_amdgcn_rcpf(vmax) : 0.f;
+    st.vs[lane] = v * vinv;
+  }
+  st.ks[lane] = ksl;
+  wave_lds_fence();
+
+  // phase 1 (Table 2 A): every batch's keys decoded once, the scores of all
+  // kT tokens kept in registers; one max per token and head afterwards
+  float m_run[kT], l_run[kT];
+  f32x4_t sc[kT][NB];
+#pragma unroll
+  for (int t = 0; t < kT; ++t) m_run[t] = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    if (16 * i >= nvalid) break;
+    u32x4_t a[4];
+    key_pairs<3>(lut, kw[i], a);
+    const f32x4_t ks = st.ks[4 * i + grp];
+#pragma unroll
+    for (int t = 0; t < kT; ++t) {
+      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const u32x4_t qb =
+            *reinterpret_cast<const u32x4_t*>(&sm.qop[t][col >> 3][col & 7][16 * grp + 4 * kb]);
+        acc = mfma(a[kb], qb, acc);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[r] += xor_lane<8>(acc[r]);
+      f32x4_t x = acc * ks;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) x[r] = (16 * i + 4 * grp + r < nv[t]) ? x[r] : -INFINITY;
+      sc[t][i] = x;
+      m_run[t] = fmaxf(fmaxf(m_run[t], fmaxf(x[0], x[1])), fmaxf(x[2], x[3]));
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < kT; ++t) m_run[t] = wave_max(m_run[t]);
+
+  // phase 2 (Table 2 B, C): value records of all batches to the stage behind
+  // one fence, then per batch the decoded values feed every token's weights
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    if (16 * i >= nvalid) break;
+#pragma unroll
+    for (int j = 0; j < 3; ++j) st.rec[i][col * kRecStride + 3 * grp + j] = vw[i][j];
+  }
+  wave_lds_fence();
+  f32x4_t o_acc[kT][4];
+  float mq[kT];
+#pragma unroll
+  for (int t = 0; t < kT; ++t) {
+    l_run[t] = 0.f;
+    // a token with nothing to attend in this wave keeps m = -inf: its
+    // weights are exp2(-inf) = 0
+    mq[t] = (m_run[t] == -INFINITY) ? 0.f : -m_run[t] * qdown[t];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) o_acc[t][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
+  const uint32_t slot_shift = (col >= 8) ? 16u : 0u;
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    if (16 * i >= nvalid) break;
+    u32x4_t vb[4];
+    value_pairs<3>(lut, st.rec[i], grp, vdw, vsh, vb);
+    const f32x4_t wv = st.vs[4 * i + grp];   // 0 past the last token's length
+#pragma unroll
+    for (int t = 0; t < kT; ++t) {
+      u32x4_t pw_hi, pw_lo;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][i][r], qdown[t], mq[t]));
+        l_run[t] += e;
+        const float pf = e * wv[r];
+        const _Float16 ph = static_cast<_Float16>(pf);
+        const _Float16 pl = static_cast<_Float16>(pf - static_cast<float>(ph));
+        pw_hi[r] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, ph)) << slot_shift;
+        pw_lo[r] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, pl)) << slot_shift;
+      }
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        o_acc[t][nb] = mfma(pw_hi, vb[nb], o_acc[t][nb]);
+        o_acc[t][nb] = mfma(pw_lo, vb[nb], o_acc[t][nb]);
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < kT; ++t) {
+    l_run[t] = wave_sum(l_run[t]);
+    m_run[t] *= qdown[t];   // log2 units
+  }
+
+  // ---- per token: merge the 8 waves in LDS, then the partial or the row ----
+  const float oscale = vmax * (1.0f / 32768.0f);
+  const int mh = qh, md = 4 * qblk;
+  const int o_r = mh & 3, o_lane = (md >> 3) + 16 * ((mh >> 2) & 1), o_nb = (md & 7) >> 1;
+#pragma unroll
+  for (int t = 0; t < kT; ++t) {
+    lds_barrier();   // the stage (t = 0) or the previous token's wave_o is done
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      sm.wave_o[wave][r][lane] =
+          f32x4_t{o_acc[t][0][r], o_acc[t][1][r], o_acc[t][2][r], o_acc[t][3][r]} * oscale;
+    if (lane < kHeads) {
+      sm.wave_ml[wave][0][lane] = m_run[t];
+      sm.wave_ml[wave][1][lane] = l_run[t];
+    }
+    lds_barrier();
+    if (tid < kRotThreads) {
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm.wave_ml[w][0][mh]);
+      float L = 0.f;
+      f32x4_t O = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const float mw = sm.wave_ml[w][0][mh];
+        const float c = (mw == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mw - M);
+        L += c * sm.wave_ml[w][1][mh];
+        const f32x2_t s0 = *reinterpret_cast<const f32x2_t*>(
+            reinterpret_cast<const float*>(&sm.wave_o[w][o_r][o_lane]) + o_nb);
+        const f32x2_t s1 = *reinterpret_cast<const f32x2_t*>(
+            reinterpret_cast<const float*>(&sm.wave_o[w][o_r][o_lane + 32]) + o_nb);
+        O += c * f32x4_t{s0[0], s1[0], s0[1], s1[1]};
+      }
+      if (n_splits == 1) {
+        const f32x4_t o = L > 0.f ? rotate_inverse(O * (1.0f / L), ql, qr, qblk)
+                                  : f32x4_t{0.f, 0.f, 0.f, 0.f};
+        *reinterpret_cast<f32x4_t*>(
+            out + ((static_cast<int64_t>(b) * kT + t) * n_q_heads +
+                   static_cast<int64_t>(g) * kHeads + mh) * kDim + md) = o;
+      } else {
+        float* pp = part_bg + (static_cast<int64_t>(split) * kT + t) * (kHeads * kPart) +
+                    mh * kPart;
+        if (qblk == 0) {
+          pp[0] = M;
+          pp[1] = L;
+        }
+        *reinterpret_cast<f32x4_t*>(pp + 2 + md) = O;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_decode_g8_multi(int nb, int64_t n_splits, int64_t split_len, int n_tok,
+                                  const float* q, const uint8_t* k_codes, const float* k_norms,
+                                  const uint8_t* v_codes, const float* v_norms,
+                                  const int32_t* seq_lens, int64_t capacity,
+                                  int64_t max_seq_len, const float* quats, int64_t batch,
+                                  int64_t n_kv_heads, float scale, float* out, float* partials,
+                                  hipStream_t stream) {
+  if (n_tok < 2 || n_tok > 4) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(n_splits), static_cast<unsigned>(n_kv_heads),
+                  static_cast<unsigned>(batch)),
+      block(kThreads);
+  constexpr int64_t kCus = 256;
+  const bool wide = n_splits * n_kv_heads * batch > kCus;
+  const size_t lds_pad = wide ? 0 : kOneWorkgroupPadBytes;
+  const float qscale = scale * kLog2e;
+  const Codebook& cb = codebook();
+#define IQ_LAUNCH_MT(NB_, WIDE_, T_)                                                            \
+  hipLaunchKernelGGL((decode_g8_multi_kernel<NB_, WIDE_, T_>), grid, block, lds_pad, stream, q, \
+                     k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials, out,        \
+                     capacity, static_cast<int>(max_seq_len), static_cast<int>(n_kv_heads),     \
+                     static_cast<int>(n_splits), static_cast<int>(split_len), qscale, cb)
+#define IQ_LAUNCH_MT_W(NB_, T_)       \
+  if (wide) {                         \
+    IQ_LAUNCH_MT(NB_, true, T_);      \
+  } else {                            \
+    IQ_LAUNCH_MT(NB_, false, T_);     \
+  }
+#define IQ_LAUNCH_MT_NB(T_)                   \
+  switch (nb) {                               \
+    case 1: IQ_LAUNCH_MT_W(1, T_) break;       \
+    case 2: IQ_LAUNCH_MT_W(2, T_) break;       \
+    case 3: IQ_LAUNCH_MT_W(3, T_) break;       \
+    case 4: IQ_LAUNCH_MT_W(4, T_) break;       \
+    default: IQ_LAUNCH_MT_W(5, T_) break;      \
+  }
+  if (n_tok == 2) {
+    IQ_LAUNCH_MT_NB(2)
+  } else if (n_tok == 3) {
+    IQ_LAUNCH_MT_NB(3)
+  } else {
+    IQ_LAUNCH_MT_NB(4)
+  }
+#undef IQ_LAUNCH_MT_NB
+#undef IQ_LAUNCH_MT_W
+#undef IQ_LAUNCH_MT
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || n_splits == 1) return e;
+  const dim3 mgrid(static_cast<unsigned>(n_kv_heads * kHeads),
+                   static_cast<unsigned>(batch * n_tok));
+#define IQ_LAUNCH_MT_MERGE(T_)                                                                 \
+  hipLaunchKernelGGL((merge_g8_kernel<false, T_>), mgrid, dim3(kMergeThreads), 0, stream,       \
+                     partials, quats, out, static_cast<int>(n_kv_heads),                        \
+                     static_cast<int>(n_splits), nullptr, capacity)
+  if (n_tok == 2) IQ_LAUNCH_MT_MERGE(2);
+  else if (n_tok == 3) IQ_LAUNCH_MT_MERGE(3);
+  else IQ_LAUNCH_MT_MERGE(4);
+#undef IQ_LAUNCH_MT_MERGE
+  return hipGetLastError();
+}
+
+}  // namespace iq

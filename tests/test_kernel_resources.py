@@ -45,7 +45,7 @@ def _kernels(asm):
 
 def test_decode_g8_occupancy_budget(tmp_path):
     asm = _device_asm("iq_decode_g8.hip", tmp_path)
-    src = open(os.path.join(B.CSRC, "iq_decode_g8.hip")).read()
+    src = open(os.path.join(B.CSRC, "iq_g8_device.h")).read()
     pad = eval(re.search(r"kOneWorkgroupPadBytes\s*=\s*([^;]+);", src).group(1))
     ks = _kernels(asm)
     dec = {n: v for n, v in ks.items() if "decode_g8_kernel" in n}
@@ -79,8 +79,8 @@ def test_multi_token_kernel_budget(tmp_path):
     """Multi-token decode instances (NB 1..5 x grid kind x 2..4 tokens): no
     scratch, at most 256 VGPRs (one workgroup per CU when above 128), and
     the one-round instances' LDS with the padding within a CU."""
-    asm = _device_asm("iq_decode_g8.hip", tmp_path)
-    src = open(os.path.join(B.CSRC, "iq_decode_g8.hip")).read()
+    asm = _device_asm("iq_decode_multi.hip", tmp_path)
+    src = open(os.path.join(B.CSRC, "iq_g8_device.h")).read()
     pad = eval(re.search(r"kOneWorkgroupPadBytes\s*=\s*([^;]+);", src).group(1))
     ks = _kernels(asm)
     mt = {n: v for n, v in ks.items() if "decode_g8_multi_kernel" in n}
