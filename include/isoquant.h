@@ -417,7 +417,8 @@ iq_status iq_decode_attention_f16(const float* q, const void* k, const void* v,
  * b = 4), code i at bits b*i .. b*i+b-1 of the little-endian bit string,
  * scales and every other layout and argument as for the 3-bit entry points.
  * b = 3 gives exactly the results of iq_codebook / iq_compress_kv /
- * iq_decode_attention.  Any other b returns IQ_ERR_UNSUPPORTED.
+ * iq_decode_attention / iq_decode_step.  Any other b returns
+ * IQ_ERR_UNSUPPORTED.
  */
 
 /* C_b: levels[2^b] and thresholds[2^b - 1] (host memory, either may be
@@ -448,6 +449,19 @@ iq_status iq_decode_attention_bits(const float* q,
                                    int64_t head_dim, float softmax_scale, float* out,
                                    void* workspace, size_t workspace_bytes, int bits,
                                    hipStream_t stream);
+
+/* iq_decode_step on b-bit records: the new key and value are compressed at
+ * b bits into position seq_lens[b] (Algorithm 1 with C_b), then attended
+ * with the cache; requirements as for iq_decode_attention_bits, status and
+ * length advance as for iq_decode_step. */
+iq_status iq_decode_step_bits(const float* q, const void* k_new, const void* v_new,
+                              iq_dtype dtype, uint8_t* k_codes, float* k_norms,
+                              uint8_t* v_codes, float* v_norms, int32_t* seq_lens,
+                              int64_t capacity, int64_t max_seq_len, const float* quats,
+                              int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                              int64_t head_dim, float softmax_scale, float* out, void* workspace,
+                              size_t workspace_bytes, int32_t* status_dev, int bits,
+                              hipStream_t stream);
 
 /*
  * Multi-token decode (the verification step of speculative decoding)

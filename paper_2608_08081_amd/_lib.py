@@ -51,6 +51,9 @@ _SIGNATURES = {
                                       _c_i64, _c_i64, _c_float, _vp, _vp, _c_size, _vp, _vp]),
     "iq_so4_to_quaternions": (_c_int, [_vp, _vp]),
     "iq_codebook_bits": (_c_int, [_c_int, _vp, _vp]),
+    "iq_decode_step_bits": (_c_int, [_vp, _vp, _vp, _c_int, _vp, _vp, _vp, _vp, _vp, _c_i64,
+                                     _c_i64, _vp, _c_i64, _c_i64, _c_i64, _c_i64, _c_float, _vp,
+                                     _vp, _c_size, _vp, _c_int, _vp]),
     "iq_decode_multi_workspace_bytes": (_c_size, [_c_i64, _c_i64, _c_i64, _c_i64, _c_i64,
                                                   _c_i64]),
     "iq_decode_attention_multi": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp,

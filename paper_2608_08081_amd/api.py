@@ -344,6 +344,20 @@ def iq_decode_step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens
     """Fused decode step: append (k_new, v_new) [B][H_kv][128] at position
     seq_lens[b], attend q [B][H_q][128] over the advanced lengths and advance
     seq_lens in place.  Returns out [B][H_q][128] fp32 (original space)."""
+    return _step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out,
+                 workspace, max_seq_len, softmax_scale, status, 3)
+
+
+def iq_decode_step_bits(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats,
+                        out=None, workspace=None, max_seq_len=None, softmax_scale: float = 0.0,
+                        status=None, bits: int = 3):
+    """iq_decode_step on b-bit records ([B][H_kv][cap][16 b])."""
+    return _step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out,
+                 workspace, max_seq_len, softmax_scale, status, bits)
+
+
+def _step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out, workspace,
+          max_seq_len, softmax_scale, status, bits):
     if q.dim() != 3 or q.shape[-1] != HEAD_DIM:
         raise ValueError("q must be [batch][n_q_heads][128]")
     b, hq, _ = q.shape
@@ -354,8 +368,8 @@ def iq_decode_step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens
     _, hkv, cap, _ = k_codes.shape
     _require(k_new, "k_new", k_new.dtype, (b, hkv, HEAD_DIM), dev)
     _require(v_new, "v_new", k_new.dtype, (b, hkv, HEAD_DIM), dev)
-    _require(k_codes, "k_codes", torch.uint8, (b, hkv, cap, RECORD_BYTES), dev)
-    _require(v_codes, "v_codes", torch.uint8, (b, hkv, cap, RECORD_BYTES), dev)
+    _require(k_codes, "k_codes", torch.uint8, (b, hkv, cap, record_bytes(bits)), dev)
+    _require(v_codes, "v_codes", torch.uint8, (b, hkv, cap, record_bytes(bits)), dev)
     _require(k_norms, "k_norms", torch.float32, (b, hkv, cap), dev)
     _require(v_norms, "v_norms", torch.float32, (b, hkv, cap), dev)
     _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
@@ -371,12 +385,15 @@ def iq_decode_step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens
         workspace = alloc_workspace(b, hq, hkv, max_seq_len, dev)
     if workspace.dtype != torch.uint8 or workspace.device != dev or not workspace.is_contiguous():
         raise ValueError("workspace must be a contiguous uint8 device tensor")
-    st = _lib.lib().iq_decode_step(
-        _ptr(q), _ptr(k_new), _ptr(v_new), _dtype_code(k_new), _ptr(k_codes), _ptr(k_norms),
-        _ptr(v_codes), _ptr(v_norms), _ptr(seq_lens), cap, max_seq_len, _ptr(quats), b, hq,
-        hkv, HEAD_DIM, float(softmax_scale), _ptr(out), _ptr(workspace), workspace.numel(),
-        _ptr(status), _stream(dev))
-    _lib.check("iq_decode_step", st)
+    args = (_ptr(q), _ptr(k_new), _ptr(v_new), _dtype_code(k_new), _ptr(k_codes), _ptr(k_norms),
+            _ptr(v_codes), _ptr(v_norms), _ptr(seq_lens), cap, max_seq_len, _ptr(quats), b, hq,
+            hkv, HEAD_DIM, float(softmax_scale), _ptr(out), _ptr(workspace), workspace.numel(),
+            _ptr(status))
+    if bits == 3:
+        _lib.check("iq_decode_step", _lib.lib().iq_decode_step(*args, _stream(dev)))
+    else:
+        _lib.check("iq_decode_step_bits",
+                   _lib.lib().iq_decode_step_bits(*args, bits, _stream(dev)))
     return out
 
 

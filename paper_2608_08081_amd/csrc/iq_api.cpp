@@ -475,6 +475,46 @@ iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, i
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 
+iq_status iq_decode_step_bits(const float* q, const void* k_new, const void* v_new,
+                              iq_dtype dtype, uint8_t* k_codes, float* k_norms,
+                              uint8_t* v_codes, float* v_norms, int32_t* seq_lens,
+                              int64_t capacity, int64_t max_seq_len, const float* quats,
+                              int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                              int64_t head_dim, float softmax_scale, float* out, void* workspace,
+                              size_t workspace_bytes, int32_t* status_dev, int bits,
+                              hipStream_t stream) {
+  if (bits == 3)
+    return iq_decode_step(q, k_new, v_new, dtype, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                          capacity, max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
+                          softmax_scale, out, workspace, workspace_bytes, status_dev, stream);
+  if (bits != 2 && bits != 4) return IQ_ERR_UNSUPPORTED;
+  if (dtype != IQ_DTYPE_F32 && dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
+  iq::DecodePlan plan;
+  const iq_status st = check_decode_args(q, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                                         capacity, max_seq_len, quats, batch, n_q_heads,
+                                         n_kv_heads, head_dim, out, workspace, workspace_bytes,
+                                         &plan);
+  if (st != IQ_OK) return st;
+  if (max_seq_len < 1 || n_kv_heads > 512) return IQ_ERR_INVALID_ARGUMENT;
+  if (!k_new || !v_new || !iq::aligned(k_new, 16) || !iq::aligned(v_new, 16) ||
+      (status_dev && !iq::aligned(status_dev, 4)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  // the matrix-core path only, as for iq_decode_attention_bits
+  if (n_q_heads != 8 * n_kv_heads || plan.g8_batches <= 0) return IQ_ERR_UNSUPPORTED;
+  if (capacity % 16 || capacity < 16 || capacity * 16 * bits > 0x7fffffff ||
+      !iq::aligned(k_norms, 16) || !iq::aligned(v_norms, 16) || batch > 65535 ||
+      n_kv_heads > 65535)
+    return IQ_ERR_UNSUPPORTED;
+  if (batch == 0) return IQ_OK;
+  const iq::StepAppend append{k_new, v_new, dtype == IQ_DTYPE_F16 ? 1 : 0, status_dev};
+  float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
+  const hipError_t e = iq::launch_decode_g8(
+      plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes, k_norms, v_codes, v_norms,
+      seq_lens, capacity, max_seq_len, quats, batch, n_kv_heads, resolve_scale(softmax_scale),
+      out, parts, &append, nullptr, bits, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
 // ---------------------------------------------------------------------------
 // Paged cache (page pools + per-sequence page tables)
 // ---------------------------------------------------------------------------

@@ -199,8 +199,8 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][kBits],
 // new token's slot are located through the page table.
 //
 // kBits: the records' code width, 3 (the paper's cache) or 2 / 4 (Algorithm
-// 1 with C_2 / C_4: records of 32 / 64 bytes).  The fused step and paged
-// pools run on 3-bit records only.
+// 1 with C_2 / C_4: records of 32 / 64 bytes).  Paged pools hold 3-bit
+// records only.
 template <int NB, bool kAppend, bool kWide, bool kPaged, int kBits>
 __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     const float* __restrict__ q, uint8_t* __restrict__ k_codes, float* __restrict__ k_norms,
@@ -210,7 +210,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     int n_kv_heads, int n_splits, int split_len, float qscale, CodebookB<kBits> cb,
     const void* __restrict__ k_new, const void* __restrict__ v_new, int new_f16,
     int32_t* __restrict__ status, PageTable pages) {
-  static_assert(kBits == 3 || (!kAppend && !kPaged), "fused step and pages: 3-bit records");
+  static_assert(kBits == 3 || !kPaged, "paged pools hold 3-bit records");
   constexpr int kRB = record_bytes<kBits>();
   constexpr int kLut = 1 << (2 * kBits);   // pairs of codes
   // All LDS of the kernel in one object, the pair table first (address 0:
@@ -220,7 +220,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     uint32_t qop[2][kHeads][kQRowWords];
     int qexp[kHeads];
     float wave_ml[kWaves][2][kHeads];
-    uint32_t new_rec[2][kRecordWords];   // append workgroup: the new key / value record
+    uint32_t new_rec[2][4 * kBits];   // append workgroup: the new key / value record
     float new_scale[2];
     // the waves' staging areas while attending, their outputs afterwards
     // (wave_o[w][r][lane] = the lane's accumulator entries r of the four
@@ -298,9 +298,9 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
           quats + static_cast<int64_t>(g) * kQuatFloats + 8 * (lane >> 1));
       const f32x4_t p0 = qs[0], p1 = qs[1];
       const float qp[8] = {p0[0], p0[1], p0[2], p0[3], p1[0], p1[1], p1[2], p1[3]};
-      const WaveCode wc = compress_vector_wave(x0, x1, qp, cb, lane);
+      const WaveCode wc = compress_vector_wave<kBits>(x0, x1, qp, cb, lane);
       const int which = wave - 4;
-      if (lane < kRecordWords) sm.new_rec[which][lane] = wc.word;
+      if (lane < 4 * kBits) sm.new_rec[which][lane] = wc.word;
       if (lane == 0) sm.new_scale[which] = wc.scale;
       // record index of the new token (its page's slot, or the row position)
       const int64_t rec =
@@ -308,16 +308,16 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
       if (rec >= 0) {
         uint8_t* codes = which == 0 ? k_codes : v_codes;
         float* norms = which == 0 ? k_norms : v_norms;
-        if (lane < kRecordWords)
-          reinterpret_cast<uint32_t*>(codes + rec * kRecordBytes)[lane] = wc.word;
+        if (lane < 4 * kBits) reinterpret_cast<uint32_t*>(codes + rec * kRB)[lane] = wc.word;
         if (lane == 0) norms[rec] = wc.scale;
       }
     }
-    if (tid < 64) {
+    if (tid < kLut) {
+      constexpr int kMask = (1 << kBits) - 1;
       const uint32_t lo =
-          __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & 7)));
+          __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & kMask)));
       const uint32_t hi =
-          __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> 3)));
+          __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> kBits)));
       lut[tid] = lo | (hi << 16);
     }
     f32x4_t y = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -328,8 +328,8 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     // thread's dims 4 qblk .. +3, summed over the head's 32 lanes (y already
     // carries the score scale, in log2 units)
     const int md = 4 * qblk;
-    const f32x4_t k4 = decode_record_dims(sm.new_rec[0], lut, md);
-    const f32x4_t v4 = decode_record_dims(sm.new_rec[1], lut, md);
+    const f32x4_t k4 = decode_record_dims<kBits>(sm.new_rec[0], lut, md);
+    const f32x4_t v4 = decode_record_dims<kBits>(sm.new_rec[1], lut, md);
     float dot = y[0] * k4[0] + y[1] * k4[1] + y[2] * k4[2] + y[3] * k4[3];
     dot += xor_lane<1>(dot);
     dot += xor_lane<2>(dot);
@@ -632,7 +632,7 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                             const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
                             float* out, float* partials, const StepAppend* append,
                             const PageTable* pages, int bits, hipStream_t stream) {
-  if (bits != 3 && (append || pages)) return hipErrorInvalidValue;
+  if (bits != 3 && pages) return hipErrorInvalidValue;
   // partials per (sequence, KV head): the splits, and the fused step's new
   // token
   const int64_t n_parts = append ? n_splits + 1 : n_splits;
@@ -663,12 +663,12 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
 #define IQ_LAUNCH_G8_W(NB_, APP_, WIDE_)                \
   if (pages) {                                          \
     IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, true, 3);        \
-  } else if (APP_ || bits == 3) {                       \
-    IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, false, 3);       \
   } else if (bits == 2) {                               \
-    IQ_LAUNCH_G8_WPB(NB_, false, WIDE_, false, 2);      \
+    IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, false, 2);       \
+  } else if (bits == 4) {                               \
+    IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, false, 4);       \
   } else {                                              \
-    IQ_LAUNCH_G8_WPB(NB_, false, WIDE_, false, 4);      \
+    IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, false, 3);       \
   }
 #define IQ_LAUNCH_G8(NB_, APP_)          \
   if (wide) {                            \

@@ -157,7 +157,7 @@ __device__ __forceinline__ void load_pair(const __half* src, int lane, float& a,
 }
 
 struct WaveCode {
-  uint32_t word;   // record word `lane` (meaningful in lanes 0..11)
+  uint32_t word;   // record word `lane` (meaningful in lanes 0 .. 4b - 1)
   float scale;     // s = ||x||_2
 };
 
@@ -169,10 +169,13 @@ struct WaveCode {
 //           the partner lane l ^ (st/2)), then the SO(4) block of the lane
 //           pair (2 blk, 2 blk + 1).
 //   Step 3: codes against the thresholds scaled by s sqrt(128).
-//   Step 4: lane w < 12 gathers the (at most 7) 6-bit fields overlapping
-//           record word w.
+//   Step 4: lane w < 4b gathers the 2b-bit fields (the lanes' code pairs)
+//           overlapping record word w (at most 7 at b = 3, where fields
+//           straddle words; 8 or 4 whole fields at b = 2 or 4).
+template <int kBits>
 __device__ __forceinline__ WaveCode compress_vector_wave(float x0, float x1, const float* qp,
-                                                        const Codebook& cb, int lane) {
+                                                        const CodebookB<kBits>& cb, int lane) {
+  constexpr int kThr = (1 << kBits) - 1;
   double ss = static_cast<double>(x0) * static_cast<double>(x0) +
               static_cast<double>(x1) * static_cast<double>(x1);
   ss += xor_lane64_f64<1>(ss);
@@ -199,24 +202,39 @@ __device__ __forceinline__ WaveCode compress_vector_wave(float x0, float x1, con
   const int r0 = odd ? 2 : 0;
   const float y0 = m[r0][0] * z0 + m[r0][1] * z1 + m[r0][2] * z2 + m[r0][3] * z3;
   const float y1 = m[r0 + 1][0] * z0 + m[r0 + 1][1] * z1 + m[r0 + 1][2] * z2 + m[r0 + 1][3] * z3;
-  float thr[7];
+  float thr[kThr];
   if (ss > 0.0) {
     const double sc = s * 11.313708498984760390;   // s sqrt(128)
 #pragma unroll
-    for (int j = 0; j < 7; ++j) thr[j] = static_cast<float>(static_cast<double>(cb.thr[j]) * sc);
+    for (int j = 0; j < kThr; ++j)
+      thr[j] = static_cast<float>(static_cast<double>(cb.thr[j]) * sc);
   } else {
 #pragma unroll
-    for (int j = 0; j < 7; ++j) thr[j] = cb.thr[j];
+    for (int j = 0; j < kThr; ++j) thr[j] = cb.thr[j];
   }
-  const uint32_t fld = quantize3(y0, thr) | (quantize3(y1, thr) << 3);
-  const int w = lane < kRecordWords ? lane : 0;
-  const int f_lo = (32 * w) / 6;
+  uint32_t fld;
+  if constexpr (kBits == 3) {
+    fld = quantize3(y0, thr) | (quantize3(y1, thr) << 3);
+  } else {
+    // #{j : t_j <= y} as a plain count (ties upward, NaN gives 0)
+    uint32_t c0 = 0u, c1 = 0u;
+#pragma unroll
+    for (int j = 0; j < kThr; ++j) {
+      c0 += y0 >= thr[j] ? 1u : 0u;
+      c1 += y1 >= thr[j] ? 1u : 0u;
+    }
+    fld = c0 | (c1 << kBits);
+  }
+  constexpr int kFw = 2 * kBits;              // field width (a lane's pair)
+  constexpr int kFields = 32 / kFw + 2;        // fields overlapping a word
+  const int w = lane < 4 * kBits ? lane : 0;
+  const int f_lo = (32 * w) / kFw;
   uint32_t word = 0u;
 #pragma unroll
-  for (int k = 0; k < 7; ++k) {
+  for (int k = 0; k < kFields; ++k) {
     const int f = f_lo + k;
     const uint32_t v = static_cast<uint32_t>(__shfl(static_cast<int>(fld), f & 63));
-    const int sh = 6 * f - 32 * w;
+    const int sh = kFw * f - 32 * w;
     if (f < 64 && sh < 32) word |= sh >= 0 ? (v << sh) : (v >> (-sh));
   }
   return WaveCode{word, static_cast<float>(s)};

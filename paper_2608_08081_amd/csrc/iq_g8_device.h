@@ -245,15 +245,17 @@ __device__ __forceinline__ f32x4_t rotate_inverse(f32x4_t o, f32x4_t ql, f32x4_t
 }
 
 // Codebook values of dims d..d+3 (d % 4 == 0) of a packed record held in
-// LDS (12 words): codes at bits 3d .. 3d+11, two 6-bit fields looked up in
-// the fp16 pair table.
+// LDS (4b words): codes at bits b d .. b d + 4b - 1, two 2b-bit fields looked
+// up in the fp16 pair table.
+template <int kBits = 3>
 __device__ __forceinline__ f32x4_t decode_record_dims(const uint32_t* rec, const uint32_t* lut,
                                                       int d) {
-  const int bit = 3 * d, w = bit >> 5, off = bit & 31;
+  constexpr uint32_t kMask = (1u << (2 * kBits)) - 1;
+  const int bit = kBits * d, w = bit >> 5, off = bit & 31;
   const uint32_t lo = rec[w];
-  const uint32_t hi = w + 1 < kRecordWords ? rec[w + 1] : 0u;
+  const uint32_t hi = w + 1 < 4 * kBits ? rec[w + 1] : 0u;
   const uint32_t bits = __builtin_amdgcn_alignbit(hi, lo, off);
-  const uint32_t p0 = lut[bits & 63u], p1 = lut[(bits >> 6) & 63u];
+  const uint32_t p0 = lut[bits & kMask], p1 = lut[(bits >> (2 * kBits)) & kMask];
   return f32x4_t{static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p0))),
                  static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p0 >> 16))),
                  static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(p1))),

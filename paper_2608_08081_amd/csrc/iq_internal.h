@@ -128,7 +128,7 @@ void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
              int64_t* n_splits, int64_t* split_len);
 // pages: null for a contiguous cache ([B][H_kv][capacity] records), else
 // the page table (capacity is then max_pages * page_size).  bits: the
-// records' code width (2, 3 or 4; the fused step and pages need 3).
+// records' code width (2, 3 or 4; paged pools need 3).
 hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const float* q,
                             uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
                             int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,

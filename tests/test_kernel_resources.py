@@ -49,9 +49,9 @@ def test_decode_g8_occupancy_budget(tmp_path):
     pad = eval(re.search(r"kOneWorkgroupPadBytes\s*=\s*([^;]+);", src).group(1))
     ks = _kernels(asm)
     dec = {n: v for n, v in ks.items() if "decode_g8_kernel" in n}
-    # NB 1..5 x (fused step, paged, plain) x grid kind at 3 bits, plain at
-    # 2 and 4 bits
-    assert len(dec) == 60, sorted(dec)
+    # NB 1..5 x (fused step, paged, plain) x grid kind at 3 bits, (fused
+    # step, plain) x grid kind at 2 and 4 bits
+    assert len(dec) == 80, sorted(dec)
     for name, (vg, lds, priv) in dec.items():
         m = re.search(r"decode_g8_kernelILi(\d)ELb(\d)ELb(\d)ELb(\d)ELi(\d)EE", name)
         nb, wide = int(m.group(1)), m.group(3) == "1"
