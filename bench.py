@@ -30,8 +30,9 @@ the default is the one above):
   paged     the varlen shape on a paged cache (iq_decode_step_paged; pages of
             --page-size positions, physical pages randomly permuted), then
             on contiguous caches with the same lengths for comparison;
-  bits32k   decode attention at the 32K shape on 2-, 3- and 4-bit records
-            (Algorithm 1 with C_b; --bits picks the one reported as value);
+  bits32k   decode attention (and the fused step) at the 32K shape on 2-, 3-
+            and 4-bit records (Algorithm 1 with C_b; --bits picks the one
+            reported as value);
   multi32k  decode of 1-4 query tokens per call at the 32K shape
             (iq_decode_attention_multi, speculative verification; --tokens picks
             the one reported as value), against single-token calls;
@@ -604,6 +605,21 @@ def run_bits32k(args, torch, api, synth, dev):
         nbytes = w.batch * w.n_kv_heads * cap * 2 * (16 * bits + 4)
         per[bits] = {"us_per_call": round(us, 3), "bytes": int(nbytes),
                      "gbs": round(nbytes / (us * 1e-6) / 1e9, 2)}
+        # the fused step (append + attention) on the same caches: the lengths
+        # advance by one per visit, so the caches are filled to cap - visits
+        reps = max(1, -(-args.steps // nl))
+        for L in layers:
+            L["cache"]["seq_lens"].fill_(cap - reps - max(1, args.warmup // nl) - 1)
+
+        def step(li, layers=layers, quats=quats, ws=ws, bits=bits):
+            L = layers[li]
+            c = L["cache"]
+            api.iq_decode_step_bits(L["q"], L["k_new"], L["v_new"], c["k_codes"], c["k_norms"],
+                                    c["v_codes"], c["v_norms"], c["seq_lens"], quats,
+                                    out=L["out"], workspace=ws, max_seq_len=cap, bits=bits)
+
+        us_step = time_graph_sweeps(torch, step, nl, args.steps, args.warmup)
+        per[bits]["step_us"] = round(us_step, 3)
         del layers, ws
         torch.cuda.empty_cache()
     b = args.bits
