@@ -332,6 +332,21 @@ float resolve_scale(float softmax_scale) {
   return softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf(static_cast<float>(kDim));
 }
 
+// Shapes the group-8 matrix-core path takes (after check_decode_args):
+// 8 query heads per KV head, rows of whole 16-position batches addressed
+// with 32-bit byte offsets (records of record_bytes bytes), 16-byte aligned
+// scale arrays, and sequences and KV heads as grid dimensions.
+iq_status check_g8_shape(int64_t n_q_heads, int64_t n_kv_heads, int64_t batch, int64_t capacity,
+                         int64_t record_bytes, const float* k_norms, const float* v_norms,
+                         const iq::DecodePlan& plan) {
+  if (n_q_heads != 8 * n_kv_heads || plan.g8_batches <= 0) return IQ_ERR_UNSUPPORTED;
+  if (capacity % 16 || capacity < 16 || capacity * record_bytes > 0x7fffffff ||
+      !iq::aligned(k_norms, 16) || !iq::aligned(v_norms, 16) || batch > 65535 ||
+      n_kv_heads > 65535)
+    return IQ_ERR_UNSUPPORTED;
+  return IQ_OK;
+}
+
 }  // namespace
 
 iq_status iq_decode_attention(const float* q, const uint8_t* k_codes, const float* k_norms,
@@ -375,14 +390,10 @@ iq_status iq_decode_attention_bits(const float* q, const uint8_t* k_codes, const
                                          n_kv_heads, head_dim, out, workspace, workspace_bytes,
                                          &plan);
   if (st != IQ_OK) return st;
-  // 2- and 4-bit records run on the group-8 matrix-core path only: rows of
-  // whole 16-position batches addressed with 32-bit byte offsets, KV heads
-  // and sequences as grid dimensions
-  if (n_q_heads != 8 * n_kv_heads || plan.g8_batches <= 0) return IQ_ERR_UNSUPPORTED;
-  if (capacity % 16 || capacity < 16 || capacity * 16 * bits > 0x7fffffff ||
-      !iq::aligned(k_norms, 16) || !iq::aligned(v_norms, 16) || batch > 65535 ||
-      n_kv_heads > 65535)
-    return IQ_ERR_UNSUPPORTED;
+  // 2- and 4-bit records run on the group-8 matrix-core path only
+  const iq_status shape = check_g8_shape(n_q_heads, n_kv_heads, batch, capacity, 16 * bits,
+                                         k_norms, v_norms, plan);
+  if (shape != IQ_OK) return shape;
   if (batch == 0) return IQ_OK;
   float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
   const hipError_t e = iq::launch_decode_g8(
@@ -429,11 +440,9 @@ iq_status iq_decode_attention_multi(const float* q, const uint8_t* k_codes,
                                          capacity, max_seq_len, quats, batch, n_q_heads,
                                          n_kv_heads, head_dim, out, workspace, SIZE_MAX, &plan);
   if (st != IQ_OK) return st;
-  if (n_q_heads != 8 * n_kv_heads || plan.g8_batches <= 0) return IQ_ERR_UNSUPPORTED;
-  if (capacity % 16 || capacity < 16 || capacity * iq::kRecordBytes > 0x7fffffff ||
-      !iq::aligned(k_norms, 16) || !iq::aligned(v_norms, 16) || batch > 65535 ||
-      n_kv_heads > 65535)
-    return IQ_ERR_UNSUPPORTED;
+  const iq_status shape = check_g8_shape(n_q_heads, n_kv_heads, batch, capacity,
+                                         iq::kRecordBytes, k_norms, v_norms, plan);
+  if (shape != IQ_OK) return shape;
   if (!iq::mul_ok(batch, n_tokens) || !iq::mul_ok(batch * n_tokens, n_q_heads))
     return IQ_ERR_INVALID_ARGUMENT;
   const size_t need = iq_decode_multi_workspace_bytes(batch, n_tokens, n_q_heads, n_kv_heads,
@@ -500,11 +509,9 @@ iq_status iq_decode_step_bits(const float* q, const void* k_new, const void* v_n
       (status_dev && !iq::aligned(status_dev, 4)))
     return IQ_ERR_INVALID_ARGUMENT;
   // the matrix-core path only, as for iq_decode_attention_bits
-  if (n_q_heads != 8 * n_kv_heads || plan.g8_batches <= 0) return IQ_ERR_UNSUPPORTED;
-  if (capacity % 16 || capacity < 16 || capacity * 16 * bits > 0x7fffffff ||
-      !iq::aligned(k_norms, 16) || !iq::aligned(v_norms, 16) || batch > 65535 ||
-      n_kv_heads > 65535)
-    return IQ_ERR_UNSUPPORTED;
+  const iq_status shape = check_g8_shape(n_q_heads, n_kv_heads, batch, capacity, 16 * bits,
+                                         k_norms, v_norms, plan);
+  if (shape != IQ_OK) return shape;
   if (batch == 0) return IQ_OK;
   const iq::StepAppend append{k_new, v_new, dtype == IQ_DTYPE_F16 ? 1 : 0, status_dev};
   float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
