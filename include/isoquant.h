@@ -9,8 +9,12 @@
  *
  * Conventions shared by every entry point
  * ---------------------------------------
- * - head_dim must be 128 and the code width is 3 bits (the configuration of
- *   Sec. 3.2 Step 4); anything else returns IQ_ERR_UNSUPPORTED.
+ * - head_dim must be 128, and the code width is 3 bits (the configuration of
+ *   Sec. 3.2 Step 4) except in the *_bits entry points (2, 3 or 4 bits; see
+ *   "Other code widths"); anything else returns IQ_ERR_UNSUPPORTED.
+ * - Sections below: the contiguous cache (rotation, compression, append,
+ *   decode, fused step), the paged cache, the reconstruct-then-compute
+ *   baseline, other code widths, multi-token decode.
  * - Device pointers are plain HIP device allocations owned by the caller.
  *   The library never allocates, frees or retains device memory and keeps no
  *   mutable global state (the codebook is an immutable constant computed once
