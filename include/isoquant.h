@@ -500,6 +500,23 @@ iq_status iq_decode_attention_multi(const float* q,
                                     float* out, void* workspace, size_t workspace_bytes,
                                     hipStream_t stream);
 
+/* iq_decode_attention_multi on a paged cache (pools, page_size, n_pages,
+ * block_tables, max_pages as for iq_decode_attention_paged; capacity is
+ * max_pages * page_size); workspace as sized by
+ * iq_decode_multi_workspace_bytes.  Results equal those of
+ * iq_decode_attention_multi on a contiguous cache holding the same records. */
+iq_status iq_decode_attention_multi_paged(const float* q,
+                                          const uint8_t* k_codes, const float* k_norms,
+                                          const uint8_t* v_codes, const float* v_norms,
+                                          int64_t page_size, int64_t n_pages,
+                                          const int32_t* block_tables, int64_t max_pages,
+                                          const int32_t* seq_lens, int64_t max_seq_len,
+                                          const float* quats, int64_t batch, int64_t n_tokens,
+                                          int64_t n_q_heads, int64_t n_kv_heads,
+                                          int64_t head_dim, float softmax_scale, float* out,
+                                          void* workspace, size_t workspace_bytes,
+                                          hipStream_t stream);
+
 #ifdef __cplusplus
 }  /* extern "C" */
 #endif

@@ -514,6 +514,37 @@ def iq_decode_step_paged(q, k_new, v_new, pool, block_tables, seq_lens, quats, o
     return out
 
 
+def iq_decode_attention_multi_paged(q, pool, block_tables, seq_lens, quats, out=None,
+                                    workspace=None, max_seq_len=None,
+                                    softmax_scale: float = 0.0):
+    """iq_decode_attention_multi on page pools; q [B][T][8 H_kv][128]."""
+    if q.dim() != 4 or q.shape[-1] != HEAD_DIM:
+        raise ValueError("q must be [batch][n_tokens][n_q_heads][128]")
+    b, t, hq, _ = q.shape
+    dev = q.device
+    _require(q, "q", torch.float32, (b, t, hq, HEAD_DIM), dev)
+    n_pages, hkv, page, max_pages = _paged_pools(pool, block_tables, dev)
+    _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
+    _require(quats, "quats", torch.float32, (hkv, 32, 2, 4), dev)
+    if max_seq_len is None:
+        max_seq_len = max_pages * page
+    if out is None:
+        out = torch.empty((b, t, hq, HEAD_DIM), dtype=torch.float32, device=dev)
+    _require(out, "out", torch.float32, (b, t, hq, HEAD_DIM), dev)
+    if workspace is None:
+        nbytes = iq_decode_multi_workspace_bytes(b, t, hq, hkv, max_seq_len)
+        if nbytes <= 0:
+            raise ValueError("unsupported multi-token decode shape")
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    st = _lib.lib().iq_decode_attention_multi_paged(
+        _ptr(q), _ptr(pool["k_codes"]), _ptr(pool["k_norms"]), _ptr(pool["v_codes"]),
+        _ptr(pool["v_norms"]), page, n_pages, _ptr(block_tables), max_pages, _ptr(seq_lens),
+        max_seq_len, _ptr(quats), b, t, hq, hkv, HEAD_DIM, float(softmax_scale), _ptr(out),
+        _ptr(workspace), workspace.numel(), _stream(dev))
+    _lib.check("iq_decode_attention_multi_paged", st)
+    return out
+
+
 # ---------------------------------------------------------------------------
 # reconstruct-then-compute baseline (materialized fp16 cache)
 # ---------------------------------------------------------------------------

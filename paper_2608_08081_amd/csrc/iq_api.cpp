@@ -453,7 +453,8 @@ iq_status iq_decode_attention_multi(const float* q, const uint8_t* k_codes,
   const hipError_t e = iq::launch_decode_g8_multi(
       plan.g8_batches, plan.g8_splits, plan.g8_split_len, static_cast<int>(n_tokens), q,
       k_codes, k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len, quats, batch,
-      n_kv_heads, resolve_scale(softmax_scale), out, static_cast<float*>(workspace), stream);
+      n_kv_heads, resolve_scale(softmax_scale), out, static_cast<float*>(workspace), nullptr,
+      stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 
@@ -664,6 +665,42 @@ iq_status iq_decode_step_paged(const float* q, const void* k_new, const void* v_
       plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes, k_norms, v_codes, v_norms,
       seq_lens, max_pages * page_size, max_seq_len, quats, batch, n_kv_heads,
       resolve_scale(softmax_scale), out, parts, &append, &pt, 3, stream);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+iq_status iq_decode_attention_multi_paged(
+    const float* q, const uint8_t* k_codes, const float* k_norms, const uint8_t* v_codes,
+    const float* v_norms, int64_t page_size, int64_t n_pages, const int32_t* block_tables,
+    int64_t max_pages, const int32_t* seq_lens, int64_t max_seq_len, const float* quats,
+    int64_t batch, int64_t n_tokens, int64_t n_q_heads, int64_t n_kv_heads, int64_t head_dim,
+    float softmax_scale, float* out, void* workspace, size_t workspace_bytes,
+    hipStream_t stream) {
+  if (n_tokens == 1)
+    return iq_decode_attention_paged(q, k_codes, k_norms, v_codes, v_norms, page_size, n_pages,
+                                     block_tables, max_pages, seq_lens, max_seq_len, quats,
+                                     batch, n_q_heads, n_kv_heads, head_dim, softmax_scale, out,
+                                     workspace, workspace_bytes, stream);
+  if (n_tokens < 2 || n_tokens > 4) return IQ_ERR_UNSUPPORTED;
+  iq::PageTable pt;
+  iq_status st = check_pages(n_kv_heads, page_size, n_pages, block_tables, max_pages, &pt);
+  if (st != IQ_OK) return st;
+  iq::DecodePlan plan;
+  st = check_paged_decode(q, k_codes, k_norms, v_codes, v_norms, seq_lens, max_seq_len, quats,
+                          batch, n_q_heads, n_kv_heads, head_dim, out, workspace, SIZE_MAX, pt,
+                          &plan);
+  if (st != IQ_OK) return st;
+  if (!iq::mul_ok(batch, n_tokens) || !iq::mul_ok(batch * n_tokens, n_q_heads))
+    return IQ_ERR_INVALID_ARGUMENT;
+  const size_t need = iq_decode_multi_workspace_bytes(batch, n_tokens, n_q_heads, n_kv_heads,
+                                                      max_seq_len, head_dim);
+  if (need == 0) return IQ_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < need) return IQ_ERR_WORKSPACE_TOO_SMALL;
+  if (batch == 0) return IQ_OK;
+  const hipError_t e = iq::launch_decode_g8_multi(
+      plan.g8_batches, plan.g8_splits, plan.g8_split_len, static_cast<int>(n_tokens), q,
+      k_codes, k_norms, v_codes, v_norms, seq_lens, max_pages << pt.page_shift, max_seq_len,
+      quats, batch, n_kv_heads, resolve_scale(softmax_scale), out,
+      static_cast<float*>(workspace), &pt, stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 

@@ -22,14 +22,16 @@ namespace {
 // first (kept in registers), one max per token and head, then the weights
 // and values.  Partials per (split, token, head); the merge kernel takes the
 // token axis.
-template <int NB, bool kWide, int kT>
+//
+// kPaged: the cache is a page pool (PageTable), as in decode_g8_kernel.
+template <int NB, bool kWide, int kT, bool kPaged>
 __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
     const float* __restrict__ q, const uint8_t* __restrict__ k_codes,
     const float* __restrict__ k_norms, const uint8_t* __restrict__ v_codes,
     const float* __restrict__ v_norms, const int32_t* __restrict__ seq_lens,
     const float* __restrict__ quats, float* __restrict__ partials, float* __restrict__ out,
     int64_t capacity, int max_seq_len, int n_kv_heads, int n_splits, int split_len, float qscale,
-    Codebook cb) {
+    Codebook cb, PageTable pages) {
   static_assert(kT >= 2 && kT <= 4, "2 to 4 tokens");
   struct Smem {
     uint32_t lut[64];
@@ -66,7 +68,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
       quats + static_cast<int64_t>(g) * kQuatFloats + 8 * qblk);
   const f32x4_t ql = qpar[0], qr = qpar[1];
   float* part_bg = partials + static_cast<int64_t>(bg) * n_splits * kT * (kHeads * kPart);
-  const int64_t row = static_cast<int64_t>(bg) * capacity;
+  const int64_t row = kPaged ? 0 : static_cast<int64_t>(bg) * capacity;
   const uint8_t* kc = k_codes + row * kRecordBytes;
   const uint8_t* vc = v_codes + row * kRecordBytes;
 
@@ -107,19 +109,39 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
   }
   const float* kn = k_norms + row;
   const float* vn = v_norms + row;
+  // paged: each batch's record delta from its page-table entry, the NB
+  // entries read together and an invalid one replaced by page 0
   int64_t dlt[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) dlt[i] = 0;
+  if constexpr (kPaged) {
+    const int32_t* trow = pages.tables + static_cast<int64_t>(b) * pages.max_pages;
+    int32_t pg[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int t = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
+      pg[i] = trow[t >> pages.page_shift];
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int t = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
+      const int64_t page =
+          static_cast<uint32_t>(pg[i]) < static_cast<uint32_t>(pages.n_pages) ? pg[i] : 0;
+      dlt[i] = ((page * n_kv_heads + g) << pages.page_shift) -
+               static_cast<int64_t>((t >> pages.page_shift) << pages.page_shift);
+    }
+  }
   uint32_t kw[NB][3], vw[NB][3];
   f32x4_t ksl, vsl;
-  load_keys<NB, false, 3>(kc, kn, vn, dlt, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
+  load_keys<NB, kPaged, 3>(kc, kn, vn, dlt, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
   const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
   int tb[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) tb[i] = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
   // every value batch goes out behind the keys
 #pragma unroll
-  for (int i = 0; i < NB; ++i) load_value_batch<3>(vc, tb[i], koff, vw[i]);
+  for (int i = 0; i < NB; ++i)
+    load_value_batch<3>(kPaged ? vc + dlt[i] * kRecordBytes : vc, tb[i], koff, vw[i]);
   const int vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
   const uint32_t vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));
 
@@ -340,8 +362,9 @@ hipError_t launch_decode_g8_multi(int nb, int64_t n_splits, int64_t split_len, i
                                   const int32_t* seq_lens, int64_t capacity,
                                   int64_t max_seq_len, const float* quats, int64_t batch,
                                   int64_t n_kv_heads, float scale, float* out, float* partials,
-                                  hipStream_t stream) {
+                                  const PageTable* pages, hipStream_t stream) {
   if (n_tok < 2 || n_tok > 4) return hipErrorInvalidValue;
+  const PageTable pt = pages ? *pages : PageTable{nullptr, 0, 4, 1};
   const dim3 grid(static_cast<unsigned>(n_splits), static_cast<unsigned>(n_kv_heads),
                   static_cast<unsigned>(batch)),
       block(kThreads);
@@ -350,16 +373,22 @@ hipError_t launch_decode_g8_multi(int nb, int64_t n_splits, int64_t split_len, i
   const size_t lds_pad = wide ? 0 : kOneWorkgroupPadBytes;
   const float qscale = scale * kLog2e;
   const Codebook& cb = codebook();
-#define IQ_LAUNCH_MT(NB_, WIDE_, T_)                                                            \
-  hipLaunchKernelGGL((decode_g8_multi_kernel<NB_, WIDE_, T_>), grid, block, lds_pad, stream, q, \
-                     k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials, out,        \
+#define IQ_LAUNCH_MTP(NB_, WIDE_, T_, P_)                                                      \
+  hipLaunchKernelGGL((decode_g8_multi_kernel<NB_, WIDE_, T_, P_>), grid, block, lds_pad, stream, \
+                     q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials, out,     \
                      capacity, static_cast<int>(max_seq_len), static_cast<int>(n_kv_heads),     \
-                     static_cast<int>(n_splits), static_cast<int>(split_len), qscale, cb)
+                     static_cast<int>(n_splits), static_cast<int>(split_len), qscale, cb, pt)
+#define IQ_LAUNCH_MT(NB_, WIDE_, T_)        \
+  if (pages) {                              \
+    IQ_LAUNCH_MTP(NB_, WIDE_, T_, true);    \
+  } else {                                  \
+    IQ_LAUNCH_MTP(NB_, WIDE_, T_, false);   \
+  }
 #define IQ_LAUNCH_MT_W(NB_, T_)       \
   if (wide) {                         \
-    IQ_LAUNCH_MT(NB_, true, T_);      \
+    IQ_LAUNCH_MT(NB_, true, T_)       \
   } else {                            \
-    IQ_LAUNCH_MT(NB_, false, T_);     \
+    IQ_LAUNCH_MT(NB_, false, T_)      \
   }
 #define IQ_LAUNCH_MT_NB(T_)                   \
   switch (nb) {                               \
@@ -379,6 +408,7 @@ hipError_t launch_decode_g8_multi(int nb, int64_t n_splits, int64_t split_len, i
 #undef IQ_LAUNCH_MT_NB
 #undef IQ_LAUNCH_MT_W
 #undef IQ_LAUNCH_MT
+#undef IQ_LAUNCH_MTP
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || n_splits == 1) return e;
   const dim3 mgrid(static_cast<unsigned>(n_kv_heads * kHeads),

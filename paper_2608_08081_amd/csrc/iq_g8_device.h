@@ -296,6 +296,17 @@ using WaveStage = WaveStageB<3>;
 // kPaged: batch i of the wave lies at record index dlt[i] + (its position)
 // of the pools (dlt[i] = the batch page's record base minus the page's first
 // logical position); contiguous caches use the row pointers as they are.
+// dlt[j] for a per-lane j < NB, as a chain of selects on compile-time
+// indices (an index that is a loop variable before unrolling can leave the
+// array in scratch memory when registers are tight).
+template <int I, int NB>
+__device__ __forceinline__ int64_t pick_batch(const int64_t (&dlt)[NB], int j) {
+  if constexpr (I == NB - 1)
+    return dlt[I];
+  else
+    return j == I ? dlt[I] : pick_batch<I + 1, NB>(dlt, j);
+}
+
 template <int NB, bool kPaged, int kBits>
 __device__ __forceinline__ void load_keys(const uint8_t* kc, const float* kn, const float* vn,
                                           const int64_t (&dlt)[NB], int wbase, int clamp16,
@@ -308,11 +319,7 @@ __device__ __forceinline__ void load_keys(const uint8_t* kc, const float* kn, co
     const int jb = lane >> 2 < NB ? lane >> 2 : NB - 1;
     const int tj = (wbase + 16 * jb < clamp16 ? wbase + 16 * jb : clamp16) + 4 * (lane & 3);
     int64_t d = 0;
-    if constexpr (kPaged) {
-      d = dlt[0];
-#pragma unroll
-      for (int i = 1; i < NB; ++i) d = jb == i ? dlt[i] : d;
-    }
+    if constexpr (kPaged) d = pick_batch<0, NB>(dlt, jb);
     ksl = *reinterpret_cast<const f32x4_t*>(kn + d + tj);
     vsl = *reinterpret_cast<const f32x4_t*>(vn + d + tj);
   }

@@ -170,3 +170,27 @@ def test_paged_compress_equals_contiguous():
     unused = sorted(set(range(n_pages)) - set(tables.ravel().tolist()))
     for p in unused:
         assert int(pool["k_codes"][p].abs().sum()) == 0
+
+
+@pytest.mark.parametrize("n_tok,lens,hkv,page,cap", [
+    (3, [4000], 4, 256, 4096),                                        # one round
+    (4, [int(x) for x in np.linspace(0, 2040, 40)], 2, 64, 2048),     # several rounds
+])
+def test_paged_multi_equals_contiguous(n_tok, lens, hkv, page, cap):
+    """Multi-token decode on the pools equals it on the contiguous cache."""
+    w = synth.Workload(87, "paged_mt", len(lens), 8 * hkv, hkv, cap, "f16", rotation_seed=1087)
+    cache, quats, _, _ = _filled(w, lens, cap, 12)
+    max_pages = cap // page
+    n_pages = len(lens) * max_pages + 2
+    tables = _tables(lens, page, max_pages, n_pages, 6)
+    pool = _scatter(cache, tables, page, n_pages)
+    g = np.random.default_rng(13)
+    q = torch.from_numpy(g.standard_normal((len(lens), n_tok, 8 * hkv, 128),
+                                           dtype=np.float32)).to(DEV)
+    ref = api.iq_decode_attention_multi(q, cache["k_codes"], cache["k_norms"], cache["v_codes"],
+                                        cache["v_norms"], cache["seq_lens"], quats,
+                                        max_seq_len=cap)
+    got = api.iq_decode_attention_multi_paged(q, pool, torch.from_numpy(tables).to(DEV),
+                                              cache["seq_lens"], quats, max_seq_len=cap)
+    torch.cuda.synchronize()
+    assert torch.equal(got, ref)
