@@ -347,3 +347,35 @@ def test_multi_token_validation():
     assert w2 > 0 and w4 >= 2 * w2 - 256
     assert L.iq_decode_multi_workspace_bytes(1, 5, 16, 2, 256, 128) == 0
     assert L.iq_decode_multi_workspace_bytes(1, 2, 8, 2, 256, 128) == 0
+
+
+def test_step_bits_and_multi_paged_validation():
+    """Argument checks of iq_decode_step_bits and iq_decode_attention_multi_paged
+    (host side only: nothing is launched on a validation error)."""
+    def step(**kw):
+        a = dict(dtype=1, b=1, hq=16, hkv=2, cap=256, msl=256, bits=4, wsb=1 << 30)
+        a.update(kw)
+        return L.iq_decode_step_bits(A, A, A, a["dtype"], A, A, B, B, A, a["cap"], a["msl"], A,
+                                     a["b"], a["hq"], a["hkv"], 128, 0.0, A, A, a["wsb"], None,
+                                     a["bits"], None)
+    assert step(bits=5) == 2
+    assert step(dtype=7) == 2
+    assert step(hq=8) == 2                       # group 4: matrix-core path only
+    assert step(cap=250, msl=250) == 2           # capacity not a multiple of 16
+    assert step(msl=0) == 1                      # the step needs room for a token
+    assert step(wsb=16) == 3
+    assert step(b=0) == 0
+
+    def mtp(**kw):
+        a = dict(page=64, n_pages=8, max_pages=4, msl=256, b=1, t=3, hq=16, hkv=2, wsb=1 << 30)
+        a.update(kw)
+        return L.iq_decode_attention_multi_paged(A, A, A, B, B, a["page"], a["n_pages"], A,
+                                                 a["max_pages"], A, a["msl"], A, a["b"], a["t"],
+                                                 a["hq"], a["hkv"], 128, 0.0, A, A, a["wsb"],
+                                                 None)
+    assert mtp(t=5) == 2
+    assert mtp(page=48) == 1                     # not a power of two
+    assert mtp(msl=257) == 1                     # beyond max_pages * page_size
+    assert mtp(hq=8) == 2
+    assert mtp(wsb=16) == 3
+    assert mtp(b=0) == 0
