@@ -7,8 +7,9 @@ attention over the whole cache (App. A), issued as one fused call
 4 KV heads, head_dim 128, ~32K cached positions.  Steps cycle through NL
 distinct layer caches (default 48 x 13.6 MB = 654 MB, more than twice the
 256 MB last-level cache), as a model's layer sweep does, so the cache bytes
-are streamed from HBM.  Steps are replayed from HIP graphs (one graph per
-sweep over the layers).
+are streamed from HBM.  Exactly --steps steps are timed, replayed from HIP
+graphs of consecutive distinct layers (whole sweeps over the layers, then one
+graph for the remainder).
 
 Prints one JSON line.  ``value`` is the achieved algorithmic HBM bandwidth of
 a step (bytes the method must move / step time); ``us_per_step`` is the
@@ -305,11 +306,86 @@ def make_paged_layers(api, synth, w, n_layers, lengths, capacity, page, seed, de
     return quats, layers
 
 
+def visits_per_layer(warmup, steps, n_layers):
+    """Upper bound of the calls one layer receives from time_graph_calls:
+    the eager pass, the set-up replays of the captured graphs (four at most)
+    and the warm-up and timed calls."""
+    return 1 + 4 + math.ceil(warmup / n_layers) + math.ceil(steps / n_layers) + 1
+
+
+def cache_capacity(longest, warmup, steps, n_layers):
+    """Capacity of the cycled layer caches: the longest sequence, one
+    appended token per visit of the layer (visits_per_layer), rounded up
+    to a multiple of 64 with at least 64 spare positions."""
+    return (longest + visits_per_layer(warmup, steps, n_layers) + 64 + 63) // 64 * 64
+
+
+def time_graph_calls(torch, fn, n_layers, steps, warmup):
+    """fn(li) issues one call for layer li.  Times exactly `steps` calls that
+    cycle the layers, replayed from HIP graphs of consecutive distinct layers
+    (whole sweeps of n_layers calls, then one graph for the remainder), with
+    HIP events on the replay stream.  Before that, untimed: one eager call
+    per layer (loads the code objects), one replay of every captured graph,
+    one whole sweep (so each layer's data was last touched n_layers - 1
+    layers ago), then `warmup` calls continuing the cycle from layer 0; the
+    timed calls go on from there.  Returns (us per call, wall seconds)."""
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        for li in range(n_layers):
+            fn(li)
+    torch.cuda.current_stream().wait_stream(stream)
+    torch.cuda.synchronize()
+
+    graphs = {}
+
+    def graph(start, count):
+        key = (start, count)
+        if key not in graphs:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for i in range(count):
+                    fn((start + i) % n_layers)
+            graphs[key] = g
+        return graphs[key]
+
+    def plan(start, count):
+        full, tail = divmod(count, n_layers)
+        seq = [graph(start, n_layers)] * full
+        if tail:
+            seq.append(graph(start, tail))
+        return seq
+
+    sweep0 = graph(0, n_layers)
+    warm = plan(0, warmup)
+    timed = plan(warmup % n_layers, steps)
+    torch.cuda.synchronize()
+    # set-up replays: every graph once (its first launch), then a whole sweep
+    for g in list(graphs.values()) + [sweep0]:
+        g.replay()
+    for g in warm:
+        g.replay()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record()
+    for g in timed:
+        g.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    us = ev0.elapsed_time(ev1) * 1e3 / steps
+    del graphs, warm, timed, sweep0
+    return us, wall
+
+
 def time_steps(api, layers, quats, ws, capacity, args):
-    """Warm-up, then `args.steps` fused steps (append + attention) cycling the
-    layers, replayed from HIP graphs and timed with HIP events on the replay
-    stream; then the attention alone (iq_decode_attention) the same way.
-    Returns (us per fused step, us per decode-only call, wall seconds)."""
+    """`args.steps` fused steps (append + attention) cycling the layers after
+    `args.warmup` untimed ones (time_graph_calls), then as many calls of the
+    attention alone (iq_decode_attention, at most 2400) the same way.
+    Returns (us per fused step, us per decode-only call, wall seconds of the
+    timed steps)."""
     import torch
 
     nl = len(layers)
@@ -334,63 +410,40 @@ def time_steps(api, layers, quats, ws, capacity, args):
                                     c["v_norms"], c["seq_lens"], quats, out=L["out"],
                                     workspace=ws, max_seq_len=capacity)
 
-    # eager warm-up of every layer once (loads the code object), then capture
-    torch.cuda.synchronize()
-    stream = torch.cuda.Stream()
-    stream.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(stream):
-        for li in range(nl):
-            step(li)
-    torch.cuda.current_stream().wait_stream(stream)
-    torch.cuda.synchronize()
-
-    def capture(fn):
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            fn()
-        return g
-
-    sweep = capture(lambda: [step(li) for li in range(nl)])
-    singles = [capture(lambda li=li: step(li)) for li in range(nl)]
-    decode_sweep = capture(lambda: [step(li, append=False) for li in range(nl)])
-    torch.cuda.synchronize()
-
-    def run_steps(n, start):
-        done = 0
-        li = start % nl
-        while done < n:
-            if li == 0 and n - done >= nl:
-                sweep.replay()
-                done += nl
-            else:
-                singles[li].replay()
-                done += 1
-                li = (li + 1) % nl
-        return (start + n) % nl
-
-    pos = run_steps(args.warmup, 0)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ev0.record()
-    pos = run_steps(args.steps, pos)
-    ev1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    us_per_step = ev0.elapsed_time(ev1) * 1e3 / args.steps
-
-    # decode-only: HIP events around graph replays of decode launches on the
-    # replay stream (the graph launches onto torch's current stream)
-    reps = max(1, min(2400, args.steps) // nl)
-    d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    d0.record()
-    for _ in range(reps):
-        decode_sweep.replay()
-    d1.record()
-    torch.cuda.synchronize()
-    decode_us = d0.elapsed_time(d1) * 1e3 / (reps * nl)
+    us_per_step, wall = time_graph_calls(torch, step, nl, args.steps, args.warmup)
+    decode_us, _ = time_graph_calls(torch, lambda li: step(li, append=False), nl,
+                                    min(args.steps, 2400), args.warmup)
     return us_per_step, decode_us, wall
+
+
+def achievable_read(torch, api, dev, nbytes, n_buffers, steps, warmup):
+    """The achievable single-launch read bandwidth at the step's size: a
+    plain streaming read (iq_stream_read) of `nbytes`, cycled over n_buffers
+    distinct buffers and timed exactly as the steps are (time_graph_calls),
+    for several workgroup sizes and loads per thread; the fastest is
+    reported."""
+    n16 = -(-nbytes // 16)
+    bufs = [torch.full((4 * n16,), i + 1, dtype=torch.int32, device=dev)
+            for i in range(n_buffers)]
+    best = None
+    for block, loads in ((256, 1), (256, 2), (256, 4), (256, 8), (512, 1), (512, 2), (512, 4),
+                         (1024, 1), (1024, 2), (1024, 4)):
+        sink = torch.zeros(api.iq_stream_read_sink_words(16 * n16, block, loads),
+                           dtype=torch.int32, device=dev)
+
+        def read(li, block=block, loads=loads, sink=sink):
+            api.iq_stream_read(bufs[li], sink, block_threads=block, loads_per_thread=loads)
+
+        us, _ = time_graph_calls(torch, read, n_buffers, max(steps, 2 * n_buffers), warmup)
+        if best is None or us < best[0]:
+            best = (us, block, loads)
+    del bufs
+    torch.cuda.empty_cache()
+    us, block, loads = best
+    return {"value": round(16 * n16 / (us * 1e-6) / 1e9, 2), "unit": "GB/s",
+            "us_per_launch": round(us, 3), "bytes": int(16 * n16),
+            "kernel": f"stream_read_kernel<{loads}>, {block}-thread workgroups (fastest of 10 "
+                      f"shapes), {n_buffers} buffers cycled (cold)"}
 
 
 def step_result(metric, workload, w, layers, nl, us_per_step, decode_us, wall, args, kernel,
@@ -442,8 +495,7 @@ def step_result(metric, workload, w, layers, nl, us_per_step, decode_us, wall, a
 def run_step32k(args, torch, api, synth, dev):
     w = synth.WORKLOADS[2]
     nl = args.layers
-    total_visits = math.ceil((args.warmup + args.steps) / nl) + 2
-    capacity = (args.context + total_visits + 64 + 63) // 64 * 64
+    capacity = cache_capacity(args.context, args.warmup, args.steps, nl)
     print(f"# building {nl} layer caches ({args.context} positions each)", file=sys.stderr,
           flush=True)
     quats, layers = make_layers(api, synth, w, nl, args.context, capacity, args.seed, dev)
@@ -460,6 +512,12 @@ def run_step32k(args, torch, api, synth, dev):
         "heads + the appended token's inputs and records")
     result["config"]["context"] = result["config"].pop("mean_context")
     result["roofline"]["traffic"] = read_traffic(digest)
+    ach = achievable_read(torch, api, dev, result["roofline"]["bytes_per_launch"], nl,
+                          args.steps, args.warmup)
+    result["roofline"]["achievable"] = ach["value"]
+    result["roofline"]["frac_of_achievable"] = round(result["roofline"]["achieved"] /
+                                                     ach["value"], 4)
+    result["roofline"]["achievable_read"] = ach
     result["source_digest"] = digest
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.context, args.cpu_seconds)
@@ -470,8 +528,7 @@ def run_varlen(args, torch, api, synth, dev):
     w = synth.WORKLOADS[3]
     nl = args.layers
     lengths = synth.context_lengths(args.seed, w)
-    total_visits = math.ceil((args.warmup + args.steps) / nl) + 2
-    capacity = (int(lengths.max()) + total_visits + 64 + 63) // 64 * 64
+    capacity = cache_capacity(int(lengths.max()), args.warmup, args.steps, nl)
     print(f"# building {nl} varlen layer caches (batch {w.batch}, mean context "
           f"{lengths.mean():.0f})", file=sys.stderr, flush=True)
     quats, layers = make_varlen_layers(api, synth, w, nl, lengths, capacity, args.seed, dev)
@@ -496,7 +553,7 @@ def run_paged(args, torch, api, synth, dev):
     nl = args.layers
     page = args.page_size
     lengths = synth.context_lengths(args.seed, w)
-    total_visits = math.ceil((args.warmup + args.steps) / nl) + 2
+    total_visits = visits_per_layer(args.warmup, args.steps, nl)
     capacity = (int(lengths.max()) + total_visits + page + page - 1) // page * page
     print(f"# building {nl} paged layer caches (batch {w.batch}, page {page})",
           file=sys.stderr, flush=True)
@@ -530,8 +587,7 @@ def run_paged(args, torch, api, synth, dev):
 def run_append8k(args, torch, api, synth, dev):
     w = synth.WORKLOADS[1]
     nl = args.layers
-    total_visits = math.ceil((args.warmup + args.steps) / nl) + 2
-    capacity = (w.context + total_visits + 64 + 63) // 64 * 64
+    capacity = cache_capacity(w.context, args.warmup, args.steps, nl)
     print(f"# building {nl} layer caches ({w.context} positions each)", file=sys.stderr,
           flush=True)
     quats, layers = make_layers(api, synth, w, nl, w.context, capacity, args.seed, dev)
@@ -546,37 +602,6 @@ def run_append8k(args, torch, api, synth, dev):
         "iq_decode_step per call = decode_g8_kernel<NB, append> + merge_g8_kernel<append>; "
         f"algorithmic bytes = {BYTES_PER_TOKEN_HEAD} B x attended positions x KV heads + the "
         "appended tokens' inputs and records")
-
-
-def time_graph_sweeps(torch, fn, n_layers, steps, warmup):
-    """fn(li) issues one call for layer li.  Captures one sweep over the layers
-    as a HIP graph, replays it for warm-up, then times replays covering at
-    least `steps` calls with HIP events on the replay stream.  Returns us per
-    call."""
-    torch.cuda.synchronize()
-    stream = torch.cuda.Stream()
-    stream.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(stream):
-        for li in range(n_layers):
-            fn(li)
-    torch.cuda.current_stream().wait_stream(stream)
-    torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        for li in range(n_layers):
-            fn(li)
-    torch.cuda.synchronize()
-    for _ in range(max(1, warmup // n_layers)):
-        g.replay()
-    reps = max(1, -(-steps // n_layers))
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    ev0.record()
-    for _ in range(reps):
-        g.replay()
-    ev1.record()
-    torch.cuda.synchronize()
-    return ev0.elapsed_time(ev1) * 1e3 / (reps * n_layers)
 
 
 def run_bits32k(args, torch, api, synth, dev):
@@ -601,15 +626,14 @@ def run_bits32k(args, torch, api, synth, dev):
                                          c["v_norms"], c["seq_lens"], quats, out=L["out"],
                                          workspace=ws, max_seq_len=cap, bits=bits)
 
-        us = time_graph_sweeps(torch, call, nl, args.steps, args.warmup)
+        us = time_graph_calls(torch, call, nl, args.steps, args.warmup)[0]
         nbytes = w.batch * w.n_kv_heads * cap * 2 * (16 * bits + 4)
         per[bits] = {"us_per_call": round(us, 3), "bytes": int(nbytes),
                      "gbs": round(nbytes / (us * 1e-6) / 1e9, 2)}
         # the fused step (append + attention) on the same caches: the lengths
         # advance by one per visit, so the caches are filled to cap - visits
-        reps = max(1, -(-args.steps // nl))
         for L in layers:
-            L["cache"]["seq_lens"].fill_(cap - reps - max(1, args.warmup // nl) - 1)
+            L["cache"]["seq_lens"].fill_(cap - visits_per_layer(args.warmup, args.steps, nl))
 
         def step(li, layers=layers, quats=quats, ws=ws, bits=bits):
             L = layers[li]
@@ -618,7 +642,7 @@ def run_bits32k(args, torch, api, synth, dev):
                                     c["v_codes"], c["v_norms"], c["seq_lens"], quats,
                                     out=L["out"], workspace=ws, max_seq_len=cap, bits=bits)
 
-        us_step = time_graph_sweeps(torch, step, nl, args.steps, args.warmup)
+        us_step = time_graph_calls(torch, step, nl, args.steps, args.warmup)[0]
         per[bits]["step_us"] = round(us_step, 3)
         del layers, ws
         torch.cuda.empty_cache()
@@ -679,7 +703,7 @@ def run_multi32k(args, torch, api, synth, dev):
                                           c["v_norms"], c["seq_lens"], quats, out=outs[li],
                                           workspace=ws, max_seq_len=cap)
 
-        us = time_graph_sweeps(torch, call, nl, args.steps, args.warmup)
+        us = time_graph_calls(torch, call, nl, args.steps, args.warmup)[0]
         nbytes = w.n_kv_heads * cap * BYTES_PER_TOKEN_HEAD + 2 * n_tok * w.n_q_heads * 128 * 4
         per[n_tok] = {"us_per_call": round(us, 3), "bytes": int(nbytes),
                       "gbs": round(nbytes / (us * 1e-6) / 1e9, 2),
@@ -783,7 +807,7 @@ def run_baseline32k(args, torch, api, synth, dev):
                                     workspace=ws16, max_seq_len=capacity)
 
     t0 = time.perf_counter()
-    us = {name: time_graph_sweeps(torch, fn, nl, args.steps, args.warmup)
+    us = {name: time_graph_calls(torch, fn, nl, args.steps, args.warmup)[0]
           for name, fn in (("packed", packed), ("fp16", fp16), ("dequantize", dequantize),
                            ("reconstruct", reconstruct))}
     wall = time.perf_counter() - t0

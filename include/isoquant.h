@@ -298,7 +298,10 @@ iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, i
  *   capacity          : max_pages * page_size (logical positions per
  *                       sequence), with capacity * 48 < 2^31.
  * A page index outside [0, n_pages) is a caller error: reads then use page 0
- * and writes are skipped, so no access leaves the pools.  The decode entry
+ * and writes are skipped, so no access leaves the pools; a fused step whose
+ * new position lies on such a page treats it as having no room (nothing
+ * written or attended for that token, seq_lens[b] unchanged, IQ_ERR_CAPACITY
+ * OR-ed into *status_dev).  The decode entry
  * points run the group-8 matrix-core path only (IQ_ERR_UNSUPPORTED unless
  * n_q_heads == 8 * n_kv_heads); batch and n_kv_heads <= 65535.  Results
  * equal those of the contiguous entry points on a cache holding the same
@@ -484,7 +487,8 @@ iq_status iq_decode_step_bits(const float* q, const void* k_new, const void* v_n
  * Other arguments as for iq_decode_attention.  n_tokens >= 2 runs on the
  * matrix-core path only (n_q_heads == 8 * n_kv_heads, capacity a multiple
  * of 16 and >= 16, 16-byte aligned scale arrays, batch and n_kv_heads <=
- * 65535); otherwise IQ_ERR_UNSUPPORTED.
+ * 65535, batch * n_tokens <= 65535); otherwise IQ_ERR_UNSUPPORTED, and
+ * iq_decode_multi_workspace_bytes returns 0 for such shapes.
  */
 size_t iq_decode_multi_workspace_bytes(int64_t batch, int64_t n_tokens, int64_t n_q_heads,
                                        int64_t n_kv_heads, int64_t max_seq_len,
@@ -516,6 +520,32 @@ iq_status iq_decode_attention_multi_paged(const float* q,
                                           int64_t head_dim, float softmax_scale, float* out,
                                           void* workspace, size_t workspace_bytes,
                                           hipStream_t stream);
+
+/*
+ * Measurement support (not part of the method)
+ * ---------------------------------------------
+ * The decode step is bound by HBM bandwidth (its algorithmic bytes are the
+ * records and scales it streams, Sec. 3.4 and Table 2).  iq_stream_read is
+ * the reference point for what one launch can reach: it reads `bytes` of
+ * `src` with 16-byte loads, loads_per_thread per thread, all issued before
+ * any is used, consecutive threads on consecutive 16-byte words; workgroups
+ * of block_threads threads (64, 128, 256, 512 or 1024), loads_per_thread
+ * 1, 2, 4, 8 or 16.
+ *
+ * src        : device, 16-byte aligned, `bytes` a multiple of 16 (0 = no-op).
+ * sink       : device uint32 [sink_words], sink_words >=
+ *              iq_stream_read_sink_words(bytes, block_threads,
+ *              loads_per_thread) (the number of workgroups); word w is
+ *              written only if the XOR of every word workgroup w read equals
+ *              `sentinel`, so a run normally writes nothing.
+ * Returns IQ_ERR_INVALID_ARGUMENT for any other shape or a null or
+ * misaligned pointer, IQ_ERR_HIP if the launch fails.
+ */
+size_t iq_stream_read_sink_words(size_t bytes, int32_t block_threads, int32_t loads_per_thread);
+
+iq_status iq_stream_read(const void* src, size_t bytes, uint32_t* sink, size_t sink_words,
+                         int32_t block_threads, int32_t loads_per_thread, uint32_t sentinel,
+                         hipStream_t stream);
 
 #ifdef __cplusplus
 }  /* extern "C" */

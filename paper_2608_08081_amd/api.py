@@ -630,3 +630,26 @@ def iq_decode_attention_f16(q, k, v, seq_lens, out=None, workspace=None, max_seq
         float(softmax_scale), _ptr(out), _ptr(workspace), workspace.numel(), _stream(dev))
     _lib.check("iq_decode_attention_f16", st)
     return out
+
+
+# ---------------------------------------------------------------------------
+# measurement support
+# ---------------------------------------------------------------------------
+
+def iq_stream_read_sink_words(nbytes: int, block_threads: int, loads_per_thread: int) -> int:
+    return int(_lib.lib().iq_stream_read_sink_words(nbytes, block_threads, loads_per_thread))
+
+
+def iq_stream_read(src, sink, block_threads: int = 256, loads_per_thread: int = 4,
+                   sentinel: int = 0x9E3779B9):
+    """Streaming read of the whole of `src` (a contiguous device tensor of a
+    multiple of 16 bytes); `sink` is a uint32 device tensor of at least
+    iq_stream_read_sink_words(...) words."""
+    if not isinstance(src, torch.Tensor) or src.device.type != "cuda" or not src.is_contiguous():
+        raise ValueError("src must be a contiguous device tensor")
+    if sink.dtype != torch.int32 or sink.device != src.device or not sink.is_contiguous():
+        raise ValueError("sink must be a contiguous int32 device tensor on src's device")
+    nbytes = src.numel() * src.element_size()
+    st = _lib.lib().iq_stream_read(_ptr(src), nbytes, _ptr(sink), sink.numel(), block_threads,
+                                   loads_per_thread, sentinel, _stream(src.device))
+    _lib.check("iq_stream_read", st)

@@ -410,7 +410,8 @@ size_t iq_decode_multi_workspace_bytes(int64_t batch, int64_t n_tokens, int64_t 
   if (n_tokens == 1)
     return iq_decode_workspace_bytes(batch, n_q_heads, n_kv_heads, max_seq_len, head_dim);
   if (head_dim != kDim || batch < 0 || n_tokens < 2 || n_tokens > 4 || n_kv_heads <= 0 ||
-      n_q_heads != 8 * n_kv_heads || max_seq_len < 0 || batch > 65535 || n_kv_heads > 65535)
+      n_q_heads != 8 * n_kv_heads || max_seq_len < 0 || batch > 65535 || n_kv_heads > 65535 ||
+      batch * n_tokens > 65535)   // the merge's grid takes (sequence, token) as one dimension
     return 0;
   int nb = 0;
   int64_t splits = 0, len = 0;
@@ -445,6 +446,8 @@ iq_status iq_decode_attention_multi(const float* q, const uint8_t* k_codes,
   if (shape != IQ_OK) return shape;
   if (!iq::mul_ok(batch, n_tokens) || !iq::mul_ok(batch * n_tokens, n_q_heads))
     return IQ_ERR_INVALID_ARGUMENT;
+  // the merge kernel's grid takes (sequence, token) as one dimension
+  if (batch * n_tokens > 65535) return IQ_ERR_UNSUPPORTED;
   const size_t need = iq_decode_multi_workspace_bytes(batch, n_tokens, n_q_heads, n_kv_heads,
                                                       max_seq_len, head_dim);
   if (need == 0) return IQ_ERR_INVALID_ARGUMENT;
@@ -691,6 +694,8 @@ iq_status iq_decode_attention_multi_paged(
   if (st != IQ_OK) return st;
   if (!iq::mul_ok(batch, n_tokens) || !iq::mul_ok(batch * n_tokens, n_q_heads))
     return IQ_ERR_INVALID_ARGUMENT;
+  // the merge kernel's grid takes (sequence, token) as one dimension
+  if (batch * n_tokens > 65535) return IQ_ERR_UNSUPPORTED;
   const size_t need = iq_decode_multi_workspace_bytes(batch, n_tokens, n_q_heads, n_kv_heads,
                                                       max_seq_len, head_dim);
   if (need == 0) return IQ_ERR_INVALID_ARGUMENT;

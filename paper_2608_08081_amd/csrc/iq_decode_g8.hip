@@ -273,9 +273,17 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   if constexpr (kAppend) if (split == n_splits) {
     // ---- the append workgroup ------------------------------------------------
     const int seq0 = seq_lens[b];
-    const bool appended = seq0 >= 0 && seq0 < capacity;
-    const bool attend_new = appended && seq0 < max_seq_len;
-    if (!appended && status != nullptr && g == 0 && tid == 0)
+    // record index of the new token (its page's slot, or the row position);
+    // -1 when there is no room: the sequence is at capacity, or (paged) the
+    // slot's page is not mapped.  Then nothing is written, the token is not
+    // attended, the capacity flag is raised, and the new-token partial's l
+    // entry carries -1 so that the merge leaves the length as it is.
+    const int64_t rec = !(seq0 >= 0 && seq0 < capacity)
+                            ? -1
+                            : (kPaged ? paged_record(pages, n_kv_heads, b, g, seq0) : row + seq0);
+    const bool written = rec >= 0;
+    const bool attend_new = written && seq0 < max_seq_len;
+    if (!written && status != nullptr && g == 0 && tid == 0)
       atomicOr(status, static_cast<int32_t>(IQ_ERR_CAPACITY));
     // waves 4 and 5 compress the new key and value: lane l holds dims 2l,
     // 2l + 1 and the parameters of SO(4) block l / 2
@@ -302,10 +310,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
       const int which = wave - 4;
       if (lane < 4 * kBits) sm.new_rec[which][lane] = wc.word;
       if (lane == 0) sm.new_scale[which] = wc.scale;
-      // record index of the new token (its page's slot, or the row position)
-      const int64_t rec =
-          !appended ? -1 : (kPaged ? paged_record(pages, n_kv_heads, b, g, seq0) : row + seq0);
-      if (rec >= 0) {
+      if (written) {
         uint8_t* codes = which == 0 ? k_codes : v_codes;
         float* norms = which == 0 ? k_norms : v_norms;
         if (lane < 4 * kBits) reinterpret_cast<uint32_t*>(codes + rec * kRB)[lane] = wc.word;
@@ -339,7 +344,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     float* pp = part_bg + static_cast<int64_t>(n_splits) * (kHeads * kPart) + qh * kPart;
     if (qblk == 0) {
       pp[0] = attend_new ? dot * sm.new_scale[0] : -INFINITY;
-      pp[1] = 1.0f;
+      pp[1] = written ? 1.0f : -1.0f;
     }
     *reinterpret_cast<f32x4_t*>(pp + 2 + md) = sm.new_scale[1] * v4;
     return;

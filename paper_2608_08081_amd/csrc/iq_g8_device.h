@@ -443,7 +443,8 @@ __device__ __forceinline__ void value_pairs(const uint32_t* lut, const uint32_t*
 // with nothing to attend carry m = -inf (their other entries are never read),
 // so the merge needs no sequence length.  kAppend: the last of the n_parts
 // partials is the new token's, and workgroup (b, head 0) then advances
-// seq_lens[b] past the token the decode kernel appended.
+// seq_lens[b] past the token the decode kernel appended, unless that
+// partial's l entry is negative (no room: nothing was written).
 //
 // kTok > 1 (multi-token decode): the partials of each split hold kTok
 // tokens' rows; grid (query head, sequence x token), output row (b, t).
@@ -463,7 +464,13 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
   const int tok = kTok == 1 ? 0 : bt % kTok;
   const int g = h / kHeads, hh = h % kHeads;
   int seq0 = 0;
-  if (kAppend && h == 0 && tid == 0) seq0 = seq_lens[b];
+  float written = 0.f;
+  if (kAppend && h == 0 && tid == 0) {
+    seq0 = seq_lens[b];
+    // the new-token partial of KV head 0 (every KV head shares the outcome)
+    written = partials[(static_cast<int64_t>(b) * n_kv_heads * n_parts + n_parts - 1) *
+                           (kHeads * kPart) + 1];
+  }
   const int sg = tid >> 5, dq = tid & 31;
   constexpr int kSplitStride = kTok * kHeads * kPart;
   const float* base = partials +
@@ -543,7 +550,8 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     *reinterpret_cast<f32x4_t*>(out + (static_cast<int64_t>(bt) * n_q_heads + h) * kDim +
                                 4 * tid) = r;
   }
-  if (kAppend && h == 0 && tid == 0 && seq0 >= 0 && seq0 < capacity) seq_lens[b] = seq0 + 1;
+  if (kAppend && h == 0 && tid == 0 && seq0 >= 0 && seq0 < capacity && written > 0.f)
+    seq_lens[b] = seq0 + 1;
 }
 
 }  // namespace

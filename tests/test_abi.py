@@ -347,6 +347,13 @@ def test_multi_token_validation():
     assert w2 > 0 and w4 >= 2 * w2 - 256
     assert L.iq_decode_multi_workspace_bytes(1, 5, 16, 2, 256, 128) == 0
     assert L.iq_decode_multi_workspace_bytes(1, 2, 8, 2, 256, 128) == 0
+    # the merge grid takes (sequence, token) as one dimension of <= 65535
+    assert L.iq_decode_multi_workspace_bytes(16383, 4, 16, 2, 256, 128) > 0
+    assert L.iq_decode_multi_workspace_bytes(16384, 4, 16, 2, 256, 128) == 0
+    assert L.iq_decode_multi_workspace_bytes(32767, 2, 16, 2, 256, 128) > 0
+    assert L.iq_decode_multi_workspace_bytes(32768, 2, 16, 2, 256, 128) == 0
+    assert call(b=16384, t=4) == 2
+    assert call(b=32768, t=2) == 2
 
 
 def test_step_bits_and_multi_paged_validation():
@@ -379,3 +386,18 @@ def test_step_bits_and_multi_paged_validation():
     assert mtp(hq=8) == 2
     assert mtp(wsb=16) == 3
     assert mtp(b=0) == 0
+    assert mtp(b=21846, t=3) == 2               # 65538 (sequence, token) rows
+
+
+def test_stream_read_validation():
+    """Argument checks of the streaming-read measurement kernel."""
+    def call(nbytes=4096, sink_words=1 << 20, block=256, loads=4, src=A, sink=A):
+        return L.iq_stream_read(src, nbytes, sink, sink_words, block, loads, 0, None)
+    assert call(block=96) == 1
+    assert call(loads=3) == 1
+    assert call(nbytes=4097) == 1
+    assert call(nbytes=0) == 0
+    assert call(src=None) == 1
+    assert L.iq_stream_read_sink_words(4096, 256, 4) == 1
+    assert L.iq_stream_read_sink_words(16384 * 3 + 16, 256, 4) == 4
+    assert call(nbytes=16384 * 3 + 16, sink_words=3) == 1

@@ -1,0 +1,173 @@
+"""GPU parity of the fused decode step (iq_decode_step) at the shapes and in
+the launch configurations bench.py times, against the oracle (App. A on the
+caches Alg. 1 produces, Table 2's per-step pipeline):
+
+* the 32K step: batch 1, 32 query heads, 4 KV heads, 32768 cached
+  positions, capacities the bench allocates for its default run and for a
+  20-step run; both take the one-round group-8 instance with 5 batches of
+  16 positions per wave and the append workgroup;
+* the batch-64 varlen step: 16 query heads, 2 KV heads, lengths drawn
+  uniform in [2048, 32768]; the several-round ("wide") instance with 5
+  batches per wave.
+
+Cache tails past every length are poisoned (random codes, NaN scales), so a
+read of a position that is not attended, or of the new position before it
+is written, shows up.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import bench
+from oracle import attention as oatt
+from oracle import codebook as ocb
+from oracle import compress as ocz
+from oracle import rotation as orot
+from paper_2608_08081_amd import api, synth
+from tests.parity import check_attention, check_codes, check_norms
+
+pytestmark = pytest.mark.gpu
+
+LEVELS, THR = ocb.isoquant_codebook(128, 3)
+DEV = torch.device("cuda:0")
+
+
+def _dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def g8_instance(batch, n_kv_heads, max_seq_len, append=True):
+    """The library's group-8 split plan (same rule as its planner): batches
+    of 16 positions per wave, splits per (sequence, KV head), and whether the
+    grid takes more than one round of 256 workgroups."""
+    cus, max_len = 256, 560
+    t = max(max_seq_len, 1)
+    bg = max(batch * n_kv_heads, 1)
+    s = -(-t // max_len)
+    wgs = bg * (s + 1)
+    if wgs <= 4 * cus:
+        rounds = -(-wgs // cus)
+        s_fill = rounds * cus // bg - 1
+        s_fill = min(s_fill, -(-t // 128))
+        s = max(s, s_fill)
+    ln = -(-t // s)
+    ln = -(-ln // 16) * 16
+    s = -(-t // ln)
+    nb = -(-(ln // 16) // 8)
+    parts = s + 1 if append else s
+    return nb, s, parts * batch * n_kv_heads > cus
+
+
+def _new_record_check(cache, k_new, v_new, quats, positions, label):
+    """Records the step wrote at positions[b], against the oracle's
+    compression of the same new key and value."""
+    rots = orot.rotation_matrices(quats)
+    for side, x in (("k", k_new), ("v", v_new)):
+        _, _, c, y, s = ocz.compress_kv(x[:, :, None, :], rots, THR)
+        got_c = np.stack([cache[f"{side}_codes"][b, :, p].cpu().numpy()
+                          for b, p in enumerate(positions)])[:, :, None]
+        got_s = np.stack([cache[f"{side}_norms"][b, :, p].cpu().numpy()
+                          for b, p in enumerate(positions)])[:, :, None]
+        check_codes(got_c, c, y, THR, f"{label} new {side}")
+        check_norms(got_s, s, f"{label} new {side} scale")
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("warmup,steps", [(480, 4800), (5, 20)])
+def test_step_32k_bench_instance(warmup, steps):
+    w = synth.WORKLOADS[2]
+    ctx = 32768
+    cap = bench.cache_capacity(ctx, warmup, steps, 48)
+    nb, splits, wide = g8_instance(1, w.n_kv_heads, cap)
+    assert (nb, wide) == (5, False), (nb, splits, wide)
+    n_steps = 3
+    seed = 21
+    k = synth.kv_tensor(seed, w, "k", n_tokens=ctx + n_steps)
+    v = synth.kv_tensor(seed, w, "v", n_tokens=ctx + n_steps)
+    qs = synth.queries(seed, w, n_steps)
+    quats = orot.make_quaternions(w.rotation_seed, w.n_kv_heads)
+    rots = orot.rotation_matrices(quats)
+    kp, kn, *_ = ocz.compress_kv(k, rots, THR)
+    vp, vn, *_ = ocz.compress_kv(v, rots, THR)
+    rng = np.random.default_rng(seed)
+    shape = (1, w.n_kv_heads, cap)
+    gk = rng.integers(0, 256, size=shape + (48,), dtype=np.uint8)
+    gv = rng.integers(0, 256, size=shape + (48,), dtype=np.uint8)
+    gkn = np.full(shape, np.nan, np.float32)
+    gvn = np.full(shape, np.nan, np.float32)
+    gk[:, :, :ctx], gv[:, :, :ctx] = kp[:, :, :ctx], vp[:, :, :ctx]
+    gkn[:, :, :ctx], gvn[:, :, :ctx] = kn[:, :, :ctx], vn[:, :, :ctx]
+    cache = dict(k_codes=_dev(gk), k_norms=_dev(gkn), v_codes=_dev(gv), v_norms=_dev(gvn),
+                 seq_lens=_dev(np.asarray([ctx], np.int32)))
+    qt = _dev(quats)
+    ws = api.alloc_workspace(1, w.n_q_heads, w.n_kv_heads, cap, DEV)
+    for s in range(n_steps):
+        pos = ctx + s
+        k_new, v_new = k[:, :, pos], v[:, :, pos]
+        out = api.iq_decode_step(_dev(qs[s]), _dev(k_new), _dev(v_new), cache["k_codes"],
+                                 cache["k_norms"], cache["v_codes"], cache["v_norms"],
+                                 cache["seq_lens"], qt, workspace=ws, max_seq_len=cap)
+        torch.cuda.synchronize()
+        assert int(cache["seq_lens"].item()) == pos + 1
+        _new_record_check(cache, k_new, v_new, quats, [pos], f"32k step {s}")
+        ref = oatt.decode_fused(qs[s], kp, kn, vp, vn, [pos + 1], quats, LEVELS)
+        check_attention(out.cpu().numpy(), ref, f"32k cap {cap} step {s}")
+
+
+@pytest.mark.timeout(900)
+def test_step_varlen_bench_instance():
+    w = synth.WORKLOADS[3]
+    seed = 0
+    lens = synth.context_lengths(seed, w)
+    cap = bench.cache_capacity(int(lens.max()), 24, 240, 3)
+    nb, splits, wide = g8_instance(w.batch, w.n_kv_heads, cap)
+    assert (nb, wide) == (5, True), (nb, splits, wide)
+    quats = orot.make_quaternions(w.rotation_seed, w.n_kv_heads)
+    qt = _dev(quats)
+    cache = api.alloc_cache(w.batch, w.n_kv_heads, cap, DEV)
+    # keys and values to the longest length + 1 (the new token of sequence
+    # b is position lens[b]), compressed on the device in slices
+    t_all = int(lens.max()) + 1
+    k = synth.kv_tensor(seed, w, "k", n_tokens=t_all)
+    v = synth.kv_tensor(seed, w, "v", n_tokens=t_all)
+    for b0 in range(0, w.batch, 16):
+        api.iq_compress_kv(_dev(k[b0:b0 + 16]), _dev(v[b0:b0 + 16]), qt,
+                           cache["k_codes"][b0:b0 + 16], cache["k_norms"][b0:b0 + 16],
+                           cache["v_codes"][b0:b0 + 16], cache["v_norms"][b0:b0 + 16])
+    # poison every position at or past each length
+    pos_idx = torch.arange(cap, device=DEV)[None, None, :]
+    tail = pos_idx >= _dev(lens.astype(np.int64))[:, None, None]
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(5)
+    for side in ("k", "v"):
+        junk = torch.randint(0, 256, cache[f"{side}_codes"].shape, generator=gen, device=DEV,
+                             dtype=torch.uint8)
+        cache[f"{side}_codes"].copy_(torch.where(tail[..., None], junk,
+                                                 cache[f"{side}_codes"]))
+        cache[f"{side}_norms"].masked_fill_(tail, float("nan"))
+        del junk
+    cache["seq_lens"].copy_(torch.from_numpy(lens))
+    bidx = np.arange(w.batch)
+    k_new = np.ascontiguousarray(k[bidx, :, lens])
+    v_new = np.ascontiguousarray(v[bidx, :, lens])
+    q = synth.queries(seed, w)[0]
+    out = api.iq_decode_step(_dev(q), _dev(k_new), _dev(v_new), cache["k_codes"],
+                             cache["k_norms"], cache["v_codes"], cache["v_norms"],
+                             cache["seq_lens"], qt, max_seq_len=cap)
+    torch.cuda.synchronize()
+    assert cache["seq_lens"].cpu().numpy().tolist() == (lens + 1).tolist()
+    _new_record_check(cache, k_new, v_new, quats, lens.tolist(), "varlen")
+    got = out.cpu().numpy()
+    assert np.all(np.isfinite(got))
+    rots = orot.rotation_matrices(quats)
+    sample = sorted({int(np.argmin(lens)), int(np.argmax(lens))} |
+                    set(np.random.default_rng(17).choice(w.batch, 6, replace=False).tolist()))
+    for b in sample:
+        n = int(lens[b]) + 1
+        kp, kn, kc, ky, _ = ocz.compress_kv(k[b:b + 1, :, :n], rots, THR)
+        vp, vn, *_ = ocz.compress_kv(v[b:b + 1, :, :n], rots, THR)
+        check_codes(cache["k_codes"][b:b + 1, :, :n].cpu().numpy(), kc, ky, THR,
+                    f"varlen b{b} k")
+        ref = oatt.decode_fused(q[b:b + 1], kp, kn, vp, vn, [n], quats, LEVELS)
+        check_attention(got[b:b + 1], ref, f"varlen b{b} len {n}")

@@ -138,6 +138,53 @@ def test_paged_step_equals_contiguous(lens, hkv, page, cap):
             assert torch.equal(pool[f"{side}_norms"][p, :, slot], cache[f"{side}_norms"][s, :, n])
 
 
+@pytest.mark.parametrize("lens,hkv,page,cap", [
+    ([128, 100], 2, 64, 256),                                    # one-round grid
+    ([128] + [int(x) for x in np.linspace(0, 1000, 39)], 4, 64, 1024),  # several rounds
+])
+def test_paged_step_unmapped_append_slot(lens, hkv, page, cap):
+    """A fused step whose new position lies on an unmapped page (sequence 0,
+    length on a page boundary, that page's entry -1): nothing is written to
+    the pools, the token is not attended, the length stays and the capacity
+    flag is raised; the other sequences step as usual."""
+    w = synth.Workload(98, "paged_u", len(lens), 8 * hkv, hkv, cap, "f16", rotation_seed=1098)
+    cache, quats, _, _ = _filled(w, lens, cap, 12)
+    max_pages = cap // page
+    n_pages = len(lens) * max_pages + 1
+    tables = _tables(lens, page, max_pages, n_pages, 5)
+    assert lens[0] % page == 0
+    tables[0, lens[0] // page] = -1
+    pool = _scatter(cache, tables, page, n_pages)
+    before = {k: t.clone() for k, t in pool.items()}
+    bt = torch.from_numpy(tables).to(DEV)
+    seq_p = cache["seq_lens"].clone()
+    kn_new, vn_new = synth.appended_tokens(12, w, 1)
+    k_new, v_new = torch.from_numpy(kn_new[0]).to(DEV), torch.from_numpy(vn_new[0]).to(DEV)
+    q = torch.from_numpy(synth.queries(12, w)[0]).to(DEV)
+    # reference: sequence 0 attends its cache as it is, the others step
+    ref0 = api.iq_decode_attention(q, cache["k_codes"], cache["k_norms"], cache["v_codes"],
+                                   cache["v_norms"], cache["seq_lens"], quats, max_seq_len=cap)
+    ref = api.iq_decode_step(q, k_new, v_new, cache["k_codes"], cache["k_norms"],
+                             cache["v_codes"], cache["v_norms"], cache["seq_lens"], quats,
+                             max_seq_len=cap)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    got = api.iq_decode_step_paged(q, k_new, v_new, pool, bt, seq_p, quats, max_seq_len=cap,
+                                   status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 5
+    want_lens = [lens[0]] + [n + 1 for n in lens[1:]]
+    assert seq_p.cpu().numpy().tolist() == want_lens
+    err0 = (got[0] - ref0[0]).abs().max() / ref0[0].abs().max()
+    assert float(err0) < 1e-5, float(err0)
+    assert torch.equal(got[1:], ref[1:])
+    # the pools changed only at the other sequences' new slots
+    touched = {(int(tables[s, n // page]), n % page) for s, n in enumerate(lens) if s > 0}
+    for side in ("k", "v"):
+        diff = (pool[f"{side}_norms"].view(torch.int32) !=
+                before[f"{side}_norms"].view(torch.int32)).nonzero().cpu().numpy()
+        assert {(int(p), int(sl)) for p, _, sl in diff} <= touched
+
+
 def test_paged_compress_equals_contiguous():
     """Bulk compression into the pools writes the records the contiguous
     compression writes, at the mapped pages; unmapped pages stay untouched."""
