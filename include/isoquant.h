@@ -18,7 +18,9 @@
  * - Device pointers are plain HIP device allocations owned by the caller.
  *   The library never allocates, frees or retains device memory and keeps no
  *   mutable global state (the codebook is an immutable constant computed once
- *   per process on first use), so calls are thread-safe.
+ *   per process on first use), so calls are thread-safe.  The one exception
+ *   is iq_decode_step_noalloc, whose scratch is a static device array of the
+ *   library (one per GPU, shared by every call of that entry point).
  * - Every device entry point is asynchronous on `stream` (0 = the null
  *   stream) and never synchronizes.  Arguments are validated on the host
  *   before any HIP call; on a validation error nothing is launched.
@@ -280,6 +282,34 @@ iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, i
                          int64_t n_kv_heads, int64_t head_dim, float softmax_scale, float* out,
                          void* workspace, size_t workspace_bytes, int32_t* status_dev,
                          hipStream_t stream);
+
+/*
+ * iq_decode_step_noalloc - iq_decode_step without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).  The split
+ * partials go to a static device array of IQ_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every GPU it runs on until the process ends; nothing is
+ * allocated or freed by the call.  The array's device address is looked up
+ * (hipGetSymbolAddress) on the first call made with each device current,
+ * before the arguments are checked.
+ *
+ * Arguments, results and errors as for iq_decode_step; shapes whose
+ * workspace (iq_decode_workspace_bytes) exceeds IQ_NOALLOC_SCRATCH_BYTES
+ * return IQ_ERR_WORKSPACE_TOO_SMALL (the 64 MiB hold, e.g., batch 64 with 16
+ * query and 2 KV heads at 33K positions, 34.6 MB).  Every call on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (other streams, other host threads) race
+ * and must be serialized by the caller.  The array needs no clearing (every
+ * byte a call reads was written earlier in the same call).
+ */
+#define IQ_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+iq_status iq_decode_step_noalloc(const float* q, const void* k_new, const void* v_new,
+                                 iq_dtype dtype, uint8_t* k_codes, float* k_norms,
+                                 uint8_t* v_codes, float* v_norms, int32_t* seq_lens,
+                                 int64_t capacity, int64_t max_seq_len, const float* quats,
+                                 int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                                 int64_t head_dim, float softmax_scale, float* out,
+                                 int32_t* status_dev, hipStream_t stream);
 
 /*
  * Paged cache (serving with page pools)

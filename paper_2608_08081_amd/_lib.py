@@ -85,6 +85,9 @@ _SIGNATURES = {
     "iq_decode_f16_workspace_bytes": (_c_size, [_c_i64, _c_i64, _c_i64, _c_i64, _c_i64]),
     "iq_decode_attention_f16": (_c_int, [_vp, _vp, _vp, _vp, _c_i64, _c_i64, _c_i64, _c_i64,
                                          _c_i64, _c_i64, _c_float, _vp, _vp, _c_size, _vp]),
+    "iq_decode_step_noalloc": (_c_int, [_vp, _vp, _vp, _c_int, _vp, _vp, _vp, _vp, _vp,
+                                        _c_i64, _c_i64, _vp, _c_i64, _c_i64, _c_i64, _c_i64,
+                                        _c_float, _vp, _vp, _vp]),
     "iq_stream_read_sink_words": (_c_size, [_c_size, ctypes.c_int32, ctypes.c_int32]),
     "iq_stream_read": (_c_int, [_vp, _c_size, _vp, _c_size, ctypes.c_int32, ctypes.c_int32,
                                 ctypes.c_uint32, _vp]),

@@ -348,6 +348,26 @@ def iq_decode_step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens
                  workspace, max_seq_len, softmax_scale, status, 3)
 
 
+def iq_decode_step_noalloc(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                           quats, out, max_seq_len=None, softmax_scale: float = 0.0,
+                           status=None):
+    """iq_decode_step with its split partials in the library's static device
+    scratch (no workspace; nothing allocated by the call, `out` is the
+    caller's).  Shapes whose workspace exceeds the scratch raise."""
+    b, hq, hkv, cap = _step_shapes(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms,
+                                   seq_lens, quats, status, 3)
+    dev = q.device
+    if max_seq_len is None:
+        max_seq_len = cap
+    _require(out, "out", torch.float32, (b, hq, HEAD_DIM), dev)
+    st = _lib.lib().iq_decode_step_noalloc(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _dtype_code(k_new), _ptr(k_codes), _ptr(k_norms),
+        _ptr(v_codes), _ptr(v_norms), _ptr(seq_lens), cap, max_seq_len, _ptr(quats), b, hq, hkv,
+        HEAD_DIM, float(softmax_scale), _ptr(out), _ptr(status), _stream(dev))
+    _lib.check("iq_decode_step_noalloc", st)
+    return out
+
+
 def iq_decode_step_bits(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats,
                         out=None, workspace=None, max_seq_len=None, softmax_scale: float = 0.0,
                         status=None, bits: int = 3):
@@ -356,8 +376,10 @@ def iq_decode_step_bits(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq
                  workspace, max_seq_len, softmax_scale, status, bits)
 
 
-def _step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out, workspace,
-          max_seq_len, softmax_scale, status, bits):
+def _step_shapes(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, status,
+                 bits):
+    """Checks of a fused step's tensors; returns (batch, n_q_heads,
+    n_kv_heads, capacity)."""
     if q.dim() != 3 or q.shape[-1] != HEAD_DIM:
         raise ValueError("q must be [batch][n_q_heads][128]")
     b, hq, _ = q.shape
@@ -376,6 +398,14 @@ def _step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, 
     _require(quats, "quats", torch.float32, (hkv, 32, 2, 4), dev)
     if status is not None:
         _require(status, "status", torch.int32, (1,), dev)
+    return b, hq, hkv, cap
+
+
+def _step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out, workspace,
+          max_seq_len, softmax_scale, status, bits):
+    b, hq, hkv, cap = _step_shapes(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms,
+                                   seq_lens, quats, status, bits)
+    dev = q.device
     if max_seq_len is None:
         max_seq_len = cap
     if out is None:

@@ -18,7 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libisoquant.so"
 SOURCES = ["iq_api.cpp", "iq_fit.cpp", "iq_compress.hip", "iq_decode.hip", "iq_decode_g8.hip",
-           "iq_decode_multi.hip", "iq_dequant.hip", "iq_decode_f16.hip", "iq_measure.hip"]
+           "iq_decode_multi.hip", "iq_dequant.hip", "iq_decode_f16.hip", "iq_measure.hip",
+           "iq_noalloc.hip"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [
