@@ -69,7 +69,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--workload", choices=("step32k", "varlen", "compress", "append8k",
                                           "baseline32k", "rotation_fit", "paged", "bits32k",
-                                          "multi32k"),
+                                          "multi32k", "tiny1k"),
                    default="step32k")
     p.add_argument("--steps", type=int, default=None,
                    help="timed steps (default: 4800; varlen 240; compress 20; append8k 1000)")
@@ -93,7 +93,7 @@ def parse():
     defaults = {"step32k": (4800, 48), "varlen": (240, 3), "compress": (20, 1),
                 "append8k": (1000, 48), "baseline32k": (960, 48),
                 "rotation_fit": (1, 1), "paged": (240, 3), "bits32k": (960, 48),
-                "multi32k": (960, 48)}[a.workload]
+                "multi32k": (960, 48), "tiny1k": (960, 48)}[a.workload]
     if a.steps is None:
         a.steps = defaults[0]
     if a.warmup is None:
@@ -604,6 +604,75 @@ def run_append8k(args, torch, api, synth, dev):
         "appended tokens' inputs and records")
 
 
+def run_tiny1k(args, torch, api, synth, dev):
+    """The single-head workload: batch 1, one query and one KV head (group 1,
+    the generic split-K path on the vector units), 1024 fp32 keys and values
+    compressed (iq_compress_kv), then one decode-attention call over them
+    (iq_decode_attention), each timed over --layers distinct layers cycled
+    (time_graph_calls).  Both are latency-bound at this size."""
+    w = synth.WORKLOADS[0]
+    nl = args.layers
+    t = w.context
+    quats = api.iq_make_rotation(w.rotation_seed, 1).to(dev)
+    layers = []
+    for li in range(nl):
+        g = torch.Generator(device=dev)
+        g.manual_seed(args.seed * 100003 + li)
+        sc = [torch.from_numpy(synth.channel_scales(synth.rng(args.seed + li, w.wid, s), 1))
+              .to(dev) for s in (0, 1)]
+        k = torch.randn((1, 1, t, 128), generator=g, device=dev) * sc[0][None, :, None, :]
+        v = torch.randn((1, 1, t, 128), generator=g, device=dev) * sc[1][None, :, None, :]
+        cache = api.alloc_cache(1, 1, t, dev)
+        cache["seq_lens"].fill_(t)
+        q = torch.randn((1, 1, 128), generator=g, device=dev)
+        layers.append(dict(k=k, v=v, cache=cache, q=q, out=torch.empty((1, 1, 128), device=dev)))
+    ws = api.alloc_workspace(1, 1, 1, t, dev)
+
+    def compress(li):
+        L = layers[li]
+        c = L["cache"]
+        api.iq_compress_kv(L["k"], L["v"], quats, c["k_codes"], c["k_norms"], c["v_codes"],
+                           c["v_norms"])
+
+    def decode(li):
+        L = layers[li]
+        c = L["cache"]
+        api.iq_decode_attention(L["q"], c["k_codes"], c["k_norms"], c["v_codes"], c["v_norms"],
+                                c["seq_lens"], quats, out=L["out"], workspace=ws,
+                                max_seq_len=t)
+
+    us_c, _ = time_graph_calls(torch, compress, nl, args.steps, args.warmup)
+    us_d, _ = time_graph_calls(torch, decode, nl, args.steps, args.warmup)
+    dec_bytes = t * BYTES_PER_TOKEN_HEAD
+    comp_bytes = 2 * t * (128 * 4 + RECORD + 4)
+    value = dec_bytes / (us_d * 1e-6) / 1e9
+    return {
+        "metric": "single-head decode-attention µs/call + achieved HBM GB/s on packed 3-bit KV, "
+                  "1K ctx",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(us_d / 1e3, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u3 codes, f32 accumulate",
+        "data": "synthetic (seeded anisotropic fp32 K/V, compressed on device)",
+        "config": {"workload": f"batch 1, 1 query head, 1 KV head (group 1: generic path), "
+                               f"head_dim 128, {t} fp32 keys and values; {nl} distinct layers "
+                               "cycled", "context": t},
+        "roofline": {"bound": "hbm", "achieved": round(value, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(value / HBM_PEAK_GBS, 5), "traffic": None,
+                     "kernel": "decode_split_kernel + decode_combine_kernel",
+                     "bytes_per_launch": dec_bytes, "launch_us": round(us_d, 3)},
+        "compress": {"us_per_call": round(us_c, 3), "bytes": comp_bytes,
+                     "gbs": round(comp_bytes / (us_c * 1e-6) / 1e9, 2),
+                     "kernel": "compress_kernel<float, false, 3>"},
+    }
+
+
 def run_bits32k(args, torch, api, synth, dev):
     """Decode attention at the 32K shape on caches of b-bit records (Algorithm
     1 with C_b; b = 2, 3, 4, each its own set of layer caches compressed from
@@ -962,7 +1031,9 @@ def run_rotation_fit(args, torch, api, synth, dev):
     """Fit the SO(4) blocks on calibration keys (host), then measure the
     held-out relative squared error ||x - x_hat||^2 / ||x||^2 of keys
     compressed (iq_compress_kv) and materialized (iq_dequantize_kv) on the
-    GPU with each parameter set.  A quality figure, not a throughput."""
+    GPU with each parameter set, and with codebooks fitted to the same
+    calibration keys (iq_fit_codebook, iq_compress_kv_cb,
+    iq_dequantize_kv_cb).  A quality figure, not a throughput."""
     n_heads, n_cal, n_held = 4, 4096, 32768
     w = synth.Workload(96, "rotation_fit", 1, 8 * n_heads, n_heads, n_cal + n_held, "f16")
     k = synth.kv_tensor(args.seed, w, "k")                      # [1][H][T][d] fp16
@@ -978,14 +1049,30 @@ def run_rotation_fit(args, torch, api, synth, dev):
     x = held.float()
     x2 = (x * x).sum(-1)
     res = {}
-    for name, q in params.items():
+
+    def distortion(q, codebook=None):
         qd = q.to(dev)
         cache = api.alloc_cache(1, n_heads, n_held, dev, values=False)
-        api.iq_compress_kv(held, None, qd, cache["k_codes"], cache["k_norms"], None, None)
+        if codebook is None:
+            api.iq_compress_kv(held, None, qd, cache["k_codes"], cache["k_norms"], None, None)
+        else:
+            api.iq_compress_kv_cb(held, None, qd, codebook, cache["k_codes"], cache["k_norms"],
+                                  None, None)
         xh, _ = api.iq_dequantize_kv(cache["k_codes"], cache["k_norms"], None, None, qd,
-                                     out_dtype=torch.float32)
+                                     out_dtype=torch.float32, codebook=codebook)
         err = ((x - xh) ** 2).sum(-1) / x2
-        res[name] = round(float(err.mean()), 6)
+        return round(float(err.mean()), 6)
+
+    for name, q in params.items():
+        res[name] = distortion(q)
+    # codebooks fitted (iq_fit_codebook) on the same calibration keys, under
+    # the fitted and the random block parameters
+    t0 = time.perf_counter()
+    cb_fitted = api.iq_fit_codebook(cal, fitted, bits=3)
+    cb_fit_s = time.perf_counter() - t0
+    cb_random = api.iq_fit_codebook(cal, params["random_so4"], bits=3)
+    res["fitted+fitted_codebook"] = distortion(fitted, cb_fitted)
+    res["random_so4+fitted_codebook"] = distortion(params["random_so4"], cb_random)
     torch.cuda.synchronize()
     return {
         "metric": "held-out 3-bit relative squared error of keys, fitted vs random SO(4) blocks",
@@ -1003,6 +1090,8 @@ def run_rotation_fit(args, torch, api, synth, dev):
                                f"keys per head, head_dim 128, 4 fitting sweeps"},
         "distortion": res,
         "fit_seconds_host": round(fit_s, 3),
+        "codebook_fit_seconds_host": round(cb_fit_s, 3),
+        "fitted_codebook_levels": [round(float(x), 7) for x in api.codebook_arrays(cb_fitted)[0]],
     }
 
 
@@ -1031,7 +1120,7 @@ def main():
     run = {"step32k": run_step32k, "varlen": run_varlen, "compress": run_compress,
            "append8k": run_append8k, "baseline32k": run_baseline32k,
            "rotation_fit": run_rotation_fit, "paged": run_paged,
-           "bits32k": run_bits32k, "multi32k": run_multi32k}[args.workload]
+           "bits32k": run_bits32k, "multi32k": run_multi32k, "tiny1k": run_tiny1k}[args.workload]
     print(json.dumps(run(args, torch, api, synth, dev)), flush=True)
 
 

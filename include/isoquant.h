@@ -552,6 +552,89 @@ iq_status iq_decode_attention_multi_paged(const float* q,
                                           hipStream_t stream);
 
 /*
+ * Fitted codebooks (Sec. 3.2 Step 3 on calibration data)
+ * ------------------------------------------------------
+ * Step 3 quantizes with the Lloyd-Max levels of the marginal of one rotated
+ * coordinate; the library's C_b reads that marginal analytically (the sphere
+ * marginal, iq_codebook).  The paper also counts codebook entries among the
+ * method's fitted parameters ("Why structured rotation works").  These entry
+ * points fit the levels to measured data and run compression, decode and
+ * the fused step with such a codebook.  A codebook is passed by host pointer
+ * (read during the call, not retained):
+ *   bits       : 2, 3 or 4;
+ *   levels     : the first 2^bits entries, strictly ascending, each exactly
+ *                representable in fp16, |level| < 1 (levels of the
+ *                normalized, rotated coordinate), and symmetric:
+ *                levels[i] == -levels[2^bits - 1 - i];
+ *   thresholds : the first 2^bits - 1 entries, exactly the fp32 midpoints
+ *                of adjacent levels.
+ * Anything else returns IQ_ERR_INVALID_ARGUMENT (IQ_ERR_UNSUPPORTED for
+ * bits).  A cache written with one codebook must be decoded with the same
+ * codebook; the record layout is that of the *_bits entry points.
+ */
+typedef struct iq_codebook_t {
+  int32_t bits;
+  float levels[16];
+  float thresholds[15];
+} iq_codebook_t;
+
+/*
+ * iq_fit_codebook - Lloyd-Max levels of the empirical distribution of the
+ * rotated, normalized calibration coordinates y = R x / ||x|| (Eq. 2, R from
+ * quats_host, the parameters the cache will be written with): the sample of
+ * every coordinate of every non-zero finite calibration vector of every
+ * head, together with its negation (the marginal is symmetric, and the
+ * compression quantizer relies on it); Lloyd's iteration (thresholds =
+ * midpoints, level = mean of its cell, cell j = {t_(j-1) <= y < t_j}, an
+ * empty cell keeps its level) from C_b until no cell changes; levels then
+ * rounded to the nearest fp16 value and made exactly symmetric, thresholds
+ * their midpoints.  Host memory: calib[n_kv_heads][n_vectors][128] fp32,
+ * quats_host[n_kv_heads][32][2][4], *out written on success.
+ * 1 <= n_vectors, n_vectors * n_kv_heads <= 2^24.  IQ_ERR_INVALID_ARGUMENT
+ * also when no calibration vector is usable.  Pure host function.
+ */
+iq_status iq_fit_codebook(const float* calib, int64_t n_vectors, int64_t n_kv_heads,
+                          int64_t head_dim, const float* quats_host, int32_t bits,
+                          iq_codebook_t* out);
+
+/* iq_compress_kv with codebook *cb: records of cb->bits bits (layout of
+ * iq_compress_kv_bits). */
+iq_status iq_compress_kv_cb(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+                            int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
+                            const float* quats, const iq_codebook_t* cb, uint8_t* k_codes,
+                            float* k_norms, uint8_t* v_codes, float* v_norms, int64_t capacity,
+                            int64_t dst_offset, hipStream_t stream);
+
+/* iq_decode_attention on records written with codebook *cb (paths and
+ * restrictions of iq_decode_attention_bits at cb->bits). */
+iq_status iq_decode_attention_cb(const float* q, const uint8_t* k_codes, const float* k_norms,
+                                 const uint8_t* v_codes, const float* v_norms,
+                                 const int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                                 const float* quats, const iq_codebook_t* cb, int64_t batch,
+                                 int64_t n_q_heads, int64_t n_kv_heads, int64_t head_dim,
+                                 float softmax_scale, float* out, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream);
+
+/* iq_decode_step with codebook *cb for the new records and the attention
+ * (restrictions of iq_decode_step_bits at cb->bits). */
+iq_status iq_decode_step_cb(const float* q, const void* k_new, const void* v_new,
+                            iq_dtype dtype, uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
+                            float* v_norms, int32_t* seq_lens, int64_t capacity,
+                            int64_t max_seq_len, const float* quats, const iq_codebook_t* cb,
+                            int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                            int64_t head_dim, float softmax_scale, float* out, void* workspace,
+                            size_t workspace_bytes, int32_t* status_dev, hipStream_t stream);
+
+/* iq_dequantize_kv of records written with codebook *cb (3-bit codebooks
+ * only; IQ_ERR_UNSUPPORTED otherwise). */
+iq_status iq_dequantize_kv_cb(const uint8_t* k_codes, const float* k_norms,
+                              const uint8_t* v_codes, const float* v_norms, const float* quats,
+                              const iq_codebook_t* cb, const int32_t* seq_lens, int64_t batch,
+                              int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
+                              int64_t capacity, int64_t src_offset, iq_dtype out_dtype,
+                              void* k_out, void* v_out, hipStream_t stream);
+
+/*
  * Measurement support (not part of the method)
  * ---------------------------------------------
  * The decode step is bound by HBM bandwidth (its algorithmic bytes are the

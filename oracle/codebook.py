@@ -161,3 +161,57 @@ def isoquant_codebook(d: int = 128, bits: int = 3):
         raise AssertionError("stored codebook is not symmetric")
     thresholds = 0.5 * (stored[:-1] + stored[1:])
     return stored, thresholds
+
+
+# --------------------------------------------------------------------------
+# Empirical codebook (Sec. 3.2 Step 3 on calibration data)
+# --------------------------------------------------------------------------
+
+def rotated_coordinates(x, rot):
+    """Post-rotation coordinates of calibration vectors: R x / ||x|| in fp64
+    for every non-zero finite row of x ([n][d]); rot is the d x d matrix R of
+    Eq. 2 (rotation.rotation_matrix).  Returns [m][d]."""
+    x = np.asarray(x, dtype=np.float64)
+    n2 = np.einsum("nd,nd->n", x, x)
+    keep = np.isfinite(n2) & (n2 > 0)
+    x = x[keep]
+    return (x / np.sqrt(n2[keep])[:, None]) @ np.asarray(rot, np.float64).T
+
+
+def empirical_lloyd_max(samples, n_levels: int, init, max_iter: int = 10000):
+    """Lloyd's iteration on the empirical distribution of `samples` made
+    symmetric (the sample and its negation), the fixed point the paper's
+    Step 3 asks for when the marginal is measured instead of derived.
+
+    Cells follow the coding rule of the pipeline: cell j holds the values y
+    with t_(j-1) <= y < t_j.  thresholds <- midpoints of adjacent levels;
+    levels <- mean of the sample values in each cell (an empty cell keeps
+    its level).  On a finite sample the cells stop changing after finitely
+    many steps and the levels are then exact fixed points.
+    Returns (levels, thresholds), unrounded fp64."""
+    y = np.asarray(samples, dtype=np.float64).ravel()
+    y = np.sort(np.concatenate([y, -y]))
+    c = np.array(init, dtype=np.float64)
+    for _ in range(max_iter):
+        t = 0.5 * (c[:-1] + c[1:])
+        cells = np.split(y, np.searchsorted(y, t, side="left"))
+        c_new = np.array([cell.mean() if cell.size else c[j] for j, cell in enumerate(cells)])
+        if np.array_equal(c_new, c):
+            break
+        c = c_new
+    else:
+        raise RuntimeError("empirical Lloyd-Max did not reach a fixed point")
+    return c, 0.5 * (c[:-1] + c[1:])
+
+
+def empirical_isoquant_codebook(samples, bits: int = 3, d: int = 128):
+    """A fitted codebook in the library's storage format: empirical
+    Lloyd-Max levels (started from the sphere-marginal levels) rounded to
+    the nearest half-precision value, made exactly symmetric, thresholds the
+    midpoints of the stored levels.  Also returns the unrounded levels."""
+    init, _ = sphere_codebook(d, bits)
+    levels, _ = empirical_lloyd_max(samples, 2 ** bits, init)
+    stored = levels.astype(np.float16).astype(np.float64)
+    n = stored.size
+    stored[: n // 2] = -stored[::-1][: n // 2]
+    return stored, 0.5 * (stored[:-1] + stored[1:]), levels

@@ -33,6 +33,15 @@ _vp = ctypes.c_void_p
 _c_size = ctypes.c_size_t
 _c_float = ctypes.c_float
 
+class IqCodebook(ctypes.Structure):
+    """iq_codebook_t: bits, then the first 2^bits levels and 2^bits - 1
+    thresholds of fixed-size arrays."""
+    _fields_ = [("bits", ctypes.c_int32), ("levels", ctypes.c_float * 16),
+                ("thresholds", ctypes.c_float * 15)]
+
+
+_cbp = ctypes.POINTER(IqCodebook)
+
 _SIGNATURES = {
     "iq_status_string": (ctypes.c_char_p, [_c_int]),
     "iq_version": (_c_int, []),
@@ -88,6 +97,17 @@ _SIGNATURES = {
     "iq_decode_step_noalloc": (_c_int, [_vp, _vp, _vp, _c_int, _vp, _vp, _vp, _vp, _vp,
                                         _c_i64, _c_i64, _vp, _c_i64, _c_i64, _c_i64, _c_i64,
                                         _c_float, _vp, _vp, _vp]),
+    "iq_fit_codebook": (_c_int, [_vp, _c_i64, _c_i64, _c_i64, _vp, ctypes.c_int32, _cbp]),
+    "iq_compress_kv_cb": (_c_int, [_vp, _vp, _c_int, _c_i64, _c_i64, _c_i64, _c_i64, _vp, _cbp,
+                                   _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp]),
+    "iq_decode_attention_cb": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp, _cbp,
+                                        _c_i64, _c_i64, _c_i64, _c_i64, _c_float, _vp, _vp,
+                                        _c_size, _vp]),
+    "iq_decode_step_cb": (_c_int, [_vp, _vp, _vp, _c_int, _vp, _vp, _vp, _vp, _vp, _c_i64,
+                                   _c_i64, _vp, _cbp, _c_i64, _c_i64, _c_i64, _c_i64, _c_float,
+                                   _vp, _vp, _c_size, _vp, _vp]),
+    "iq_dequantize_kv_cb": (_c_int, [_vp, _vp, _vp, _vp, _vp, _cbp, _vp, _c_i64, _c_i64, _c_i64,
+                                     _c_i64, _c_i64, _c_i64, _c_int, _vp, _vp, _vp]),
     "iq_stream_read_sink_words": (_c_size, [_c_size, ctypes.c_int32, ctypes.c_int32]),
     "iq_stream_read": (_c_int, [_vp, _c_size, _vp, _c_size, ctypes.c_int32, ctypes.c_int32,
                                 ctypes.c_uint32, _vp]),

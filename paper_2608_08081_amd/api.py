@@ -74,6 +74,48 @@ def iq_codebook_bits(bits: int):
     return lv, th
 
 
+def make_codebook(levels, thresholds=None):
+    """An iq_codebook_t from 2^b levels (thresholds default to the fp32
+    midpoints of adjacent levels).  The library validates it on use."""
+    lv = np.asarray(levels, dtype=np.float64)
+    n = lv.size
+    bits = {4: 2, 8: 3, 16: 4}.get(n)
+    if bits is None:
+        raise ValueError("a codebook has 4, 8 or 16 levels")
+    th = (0.5 * (lv[:-1] + lv[1:]) if thresholds is None
+          else np.asarray(thresholds, dtype=np.float64))
+    cb = _lib.IqCodebook()
+    cb.bits = bits
+    for i in range(n):
+        cb.levels[i] = float(np.float32(lv[i]))
+    for i in range(n - 1):
+        cb.thresholds[i] = float(np.float32(th[i]))
+    return cb
+
+
+def codebook_arrays(cb):
+    """(levels, thresholds) of an iq_codebook_t as float32 numpy arrays."""
+    n = 1 << cb.bits
+    return (np.array(cb.levels[:n], dtype=np.float32),
+            np.array(cb.thresholds[:n - 1], dtype=np.float32))
+
+
+def iq_fit_codebook(calib, quats, bits: int = 3):
+    """Codebook fitted to calibration vectors (host fp32 [n_kv_heads][n][128])
+    rotated with the parameters quats ([n_kv_heads][32][2][4])."""
+    x = np.ascontiguousarray(np.asarray(calib.cpu() if hasattr(calib, "cpu") else calib,
+                                        dtype=np.float32))
+    qh = np.ascontiguousarray(np.asarray(quats.cpu() if hasattr(quats, "cpu") else quats,
+                                         dtype=np.float32))
+    if x.ndim != 3 or x.shape[2] != HEAD_DIM or qh.shape != (x.shape[0], 32, 2, 4):
+        raise ValueError("calib must be [n_kv_heads][n_vectors][128], quats [n_kv_heads][32][2][4]")
+    cb = _lib.IqCodebook()
+    _lib.check("iq_fit_codebook", _lib.lib().iq_fit_codebook(
+        x.ctypes.data_as(ctypes.c_void_p), x.shape[1], x.shape[0], HEAD_DIM,
+        qh.ctypes.data_as(ctypes.c_void_p), bits, ctypes.byref(cb)))
+    return cb
+
+
 def record_bytes(bits: int = 3) -> int:
     """Bytes of one packed record of 128 b-bit codes."""
     return HEAD_DIM * bits // 8
@@ -165,7 +207,15 @@ def iq_compress_kv_bits(k, v, quats, k_codes=None, k_norms=None, v_codes=None, v
     _compress(k, v, quats, k_codes, k_norms, v_codes, v_norms, dst_offset, bits)
 
 
-def _compress(k, v, quats, k_codes, k_norms, v_codes, v_norms, dst_offset, bits):
+def iq_compress_kv_cb(k, v, quats, codebook, k_codes=None, k_norms=None, v_codes=None,
+                      v_norms=None, dst_offset: int = 0):
+    """iq_compress_kv with a caller codebook (records of codebook.bits bits)."""
+    _compress(k, v, quats, k_codes, k_norms, v_codes, v_norms, dst_offset, codebook.bits,
+              codebook)
+
+
+def _compress(k, v, quats, k_codes, k_norms, v_codes, v_norms, dst_offset, bits,
+              codebook=None):
     src = k if k is not None else v
     if src is None:
         raise ValueError("k and v are both None")
@@ -184,11 +234,14 @@ def _compress(k, v, quats, k_codes, k_norms, v_codes, v_norms, dst_offset, bits)
         _require(x, name, src.dtype, (b, h, t, HEAD_DIM), dev)
         _require(codes, f"{name}_codes", torch.uint8, (b, h, cap, record_bytes(bits)), dev)
         _require(norms, f"{name}_norms", torch.float32, (b, h, cap), dev)
-    args = (_ptr(k), _ptr(v), _dtype_code(src), b, h, t, HEAD_DIM, _ptr(quats),
-            _ptr(k_codes) if k is not None else None, _ptr(k_norms) if k is not None else None,
+    outs = (_ptr(k_codes) if k is not None else None, _ptr(k_norms) if k is not None else None,
             _ptr(v_codes) if v is not None else None, _ptr(v_norms) if v is not None else None,
             cap, dst_offset)
-    if bits == 3:
+    args = (_ptr(k), _ptr(v), _dtype_code(src), b, h, t, HEAD_DIM, _ptr(quats)) + outs
+    if codebook is not None:
+        _lib.check("iq_compress_kv_cb", _lib.lib().iq_compress_kv_cb(
+            *args[:8], ctypes.byref(codebook), *outs, _stream(dev)))
+    elif bits == 3:
         _lib.check("iq_compress_kv", _lib.lib().iq_compress_kv(*args, _stream(dev)))
     else:
         _lib.check("iq_compress_kv_bits",
@@ -258,8 +311,16 @@ def iq_decode_attention_bits(q, k_codes, k_norms, v_codes, v_norms, seq_lens, qu
                    max_seq_len, softmax_scale, bits)
 
 
+def iq_decode_attention_cb(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, codebook,
+                           out=None, workspace=None, max_seq_len=None,
+                           softmax_scale: float = 0.0):
+    """iq_decode_attention on records written with a caller codebook."""
+    return _decode(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out, workspace,
+                   max_seq_len, softmax_scale, codebook.bits, codebook)
+
+
 def _decode(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out, workspace,
-            max_seq_len, softmax_scale, bits):
+            max_seq_len, softmax_scale, bits, codebook=None):
     if q.dim() != 3 or q.shape[-1] != HEAD_DIM:
         raise ValueError("q must be [batch][n_q_heads][128]")
     b, hq, _ = q.shape
@@ -286,7 +347,10 @@ def _decode(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out, workspa
     args = (_ptr(q), _ptr(k_codes), _ptr(k_norms), _ptr(v_codes), _ptr(v_norms), _ptr(seq_lens),
             cap, max_seq_len, _ptr(quats), b, hq, hkv, HEAD_DIM, float(softmax_scale), _ptr(out),
             _ptr(workspace), workspace.numel())
-    if bits == 3:
+    if codebook is not None:
+        _lib.check("iq_decode_attention_cb", _lib.lib().iq_decode_attention_cb(
+            *args[:9], ctypes.byref(codebook), *args[9:], _stream(dev)))
+    elif bits == 3:
         _lib.check("iq_decode_attention", _lib.lib().iq_decode_attention(*args, _stream(dev)))
     else:
         _lib.check("iq_decode_attention_bits",
@@ -401,8 +465,17 @@ def _step_shapes(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, 
     return b, hq, hkv, cap
 
 
+def iq_decode_step_cb(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats,
+                      codebook, out=None, workspace=None, max_seq_len=None,
+                      softmax_scale: float = 0.0, status=None):
+    """iq_decode_step with a caller codebook for the new records and the
+    attention."""
+    return _step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out,
+                 workspace, max_seq_len, softmax_scale, status, codebook.bits, codebook)
+
+
 def _step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out, workspace,
-          max_seq_len, softmax_scale, status, bits):
+          max_seq_len, softmax_scale, status, bits, codebook=None):
     b, hq, hkv, cap = _step_shapes(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms,
                                    seq_lens, quats, status, bits)
     dev = q.device
@@ -419,7 +492,10 @@ def _step(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, 
             _ptr(v_codes), _ptr(v_norms), _ptr(seq_lens), cap, max_seq_len, _ptr(quats), b, hq,
             hkv, HEAD_DIM, float(softmax_scale), _ptr(out), _ptr(workspace), workspace.numel(),
             _ptr(status))
-    if bits == 3:
+    if codebook is not None:
+        _lib.check("iq_decode_step_cb", _lib.lib().iq_decode_step_cb(
+            *args[:12], ctypes.byref(codebook), *args[12:], _stream(dev)))
+    elif bits == 3:
         _lib.check("iq_decode_step", _lib.lib().iq_decode_step(*args, _stream(dev)))
     else:
         _lib.check("iq_decode_step_bits",
@@ -579,9 +655,17 @@ def iq_decode_attention_multi_paged(q, pool, block_tables, seq_lens, quats, out=
 # reconstruct-then-compute baseline (materialized fp16 cache)
 # ---------------------------------------------------------------------------
 
+def iq_dequantize_kv_cb(k_codes, k_norms, v_codes, v_norms, quats, codebook, n_tokens=None,
+                        src_offset: int = 0, seq_lens=None, out_dtype=torch.float16,
+                        k_out=None, v_out=None):
+    """iq_dequantize_kv of records written with a caller (3-bit) codebook."""
+    return iq_dequantize_kv(k_codes, k_norms, v_codes, v_norms, quats, n_tokens, src_offset,
+                            seq_lens, out_dtype, k_out, v_out, codebook=codebook)
+
+
 def iq_dequantize_kv(k_codes, k_norms, v_codes, v_norms, quats, n_tokens=None,
                      src_offset: int = 0, seq_lens=None, out_dtype=torch.float16,
-                     k_out=None, v_out=None):
+                     k_out=None, v_out=None, codebook=None):
     """Materialize cache positions src_offset .. src_offset + n_tokens - 1 as
     original-space vectors [B][H_kv][n_tokens][128] of out_dtype (fp16 or
     fp32).  Either side may be None.  With seq_lens, tokens at or past a
@@ -611,6 +695,13 @@ def iq_dequantize_kv(k_codes, k_norms, v_codes, v_norms, quats, n_tokens=None,
     if seq_lens is not None:
         _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
     code = _lib.IQ_DTYPE_F16 if out_dtype == torch.float16 else _lib.IQ_DTYPE_F32
+    if codebook is not None:
+        st = _lib.lib().iq_dequantize_kv_cb(
+            _ptr(k_codes), _ptr(k_norms), _ptr(v_codes), _ptr(v_norms), _ptr(quats),
+            ctypes.byref(codebook), _ptr(seq_lens), b, hkv, n_tokens, HEAD_DIM, cap, src_offset,
+            code, _ptr(outs[0]), _ptr(outs[1]), _stream(dev))
+        _lib.check("iq_dequantize_kv_cb", st)
+        return outs[0], outs[1]
     st = _lib.lib().iq_dequantize_kv(
         _ptr(k_codes), _ptr(k_norms), _ptr(v_codes), _ptr(v_norms), _ptr(quats), _ptr(seq_lens),
         b, hkv, n_tokens, HEAD_DIM, cap, src_offset, code, _ptr(outs[0]), _ptr(outs[1]),

@@ -222,11 +222,35 @@ iq_status iq_compress_kv(const void* k, const void* v, iq_dtype dtype, int64_t b
                              k_norms, v_codes, v_norms, capacity, dst_offset, 3, stream);
 }
 
-iq_status iq_compress_kv_bits(const void* k, const void* v, iq_dtype dtype, int64_t batch,
-                              int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
-                              const float* quats, uint8_t* k_codes, float* k_norms,
-                              uint8_t* v_codes, float* v_norms, int64_t capacity,
-                              int64_t dst_offset, int bits, hipStream_t stream) {
+namespace {
+
+// A caller codebook the kernels can take: b in {2, 3, 4}; 2^b finite levels,
+// strictly ascending, fp16-exact, below 1 in magnitude and symmetric
+// (level[i] = -level[2^b - 1 - i], the compression quantizer's sign rule);
+// thresholds exactly the fp32 midpoints of adjacent levels.
+iq_status check_codebook(const iq_codebook_t* cb) {
+  if (cb == nullptr) return IQ_ERR_INVALID_ARGUMENT;
+  if (cb->bits != 2 && cb->bits != 3 && cb->bits != 4) return IQ_ERR_UNSUPPORTED;
+  const int n = 1 << cb->bits;
+  for (int i = 0; i < n; ++i) {
+    const double l = cb->levels[i];
+    if (!(fabs(l) < 1.0) || iq::round_to_half(l) != l) return IQ_ERR_INVALID_ARGUMENT;
+    if (cb->levels[i] != -cb->levels[n - 1 - i]) return IQ_ERR_INVALID_ARGUMENT;
+    if (i > 0 && !(cb->levels[i] > cb->levels[i - 1])) return IQ_ERR_INVALID_ARGUMENT;
+  }
+  for (int i = 0; i < n - 1; ++i)
+    if (cb->thresholds[i] !=
+        static_cast<float>(0.5 * (static_cast<double>(cb->levels[i]) + cb->levels[i + 1])))
+      return IQ_ERR_INVALID_ARGUMENT;
+  return IQ_OK;
+}
+
+iq_status compress_common(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+                          int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
+                          const float* quats, uint8_t* k_codes, float* k_norms,
+                          uint8_t* v_codes, float* v_norms, int64_t capacity,
+                          int64_t dst_offset, int bits, const iq_codebook_t* cb,
+                          hipStream_t stream) {
   if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
   if (bits < 2 || bits > 4) return IQ_ERR_UNSUPPORTED;
   if (dtype != IQ_DTYPE_F32 && dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
@@ -248,8 +272,30 @@ iq_status iq_compress_kv_bits(const void* k, const void* v, iq_dtype dtype, int6
     return IQ_ERR_INVALID_ARGUMENT;
   const hipError_t e = iq::launch_compress(k, v, dtype, batch, n_kv_heads, n_tokens, quats,
                                            k_codes, k_norms, v_codes, v_norms, capacity,
-                                           dst_offset, bits, stream);
+                                           dst_offset, bits, stream, cb);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+}  // namespace
+
+iq_status iq_compress_kv_bits(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+                              int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
+                              const float* quats, uint8_t* k_codes, float* k_norms,
+                              uint8_t* v_codes, float* v_norms, int64_t capacity,
+                              int64_t dst_offset, int bits, hipStream_t stream) {
+  return compress_common(k, v, dtype, batch, n_kv_heads, n_tokens, head_dim, quats, k_codes,
+                         k_norms, v_codes, v_norms, capacity, dst_offset, bits, nullptr, stream);
+}
+
+iq_status iq_compress_kv_cb(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+                            int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
+                            const float* quats, const iq_codebook_t* cb, uint8_t* k_codes,
+                            float* k_norms, uint8_t* v_codes, float* v_norms, int64_t capacity,
+                            int64_t dst_offset, hipStream_t stream) {
+  const iq_status st = check_codebook(cb);
+  if (st != IQ_OK) return st;
+  return compress_common(k, v, dtype, batch, n_kv_heads, n_tokens, head_dim, quats, k_codes,
+                         k_norms, v_codes, v_norms, capacity, dst_offset, cb->bits, cb, stream);
 }
 
 iq_status iq_append_token(const void* k_new, const void* v_new, iq_dtype dtype, int64_t batch,
@@ -349,6 +395,54 @@ iq_status check_g8_shape(int64_t n_q_heads, int64_t n_kv_heads, int64_t batch, i
 
 }  // namespace
 
+namespace {
+
+// Decode attention on records of `bits` bits with codebook cb (null: the
+// library's C_b).  3-bit records take the group-8 matrix-core path where the
+// shapes allow it and the generic path otherwise; 2- and 4-bit records the
+// matrix-core path only.
+iq_status decode_common(const float* q, const uint8_t* k_codes, const float* k_norms,
+                        const uint8_t* v_codes, const float* v_norms, const int32_t* seq_lens,
+                        int64_t capacity, int64_t max_seq_len, const float* quats, int64_t batch,
+                        int64_t n_q_heads, int64_t n_kv_heads, int64_t head_dim,
+                        float softmax_scale, float* out, void* workspace,
+                        size_t workspace_bytes, int bits, const iq_codebook_t* cb,
+                        hipStream_t stream) {
+  if (bits != 2 && bits != 3 && bits != 4) return IQ_ERR_UNSUPPORTED;
+  iq::DecodePlan plan;
+  const iq_status st = check_decode_args(q, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                                         capacity, max_seq_len, quats, batch, n_q_heads,
+                                         n_kv_heads, head_dim, out, workspace, workspace_bytes,
+                                         &plan);
+  if (st != IQ_OK) return st;
+  if (bits != 3) {
+    const iq_status shape = check_g8_shape(n_q_heads, n_kv_heads, batch, capacity, 16 * bits,
+                                           k_norms, v_norms, plan);
+    if (shape != IQ_OK) return shape;
+  }
+  if (batch == 0) return IQ_OK;
+  hipError_t e;
+  if (bits == 3) {
+    // without an append the launch only reads the cache and the lengths
+    e = iq::launch_decode(plan, q, const_cast<uint8_t*>(k_codes), const_cast<float*>(k_norms),
+                          const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms),
+                          const_cast<int32_t*>(seq_lens), capacity, max_seq_len, quats, batch,
+                          n_q_heads, n_kv_heads, resolve_scale(softmax_scale), out, workspace,
+                          nullptr, stream, cb);
+  } else {
+    float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
+    e = iq::launch_decode_g8(plan.g8_batches, plan.g8_splits, plan.g8_split_len, q,
+                             const_cast<uint8_t*>(k_codes), const_cast<float*>(k_norms),
+                             const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms),
+                             const_cast<int32_t*>(seq_lens), capacity, max_seq_len, quats, batch,
+                             n_kv_heads, resolve_scale(softmax_scale), out, parts, nullptr,
+                             nullptr, bits, stream, cb);
+  }
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+}  // namespace
+
 iq_status iq_decode_attention(const float* q, const uint8_t* k_codes, const float* k_norms,
                               const uint8_t* v_codes, const float* v_norms,
                               const int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
@@ -356,20 +450,9 @@ iq_status iq_decode_attention(const float* q, const uint8_t* k_codes, const floa
                               int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
                               float* out, void* workspace, size_t workspace_bytes,
                               hipStream_t stream) {
-  iq::DecodePlan plan;
-  const iq_status st = check_decode_args(q, k_codes, k_norms, v_codes, v_norms, seq_lens,
-                                         capacity, max_seq_len, quats, batch, n_q_heads,
-                                         n_kv_heads, head_dim, out, workspace, workspace_bytes,
-                                         &plan);
-  if (st != IQ_OK) return st;
-  if (batch == 0) return IQ_OK;
-  // without an append the launch only reads the cache and the lengths
-  const hipError_t e = iq::launch_decode(
-      plan, q, const_cast<uint8_t*>(k_codes), const_cast<float*>(k_norms),
-      const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms), const_cast<int32_t*>(seq_lens),
-      capacity, max_seq_len, quats, batch, n_q_heads, n_kv_heads, resolve_scale(softmax_scale),
-      out, workspace, nullptr, stream);
-  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+  return decode_common(q, k_codes, k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len,
+                       quats, batch, n_q_heads, n_kv_heads, head_dim, softmax_scale, out,
+                       workspace, workspace_bytes, 3, nullptr, stream);
 }
 
 iq_status iq_decode_attention_bits(const float* q, const uint8_t* k_codes, const float* k_norms,
@@ -379,29 +462,23 @@ iq_status iq_decode_attention_bits(const float* q, const uint8_t* k_codes, const
                                    int64_t n_q_heads, int64_t n_kv_heads, int64_t head_dim,
                                    float softmax_scale, float* out, void* workspace,
                                    size_t workspace_bytes, int bits, hipStream_t stream) {
-  if (bits == 3)
-    return iq_decode_attention(q, k_codes, k_norms, v_codes, v_norms, seq_lens, capacity,
-                               max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
-                               softmax_scale, out, workspace, workspace_bytes, stream);
-  if (bits != 2 && bits != 4) return IQ_ERR_UNSUPPORTED;
-  iq::DecodePlan plan;
-  const iq_status st = check_decode_args(q, k_codes, k_norms, v_codes, v_norms, seq_lens,
-                                         capacity, max_seq_len, quats, batch, n_q_heads,
-                                         n_kv_heads, head_dim, out, workspace, workspace_bytes,
-                                         &plan);
+  return decode_common(q, k_codes, k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len,
+                       quats, batch, n_q_heads, n_kv_heads, head_dim, softmax_scale, out,
+                       workspace, workspace_bytes, bits, nullptr, stream);
+}
+
+iq_status iq_decode_attention_cb(const float* q, const uint8_t* k_codes, const float* k_norms,
+                                 const uint8_t* v_codes, const float* v_norms,
+                                 const int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                                 const float* quats, const iq_codebook_t* cb, int64_t batch,
+                                 int64_t n_q_heads, int64_t n_kv_heads, int64_t head_dim,
+                                 float softmax_scale, float* out, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  const iq_status st = check_codebook(cb);
   if (st != IQ_OK) return st;
-  // 2- and 4-bit records run on the group-8 matrix-core path only
-  const iq_status shape = check_g8_shape(n_q_heads, n_kv_heads, batch, capacity, 16 * bits,
-                                         k_norms, v_norms, plan);
-  if (shape != IQ_OK) return shape;
-  if (batch == 0) return IQ_OK;
-  float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
-  const hipError_t e = iq::launch_decode_g8(
-      plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, const_cast<uint8_t*>(k_codes),
-      const_cast<float*>(k_norms), const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms),
-      const_cast<int32_t*>(seq_lens), capacity, max_seq_len, quats, batch, n_kv_heads,
-      resolve_scale(softmax_scale), out, parts, nullptr, nullptr, bits, stream);
-  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+  return decode_common(q, k_codes, k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len,
+                       quats, batch, n_q_heads, n_kv_heads, head_dim, softmax_scale, out,
+                       workspace, workspace_bytes, cb->bits, cb, stream);
 }
 
 size_t iq_decode_multi_workspace_bytes(int64_t batch, int64_t n_tokens, int64_t n_q_heads,
@@ -461,13 +538,18 @@ iq_status iq_decode_attention_multi(const float* q, const uint8_t* k_codes,
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 
-iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, iq_dtype dtype,
-                         uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
-                         int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
-                         const float* quats, int64_t batch, int64_t n_q_heads,
-                         int64_t n_kv_heads, int64_t head_dim, float softmax_scale, float* out,
-                         void* workspace, size_t workspace_bytes, int32_t* status_dev,
-                         hipStream_t stream) {
+namespace {
+
+// The fused step on records of `bits` bits with codebook cb (null: C_b); the
+// paths as in decode_common.
+iq_status step_common(const float* q, const void* k_new, const void* v_new, iq_dtype dtype,
+                      uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
+                      int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                      const float* quats, int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                      int64_t head_dim, float softmax_scale, float* out, void* workspace,
+                      size_t workspace_bytes, int32_t* status_dev, int bits,
+                      const iq_codebook_t* cb, hipStream_t stream) {
+  if (bits != 2 && bits != 3 && bits != 4) return IQ_ERR_UNSUPPORTED;
   if (dtype != IQ_DTYPE_F32 && dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
   iq::DecodePlan plan;
   const iq_status st = check_decode_args(q, k_codes, k_norms, v_codes, v_norms, seq_lens,
@@ -479,13 +561,42 @@ iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, i
   if (!k_new || !v_new || !iq::aligned(k_new, 16) || !iq::aligned(v_new, 16) ||
       (status_dev && !iq::aligned(status_dev, 4)))
     return IQ_ERR_INVALID_ARGUMENT;
+  if (bits != 3) {
+    // the matrix-core path only, as for iq_decode_attention_bits
+    const iq_status shape = check_g8_shape(n_q_heads, n_kv_heads, batch, capacity, 16 * bits,
+                                           k_norms, v_norms, plan);
+    if (shape != IQ_OK) return shape;
+  }
   if (batch == 0) return IQ_OK;
   const iq::StepAppend append{k_new, v_new, dtype == IQ_DTYPE_F16 ? 1 : 0, status_dev};
-  const hipError_t e = iq::launch_decode(plan, q, k_codes, k_norms, v_codes, v_norms, seq_lens,
-                                         capacity, max_seq_len, quats, batch, n_q_heads,
-                                         n_kv_heads, resolve_scale(softmax_scale), out, workspace,
-                                         &append, stream);
+  hipError_t e;
+  if (bits == 3) {
+    e = iq::launch_decode(plan, q, k_codes, k_norms, v_codes, v_norms, seq_lens, capacity,
+                          max_seq_len, quats, batch, n_q_heads, n_kv_heads,
+                          resolve_scale(softmax_scale), out, workspace, &append, stream, cb);
+  } else {
+    float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
+    e = iq::launch_decode_g8(plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes,
+                             k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len, quats,
+                             batch, n_kv_heads, resolve_scale(softmax_scale), out, parts,
+                             &append, nullptr, bits, stream, cb);
+  }
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+}  // namespace
+
+iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, iq_dtype dtype,
+                         uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
+                         int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
+                         const float* quats, int64_t batch, int64_t n_q_heads,
+                         int64_t n_kv_heads, int64_t head_dim, float softmax_scale, float* out,
+                         void* workspace, size_t workspace_bytes, int32_t* status_dev,
+                         hipStream_t stream) {
+  return step_common(q, k_new, v_new, dtype, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                     capacity, max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
+                     softmax_scale, out, workspace, workspace_bytes, status_dev, 3, nullptr,
+                     stream);
 }
 
 iq_status iq_decode_step_bits(const float* q, const void* k_new, const void* v_new,
@@ -496,34 +607,25 @@ iq_status iq_decode_step_bits(const float* q, const void* k_new, const void* v_n
                               int64_t head_dim, float softmax_scale, float* out, void* workspace,
                               size_t workspace_bytes, int32_t* status_dev, int bits,
                               hipStream_t stream) {
-  if (bits == 3)
-    return iq_decode_step(q, k_new, v_new, dtype, k_codes, k_norms, v_codes, v_norms, seq_lens,
-                          capacity, max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
-                          softmax_scale, out, workspace, workspace_bytes, status_dev, stream);
-  if (bits != 2 && bits != 4) return IQ_ERR_UNSUPPORTED;
-  if (dtype != IQ_DTYPE_F32 && dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
-  iq::DecodePlan plan;
-  const iq_status st = check_decode_args(q, k_codes, k_norms, v_codes, v_norms, seq_lens,
-                                         capacity, max_seq_len, quats, batch, n_q_heads,
-                                         n_kv_heads, head_dim, out, workspace, workspace_bytes,
-                                         &plan);
+  return step_common(q, k_new, v_new, dtype, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                     capacity, max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
+                     softmax_scale, out, workspace, workspace_bytes, status_dev, bits, nullptr,
+                     stream);
+}
+
+iq_status iq_decode_step_cb(const float* q, const void* k_new, const void* v_new,
+                            iq_dtype dtype, uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
+                            float* v_norms, int32_t* seq_lens, int64_t capacity,
+                            int64_t max_seq_len, const float* quats, const iq_codebook_t* cb,
+                            int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                            int64_t head_dim, float softmax_scale, float* out, void* workspace,
+                            size_t workspace_bytes, int32_t* status_dev, hipStream_t stream) {
+  const iq_status st = check_codebook(cb);
   if (st != IQ_OK) return st;
-  if (max_seq_len < 1 || n_kv_heads > 512) return IQ_ERR_INVALID_ARGUMENT;
-  if (!k_new || !v_new || !iq::aligned(k_new, 16) || !iq::aligned(v_new, 16) ||
-      (status_dev && !iq::aligned(status_dev, 4)))
-    return IQ_ERR_INVALID_ARGUMENT;
-  // the matrix-core path only, as for iq_decode_attention_bits
-  const iq_status shape = check_g8_shape(n_q_heads, n_kv_heads, batch, capacity, 16 * bits,
-                                         k_norms, v_norms, plan);
-  if (shape != IQ_OK) return shape;
-  if (batch == 0) return IQ_OK;
-  const iq::StepAppend append{k_new, v_new, dtype == IQ_DTYPE_F16 ? 1 : 0, status_dev};
-  float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
-  const hipError_t e = iq::launch_decode_g8(
-      plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes, k_norms, v_codes, v_norms,
-      seq_lens, capacity, max_seq_len, quats, batch, n_kv_heads, resolve_scale(softmax_scale),
-      out, parts, &append, nullptr, bits, stream);
-  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+  return step_common(q, k_new, v_new, dtype, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                     capacity, max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
+                     softmax_scale, out, workspace, workspace_bytes, status_dev, cb->bits, cb,
+                     stream);
 }
 
 // ---------------------------------------------------------------------------
@@ -709,12 +811,13 @@ iq_status iq_decode_attention_multi_paged(
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 
-iq_status iq_dequantize_kv(const uint8_t* k_codes, const float* k_norms,
-                           const uint8_t* v_codes, const float* v_norms, const float* quats,
-                           const int32_t* seq_lens, int64_t batch, int64_t n_kv_heads,
-                           int64_t n_tokens, int64_t head_dim, int64_t capacity,
-                           int64_t src_offset, iq_dtype out_dtype, void* k_out, void* v_out,
-                           hipStream_t stream) {
+namespace {
+
+iq_status dequant_common(const uint8_t* k_codes, const float* k_norms, const uint8_t* v_codes,
+                         const float* v_norms, const float* quats, const int32_t* seq_lens,
+                         int64_t batch, int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
+                         int64_t capacity, int64_t src_offset, iq_dtype out_dtype, void* k_out,
+                         void* v_out, const iq_codebook_t* cb, hipStream_t stream) {
   if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
   if (out_dtype != IQ_DTYPE_F32 && out_dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
   if (batch < 0 || n_kv_heads <= 0 || n_tokens < 0 || capacity < 0 || src_offset < 0)
@@ -736,8 +839,36 @@ iq_status iq_dequantize_kv(const uint8_t* k_codes, const float* k_norms,
   const hipError_t e = iq::launch_dequant(k_codes, k_norms, v_codes, v_norms, quats, seq_lens,
                                           batch, n_kv_heads, n_tokens, capacity, src_offset,
                                           out_dtype == IQ_DTYPE_F16 ? 1 : 0, k_out, v_out,
-                                          stream);
+                                          stream, cb);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+}  // namespace
+
+iq_status iq_dequantize_kv(const uint8_t* k_codes, const float* k_norms,
+                           const uint8_t* v_codes, const float* v_norms, const float* quats,
+                           const int32_t* seq_lens, int64_t batch, int64_t n_kv_heads,
+                           int64_t n_tokens, int64_t head_dim, int64_t capacity,
+                           int64_t src_offset, iq_dtype out_dtype, void* k_out, void* v_out,
+                           hipStream_t stream) {
+  return dequant_common(k_codes, k_norms, v_codes, v_norms, quats, seq_lens, batch, n_kv_heads,
+                        n_tokens, head_dim, capacity, src_offset, out_dtype, k_out, v_out,
+                        nullptr, stream);
+}
+
+iq_status iq_dequantize_kv_cb(const uint8_t* k_codes, const float* k_norms,
+                              const uint8_t* v_codes, const float* v_norms, const float* quats,
+                              const iq_codebook_t* cb, const int32_t* seq_lens, int64_t batch,
+                              int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
+                              int64_t capacity, int64_t src_offset, iq_dtype out_dtype,
+                              void* k_out, void* v_out, hipStream_t stream) {
+  const iq_status st = check_codebook(cb);
+  if (st != IQ_OK) return st;
+  // the materialization kernel decodes 3-bit records
+  if (cb->bits != 3) return IQ_ERR_UNSUPPORTED;
+  return dequant_common(k_codes, k_norms, v_codes, v_norms, quats, seq_lens, batch, n_kv_heads,
+                        n_tokens, head_dim, capacity, src_offset, out_dtype, k_out, v_out, cb,
+                        stream);
 }
 
 size_t iq_decode_f16_workspace_bytes(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,

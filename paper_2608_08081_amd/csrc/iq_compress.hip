@@ -305,7 +305,8 @@ hipError_t launch_compress_any(const void* k, const void* v, int dtype, int64_t 
                                int64_t n_heads, int64_t n_tokens, const float* quats,
                                uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
                                float* v_norms, int64_t capacity, int64_t dst_offset,
-                               const PageTable* pages, int bits, hipStream_t stream) {
+                               const PageTable* pages, int bits, hipStream_t stream,
+                               const iq_codebook_t* cb) {
   // slot 0 is whichever side is present first, slot 1 the other (if any)
   const void* s0 = k ? k : v;
   uint8_t* c0 = k ? k_codes : v_codes;
@@ -326,7 +327,7 @@ hipError_t launch_compress_any(const void* k, const void* v, int dtype, int64_t 
   hipLaunchKernelGGL((compress_kernel<T_, P_, B_>), grid, block, 0, stream,                     \
                      static_cast<const T_*>(s0), static_cast<const T_*>(s1), quats, c0, n0, c1, \
                      n1, static_cast<int>(n_heads), n_bh, n_tokens, chunks, capacity,           \
-                     dst_offset, codebook_b<B_>(), pt)
+                     dst_offset, codebook_for<B_>(cb), pt)
 #define IQ_LAUNCH_COMPRESS_T(T_)                   \
   if (pages) IQ_LAUNCH_COMPRESS(T_, true, 3);      \
   else if (bits == 2) IQ_LAUNCH_COMPRESS(T_, false, 2); \
@@ -348,9 +349,9 @@ hipError_t launch_compress(const void* k, const void* v, int dtype, int64_t batc
                            int64_t n_heads, int64_t n_tokens, const float* quats,
                            uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
                            float* v_norms, int64_t capacity, int64_t dst_offset, int bits,
-                           hipStream_t stream) {
+                           hipStream_t stream, const iq_codebook_t* cb) {
   return launch_compress_any(k, v, dtype, batch, n_heads, n_tokens, quats, k_codes, k_norms,
-                             v_codes, v_norms, capacity, dst_offset, nullptr, bits, stream);
+                             v_codes, v_norms, capacity, dst_offset, nullptr, bits, stream, cb);
 }
 
 hipError_t launch_compress_paged(const void* k, const void* v, int dtype, int64_t batch,
@@ -360,14 +361,14 @@ hipError_t launch_compress_paged(const void* k, const void* v, int dtype, int64_
                                  hipStream_t stream) {
   return launch_compress_any(k, v, dtype, batch, n_heads, n_tokens, quats, k_codes, k_norms,
                              v_codes, v_norms, (pages.max_pages << pages.page_shift), dst_offset,
-                             &pages, 3, stream);
+                             &pages, 3, stream, nullptr);
 }
 
 hipError_t launch_append(const void* k, const void* v, int dtype, int64_t batch,
                          int64_t n_heads, const float* quats, uint8_t* k_codes,
                          float* k_norms, uint8_t* v_codes, float* v_norms,
                          int64_t capacity, int32_t* seq_lens, int32_t* status,
-                         hipStream_t stream) {
+                         hipStream_t stream, const iq_codebook_t* codebook_arg) {
   if (batch == 0) return hipSuccess;
   const void* s0 = k ? k : v;
   uint8_t* c0 = k ? k_codes : v_codes;
@@ -378,7 +379,7 @@ hipError_t launch_append(const void* k, const void* v, int dtype, int64_t batch,
   const int n_vectors = static_cast<int>(n_heads * (s1 ? 2 : 1));
   const int waves = n_vectors < kAppendMaxWaves ? n_vectors : kAppendMaxWaves;
   const dim3 block(static_cast<unsigned>(64 * waves));
-  const Codebook& cb = codebook();
+  const Codebook cb = codebook_for<3>(codebook_arg);
   if (dtype == IQ_DTYPE_F16) {
     hipLaunchKernelGGL(append_kernel<__half>, dim3(static_cast<unsigned>(batch)), block, 0,
                        stream, static_cast<const __half*>(s0), static_cast<const __half*>(s1),

@@ -295,7 +295,7 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, uint8_t* k_code
                          int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                          const float* quats, int64_t batch, int64_t n_q_heads,
                          int64_t n_kv_heads, float scale, float* out, void* workspace,
-                         const StepAppend* append, hipStream_t stream) {
+                         const StepAppend* append, hipStream_t stream, const iq_codebook_t* cb) {
   if (batch == 0) return hipSuccess;
   const int group = static_cast<int>(n_q_heads / n_kv_heads);
   const bool aligned16 = (reinterpret_cast<uintptr_t>(k_norms) % 16 == 0) &&
@@ -311,7 +311,8 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, uint8_t* k_code
     float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
     return launch_decode_g8(plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes,
                             k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len, quats,
-                            batch, n_kv_heads, scale, out, parts, append, nullptr, 3, stream);
+                            batch, n_kv_heads, scale, out, parts, append, nullptr, 3, stream,
+                            cb);
   }
   if (append) {
     // generic path of the fused step: the append kernel, then attention
@@ -319,7 +320,7 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, uint8_t* k_code
     const hipError_t e =
         launch_append(append->k_new, append->v_new, append->f16 ? IQ_DTYPE_F16 : IQ_DTYPE_F32,
                       batch, n_kv_heads, quats, k_codes, k_norms, v_codes, v_norms, capacity,
-                      seq_lens, append->status, stream);
+                      seq_lens, append->status, stream, cb);
     if (e != hipSuccess) return e;
   }
   float* partials = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
@@ -329,7 +330,7 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, uint8_t* k_code
                      seq_lens, quats, partials, capacity, max_seq_len,
                      static_cast<int>(n_q_heads), static_cast<int>(n_kv_heads), group,
                      static_cast<int>(plan.split_len), static_cast<int>(plan.n_splits), scale,
-                     codebook());
+                     codebook_for<3>(cb));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(decode_combine_kernel, dim3(static_cast<unsigned>(batch * n_q_heads)),

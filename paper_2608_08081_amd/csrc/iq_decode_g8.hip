@@ -636,7 +636,8 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                             int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                             const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
                             float* out, float* partials, const StepAppend* append,
-                            const PageTable* pages, int bits, hipStream_t stream) {
+                            const PageTable* pages, int bits, hipStream_t stream,
+                            const iq_codebook_t* cb) {
   if (bits != 3 && pages) return hipErrorInvalidValue;
   // partials per (sequence, KV head): the splits, and the fused step's new
   // token
@@ -663,7 +664,7 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                      stream, q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials,  \
                      out, capacity, static_cast<int>(max_seq_len),                              \
                      static_cast<int>(n_kv_heads), static_cast<int>(n_splits),                  \
-                     static_cast<int>(split_len), qscale, codebook_b<BITS_>(), k_new, v_new,    \
+                     static_cast<int>(split_len), qscale, codebook_for<BITS_>(cb), k_new, v_new, \
                      new_f16, status, pt)
 #define IQ_LAUNCH_G8_W(NB_, APP_, WIDE_)                \
   if (pages) {                                          \

@@ -212,7 +212,7 @@ hipError_t launch_dequant(const uint8_t* k_codes, const float* k_norms, const ui
                           const float* v_norms, const float* quats, const int32_t* seq_lens,
                           int64_t batch, int64_t n_heads, int64_t n_tokens, int64_t capacity,
                           int64_t src_offset, int out_f16, void* k_out, void* v_out,
-                          hipStream_t stream) {
+                          hipStream_t stream, const iq_codebook_t* codebook_arg) {
   // side 0 is whichever of K and V is present first, side 1 the other
   const bool has_k = k_codes != nullptr, has_v = v_codes != nullptr;
   const uint8_t* c0 = has_k ? k_codes : v_codes;
@@ -226,7 +226,7 @@ hipError_t launch_dequant(const uint8_t* k_codes, const float* k_norms, const ui
   const int64_t chunks = (n_tokens + kDqTokens - 1) / kDqTokens;
   const int64_t blocks = chunks * n_bh * nwhich;
   if (blocks == 0) return hipSuccess;
-  const Codebook& cb = codebook();
+  const Codebook cb = codebook_for<3>(codebook_arg);
   const dim3 grid(static_cast<unsigned>(blocks)), block(kDqThreads);
   if (out_f16) {
     hipLaunchKernelGGL(dequant_kernel<__half>, grid, block, 0, stream, c0, n0,

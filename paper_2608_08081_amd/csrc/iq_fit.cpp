@@ -277,3 +277,122 @@ iq_status iq_fit_rotation(const float* calib, int64_t n_vectors, int64_t n_kv_he
   }
   return status;
 }
+
+// ---------------------------------------------------------------------------
+// Empirical codebook (Sec. 3.2 Step 3 measured on calibration data): the
+// Lloyd-Max levels of the distribution of the rotated, normalized
+// coordinates of calibration vectors, instead of the analytic sphere
+// marginal.  Reading: one codebook for all heads (as the library's), fitted
+// to the sample made symmetric (each coordinate and its negation: the
+// marginal of an isotropic rotation is symmetric, and the kernels' quantizer
+// relies on it), started from the library's C_b, iterated until the cells
+// stop changing; then stored like C_b (levels rounded to fp16, made exactly
+// symmetric, thresholds their midpoints).
+// ---------------------------------------------------------------------------
+namespace iq {
+namespace {
+
+// Nearest binary16 value (ties to even) of v, for |v| in the normal range
+// or zero.
+double nearest_half(double v) {
+  if (v == 0.0) return 0.0;
+  int e = 0;
+  frexp(fabs(v), &e);
+  const double ulp = ldexp(1.0, e - 11);
+  return nearbyint(v / ulp) * ulp;
+}
+
+// y = R x / ||x|| (Eq. 2) of one calibration vector in fp64; false for a
+// zero or non-finite vector.  quats: the head's 32 (q_L, q_R) pairs.
+bool rotate_normalized(const float* src, const float* quats, double* y) {
+  double ss = 0.0;
+  for (int i = 0; i < kDim; ++i) ss += static_cast<double>(src[i]) * src[i];
+  if (!(ss > 0.0) || !std::isfinite(ss)) return false;
+  const double inv = 1.0 / sqrt(ss);
+  for (int i = 0; i < kDim; ++i) y[i] = src[i] * inv;
+  wht128(y);
+  for (int b = 0; b < kNumBlocks; ++b) {
+    double ql[4], qr[4];
+    for (int i = 0; i < 4; ++i) {
+      ql[i] = quats[8 * b + i];
+      qr[i] = quats[8 * b + 4 + i];
+    }
+    // the stored pair, made unit in fp64, acting as v -> q_L v conj(q_R)
+    const double nl = sqrt(ql[0] * ql[0] + ql[1] * ql[1] + ql[2] * ql[2] + ql[3] * ql[3]);
+    const double nr = sqrt(qr[0] * qr[0] + qr[1] * qr[1] + qr[2] * qr[2] + qr[3] * qr[3]);
+    for (int i = 0; i < 4; ++i) ql[i] /= nl;
+    const double qrc[4] = {qr[0] / nr, -qr[1] / nr, -qr[2] / nr, -qr[3] / nr};
+    double t[4];
+    qmul(ql, &y[4 * b], t);
+    qmul(t, qrc, &y[4 * b]);
+  }
+  return true;
+}
+
+}  // namespace
+}  // namespace iq
+
+iq_status iq_fit_codebook(const float* calib, int64_t n_vectors, int64_t n_kv_heads,
+                          int64_t head_dim, const float* quats_host, int32_t bits,
+                          iq_codebook_t* out) {
+  if (head_dim != iq::kDim || (bits != 2 && bits != 3 && bits != 4)) return IQ_ERR_UNSUPPORTED;
+  if (calib == nullptr || quats_host == nullptr || out == nullptr || n_vectors <= 0 ||
+      n_kv_heads <= 0 || n_vectors > (int64_t(1) << 24) || n_kv_heads > (int64_t(1) << 16) ||
+      n_vectors * n_kv_heads > (int64_t(1) << 24))
+    return IQ_ERR_INVALID_ARGUMENT;
+  const int n = 1 << bits;
+  float init_levels[16], init_thr[15];
+  iq_codebook_bits(bits, init_levels, init_thr);
+  // the symmetrized sample, sorted
+  std::vector<double> ys;
+  ys.reserve(static_cast<size_t>(2 * iq::kDim * n_vectors * n_kv_heads));
+  std::vector<double> y(iq::kDim);
+  for (int64_t h = 0; h < n_kv_heads; ++h)
+    for (int64_t t = 0; t < n_vectors; ++t) {
+      if (!iq::rotate_normalized(calib + (h * n_vectors + t) * iq::kDim,
+                                 quats_host + h * iq::kQuatFloats, y.data()))
+        continue;
+      for (int i = 0; i < iq::kDim; ++i) {
+        ys.push_back(y[i]);
+        ys.push_back(-y[i]);
+      }
+    }
+  if (ys.empty()) return IQ_ERR_INVALID_ARGUMENT;
+  std::sort(ys.begin(), ys.end());
+  // prefix sums: the mean of a cell [lo, hi) of the sorted sample is
+  // (P[hi] - P[lo]) / (hi - lo)
+  std::vector<double> prefix(ys.size() + 1, 0.0);
+  for (size_t i = 0; i < ys.size(); ++i) prefix[i + 1] = prefix[i] + ys[i];
+  double c[16];
+  for (int i = 0; i < n; ++i) c[i] = init_levels[i];
+  bool fixed = false;
+  for (int it = 0; it < 10000 && !fixed; ++it) {
+    // cell j: t_(j-1) <= y < t_j, t_j the midpoints (the coding rule)
+    size_t edge[17];
+    edge[0] = 0;
+    edge[n] = ys.size();
+    for (int j = 1; j < n; ++j)
+      edge[j] = static_cast<size_t>(
+          std::lower_bound(ys.begin(), ys.end(), 0.5 * (c[j - 1] + c[j])) - ys.begin());
+    fixed = true;
+    for (int j = 0; j < n; ++j) {
+      if (edge[j + 1] <= edge[j]) continue;   // an empty cell keeps its level
+      const double m = (prefix[edge[j + 1]] - prefix[edge[j]]) /
+                       static_cast<double>(edge[j + 1] - edge[j]);
+      if (m != c[j]) fixed = false;
+      c[j] = m;
+    }
+  }
+  if (!fixed) return IQ_ERR_INVALID_ARGUMENT;
+  iq_codebook_t cb{};
+  cb.bits = bits;
+  for (int i = 0; i < n; ++i) cb.levels[i] = static_cast<float>(iq::nearest_half(c[i]));
+  for (int i = 0; i < n / 2; ++i) cb.levels[i] = -cb.levels[n - 1 - i];
+  for (int i = 0; i < n - 1; ++i)
+    cb.thresholds[i] =
+        static_cast<float>(0.5 * (static_cast<double>(cb.levels[i]) + cb.levels[i + 1]));
+  for (int i = 1; i < n; ++i)
+    if (!(cb.levels[i] > cb.levels[i - 1])) return IQ_ERR_INVALID_ARGUMENT;
+  *out = cb;
+  return IQ_OK;
+}

@@ -41,6 +41,17 @@ template <int kBits>
 const CodebookB<kBits>& codebook_b();
 const Codebook& codebook();
 
+// The codebook a launch uses: the caller's (an iq_codebook_t of kBits bits,
+// already validated), or the library's C_b when cb is null.
+template <int kBits>
+CodebookB<kBits> codebook_for(const iq_codebook_t* cb) {
+  if (cb == nullptr) return codebook_b<kBits>();
+  CodebookB<kBits> r;
+  for (int i = 0; i < (1 << kBits); ++i) r.level[i] = cb->levels[i];
+  for (int i = 0; i < (1 << kBits) - 1; ++i) r.thr[i] = cb->thresholds[i];
+  return r;
+}
+
 // A paged cache: records of logical position t of (sequence b, KV head g)
 // live in page tables[b * max_pages + t / page_size], slot t % page_size, of
 // pools laid out [n_pages][n_kv_heads][page_size][48] (codes) and
@@ -89,7 +100,7 @@ hipError_t launch_compress(const void* k, const void* v, int dtype, int64_t batc
                            int64_t n_heads, int64_t n_tokens, const float* quats,
                            uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
                            float* v_norms, int64_t capacity, int64_t dst_offset, int bits,
-                           hipStream_t stream);
+                           hipStream_t stream, const iq_codebook_t* cb = nullptr);
 
 // Bulk compression into a paged cache: tokens [0, n_tokens) of every
 // sequence to logical positions dst_offset ..
@@ -103,7 +114,7 @@ hipError_t launch_append(const void* k, const void* v, int dtype, int64_t batch,
                          int64_t n_heads, const float* quats, uint8_t* k_codes,
                          float* k_norms, uint8_t* v_codes, float* v_norms,
                          int64_t capacity, int32_t* seq_lens, int32_t* status,
-                         hipStream_t stream);
+                         hipStream_t stream, const iq_codebook_t* cb = nullptr);
 
 // The new token of a fused decode step (keys and values of every KV head).
 struct StepAppend {
@@ -120,7 +131,8 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, uint8_t* k_code
                          int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                          const float* quats, int64_t batch, int64_t n_q_heads,
                          int64_t n_kv_heads, float scale, float* out, void* workspace,
-                         const StepAppend* append, hipStream_t stream);
+                         const StepAppend* append, hipStream_t stream,
+                         const iq_codebook_t* cb = nullptr);
 
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 
@@ -134,7 +146,8 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                             int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                             const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
                             float* out, float* partials, const StepAppend* append,
-                            const PageTable* pages, int bits, hipStream_t stream);
+                            const PageTable* pages, int bits, hipStream_t stream,
+                            const iq_codebook_t* cb = nullptr);
 
 // Multi-token decode on 3-bit records (group 8): n_tok (2..4) query tokens
 // per sequence, q / out [batch][n_tok][8 n_kv_heads][128]; the plan is
@@ -154,7 +167,7 @@ hipError_t launch_dequant(const uint8_t* k_codes, const float* k_norms, const ui
                           const float* v_norms, const float* quats, const int32_t* seq_lens,
                           int64_t batch, int64_t n_heads, int64_t n_tokens, int64_t capacity,
                           int64_t src_offset, int out_f16, void* k_out, void* v_out,
-                          hipStream_t stream);
+                          hipStream_t stream, const iq_codebook_t* cb = nullptr);
 
 void f16_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
               int64_t* n_splits, int64_t* split_len);

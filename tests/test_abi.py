@@ -401,3 +401,62 @@ def test_stream_read_validation():
     assert L.iq_stream_read_sink_words(4096, 256, 4) == 1
     assert L.iq_stream_read_sink_words(16384 * 3 + 16, 256, 4) == 4
     assert call(nbytes=16384 * 3 + 16, sink_words=3) == 1
+
+
+def test_caller_codebook_validation():
+    """The *_cb entry points reject codebooks the kernels cannot take, before
+    any HIP call: levels not fp16 values, not symmetric, not ascending,
+    thresholds not the midpoints, unknown widths."""
+    from paper_2608_08081_amd import api
+
+    lv, _ = api.iq_codebook_bits(3)
+
+    def compress(cb):
+        # called only with codebooks that are rejected (nothing is launched)
+        return L.iq_compress_kv_cb(A, B, 1, 1, 2, 16, 128, A, ctypes.byref(cb), A, A, B, B, 16,
+                                   0, None)
+
+    def decode(cb):
+        # head_dim 64: IQ_ERR_UNSUPPORTED once the codebook has been accepted
+        return L.iq_decode_attention_cb(A, A, A, B, B, A, 256, 256, A, ctypes.byref(cb), 1, 16,
+                                        2, 64, 0.0, A, A, 1 << 30, None)
+
+    good = api.make_codebook(lv)
+    assert decode(good) == 2                      # head_dim 64: the codebook was accepted
+    bad_half = api.make_codebook(lv)
+    bad_half.levels[7] = 0.1883                   # not an fp16 value
+    bad_half.levels[0] = -0.1883
+    bad_sym = api.make_codebook(lv * np.array([1, 1, 1, 1, 1, 1, 1, 2], np.float32))
+    bad_thr = api.make_codebook(lv)
+    bad_thr.thresholds[2] = 0.5 * (bad_thr.thresholds[2] + bad_thr.thresholds[3])
+    bad_order = api.make_codebook(lv[[0, 2, 1, 3, 4, 6, 5, 7]])
+    big = api.make_codebook(lv * 8)               # |level| >= 1
+    for cb in (bad_half, bad_sym, bad_thr, bad_order, big):
+        assert compress(cb) == 1
+        assert decode(cb) == 1
+    width = api.make_codebook(lv)
+    width.bits = 5
+    assert compress(width) == 2
+    assert L.iq_compress_kv_cb(A, B, 1, 1, 2, 16, 128, A, None, A, A, B, B, 16, 0, None) == 1
+    # dequantization with a codebook: 3-bit codebooks only
+    cb2 = api.make_codebook(api.iq_codebook_bits(2)[0])
+    assert L.iq_dequantize_kv_cb(A, A, B, B, A, ctypes.byref(cb2), None, 1, 2, 16, 128, 16, 0, 1,
+                                 A, B, None) == 2
+
+
+def test_fit_codebook_validation():
+    from paper_2608_08081_amd import api
+
+    x = np.zeros((2, 5, 128), np.float32)        # only zero vectors: nothing to fit
+    q = np.zeros((2, 32, 2, 4), np.float32)
+    q[..., 0] = 1.0
+    cb = _lib.IqCodebook()
+    vp = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    assert L.iq_fit_codebook(vp(x), 5, 2, 128, vp(q), 3, ctypes.byref(cb)) == 1
+    assert L.iq_fit_codebook(vp(x), 5, 2, 128, vp(q), 5, ctypes.byref(cb)) == 2
+    assert L.iq_fit_codebook(vp(x), 5, 2, 64, vp(q), 3, ctypes.byref(cb)) == 2
+    assert L.iq_fit_codebook(vp(x), 0, 2, 128, vp(q), 3, ctypes.byref(cb)) == 1
+    x[1, 3, 7] = 1.0                             # one usable vector: a codebook comes out
+    assert L.iq_fit_codebook(vp(x), 5, 2, 128, vp(q), 3, ctypes.byref(cb)) == 0
+    lv, th = api.codebook_arrays(cb)
+    assert np.all(np.diff(lv) > 0) and np.array_equal(lv, -lv[::-1])
