@@ -238,7 +238,11 @@ iq_status iq_decode_workspace_init(void* workspace, size_t workspace_bytes,
  * workspace : device, >= iq_decode_workspace_bytes(...) bytes, 256-byte
  *             aligned, contents ignored on entry.  Calls that share a
  *             workspace must not overlap in time.
- * n_q_heads / n_kv_heads must be an integer <= 16.
+ * n_q_heads / n_kv_heads must be an integer <= 16.  Caches whose capacity
+ * is a multiple of 16 (>= 16, capacity * 48 < 2^31) with 16-byte aligned
+ * scale arrays run on the matrix cores (query heads in groups of 8 per KV
+ * head; batch and n_kv_heads * ceil(group / 8) <= 65535), other caches on a
+ * vector-unit path with the same results to rounding.
  */
 iq_status iq_decode_attention(const float* q,
                               const uint8_t* k_codes, const float* k_norms,
@@ -332,8 +336,9 @@ iq_status iq_decode_step_noalloc(const float* q, const void* k_new, const void* 
  * new position lies on such a page treats it as having no room (nothing
  * written or attended for that token, seq_lens[b] unchanged, IQ_ERR_CAPACITY
  * OR-ed into *status_dev).  The decode entry
- * points run the group-8 matrix-core path only (IQ_ERR_UNSUPPORTED unless
- * n_q_heads == 8 * n_kv_heads); batch and n_kv_heads <= 65535.  Results
+ * points run on the matrix cores only: n_q_heads / n_kv_heads an integer
+ * <= 16 (IQ_ERR_UNSUPPORTED above), batch and n_kv_heads * ceil(group / 8)
+ * <= 65535 (multi-token decode: n_q_heads == 8 * n_kv_heads).  Results
  * equal those of the contiguous entry points on a cache holding the same
  * records; the workspace is sized by iq_decode_workspace_bytes.
  */
@@ -474,9 +479,10 @@ iq_status iq_compress_kv_bits(const void* k, const void* v, iq_dtype dtype,
 
 /* iq_decode_attention on b-bit records (workspace as sized by
  * iq_decode_workspace_bytes).  b = 2 and b = 4 run on the matrix-core path
- * only: n_q_heads == 8 * n_kv_heads, capacity a multiple of 16 (>= 16) with
- * capacity * 16 * bits < 2^31, 16-byte aligned scale arrays, batch and
- * n_kv_heads <= 65535; otherwise IQ_ERR_UNSUPPORTED. */
+ * only: capacity a multiple of 16 (>= 16) with capacity * 16 * bits < 2^31,
+ * 16-byte aligned scale arrays, batch and n_kv_heads * ceil(group / 8) <=
+ * 65535 (group = n_q_heads / n_kv_heads <= 16); otherwise
+ * IQ_ERR_UNSUPPORTED. */
 iq_status iq_decode_attention_bits(const float* q,
                                    const uint8_t* k_codes, const float* k_norms,
                                    const uint8_t* v_codes, const float* v_norms,

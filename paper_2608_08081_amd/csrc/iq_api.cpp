@@ -378,17 +378,18 @@ float resolve_scale(float softmax_scale) {
   return softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf(static_cast<float>(kDim));
 }
 
-// Shapes the group-8 matrix-core path takes (after check_decode_args):
-// 8 query heads per KV head, rows of whole 16-position batches addressed
-// with 32-bit byte offsets (records of record_bytes bytes), 16-byte aligned
-// scale arrays, and sequences and KV heads as grid dimensions.
+// Shapes the matrix-core path takes (after check_decode_args, which bounds
+// the group by 16): rows of whole 16-position batches addressed with 32-bit
+// byte offsets (records of record_bytes bytes), 16-byte aligned scale
+// arrays, and sequences and (KV head, head group of 8) rows as grid
+// dimensions.
 iq_status check_g8_shape(int64_t n_q_heads, int64_t n_kv_heads, int64_t batch, int64_t capacity,
                          int64_t record_bytes, const float* k_norms, const float* v_norms,
                          const iq::DecodePlan& plan) {
-  if (n_q_heads != 8 * n_kv_heads || plan.g8_batches <= 0) return IQ_ERR_UNSUPPORTED;
+  if (plan.g8_batches <= 0) return IQ_ERR_UNSUPPORTED;
+  const int64_t rows = n_kv_heads * ((n_q_heads / n_kv_heads + 7) / 8);
   if (capacity % 16 || capacity < 16 || capacity * record_bytes > 0x7fffffff ||
-      !iq::aligned(k_norms, 16) || !iq::aligned(v_norms, 16) || batch > 65535 ||
-      n_kv_heads > 65535)
+      !iq::aligned(k_norms, 16) || !iq::aligned(v_norms, 16) || batch > 65535 || rows > 65535)
     return IQ_ERR_UNSUPPORTED;
   return IQ_OK;
 }
@@ -435,8 +436,8 @@ iq_status decode_common(const float* q, const uint8_t* k_codes, const float* k_n
                              const_cast<uint8_t*>(k_codes), const_cast<float*>(k_norms),
                              const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms),
                              const_cast<int32_t*>(seq_lens), capacity, max_seq_len, quats, batch,
-                             n_kv_heads, resolve_scale(softmax_scale), out, parts, nullptr,
-                             nullptr, bits, stream, cb);
+                             n_kv_heads, n_q_heads / n_kv_heads, resolve_scale(softmax_scale),
+                             out, parts, nullptr, nullptr, bits, stream, cb);
   }
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
@@ -518,6 +519,8 @@ iq_status iq_decode_attention_multi(const float* q, const uint8_t* k_codes,
                                          capacity, max_seq_len, quats, batch, n_q_heads,
                                          n_kv_heads, head_dim, out, workspace, SIZE_MAX, &plan);
   if (st != IQ_OK) return st;
+  // multi-token decode runs 8 query heads per KV head
+  if (n_q_heads != 8 * n_kv_heads) return IQ_ERR_UNSUPPORTED;
   const iq_status shape = check_g8_shape(n_q_heads, n_kv_heads, batch, capacity,
                                          iq::kRecordBytes, k_norms, v_norms, plan);
   if (shape != IQ_OK) return shape;
@@ -578,8 +581,9 @@ iq_status step_common(const float* q, const void* k_new, const void* v_new, iq_d
     float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
     e = iq::launch_decode_g8(plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes,
                              k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len, quats,
-                             batch, n_kv_heads, resolve_scale(softmax_scale), out, parts,
-                             &append, nullptr, bits, stream, cb);
+                             batch, n_kv_heads, n_q_heads / n_kv_heads,
+                             resolve_scale(softmax_scale), out, parts, &append, nullptr, bits,
+                             stream, cb);
   }
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
@@ -664,8 +668,12 @@ iq_status check_paged_decode(const float* q, const void* k_codes, const float* k
   if (batch < 0 || n_kv_heads <= 0 || n_q_heads <= 0 || max_seq_len < 0 ||
       max_seq_len > (pt.max_pages << pt.page_shift) || batch > 65535 || n_kv_heads > 65535)
     return IQ_ERR_INVALID_ARGUMENT;
-  // paged caches run on the matrix-core path: 8 query heads per KV head
-  if (n_q_heads != 8 * n_kv_heads) return IQ_ERR_UNSUPPORTED;
+  // paged caches run on the matrix-core path: up to 16 query heads per KV
+  // head, (KV head, head group of 8) rows as a grid dimension
+  if (n_q_heads % n_kv_heads) return IQ_ERR_INVALID_ARGUMENT;
+  if (n_q_heads / n_kv_heads > iq::kMaxGroup ||
+      n_kv_heads * ((n_q_heads / n_kv_heads + 7) / 8) > 65535)
+    return IQ_ERR_UNSUPPORTED;
   if (!q || !k_codes || !k_norms || !v_codes || !v_norms || !seq_lens || !quats || !out ||
       !workspace)
     return IQ_ERR_INVALID_ARGUMENT;
@@ -737,7 +745,8 @@ iq_status iq_decode_attention_paged(const float* q, const uint8_t* k_codes,
       plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, const_cast<uint8_t*>(k_codes),
       const_cast<float*>(k_norms), const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms),
       const_cast<int32_t*>(seq_lens), max_pages * page_size, max_seq_len, quats, batch,
-      n_kv_heads, resolve_scale(softmax_scale), out, parts, nullptr, &pt, 3, stream);
+      n_kv_heads, n_q_heads / n_kv_heads, resolve_scale(softmax_scale), out, parts, nullptr, &pt,
+      3, stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 
@@ -769,7 +778,7 @@ iq_status iq_decode_step_paged(const float* q, const void* k_new, const void* v_
   const hipError_t e = iq::launch_decode_g8(
       plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes, k_norms, v_codes, v_norms,
       seq_lens, max_pages * page_size, max_seq_len, quats, batch, n_kv_heads,
-      resolve_scale(softmax_scale), out, parts, &append, &pt, 3, stream);
+      n_q_heads / n_kv_heads, resolve_scale(softmax_scale), out, parts, &append, &pt, 3, stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 
@@ -794,6 +803,8 @@ iq_status iq_decode_attention_multi_paged(
                           batch, n_q_heads, n_kv_heads, head_dim, out, workspace, SIZE_MAX, pt,
                           &plan);
   if (st != IQ_OK) return st;
+  // multi-token decode runs 8 query heads per KV head
+  if (n_q_heads != 8 * n_kv_heads) return IQ_ERR_UNSUPPORTED;
   if (!iq::mul_ok(batch, n_tokens) || !iq::mul_ok(batch * n_tokens, n_q_heads))
     return IQ_ERR_INVALID_ARGUMENT;
   // the merge kernel's grid takes (sequence, token) as one dimension

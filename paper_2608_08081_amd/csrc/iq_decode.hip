@@ -272,16 +272,18 @@ bool plan_decode(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads, int64_t m
   p.partial_bytes =
       round256(static_cast<size_t>(batch) * n_q_heads * p.n_splits * kPartialFloats * 4);
   size_t need = p.partial_bytes;
-  if (group == 8) {
+  {
+    // the matrix-core path: KV heads in head groups of 8 query heads
+    const int64_t rows = n_kv_heads * ((group + 7) / 8);
     int nb = 0;
     int64_t splits = 0, len = 0;
-    g8_plan(batch, n_kv_heads, max_seq_len, &nb, &splits, &len);
+    g8_plan(batch, rows, max_seq_len, &nb, &splits, &len);
     p.g8_batches = nb;
     p.g8_splits = splits;
     p.g8_split_len = len;
     // one partial per split, and one for the fused step's new token
-    p.g8_partial_bytes = round256(static_cast<size_t>(batch) * n_kv_heads * (splits + 1) * 8 *
-                                  kPartialFloats * 4);
+    p.g8_partial_bytes =
+        round256(static_cast<size_t>(batch) * rows * (splits + 1) * 8 * kPartialFloats * 4);
     if (p.g8_partial_bytes > need) need = p.g8_partial_bytes;
   }
   size_t generic_bytes = p.ticket_bytes + need;
@@ -300,19 +302,20 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, uint8_t* k_code
   const int group = static_cast<int>(n_q_heads / n_kv_heads);
   const bool aligned16 = (reinterpret_cast<uintptr_t>(k_norms) % 16 == 0) &&
                          (reinterpret_cast<uintptr_t>(v_norms) % 16 == 0);
-  // the group-8 kernel addresses one (sequence, KV head) row with 32-bit
-  // byte offsets, loads whole batches of 16 positions below max_seq_len
-  // (clamped to the row: capacity a multiple of 16, at least 16), and takes
-  // KV heads and sequences as grid dimensions (at most 65535 each)
+  // the matrix-core kernel addresses one (sequence, KV head) row with
+  // 32-bit byte offsets, loads whole batches of 16 positions below
+  // max_seq_len (clamped to the row: capacity a multiple of 16, at least
+  // 16), and takes (KV head, head group) rows and sequences as grid
+  // dimensions (at most 65535 each)
   const bool row32 = capacity * kRecordBytes <= 0x7fffffff;
-  const bool grid_ok = batch <= 65535 && n_kv_heads <= 65535;
-  if (group == 8 && plan.g8_batches > 0 && capacity % 16 == 0 && capacity >= 16 && aligned16 &&
-      row32 && grid_ok) {
+  const bool grid_ok = batch <= 65535 && n_kv_heads * ((group + 7) / 8) <= 65535;
+  if (plan.g8_batches > 0 && capacity % 16 == 0 && capacity >= 16 && aligned16 && row32 &&
+      grid_ok) {
     float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
     return launch_decode_g8(plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, k_codes,
                             k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len, quats,
-                            batch, n_kv_heads, scale, out, parts, append, nullptr, 3, stream,
-                            cb);
+                            batch, n_kv_heads, group, scale, out, parts, append, nullptr, 3,
+                            stream, cb);
   }
   if (append) {
     // generic path of the fused step: the append kernel, then attention

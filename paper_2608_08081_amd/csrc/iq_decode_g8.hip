@@ -209,7 +209,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     float* __restrict__ partials, float* __restrict__ out, int64_t capacity, int max_seq_len,
     int n_kv_heads, int n_splits, int split_len, float qscale, CodebookB<kBits> cb,
     const void* __restrict__ k_new, const void* __restrict__ v_new, int new_f16,
-    int32_t* __restrict__ status, PageTable pages) {
+    int32_t* __restrict__ status, PageTable pages, int group) {
   static_assert(kBits == 3 || !kPaged, "paged pools hold 3-bit records");
   constexpr int kRB = record_bytes<kBits>();
   constexpr int kLut = 1 << (2 * kBits);   // pairs of codes
@@ -245,25 +245,34 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   const int lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
 
+  // Grid y: (KV head g, head group vg) with vg < ceil(group / 8): the
+  // workgroup serves query heads g * group + 8 vg + 0 .. nh - 1 (nh = 8,
+  // fewer in the last head group when group is not a multiple of 8); the
+  // other query rows of its products are zero and their results unused.
   const int split = blockIdx.x;
-  const int g = blockIdx.y;
+  const int vshift = group > kHeads ? 1 : 0;
+  const int g = blockIdx.y >> vshift;
+  const int vg = blockIdx.y & vshift;
   const int b = blockIdx.z;
-  const int bg = b * n_kv_heads + g;
-  const int n_q_heads = n_kv_heads * kHeads;
+  const int bg = b * n_kv_heads + g;                          // the cache row
+  const int bgv = b * static_cast<int>(gridDim.y) + blockIdx.y;   // the partial rows
+  const int n_q_heads = n_kv_heads * group;
+  const int hq0 = g * group + kHeads * vg;
+  const int nh = group - kHeads * vg < kHeads ? group - kHeads * vg : kHeads;
   const int n_parts = kAppend ? n_splits + 1 : n_splits;
 
   // The query and rotation loads go out first (thread (head qh, SO(4) block
   // qblk) for tid < 256; the other waves load the same values).
   const int qh = (tid >> 5) & 7, qblk = tid & 31;
-  const f32x4_t qv = *reinterpret_cast<const f32x4_t*>(
-      q + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * kHeads + qh) * kDim +
+  const f32x4_t qload = *reinterpret_cast<const f32x4_t*>(
+      q + (static_cast<int64_t>(b) * n_q_heads + hq0 + (qh < nh ? qh : nh - 1)) * kDim +
       4 * qblk);
+  const f32x4_t qv = qh < nh ? qload : f32x4_t{0.f, 0.f, 0.f, 0.f};
   const f32x4_t* qpar = reinterpret_cast<const f32x4_t*>(
       quats + static_cast<int64_t>(g) * kQuatFloats + 8 * qblk);
   const f32x4_t ql = qpar[0], qr = qpar[1];
-  float* out_bg =
-      out + (static_cast<int64_t>(b) * n_q_heads + static_cast<int64_t>(g) * kHeads) * kDim;
-  float* part_bg = partials + static_cast<int64_t>(bg) * n_parts * (kHeads * kPart);
+  float* out_bg = out + (static_cast<int64_t>(b) * n_q_heads + hq0) * kDim;
+  float* part_bg = partials + static_cast<int64_t>(bgv) * n_parts * (kHeads * kPart);
   // contiguous: the (b, g) row; paged: the pools (positions are placed by
   // the per-batch deltas)
   const int64_t row = kPaged ? 0 : static_cast<int64_t>(bg) * capacity;
@@ -283,7 +292,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
                             : (kPaged ? paged_record(pages, n_kv_heads, b, g, seq0) : row + seq0);
     const bool written = rec >= 0;
     const bool attend_new = written && seq0 < max_seq_len;
-    if (!written && status != nullptr && g == 0 && tid == 0)
+    if (!written && status != nullptr && g == 0 && vg == 0 && tid == 0)
       atomicOr(status, static_cast<int32_t>(IQ_ERR_CAPACITY));
     // waves 4 and 5 compress the new key and value: lane l holds dims 2l,
     // 2l + 1 and the parameters of SO(4) block l / 2
@@ -310,7 +319,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
       const int which = wave - 4;
       if (lane < 4 * kBits) sm.new_rec[which][lane] = wc.word;
       if (lane == 0) sm.new_scale[which] = wc.scale;
-      if (written) {
+      if (written && vg == 0) {   // one head group of the KV head writes
         uint8_t* codes = which == 0 ? k_codes : v_codes;
         float* norms = which == 0 ? k_norms : v_norms;
         if (lane < 4 * kBits) reinterpret_cast<uint32_t*>(codes + rec * kRB)[lane] = wc.word;
@@ -384,7 +393,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
         if (tid < kHeads)
           part_bg[static_cast<int64_t>(split) * (kHeads * kPart) + tid * kPart] = -INFINITY;
       } else {
-        for (int e = tid; e < kHeads * kDim; e += kThreads) out_bg[e] = 0.f;
+        for (int e = tid; e < nh * kDim; e += kThreads) out_bg[e] = 0.f;
       }
       return;
     }
@@ -586,7 +595,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     // place (an empty sequence gives a zero row)
     const f32x4_t o = L > 0.f ? rotate_inverse(O * (1.0f / L), ql, qr, qblk)
                               : f32x4_t{0.f, 0.f, 0.f, 0.f};
-    *reinterpret_cast<f32x4_t*>(out_bg + mh * kDim + md) = o;
+    if (mh < nh) *reinterpret_cast<f32x4_t*>(out_bg + mh * kDim + md) = o;
     return;
   }
   // ---- partial result of this split ------------------------------------------
@@ -606,13 +615,14 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
 // splits; while the grid is small (<= 4 rounds of one workgroup per CU) the
 // split count is raised so that the grid, with the fused step's append
 // workgroup per (sequence, KV head), fills whole rounds, but a split keeps at
-// least one batch per wave.
-void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
-             int64_t* n_splits, int64_t* split_len) {
+// least one batch per wave.  n_rows: the (KV head, head group) rows of the
+// grid per sequence (n_kv_heads * ceil(group / 8)).
+void g8_plan(int64_t batch, int64_t n_rows, int64_t max_seq_len, int* nb, int64_t* n_splits,
+             int64_t* split_len) {
   constexpr int64_t kCus = 256;
   constexpr int64_t kMaxLen = 560;
   const int64_t t = max_seq_len > 0 ? max_seq_len : 1;
-  const int64_t bg = batch * n_kv_heads > 0 ? batch * n_kv_heads : 1;
+  const int64_t bg = batch * n_rows > 0 ? batch * n_rows : 1;
   int64_t s = (t + kMaxLen - 1) / kMaxLen;
   const int64_t wgs = bg * (s + 1);
   if (wgs <= 4 * kCus) {
@@ -634,15 +644,17 @@ void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
 hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const float* q,
                             uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
                             int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
-                            const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
-                            float* out, float* partials, const StepAppend* append,
-                            const PageTable* pages, int bits, hipStream_t stream,
-                            const iq_codebook_t* cb) {
+                            const float* quats, int64_t batch, int64_t n_kv_heads,
+                            int64_t group, float scale, float* out, float* partials,
+                            const StepAppend* append, const PageTable* pages, int bits,
+                            hipStream_t stream, const iq_codebook_t* cb) {
   if (bits != 3 && pages) return hipErrorInvalidValue;
-  // partials per (sequence, KV head): the splits, and the fused step's new
-  // token
+  if (group < 1 || group > 2 * kHeads) return hipErrorInvalidValue;
+  // partials per (sequence, KV head, head group): the splits, and the fused
+  // step's new token
+  const int64_t n_rows = n_kv_heads * ((group + kHeads - 1) / kHeads);
   const int64_t n_parts = append ? n_splits + 1 : n_splits;
-  const dim3 grid(static_cast<unsigned>(n_parts), static_cast<unsigned>(n_kv_heads),
+  const dim3 grid(static_cast<unsigned>(n_parts), static_cast<unsigned>(n_rows),
                   static_cast<unsigned>(batch)),
       block(kThreads);
   // Up to 5 batches per wave the kernel needs at most 128 VGPRs and ~55 KB of
@@ -651,7 +663,7 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   // of at most one round would instead pile two workgroups on some CUs and
   // leave others idle; padding its LDS request keeps one workgroup per CU.
   constexpr int64_t kCus = 256;
-  const bool wide = n_parts * n_kv_heads * batch > kCus;
+  const bool wide = n_parts * n_rows * batch > kCus;
   const size_t lds_pad = wide ? 0 : kOneWorkgroupPadBytes;
   const float qscale = scale * kLog2e;
   const void* k_new = append ? append->k_new : nullptr;
@@ -665,7 +677,7 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                      out, capacity, static_cast<int>(max_seq_len),                              \
                      static_cast<int>(n_kv_heads), static_cast<int>(n_splits),                  \
                      static_cast<int>(split_len), qscale, codebook_for<BITS_>(cb), k_new, v_new, \
-                     new_f16, status, pt)
+                     new_f16, status, pt, static_cast<int>(group))
 #define IQ_LAUNCH_G8_W(NB_, APP_, WIDE_)                \
   if (pages) {                                          \
     IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, true, 3);        \
@@ -704,15 +716,15 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   // the partials of every (sequence, query head) merged by a second launch,
   // which in the fused step also advances the lengths
   if (n_parts > 1) {
-    const dim3 mgrid(static_cast<unsigned>(n_kv_heads * kHeads), static_cast<unsigned>(batch));
+    const dim3 mgrid(static_cast<unsigned>(n_kv_heads * group), static_cast<unsigned>(batch));
     if (append)
       hipLaunchKernelGGL(merge_g8_kernel<true>, mgrid, dim3(kMergeThreads), 0, stream, partials,
                          quats, out, static_cast<int>(n_kv_heads), static_cast<int>(n_parts),
-                         seq_lens, capacity);
+                         seq_lens, capacity, static_cast<int>(group));
     else
       hipLaunchKernelGGL(merge_g8_kernel<false>, mgrid, dim3(kMergeThreads), 0, stream, partials,
                          quats, out, static_cast<int>(n_kv_heads), static_cast<int>(n_parts),
-                         seq_lens, capacity);
+                         seq_lens, capacity, static_cast<int>(group));
     e = hipGetLastError();
   }
   return e;

@@ -416,7 +416,7 @@ hipError_t launch_decode_g8_multi(int nb, int64_t n_splits, int64_t split_len, i
 #define IQ_LAUNCH_MT_MERGE(T_)                                                                 \
   hipLaunchKernelGGL((merge_g8_kernel<false, T_>), mgrid, dim3(kMergeThreads), 0, stream,       \
                      partials, quats, out, static_cast<int>(n_kv_heads),                        \
-                     static_cast<int>(n_splits), nullptr, capacity)
+                     static_cast<int>(n_splits), nullptr, capacity, kHeads)
   if (n_tok == 2) IQ_LAUNCH_MT_MERGE(2);
   else if (n_tok == 3) IQ_LAUNCH_MT_MERGE(3);
   else IQ_LAUNCH_MT_MERGE(4);

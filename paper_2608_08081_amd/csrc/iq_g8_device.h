@@ -448,34 +448,38 @@ __device__ __forceinline__ void value_pairs(const uint32_t* lut, const uint32_t*
 //
 // kTok > 1 (multi-token decode): the partials of each split hold kTok
 // tokens' rows; grid (query head, sequence x token), output row (b, t).
+// group: query heads per KV head; the partial rows are per (sequence, KV
+// head, head group of 8), the layout of the decode kernels' grid.
 template <bool kAppend, int kTok = 1>
 __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     const float* __restrict__ partials, const float* __restrict__ quats, float* __restrict__ out,
-    int n_kv_heads, int n_parts, int32_t* __restrict__ seq_lens, int64_t capacity) {
+    int n_kv_heads, int n_parts, int32_t* __restrict__ seq_lens, int64_t capacity, int group) {
   static_assert(kTok == 1 || !kAppend, "the fused step decodes one token");
   constexpr int kUnroll = 8;   // 8 x 8 = 64 splits per pass, all loads in flight
   __shared__ __attribute__((aligned(16))) float red_o[8][kDim];
   __shared__ float red_m[8], red_l[8];
   const int tid = threadIdx.x;
-  const int n_q_heads = n_kv_heads * kHeads;
+  const int n_q_heads = n_kv_heads * group;
+  const int n_vg = (group + kHeads - 1) / kHeads;
   const int h = blockIdx.x;
   const int bt = blockIdx.y;   // sequence (x token)
   const int b = kTok == 1 ? bt : bt / kTok;
   const int tok = kTok == 1 ? 0 : bt % kTok;
-  const int g = h / kHeads, hh = h % kHeads;
+  const int g = h / group, hr = h - g * group;
+  const int hh = hr % kHeads;
+  const int bgv = (b * n_kv_heads + g) * n_vg + hr / kHeads;   // the partial row
   int seq0 = 0;
   float written = 0.f;
   if (kAppend && h == 0 && tid == 0) {
     seq0 = seq_lens[b];
     // the new-token partial of KV head 0 (every KV head shares the outcome)
-    written = partials[(static_cast<int64_t>(b) * n_kv_heads * n_parts + n_parts - 1) *
+    written = partials[(static_cast<int64_t>(b) * n_kv_heads * n_vg * n_parts + n_parts - 1) *
                            (kHeads * kPart) + 1];
   }
   const int sg = tid >> 5, dq = tid & 31;
   constexpr int kSplitStride = kTok * kHeads * kPart;
   const float* base = partials +
-                      (static_cast<int64_t>(b * n_kv_heads + g) * n_parts * kTok + tok) *
-                          (kHeads * kPart) +
+                      (static_cast<int64_t>(bgv) * n_parts * kTok + tok) * (kHeads * kPart) +
                       hh * kPart;
   // block parameters for the inverse rotation (threads 0..31: block tid)
   const f32x4_t* qg =

@@ -84,11 +84,12 @@ struct DecodePlan {
   int64_t split_len;        // generic path: positions per split
   int64_t n_splits;         // generic path: splits per (sequence, KV head)
   size_t partial_bytes;     // generic path: B * H_q * n_splits * 130 floats
-  int g8_batches;           // group-8 path: 16-position batches per wave (0 = n/a)
-  int64_t g8_splits;        // group-8 path: splits per (sequence, KV head)
-  int64_t g8_split_len;     // group-8 path: positions per split
+  // matrix-core path (any group <= 16, in head groups of 8 query heads)
+  int g8_batches;           // 16-position batches per wave (0 = n/a)
+  int64_t g8_splits;        // splits per (sequence, KV head, head group)
+  int64_t g8_split_len;     // positions per split
   size_t ticket_bytes;      // reserved (0)
-  size_t g8_partial_bytes;  // group-8 path: B * H_kv * (splits + 1) * 8 * 130 floats
+  size_t g8_partial_bytes;  // B * H_kv * head groups * (splits + 1) * 8 * 130 floats
   size_t total_bytes;       // max over both paths
 };
 bool plan_decode(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
@@ -136,18 +137,20 @@ hipError_t launch_decode(const DecodePlan& plan, const float* q, uint8_t* k_code
 
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 
-void g8_plan(int64_t batch, int64_t n_kv_heads, int64_t max_seq_len, int* nb,
-             int64_t* n_splits, int64_t* split_len);
+// n_rows: (KV head, head group of 8 query heads) rows per sequence.
+void g8_plan(int64_t batch, int64_t n_rows, int64_t max_seq_len, int* nb, int64_t* n_splits,
+             int64_t* split_len);
 // pages: null for a contiguous cache ([B][H_kv][capacity] records), else
 // the page table (capacity is then max_pages * page_size).  bits: the
 // records' code width (2, 3 or 4; paged pools need 3).
+// group: query heads per KV head (1 .. 16), served in head groups of 8.
 hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const float* q,
                             uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
                             int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
-                            const float* quats, int64_t batch, int64_t n_kv_heads, float scale,
-                            float* out, float* partials, const StepAppend* append,
-                            const PageTable* pages, int bits, hipStream_t stream,
-                            const iq_codebook_t* cb = nullptr);
+                            const float* quats, int64_t batch, int64_t n_kv_heads,
+                            int64_t group, float scale, float* out, float* partials,
+                            const StepAppend* append, const PageTable* pages, int bits,
+                            hipStream_t stream, const iq_codebook_t* cb = nullptr);
 
 // Multi-token decode on 3-bit records (group 8): n_tok (2..4) query tokens
 // per sequence, q / out [batch][n_tok][8 n_kv_heads][128]; the plan is

@@ -267,7 +267,8 @@ def test_paged_decode_validation():
     assert _paged_decode(max_pages=0) == 1
     assert _paged_decode(bt=None) == 1
     assert _paged_decode(msl=257) == 1           # beyond max_pages * page_size
-    assert _paged_decode(hq=8) == 2              # group 4: not the matrix-core path
+    assert _paged_decode(hq=34) == 2             # group 17 > 16
+    assert _paged_decode(hq=7) == 1              # not a multiple of H_kv
     assert _paged_decode(hd=64) == 2
     assert _paged_decode(batch=70000) == 1
     assert _paged_decode(max_pages=1 << 40) == 1
@@ -317,7 +318,7 @@ def test_bits_entry_point_validation():
                                           None)
     assert dec(bits=5) == 2
     assert dec(bits=1) == 2
-    assert dec(hq=8) == 2                        # group 4: matrix-core path only
+    assert dec(hq=34) == 2                       # group 17 > 16
     assert dec(cap=250, msl=250) == 2            # capacity not a multiple of 16
     assert dec(msl=300) == 1                     # max_seq_len beyond capacity
     assert dec(b=0) == 0
@@ -335,7 +336,7 @@ def test_multi_token_validation():
                                            None)
     assert call(t=5) == 2
     assert call(t=0) == 2
-    assert call(hq=8) == 2                       # group 4: matrix-core path only
+    assert call(hq=8) == 2                       # multi-token: group 8 only
     assert call(cap=250, msl=250) == 2
     assert call(msl=300) == 1
     assert call(wsb=16) == 3
@@ -367,7 +368,7 @@ def test_step_bits_and_multi_paged_validation():
                                      a["bits"], None)
     assert step(bits=5) == 2
     assert step(dtype=7) == 2
-    assert step(hq=8) == 2                       # group 4: matrix-core path only
+    assert step(hq=34) == 2                      # group 17 > 16
     assert step(cap=250, msl=250) == 2           # capacity not a multiple of 16
     assert step(msl=0) == 1                      # the step needs room for a token
     assert step(wsb=16) == 3
@@ -383,7 +384,7 @@ def test_step_bits_and_multi_paged_validation():
     assert mtp(t=5) == 2
     assert mtp(page=48) == 1                     # not a power of two
     assert mtp(msl=257) == 1                     # beyond max_pages * page_size
-    assert mtp(hq=8) == 2
+    assert mtp(hq=8) == 2                        # multi-token: group 8 only
     assert mtp(wsb=16) == 3
     assert mtp(b=0) == 0
     assert mtp(b=21846, t=3) == 2               # 65538 (sequence, token) rows
