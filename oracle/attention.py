@@ -160,3 +160,49 @@ def attention_exact(q, k, v, seq_lens, n_kv_heads, scale=None):
             vv = np.asarray(v[b, g, :n], dtype=np.float64)
             out[b, h] = softmax((kk @ q[b, h]) * sc) @ vv
     return out
+
+
+def decode_fused_rope(q, q_rope, k_packed, k_norms, k_rope, v_packed, v_norms, seq_lens, quats,
+                      levels, scale=None):
+    """Decode attention with the content / RoPE sub-block split that the
+    paper names as the missing piece for latent-attention models (Sec. 5,
+    "MLA/RoPE hard blocker"; Sec. 6): each key is a content part of d dims,
+    compressed as every other key (Alg. 1), and a positional part of d_r
+    dims that carries the rotary phase and therefore is neither rotated nor
+    quantized, stored as given.  Values are content only.  For query head h
+    of KV head g:
+
+        score_j = scale * ( s^K_j (R_g q_h) . C[codeK_j]  +  q_rope_h . k_rope_j )
+        o       = R_g^T sum_j softmax_j(score) s^V_j C[codeV_j]
+
+    q: [B][H_q][d]; q_rope: [B][H_q][d_r]; k_rope: [B][H_r][cap][d_r] with
+    H_r = 1 (one positional key per token shared by every head, as in
+    latent attention) or H_r = H_kv; other arguments as for decode_fused.
+    scale defaults to 1/sqrt(d + d_r).  Returns [B][H_q][d] fp64."""
+    q = np.asarray(q, dtype=np.float64)
+    qr = np.asarray(q_rope, dtype=np.float64)
+    kr = np.asarray(k_rope, dtype=np.float64)
+    bsz, hq, d = q.shape
+    d_r = qr.shape[-1]
+    hkv = k_packed.shape[1]
+    group = hq // hkv
+    sc = _default_scale(d + d_r, scale)
+    rots = _rot.rotation_matrices(np.asarray(quats))
+    bits = _cz.bits_of(levels)
+    out = np.zeros((bsz, hq, d))
+    for b in range(bsz):
+        n = int(seq_lens[b])
+        if n == 0:
+            continue
+        for g in range(hkv):
+            heads = slice(g * group, (g + 1) * group)
+            kt = _cz.dequantize_rotated(_cz.unpack(k_packed[b, g, :n], d, bits),
+                                        k_norms[b, g, :n], levels)     # [n][d] rotated space
+            qt = q[b, heads] @ rots[g].T                                # [G][d]
+            pos = kr[b, g if kr.shape[1] > 1 else 0, :n]                # [n][d_r]
+            scores = (qt @ kt.T + qr[b, heads] @ pos.T) * sc
+            alpha = softmax(scores)
+            vt = _cz.dequantize_rotated(_cz.unpack(v_packed[b, g, :n], d, bits),
+                                        v_norms[b, g, :n], levels)
+            out[b, heads] = (alpha @ vt) @ rots[g]
+    return out
