@@ -558,6 +558,40 @@ iq_status iq_decode_attention_multi_paged(const float* q,
                                           hipStream_t stream);
 
 /*
+ * Content / RoPE sub-block split (Sec. 5, "MLA/RoPE hard blocker"; Sec. 6)
+ * -------------------------------------------------------------------------
+ * Latent-attention models (e.g. DeepSeek-V2) split each key into a content
+ * part and a positional part that carries the rotary phase; the positional
+ * part must be neither rotated nor quantized.  Here the content part of
+ * every key (128 dims) is compressed as any other key (iq_compress_kv), the
+ * positional part (64 dims) is stored by the caller as fp16 as it is, and
+ * values are content only.  For query head h of KV head g:
+ *   score_j = scale * ( s^K_j (R_g q_h) . C[codeK_j] + q_rope_h . k_rope_j )
+ *   o       = R_g^T sum_j softmax_j(score) s^V_j C[codeV_j].
+ *
+ * q, caches, seq_lens, capacity, max_seq_len, quats, out, workspace : as for
+ *            iq_decode_attention (same workspace size).
+ * q_rope   : device fp32 [batch][n_q_heads][64], 16-byte aligned.
+ * k_rope   : device fp16 [batch][n_rope_heads][capacity][64], 16-byte
+ *            aligned; n_rope_heads 1 (one positional key per token shared by
+ *            every head, the latent-attention layout) or n_kv_heads.
+ * rope_dim : 64 (IQ_ERR_UNSUPPORTED otherwise).
+ * softmax_scale : <= 0 selects 1/sqrt(128 + 64).
+ * |q_rope_i| * scale must stay below 4e4 (carried as fp16 hi + lo parts).
+ * Runs on the matrix-core path only (capacity a multiple of 16 and >= 16,
+ * 16-byte aligned scale arrays, group <= 16; IQ_ERR_UNSUPPORTED otherwise).
+ */
+iq_status iq_decode_attention_rope(const float* q, const float* q_rope, const uint8_t* k_codes,
+                                   const float* k_norms, const void* k_rope,
+                                   int64_t n_rope_heads, const uint8_t* v_codes,
+                                   const float* v_norms, const int32_t* seq_lens,
+                                   int64_t capacity, int64_t max_seq_len, const float* quats,
+                                   int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                                   int64_t head_dim, int64_t rope_dim, float softmax_scale,
+                                   float* out, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/*
  * Fitted codebooks (Sec. 3.2 Step 3 on calibration data)
  * ------------------------------------------------------
  * Step 3 quantizes with the Lloyd-Max levels of the marginal of one rotated

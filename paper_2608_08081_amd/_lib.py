@@ -97,6 +97,9 @@ _SIGNATURES = {
     "iq_decode_step_noalloc": (_c_int, [_vp, _vp, _vp, _c_int, _vp, _vp, _vp, _vp, _vp,
                                         _c_i64, _c_i64, _vp, _c_i64, _c_i64, _c_i64, _c_i64,
                                         _c_float, _vp, _vp, _vp]),
+    "iq_decode_attention_rope": (_c_int, [_vp, _vp, _vp, _vp, _vp, _c_i64, _vp, _vp, _vp, _c_i64,
+                                          _c_i64, _vp, _c_i64, _c_i64, _c_i64, _c_i64, _c_i64,
+                                          _c_float, _vp, _vp, _c_size, _vp]),
     "iq_fit_codebook": (_c_int, [_vp, _c_i64, _c_i64, _c_i64, _vp, ctypes.c_int32, _cbp]),
     "iq_compress_kv_cb": (_c_int, [_vp, _vp, _c_int, _c_i64, _c_i64, _c_i64, _c_i64, _vp, _cbp,
                                    _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp]),

@@ -358,6 +358,45 @@ def _decode(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out, workspa
     return out
 
 
+def iq_decode_attention_rope(q, q_rope, k_codes, k_norms, k_rope, v_codes, v_norms, seq_lens,
+                             quats, out=None, workspace=None, max_seq_len=None,
+                             softmax_scale: float = 0.0):
+    """Decode with the content / RoPE sub-block split: q [B][H_q][128] and
+    q_rope [B][H_q][64] fp32; the compressed content cache; k_rope fp16
+    [B][1 or H_kv][cap][64] (stored as given).  Returns out [B][H_q][128]."""
+    if q.dim() != 3 or q.shape[-1] != HEAD_DIM:
+        raise ValueError("q must be [batch][n_q_heads][128]")
+    b, hq, _ = q.shape
+    dev = q.device
+    _require(q, "q", torch.float32, (b, hq, HEAD_DIM), dev)
+    _require(q_rope, "q_rope", torch.float32, (b, hq, 64), dev)
+    if k_codes.dim() != 4 or k_rope.dim() != 4:
+        raise ValueError("k_codes must be [batch][n_kv_heads][capacity][48], "
+                         "k_rope [batch][n_rope_heads][capacity][64]")
+    _, hkv, cap, _ = k_codes.shape
+    hr = k_rope.shape[1]
+    _require(k_codes, "k_codes", torch.uint8, (b, hkv, cap, RECORD_BYTES), dev)
+    _require(v_codes, "v_codes", torch.uint8, (b, hkv, cap, RECORD_BYTES), dev)
+    _require(k_norms, "k_norms", torch.float32, (b, hkv, cap), dev)
+    _require(v_norms, "v_norms", torch.float32, (b, hkv, cap), dev)
+    _require(k_rope, "k_rope", torch.float16, (b, hr, cap, 64), dev)
+    _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
+    _require(quats, "quats", torch.float32, (hkv, 32, 2, 4), dev)
+    if max_seq_len is None:
+        max_seq_len = cap
+    if out is None:
+        out = torch.empty((b, hq, HEAD_DIM), dtype=torch.float32, device=dev)
+    _require(out, "out", torch.float32, (b, hq, HEAD_DIM), dev)
+    if workspace is None:
+        workspace = alloc_workspace(b, hq, hkv, max_seq_len, dev)
+    st = _lib.lib().iq_decode_attention_rope(
+        _ptr(q), _ptr(q_rope), _ptr(k_codes), _ptr(k_norms), _ptr(k_rope), hr, _ptr(v_codes),
+        _ptr(v_norms), _ptr(seq_lens), cap, max_seq_len, _ptr(quats), b, hq, hkv, HEAD_DIM, 64,
+        float(softmax_scale), _ptr(out), _ptr(workspace), workspace.numel(), _stream(dev))
+    _lib.check("iq_decode_attention_rope", st)
+    return out
+
+
 def iq_decode_multi_workspace_bytes(batch, n_tokens, n_q_heads, n_kv_heads, max_seq_len) -> int:
     return int(_lib.lib().iq_decode_multi_workspace_bytes(batch, n_tokens, n_q_heads, n_kv_heads,
                                                           max_seq_len, HEAD_DIM))

@@ -482,6 +482,47 @@ iq_status iq_decode_attention_cb(const float* q, const uint8_t* k_codes, const f
                        workspace, workspace_bytes, cb->bits, cb, stream);
 }
 
+iq_status iq_decode_attention_rope(const float* q, const float* q_rope, const uint8_t* k_codes,
+                                   const float* k_norms, const void* k_rope,
+                                   int64_t n_rope_heads, const uint8_t* v_codes,
+                                   const float* v_norms, const int32_t* seq_lens,
+                                   int64_t capacity, int64_t max_seq_len, const float* quats,
+                                   int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                                   int64_t head_dim, int64_t rope_dim, float softmax_scale,
+                                   float* out, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  if (rope_dim != 64) return IQ_ERR_UNSUPPORTED;
+  iq::DecodePlan plan;
+  const iq_status st = check_decode_args(q, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                                         capacity, max_seq_len, quats, batch, n_q_heads,
+                                         n_kv_heads, head_dim, out, workspace, workspace_bytes,
+                                         &plan);
+  if (st != IQ_OK) return st;
+  if (n_rope_heads != 1 && n_rope_heads != n_kv_heads) return IQ_ERR_INVALID_ARGUMENT;
+  if (!q_rope || !k_rope || !iq::aligned(q_rope, 16) || !iq::aligned(k_rope, 16))
+    return IQ_ERR_INVALID_ARGUMENT;
+  if (!iq::mul_ok(batch * n_rope_heads, capacity + 1) ||
+      !iq::mul_ok(batch * n_rope_heads * (capacity + 1), rope_dim))
+    return IQ_ERR_INVALID_ARGUMENT;
+  // the matrix-core path only
+  const iq_status shape = check_g8_shape(n_q_heads, n_kv_heads, batch, capacity,
+                                         iq::kRecordBytes, k_norms, v_norms, plan);
+  if (shape != IQ_OK) return shape;
+  if (batch == 0) return IQ_OK;
+  const float scale = softmax_scale > 0.f
+                          ? softmax_scale
+                          : 1.0f / sqrtf(static_cast<float>(kDim + rope_dim));
+  const iq::RopeKeys rope{static_cast<const uint16_t*>(k_rope), q_rope,
+                          n_rope_heads == 1 && n_kv_heads > 1 ? 1 : 0};
+  float* parts = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.ticket_bytes);
+  const hipError_t e = iq::launch_decode_g8(
+      plan.g8_batches, plan.g8_splits, plan.g8_split_len, q, const_cast<uint8_t*>(k_codes),
+      const_cast<float*>(k_norms), const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms),
+      const_cast<int32_t*>(seq_lens), capacity, max_seq_len, quats, batch, n_kv_heads,
+      n_q_heads / n_kv_heads, scale, out, parts, nullptr, nullptr, 3, stream, nullptr, &rope);
+  return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
 size_t iq_decode_multi_workspace_bytes(int64_t batch, int64_t n_tokens, int64_t n_q_heads,
                                        int64_t n_kv_heads, int64_t max_seq_len,
                                        int64_t head_dim) {

@@ -72,7 +72,14 @@ namespace {
 // (lane (t, gk) writes its 12 bytes of record t, lane (u, grp) reads the
 // 8-byte window holding bytes 3u..3u+2 of records 4 grp + r); the wave's own
 // LDS operations complete in order.
-template <int NB, int NBX, bool kFull, bool kWide, bool kPaged, int kBits>
+//
+// kRope (the content / RoPE sub-block split, Sec. 5): every position also
+// has a 64-dim positional key kept in fp16, neither rotated nor quantized;
+// its scores come from two more matrix instructions per batch on the
+// positional keys as loaded (rp: lane (t, gk) holds dims 32 m + 8 gk .. + 7
+// of position t in rk[i][m], batch 0 loaded by the caller, batch i + 1 as
+// batch i starts) against the positional query operands qbr.
+template <int NB, int NBX, bool kFull, bool kWide, bool kPaged, int kBits, bool kRope = false>
 __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][kBits],
                                             uint32_t (&vw)[NB][kBits], const uint8_t* vc,
                                             uint32_t koff, const int (&tb)[NB],
@@ -80,29 +87,57 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][kBits],
                                             const u32x4_t (&qb)[4],
                                             const uint32_t* lut, int col, int grp, int nvalid,
                                             int vdw, uint32_t vsh, float qdown, float& m_run,
-                                            float& l_run, float& vmax, f32x4_t (&o_acc)[4]) {
+                                            float& l_run, float& vmax, f32x4_t (&o_acc)[4],
+                                            const uint16_t* rp = nullptr,
+                                            const u32x4_t* rk0 = nullptr,
+                                            const u32x4_t* qbr = nullptr) {
   // ---- phase 1: scores (Table 2 A) -----------------------------------------
   // the value load of batch i goes out as batch i's scores start, so that
   // phase 1 begins without waiting to issue every value load first
   f32x4_t sc[NBX];
+  u32x4_t rk[NBX][2];
+  if constexpr (kRope) {
+    rk[0][0] = rk0[0];
+    rk[0][1] = rk0[1];
+  }
 #pragma unroll
   for (int i = 0; i < NBX; ++i) {
     if (!kFull && 16 * i >= nvalid) break;
     __builtin_amdgcn_sched_barrier(kNoVmemAcross);
     load_value_batch<kBits>(kPaged ? vc + dlt[i] * record_bytes<kBits>() : vc, tb[i], koff,
                             vw[i]);
+    if constexpr (kRope) {
+      if (i + 1 < NBX) {
+        const u32x4_t* src =
+            reinterpret_cast<const u32x4_t*>(rp + static_cast<int64_t>(tb[i + 1] + col) * 64);
+        rk[i + 1][0] = src[grp];
+        rk[i + 1][1] = src[4 + grp];
+      }
+    }
     __builtin_amdgcn_sched_barrier(kNoVmemAcross);
     u32x4_t a[4];
     key_pairs<kBits>(lut, kw[i], a);
     f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) acc = mfma(a[kb], qb[kb], acc);
-    // column col holds the hi (col < 8) or lo (col >= 8) product of head
-    // col % 8: both lanes of the pair get the sum
-#pragma unroll
-    for (int r = 0; r < 4; ++r) acc[r] += xor_lane<8>(acc[r]);
     // lane (col, grp) holds positions 16 i + 4 grp + r of head col % 8
-    f32x4_t x = acc * st.ks[4 * i + grp];
+    f32x4_t x;
+    if constexpr (kRope) {
+      f32x4_t accr = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      accr = mfma(rk[i][0], qbr[0], accr);
+      accr = mfma(rk[i][1], qbr[1], accr);
+      // content score (times the key scale) plus positional score, then the
+      // hi and lo columns of the head joined as below
+      x = acc * st.ks[4 * i + grp] + accr;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) x[r] += xor_lane<8>(x[r]);
+    } else {
+      // column col holds the hi (col < 8) or lo (col >= 8) product of head
+      // col % 8: both lanes of the pair get the sum
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[r] += xor_lane<8>(acc[r]);
+      x = acc * st.ks[4 * i + grp];
+    }
     if (!kFull && 16 * i + 16 > nvalid) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) x[r] = (16 * i + 4 * grp + r < nvalid) ? x[r] : -INFINITY;
@@ -201,7 +236,14 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][kBits],
 // kBits: the records' code width, 3 (the paper's cache) or 2 / 4 (Algorithm
 // 1 with C_2 / C_4: records of 32 / 64 bytes).  Paged pools hold 3-bit
 // records only.
-template <int NB, bool kAppend, bool kWide, bool kPaged, int kBits>
+//
+// kRope: the content / RoPE sub-block split (Sec. 5, "MLA/RoPE hard
+// blocker"): each key also has a 64-dim positional part in fp16
+// (k_rope [b][rope row][capacity][64], rope row g, or 0 when rope_shared),
+// never rotated or quantized, and each query head a positional part
+// (q_rope [b][head][64] fp32); the score adds their dot product.  Decode
+// only (no append), contiguous 3-bit caches.
+template <int NB, bool kAppend, bool kWide, bool kPaged, int kBits, bool kRope = false>
 __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     const float* __restrict__ q, uint8_t* __restrict__ k_codes, float* __restrict__ k_norms,
     uint8_t* __restrict__ v_codes, float* __restrict__ v_norms,
@@ -209,8 +251,11 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     float* __restrict__ partials, float* __restrict__ out, int64_t capacity, int max_seq_len,
     int n_kv_heads, int n_splits, int split_len, float qscale, CodebookB<kBits> cb,
     const void* __restrict__ k_new, const void* __restrict__ v_new, int new_f16,
-    int32_t* __restrict__ status, PageTable pages, int group) {
+    int32_t* __restrict__ status, PageTable pages, int group,
+    const uint16_t* __restrict__ k_rope, const float* __restrict__ q_rope, int rope_shared) {
   static_assert(kBits == 3 || !kPaged, "paged pools hold 3-bit records");
+  static_assert(!kRope || (!kAppend && !kPaged && kBits == 3),
+                "the positional split runs on contiguous 3-bit caches, decode only");
   constexpr int kRB = record_bytes<kBits>();
   constexpr int kLut = 1 << (2 * kBits);   // pairs of codes
   // All LDS of the kernel in one object, the pair table first (address 0:
@@ -218,6 +263,8 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   struct Smem {
     uint32_t lut[kLut];   // fp16 pair table: entry f = (C[f % 2^b], C[f / 2^b])
     uint32_t qop[2][kHeads][kQRowWords];
+    // positional query operands (kRope): fp16 hi / lo pair rows of 32 words
+    uint32_t qop_r[kRope ? 2 : 1][kHeads][kRope ? kRopeRowWords : 1];
     int qexp[kHeads];
     float wave_ml[kWaves][2][kHeads];
     uint32_t new_rec[2][4 * kBits];   // append workgroup: the new key / value record
@@ -268,6 +315,16 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
       q + (static_cast<int64_t>(b) * n_q_heads + hq0 + (qh < nh ? qh : nh - 1)) * kDim +
       4 * qblk);
   const f32x4_t qv = qh < nh ? qload : f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // positional query part (kRope): thread (qh, qblk < 16) holds its dims
+  // 4 qblk .. 4 qblk + 3
+  f32x4_t qrv = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  if constexpr (kRope) {
+    const f32x4_t t = *reinterpret_cast<const f32x4_t*>(
+        q_rope + (static_cast<int64_t>(b) * n_q_heads + hq0 + (qh < nh ? qh : nh - 1)) *
+                     kRopeDim +
+        4 * (qblk & 15));
+    qrv = (qh < nh && qblk < 16) ? t : f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
   const f32x4_t* qpar = reinterpret_cast<const f32x4_t*>(
       quats + static_cast<int64_t>(g) * kQuatFloats + 8 * qblk);
   const f32x4_t ql = qpar[0], qr = qpar[1];
@@ -433,6 +490,21 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   uint32_t kw[NB][kBits], vw[NB][kBits];
   f32x4_t ksl, vsl;
   load_keys<NB, kPaged, kBits>(kc, kn, vn, dlt, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
+  // kRope: the positional keys of the wave's first batch (the others are
+  // loaded one batch ahead while attending); lane (t, gk) takes dims
+  // 8 gk .. + 7 and 32 + 8 gk .. + 7 of position t
+  const uint16_t* rp = nullptr;
+  u32x4_t rk0[2];
+  if constexpr (kRope) {
+    rp = k_rope + (static_cast<int64_t>(b) * (rope_shared ? 1 : n_kv_heads) +
+                   (rope_shared ? 0 : g)) *
+                      capacity * kRopeDim;
+    const int tb0 = wbase < clamp16 ? wbase : clamp16;
+    const u32x4_t* src =
+        reinterpret_cast<const u32x4_t*>(rp + static_cast<int64_t>(tb0 + col) * kRopeDim);
+    rk0[0] = src[grp];
+    rk0[1] = src[4 + grp];
+  }
   // the word of the value window of lane u = col (see value_pairs)
   int vdw;
   uint32_t vsh;
@@ -471,8 +543,13 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     // scale per head: the largest rotated entry is brought below 2^14 (hi
     // and lo parts both normal) and the scale is undone on the scores
     int qexp = 0;
-    const float am = group32_max(
-        fmaxf(fmaxf(fabsf(y[0]), fabsf(y[1])), fmaxf(fabsf(y[2]), fabsf(y[3]))));
+    // kRope: the positional part, scaled like the scores but not rotated,
+    // shares the head's power-of-two operand scale
+    const f32x4_t yr = qrv * qscale;
+    float amx = fmaxf(fmaxf(fabsf(y[0]), fabsf(y[1])), fmaxf(fabsf(y[2]), fabsf(y[3])));
+    if constexpr (kRope)
+      amx = fmaxf(amx, fmaxf(fmaxf(fabsf(yr[0]), fabsf(yr[1])), fmaxf(fabsf(yr[2]), fabsf(yr[3]))));
+    const float am = group32_max(amx);
     if (am > 0.f) {
       int e = 0;
       frexpf(am, &e);   // am < 2^e
@@ -497,6 +574,23 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     qop[0][qh][2 * qblk + 1] = hw[1];
     qop[1][qh][2 * qblk] = lw[0];
     qop[1][qh][2 * qblk + 1] = lw[1];
+    if constexpr (kRope) {
+      if (qblk < 16) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const float x0 = yr[2 * j] * qup, x1 = yr[2 * j + 1] * qup;
+          const _Float16 h0 = static_cast<_Float16>(x0), h1 = static_cast<_Float16>(x1);
+          const _Float16 l0 = static_cast<_Float16>(x0 - static_cast<float>(h0));
+          const _Float16 l1 = static_cast<_Float16>(x1 - static_cast<float>(h1));
+          sm.qop_r[0][qh][2 * qblk + j] =
+              static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h0)) |
+              (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h1)) << 16);
+          sm.qop_r[1][qh][2 * qblk + j] =
+              static_cast<uint32_t>(__builtin_bit_cast(uint16_t, l0)) |
+              (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, l1)) << 16);
+        }
+      }
+    }
     if (qblk == 0) qexp_s[qh] = qexp;
   }
   lds_barrier();   // lut, qop, qexp_s
@@ -511,6 +605,14 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
     qb[kb] = *reinterpret_cast<const u32x4_t*>(&qop[col >> 3][col & 7][16 * grp + 4 * kb]);
+  // positional operands: MFMA m, lane group grp -> dims 32 m + 8 grp .. + 7
+  // (pair words 16 m + 4 grp .. + 3)
+  u32x4_t qbr[2];
+  if constexpr (kRope) {
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+      qbr[m] = *reinterpret_cast<const u32x4_t*>(&sm.qop_r[col >> 3][col & 7][16 * m + 4 * grp]);
+  }
   const float qdown = ldexpf(1.0f, -qexp_s[col & 7]);
   // this wave's scales to its LDS stage (read back per batch).  Lane j
   // holds positions 4j .. 4j+3 of the wave; the value scales of positions at
@@ -537,17 +639,17 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) o_acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if (nvalid == 16 * NB)
-    attend_wave<NB, NB, true, kWide, kPaged, kBits>(kw, vw, vc, koff, tb, dlt, stage[wave], qb,
-                                                    lut, col, grp, nvalid, vdw, vsh, qdown,
-                                                    m_run, l_run, vmax, o_acc);
-  else if (NB > 1 && nvalid == 16 * (NB - 1))
-    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true, kWide, kPaged, kBits>(
+    attend_wave<NB, NB, true, kWide, kPaged, kBits, kRope>(
         kw, vw, vc, koff, tb, dlt, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh, qdown,
-        m_run, l_run, vmax, o_acc);
+        m_run, l_run, vmax, o_acc, rp, rk0, qbr);
+  else if (NB > 1 && nvalid == 16 * (NB - 1))
+    attend_wave<NB, (NB > 1 ? NB - 1 : 1), true, kWide, kPaged, kBits, kRope>(
+        kw, vw, vc, koff, tb, dlt, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh, qdown,
+        m_run, l_run, vmax, o_acc, rp, rk0, qbr);
   else if (nvalid > 0)
-    attend_wave<NB, NB, false, kWide, kPaged, kBits>(kw, vw, vc, koff, tb, dlt, stage[wave], qb,
-                                                     lut, col, grp, nvalid, vdw, vsh, qdown,
-                                                     m_run, l_run, vmax, o_acc);
+    attend_wave<NB, NB, false, kWide, kPaged, kBits, kRope>(
+        kw, vw, vc, koff, tb, dlt, stage[wave], qb, lut, col, grp, nvalid, vdw, vsh, qdown,
+        m_run, l_run, vmax, o_acc, rp, rk0, qbr);
 
   // ---- merge the 8 waves in LDS ---------------------------------------------
   lds_barrier();   // every wave is done with its staging area
@@ -647,8 +749,10 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                             const float* quats, int64_t batch, int64_t n_kv_heads,
                             int64_t group, float scale, float* out, float* partials,
                             const StepAppend* append, const PageTable* pages, int bits,
-                            hipStream_t stream, const iq_codebook_t* cb) {
+                            hipStream_t stream, const iq_codebook_t* cb,
+                            const RopeKeys* rope) {
   if (bits != 3 && pages) return hipErrorInvalidValue;
+  if (rope && (append || pages || bits != 3)) return hipErrorInvalidValue;
   if (group < 1 || group > 2 * kHeads) return hipErrorInvalidValue;
   // partials per (sequence, KV head, head group): the splits, and the fused
   // step's new token
@@ -671,13 +775,18 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   const int new_f16 = append ? append->f16 : 0;
   int32_t* status = append ? append->status : nullptr;
   const PageTable pt = pages ? *pages : PageTable{nullptr, 0, 4, 1};
-#define IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, PAGED_, BITS_)                                     \
-  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_, PAGED_, BITS_>), grid, block, lds_pad, \
-                     stream, q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials,  \
-                     out, capacity, static_cast<int>(max_seq_len),                              \
+  const uint16_t* k_rope = rope ? rope->k_rope : nullptr;
+  const float* q_rope = rope ? rope->q_rope : nullptr;
+  const int rope_shared = rope ? rope->shared : 0;
+#define IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_)                                \
+  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_>), grid, block,   \
+                     lds_pad, stream, q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats,   \
+                     partials, out, capacity, static_cast<int>(max_seq_len),                    \
                      static_cast<int>(n_kv_heads), static_cast<int>(n_splits),                  \
                      static_cast<int>(split_len), qscale, codebook_for<BITS_>(cb), k_new, v_new, \
-                     new_f16, status, pt, static_cast<int>(group))
+                     new_f16, status, pt, static_cast<int>(group), k_rope, q_rope, rope_shared)
+#define IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, PAGED_, BITS_) \
+  IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, false)
 #define IQ_LAUNCH_G8_W(NB_, APP_, WIDE_)                \
   if (pages) {                                          \
     IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, true, 3);        \
@@ -702,15 +811,31 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
     case 4: IQ_LAUNCH_G8(4, APP_); break; \
     default: IQ_LAUNCH_G8(5, APP_); break; \
   }
-  if (append) {
+#define IQ_LAUNCH_G8_ROPE(NB_)                        \
+  if (wide) {                                         \
+    IQ_LAUNCH_G8_K(NB_, false, true, false, 3, true); \
+  } else {                                            \
+    IQ_LAUNCH_G8_K(NB_, false, false, false, 3, true); \
+  }
+  if (rope) {
+    switch (nb) {
+      case 1: IQ_LAUNCH_G8_ROPE(1); break;
+      case 2: IQ_LAUNCH_G8_ROPE(2); break;
+      case 3: IQ_LAUNCH_G8_ROPE(3); break;
+      case 4: IQ_LAUNCH_G8_ROPE(4); break;
+      default: IQ_LAUNCH_G8_ROPE(5); break;
+    }
+  } else if (append) {
     IQ_LAUNCH_G8_NB(true)
   } else {
     IQ_LAUNCH_G8_NB(false)
   }
+#undef IQ_LAUNCH_G8_ROPE
 #undef IQ_LAUNCH_G8_NB
 #undef IQ_LAUNCH_G8
 #undef IQ_LAUNCH_G8_W
 #undef IQ_LAUNCH_G8_WPB
+#undef IQ_LAUNCH_G8_K
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // the partials of every (sequence, query head) merged by a second launch,

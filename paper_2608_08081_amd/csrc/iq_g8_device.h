@@ -32,6 +32,8 @@ constexpr int kMergeThreads = 256;
 constexpr size_t kOneWorkgroupPadBytes = 48 * 1024;
 constexpr int kRecStride = kRecordWords + 1;   // staged record stride (words): spreads banks
 constexpr int kQRowWords = kDim / 2 + 4;  // fp16-pair row of one head, padded (68 words)
+constexpr int kRopeDim = 64;              // positional key / query part (RoPE sub-block)
+constexpr int kRopeRowWords = kRopeDim / 2 + 4;   // its fp16-pair row, padded (36 words)
 constexpr int kHeads = 8;                 // query heads per KV head
 constexpr int kPart = 2 + kDim;           // m, l, o[128] per head
 constexpr float kLog2e = 1.4426950408889634f;

@@ -143,14 +143,25 @@ void g8_plan(int64_t batch, int64_t n_rows, int64_t max_seq_len, int* nb, int64_
 // pages: null for a contiguous cache ([B][H_kv][capacity] records), else
 // the page table (capacity is then max_pages * page_size).  bits: the
 // records' code width (2, 3 or 4; paged pools need 3).
+// The positional parts of a decode with the content / RoPE sub-block split:
+// k_rope fp16 [batch][shared ? 1 : n_kv_heads][capacity][64], q_rope fp32
+// [batch][n_q_heads][64].
+struct RopeKeys {
+  const uint16_t* k_rope;
+  const float* q_rope;
+  int shared;
+};
+
 // group: query heads per KV head (1 .. 16), served in head groups of 8.
+// rope: the positional parts (decode of contiguous 3-bit caches only).
 hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const float* q,
                             uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
                             int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                             const float* quats, int64_t batch, int64_t n_kv_heads,
                             int64_t group, float scale, float* out, float* partials,
                             const StepAppend* append, const PageTable* pages, int bits,
-                            hipStream_t stream, const iq_codebook_t* cb = nullptr);
+                            hipStream_t stream, const iq_codebook_t* cb = nullptr,
+                            const RopeKeys* rope = nullptr);
 
 // Multi-token decode on 3-bit records (group 8): n_tok (2..4) query tokens
 // per sequence, q / out [batch][n_tok][8 n_kv_heads][128]; the plan is

@@ -461,3 +461,19 @@ def test_fit_codebook_validation():
     assert L.iq_fit_codebook(vp(x), 5, 2, 128, vp(q), 3, ctypes.byref(cb)) == 0
     lv, th = api.codebook_arrays(cb)
     assert np.all(np.diff(lv) > 0) and np.array_equal(lv, -lv[::-1])
+
+
+def test_rope_decode_validation():
+    def call(**kw):
+        a = dict(hr=1, rd=64, hq=16, hkv=2, cap=256, msl=256, b=1, qr=A, kr=A)
+        a.update(kw)
+        return L.iq_decode_attention_rope(A, a["qr"], A, A, a["kr"], a["hr"], B, B, A, a["cap"],
+                                          a["msl"], A, a["b"], a["hq"], a["hkv"], 128, a["rd"],
+                                          0.0, A, A, 1 << 30, None)
+    assert call(rd=32) == 2
+    assert call(hr=3) == 1                       # neither shared nor one per KV head
+    assert call(qr=None) == 1
+    assert call(kr=ctypes.c_void_p(0x100008)) == 1   # not 16-byte aligned
+    assert call(cap=250, msl=250) == 2           # capacity not a multiple of 16
+    assert call(hq=34) == 2                      # group 17
+    assert call(b=0) == 0

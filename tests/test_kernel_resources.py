@@ -1,7 +1,8 @@
 """CPU checks of the decode kernel's resource budget (compiled for gfx950
 here, no GPU needed): the instances launched on grids of several rounds
 must let two 512-thread workgroups share a CU (at most 128 VGPRs, at most
-80 KB of LDS), every instance must fit two waves per SIMD with no scratch,
+80 KB of LDS; the positional-split instances: the LDS bound only), every
+instance must fit two waves per SIMD with no scratch,
 and the dynamic LDS the launcher adds to one-round grids must leave room for
 only one workgroup per CU (160 KB of LDS per CU)."""
 
@@ -49,15 +50,19 @@ def test_decode_g8_occupancy_budget(tmp_path):
     pad = eval(re.search(r"kOneWorkgroupPadBytes\s*=\s*([^;]+);", src).group(1))
     ks = _kernels(asm)
     dec = {n: v for n, v in ks.items() if "decode_g8_kernel" in n}
-    # NB 1..5 x (fused step, paged, plain) x grid kind at 3 bits, (fused
-    # step, plain) x grid kind at 2 and 4 bits
-    assert len(dec) == 80, sorted(dec)
+    # NB 1..5 x (fused step, paged, plain, plain with the positional split)
+    # x grid kind at 3 bits, (fused step, plain) x grid kind at 2 and 4 bits
+    assert len(dec) == 90, sorted(dec)
     for name, (vg, lds, priv) in dec.items():
-        m = re.search(r"decode_g8_kernelILi(\d)ELb(\d)ELb(\d)ELb(\d)ELi(\d)EE", name)
-        nb, wide = int(m.group(1)), m.group(3) == "1"
+        m = re.search(r"decode_g8_kernelILi(\d)ELb(\d)ELb(\d)ELb(\d)ELi(\d)ELb(\d)EE", name)
+        nb, wide, rope = int(m.group(1)), m.group(3) == "1", m.group(6) == "1"
         assert priv == 0, f"{name}: scratch {priv}"
         assert vg <= 256, f"{name}: {vg} VGPRs"
-        if wide:
+        if wide and rope:
+            # the positional split's wide instances may hold one workgroup
+            # per CU (their positional operands take up to 32 more VGPRs)
+            assert 2 * lds <= LDS_PER_CU, f"wide rope NB={nb}: {lds} B LDS"
+        elif wide:
             assert vg <= 128, f"wide NB={nb}: {vg} VGPRs, two workgroups no longer fit a CU"
             assert 2 * lds <= LDS_PER_CU, f"wide NB={nb}: {lds} B LDS"
         else:
