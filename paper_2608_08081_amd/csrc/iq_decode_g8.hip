@@ -242,8 +242,14 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][kBits],
 // (k_rope [b][rope row][capacity][64], rope row g, or 0 when rope_shared),
 // never rotated or quantized, and each query head a positional part
 // (q_rope [b][head][64] fp32); the score adds their dot product.  Decode
-// only (no append), contiguous 3-bit caches.
-template <int NB, bool kAppend, bool kWide, bool kPaged, int kBits, bool kRope = false>
+// only (no append), contiguous 3-bit caches; the three arguments of the
+// append (k_new, v_new, new_f16) carry k_rope, q_rope and rope_shared.
+//
+// kAnyGroup: `group` query heads per KV head (1 .. 16) in head groups of 8;
+// otherwise exactly 8 (the argument is not read, and the grid's y index is
+// the KV head).
+template <int NB, bool kAppend, bool kWide, bool kPaged, int kBits, bool kRope = false,
+          bool kAnyGroup = false>
 __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     const float* __restrict__ q, uint8_t* __restrict__ k_codes, float* __restrict__ k_norms,
     uint8_t* __restrict__ v_codes, float* __restrict__ v_norms,
@@ -251,11 +257,13 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     float* __restrict__ partials, float* __restrict__ out, int64_t capacity, int max_seq_len,
     int n_kv_heads, int n_splits, int split_len, float qscale, CodebookB<kBits> cb,
     const void* __restrict__ k_new, const void* __restrict__ v_new, int new_f16,
-    int32_t* __restrict__ status, PageTable pages, int group,
-    const uint16_t* __restrict__ k_rope, const float* __restrict__ q_rope, int rope_shared) {
+    int32_t* __restrict__ status, PageTable pages, int group) {
   static_assert(kBits == 3 || !kPaged, "paged pools hold 3-bit records");
-  static_assert(!kRope || (!kAppend && !kPaged && kBits == 3),
+  static_assert(!kRope || (!kAppend && !kPaged && kBits == 3 && kAnyGroup),
                 "the positional split runs on contiguous 3-bit caches, decode only");
+  const uint16_t* __restrict__ k_rope = static_cast<const uint16_t*>(k_new);
+  const float* __restrict__ q_rope = static_cast<const float*>(v_new);
+  const int rope_shared = new_f16;
   constexpr int kRB = record_bytes<kBits>();
   constexpr int kLut = 1 << (2 * kBits);   // pairs of codes
   // All LDS of the kernel in one object, the pair table first (address 0:
@@ -297,15 +305,17 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   // fewer in the last head group when group is not a multiple of 8); the
   // other query rows of its products are zero and their results unused.
   const int split = blockIdx.x;
-  const int vshift = group > kHeads ? 1 : 0;
+  const int gsize = kAnyGroup ? group : kHeads;
+  const int vshift = kAnyGroup && gsize > kHeads ? 1 : 0;
   const int g = blockIdx.y >> vshift;
   const int vg = blockIdx.y & vshift;
   const int b = blockIdx.z;
   const int bg = b * n_kv_heads + g;                          // the cache row
-  const int bgv = b * static_cast<int>(gridDim.y) + blockIdx.y;   // the partial rows
-  const int n_q_heads = n_kv_heads * group;
-  const int hq0 = g * group + kHeads * vg;
-  const int nh = group - kHeads * vg < kHeads ? group - kHeads * vg : kHeads;
+  const int bgv = kAnyGroup ? b * static_cast<int>(gridDim.y) + blockIdx.y : bg;  // partials
+  const int n_q_heads = n_kv_heads * gsize;
+  const int hq0 = g * gsize + kHeads * vg;
+  const int nh = !kAnyGroup ? kHeads
+                            : (gsize - kHeads * vg < kHeads ? gsize - kHeads * vg : kHeads);
   const int n_parts = kAppend ? n_splits + 1 : n_splits;
 
   // The query and rotation loads go out first (thread (head qh, SO(4) block
@@ -775,18 +785,24 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   const int new_f16 = append ? append->f16 : 0;
   int32_t* status = append ? append->status : nullptr;
   const PageTable pt = pages ? *pages : PageTable{nullptr, 0, 4, 1};
-  const uint16_t* k_rope = rope ? rope->k_rope : nullptr;
-  const float* q_rope = rope ? rope->q_rope : nullptr;
-  const int rope_shared = rope ? rope->shared : 0;
-#define IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_)                                \
-  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_>), grid, block,   \
-                     lds_pad, stream, q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats,   \
-                     partials, out, capacity, static_cast<int>(max_seq_len),                    \
+  // the positional split passes its arguments in the append's three
+  const void* k_side = rope ? static_cast<const void*>(rope->k_rope) : k_new;
+  const void* v_side = rope ? static_cast<const void*>(rope->q_rope) : v_new;
+  const int flag = rope ? rope->shared : new_f16;
+  const bool any_group = group != kHeads;
+#define IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_, ANY_)                          \
+  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_, ANY_>), grid,    \
+                     block, lds_pad, stream, q, k_codes, k_norms, v_codes, v_norms, seq_lens,   \
+                     quats, partials, out, capacity, static_cast<int>(max_seq_len),             \
                      static_cast<int>(n_kv_heads), static_cast<int>(n_splits),                  \
-                     static_cast<int>(split_len), qscale, codebook_for<BITS_>(cb), k_new, v_new, \
-                     new_f16, status, pt, static_cast<int>(group), k_rope, q_rope, rope_shared)
-#define IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, PAGED_, BITS_) \
-  IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, false)
+                     static_cast<int>(split_len), qscale, codebook_for<BITS_>(cb), k_side,      \
+                     v_side, flag, status, pt, static_cast<int>(group))
+#define IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, PAGED_, BITS_)         \
+  if (any_group) {                                                \
+    IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, false, true);  \
+  } else {                                                        \
+    IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, false, false); \
+  }
 #define IQ_LAUNCH_G8_W(NB_, APP_, WIDE_)                \
   if (pages) {                                          \
     IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, true, 3);        \
@@ -811,11 +827,11 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
     case 4: IQ_LAUNCH_G8(4, APP_); break; \
     default: IQ_LAUNCH_G8(5, APP_); break; \
   }
-#define IQ_LAUNCH_G8_ROPE(NB_)                        \
-  if (wide) {                                         \
-    IQ_LAUNCH_G8_K(NB_, false, true, false, 3, true); \
-  } else {                                            \
-    IQ_LAUNCH_G8_K(NB_, false, false, false, 3, true); \
+#define IQ_LAUNCH_G8_ROPE(NB_)                              \
+  if (wide) {                                               \
+    IQ_LAUNCH_G8_K(NB_, false, true, false, 3, true, true);  \
+  } else {                                                  \
+    IQ_LAUNCH_G8_K(NB_, false, false, false, 3, true, true); \
   }
   if (rope) {
     switch (nb) {
@@ -842,14 +858,15 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   // which in the fused step also advances the lengths
   if (n_parts > 1) {
     const dim3 mgrid(static_cast<unsigned>(n_kv_heads * group), static_cast<unsigned>(batch));
-    if (append)
-      hipLaunchKernelGGL(merge_g8_kernel<true>, mgrid, dim3(kMergeThreads), 0, stream, partials,
-                         quats, out, static_cast<int>(n_kv_heads), static_cast<int>(n_parts),
-                         seq_lens, capacity, static_cast<int>(group));
-    else
-      hipLaunchKernelGGL(merge_g8_kernel<false>, mgrid, dim3(kMergeThreads), 0, stream, partials,
-                         quats, out, static_cast<int>(n_kv_heads), static_cast<int>(n_parts),
-                         seq_lens, capacity, static_cast<int>(group));
+#define IQ_LAUNCH_MERGE(APP_, ANY_)                                                            \
+  hipLaunchKernelGGL((merge_g8_kernel<APP_, 1, ANY_>), mgrid, dim3(kMergeThreads), 0, stream,  \
+                     partials, quats, out, static_cast<int>(n_kv_heads),                        \
+                     static_cast<int>(n_parts), seq_lens, capacity, static_cast<int>(group))
+    if (append && any_group) IQ_LAUNCH_MERGE(true, true);
+    else if (append) IQ_LAUNCH_MERGE(true, false);
+    else if (any_group) IQ_LAUNCH_MERGE(false, true);
+    else IQ_LAUNCH_MERGE(false, false);
+#undef IQ_LAUNCH_MERGE
     e = hipGetLastError();
   }
   return e;

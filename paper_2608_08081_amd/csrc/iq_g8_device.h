@@ -450,9 +450,10 @@ __device__ __forceinline__ void value_pairs(const uint32_t* lut, const uint32_t*
 //
 // kTok > 1 (multi-token decode): the partials of each split hold kTok
 // tokens' rows; grid (query head, sequence x token), output row (b, t).
-// group: query heads per KV head; the partial rows are per (sequence, KV
-// head, head group of 8), the layout of the decode kernels' grid.
-template <bool kAppend, int kTok = 1>
+// kAnyGroup: group query heads per KV head (1 .. 16); the partial rows are
+// per (sequence, KV head, head group of 8), the layout of the decode
+// kernels' grid.  Otherwise 8 (group is not read).
+template <bool kAppend, int kTok = 1, bool kAnyGroup = false>
 __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     const float* __restrict__ partials, const float* __restrict__ quats, float* __restrict__ out,
     int n_kv_heads, int n_parts, int32_t* __restrict__ seq_lens, int64_t capacity, int group) {
@@ -461,13 +462,14 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
   __shared__ __attribute__((aligned(16))) float red_o[8][kDim];
   __shared__ float red_m[8], red_l[8];
   const int tid = threadIdx.x;
-  const int n_q_heads = n_kv_heads * group;
-  const int n_vg = (group + kHeads - 1) / kHeads;
+  const int gsize = kAnyGroup ? group : kHeads;
+  const int n_q_heads = n_kv_heads * gsize;
+  const int n_vg = (gsize + kHeads - 1) / kHeads;
   const int h = blockIdx.x;
   const int bt = blockIdx.y;   // sequence (x token)
   const int b = kTok == 1 ? bt : bt / kTok;
   const int tok = kTok == 1 ? 0 : bt % kTok;
-  const int g = h / group, hr = h - g * group;
+  const int g = h / gsize, hr = h - g * gsize;
   const int hh = hr % kHeads;
   const int bgv = (b * n_kv_heads + g) * n_vg + hr / kHeads;   // the partial row
   int seq0 = 0;

@@ -50,11 +50,13 @@ def test_decode_g8_occupancy_budget(tmp_path):
     pad = eval(re.search(r"kOneWorkgroupPadBytes\s*=\s*([^;]+);", src).group(1))
     ks = _kernels(asm)
     dec = {n: v for n, v in ks.items() if "decode_g8_kernel" in n}
-    # NB 1..5 x (fused step, paged, plain, plain with the positional split)
-    # x grid kind at 3 bits, (fused step, plain) x grid kind at 2 and 4 bits
-    assert len(dec) == 90, sorted(dec)
+    # NB 1..5 x grid kind x (group 8, any group) x ((fused step, paged,
+    # plain) at 3 bits, (fused step, plain) at 2 and 4 bits), and NB 1..5 x
+    # grid kind with the positional split (any group)
+    assert len(dec) == 170, sorted(dec)
     for name, (vg, lds, priv) in dec.items():
-        m = re.search(r"decode_g8_kernelILi(\d)ELb(\d)ELb(\d)ELb(\d)ELi(\d)ELb(\d)EE", name)
+        m = re.search(r"decode_g8_kernelILi(\d)ELb(\d)ELb(\d)ELb(\d)ELi(\d)ELb(\d)ELb(\d)EE",
+                      name)
         nb, wide, rope = int(m.group(1)), m.group(3) == "1", m.group(6) == "1"
         assert priv == 0, f"{name}: scratch {priv}"
         assert vg <= 256, f"{name}: {vg} VGPRs"
