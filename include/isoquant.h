@@ -67,13 +67,16 @@ typedef enum iq_status {
   IQ_ERR_CAPACITY = 5            /* written to status_dev by iq_append_token */
 } iq_status;
 
+/* Element types of K/V inputs and outputs.  Entry points take them as an
+ * int32_t `dtype` argument (any other value returns IQ_ERR_UNSUPPORTED). */
 typedef enum iq_dtype {
   IQ_DTYPE_F32 = 0,
   IQ_DTYPE_F16 = 1
 } iq_dtype;
 
-/* Human-readable name of a status code (static string, never NULL). */
-const char* iq_status_string(iq_status s);
+/* Human-readable name of a status code (static string, never NULL; unknown
+ * codes give "unknown status"). */
+const char* iq_status_string(int32_t s);
 
 /* ABI version of this header (major * 100 + minor). */
 int iq_version(void);
@@ -171,7 +174,7 @@ iq_status iq_so4_to_quaternions(const double* m, float* q_pair);
  * Requires 0 <= dst_offset and dst_offset + n_tokens <= capacity.
  * n_tokens == 0 or batch == 0 is a valid no-op.
  */
-iq_status iq_compress_kv(const void* k, const void* v, iq_dtype dtype,
+iq_status iq_compress_kv(const void* k, const void* v, int32_t dtype,
                          int64_t batch, int64_t n_kv_heads, int64_t n_tokens,
                          int64_t head_dim, const float* quats,
                          uint8_t* k_codes, float* k_norms,
@@ -193,7 +196,7 @@ iq_status iq_compress_kv(const void* k, const void* v, iq_dtype dtype,
  *                IQ_ERR_CAPACITY is OR-ed into *status_dev.  Never cleared by
  *                the library.
  */
-iq_status iq_append_token(const void* k_new, const void* v_new, iq_dtype dtype,
+iq_status iq_append_token(const void* k_new, const void* v_new, int32_t dtype,
                           int64_t batch, int64_t n_kv_heads, int64_t head_dim,
                           const float* quats,
                           uint8_t* k_codes, float* k_norms,
@@ -279,7 +282,7 @@ iq_status iq_decode_attention(const float* q,
  * iq_decode_workspace_bytes) and iq_append_token; seq_lens is read and
  * updated in place.
  */
-iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, iq_dtype dtype,
+iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, int32_t dtype,
                          uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
                          int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                          const float* quats, int64_t batch, int64_t n_q_heads,
@@ -308,7 +311,7 @@ iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, i
 #define IQ_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
 
 iq_status iq_decode_step_noalloc(const float* q, const void* k_new, const void* v_new,
-                                 iq_dtype dtype, uint8_t* k_codes, float* k_norms,
+                                 int32_t dtype, uint8_t* k_codes, float* k_norms,
                                  uint8_t* v_codes, float* v_norms, int32_t* seq_lens,
                                  int64_t capacity, int64_t max_seq_len, const float* quats,
                                  int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
@@ -346,7 +349,7 @@ iq_status iq_decode_step_noalloc(const float* q, const void* k_new, const void* 
 /* iq_compress_kv_paged - iq_compress_kv into a paged cache: tokens
  * [0, n_tokens) of every sequence to logical positions dst_offset ..
  * dst_offset + n_tokens - 1 (<= capacity). */
-iq_status iq_compress_kv_paged(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+iq_status iq_compress_kv_paged(const void* k, const void* v, int32_t dtype, int64_t batch,
                                int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
                                const float* quats, uint8_t* k_codes, float* k_norms,
                                uint8_t* v_codes, float* v_norms, int64_t page_size,
@@ -369,7 +372,7 @@ iq_status iq_decode_attention_paged(const float* q, const uint8_t* k_codes,
  * to logical position seq_lens[b] (the caller has mapped its page), if
  * below capacity. */
 iq_status iq_decode_step_paged(const float* q, const void* k_new, const void* v_new,
-                               iq_dtype dtype, uint8_t* k_codes, float* k_norms,
+                               int32_t dtype, uint8_t* k_codes, float* k_norms,
                                uint8_t* v_codes, float* v_norms, int64_t page_size,
                                int64_t n_pages, const int32_t* block_tables, int64_t max_pages,
                                int32_t* seq_lens, int64_t max_seq_len, const float* quats,
@@ -414,7 +417,7 @@ iq_status iq_dequantize_kv(const uint8_t* k_codes, const float* k_norms,
                            const float* quats, const int32_t* seq_lens,
                            int64_t batch, int64_t n_kv_heads, int64_t n_tokens,
                            int64_t head_dim, int64_t capacity, int64_t src_offset,
-                           iq_dtype out_dtype, void* k_out, void* v_out,
+                           int32_t out_dtype, void* k_out, void* v_out,
                            hipStream_t stream);
 
 /*
@@ -469,7 +472,7 @@ iq_status iq_codebook_bits(int bits, float* levels, float* thresholds);
 
 /* iq_compress_kv writing b-bit records: k_codes / v_codes are
  * [batch][n_kv_heads][capacity][16*bits] uint8, 16-byte aligned. */
-iq_status iq_compress_kv_bits(const void* k, const void* v, iq_dtype dtype,
+iq_status iq_compress_kv_bits(const void* k, const void* v, int32_t dtype,
                               int64_t batch, int64_t n_kv_heads, int64_t n_tokens,
                               int64_t head_dim, const float* quats,
                               uint8_t* k_codes, float* k_norms,
@@ -498,7 +501,7 @@ iq_status iq_decode_attention_bits(const float* q,
  * with the cache; requirements as for iq_decode_attention_bits, status and
  * length advance as for iq_decode_step. */
 iq_status iq_decode_step_bits(const float* q, const void* k_new, const void* v_new,
-                              iq_dtype dtype, uint8_t* k_codes, float* k_norms,
+                              int32_t dtype, uint8_t* k_codes, float* k_norms,
                               uint8_t* v_codes, float* v_norms, int32_t* seq_lens,
                               int64_t capacity, int64_t max_seq_len, const float* quats,
                               int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
@@ -639,7 +642,7 @@ iq_status iq_fit_codebook(const float* calib, int64_t n_vectors, int64_t n_kv_he
 
 /* iq_compress_kv with codebook *cb: records of cb->bits bits (layout of
  * iq_compress_kv_bits). */
-iq_status iq_compress_kv_cb(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+iq_status iq_compress_kv_cb(const void* k, const void* v, int32_t dtype, int64_t batch,
                             int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
                             const float* quats, const iq_codebook_t* cb, uint8_t* k_codes,
                             float* k_norms, uint8_t* v_codes, float* v_norms, int64_t capacity,
@@ -658,7 +661,7 @@ iq_status iq_decode_attention_cb(const float* q, const uint8_t* k_codes, const f
 /* iq_decode_step with codebook *cb for the new records and the attention
  * (restrictions of iq_decode_step_bits at cb->bits). */
 iq_status iq_decode_step_cb(const float* q, const void* k_new, const void* v_new,
-                            iq_dtype dtype, uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
+                            int32_t dtype, uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
                             float* v_norms, int32_t* seq_lens, int64_t capacity,
                             int64_t max_seq_len, const float* quats, const iq_codebook_t* cb,
                             int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
@@ -671,7 +674,7 @@ iq_status iq_dequantize_kv_cb(const uint8_t* k_codes, const float* k_norms,
                               const uint8_t* v_codes, const float* v_norms, const float* quats,
                               const iq_codebook_t* cb, const int32_t* seq_lens, int64_t batch,
                               int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
-                              int64_t capacity, int64_t src_offset, iq_dtype out_dtype,
+                              int64_t capacity, int64_t src_offset, int32_t out_dtype,
                               void* k_out, void* v_out, hipStream_t stream);
 
 /*

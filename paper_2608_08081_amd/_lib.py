@@ -11,7 +11,9 @@ import os
 import re
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libisoquant.so")
+# IQ_LIB_PATH selects another build of the same library (e.g. the
+# host-sanitized one of build.py); there is no fallback either way
+LIB_PATH = os.environ.get("IQ_LIB_PATH") or os.path.join(_PKG, "libisoquant.so")
 HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "isoquant.h")
 
 IQ_OK = 0

@@ -37,11 +37,26 @@ def _hipcc() -> str:
     return cand
 
 
-def build(verbose: bool = False, extra_flags: list[str] | None = None) -> str:
+# Host-code sanitizers (AddressSanitizer and UndefinedBehaviorSanitizer on
+# the CPU side only: argument validation, planning, codebook construction,
+# the seeded parameter generator and the fitters; device code is built as
+# usual).  Each -fsanitize goes to the host compilation alone.
+HOST_SANITIZE_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host",
+                       "-fsanitize=undefined", "-Xarch_host", "-fno-sanitize-recover=undefined",
+                       "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+
+
+def build(verbose: bool = False, extra_flags: list[str] | None = None,
+          host_sanitize: bool = False) -> str:
     """Compile every source for gfx950 and link the shared library.
-    Returns the path of the built library."""
+    Returns the path of the built library.  host_sanitize: a separate build
+    with sanitized host code, written to _build/host_sanitize/ (load it with
+    the AddressSanitizer runtime preloaded; IQ_LIB_PATH selects it)."""
     hipcc = _hipcc()
-    bdir = os.path.join(ROOT, "_build")
+    bdir = os.path.join(ROOT, "_build", "host_sanitize") if host_sanitize else \
+        os.path.join(ROOT, "_build")
+    if host_sanitize:
+        extra_flags = list(extra_flags or []) + HOST_SANITIZE_FLAGS
     os.makedirs(bdir, exist_ok=True)
     flags = COMMON_FLAGS + ["-I", INCLUDE, "-I", CSRC] + list(extra_flags or [])
 
@@ -59,9 +74,10 @@ def build(verbose: bool = False, extra_flags: list[str] | None = None) -> str:
 
     with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         objs = list(ex.map(compile_one, SOURCES))
-    out = os.path.join(PKG, LIB_NAME)
+    out = os.path.join(bdir, LIB_NAME) if host_sanitize else os.path.join(PKG, LIB_NAME)
     tmp = out + ".tmp"
-    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+    link_extra = ["-fsanitize=address,undefined", "-shared-libsan"] if host_sanitize else []
+    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs, *link_extra]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
@@ -70,4 +86,4 @@ def build(verbose: bool = False, extra_flags: list[str] | None = None) -> str:
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, host_sanitize="--host-sanitize" in sys.argv))

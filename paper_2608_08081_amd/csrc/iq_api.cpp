@@ -146,7 +146,7 @@ using iq::kDim;
 
 extern "C" {
 
-const char* iq_status_string(iq_status s) {
+const char* iq_status_string(int32_t s) {
   switch (s) {
     case IQ_OK: return "IQ_OK";
     case IQ_ERR_INVALID_ARGUMENT: return "IQ_ERR_INVALID_ARGUMENT";
@@ -155,10 +155,10 @@ const char* iq_status_string(iq_status s) {
     case IQ_ERR_HIP: return "IQ_ERR_HIP";
     case IQ_ERR_CAPACITY: return "IQ_ERR_CAPACITY";
   }
-  return "IQ_ERR_UNKNOWN";
+  return "unknown status";
 }
 
-int iq_version(void) { return 104; }
+int iq_version(void) { return 200; }
 
 iq_status iq_codebook(float* levels, float* thresholds) { return iq_codebook_bits(3, levels, thresholds); }
 
@@ -213,7 +213,7 @@ iq_status iq_make_rotation_variant(uint64_t seed, int64_t n_kv_heads, int64_t he
   return IQ_OK;
 }
 
-iq_status iq_compress_kv(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+iq_status iq_compress_kv(const void* k, const void* v, int32_t dtype, int64_t batch,
                          int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
                          const float* quats, uint8_t* k_codes, float* k_norms,
                          uint8_t* v_codes, float* v_norms, int64_t capacity,
@@ -245,7 +245,7 @@ iq_status check_codebook(const iq_codebook_t* cb) {
   return IQ_OK;
 }
 
-iq_status compress_common(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+iq_status compress_common(const void* k, const void* v, int32_t dtype, int64_t batch,
                           int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
                           const float* quats, uint8_t* k_codes, float* k_norms,
                           uint8_t* v_codes, float* v_norms, int64_t capacity,
@@ -278,7 +278,7 @@ iq_status compress_common(const void* k, const void* v, iq_dtype dtype, int64_t 
 
 }  // namespace
 
-iq_status iq_compress_kv_bits(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+iq_status iq_compress_kv_bits(const void* k, const void* v, int32_t dtype, int64_t batch,
                               int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
                               const float* quats, uint8_t* k_codes, float* k_norms,
                               uint8_t* v_codes, float* v_norms, int64_t capacity,
@@ -287,7 +287,7 @@ iq_status iq_compress_kv_bits(const void* k, const void* v, iq_dtype dtype, int6
                          k_norms, v_codes, v_norms, capacity, dst_offset, bits, nullptr, stream);
 }
 
-iq_status iq_compress_kv_cb(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+iq_status iq_compress_kv_cb(const void* k, const void* v, int32_t dtype, int64_t batch,
                             int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
                             const float* quats, const iq_codebook_t* cb, uint8_t* k_codes,
                             float* k_norms, uint8_t* v_codes, float* v_norms, int64_t capacity,
@@ -298,7 +298,7 @@ iq_status iq_compress_kv_cb(const void* k, const void* v, iq_dtype dtype, int64_
                          k_norms, v_codes, v_norms, capacity, dst_offset, cb->bits, cb, stream);
 }
 
-iq_status iq_append_token(const void* k_new, const void* v_new, iq_dtype dtype, int64_t batch,
+iq_status iq_append_token(const void* k_new, const void* v_new, int32_t dtype, int64_t batch,
                           int64_t n_kv_heads, int64_t head_dim, const float* quats,
                           uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
                           int64_t capacity, int32_t* seq_lens, int32_t* status_dev,
@@ -586,7 +586,7 @@ namespace {
 
 // The fused step on records of `bits` bits with codebook cb (null: C_b); the
 // paths as in decode_common.
-iq_status step_common(const float* q, const void* k_new, const void* v_new, iq_dtype dtype,
+iq_status step_common(const float* q, const void* k_new, const void* v_new, int32_t dtype,
                       uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
                       int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                       const float* quats, int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
@@ -631,7 +631,7 @@ iq_status step_common(const float* q, const void* k_new, const void* v_new, iq_d
 
 }  // namespace
 
-iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, iq_dtype dtype,
+iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, int32_t dtype,
                          uint8_t* k_codes, float* k_norms, uint8_t* v_codes, float* v_norms,
                          int32_t* seq_lens, int64_t capacity, int64_t max_seq_len,
                          const float* quats, int64_t batch, int64_t n_q_heads,
@@ -645,7 +645,7 @@ iq_status iq_decode_step(const float* q, const void* k_new, const void* v_new, i
 }
 
 iq_status iq_decode_step_bits(const float* q, const void* k_new, const void* v_new,
-                              iq_dtype dtype, uint8_t* k_codes, float* k_norms,
+                              int32_t dtype, uint8_t* k_codes, float* k_norms,
                               uint8_t* v_codes, float* v_norms, int32_t* seq_lens,
                               int64_t capacity, int64_t max_seq_len, const float* quats,
                               int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
@@ -659,7 +659,7 @@ iq_status iq_decode_step_bits(const float* q, const void* k_new, const void* v_n
 }
 
 iq_status iq_decode_step_cb(const float* q, const void* k_new, const void* v_new,
-                            iq_dtype dtype, uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
+                            int32_t dtype, uint8_t* k_codes, float* k_norms, uint8_t* v_codes,
                             float* v_norms, int32_t* seq_lens, int64_t capacity,
                             int64_t max_seq_len, const float* quats, const iq_codebook_t* cb,
                             int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
@@ -730,7 +730,7 @@ iq_status check_paged_decode(const float* q, const void* k_codes, const float* k
 
 }  // namespace
 
-iq_status iq_compress_kv_paged(const void* k, const void* v, iq_dtype dtype, int64_t batch,
+iq_status iq_compress_kv_paged(const void* k, const void* v, int32_t dtype, int64_t batch,
                                int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
                                const float* quats, uint8_t* k_codes, float* k_norms,
                                uint8_t* v_codes, float* v_norms, int64_t page_size,
@@ -792,7 +792,7 @@ iq_status iq_decode_attention_paged(const float* q, const uint8_t* k_codes,
 }
 
 iq_status iq_decode_step_paged(const float* q, const void* k_new, const void* v_new,
-                               iq_dtype dtype, uint8_t* k_codes, float* k_norms,
+                               int32_t dtype, uint8_t* k_codes, float* k_norms,
                                uint8_t* v_codes, float* v_norms, int64_t page_size,
                                int64_t n_pages, const int32_t* block_tables, int64_t max_pages,
                                int32_t* seq_lens, int64_t max_seq_len, const float* quats,
@@ -868,7 +868,7 @@ namespace {
 iq_status dequant_common(const uint8_t* k_codes, const float* k_norms, const uint8_t* v_codes,
                          const float* v_norms, const float* quats, const int32_t* seq_lens,
                          int64_t batch, int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
-                         int64_t capacity, int64_t src_offset, iq_dtype out_dtype, void* k_out,
+                         int64_t capacity, int64_t src_offset, int32_t out_dtype, void* k_out,
                          void* v_out, const iq_codebook_t* cb, hipStream_t stream) {
   if (head_dim != kDim) return IQ_ERR_UNSUPPORTED;
   if (out_dtype != IQ_DTYPE_F32 && out_dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
@@ -901,7 +901,7 @@ iq_status iq_dequantize_kv(const uint8_t* k_codes, const float* k_norms,
                            const uint8_t* v_codes, const float* v_norms, const float* quats,
                            const int32_t* seq_lens, int64_t batch, int64_t n_kv_heads,
                            int64_t n_tokens, int64_t head_dim, int64_t capacity,
-                           int64_t src_offset, iq_dtype out_dtype, void* k_out, void* v_out,
+                           int64_t src_offset, int32_t out_dtype, void* k_out, void* v_out,
                            hipStream_t stream) {
   return dequant_common(k_codes, k_norms, v_codes, v_norms, quats, seq_lens, batch, n_kv_heads,
                         n_tokens, head_dim, capacity, src_offset, out_dtype, k_out, v_out,
@@ -912,7 +912,7 @@ iq_status iq_dequantize_kv_cb(const uint8_t* k_codes, const float* k_norms,
                               const uint8_t* v_codes, const float* v_norms, const float* quats,
                               const iq_codebook_t* cb, const int32_t* seq_lens, int64_t batch,
                               int64_t n_kv_heads, int64_t n_tokens, int64_t head_dim,
-                              int64_t capacity, int64_t src_offset, iq_dtype out_dtype,
+                              int64_t capacity, int64_t src_offset, int32_t out_dtype,
                               void* k_out, void* v_out, hipStream_t stream) {
   const iq_status st = check_codebook(cb);
   if (st != IQ_OK) return st;

@@ -43,7 +43,7 @@ iq_status scratch_address(void** out) {
 }  // namespace
 
 extern "C" iq_status iq_decode_step_noalloc(const float* q, const void* k_new, const void* v_new,
-                                            iq_dtype dtype, uint8_t* k_codes, float* k_norms,
+                                            int32_t dtype, uint8_t* k_codes, float* k_norms,
                                             uint8_t* v_codes, float* v_norms, int32_t* seq_lens,
                                             int64_t capacity, int64_t max_seq_len,
                                             const float* quats, int64_t batch,

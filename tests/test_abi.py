@@ -32,7 +32,9 @@ def test_exports_every_declared_symbol():
 def test_status_strings():
     for code, name in _lib.STATUS_NAMES.items():
         assert L.iq_status_string(code).decode() == name
-    assert L.iq_version() >= 100
+    assert L.iq_status_string(99).decode() == "unknown status"
+    assert L.iq_status_string(-1).decode() == "unknown status"
+    assert L.iq_version() >= 200
 
 
 def test_codebook_matches_oracle_bit_for_bit():
