@@ -454,14 +454,11 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     seq0 = seq_lens[b];
     const int seq_w = seq0 < 0 ? 0 : (seq0 > max_seq_len ? max_seq_len : seq0);
     if (start >= seq_w) {
-      // nothing to attend: an empty partial (m = -inf) for the merge, or a
-      // zero output row for an empty sequence
-      if (n_parts > 1) {
-        if (tid < kHeads)
-          part_bg[static_cast<int64_t>(split) * (kHeads * kPart) + tid * kPart] = -INFINITY;
-      } else {
+      // nothing to attend: the merge of these grids reads only the splits
+      // before the length; with a single split, a zero output row for an
+      // empty sequence
+      if (n_parts == 1)
         for (int e = tid; e < nh * kDim; e += kThreads) out_bg[e] = 0.f;
-      }
       return;
     }
     lim = lim < seq_w ? lim : seq_w;
@@ -858,15 +855,30 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   // which in the fused step also advances the lengths
   if (n_parts > 1) {
     const dim3 mgrid(static_cast<unsigned>(n_kv_heads * group), static_cast<unsigned>(batch));
-#define IQ_LAUNCH_MERGE(APP_, ANY_)                                                            \
-  hipLaunchKernelGGL((merge_g8_kernel<APP_, 1, ANY_>), mgrid, dim3(kMergeThreads), 0, stream,  \
-                     partials, quats, out, static_cast<int>(n_kv_heads),                        \
-                     static_cast<int>(n_parts), seq_lens, capacity, static_cast<int>(group))
-    if (append && any_group) IQ_LAUNCH_MERGE(true, true);
-    else if (append) IQ_LAUNCH_MERGE(true, false);
-    else if (any_group) IQ_LAUNCH_MERGE(false, true);
-    else IQ_LAUNCH_MERGE(false, false);
+    // grids of several rounds leave the splits past each length unwritten:
+    // their merge reads the live ones only
+#define IQ_LAUNCH_MERGE_L(APP_, ANY_, LIVE_)                                                   \
+  hipLaunchKernelGGL((merge_g8_kernel<APP_, 1, ANY_, LIVE_>), mgrid, dim3(kMergeThreads), 0,    \
+                     stream, partials, quats, out, static_cast<int>(n_kv_heads),                \
+                     static_cast<int>(n_parts), seq_lens, capacity, static_cast<int>(group),    \
+                     static_cast<int>(split_len), static_cast<int>(max_seq_len))
+#define IQ_LAUNCH_MERGE(APP_, ANY_)        \
+  if (wide) {                              \
+    IQ_LAUNCH_MERGE_L(APP_, ANY_, true);   \
+  } else {                                 \
+    IQ_LAUNCH_MERGE_L(APP_, ANY_, false);  \
+  }
+    if (append && any_group) {
+      IQ_LAUNCH_MERGE(true, true)
+    } else if (append) {
+      IQ_LAUNCH_MERGE(true, false)
+    } else if (any_group) {
+      IQ_LAUNCH_MERGE(false, true)
+    } else {
+      IQ_LAUNCH_MERGE(false, false)
+    }
 #undef IQ_LAUNCH_MERGE
+#undef IQ_LAUNCH_MERGE_L
     e = hipGetLastError();
   }
   return e;

@@ -453,10 +453,17 @@ __device__ __forceinline__ void value_pairs(const uint32_t* lut, const uint32_t*
 // kAnyGroup: group query heads per KV head (1 .. 16); the partial rows are
 // per (sequence, KV head, head group of 8), the layout of the decode
 // kernels' grid.  Otherwise 8 (group is not read).
-template <bool kAppend, int kTok = 1, bool kAnyGroup = false>
+//
+// kLive (grids of several rounds, whose decode workgroups skip the splits
+// past a sequence's length): only the splits holding positions before
+// min(seq_lens[b], max_seq_len) are read (ceil of that over split_len), and
+// the new-token partial; the others were never written.
+template <bool kAppend, int kTok = 1, bool kAnyGroup = false, bool kLive = false>
 __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     const float* __restrict__ partials, const float* __restrict__ quats, float* __restrict__ out,
-    int n_kv_heads, int n_parts, int32_t* __restrict__ seq_lens, int64_t capacity, int group) {
+    int n_kv_heads, int n_parts, int32_t* __restrict__ seq_lens, int64_t capacity, int group,
+    int split_len = 0, int max_seq_len = 0) {
+  static_assert(kTok == 1 || !kLive, "multi-token partials are read in full");
   static_assert(kTok == 1 || !kAppend, "the fused step decodes one token");
   constexpr int kUnroll = 8;   // 8 x 8 = 64 splits per pass, all loads in flight
   __shared__ __attribute__((aligned(16))) float red_o[8][kDim];
@@ -491,14 +498,25 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
   const f32x4_t ql = qg[0], qr = qg[1];
   float M = -INFINITY, L = 0.f;
   f32x4_t O = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  for (int s0 = sg; s0 < n_parts; s0 += 8 * kUnroll) {
+  // partials read: n_iter of them; with kLive the live splits, then (fused
+  // step) the new token's at index n_parts - 1
+  int n_iter = n_parts;
+  if constexpr (kLive) {
+    int seq = seq_lens[b];
+    seq = seq < 0 ? 0 : (seq > max_seq_len ? max_seq_len : seq);
+    n_iter = (seq + split_len - 1) / split_len + (kAppend ? 1 : 0);
+  }
+  auto part_index = [&](int s) {
+    return (kLive && kAppend && s == n_iter - 1) ? n_parts - 1 : s;
+  };
+  for (int s0 = sg; s0 < n_iter; s0 += 8 * kUnroll) {
     float mv[kUnroll], lv[kUnroll];
     f32x2_t mlv[kUnroll];
     f32x4_t ov[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int s = s0 + 8 * u;
-      const int sc = s < n_parts ? s : s0;
+      const int sc = part_index(s < n_iter ? s : s0);
       const float* p = base + static_cast<int64_t>(sc) * kSplitStride;
       mlv[u] = *reinterpret_cast<const f32x2_t*>(p);   // (m, l)
       ov[u] = *reinterpret_cast<const f32x4_t*>(p + 2 + 4 * dq);
@@ -507,7 +525,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      mv[u] = s0 + 8 * u < n_parts ? mlv[u][0] : -INFINITY;
+      mv[u] = s0 + 8 * u < n_iter ? mlv[u][0] : -INFINITY;
       lv[u] = mlv[u][1];
     }
     float Mn = M;
