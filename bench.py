@@ -605,8 +605,8 @@ def run_append8k(args, torch, api, synth, dev):
 
 
 def run_tiny1k(args, torch, api, synth, dev):
-    """The single-head workload: batch 1, one query and one KV head (group 1,
-    the generic split-K path on the vector units), 1024 fp32 keys and values
+    """The single-head workload: batch 1, one query and one KV head (group 1:
+    the matrix-core kernel with one query row of eight in use), 1024 fp32 keys and values
     compressed (iq_compress_kv), then one decode-attention call over them
     (iq_decode_attention), each timed over --layers distinct layers cycled
     (time_graph_calls).  Both are latency-bound at this size."""
@@ -660,12 +660,13 @@ def run_tiny1k(args, torch, api, synth, dev):
         "vs_baseline": None,
         "dtype": "u3 codes, f32 accumulate",
         "data": "synthetic (seeded anisotropic fp32 K/V, compressed on device)",
-        "config": {"workload": f"batch 1, 1 query head, 1 KV head (group 1: generic path), "
+        "config": {"workload": f"batch 1, 1 query head, 1 KV head (group 1), "
                                f"head_dim 128, {t} fp32 keys and values; {nl} distinct layers "
                                "cycled", "context": t},
         "roofline": {"bound": "hbm", "achieved": round(value, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(value / HBM_PEAK_GBS, 5), "traffic": None,
-                     "kernel": "decode_split_kernel + decode_combine_kernel",
+                     "kernel": "decode_g8_kernel<NB, false, false, false, 3, false, true> + "
+                               "merge_g8_kernel<false, 1, true, false>",
                      "bytes_per_launch": dec_bytes, "launch_us": round(us_d, 3)},
         "compress": {"us_per_call": round(us_c, 3), "bytes": comp_bytes,
                      "gbs": round(comp_bytes / (us_c * 1e-6) / 1e9, 2),
