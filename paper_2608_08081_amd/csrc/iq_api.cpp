@@ -391,6 +391,8 @@ iq_status check_g8_shape(int64_t n_q_heads, int64_t n_kv_heads, int64_t batch, i
   if (capacity % 16 || capacity < 16 || capacity * record_bytes > 0x7fffffff ||
       !iq::aligned(k_norms, 16) || !iq::aligned(v_norms, 16) || batch > 65535 || rows > 65535)
     return IQ_ERR_UNSUPPORTED;
+  // work items of a grid of several rounds (32-bit indices)
+  if (batch * rows * (plan.g8_splits + 1) > (int64_t{1} << 30)) return IQ_ERR_UNSUPPORTED;
   return IQ_OK;
 }
 

@@ -213,79 +213,189 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][kBits],
   m_run *= qdown;
 }
 
-// Grid (split, KV head g, sequence b).  The attention workgroups attend the
-// positions before min(seq_lens[b], max_seq_len); their work split does not
-// depend on the length, so every cache load is addressed from the split
-// range alone (clamped to max_seq_len, hence inside the capacity) and issued
-// before the length is read; positions at or past the length are masked.
-// With several splits each workgroup writes its partial (m, l, O) per head;
-// with one it writes the output row itself.
-//
-// kAppend, the fused decode step: one more workgroup per (b, g), split index
-// n_splits, compresses the new key and value (Alg. 1), writes their records
-// at position seq_lens[b] and publishes the new token's score and value as
-// the partial of that extra split (m = -inf when the token is not attended:
-// at capacity, or at or past max_seq_len).  No attention workgroup reads the
+// LDS of the decode kernel, the pair table first (address 0: a lookup
+// address is just field * 4).
+template <int kBits, bool kRope>
+struct G8Smem {
+  uint32_t lut[1 << (2 * kBits)];   // fp16 pair table: entry f = (C[f % 2^b], C[f / 2^b])
+  uint32_t qop[2][kHeads][kQRowWords];
+  // positional query operands (kRope): fp16 hi / lo pair rows of 32 words
+  uint32_t qop_r[kRope ? 2 : 1][kHeads][kRope ? kRopeRowWords : 1];
+  int qexp[kHeads];
+  float wave_ml[kWaves][2][kHeads];
+  uint32_t new_rec[2][4 * kBits];   // append: the new key / value record
+  float new_scale[2];
+  // persistent workgroups: each wave's copy of the current chunk of 64
+  // sequences' inclusive item offsets and clamped lengths
+  int chunk_incl[kWaves][64];
+  int chunk_len[kWaves][64];
+  // the waves' staging areas while attending, their outputs afterwards
+  // (wave_o[w][r][lane] = the lane's accumulator entries r of the four
+  // PV products, as written by the matrix cores)
+  union {
+    WaveStageB<kBits> stage[kWaves];
+    f32x4_t wave_o[kWaves][4][64];
+  };
+};
+
+// Writes the fp16 pair table of the codebook (threads 0 .. 2^(2b) - 1).
+template <int kBits, bool kRope>
+__device__ __forceinline__ void build_pair_table(G8Smem<kBits, kRope>& sm,
+                                                 const CodebookB<kBits>& cb, int tid) {
+  constexpr int kLut = 1 << (2 * kBits);
+  if (tid < kLut) {
+    constexpr int kMask = (1 << kBits) - 1;
+    const uint32_t lo =
+        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & kMask)));
+    const uint32_t hi =
+        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> kBits)));
+    sm.lut[tid] = lo | (hi << 16);
+  }
+}
+
+// The kernel's arguments, as passed (see decode_g8_kernel).
+template <int kBits>
+struct G8Args {
+  const float* q;
+  uint8_t* k_codes;
+  float* k_norms;
+  uint8_t* v_codes;
+  float* v_norms;
+  const int32_t* seq_lens;
+  const float* quats;
+  float* partials;
+  float* out;
+  int64_t capacity;
+  int max_seq_len, n_kv_heads, n_splits, split_len;
+  float qscale;
+  CodebookB<kBits> cb;
+  const void* k_new;
+  const void* v_new;
+  int new_f16;
+  int32_t* status;
+  PageTable pages;
+  int group, batch;
+};
+
+// The fused step's new token for (sequence b, KV head g, head group vg):
+// compresses the new key and value (Alg. 1), writes their records at
+// position seq_lens[b] and publishes the new token's score and value as the
+// partial of split index n_splits (m = -inf when the token is not attended:
+// at capacity, or at or past max_seq_len).  No attention work reads the
 // records being written, and seq_lens is advanced by the merge kernel after
 // every workgroup has read it.
-//
-// kPaged: the cache is a page pool (PageTable); capacity is then the logical
-// capacity max_pages * page_size, and every batch of 16 positions and the
-// new token's slot are located through the page table.
-//
-// kBits: the records' code width, 3 (the paper's cache) or 2 / 4 (Algorithm
-// 1 with C_2 / C_4: records of 32 / 64 bytes).  Paged pools hold 3-bit
-// records only.
-//
-// kRope: the content / RoPE sub-block split (Sec. 5, "MLA/RoPE hard
-// blocker"): each key also has a 64-dim positional part in fp16
-// (k_rope [b][rope row][capacity][64], rope row g, or 0 when rope_shared),
-// never rotated or quantized, and each query head a positional part
-// (q_rope [b][head][64] fp32); the score adds their dot product.  Decode
-// only (no append), contiguous 3-bit caches; the three arguments of the
-// append (k_new, v_new, new_f16) carry k_rope, q_rope and rope_shared.
-//
-// kAnyGroup: `group` query heads per KV head (1 .. 16) in head groups of 8;
-// otherwise exactly 8 (the argument is not read, and the grid's y index is
-// the KV head).
-template <int NB, bool kAppend, bool kWide, bool kPaged, int kBits, bool kRope = false,
-          bool kAnyGroup = false>
-__global__ __launch_bounds__(kThreads) void decode_g8_kernel(
-    const float* __restrict__ q, uint8_t* __restrict__ k_codes, float* __restrict__ k_norms,
-    uint8_t* __restrict__ v_codes, float* __restrict__ v_norms,
-    const int32_t* __restrict__ seq_lens, const float* __restrict__ quats,
-    float* __restrict__ partials, float* __restrict__ out, int64_t capacity, int max_seq_len,
-    int n_kv_heads, int n_splits, int split_len, float qscale, CodebookB<kBits> cb,
-    const void* __restrict__ k_new, const void* __restrict__ v_new, int new_f16,
-    int32_t* __restrict__ status, PageTable pages, int group) {
-  static_assert(kBits == 3 || !kPaged, "paged pools hold 3-bit records");
-  static_assert(!kRope || (!kAppend && !kPaged && kBits == 3 && kAnyGroup),
-                "the positional split runs on contiguous 3-bit caches, decode only");
-  const uint16_t* __restrict__ k_rope = static_cast<const uint16_t*>(k_new);
-  const float* __restrict__ q_rope = static_cast<const float*>(v_new);
-  const int rope_shared = new_f16;
+template <bool kPaged, int kBits, bool kRope>
+__device__ __forceinline__ void append_token(G8Smem<kBits, kRope>& sm, const G8Args<kBits>& a,
+                                             int gsize, int g, int vg, int b, int bgv,
+                                             bool build_lut) {
   constexpr int kRB = record_bytes<kBits>();
-  constexpr int kLut = 1 << (2 * kBits);   // pairs of codes
-  // All LDS of the kernel in one object, the pair table first (address 0:
-  // a lookup address is just field * 4).
-  struct Smem {
-    uint32_t lut[kLut];   // fp16 pair table: entry f = (C[f % 2^b], C[f / 2^b])
-    uint32_t qop[2][kHeads][kQRowWords];
-    // positional query operands (kRope): fp16 hi / lo pair rows of 32 words
-    uint32_t qop_r[kRope ? 2 : 1][kHeads][kRope ? kRopeRowWords : 1];
-    int qexp[kHeads];
-    float wave_ml[kWaves][2][kHeads];
-    uint32_t new_rec[2][4 * kBits];   // append workgroup: the new key / value record
-    float new_scale[2];
-    // the waves' staging areas while attending, their outputs afterwards
-    // (wave_o[w][r][lane] = the lane's accumulator entries r of the four
-    // PV products, as written by the matrix cores)
-    union {
-      WaveStageB<kBits> stage[kWaves];
-      f32x4_t wave_o[kWaves][4][64];
-    };
-  };
-  __shared__ __attribute__((aligned(16))) Smem sm;
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));   // recomputed per item (see attend_split)
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int n_q_heads = a.n_kv_heads * gsize;
+  const int hq0 = g * gsize + kHeads * vg;
+  const int nh = gsize - kHeads * vg < kHeads ? gsize - kHeads * vg : kHeads;
+  const int n_parts = a.n_splits + 1;
+  const int qh = (tid >> 5) & 7, qblk = tid & 31;
+  const f32x4_t qload = *reinterpret_cast<const f32x4_t*>(
+      a.q + (static_cast<int64_t>(b) * n_q_heads + hq0 + (qh < nh ? qh : nh - 1)) * kDim +
+      4 * qblk);
+  const f32x4_t qv = qh < nh ? qload : f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const f32x4_t* qpar = reinterpret_cast<const f32x4_t*>(
+      a.quats + static_cast<int64_t>(g) * kQuatFloats + 8 * qblk);
+  const f32x4_t ql = qpar[0], qr = qpar[1];
+  float* part_bg = a.partials + static_cast<int64_t>(bgv) * n_parts * (kHeads * kPart);
+  const int64_t row = kPaged ? 0 : static_cast<int64_t>(b * a.n_kv_heads + g) * a.capacity;
+
+  const int seq0 = a.seq_lens[b];
+  // record index of the new token (its page's slot, or the row position);
+  // -1 when there is no room: the sequence is at capacity, or (paged) the
+  // slot's page is not mapped.  Then nothing is written, the token is not
+  // attended, the capacity flag is raised, and the new-token partial's l
+  // entry carries -1 so that the merge leaves the length as it is.
+  const int64_t rec = !(seq0 >= 0 && seq0 < a.capacity)
+                          ? -1
+                          : (kPaged ? paged_record(a.pages, a.n_kv_heads, b, g, seq0) : row + seq0);
+  const bool written = rec >= 0;
+  const bool attend_new = written && seq0 < a.max_seq_len;
+  if (!written && a.status != nullptr && g == 0 && vg == 0 && tid == 0)
+    atomicOr(a.status, static_cast<int32_t>(IQ_ERR_CAPACITY));
+  // waves 4 and 5 compress the new key and value: lane l holds dims 2l,
+  // 2l + 1 and the parameters of SO(4) block l / 2
+  if (wave == 4 || wave == 5) {
+    const void* src = wave == 4 ? a.k_new : a.v_new;
+    const int64_t off = (static_cast<int64_t>(b) * a.n_kv_heads + g) * kDim;
+    float x0, x1;
+    if (a.new_f16) {
+      const uint32_t w =
+          reinterpret_cast<const uint32_t*>(static_cast<const __half*>(src) + off)[lane];
+      x0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w)));
+      x1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16)));
+    } else {
+      const f32x2_t w =
+          reinterpret_cast<const f32x2_t*>(static_cast<const float*>(src) + off)[lane];
+      x0 = w[0];
+      x1 = w[1];
+    }
+    const f32x4_t* qs = reinterpret_cast<const f32x4_t*>(
+        a.quats + static_cast<int64_t>(g) * kQuatFloats + 8 * (lane >> 1));
+    const f32x4_t p0 = qs[0], p1 = qs[1];
+    const float qp[8] = {p0[0], p0[1], p0[2], p0[3], p1[0], p1[1], p1[2], p1[3]};
+    const WaveCode wc = compress_vector_wave<kBits>(x0, x1, qp, a.cb, lane);
+    const int which = wave - 4;
+    if (lane < 4 * kBits) sm.new_rec[which][lane] = wc.word;
+    if (lane == 0) sm.new_scale[which] = wc.scale;
+    if (written && vg == 0) {   // one head group of the KV head writes
+      uint8_t* codes = which == 0 ? a.k_codes : a.v_codes;
+      float* norms = which == 0 ? a.k_norms : a.v_norms;
+      if (lane < 4 * kBits) reinterpret_cast<uint32_t*>(codes + rec * kRB)[lane] = wc.word;
+      if (lane == 0) norms[rec] = wc.scale;
+    }
+  }
+  if (build_lut) build_pair_table(sm, a.cb, tid);
+  f32x4_t y = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  if (tid < kRotThreads) y = rotate_forward(qv, ql, qr, qblk, kInvSqrtDim * a.qscale);
+  lds_barrier();   // new_rec, new_scale, lut
+  if (tid >= kRotThreads) return;
+  // score of the new key for head qh: s^K (q_tilde . C[code]) over this
+  // thread's dims 4 qblk .. +3, summed over the head's 32 lanes (y already
+  // carries the score scale, in log2 units)
+  const int md = 4 * qblk;
+  const f32x4_t k4 = decode_record_dims<kBits>(sm.new_rec[0], sm.lut, md);
+  const f32x4_t v4 = decode_record_dims<kBits>(sm.new_rec[1], sm.lut, md);
+  float dot = y[0] * k4[0] + y[1] * k4[1] + y[2] * k4[2] + y[3] * k4[3];
+  dot += xor_lane<1>(dot);
+  dot += xor_lane<2>(dot);
+  dot += xor_lane<4>(dot);
+  dot += xor_lane<8>(dot);
+  dot += xor_lane<16>(dot);
+  float* pp = part_bg + static_cast<int64_t>(a.n_splits) * (kHeads * kPart) + qh * kPart;
+  if (qblk == 0) {
+    pp[0] = attend_new ? dot * sm.new_scale[0] : -INFINITY;
+    pp[1] = written ? 1.0f : -1.0f;
+  }
+  *reinterpret_cast<f32x4_t*>(pp + 2 + md) = sm.new_scale[1] * v4;
+}
+
+// One attention work item: split `split` of the row (KV head g, head group
+// vg) of sequence b, partial row bgv.  It attends the positions before
+// min(seq_lens[b], max_seq_len).  One-round grids: the work split does not
+// depend on the length, so every cache load is addressed from the split range
+// alone (clamped to max_seq_len, hence inside the capacity) and issued before
+// the length is read; positions at or past the length are masked.  kWide:
+// the clamped length is known (seq_w) and the loads cover exactly the
+// positions attended.  With several splits the item writes its partial
+// (m, l, O) per head; with one it writes the output row itself.
+// build_lut: the item writes the pair table (the workgroup's first item).
+template <int NB, bool kAppend, bool kWide, bool kPaged, int kBits, bool kRope>
+__device__ __forceinline__ void attend_split(G8Smem<kBits, kRope>& sm, const G8Args<kBits>& a,
+                                             int gsize, int split, int g, int vg, int b,
+                                             int bgv, int seq_w, bool build_lut) {
+  constexpr int kRB = record_bytes<kBits>();
+  const uint16_t* __restrict__ k_rope = static_cast<const uint16_t*>(a.k_new);
+  const float* __restrict__ q_rope = static_cast<const float*>(a.v_new);
+  const int rope_shared = a.new_f16;
   uint32_t* lut = sm.lut;
   uint32_t(*qop)[kHeads][kQRowWords] = sm.qop;
   int* qexp_s = sm.qexp;
@@ -293,36 +403,38 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   WaveStageB<kBits>* stage = sm.stage;
   f32x4_t(*wave_o)[4][64] = sm.wave_o;
 
-  const int tid = threadIdx.x;
+  // the thread index, opaque to the compiler: in a persistent workgroup's
+  // loop over items, values derived from it are then recomputed per item
+  // rather than held in registers across the loop
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
   // the wave index as a scalar: every per-wave branch is then a scalar
   // branch, and per-wave positions are scalars
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
-
-  // Grid y: (KV head g, head group vg) with vg < ceil(group / 8): the
-  // workgroup serves query heads g * group + 8 vg + 0 .. nh - 1 (nh = 8,
-  // fewer in the last head group when group is not a multiple of 8); the
-  // other query rows of its products are zero and their results unused.
-  const int split = blockIdx.x;
-  const int gsize = kAnyGroup ? group : kHeads;
-  const int vshift = kAnyGroup && gsize > kHeads ? 1 : 0;
-  const int g = blockIdx.y >> vshift;
-  const int vg = blockIdx.y & vshift;
-  const int b = blockIdx.z;
-  const int bg = b * n_kv_heads + g;                          // the cache row
-  const int bgv = kAnyGroup ? b * static_cast<int>(gridDim.y) + blockIdx.y : bg;  // partials
-  const int n_q_heads = n_kv_heads * gsize;
+  const int n_q_heads = a.n_kv_heads * gsize;
   const int hq0 = g * gsize + kHeads * vg;
-  const int nh = !kAnyGroup ? kHeads
-                            : (gsize - kHeads * vg < kHeads ? gsize - kHeads * vg : kHeads);
-  const int n_parts = kAppend ? n_splits + 1 : n_splits;
+  const int nh = gsize - kHeads * vg < kHeads ? gsize - kHeads * vg : kHeads;
+  const int n_parts = kAppend ? a.n_splits + 1 : a.n_splits;
+  const int split_len = a.split_len, max_seq_len = a.max_seq_len;
+  float* out_bg = a.out + (static_cast<int64_t>(b) * n_q_heads + hq0) * kDim;
+  const int start = split * split_len;
+  if constexpr (kWide) {
+    if (start >= seq_w) {
+      // nothing to attend (an empty sequence, with a single split): a zero
+      // output row
+      if (n_parts == 1)
+        for (int e = tid; e < nh * kDim; e += kThreads) out_bg[e] = 0.f;
+      return;
+    }
+  }
 
   // The query and rotation loads go out first (thread (head qh, SO(4) block
   // qblk) for tid < 256; the other waves load the same values).
   const int qh = (tid >> 5) & 7, qblk = tid & 31;
   const f32x4_t qload = *reinterpret_cast<const f32x4_t*>(
-      q + (static_cast<int64_t>(b) * n_q_heads + hq0 + (qh < nh ? qh : nh - 1)) * kDim +
+      a.q + (static_cast<int64_t>(b) * n_q_heads + hq0 + (qh < nh ? qh : nh - 1)) * kDim +
       4 * qblk);
   const f32x4_t qv = qh < nh ? qload : f32x4_t{0.f, 0.f, 0.f, 0.f};
   // positional query part (kRope): thread (qh, qblk < 16) holds its dims
@@ -336,144 +448,38 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
     qrv = (qh < nh && qblk < 16) ? t : f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
   const f32x4_t* qpar = reinterpret_cast<const f32x4_t*>(
-      quats + static_cast<int64_t>(g) * kQuatFloats + 8 * qblk);
+      a.quats + static_cast<int64_t>(g) * kQuatFloats + 8 * qblk);
   const f32x4_t ql = qpar[0], qr = qpar[1];
-  float* out_bg = out + (static_cast<int64_t>(b) * n_q_heads + hq0) * kDim;
-  float* part_bg = partials + static_cast<int64_t>(bgv) * n_parts * (kHeads * kPart);
+  float* part_bg = a.partials + static_cast<int64_t>(bgv) * n_parts * (kHeads * kPart);
   // contiguous: the (b, g) row; paged: the pools (positions are placed by
   // the per-batch deltas)
-  const int64_t row = kPaged ? 0 : static_cast<int64_t>(bg) * capacity;
-  uint8_t* kc = k_codes + row * kRB;
-  uint8_t* vc = v_codes + row * kRB;
+  const int64_t row = kPaged ? 0 : static_cast<int64_t>(b * a.n_kv_heads + g) * a.capacity;
+  const uint8_t* kc = a.k_codes + row * kRB;
+  const uint8_t* vc = a.v_codes + row * kRB;
 
-  if constexpr (kAppend) if (split == n_splits) {
-    // ---- the append workgroup ------------------------------------------------
-    const int seq0 = seq_lens[b];
-    // record index of the new token (its page's slot, or the row position);
-    // -1 when there is no room: the sequence is at capacity, or (paged) the
-    // slot's page is not mapped.  Then nothing is written, the token is not
-    // attended, the capacity flag is raised, and the new-token partial's l
-    // entry carries -1 so that the merge leaves the length as it is.
-    const int64_t rec = !(seq0 >= 0 && seq0 < capacity)
-                            ? -1
-                            : (kPaged ? paged_record(pages, n_kv_heads, b, g, seq0) : row + seq0);
-    const bool written = rec >= 0;
-    const bool attend_new = written && seq0 < max_seq_len;
-    if (!written && status != nullptr && g == 0 && vg == 0 && tid == 0)
-      atomicOr(status, static_cast<int32_t>(IQ_ERR_CAPACITY));
-    // waves 4 and 5 compress the new key and value: lane l holds dims 2l,
-    // 2l + 1 and the parameters of SO(4) block l / 2
-    if (wave == 4 || wave == 5) {
-      const void* src = wave == 4 ? k_new : v_new;
-      const int64_t off = (static_cast<int64_t>(b) * n_kv_heads + g) * kDim;
-      float x0, x1;
-      if (new_f16) {
-        const uint32_t w = reinterpret_cast<const uint32_t*>(static_cast<const __half*>(src) +
-                                                             off)[lane];
-        x0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w)));
-        x1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16)));
-      } else {
-        const f32x2_t w =
-            reinterpret_cast<const f32x2_t*>(static_cast<const float*>(src) + off)[lane];
-        x0 = w[0];
-        x1 = w[1];
-      }
-      const f32x4_t* qs = reinterpret_cast<const f32x4_t*>(
-          quats + static_cast<int64_t>(g) * kQuatFloats + 8 * (lane >> 1));
-      const f32x4_t p0 = qs[0], p1 = qs[1];
-      const float qp[8] = {p0[0], p0[1], p0[2], p0[3], p1[0], p1[1], p1[2], p1[3]};
-      const WaveCode wc = compress_vector_wave<kBits>(x0, x1, qp, cb, lane);
-      const int which = wave - 4;
-      if (lane < 4 * kBits) sm.new_rec[which][lane] = wc.word;
-      if (lane == 0) sm.new_scale[which] = wc.scale;
-      if (written && vg == 0) {   // one head group of the KV head writes
-        uint8_t* codes = which == 0 ? k_codes : v_codes;
-        float* norms = which == 0 ? k_norms : v_norms;
-        if (lane < 4 * kBits) reinterpret_cast<uint32_t*>(codes + rec * kRB)[lane] = wc.word;
-        if (lane == 0) norms[rec] = wc.scale;
-      }
-    }
-    if (tid < kLut) {
-      constexpr int kMask = (1 << kBits) - 1;
-      const uint32_t lo =
-          __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & kMask)));
-      const uint32_t hi =
-          __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> kBits)));
-      lut[tid] = lo | (hi << 16);
-    }
-    f32x4_t y = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    if (tid < kRotThreads) y = rotate_forward(qv, ql, qr, qblk, kInvSqrtDim * qscale);
-    lds_barrier();   // new_rec, new_scale, lut
-    if (tid >= kRotThreads) return;
-    // score of the new key for head qh: s^K (q_tilde . C[code]) over this
-    // thread's dims 4 qblk .. +3, summed over the head's 32 lanes (y already
-    // carries the score scale, in log2 units)
-    const int md = 4 * qblk;
-    const f32x4_t k4 = decode_record_dims<kBits>(sm.new_rec[0], lut, md);
-    const f32x4_t v4 = decode_record_dims<kBits>(sm.new_rec[1], lut, md);
-    float dot = y[0] * k4[0] + y[1] * k4[1] + y[2] * k4[2] + y[3] * k4[3];
-    dot += xor_lane<1>(dot);
-    dot += xor_lane<2>(dot);
-    dot += xor_lane<4>(dot);
-    dot += xor_lane<8>(dot);
-    dot += xor_lane<16>(dot);
-    float* pp = part_bg + static_cast<int64_t>(n_splits) * (kHeads * kPart) + qh * kPart;
-    if (qblk == 0) {
-      pp[0] = attend_new ? dot * sm.new_scale[0] : -INFINITY;
-      pp[1] = written ? 1.0f : -1.0f;
-    }
-    *reinterpret_cast<f32x4_t*>(pp + 2 + md) = sm.new_scale[1] * v4;
-    return;
-  }
-
-  // ---- attention workgroups -------------------------------------------------
   // this wave's run of batches: nbat / 8 each, one more for the first
   // nbat % 8 waves
-  const int start = split * split_len;
   const int nbat = split_len >> 4;
   const int nb_base = nbat / kWaves, nb_rem = nbat % kWaves;
   const int nb_w = nb_base + (wave < nb_rem ? 1 : 0);
   const int wbase = start + 16 * (wave * nb_base + (wave < nb_rem ? wave : nb_rem));
-  // Grids of one round (at most one workgroup per CU) are bound by latency:
-  // their loads are addressed from the split range clamped to max_seq_len
-  // and go out before the length is read.  Grids of several rounds read the
-  // length first and skip splits past it, whose loads would take bandwidth
-  // from the other workgroups.
-  int seq0 = 0;
   int lim = start + split_len < max_seq_len ? start + split_len : max_seq_len;
+  if constexpr (kWide) lim = lim < seq_w ? lim : seq_w;
   // start of the wave's last batch before lim (the clamp of the loads):
   // lim <= max_seq_len <= capacity, a multiple of 16, so every loaded batch
   // lies in the row (in a mapped or the fallback page when paged)
-  auto last_batch = [&](int l) {
-    int c = (l > 0 ? l - 1 : 0) & ~15;
-    c = c < wbase + 16 * (nb_w - 1) ? c : wbase + 16 * (nb_w - 1);
-    return c > 0 ? c : 0;
-  };
-  int clamp16 = last_batch(lim);
-  if constexpr (kWide) {
-    seq0 = seq_lens[b];
-    const int seq_w = seq0 < 0 ? 0 : (seq0 > max_seq_len ? max_seq_len : seq0);
-    if (start >= seq_w) {
-      // nothing to attend: the merge of these grids reads only the splits
-      // before the length; with a single split, a zero output row for an
-      // empty sequence
-      if (n_parts == 1)
-        for (int e = tid; e < nh * kDim; e += kThreads) out_bg[e] = 0.f;
-      return;
-    }
-    lim = lim < seq_w ? lim : seq_w;
-    clamp16 = last_batch(lim);
-  }
+  int clamp16 = (lim > 0 ? lim - 1 : 0) & ~15;
+  clamp16 = clamp16 < wbase + 16 * (nb_w - 1) ? clamp16 : wbase + 16 * (nb_w - 1);
+  clamp16 = clamp16 > 0 ? clamp16 : 0;
   // paged: each batch's record delta (its page's record base minus the
   // page's first logical position; page 0 for an invalid page index).  All
   // NB table entries are read before any is used, and an invalid entry is
   // replaced by a select, so the reads go out together (one round trip).
-  // In grids of several rounds they follow the length read: issued beside
-  // it, they would hold every empty split until they return.
   int64_t dlt[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) dlt[i] = 0;
   if constexpr (kPaged) {
+    const PageTable& pages = a.pages;
     const int32_t* trow = pages.tables + static_cast<int64_t>(b) * pages.max_pages;
     int32_t pg[NB];
 #pragma unroll
@@ -486,12 +492,12 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
       const int t = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
       const int64_t page =
           static_cast<uint32_t>(pg[i]) < static_cast<uint32_t>(pages.n_pages) ? pg[i] : 0;
-      dlt[i] = ((page * n_kv_heads + g) << pages.page_shift) -
+      dlt[i] = ((page * a.n_kv_heads + g) << pages.page_shift) -
                static_cast<int64_t>((t >> pages.page_shift) << pages.page_shift);
     }
   }
-  const float* kn = k_norms + row;
-  const float* vn = v_norms + row;
+  const float* kn = a.k_norms + row;
+  const float* vn = a.v_norms + row;
 
   // ---- the cache loads (keys and scales now, values as the scores proceed)
   uint32_t kw[NB][kBits], vw[NB][kBits];
@@ -503,9 +509,9 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   const uint16_t* rp = nullptr;
   u32x4_t rk0[2];
   if constexpr (kRope) {
-    rp = k_rope + (static_cast<int64_t>(b) * (rope_shared ? 1 : n_kv_heads) +
+    rp = k_rope + (static_cast<int64_t>(b) * (rope_shared ? 1 : a.n_kv_heads) +
                    (rope_shared ? 0 : g)) *
-                      capacity * kRopeDim;
+                      a.capacity * kRopeDim;
     const int tb0 = wbase < clamp16 ? wbase : clamp16;
     const u32x4_t* src =
         reinterpret_cast<const u32x4_t*>(rp + static_cast<int64_t>(tb0 + col) * kRopeDim);
@@ -527,32 +533,30 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   }
 
   // one-round grids: the length, read once the loads are in flight
-  if constexpr (!kWide) seq0 = seq_lens[b];
-  const int seq = seq0 < 0 ? 0 : (seq0 > max_seq_len ? max_seq_len : seq0);
+  int seq;
+  if constexpr (kWide) {
+    seq = seq_w;
+  } else {
+    const int seq0 = a.seq_lens[b];
+    seq = seq0 < 0 ? 0 : (seq0 > max_seq_len ? max_seq_len : seq0);
+  }
   const int end = seq < start + split_len ? seq : start + split_len;
   int nvalid = end - wbase;   // this wave's positions (may be <= 0)
   nvalid = nvalid < 16 * nb_w ? nvalid : 16 * nb_w;
 
   // ---- while the loads fly: LUT and the rotated query --------------------
-  if (tid < kLut) {
-    constexpr int kMask = (1 << kBits) - 1;
-    const uint32_t lo =
-        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & kMask)));
-    const uint32_t hi =
-        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> kBits)));
-    lut[tid] = lo | (hi << 16);
-  }
+  if (build_lut) build_pair_table(sm, a.cb, tid);
   // the 32 blocks of a head are 32 consecutive lanes of one wave, so the
   // rotation needs no barrier
   if (tid < kRotThreads) {
-    const f32x4_t y = rotate_forward(qv, ql, qr, qblk, kInvSqrtDim * qscale);
+    const f32x4_t y = rotate_forward(qv, ql, qr, qblk, kInvSqrtDim * a.qscale);
     // fp16 operands are kept in the normal range by an exact power-of-two
     // scale per head: the largest rotated entry is brought below 2^14 (hi
     // and lo parts both normal) and the scale is undone on the scores
     int qexp = 0;
     // kRope: the positional part, scaled like the scores but not rotated,
     // shares the head's power-of-two operand scale
-    const f32x4_t yr = qrv * qscale;
+    const f32x4_t yr = qrv * a.qscale;
     float amx = fmaxf(fmaxf(fabsf(y[0]), fabsf(y[1])), fmaxf(fabsf(y[2]), fabsf(y[3])));
     if constexpr (kRope)
       amx = fmaxf(amx, fmaxf(fmaxf(fabsf(yr[0]), fabsf(yr[1])), fmaxf(fabsf(yr[2]), fabsf(yr[3]))));
@@ -675,8 +679,8 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   if (tid >= kRotThreads) return;
 
   // thread -> (head h = tid / 32, dims 4 (tid % 32) .. +3), the same
-  // (head, block) as in the query rotation.  A workgroup with nothing to
-  // attend (split at or past the length) ends with M = -inf, L = 0, O = 0.
+  // (head, block) as in the query rotation.  An item with nothing to attend
+  // (split at or past the length) ends with M = -inf, L = 0, O = 0.
   const int mh = qh, md = 4 * qblk;
   float M = -INFINITY;
 #pragma unroll
@@ -716,6 +720,141 @@ __global__ __launch_bounds__(kThreads) void decode_g8_kernel(
   *reinterpret_cast<f32x4_t*>(pp + 2 + md) = O;
 }
 
+// The decode kernel.  Rows of a sequence: (KV head g, head group vg) with vg
+// < ceil(group / 8); row (g, vg) serves query heads g * group + 8 vg + 0 ..
+// nh - 1 (nh = 8, fewer in the last head group when group is not a multiple
+// of 8), whose other query rows of the products are zero and unused.
+//
+// One-round grids (kWide false; at most one workgroup per CU): grid (split,
+// row, sequence b), one work item per workgroup, bound by latency (the
+// loads go out before the length is read).  The fused step (kAppend) adds
+// split index n_splits per (b, row) for the new token.
+//
+// Grids of several rounds (kWide): gridDim.x persistent workgroups.  The
+// work items are the fused step's new tokens (batch * rows of them, kAppend)
+// and then the live splits, enumerated sequence by sequence (a sequence of
+// clamped length L has ceil(L / split_len) live splits, each with its rows;
+// exactly one when there is a single split, so that an empty sequence still
+// gets its zero row); workgroup w takes items w, w + gridDim.x, ...  The
+// lengths are read 64 at a time (one per lane) and turned into item offsets
+// by a prefix sum across the lanes; every wave computes the same mapping.
+// Splits past a length take no workgroup, and the merge kernel reads only
+// the splits before each length.
+//
+// kPaged: the cache is a page pool (PageTable); capacity is then the logical
+// capacity max_pages * page_size, and every batch of 16 positions and the
+// new token's slot are located through the page table.
+//
+// kBits: the records' code width, 3 (the paper's cache) or 2 / 4 (Algorithm
+// 1 with C_2 / C_4: records of 32 / 64 bytes).  Paged pools hold 3-bit
+// records only.
+//
+// kRope: the content / RoPE sub-block split (Sec. 5, "MLA/RoPE hard
+// blocker"): each key also has a 64-dim positional part in fp16
+// (k_rope [b][rope row][capacity][64], rope row g, or 0 when rope_shared),
+// never rotated or quantized, and each query head a positional part
+// (q_rope [b][head][64] fp32); the score adds their dot product.  Decode
+// only (no append), contiguous 3-bit caches; the three arguments of the
+// append (k_new, v_new, new_f16) carry k_rope, q_rope and rope_shared.
+//
+// kAnyGroup: `group` query heads per KV head (1 .. 16) in head groups of 8;
+// otherwise exactly 8 (the argument is not read).
+template <int NB, bool kAppend, bool kWide, bool kPaged, int kBits, bool kRope = false,
+          bool kAnyGroup = false>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWide && !kRope ? 4 : 2)))
+void decode_g8_kernel(G8Args<kBits> a) {
+  static_assert(kBits == 3 || !kPaged, "paged pools hold 3-bit records");
+  static_assert(!kRope || (!kAppend && !kPaged && kBits == 3 && kAnyGroup),
+                "the positional split runs on contiguous 3-bit caches, decode only");
+  __shared__ __attribute__((aligned(16))) G8Smem<kBits, kRope> sm;
+  const int gsize = kAnyGroup ? a.group : kHeads;
+  const int vshift = kAnyGroup && gsize > kHeads ? 1 : 0;
+  const int n_rows = a.n_kv_heads << vshift;
+
+  if constexpr (!kWide) {
+    const int split = blockIdx.x, yrow = blockIdx.y, b = blockIdx.z;
+    const int g = yrow >> vshift, vg = yrow & vshift;
+    const int bgv = b * n_rows + yrow;
+    if constexpr (kAppend) {
+      if (split == a.n_splits) {
+        append_token<kPaged, kBits, kRope>(sm, a, gsize, g, vg, b, bgv, true);
+        return;
+      }
+    }
+    attend_split<NB, kAppend, false, kPaged, kBits, kRope>(sm, a, gsize, split, g, vg, b, bgv,
+                                                          0, true);
+  } else {
+    const int lane = threadIdx.x & 63;
+    const int n_parts = kAppend ? a.n_splits + 1 : a.n_splits;
+    const int n_app = kAppend ? a.batch * n_rows : 0;
+    const int stride = static_cast<int>(gridDim.x);
+    int j = static_cast<int>(blockIdx.x);   // this workgroup's next item
+    bool first = true;
+    // the pair table, once (ordered before its first use by the first
+    // item's barriers)
+    build_pair_table(sm, a.cb, threadIdx.x);
+    if constexpr (kAppend) {
+      for (; j < n_app; j += stride) {
+        if (!first) lds_barrier();   // the previous item is done with the LDS
+        const int b = j / n_rows, yrow = j - b * n_rows;
+        append_token<kPaged, kBits, kRope>(sm, a, gsize, yrow >> vshift, yrow & vshift, b, j,
+                                           false);
+        first = false;
+      }
+    }
+    int base = n_app;   // items before the current chunk of sequences
+    for (int c0 = 0; c0 < a.batch; c0 += 64) {
+      // the chunk's clamped lengths (lane l: sequence c0 + l) and the
+      // inclusive prefix sum of their items
+      int len = 0;
+      if (c0 + lane < a.batch) {
+        const int s = a.seq_lens[c0 + lane];
+        len = s < 0 ? 0 : (s > a.max_seq_len ? a.max_seq_len : s);
+      }
+      // (the divisor opaque here: its reciprocal is then not held in a
+      // register across the loop)
+      int sl = a.split_len;
+      asm volatile("" : "+s"(sl));
+      const int live = c0 + lane < a.batch ? (n_parts == 1 ? 1 : (len + sl - 1) / sl) : 0;
+      int incl = live * n_rows;
+      {
+        // the lane index opaque here, so that the permute addresses are not
+        // computed once and held in registers for the whole kernel
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+          const int t = __builtin_amdgcn_ds_bpermute(((ln - d) & 63) << 2, incl);
+          incl += ln >= d ? t : 0;
+        }
+      }
+      const int total = __builtin_amdgcn_readlane(incl, 63);
+      // kept in the wave's LDS copy rather than in registers across the items
+      const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+      sm.chunk_incl[wv][lane] = incl;
+      sm.chunk_len[wv][lane] = len;
+      for (; j < base + total; j += stride) {
+        const int r = j - base;
+        // the item's sequence: the lanes whose inclusive prefix is <= r
+        // (a prefix of the lanes: the sums do not decrease) come before it.
+        // The wave's own LDS writes are complete before its later reads.
+        const int inc = sm.chunk_incl[wv][threadIdx.x & 63];
+        const int bi = __builtin_popcountll(__ballot(inc <= r));
+        const int excl = bi > 0 ? __builtin_amdgcn_readlane(inc, bi - 1) : 0;
+        const int seq_w = sm.chunk_len[wv][bi];
+        const int rr = r - excl;
+        const int split = rr / n_rows, yrow = rr - split * n_rows;
+        const int b = c0 + bi;
+        if (!first) lds_barrier();   // the previous item is done with the LDS
+        attend_split<NB, kAppend, true, kPaged, kBits, kRope>(
+            sm, a, gsize, split, yrow >> vshift, yrow & vshift, b, b * n_rows + yrow, seq_w,
+            false);
+        first = false;
+      }
+      base += total;
+    }
+  }
+}
 }  // namespace
 
 // Split plan of the group-8 path: splits per (sequence, KV head) and their
@@ -765,17 +904,24 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   // step's new token
   const int64_t n_rows = n_kv_heads * ((group + kHeads - 1) / kHeads);
   const int64_t n_parts = append ? n_splits + 1 : n_splits;
-  const dim3 grid(static_cast<unsigned>(n_parts), static_cast<unsigned>(n_rows),
-                  static_cast<unsigned>(batch)),
-      block(kThreads);
   // Up to 5 batches per wave the kernel needs at most 128 VGPRs and ~55 KB of
-  // LDS, so two workgroups fit on a CU: a grid of several rounds then runs
-  // one workgroup's prologue and merge beside another's attention.  A grid
-  // of at most one round would instead pile two workgroups on some CUs and
-  // leave others idle; padding its LDS request keeps one workgroup per CU.
+  // LDS, so two workgroups fit on a CU.  A grid of at most one round gets one
+  // workgroup per work item, and its LDS request is padded so that no CU
+  // takes two while another idles.  Larger grids run two persistent
+  // workgroups per CU over the work items (fewer when there are fewer
+  // items): one workgroup's prologue and merge then run beside the other's
+  // attention, and splits past a length take no workgroup.
   constexpr int64_t kCus = 256;
   const bool wide = n_parts * n_rows * batch > kCus;
   const size_t lds_pad = wide ? 0 : kOneWorkgroupPadBytes;
+  const int64_t n_items = n_parts * n_rows * batch;
+  if (n_items > (int64_t{1} << 30)) return hipErrorInvalidValue;   // 32-bit item indices
+  // (the positional split's wide instances hold one workgroup per CU)
+  const int64_t workers = (rope ? 1 : 2) * kCus;
+  const dim3 grid = wide ? dim3(static_cast<unsigned>(n_items < workers ? n_items : workers))
+                         : dim3(static_cast<unsigned>(n_parts), static_cast<unsigned>(n_rows),
+                                static_cast<unsigned>(batch));
+  const dim3 block(kThreads);
   const float qscale = scale * kLog2e;
   const void* k_new = append ? append->k_new : nullptr;
   const void* v_new = append ? append->v_new : nullptr;
@@ -787,13 +933,15 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   const void* v_side = rope ? static_cast<const void*>(rope->q_rope) : v_new;
   const int flag = rope ? rope->shared : new_f16;
   const bool any_group = group != kHeads;
-#define IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_, ANY_)                          \
-  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_, ANY_>), grid,    \
-                     block, lds_pad, stream, q, k_codes, k_norms, v_codes, v_norms, seq_lens,   \
-                     quats, partials, out, capacity, static_cast<int>(max_seq_len),             \
-                     static_cast<int>(n_kv_heads), static_cast<int>(n_splits),                  \
-                     static_cast<int>(split_len), qscale, codebook_for<BITS_>(cb), k_side,      \
-                     v_side, flag, status, pt, static_cast<int>(group))
+#define IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_, ANY_)                           \
+  hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_, ANY_>), grid,     \
+                     block, lds_pad, stream,                                                     \
+                     G8Args<BITS_>{q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats,       \
+                                   partials, out, capacity, static_cast<int>(max_seq_len),       \
+                                   static_cast<int>(n_kv_heads), static_cast<int>(n_splits),     \
+                                   static_cast<int>(split_len), qscale, codebook_for<BITS_>(cb), \
+                                   k_side, v_side, flag, status, pt, static_cast<int>(group),    \
+                                   static_cast<int>(batch)})
 #define IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, PAGED_, BITS_)         \
   if (any_group) {                                                \
     IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, false, true);  \
