@@ -762,10 +762,24 @@ __device__ __forceinline__ void attend_split(G8Smem<kBits, kRope>& sm, const G8A
 template <int NB, bool kAppend, bool kWide, bool kPaged, int kBits, bool kRope = false,
           bool kAnyGroup = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWide && !kRope ? 4 : 2)))
-void decode_g8_kernel(G8Args<kBits> a) {
+void decode_g8_kernel(
+    const float* __restrict__ q, uint8_t* __restrict__ k_codes, float* __restrict__ k_norms,
+    uint8_t* __restrict__ v_codes, float* __restrict__ v_norms,
+    const int32_t* __restrict__ seq_lens, const float* __restrict__ quats,
+    float* __restrict__ partials, float* __restrict__ out, int64_t capacity, int max_seq_len,
+    int n_kv_heads, int n_splits, int split_len, float qscale, CodebookB<kBits> cb,
+    const void* __restrict__ k_new, const void* __restrict__ v_new, int new_f16,
+    int32_t* __restrict__ status, PageTable pages, int group, int batch) {
   static_assert(kBits == 3 || !kPaged, "paged pools hold 3-bit records");
   static_assert(!kRope || (!kAppend && !kPaged && kBits == 3 && kAnyGroup),
                 "the positional split runs on contiguous 3-bit caches, decode only");
+  // the arguments gathered for the device functions (the pointers keep the
+  // kernel parameters' no-alias property: the lengths, for one, are then
+  // read through the scalar cache)
+  const G8Args<kBits> a{q,        k_codes,  k_norms, v_codes,    v_norms,     seq_lens,
+                        quats,    partials, out,     capacity,   max_seq_len, n_kv_heads,
+                        n_splits, split_len, qscale, cb,         k_new,       v_new,
+                        new_f16,  status,   pages,   group,      batch};
   __shared__ __attribute__((aligned(16))) G8Smem<kBits, kRope> sm;
   const int gsize = kAnyGroup ? a.group : kHeads;
   const int vshift = kAnyGroup && gsize > kHeads ? 1 : 0;
@@ -935,13 +949,11 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   const bool any_group = group != kHeads;
 #define IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_, ANY_)                           \
   hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_, ANY_>), grid,     \
-                     block, lds_pad, stream,                                                     \
-                     G8Args<BITS_>{q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats,       \
-                                   partials, out, capacity, static_cast<int>(max_seq_len),       \
-                                   static_cast<int>(n_kv_heads), static_cast<int>(n_splits),     \
-                                   static_cast<int>(split_len), qscale, codebook_for<BITS_>(cb), \
-                                   k_side, v_side, flag, status, pt, static_cast<int>(group),    \
-                                   static_cast<int>(batch)})
+                     block, lds_pad, stream, q, k_codes, k_norms, v_codes, v_norms, seq_lens,   \
+                     quats, partials, out, capacity, static_cast<int>(max_seq_len),             \
+                     static_cast<int>(n_kv_heads), static_cast<int>(n_splits),                  \
+                     static_cast<int>(split_len), qscale, codebook_for<BITS_>(cb), k_side,      \
+                     v_side, flag, status, pt, static_cast<int>(group), static_cast<int>(batch))
 #define IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, PAGED_, BITS_)         \
   if (any_group) {                                                \
     IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, false, true);  \
