@@ -35,7 +35,9 @@
 //    the other half, so row (h, 0) accumulates dim 2F and row (h, 1) dim
 //    2F+1.  Lane group gk of the PV operands holds positions 4gk..4gk+3,
 //    exactly the rows the QK accumulator left in that lane group, so the
-//    weights never leave their lanes.
+//    weights never leave their lanes.  Each weight is split into fp16 hi +
+//    lo parts, one product each: with the weights rounded to fp16 once the
+//    outputs of long contexts drift past 2e-3 of the fp64 result.
 //
 // Softmax (Table 2 B) is two-phase per wave: all QK products of the wave's
 // positions first (scores kept in registers), one max per head, then the
@@ -522,8 +524,8 @@ __device__ __forceinline__ void attend_split(G8Smem<kBits, kRope>& sm, const G8A
   int vdw;
   uint32_t vsh;
   if constexpr (kBits == 3) {
-    vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
-    vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));   // 0..40
+    vdw = (3 * col) / 4;
+    vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));   // 0, 8, 16 or 24
   } else if constexpr (kBits == 4) {
     vdw = col;
     vsh = 0;

@@ -142,7 +142,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
 #pragma unroll
   for (int i = 0; i < NB; ++i)
     load_value_batch<3>(kPaged ? vc + dlt[i] * kRecordBytes : vc, tb[i], koff, vw[i]);
-  const int vdw = (3 * col) / 4 < 10 ? (3 * col) / 4 : 10;
+  const int vdw = (3 * col) / 4;
   const uint32_t vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));
 
   if constexpr (!kWide) seq0 = seq_lens[b];

@@ -398,9 +398,10 @@ __device__ __forceinline__ void key_pairs(const uint32_t* lut, const uint32_t (&
 
 // PV operand dwords of lane u = col for the position rows 4 gk + r of a
 // staged batch: pairs F = 4u + nb (nb = 0..3), i.e. dims 8u .. 8u + 7.
-// 3 bits: bytes 3u .. 3u + 2 of the record, found in the 8-byte window at
-// word vdw shifted right by vsh; 4 bits: word u (vdw = u); 2 bits: the half
-// of word u / 2 (vdw) at bit vsh = 16 (u % 2).
+// 3 bits: bytes 3u .. 3u + 2 of the record, at bit vsh (0, 8, 16 or 24) of
+// words vdw, vdw + 1 (vdw = 3u / 4; for u = 15 the second word is the
+// staged row's padding word, whose bits are never used); 4 bits: word u
+// (vdw = u); 2 bits: the half of word u / 2 (vdw) at bit vsh = 16 (u % 2).
 template <int kBits>
 __device__ __forceinline__ void value_pairs(const uint32_t* lut, const uint32_t* rec, int grp,
                                             int vdw, uint32_t vsh, u32x4_t (&vb)[4]) {
@@ -409,13 +410,12 @@ __device__ __forceinline__ void value_pairs(const uint32_t* lut, const uint32_t*
   for (int r = 0; r < 4; ++r) {
     const uint32_t* wp = rec + (4 * grp + r) * kStride + vdw;
     if constexpr (kBits == 3) {
-      // bytes 3u .. 3u+2 of the 8-byte window (a 64-bit shift: lane 15's
-      // bytes start 5 bytes in)
-      const uint64_t w64 = (static_cast<uint64_t>(wp[1]) << 32) | wp[0];
-      // fields at bits 0, 6, 12, 18 of the window: bits 0 and 18 are byte
+      // the 32-bit window starting at byte 3u (one funnel shift of the word
+      // pair); fields at bits 0, 6, 12, 18 of it: bits 0 and 18 are byte
       // selects of it, bits 6 and 12 of the window shifted right by 4
-      const uint32_t win = static_cast<uint32_t>(w64 >> vsh);
-      const uint32_t wu = static_cast<uint32_t>(w64 >> (vsh + 4));
+      const uint32_t lo = wp[0], hi = wp[1];
+      const uint32_t win = __builtin_amdgcn_alignbit(hi, lo, vsh);
+      const uint32_t wu = __builtin_amdgcn_alignbit(hi, lo, vsh + 4);
       vb[0][r] = lut_at(lut, low6x4<0>(win));
       vb[1][r] = lut_at(lut, top6x4<0>(wu));
       vb[2][r] = lut_at(lut, low6x4<1>(wu));
