@@ -512,7 +512,7 @@ iq_status iq_decode_step_bits(const float* q, const void* k_new, const void* v_n
 /*
  * Multi-token decode (the verification step of speculative decoding)
  * ------------------------------------------------------------------
- * n_tokens query tokens per sequence attend one packed 3-bit cache that
+ * n_tokens query tokens per sequence attend one packed cache that
  * already holds them at its last n_tokens positions: token t of sequence b
  * attends positions 0 .. L_b - n_tokens + t, with L_b = min(seq_lens[b],
  * max_seq_len) (causal among the new tokens; a token with no position gives
@@ -521,6 +521,7 @@ iq_status iq_decode_step_bits(const float* q, const void* k_new, const void* v_n
  *   q, out    : device fp32 [batch][n_tokens][n_q_heads][128], 16-byte
  *               aligned (original space).
  *   n_tokens  : 1 .. 4 (1 is iq_decode_attention);
+ *   iq_decode_attention_multi reads 3-bit records (the paper's cache);
  *   workspace : >= iq_decode_multi_workspace_bytes(...) bytes, 256-byte
  *               aligned, contents ignored on entry.
  * Other arguments as for iq_decode_attention.  n_tokens >= 2 runs on the
@@ -559,6 +560,45 @@ iq_status iq_decode_attention_multi_paged(const float* q,
                                           int64_t head_dim, float softmax_scale, float* out,
                                           void* workspace, size_t workspace_bytes,
                                           hipStream_t stream);
+
+/* iq_decode_attention_multi on records of `bits` bits (2, 3 or 4; Algorithm
+ * 1 with C_b, records of 4 * bits words written by iq_compress_kv_bits).
+ * n_tokens == 1 is iq_decode_attention_bits. */
+iq_status iq_decode_attention_multi_bits(const float* q,
+                                         const uint8_t* k_codes, const float* k_norms,
+                                         const uint8_t* v_codes, const float* v_norms,
+                                         const int32_t* seq_lens, int64_t capacity,
+                                         int64_t max_seq_len, const float* quats,
+                                         int64_t batch, int64_t n_tokens, int64_t n_q_heads,
+                                         int64_t n_kv_heads, int64_t head_dim,
+                                         float softmax_scale, float* out, void* workspace,
+                                         size_t workspace_bytes, int bits,
+                                         hipStream_t stream);
+
+/* The fused multi-token step (speculative verification with its append):
+ * the n_tokens new keys and values of each sequence (k_new, v_new: device
+ * [batch][n_tokens][n_kv_heads][128] of `dtype`, 16-byte aligned) are
+ * compressed to `bits`-bit records (Algorithm 1 with C_b) and written at
+ * positions seq_lens[b] .. seq_lens[b] + n_tokens - 1; token t attends the
+ * cached positions before seq_lens[b] and the new positions 0 .. t (causal
+ * among the new tokens; a position at or past max_seq_len is not attended);
+ * seq_lens[b] is then advanced by n_tokens.  The result equals that of
+ * iq_compress_kv_bits of the new tokens at dst_offset seq_lens[b] followed
+ * by iq_decode_attention_multi_bits with the advanced lengths.  When the
+ * n_tokens records do not all fit (seq_lens[b] + n_tokens > capacity) none
+ * is written, the length is left as it was, the tokens attend the cached
+ * positions only, and IQ_ERR_CAPACITY is ORed into *status_dev (optional,
+ * device int32).  n_tokens == 1 is iq_decode_step_bits.  Other arguments
+ * and restrictions as for iq_decode_attention_multi_bits; the workspace as
+ * sized by iq_decode_multi_workspace_bytes. */
+iq_status iq_decode_step_multi(const float* q, const void* k_new, const void* v_new,
+                               int32_t dtype, uint8_t* k_codes, float* k_norms,
+                               uint8_t* v_codes, float* v_norms, int32_t* seq_lens,
+                               int64_t capacity, int64_t max_seq_len, const float* quats,
+                               int64_t batch, int64_t n_tokens, int64_t n_q_heads,
+                               int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
+                               float* out, void* workspace, size_t workspace_bytes,
+                               int32_t* status_dev, int bits, hipStream_t stream);
 
 /*
  * Content / RoPE sub-block split (Sec. 5, "MLA/RoPE hard blocker"; Sec. 6)

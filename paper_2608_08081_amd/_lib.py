@@ -70,6 +70,12 @@ _SIGNATURES = {
     "iq_decode_attention_multi": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp,
                                            _c_i64, _c_i64, _c_i64, _c_i64, _c_i64, _c_float,
                                            _vp, _vp, _c_size, _vp]),
+    "iq_decode_attention_multi_bits": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64,
+                                                _vp, _c_i64, _c_i64, _c_i64, _c_i64, _c_i64,
+                                                _c_float, _vp, _vp, _c_size, _c_int, _vp]),
+    "iq_decode_step_multi": (_c_int, [_vp, _vp, _vp, _c_int, _vp, _vp, _vp, _vp, _vp, _c_i64,
+                                      _c_i64, _vp, _c_i64, _c_i64, _c_i64, _c_i64, _c_i64,
+                                      _c_float, _vp, _vp, _c_size, _vp, _c_int, _vp]),
     "iq_decode_attention_multi_paged": (_c_int, [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _vp,
                                                  _c_i64, _vp, _c_i64, _vp, _c_i64, _c_i64,
                                                  _c_i64, _c_i64, _c_i64, _c_float, _vp, _vp,

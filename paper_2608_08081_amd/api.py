@@ -403,20 +403,22 @@ def iq_decode_multi_workspace_bytes(batch, n_tokens, n_q_heads, n_kv_heads, max_
 
 
 def iq_decode_attention_multi(q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, out=None,
-                              workspace=None, max_seq_len=None, softmax_scale: float = 0.0):
+                              workspace=None, max_seq_len=None, softmax_scale: float = 0.0,
+                              bits: int = 3):
     """Multi-token decode: q [B][T][H_q][128] fp32 (T = 1..4 query tokens per
     sequence, the last T of its seq_lens[b] cached positions; token t attends
-    positions before seq_lens[b] - T + 1 + t).  Returns out [B][T][H_q][128]."""
+    positions before seq_lens[b] - T + 1 + t) on b-bit records
+    ([B][H_kv][cap][16 b]).  Returns out [B][T][H_q][128]."""
     if q.dim() != 4 or q.shape[-1] != HEAD_DIM:
         raise ValueError("q must be [batch][n_tokens][n_q_heads][128]")
     b, t, hq, _ = q.shape
     dev = q.device
     _require(q, "q", torch.float32, (b, t, hq, HEAD_DIM), dev)
     if k_codes.dim() != 4:
-        raise ValueError("k_codes must be [batch][n_kv_heads][capacity][48]")
+        raise ValueError("k_codes must be [batch][n_kv_heads][capacity][16 bits]")
     _, hkv, cap, _ = k_codes.shape
-    _require(k_codes, "k_codes", torch.uint8, (b, hkv, cap, RECORD_BYTES), dev)
-    _require(v_codes, "v_codes", torch.uint8, (b, hkv, cap, RECORD_BYTES), dev)
+    _require(k_codes, "k_codes", torch.uint8, (b, hkv, cap, record_bytes(bits)), dev)
+    _require(v_codes, "v_codes", torch.uint8, (b, hkv, cap, record_bytes(bits)), dev)
     _require(k_norms, "k_norms", torch.float32, (b, hkv, cap), dev)
     _require(v_norms, "v_norms", torch.float32, (b, hkv, cap), dev)
     _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
@@ -433,11 +435,62 @@ def iq_decode_attention_multi(q, k_codes, k_norms, v_codes, v_norms, seq_lens, q
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     if workspace.dtype != torch.uint8 or workspace.device != dev or not workspace.is_contiguous():
         raise ValueError("workspace must be a contiguous uint8 device tensor")
-    st = _lib.lib().iq_decode_attention_multi(
-        _ptr(q), _ptr(k_codes), _ptr(k_norms), _ptr(v_codes), _ptr(v_norms), _ptr(seq_lens),
-        cap, max_seq_len, _ptr(quats), b, t, hq, hkv, HEAD_DIM, float(softmax_scale), _ptr(out),
-        _ptr(workspace), workspace.numel(), _stream(dev))
-    _lib.check("iq_decode_attention_multi", st)
+    args = (_ptr(q), _ptr(k_codes), _ptr(k_norms), _ptr(v_codes), _ptr(v_norms), _ptr(seq_lens),
+            cap, max_seq_len, _ptr(quats), b, t, hq, hkv, HEAD_DIM, float(softmax_scale))
+    tail = (_ptr(out), _ptr(workspace), workspace.numel(), _stream(dev))
+    if bits == 3:
+        _lib.check("iq_decode_attention_multi",
+                   _lib.lib().iq_decode_attention_multi(*args, *tail))
+    else:
+        _lib.check("iq_decode_attention_multi_bits",
+                   _lib.lib().iq_decode_attention_multi_bits(*args, *tail[:3], bits, tail[3]))
+    return out
+
+
+def iq_decode_step_multi(q, k_new, v_new, k_codes, k_norms, v_codes, v_norms, seq_lens, quats,
+                         out=None, workspace=None, max_seq_len=None, softmax_scale: float = 0.0,
+                         status=None, bits: int = 3):
+    """Fused multi-token step: append the T new tokens (k_new, v_new
+    [B][T][H_kv][128], fp16 or fp32) at positions seq_lens[b] .. + T - 1 as
+    b-bit records, attend q [B][T][H_q][128] (token t: the cached positions
+    and new positions 0 .. t) and advance seq_lens by T in place.  Returns
+    out [B][T][H_q][128] fp32 (original space)."""
+    if q.dim() != 4 or q.shape[-1] != HEAD_DIM:
+        raise ValueError("q must be [batch][n_tokens][n_q_heads][128]")
+    b, t, hq, _ = q.shape
+    dev = q.device
+    _require(q, "q", torch.float32, (b, t, hq, HEAD_DIM), dev)
+    if k_codes.dim() != 4:
+        raise ValueError("k_codes must be [batch][n_kv_heads][capacity][16 bits]")
+    _, hkv, cap, _ = k_codes.shape
+    _require(k_new, "k_new", k_new.dtype, (b, t, hkv, HEAD_DIM), dev)
+    _require(v_new, "v_new", k_new.dtype, (b, t, hkv, HEAD_DIM), dev)
+    _require(k_codes, "k_codes", torch.uint8, (b, hkv, cap, record_bytes(bits)), dev)
+    _require(v_codes, "v_codes", torch.uint8, (b, hkv, cap, record_bytes(bits)), dev)
+    _require(k_norms, "k_norms", torch.float32, (b, hkv, cap), dev)
+    _require(v_norms, "v_norms", torch.float32, (b, hkv, cap), dev)
+    _require(seq_lens, "seq_lens", torch.int32, (b,), dev)
+    _require(quats, "quats", torch.float32, (hkv, 32, 2, 4), dev)
+    if status is not None:
+        _require(status, "status", torch.int32, (1,), dev)
+    if max_seq_len is None:
+        max_seq_len = cap
+    if out is None:
+        out = torch.empty((b, t, hq, HEAD_DIM), dtype=torch.float32, device=dev)
+    _require(out, "out", torch.float32, (b, t, hq, HEAD_DIM), dev)
+    if workspace is None:
+        nbytes = iq_decode_multi_workspace_bytes(b, t, hq, hkv, max_seq_len)
+        if nbytes <= 0:
+            raise ValueError("unsupported multi-token step shape")
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    if workspace.dtype != torch.uint8 or workspace.device != dev or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 device tensor")
+    st = _lib.lib().iq_decode_step_multi(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _dtype_code(k_new), _ptr(k_codes), _ptr(k_norms),
+        _ptr(v_codes), _ptr(v_norms), _ptr(seq_lens), cap, max_seq_len, _ptr(quats), b, t, hq,
+        hkv, HEAD_DIM, float(softmax_scale), _ptr(out), _ptr(workspace), workspace.numel(),
+        _ptr(status), bits, _stream(dev))
+    _lib.check("iq_decode_step_multi", st)
     return out
 
 

@@ -537,24 +537,24 @@ size_t iq_decode_multi_workspace_bytes(int64_t batch, int64_t n_tokens, int64_t 
   int nb = 0;
   int64_t splits = 0, len = 0;
   iq::g8_plan(batch, n_kv_heads, max_seq_len, &nb, &splits, &len);
-  const size_t bytes = static_cast<size_t>(batch) * n_kv_heads * splits * n_tokens * 8 *
+  // the splits' partial rows and the fused step's new-token rows
+  const size_t bytes = static_cast<size_t>(batch) * n_kv_heads * (splits + 1) * n_tokens * 8 *
                        (2 + kDim) * sizeof(float);
   return bytes > 0 ? (bytes + 255) / 256 * 256 : 256;
 }
 
-iq_status iq_decode_attention_multi(const float* q, const uint8_t* k_codes,
-                                    const float* k_norms, const uint8_t* v_codes,
-                                    const float* v_norms, const int32_t* seq_lens,
-                                    int64_t capacity, int64_t max_seq_len, const float* quats,
-                                    int64_t batch, int64_t n_tokens, int64_t n_q_heads,
-                                    int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
-                                    float* out, void* workspace, size_t workspace_bytes,
-                                    hipStream_t stream) {
-  if (n_tokens == 1)
-    return iq_decode_attention(q, k_codes, k_norms, v_codes, v_norms, seq_lens, capacity,
-                               max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
-                               softmax_scale, out, workspace, workspace_bytes, stream);
+namespace {
+
+// Multi-token decode and the fused multi-token step (append != null) on
+// contiguous caches of `bits`-bit records.
+iq_status multi_common(const float* q, const iq::StepAppend* append, uint8_t* k_codes,
+                       float* k_norms, uint8_t* v_codes, float* v_norms, int32_t* seq_lens,
+                       int64_t capacity, int64_t max_seq_len, const float* quats, int64_t batch,
+                       int64_t n_tokens, int64_t n_q_heads, int64_t n_kv_heads,
+                       int64_t head_dim, float softmax_scale, int bits, float* out,
+                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (n_tokens < 2 || n_tokens > 4) return IQ_ERR_UNSUPPORTED;
+  if (bits != 2 && bits != 3 && bits != 4) return IQ_ERR_UNSUPPORTED;
   iq::DecodePlan plan;
   // the single-token checks cover the cache, pointers and alignment; the
   // workspace is checked against the multi-token size below
@@ -564,8 +564,8 @@ iq_status iq_decode_attention_multi(const float* q, const uint8_t* k_codes,
   if (st != IQ_OK) return st;
   // multi-token decode runs 8 query heads per KV head
   if (n_q_heads != 8 * n_kv_heads) return IQ_ERR_UNSUPPORTED;
-  const iq_status shape = check_g8_shape(n_q_heads, n_kv_heads, batch, capacity,
-                                         iq::kRecordBytes, k_norms, v_norms, plan);
+  const iq_status shape = check_g8_shape(n_q_heads, n_kv_heads, batch, capacity, 16 * bits,
+                                         k_norms, v_norms, plan);
   if (shape != IQ_OK) return shape;
   if (!iq::mul_ok(batch, n_tokens) || !iq::mul_ok(batch * n_tokens, n_q_heads))
     return IQ_ERR_INVALID_ARGUMENT;
@@ -580,8 +580,51 @@ iq_status iq_decode_attention_multi(const float* q, const uint8_t* k_codes,
       plan.g8_batches, plan.g8_splits, plan.g8_split_len, static_cast<int>(n_tokens), q,
       k_codes, k_norms, v_codes, v_norms, seq_lens, capacity, max_seq_len, quats, batch,
       n_kv_heads, resolve_scale(softmax_scale), out, static_cast<float*>(workspace), nullptr,
-      stream);
+      bits, append, stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
+}
+
+}  // namespace
+
+iq_status iq_decode_attention_multi(const float* q, const uint8_t* k_codes,
+                                    const float* k_norms, const uint8_t* v_codes,
+                                    const float* v_norms, const int32_t* seq_lens,
+                                    int64_t capacity, int64_t max_seq_len, const float* quats,
+                                    int64_t batch, int64_t n_tokens, int64_t n_q_heads,
+                                    int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
+                                    float* out, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream) {
+  if (n_tokens == 1)
+    return iq_decode_attention(q, k_codes, k_norms, v_codes, v_norms, seq_lens, capacity,
+                               max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
+                               softmax_scale, out, workspace, workspace_bytes, stream);
+  // without an append the launch only reads the cache and the lengths
+  return multi_common(q, nullptr, const_cast<uint8_t*>(k_codes), const_cast<float*>(k_norms),
+                      const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms),
+                      const_cast<int32_t*>(seq_lens), capacity, max_seq_len, quats, batch,
+                      n_tokens, n_q_heads, n_kv_heads, head_dim, softmax_scale, 3, out,
+                      workspace, workspace_bytes, stream);
+}
+
+iq_status iq_decode_attention_multi_bits(const float* q, const uint8_t* k_codes,
+                                         const float* k_norms, const uint8_t* v_codes,
+                                         const float* v_norms, const int32_t* seq_lens,
+                                         int64_t capacity, int64_t max_seq_len,
+                                         const float* quats, int64_t batch, int64_t n_tokens,
+                                         int64_t n_q_heads, int64_t n_kv_heads,
+                                         int64_t head_dim, float softmax_scale, float* out,
+                                         void* workspace, size_t workspace_bytes, int bits,
+                                         hipStream_t stream) {
+  if (n_tokens == 1)
+    return iq_decode_attention_bits(q, k_codes, k_norms, v_codes, v_norms, seq_lens, capacity,
+                                    max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
+                                    softmax_scale, out, workspace, workspace_bytes, bits,
+                                    stream);
+  return multi_common(q, nullptr, const_cast<uint8_t*>(k_codes), const_cast<float*>(k_norms),
+                      const_cast<uint8_t*>(v_codes), const_cast<float*>(v_norms),
+                      const_cast<int32_t*>(seq_lens), capacity, max_seq_len, quats, batch,
+                      n_tokens, n_q_heads, n_kv_heads, head_dim, softmax_scale, bits, out,
+                      workspace, workspace_bytes, stream);
 }
 
 namespace {
@@ -673,6 +716,30 @@ iq_status iq_decode_step_cb(const float* q, const void* k_new, const void* v_new
                      capacity, max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
                      softmax_scale, out, workspace, workspace_bytes, status_dev, cb->bits, cb,
                      stream);
+}
+
+iq_status iq_decode_step_multi(const float* q, const void* k_new, const void* v_new,
+                               int32_t dtype, uint8_t* k_codes, float* k_norms,
+                               uint8_t* v_codes, float* v_norms, int32_t* seq_lens,
+                               int64_t capacity, int64_t max_seq_len, const float* quats,
+                               int64_t batch, int64_t n_tokens, int64_t n_q_heads,
+                               int64_t n_kv_heads, int64_t head_dim, float softmax_scale,
+                               float* out, void* workspace, size_t workspace_bytes,
+                               int32_t* status_dev, int bits, hipStream_t stream) {
+  if (n_tokens == 1)
+    return step_common(q, k_new, v_new, dtype, k_codes, k_norms, v_codes, v_norms, seq_lens,
+                       capacity, max_seq_len, quats, batch, n_q_heads, n_kv_heads, head_dim,
+                       softmax_scale, out, workspace, workspace_bytes, status_dev, bits, nullptr,
+                       stream);
+  if (dtype != IQ_DTYPE_F32 && dtype != IQ_DTYPE_F16) return IQ_ERR_UNSUPPORTED;
+  if (max_seq_len < 1) return IQ_ERR_INVALID_ARGUMENT;
+  if (!k_new || !v_new || !iq::aligned(k_new, 16) || !iq::aligned(v_new, 16) ||
+      (status_dev && !iq::aligned(status_dev, 4)))
+    return IQ_ERR_INVALID_ARGUMENT;
+  const iq::StepAppend append{k_new, v_new, dtype == IQ_DTYPE_F16 ? 1 : 0, status_dev};
+  return multi_common(q, &append, k_codes, k_norms, v_codes, v_norms, seq_lens, capacity,
+                      max_seq_len, quats, batch, n_tokens, n_q_heads, n_kv_heads, head_dim,
+                      softmax_scale, bits, out, workspace, workspace_bytes, stream);
 }
 
 // ---------------------------------------------------------------------------
@@ -859,9 +926,10 @@ iq_status iq_decode_attention_multi_paged(
   if (batch == 0) return IQ_OK;
   const hipError_t e = iq::launch_decode_g8_multi(
       plan.g8_batches, plan.g8_splits, plan.g8_split_len, static_cast<int>(n_tokens), q,
-      k_codes, k_norms, v_codes, v_norms, seq_lens, max_pages << pt.page_shift, max_seq_len,
-      quats, batch, n_kv_heads, resolve_scale(softmax_scale), out,
-      static_cast<float*>(workspace), &pt, stream);
+      const_cast<uint8_t*>(k_codes), const_cast<float*>(k_norms), const_cast<uint8_t*>(v_codes),
+      const_cast<float*>(v_norms), const_cast<int32_t*>(seq_lens), max_pages << pt.page_shift,
+      max_seq_len, quats, batch, n_kv_heads, resolve_scale(softmax_scale), out,
+      static_cast<float*>(workspace), &pt, 3, nullptr, stream);
   return e == hipSuccess ? IQ_OK : IQ_ERR_HIP;
 }
 

@@ -1,8 +1,10 @@
-// Multi-token decode on the packed 3-bit cache for groups of 8 query heads
-// per KV head (App. A applied to each of 2-4 query tokens; Table 2 A-D),
-// gfx950: the verification step of speculative decoding, the tokens causal
-// among themselves.  Same split grid, loads, record decoding and merge as
-// the single-token kernel (iq_decode_g8.hip); see the kernel comment.
+// Multi-token decode on the packed cache for groups of 8 query heads per KV
+// head (App. A applied to each of 2-4 query tokens; Table 2 A-D), gfx950:
+// the verification step of speculative decoding, the tokens causal among
+// themselves.  Same split grid, loads, record decoding and merge as the
+// single-token kernel (iq_decode_g8.hip); see the kernel comment.  Records
+// of 2, 3 or 4 bits (Algorithm 1 with C_b), and a fused step that appends
+// the kT new tokens itself.
 #include <hip/hip_runtime.h>
 #include <math.h>
 
@@ -12,34 +14,54 @@ namespace iq {
 namespace {
 
 // Multi-token decode (speculative verification): kT query tokens per
-// sequence over the same cache, token t attending positions before
-// seq - kT + 1 + t (causal among the new tokens, which the caller has
-// already compressed into the last kT positions).  Same grid, split plan,
-// loads and record decoding as decode_g8_kernel on 3-bit records: every
-// batch of keys and values is decoded once and feeds kT sets of matrix
-// instructions (the QK B operand of token t is read from LDS per batch).  The
-// softmax is two-phase as in decode_g8_kernel: all scores of every token
-// first (kept in registers), one max per token and head, then the weights
-// and values.  Partials per (split, token, head); the merge kernel takes the
-// token axis.
+// sequence over the same cache.  Every batch of keys and values is decoded
+// once and feeds kT sets of matrix instructions (the QK B operand of token t
+// is read from LDS per batch).  The softmax is two-phase as in
+// decode_g8_kernel: all scores of every token first (kept in registers), one
+// max per token and head, then the weights and values.  Partials per (split,
+// token, head); the merge kernel takes the token axis.
 //
-// kPaged: the cache is a page pool (PageTable), as in decode_g8_kernel.
-template <int NB, bool kWide, int kT, bool kPaged>
+// Without kAppend the caller has already compressed the kT new tokens into
+// the last kT of the seq_lens[b] positions, and token t attends the
+// positions before seq_lens[b] - kT + 1 + t.
+//
+// kAppend, the fused step: one more workgroup per (b, g), split index
+// n_splits, compresses the kT new keys and values (Alg. 1) and writes their
+// records at positions seq_lens[b] .. seq_lens[b] + kT - 1, then publishes,
+// per token t, the partial (m, l, O) over the new positions u <= t (causal
+// among the new tokens; a new position at or past max_seq_len is not
+// attended).  The attention workgroups serve the cached positions before
+// seq_lens[b], which every token attends.  When the kT records do not all
+// fit the capacity nothing is written, the capacity flag is raised, the new
+// positions are not attended, and the partial's l entry carries -1, so that
+// the merge leaves the length as it is; otherwise the merge advances it by
+// kT.  No attention workgroup reads the records being written.
+//
+// kPaged: the cache is a page pool (PageTable), as in decode_g8_kernel
+// (3-bit records, decode only).  kBits: the records' code width.
+template <int NB, bool kWide, int kT, bool kPaged, int kBits, bool kAppend>
 __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
-    const float* __restrict__ q, const uint8_t* __restrict__ k_codes,
-    const float* __restrict__ k_norms, const uint8_t* __restrict__ v_codes,
-    const float* __restrict__ v_norms, const int32_t* __restrict__ seq_lens,
-    const float* __restrict__ quats, float* __restrict__ partials, float* __restrict__ out,
-    int64_t capacity, int max_seq_len, int n_kv_heads, int n_splits, int split_len, float qscale,
-    Codebook cb, PageTable pages) {
+    const float* __restrict__ q, uint8_t* __restrict__ k_codes, float* __restrict__ k_norms,
+    uint8_t* __restrict__ v_codes, float* __restrict__ v_norms,
+    const int32_t* __restrict__ seq_lens, const float* __restrict__ quats,
+    float* __restrict__ partials, float* __restrict__ out, int64_t capacity, int max_seq_len,
+    int n_kv_heads, int n_splits, int split_len, float qscale, CodebookB<kBits> cb,
+    PageTable pages, const void* __restrict__ k_new, const void* __restrict__ v_new,
+    int new_f16, int32_t* __restrict__ status) {
   static_assert(kT >= 2 && kT <= 4, "2 to 4 tokens");
+  static_assert(!kPaged || (kBits == 3 && !kAppend), "paged pools: 3-bit decode only");
+  constexpr int kRB = record_bytes<kBits>();
+  constexpr int kLut = 1 << (2 * kBits);
+  constexpr int kNew = kAppend ? 2 * kT : 1;
   struct Smem {
-    uint32_t lut[64];
+    uint32_t lut[kLut];   // fp16 pair table (address 0: a lookup address is field * 4)
     uint32_t qop[kT][2][kHeads][kQRowWords];
     int qexp[kT][kHeads];
     float wave_ml[kWaves][2][kHeads];
+    uint32_t new_rec[kNew][4 * kBits];   // append: record of token w / 2's key (w even) or value
+    float new_scale[kNew];
     union {
-      WaveStage stage[kWaves];
+      WaveStageB<kBits> stage[kWaves];
       f32x4_t wave_o[kWaves][4][64];
     };
   };
@@ -55,6 +77,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
   const int b = blockIdx.z;
   const int bg = b * n_kv_heads + g;
   const int n_q_heads = n_kv_heads * kHeads;
+  const int n_parts = kAppend ? n_splits + 1 : n_splits;
 
   // queries of the kT tokens (thread (head qh, block qblk) for tid < 256)
   const int qh = (tid >> 5) & 7, qblk = tid & 31;
@@ -67,10 +90,115 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
   const f32x4_t* qpar = reinterpret_cast<const f32x4_t*>(
       quats + static_cast<int64_t>(g) * kQuatFloats + 8 * qblk);
   const f32x4_t ql = qpar[0], qr = qpar[1];
-  float* part_bg = partials + static_cast<int64_t>(bg) * n_splits * kT * (kHeads * kPart);
+  float* part_bg = partials + static_cast<int64_t>(bg) * n_parts * kT * (kHeads * kPart);
   const int64_t row = kPaged ? 0 : static_cast<int64_t>(bg) * capacity;
-  const uint8_t* kc = k_codes + row * kRecordBytes;
-  const uint8_t* vc = v_codes + row * kRecordBytes;
+
+  if constexpr (kAppend) if (split == n_splits) {
+    // ---- the append workgroup ------------------------------------------------
+    const int seq0 = seq_lens[b];
+    const bool fits = seq0 >= 0 && seq0 <= capacity - kT;
+    if (!fits && status != nullptr && g == 0 && tid == 0)
+      atomicOr(status, static_cast<int32_t>(IQ_ERR_CAPACITY));
+    // waves 0 .. 2 kT - 1: wave w compresses token w / 2's key (w even) or
+    // value (w odd); lane l holds dims 2l, 2l + 1 and the parameters of
+    // SO(4) block l / 2
+    if (wave < 2 * kT) {
+      const int t = wave >> 1, which = wave & 1;
+      const void* src = which ? v_new : k_new;
+      const int64_t off = ((static_cast<int64_t>(b) * kT + t) * n_kv_heads + g) * kDim;
+      float x0, x1;
+      if (new_f16) {
+        const uint32_t w = reinterpret_cast<const uint32_t*>(static_cast<const __half*>(src) +
+                                                             off)[lane];
+        x0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w)));
+        x1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16)));
+      } else {
+        const f32x2_t w =
+            reinterpret_cast<const f32x2_t*>(static_cast<const float*>(src) + off)[lane];
+        x0 = w[0];
+        x1 = w[1];
+      }
+      const f32x4_t* qs = reinterpret_cast<const f32x4_t*>(
+          quats + static_cast<int64_t>(g) * kQuatFloats + 8 * (lane >> 1));
+      const f32x4_t p0 = qs[0], p1 = qs[1];
+      const float qp[8] = {p0[0], p0[1], p0[2], p0[3], p1[0], p1[1], p1[2], p1[3]};
+      const WaveCode wc = compress_vector_wave<kBits>(x0, x1, qp, cb, lane);
+      if (lane < 4 * kBits) sm.new_rec[wave][lane] = wc.word;
+      if (lane == 0) sm.new_scale[wave] = wc.scale;
+      if (fits) {
+        const int64_t rec = row + seq0 + t;
+        uint8_t* codes = which ? v_codes : k_codes;
+        float* norms = which ? v_norms : k_norms;
+        if (lane < 4 * kBits) reinterpret_cast<uint32_t*>(codes + rec * kRB)[lane] = wc.word;
+        if (lane == 0) norms[rec] = wc.scale;
+      }
+    }
+    if (tid < kLut) {
+      constexpr int kMask = (1 << kBits) - 1;
+      const uint32_t lo =
+          __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & kMask)));
+      const uint32_t hi =
+          __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> kBits)));
+      lut[tid] = lo | (hi << 16);
+    }
+    f32x4_t y[kT];
+#pragma unroll
+    for (int t = 0; t < kT; ++t)
+      y[t] = tid < kRotThreads ? rotate_forward(qv[t], ql, qr, qblk, kInvSqrtDim * qscale)
+                               : f32x4_t{0.f, 0.f, 0.f, 0.f};
+    lds_barrier();   // new_rec, new_scale, lut
+    if (tid >= kRotThreads) return;
+    // scores of the new keys u <= t for head qh, in log2 units (y carries
+    // the score scale): s^K_u (q_tilde_t . C[code_u]) over this thread's dims
+    // 4 qblk .. +3, summed over the head's 32 lanes
+    const int md = 4 * qblk;
+    float sc[kT][kT];
+    f32x4_t v4[kT];
+#pragma unroll
+    for (int u = 0; u < kT; ++u) {
+      const f32x4_t k4 = decode_record_dims<kBits>(sm.new_rec[2 * u], lut, md);
+      v4[u] = sm.new_scale[2 * u + 1] * decode_record_dims<kBits>(sm.new_rec[2 * u + 1], lut, md);
+#pragma unroll
+      for (int t = u; t < kT; ++t) {
+        float dot = y[t][0] * k4[0] + y[t][1] * k4[1] + y[t][2] * k4[2] + y[t][3] * k4[3];
+        dot += xor_lane<1>(dot);
+        dot += xor_lane<2>(dot);
+        dot += xor_lane<4>(dot);
+        dot += xor_lane<8>(dot);
+        dot += xor_lane<16>(dot);
+        sc[t][u] = dot * sm.new_scale[2 * u];
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < kT; ++t) {
+      float m = -INFINITY;
+#pragma unroll
+      for (int u = 0; u <= t; ++u)
+        if (fits && seq0 + u < max_seq_len) m = fmaxf(m, sc[t][u]);
+      float l = 0.f;
+      f32x4_t o = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = 0; u <= t; ++u) {
+        if (fits && seq0 + u < max_seq_len) {
+          const float c = __builtin_amdgcn_exp2f(sc[t][u] - m);
+          l += c;
+          o += c * v4[u];
+        }
+      }
+      float* pp = part_bg + (static_cast<int64_t>(n_splits) * kT + t) * (kHeads * kPart) +
+                  qh * kPart;
+      if (qblk == 0) {
+        pp[0] = m;
+        // > 0: the records were written (the merge then advances the length)
+        pp[1] = !fits ? -1.0f : (m == -INFINITY ? 1.0f : l);
+      }
+      *reinterpret_cast<f32x4_t*>(pp + 2 + md) = o;
+    }
+    return;
+  }
+
+  const uint8_t* kc = k_codes + row * kRB;
+  const uint8_t* vc = v_codes + row * kRB;
 
   // this wave's run of batches (as in decode_g8_kernel)
   const int start = split * split_len;
@@ -91,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
     const int seq_w = seq0 < 0 ? 0 : (seq0 > max_seq_len ? max_seq_len : seq0);
     if (start >= seq_w) {
       // nothing to attend for any token
-      if (n_splits > 1) {
+      if (n_parts > 1) {
         if (tid < kT * kHeads)
           part_bg[(static_cast<int64_t>(split) * kT + tid / kHeads) * (kHeads * kPart) +
                   (tid % kHeads) * kPart] = -INFINITY;
@@ -131,27 +259,40 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
                static_cast<int64_t>((t >> pages.page_shift) << pages.page_shift);
     }
   }
-  uint32_t kw[NB][3], vw[NB][3];
+  uint32_t kw[NB][kBits], vw[NB][kBits];
   f32x4_t ksl, vsl;
-  load_keys<NB, kPaged, 3>(kc, kn, vn, dlt, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
-  const uint32_t koff = static_cast<uint32_t>(col * kRecordBytes + 12 * grp);
+  load_keys<NB, kPaged, kBits>(kc, kn, vn, dlt, wbase, clamp16, lane, col, grp, kw, ksl, vsl);
+  const uint32_t koff = static_cast<uint32_t>(col * kRB + 4 * kBits * grp);
   int tb[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) tb[i] = wbase + 16 * i < clamp16 ? wbase + 16 * i : clamp16;
   // every value batch goes out behind the keys
 #pragma unroll
   for (int i = 0; i < NB; ++i)
-    load_value_batch<3>(kPaged ? vc + dlt[i] * kRecordBytes : vc, tb[i], koff, vw[i]);
-  const int vdw = (3 * col) / 4;
-  const uint32_t vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));
+    load_value_batch<kBits>(kPaged ? vc + dlt[i] * kRB : vc, tb[i], koff, vw[i]);
+  // the word of the value window of lane u = col (see value_pairs)
+  int vdw;
+  uint32_t vsh;
+  if constexpr (kBits == 3) {
+    vdw = (3 * col) / 4;
+    vsh = static_cast<uint32_t>(8 * (3 * col - 4 * vdw));   // 0, 8, 16 or 24
+  } else if constexpr (kBits == 4) {
+    vdw = col;
+    vsh = 0;
+  } else {
+    vdw = col >> 1;
+    vsh = static_cast<uint32_t>(16 * (col & 1));
+  }
 
   if constexpr (!kWide) seq0 = seq_lens[b];
   const int seq = seq0 < 0 ? 0 : (seq0 > max_seq_len ? max_seq_len : seq0);
-  // positions of this wave each token attends (may be <= 0)
+  // positions of this wave each token attends (may be <= 0): with kAppend
+  // every token attends the whole cache (the new positions are the append
+  // workgroup's)
   int nv[kT];
 #pragma unroll
   for (int t = 0; t < kT; ++t) {
-    int st = seq - (kT - 1 - t);
+    int st = kAppend ? seq : seq - (kT - 1 - t);
     st = st > 0 ? st : 0;
     const int end = st < start + split_len ? st : start + split_len;
     int n = end - wbase;
@@ -160,11 +301,12 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
   const int nvalid = nv[kT - 1];
 
   // ---- while the loads fly: LUT and the rotated queries --------------------
-  if (tid < 64) {
+  if (tid < kLut) {
+    constexpr int kMask = (1 << kBits) - 1;
     const uint32_t lo =
-        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & 7)));
+        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid & kMask)));
     const uint32_t hi =
-        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> 3)));
+        __builtin_bit_cast(uint16_t, static_cast<_Float16>(codebook_level(cb, tid >> kBits)));
     lut[tid] = lo | (hi << 16);
   }
   if (tid < kRotThreads) {
@@ -203,7 +345,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
   for (int t = 0; t < kT; ++t) qdown[t] = ldexpf(1.0f, -sm.qexp[t][col & 7]);
   // scales to the wave's stage; value scales past the last token's length
   // are 0 and the rest are brought to [0, 2^15] by the wave's largest
-  WaveStage& st = sm.stage[wave];
+  WaveStageB<kBits>& st = sm.stage[wave];
   float vmax;
   {
     f32x4_t v = vsl;
@@ -226,7 +368,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
   for (int i = 0; i < NB; ++i) {
     if (16 * i >= nvalid) break;
     u32x4_t a[4];
-    key_pairs<3>(lut, kw[i], a);
+    key_pairs<kBits>(lut, kw[i], a);
     const f32x4_t ks = st.ks[4 * i + grp];
 #pragma unroll
     for (int t = 0; t < kT; ++t) {
@@ -255,7 +397,8 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
   for (int i = 0; i < NB; ++i) {
     if (16 * i >= nvalid) break;
 #pragma unroll
-    for (int j = 0; j < 3; ++j) st.rec[i][col * kRecStride + 3 * grp + j] = vw[i][j];
+    for (int j = 0; j < kBits; ++j)
+      st.rec[i][col * rec_stride<kBits>() + kBits * grp + j] = vw[i][j];
   }
   wave_lds_fence();
   f32x4_t o_acc[kT][4];
@@ -274,7 +417,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
   for (int i = 0; i < NB; ++i) {
     if (16 * i >= nvalid) break;
     u32x4_t vb[4];
-    value_pairs<3>(lut, st.rec[i], grp, vdw, vsh, vb);
+    value_pairs<kBits>(lut, st.rec[i], grp, vdw, vsh, vb);
     const f32x4_t wv = st.vs[4 * i + grp];   // 0 past the last token's length
 #pragma unroll
     for (int t = 0; t < kT; ++t) {
@@ -335,7 +478,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
             reinterpret_cast<const float*>(&sm.wave_o[w][o_r][o_lane + 32]) + o_nb);
         O += c * f32x4_t{s0[0], s1[0], s0[1], s1[1]};
       }
-      if (n_splits == 1) {
+      if (n_parts == 1) {
         const f32x4_t o = L > 0.f ? rotate_inverse(O * (1.0f / L), ql, qr, qblk)
                                   : f32x4_t{0.f, 0.f, 0.f, 0.f};
         *reinterpret_cast<f32x4_t*>(
@@ -357,32 +500,50 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
 }  // namespace
 
 hipError_t launch_decode_g8_multi(int nb, int64_t n_splits, int64_t split_len, int n_tok,
-                                  const float* q, const uint8_t* k_codes, const float* k_norms,
-                                  const uint8_t* v_codes, const float* v_norms,
-                                  const int32_t* seq_lens, int64_t capacity,
-                                  int64_t max_seq_len, const float* quats, int64_t batch,
-                                  int64_t n_kv_heads, float scale, float* out, float* partials,
-                                  const PageTable* pages, hipStream_t stream) {
+                                  const float* q, uint8_t* k_codes, float* k_norms,
+                                  uint8_t* v_codes, float* v_norms, int32_t* seq_lens,
+                                  int64_t capacity, int64_t max_seq_len, const float* quats,
+                                  int64_t batch, int64_t n_kv_heads, float scale, float* out,
+                                  float* partials, const PageTable* pages, int bits,
+                                  const StepAppend* append, hipStream_t stream,
+                                  const iq_codebook_t* cb) {
   if (n_tok < 2 || n_tok > 4) return hipErrorInvalidValue;
+  if (bits != 2 && bits != 3 && bits != 4) return hipErrorInvalidValue;
+  if (pages && (bits != 3 || append)) return hipErrorInvalidValue;
   const PageTable pt = pages ? *pages : PageTable{nullptr, 0, 4, 1};
-  const dim3 grid(static_cast<unsigned>(n_splits), static_cast<unsigned>(n_kv_heads),
+  const int64_t n_parts = append ? n_splits + 1 : n_splits;
+  const dim3 grid(static_cast<unsigned>(n_parts), static_cast<unsigned>(n_kv_heads),
                   static_cast<unsigned>(batch)),
       block(kThreads);
   constexpr int64_t kCus = 256;
-  const bool wide = n_splits * n_kv_heads * batch > kCus;
+  const bool wide = n_parts * n_kv_heads * batch > kCus;
   const size_t lds_pad = wide ? 0 : kOneWorkgroupPadBytes;
   const float qscale = scale * kLog2e;
-  const Codebook& cb = codebook();
-#define IQ_LAUNCH_MTP(NB_, WIDE_, T_, P_)                                                      \
-  hipLaunchKernelGGL((decode_g8_multi_kernel<NB_, WIDE_, T_, P_>), grid, block, lds_pad, stream, \
-                     q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials, out,     \
-                     capacity, static_cast<int>(max_seq_len), static_cast<int>(n_kv_heads),     \
-                     static_cast<int>(n_splits), static_cast<int>(split_len), qscale, cb, pt)
-#define IQ_LAUNCH_MT(NB_, WIDE_, T_)        \
-  if (pages) {                              \
-    IQ_LAUNCH_MTP(NB_, WIDE_, T_, true);    \
-  } else {                                  \
-    IQ_LAUNCH_MTP(NB_, WIDE_, T_, false);   \
+  const void* k_new = append ? append->k_new : nullptr;
+  const void* v_new = append ? append->v_new : nullptr;
+  const int new_f16 = append ? append->f16 : 0;
+  int32_t* status = append ? append->status : nullptr;
+#define IQ_LAUNCH_MTK(NB_, WIDE_, T_, P_, B_, A_)                                                \
+  hipLaunchKernelGGL((decode_g8_multi_kernel<NB_, WIDE_, T_, P_, B_, A_>), grid, block, lds_pad,  \
+                     stream, q, k_codes, k_norms, v_codes, v_norms, seq_lens, quats, partials,    \
+                     out, capacity, static_cast<int>(max_seq_len), static_cast<int>(n_kv_heads),  \
+                     static_cast<int>(n_splits), static_cast<int>(split_len), qscale,             \
+                     codebook_for<B_>(cb), pt, k_new, v_new, new_f16, status)
+#define IQ_LAUNCH_MTA(NB_, WIDE_, T_, B_)            \
+  if (append) {                                      \
+    IQ_LAUNCH_MTK(NB_, WIDE_, T_, false, B_, true);  \
+  } else {                                           \
+    IQ_LAUNCH_MTK(NB_, WIDE_, T_, false, B_, false); \
+  }
+#define IQ_LAUNCH_MT(NB_, WIDE_, T_)                  \
+  if (pages) {                                        \
+    IQ_LAUNCH_MTK(NB_, WIDE_, T_, true, 3, false);    \
+  } else if (bits == 2) {                             \
+    IQ_LAUNCH_MTA(NB_, WIDE_, T_, 2)                  \
+  } else if (bits == 4) {                             \
+    IQ_LAUNCH_MTA(NB_, WIDE_, T_, 4)                  \
+  } else {                                            \
+    IQ_LAUNCH_MTA(NB_, WIDE_, T_, 3)                  \
   }
 #define IQ_LAUNCH_MT_W(NB_, T_)       \
   if (wide) {                         \
@@ -408,18 +569,32 @@ hipError_t launch_decode_g8_multi(int nb, int64_t n_splits, int64_t split_len, i
 #undef IQ_LAUNCH_MT_NB
 #undef IQ_LAUNCH_MT_W
 #undef IQ_LAUNCH_MT
-#undef IQ_LAUNCH_MTP
+#undef IQ_LAUNCH_MTA
+#undef IQ_LAUNCH_MTK
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || n_splits == 1) return e;
+  if (e != hipSuccess || n_parts == 1) return e;
+  // the partials of every (sequence, token, query head) merged by a second
+  // launch, which in the fused step also advances the lengths by n_tok
   const dim3 mgrid(static_cast<unsigned>(n_kv_heads * kHeads),
                    static_cast<unsigned>(batch * n_tok));
-#define IQ_LAUNCH_MT_MERGE(T_)                                                                 \
-  hipLaunchKernelGGL((merge_g8_kernel<false, T_>), mgrid, dim3(kMergeThreads), 0, stream,       \
+#define IQ_LAUNCH_MT_MERGE(A_, T_)                                                             \
+  hipLaunchKernelGGL((merge_g8_kernel<A_, T_>), mgrid, dim3(kMergeThreads), 0, stream,         \
                      partials, quats, out, static_cast<int>(n_kv_heads),                        \
-                     static_cast<int>(n_splits), nullptr, capacity, kHeads)
-  if (n_tok == 2) IQ_LAUNCH_MT_MERGE(2);
-  else if (n_tok == 3) IQ_LAUNCH_MT_MERGE(3);
-  else IQ_LAUNCH_MT_MERGE(4);
+                     static_cast<int>(n_parts), seq_lens, capacity, kHeads)
+#define IQ_LAUNCH_MT_MERGE_T(A_)                            \
+  if (n_tok == 2) {                                         \
+    IQ_LAUNCH_MT_MERGE(A_, 2);                              \
+  } else if (n_tok == 3) {                                  \
+    IQ_LAUNCH_MT_MERGE(A_, 3);                              \
+  } else {                                                  \
+    IQ_LAUNCH_MT_MERGE(A_, 4);                              \
+  }
+  if (append) {
+    IQ_LAUNCH_MT_MERGE_T(true)
+  } else {
+    IQ_LAUNCH_MT_MERGE_T(false)
+  }
+#undef IQ_LAUNCH_MT_MERGE_T
 #undef IQ_LAUNCH_MT_MERGE
   return hipGetLastError();
 }

@@ -450,6 +450,9 @@ __device__ __forceinline__ void value_pairs(const uint32_t* lut, const uint32_t*
 //
 // kTok > 1 (multi-token decode): the partials of each split hold kTok
 // tokens' rows; grid (query head, sequence x token), output row (b, t).
+// With kAppend (the fused multi-token step) the last partial holds the new
+// tokens' rows, and workgroup (b, token 0, head 0) advances seq_lens[b] by
+// kTok.
 // kAnyGroup: group query heads per KV head (1 .. 16); the partial rows are
 // per (sequence, KV head, head group of 8), the layout of the decode
 // kernels' grid.  Otherwise 8 (group is not read).
@@ -464,7 +467,6 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     int n_kv_heads, int n_parts, int32_t* __restrict__ seq_lens, int64_t capacity, int group,
     int split_len = 0, int max_seq_len = 0) {
   static_assert(kTok == 1 || !kLive, "multi-token partials are read in full");
-  static_assert(kTok == 1 || !kAppend, "the fused step decodes one token");
   constexpr int kUnroll = 8;   // 8 x 8 = 64 splits per pass, all loads in flight
   __shared__ __attribute__((aligned(16))) float red_o[8][kDim];
   __shared__ float red_m[8], red_l[8];
@@ -481,11 +483,12 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
   const int bgv = (b * n_kv_heads + g) * n_vg + hr / kHeads;   // the partial row
   int seq0 = 0;
   float written = 0.f;
-  if (kAppend && h == 0 && tid == 0) {
+  if (kAppend && h == 0 && tok == 0 && tid == 0) {
     seq0 = seq_lens[b];
-    // the new-token partial of KV head 0 (every KV head shares the outcome)
+    // the new-token partial (token 0) of KV head 0 (every KV head shares
+    // the outcome)
     written = partials[(static_cast<int64_t>(b) * n_kv_heads * n_vg * n_parts + n_parts - 1) *
-                           (kHeads * kPart) + 1];
+                           kTok * (kHeads * kPart) + 1];
   }
   const int sg = tid >> 5, dq = tid & 31;
   constexpr int kSplitStride = kTok * kHeads * kPart;
@@ -576,8 +579,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     *reinterpret_cast<f32x4_t*>(out + (static_cast<int64_t>(bt) * n_q_heads + h) * kDim +
                                 4 * tid) = r;
   }
-  if (kAppend && h == 0 && tid == 0 && seq0 >= 0 && seq0 < capacity && written > 0.f)
-    seq_lens[b] = seq0 + 1;
+  if (kAppend && h == 0 && tok == 0 && tid == 0 && seq0 >= 0 && seq0 <= capacity - kTok &&
+      written > 0.f)
+    seq_lens[b] = seq0 + kTok;
 }
 
 }  // namespace

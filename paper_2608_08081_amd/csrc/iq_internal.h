@@ -163,17 +163,22 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
                             hipStream_t stream, const iq_codebook_t* cb = nullptr,
                             const RopeKeys* rope = nullptr);
 
-// Multi-token decode on 3-bit records (group 8): n_tok (2..4) query tokens
-// per sequence, q / out [batch][n_tok][8 n_kv_heads][128]; the plan is
-// g8_plan's, partials [batch][n_kv_heads][n_splits][n_tok][8][130] floats;
-// pages: null for a contiguous cache, else the page table.
+// Multi-token decode on records of `bits` bits (group 8): n_tok (2..4)
+// query tokens per sequence, q / out [batch][n_tok][8 n_kv_heads][128]; the
+// plan is g8_plan's, partials [batch][n_kv_heads][n_parts][n_tok][8][130]
+// floats with n_parts = n_splits (+ 1 with `append`); pages: null for a
+// contiguous cache, else the page table (3-bit records, no append).  With
+// `append` (k_new / v_new [batch][n_tok][n_kv_heads][128]), the fused
+// step: the n_tok tokens are appended at seq_lens[b], attended causally and
+// seq_lens advanced by n_tok.
 hipError_t launch_decode_g8_multi(int nb, int64_t n_splits, int64_t split_len, int n_tok,
-                                  const float* q, const uint8_t* k_codes, const float* k_norms,
-                                  const uint8_t* v_codes, const float* v_norms,
-                                  const int32_t* seq_lens, int64_t capacity,
-                                  int64_t max_seq_len, const float* quats, int64_t batch,
-                                  int64_t n_kv_heads, float scale, float* out, float* partials,
-                                  const PageTable* pages, hipStream_t stream);
+                                  const float* q, uint8_t* k_codes, float* k_norms,
+                                  uint8_t* v_codes, float* v_norms, int32_t* seq_lens,
+                                  int64_t capacity, int64_t max_seq_len, const float* quats,
+                                  int64_t batch, int64_t n_kv_heads, float scale, float* out,
+                                  float* partials, const PageTable* pages, int bits,
+                                  const StepAppend* append, hipStream_t stream,
+                                  const iq_codebook_t* cb = nullptr);
 
 // Reconstruct-then-compute baseline (Fig. 1 top): materialize the packed
 // cache as fp16 or fp32 vectors, and decode attention on an fp16 cache.

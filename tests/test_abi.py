@@ -392,6 +392,50 @@ def test_step_bits_and_multi_paged_validation():
     assert mtp(b=21846, t=3) == 2               # 65538 (sequence, token) rows
 
 
+def test_multi_bits_and_multi_step_validation():
+    """Argument checks of iq_decode_attention_multi_bits and
+    iq_decode_step_multi (host side only: nothing is launched on a
+    validation error)."""
+    def mb(**kw):
+        a = dict(b=1, t=2, hq=16, hkv=2, cap=256, msl=256, bits=2, wsb=1 << 30)
+        a.update(kw)
+        return L.iq_decode_attention_multi_bits(A, A, A, B, B, A, a["cap"], a["msl"], A, a["b"],
+                                                a["t"], a["hq"], a["hkv"], 128, 0.0, A, A,
+                                                a["wsb"], a["bits"], None)
+    assert mb(bits=5) == 2
+    assert mb(bits=1) == 2
+    assert mb(t=5) == 2
+    assert mb(hq=8) == 2                         # multi-token: group 8 only
+    assert mb(cap=250, msl=250) == 2
+    assert mb(msl=300) == 1
+    assert mb(wsb=16) == 3
+    assert mb(b=0) == 0
+
+    def st(**kw):
+        a = dict(dtype=1, b=1, t=3, hq=16, hkv=2, cap=256, msl=256, bits=4, wsb=1 << 30,
+                 kn=A, st=None)
+        a.update(kw)
+        return L.iq_decode_step_multi(A, a["kn"], A, a["dtype"], A, A, B, B, A, a["cap"],
+                                      a["msl"], A, a["b"], a["t"], a["hq"], a["hkv"], 128, 0.0,
+                                      A, A, a["wsb"], a["st"], a["bits"], None)
+    assert st(bits=5) == 2
+    assert st(dtype=7) == 2
+    assert st(t=5) == 2
+    assert st(hq=8) == 2
+    assert st(cap=250, msl=250) == 2
+    assert st(msl=0) == 1                        # the step needs room for its tokens
+    assert st(kn=None) == 1
+    assert st(kn=ctypes.c_void_p(0x100002)) == 1   # k_new not 16-byte aligned
+    assert st(st=ctypes.c_void_p(0x100002)) == 1   # status not 4-byte aligned
+    assert st(wsb=16) == 3
+    assert st(b=0) == 0
+    assert st(b=16384, t=4) == 2                 # 65536 (sequence, token) rows
+    # the workspace covers the step's new-token rows: one more row per
+    # (sequence, KV head) than the splits
+    w = L.iq_decode_multi_workspace_bytes(1, 2, 16, 2, 16, 128)
+    assert w >= 2 * 2 * 2 * 8 * 130 * 4
+
+
 def test_stream_read_validation():
     """Argument checks of the streaming-read measurement kernel."""
     def call(nbytes=4096, sink_words=1 << 20, block=256, loads=4, src=A, sink=A):
