@@ -84,17 +84,19 @@ def test_compress_kernel_has_no_scratch(tmp_path):
 
 def test_multi_token_kernel_budget(tmp_path):
     """Multi-token decode instances (NB 1..5 x grid kind x 2..4 tokens x
-    contiguous / paged cache): no
-    scratch, at most 256 VGPRs (one workgroup per CU when above 128), and
-    the one-round instances' LDS with the padding within a CU."""
+    (3-bit paged decode; contiguous 2-, 3- and 4-bit records, decode and the
+    fused step)): no scratch, at most 256 VGPRs (one workgroup per CU when
+    above 128), and the one-round instances' LDS with the padding within a
+    CU."""
     asm = _device_asm("iq_decode_multi.hip", tmp_path)
     src = open(os.path.join(B.CSRC, "iq_g8_device.h")).read()
     pad = eval(re.search(r"kOneWorkgroupPadBytes\s*=\s*([^;]+);", src).group(1))
     ks = _kernels(asm)
     mt = {n: v for n, v in ks.items() if "decode_g8_multi_kernel" in n}
-    assert len(mt) == 60, sorted(mt)
+    assert len(mt) == 210, sorted(mt)
     for name, (vg, lds, priv) in mt.items():
-        m = re.search(r"decode_g8_multi_kernelILi(\d)ELb(\d)ELi(\d)ELb(\d)EE", name)
+        m = re.search(r"decode_g8_multi_kernelILi(\d)ELb(\d)ELi(\d)ELb(\d)ELi(\d)ELb(\d)EE",
+                      name)
         wide = m.group(2) == "1"
         assert priv == 0, f"{name}: scratch {priv}"
         assert vg <= 256, f"{name}: {vg} VGPRs"
