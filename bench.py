@@ -748,14 +748,20 @@ def run_multi32k(args, torch, api, synth, dev):
     """Multi-token decode at the 32K shape: T = 1..4 query tokens per call
     over the same 48 cycled layer caches (iq_decode_attention_multi), against
     T single-token calls.  Algorithmic bytes per call: the cache read once
-    (104 B per position and KV head) plus the T tokens' queries and outputs."""
+    (104 B per position and KV head) plus the T tokens' queries and outputs.
+    Then the fused multi-token step (iq_decode_step_multi, T = 2 and 4: the T
+    new tokens compressed, appended and attended causally in the same call)
+    on the same caches, whose capacity leaves room for the appended tokens;
+    its bytes add the new fp16 keys and values read and their records
+    written."""
     import numpy as np
 
     w = synth.WORKLOADS[2]
     nl = args.layers
     cap = args.context
+    capacity = (cap + 4 * visits_per_layer(args.warmup, args.steps, nl) + 64 + 63) // 64 * 64
     print(f"# building {nl} layer caches", file=sys.stderr, flush=True)
-    quats, layers = make_layers(api, synth, w, nl, cap, cap, args.seed, dev)
+    quats, layers = make_layers(api, synth, w, nl, cap, capacity, args.seed, dev)
     per = {}
     for n_tok in (1, 2, 3, 4):
         g = torch.Generator(device=dev)
@@ -783,6 +789,39 @@ def run_multi32k(args, torch, api, synth, dev):
     single = per[1]["us_per_call"]
     for n_tok, d in per.items():
         d["vs_single_calls"] = round(n_tok * single / d["us_per_call"], 3)
+    fused = {}
+    for n_tok in (2, 4):
+        for layer in layers:
+            layer["cache"]["seq_lens"].fill_(cap)
+        g = torch.Generator(device=dev)
+        g.manual_seed(args.seed * 11 + n_tok)
+        qs = [torch.randn((w.batch, n_tok, w.n_q_heads, 128), generator=g, device=dev)
+              for _ in range(nl)]
+        kv = [[torch.randn((w.batch, n_tok, w.n_kv_heads, 128), generator=g, device=dev).half()
+               for _ in range(2)] for _ in range(nl)]
+        outs = [torch.empty_like(x) for x in qs]
+        ws = torch.empty(api.iq_decode_multi_workspace_bytes(w.batch, n_tok, w.n_q_heads,
+                                                             w.n_kv_heads, capacity),
+                         dtype=torch.uint8, device=dev)
+
+        def step(li, qs=qs, kv=kv, outs=outs, ws=ws):
+            c = layers[li]["cache"]
+            api.iq_decode_step_multi(qs[li], kv[li][0], kv[li][1], c["k_codes"], c["k_norms"],
+                                     c["v_codes"], c["v_norms"], c["seq_lens"], quats,
+                                     out=outs[li], workspace=ws, max_seq_len=capacity)
+
+        us = time_graph_calls(torch, step, nl, args.steps, args.warmup)[0]
+        grown = int(layers[0]["cache"]["seq_lens"][0].item())
+        assert cap < grown <= capacity, (cap, grown, capacity)
+        nbytes = (w.n_kv_heads * cap * BYTES_PER_TOKEN_HEAD + 2 * n_tok * w.n_q_heads * 128 * 4
+                  + n_tok * w.n_kv_heads * (2 * 128 * 2 + BYTES_PER_TOKEN_HEAD))
+        fused[n_tok] = {"us_per_call": round(us, 3), "bytes": int(nbytes),
+                        "gbs": round(nbytes / (us * 1e-6) / 1e9, 2),
+                        "vs_multi_decode": round(us / per[n_tok]["us_per_call"], 3),
+                        "length_after": grown}
+        del qs, kv, outs, ws
+    for layer in layers:
+        layer["cache"]["seq_lens"].fill_(cap)
     value = per[t]["gbs"]
     return {
         "metric": f"{t}-token decode-attention µs/call + achieved HBM GB/s, 32K ctx",
@@ -808,6 +847,7 @@ def run_multi32k(args, torch, api, synth, dev):
                                f"{t}>" if t > 1 else "decode_g8_kernel + merge_g8_kernel",
                      "bytes_per_launch": per[t]["bytes"], "launch_us": per[t]["us_per_call"]},
         "per_tokens": {str(k): v for k, v in per.items()},
+        "fused_step": {str(k): v for k, v in fused.items()},
     }
 
 
