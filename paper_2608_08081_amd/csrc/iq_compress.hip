@@ -1,15 +1,25 @@
 // IsoQuant compression kernels (Algorithm 1; Sec. 3.2 Steps 1-4) for gfx950.
 //
-// Bulk compression: one lane compresses one 128-dim vector entirely in
-// registers, with no cross-lane traffic.  A workgroup (4 waves) takes 256
-// consecutive tokens of one (K|V, sequence, KV head); it first builds the
-// head's 32 block matrices M_i H_4 in LDS (2 KB), which every lane then reads
-// as wave-uniform 16-byte rows (LDS broadcasts).
+// Bulk compression: two adjacent lanes compress one 128-dim vector in
+// registers, lane 2j + h holding dims 64 h .. 64 h + 63 of vector j.  A
+// workgroup (4 waves) takes 128 consecutive tokens of one (K|V, sequence, KV
+// head); it first builds the head's 32 block matrices M_i H_4 in LDS (2 KB),
+// which the lanes then read as 16-byte rows (two addresses per read, one per
+// half: LDS broadcasts).  Half a vector per lane keeps about 100 registers
+// per lane, so five waves share a SIMD and the vector-ALU work of one wave
+// runs while the others wait on memory.
 //
 // Per vector:
 //   s^2  = sum x_i^2 in fp64 (products of fp16/fp32 inputs are exact in fp64),
-//          stored scale = fp32(sqrt(s^2))  (Step 1);
-//   y    = diag(M_i H_4) (H_32 (x) I_4) x   unnormalized, fp32  (Step 2);
+//          each half summed in its lane, the two sums added (Step 1);
+//          stored scale = fp32(sqrt(s^2));
+//   y    = diag(M_i H_4) (H_32 (x) I_4) x   unnormalized, fp32  (Step 2).
+//          H_32 acts on index bits 2..6; bit 6 is the lane of the pair, so
+//          its butterfly is one fused multiply-add per value with the
+//          partner's value (a cross-lane read): the lower lane gets a + b,
+//          the upper lane b - a = -(a - b).  The upper lane's values then
+//          carry a factor -1 through the remaining (linear) butterflies on
+//          bits 2..5, which it undoes by using -M_i for its blocks 16..31;
 //   code = #{j : y >= t_j * s * sqrt(128)}  (Step 3; comparing the
 //          unnormalized y against scaled thresholds is the same test as
 //          comparing R x / s against t_j, and saves 128 multiplies).  The
@@ -17,9 +27,12 @@
 //          4 + m for y >= 0 and 3 - m = (4 + m) ^ 7 for y < 0, where
 //          m = #{k = 1..3 : |y| >= T_k} comes from a two-step search; the
 //          two rules differ only when |y| equals a threshold exactly;
-//   pack = 3-bit codes into 12 words, stored as three 16-byte writes (Step 4).
+//   pack = 3-bit codes into 12 words; codes 0..63 fill words 0..5 (lower
+//          lane) and codes 64..127 words 6..11 (upper lane), each lane
+//          storing its 24 bytes (Step 4).
 // The same kernel compresses to b = 2 or b = 4 bit codes (Algorithm 1 with
-// C_2 or C_4: 2^(b-1) - 1 positive thresholds, records of 4b words).
+// C_2 or C_4: 2^(b-1) - 1 positive thresholds, records of 4b words, 2b per
+// lane).
 // A vector whose s^2 is not finite (NaN or infinite input) gets the record of
 // all-NaN coordinates, code 0 everywhere, as #{j : t_j <= NaN} = 0.
 #include <hip/hip_fp16.h>
@@ -33,12 +46,15 @@ namespace {
 
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kCompressThreads = 256;   // tokens per workgroup
+constexpr int kCompressThreads = 256;
+constexpr int kCompressTokens = kCompressThreads / 2;   // two lanes per vector
+constexpr int kHalfDim = kDim / 2;
 
-__device__ __forceinline__ void load_vector(const __half* src, float (&x)[kDim]) {
+// One half (64 dims) of a vector of fp16 or fp32 input.
+__device__ __forceinline__ void load_half(const __half* src, float (&x)[kHalfDim]) {
   const uint4* p = reinterpret_cast<const uint4*>(src);
 #pragma unroll
-  for (int i = 0; i < kDim / 8; ++i) {
+  for (int i = 0; i < kHalfDim / 8; ++i) {
     const uint4 u = p[i];
     const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
@@ -49,10 +65,10 @@ __device__ __forceinline__ void load_vector(const __half* src, float (&x)[kDim])
   }
 }
 
-__device__ __forceinline__ void load_vector(const float* src, float (&x)[kDim]) {
+__device__ __forceinline__ void load_half(const float* src, float (&x)[kHalfDim]) {
   const float4* p = reinterpret_cast<const float4*>(src);
 #pragma unroll
-  for (int i = 0; i < kDim / 4; ++i) {
+  for (int i = 0; i < kHalfDim / 4; ++i) {
     const float4 f = p[i];
     x[4 * i] = f.x;
     x[4 * i + 1] = f.y;
@@ -99,8 +115,9 @@ __device__ __forceinline__ uint32_t quantize_sym_b(float y, const float (&t)[(1 
   return ((h + m) ^ flip) << off;
 }
 
-// OR the code of coordinate i (bits 3i .. 3i+2 of the record) into w.
-__device__ __forceinline__ void put_code_sym(uint32_t (&w)[kRecordWords], int i, float y,
+// OR the code of coordinate i of a half (bits 3i .. 3i+2 of the half
+// record) into w.
+__device__ __forceinline__ void put_code_sym(uint32_t (&w)[kRecordWords / 2], int i, float y,
                                              float t1, float t2, float t3) {
   const int bit = 3 * i;
   const int word = bit >> 5, off = bit & 31;
@@ -113,29 +130,57 @@ __device__ __forceinline__ void put_code_sym(uint32_t (&w)[kRecordWords], int i,
   }
 }
 
-// Compress one vector (Algorithm 1) and write its record and scale.
-// mtab: rows of the head's block matrices M_i H_4 (row r of block i at
-// mtab[4 i + r]).  The record has 4 kBits words.
-template <typename T, int kBits>
-__device__ __forceinline__ void compress_one(const T* __restrict__ src, const f32x4_t* mtab,
-                                             uint8_t* __restrict__ dst_code,
-                                             float* __restrict__ dst_norm,
-                                             const CodebookB<kBits>& cb) {
-  constexpr int kWords = 4 * kBits;
-  constexpr int kHalf = 1 << (kBits - 1);
-  float x[kDim];
-  load_vector(src, x);
+// x[i] += x_partner[i] * sg for i = i0 .. i0 + 7, the partner lane being
+// lane ^ 1: one multiply-add per value whose first operand is read from the
+// partner lane (DPP quad permutation [1, 0, 3, 2]).  Written out because the
+// compiler keeps the lane move as a separate instruction.  The leading
+// s_nop 1 gives the two wait states a DPP read needs after the VALU write of
+// its source register; the eight instructions read only registers written
+// before the block.
+__device__ __forceinline__ void cross_butterfly8(float (&x)[kDim / 2], int i0, float sg) {
+  asm volatile(
+      "s_nop 1\n\t"
+      "v_fmac_f32_dpp %0, %0, %8 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_fmac_f32_dpp %1, %1, %8 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_fmac_f32_dpp %2, %2, %8 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_fmac_f32_dpp %3, %3, %8 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_fmac_f32_dpp %4, %4, %8 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_fmac_f32_dpp %5, %5, %8 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_fmac_f32_dpp %6, %6, %8 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_fmac_f32_dpp %7, %7, %8 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf"
+      : "+v"(x[i0]), "+v"(x[i0 + 1]), "+v"(x[i0 + 2]), "+v"(x[i0 + 3]), "+v"(x[i0 + 4]),
+        "+v"(x[i0 + 5]), "+v"(x[i0 + 6]), "+v"(x[i0 + 7])
+      : "v"(sg));
+}
 
-  // Step 1: fp64 sum of squares, four independent chains.
+// Compress one half of a vector (Algorithm 1) and write its half of the
+// record (and, lower lane, the scale).  half: 0 for dims 0..63, 1 for dims
+// 64..127; the partner lane (lane ^ 1) holds the other half and must run
+// the same code.  mtab: rows of the head's block matrices M_i H_4 (row r of
+// block i at mtab[4 i + r]), negated for blocks 16..31.
+template <typename T, int kBits>
+__device__ __forceinline__ void compress_half(const T* __restrict__ src, const f32x4_t* mtab,
+                                              uint8_t* __restrict__ dst_code,
+                                              float* __restrict__ dst_norm,
+                                              const CodebookB<kBits>& cb, int half) {
+  constexpr int kWords = 2 * kBits;   // this lane's half of the record
+  constexpr int kHalf = 1 << (kBits - 1);
+  float x[kHalfDim];
+  load_half(src + kHalfDim * half, x);
+
+  // Step 1: fp64 sum of squares of this half (four independent chains),
+  // plus the partner's
   double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
 #pragma unroll
-  for (int i = 0; i < kDim; i += 4) {
+  for (int i = 0; i < kHalfDim; i += 4) {
     a0 = fma(static_cast<double>(x[i]), static_cast<double>(x[i]), a0);
     a1 = fma(static_cast<double>(x[i + 1]), static_cast<double>(x[i + 1]), a1);
     a2 = fma(static_cast<double>(x[i + 2]), static_cast<double>(x[i + 2]), a2);
     a3 = fma(static_cast<double>(x[i + 3]), static_cast<double>(x[i + 3]), a3);
   }
-  const double ss = (a0 + a1) + (a2 + a3);
+  double ss = (a0 + a1) + (a2 + a3);
+  // the two halves' sums (the same sum in both lanes: addition commutes)
+  ss += xor_lane64_f64<1>(ss);
   const double s = sqrt(ss);
   const bool finite = ss < static_cast<double>(INFINITY);
 
@@ -152,11 +197,15 @@ __device__ __forceinline__ void compress_one(const T* __restrict__ src, const f3
     asm volatile("" : "+v"(tp[j]));
   }
 
-  // Step 2a: Walsh-Hadamard butterflies on index bits 2..6 (H_32 (x) I_4).
+  // Step 2a: the butterfly on index bit 6 (across the lane pair: the lower
+  // lane a + b, the upper lane b - a), then bits 2..5 in the lane.
+  const float sg = half ? -1.0f : 1.0f;
 #pragma unroll
-  for (int st = 4; st < kDim; st <<= 1) {
+  for (int i = 0; i < kHalfDim; i += 8) cross_butterfly8(x, i, sg);
 #pragma unroll
-    for (int i = 0; i < kDim; ++i) {
+  for (int st = 4; st < kHalfDim; st <<= 1) {
+#pragma unroll
+    for (int i = 0; i < kHalfDim; ++i) {
       if (!(i & st)) {
         const float a = x[i], b = x[i + st];
         x[i] = a + b;
@@ -166,15 +215,16 @@ __device__ __forceinline__ void compress_one(const T* __restrict__ src, const f3
   }
 
   // Step 2b + 3 + 4: per block, y = (M_i H_4) z, quantize, pack.
+  const f32x4_t* mt = mtab + 64 * half;   // blocks 16 half .. 16 half + 15
   uint32_t w[kWords];
 #pragma unroll
   for (int i = 0; i < kWords; ++i) w[i] = 0u;
 #pragma unroll
-  for (int blk = 0; blk < kNumBlocks; ++blk) {
+  for (int blk = 0; blk < kNumBlocks / 2; ++blk) {
     const float z0 = x[4 * blk], z1 = x[4 * blk + 1], z2 = x[4 * blk + 2], z3 = x[4 * blk + 3];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const f32x4_t m = mtab[4 * blk + r];
+      const f32x4_t m = mt[4 * blk + r];
       const float y = m[0] * z0 + m[1] * z1 + m[2] * z2 + m[3] * z3;
       const int i = 4 * blk + r;
       if constexpr (kBits == 3) {
@@ -190,15 +240,24 @@ __device__ __forceinline__ void compress_one(const T* __restrict__ src, const f3
     for (int i = 0; i < kWords; ++i) w[i] = 0u;
   }
 
-  uint4* out = reinterpret_cast<uint4*>(dst_code);
+  uint32_t* out = reinterpret_cast<uint32_t*>(dst_code) + kWords * half;
+  if constexpr (kWords % 4 == 0) {
 #pragma unroll
-  for (int j = 0; j < kBits; ++j)
-    out[j] = make_uint4(w[4 * j], w[4 * j + 1], w[4 * j + 2], w[4 * j + 3]);
-  *dst_norm = static_cast<float>(s);
+    for (int j = 0; j < kWords / 4; ++j)
+      reinterpret_cast<uint4*>(out)[j] = make_uint4(w[4 * j], w[4 * j + 1], w[4 * j + 2],
+                                                    w[4 * j + 3]);
+  } else {
+    // 24 bytes at byte 0 or 24 of the record: 8-byte aligned
+#pragma unroll
+    for (int j = 0; j < kWords / 2; ++j)
+      reinterpret_cast<uint2*>(out)[j] = make_uint2(w[2 * j], w[2 * j + 1]);
+  }
+  if (half == 0) *dst_norm = static_cast<float>(s);
 }
 
 // Bulk compression.  1-D grid of 256-thread workgroups:
-//   blockIdx.x = (which * (B*H) + bh) * chunks + chunk,  thread = token in chunk.
+//   blockIdx.x = (which * (B*H) + bh) * chunks + chunk,  thread 2 j + h =
+//   half h of token j of the chunk (128 tokens).
 // kPaged: the destination is a page pool; a token whose page index is
 // invalid is not written.
 template <typename T, bool kPaged, int kBits>
@@ -215,7 +274,8 @@ __global__ __launch_bounds__(kCompressThreads) void compress_kernel(
   const int which = static_cast<int>(rest / n_bh);
   const int h = static_cast<int>(bh % n_heads);
   const int tid = threadIdx.x;
-  // rows of M_i H_4: thread tid < 128 builds row tid % 4 of block tid / 4
+  // rows of M_i H_4: thread tid < 128 builds row tid % 4 of block tid / 4,
+  // negated for blocks 16..31 (whose lane holds its values negated)
   if (tid < kNumBlocks * 4) {
     float m[4][4];
     so4_matrix_h4(quats + static_cast<int64_t>(h) * kQuatFloats + 8 * (tid >> 2), m);
@@ -224,10 +284,10 @@ __global__ __launch_bounds__(kCompressThreads) void compress_kernel(
 #pragma unroll
     for (int i = 1; i < 4; ++i)
       if (r == i) row = f32x4_t{m[i][0], m[i][1], m[i][2], m[i][3]};
-    mtab[tid] = row;
+    mtab[tid] = (tid >> 2) >= kNumBlocks / 2 ? -row : row;
   }
   __syncthreads();
-  const int64_t t = chunk * kCompressThreads + tid;
+  const int64_t t = chunk * kCompressTokens + (tid >> 1);
   if (t >= n_tokens) return;
   const T* src = which ? src1 : src0;
   uint8_t* codes = which ? codes1 : codes0;
@@ -237,8 +297,8 @@ __global__ __launch_bounds__(kCompressThreads) void compress_kernel(
     pos = paged_record(pages, n_heads, static_cast<int>(bh / n_heads), h, dst_offset + t);
     if (pos < 0) return;
   }
-  compress_one<T, kBits>(src + (bh * n_tokens + t) * kDim, mtab,
-                         codes + pos * record_bytes<kBits>(), norms + pos, cb);
+  compress_half<T, kBits>(src + (bh * n_tokens + t) * kDim, mtab,
+                          codes + pos * record_bytes<kBits>(), norms + pos, cb, tid & 1);
 }
 
 // Per-step append: one workgroup per sequence, one wave per vector (keys and
@@ -316,7 +376,7 @@ hipError_t launch_compress_any(const void* k, const void* v, int dtype, int64_t 
   float* n1 = (k && v) ? v_norms : nullptr;
   const int nwhich = s1 ? 2 : 1;
   const int64_t n_bh = batch * n_heads;
-  const int64_t chunks = (n_tokens + kCompressThreads - 1) / kCompressThreads;
+  const int64_t chunks = (n_tokens + kCompressTokens - 1) / kCompressTokens;
   const int64_t blocks = chunks * n_bh * nwhich;
   if (blocks == 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>(blocks)), block(kCompressThreads);
