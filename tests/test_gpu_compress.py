@@ -83,6 +83,49 @@ def test_compress_special_vectors():
     assert rec[1].tobytes() == bytes([0x6D, 0xDB, 0xB6]) * 16
 
 
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_compress_special_vectors_f16(bits):
+    """fp16 input (the matrix-core kernel).  Zero and negative-zero vectors:
+    scale 0 and every code the first non-negative level; e_0 with identity
+    SO(4) parameters: the hand-derived 3-bit record; vectors of fp16
+    subnormals (alone and next to normal values) compress like any other
+    values; an infinite or NaN entry gives the all-zero record."""
+    levels, thr = ocb.isoquant_codebook(128, bits)
+    g = np.random.default_rng(7)
+    x = np.zeros((1, 1, 40, 128), np.float16)
+    x[0, 0, 1] = -0.0
+    x[0, 0, 2, 0] = 1.0
+    x[0, 0, 3, 7] = np.inf
+    x[0, 0, 4, 100] = np.nan
+    sub = (g.integers(-1023, 1024, (16, 128)) * 2.0 ** -24).astype(np.float16)
+    x[0, 0, 5:21] = sub                                       # subnormals only
+    x[0, 0, 21:37] = sub
+    x[0, 0, 21:37, ::17] = g.standard_normal((16, 8)).astype(np.float16)
+    x[0, 0, 37:] = g.standard_normal((3, 128)).astype(np.float16)
+    assert np.all(np.abs(sub.astype(np.float64)) < 2.0 ** -14)
+    for ident, quats_np in ((True, orot.identity_quaternions(1)),
+                            (False, orot.make_quaternions(11, 1))):
+        quats = torch.from_numpy(quats_np).to(DEV)
+        cache = api.alloc_cache(1, 1, 40, DEV, values=False, bits=bits)
+        print(f"[compress f16 special] bits={bits}", flush=True)
+        api.iq_compress_kv_bits(_dev(x), None, quats, cache["k_codes"], cache["k_norms"],
+                                bits=bits)
+        torch.cuda.synchronize()
+        rec = cache["k_codes"].cpu().numpy()[0, 0]
+        nrm = cache["k_norms"].cpu().numpy()[0, 0]
+        assert nrm[0] == 0 and nrm[1] == 0 and nrm[2] == 1.0
+        for i in (0, 1):
+            assert np.all(ocz.unpack(rec[i], 128, bits) == 1 << (bits - 1))
+        assert not rec[3].any() and not rec[4].any()
+        if bits == 3 and ident:
+            assert rec[2].tobytes() == bytes([0x6D, 0xDB, 0xB6]) * 16
+        ok = [2] + list(range(5, 40))
+        rots = orot.rotation_matrices(quats_np)
+        _, _, codes, y, s64 = ocz.compress_kv(x[:, :, ok].astype(np.float32), rots, thr)
+        check_codes(rec[None, None, ok], codes, y, thr, f"f16 special b{bits}")
+        check_norms(nrm[None, None, ok], s64, f"f16 special b{bits}")
+
+
 def test_compress_empty_is_noop():
     w = synth.WORKLOADS[1]
     quats = api.iq_make_rotation(w.rotation_seed, w.n_kv_heads).to(DEV)
