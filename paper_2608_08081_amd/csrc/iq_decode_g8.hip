@@ -95,8 +95,13 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][kBits],
                                             const u32x4_t* qbr = nullptr) {
   // ---- phase 1: scores (Table 2 A) -----------------------------------------
   // the value load of batch i goes out as batch i's scores start, so that
-  // phase 1 begins without waiting to issue every value load first
-  f32x4_t sc[NBX];
+  // phase 1 begins without waiting to issue every value load first.
+  // Lanes col and col ^ 8 hold the same four scores (positions 4 grp + r);
+  // from here on the lane with col < 8 keeps positions r = 0, 1 and its
+  // partner r = 2, 3 (rs = 0 or 2), so each weight is computed once.
+  const bool upper = col >= 8;
+  const int rs = upper ? 2 : 0;
+  f32x2_t sc[NBX];
   u32x4_t rk[NBX][2];
   if constexpr (kRope) {
     rk[0][0] = rk0[0];
@@ -140,40 +145,49 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][kBits],
       for (int r = 0; r < 4; ++r) acc[r] += xor_lane<8>(acc[r]);
       x = acc * st.ks[4 * i + grp];
     }
+    f32x2_t xs = upper ? f32x2_t{x[2], x[3]} : f32x2_t{x[0], x[1]};
     if (!kFull && 16 * i + 16 > nvalid) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) x[r] = (16 * i + 4 * grp + r < nvalid) ? x[r] : -INFINITY;
+      for (int j = 0; j < 2; ++j) xs[j] = (16 * i + 4 * grp + rs + j < nvalid) ? xs[j] : -INFINITY;
     }
-    sc[i] = x;
-    m_run = fmaxf(fmaxf(m_run, x[0]), x[1]);
-    m_run = fmaxf(fmaxf(m_run, x[2]), x[3]);
+    sc[i] = xs;
+    m_run = fmaxf(fmaxf(m_run, xs[0]), xs[1]);
   }
-  m_run = wave_max(m_run);
+  m_run = wave_max(fmaxf(m_run, xor_lane<8>(m_run)));
   // weight scales s^V * 2^15 / vmax.  Wide grids: staged that way in the
   // prologue and read per batch, so the kernel stays within 128 VGPRs.
   // Otherwise: the batches' value scales are read into registers here,
   // before the fence below (which would hold the reads back), with vmax
   // taken over them (off the prologue's critical path).
-  f32x4_t wvv[NBX];
+  f32x2_t wvv[NBX];
   if constexpr (!kWide) {
 #pragma unroll
     for (int i = 0; i < NBX; ++i) {
       if (!kFull && 16 * i >= nvalid) break;
-      f32x4_t v = st.vs[4 * i + grp];
+      f32x2_t v = *reinterpret_cast<const f32x2_t*>(
+          reinterpret_cast<const float*>(&st.vs[4 * i + grp]) + rs);
       if (!kFull && 16 * i + 16 > nvalid) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = (16 * i + 4 * grp + r < nvalid) ? v[r] : 0.f;
+        for (int j = 0; j < 2; ++j) v[j] = (16 * i + 4 * grp + rs + j < nvalid) ? v[j] : 0.f;
       }
       wvv[i] = v;
       vmax = fmaxf(fmaxf(vmax, v[0]), v[1]);
-      vmax = fmaxf(fmaxf(vmax, v[2]), v[3]);
     }
-    vmax = wave_max(vmax);
+    vmax = wave_max(fmaxf(vmax, xor_lane<8>(vmax)));
     const float vinv = vmax > 0.f ? 32768.0f * __builtin_amdgcn_rcpf(vmax) : 0.f;
 #pragma unroll
     for (int i = 0; i < NBX; ++i) wvv[i] *= vinv;
   }
-  const uint32_t slot_shift = (col >= 8) ? 16u : 0u;
+  // v_perm_b32 selectors of the PV operand dwords.  Operand dword r of the
+  // lane holds the hi (lo) part of position r's weight in half `upper`, zero
+  // in the other half.  Position j (j = 0, 1) comes from the lower lane of
+  // the pair, position 2 + j from the upper one; perm(x, y, sel) reads the
+  // packed pair x as bytes 4..7 and y as bytes 0..3, so with (own, partner)
+  // for positions j and (partner, own) for positions 2 + j one selector
+  // serves both.  The zero bytes use selector values 8 and 10 (a copy of
+  // the sign bit of a weight part, 0: the weights are not negative), so
+  // the lo selector is the hi one with bit 1 of every byte set.
+  const uint32_t sel_hi = upper ? 0x01000808u : 0x08080504u;
   const float mq = -m_run * qdown;
 
   // ---- phase 2: weights (Table 2 B) and values (Table 2 C) -----------------
@@ -191,18 +205,41 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][kBits],
   for (int i = 0; i < NBX; ++i) {
     if (!kFull && 16 * i >= nvalid) break;
     const uint32_t* rec = st.rec[i];
-    const f32x4_t wv = kWide ? st.vs[4 * i + grp] : wvv[i];   // 0 past nvalid
-    u32x4_t pw_hi, pw_lo;
+    // the weight scales of this lane's two positions (0 past nvalid)
+    const f32x2_t wv =
+        kWide ? *reinterpret_cast<const f32x2_t*>(
+                    reinterpret_cast<const float*>(&st.vs[4 * i + grp]) + rs)
+              : wvv[i];
+    // weight p split into p_hi (p with its low 13 mantissa bits cleared:
+    // exact in fp16 over the weights' range) and p_lo = p - p_hi (exact in
+    // fp32, then fp16), packed as one dword (hi in bits 0..15)
+    uint32_t pk[2];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[i][r], qdown, mq));
+    for (int j = 0; j < 2; ++j) {
+      const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[i][j], qdown, mq));
       l_run += e;
-      const float pf = e * wv[r];
-      const _Float16 ph = static_cast<_Float16>(pf);
-      const _Float16 pl = static_cast<_Float16>(pf - static_cast<float>(ph));
-      pw_hi[r] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, ph)) << slot_shift;
-      pw_lo[r] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, pl)) << slot_shift;
+      const float pf = e * wv[j];
+      const float ph = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, pf) & 0xFFFFE000u);
+      pk[j] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(ph, pf - ph));
     }
+    // the partner lane's pairs (row_ror:8 inside each row of 16 lanes)
+    const uint32_t pp0 = static_cast<uint32_t>(
+        __builtin_amdgcn_mov_dpp(static_cast<int>(pk[0]), 0x128, 0xF, 0xF, true));
+    const uint32_t pp1 = static_cast<uint32_t>(
+        __builtin_amdgcn_mov_dpp(static_cast<int>(pk[1]), 0x128, 0xF, 0xF, true));
+    const u32x4_t pw_hi = u32x4_t{__builtin_amdgcn_perm(pk[0], pp0, sel_hi),
+                                  __builtin_amdgcn_perm(pk[1], pp1, sel_hi),
+                                  __builtin_amdgcn_perm(pp0, pk[0], sel_hi),
+                                  __builtin_amdgcn_perm(pp1, pk[1], sel_hi)};
+    // (formed per batch: one instruction rather than a register held
+    // across the loop)
+    uint32_t sel_lo = sel_hi;
+    asm volatile("" : "+v"(sel_lo));
+    sel_lo |= 0x02020202u;
+    const u32x4_t pw_lo = u32x4_t{__builtin_amdgcn_perm(pk[0], pp0, sel_lo),
+                                  __builtin_amdgcn_perm(pk[1], pp1, sel_lo),
+                                  __builtin_amdgcn_perm(pp0, pk[0], sel_lo),
+                                  __builtin_amdgcn_perm(pp1, pk[1], sel_lo)};
     u32x4_t vb[4];
     value_pairs<kBits>(lut, rec, grp, vdw, vsh, vb);
 #pragma unroll
@@ -211,7 +248,7 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][kBits],
       o_acc[nb] = mfma(pw_lo, vb[nb], o_acc[nb]);
     }
   }
-  l_run = wave_sum(l_run);
+  l_run = wave_sum(l_run + xor_lane<8>(l_run));
   m_run *= qdown;
 }
 
