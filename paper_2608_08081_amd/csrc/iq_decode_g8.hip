@@ -252,9 +252,30 @@ __device__ __forceinline__ void attend_wave(const uint32_t (&kw)[NB][kBits],
   m_run *= qdown;
 }
 
+// The waves' staging areas while attending and their outputs afterwards
+// (wave_o[w][r][lane] = the lane's accumulator entries r of the four PV
+// products, as written by the matrix cores).  kSepO: separate, so each wave
+// stores its outputs as soon as it is done (one-round grids, which have LDS
+// to spare); otherwise they share the space (grids of several rounds, two
+// workgroups per CU).
+template <int kBits, bool kSepO>
+struct G8Stage;
+template <int kBits>
+struct G8Stage<kBits, false> {
+  union {
+    WaveStageB<kBits> stage[kWaves];
+    f32x4_t wave_o[kWaves][4][64];
+  };
+};
+template <int kBits>
+struct G8Stage<kBits, true> {
+  WaveStageB<kBits> stage[kWaves];
+  f32x4_t wave_o[kWaves][4][64];
+};
+
 // LDS of the decode kernel, the pair table first (address 0: a lookup
 // address is just field * 4).
-template <int kBits, bool kRope>
+template <int kBits, bool kRope, bool kSepO>
 struct G8Smem {
   uint32_t lut[1 << (2 * kBits)];   // fp16 pair table: entry f = (C[f % 2^b], C[f / 2^b])
   uint32_t qop[2][kHeads][kQRowWords];
@@ -268,19 +289,12 @@ struct G8Smem {
   // sequences' inclusive item offsets and clamped lengths
   int chunk_incl[kWaves][64];
   int chunk_len[kWaves][64];
-  // the waves' staging areas while attending, their outputs afterwards
-  // (wave_o[w][r][lane] = the lane's accumulator entries r of the four
-  // PV products, as written by the matrix cores)
-  union {
-    WaveStageB<kBits> stage[kWaves];
-    f32x4_t wave_o[kWaves][4][64];
-  };
+  G8Stage<kBits, kSepO> st;
 };
 
 // Writes the fp16 pair table of the codebook (threads 0 .. 2^(2b) - 1).
-template <int kBits, bool kRope>
-__device__ __forceinline__ void build_pair_table(G8Smem<kBits, kRope>& sm,
-                                                 const CodebookB<kBits>& cb, int tid) {
+template <class Smem, int kBits>
+__device__ __forceinline__ void build_pair_table(Smem& sm, const CodebookB<kBits>& cb, int tid) {
   constexpr int kLut = 1 << (2 * kBits);
   if (tid < kLut) {
     constexpr int kMask = (1 << kBits) - 1;
@@ -323,8 +337,8 @@ struct G8Args {
 // at capacity, or at or past max_seq_len).  No attention work reads the
 // records being written, and seq_lens is advanced by the merge kernel after
 // every workgroup has read it.
-template <bool kPaged, int kBits, bool kRope>
-__device__ __forceinline__ void append_token(G8Smem<kBits, kRope>& sm, const G8Args<kBits>& a,
+template <bool kPaged, int kBits, bool kRope, class Smem>
+__device__ __forceinline__ void append_token(Smem& sm, const G8Args<kBits>& a,
                                              int gsize, int g, int vg, int b, int bgv,
                                              bool build_lut) {
   constexpr int kRB = record_bytes<kBits>();
@@ -427,8 +441,8 @@ __device__ __forceinline__ void append_token(G8Smem<kBits, kRope>& sm, const G8A
 // positions attended.  With several splits the item writes its partial
 // (m, l, O) per head; with one it writes the output row itself.
 // build_lut: the item writes the pair table (the workgroup's first item).
-template <int NB, bool kAppend, bool kWide, bool kPaged, int kBits, bool kRope>
-__device__ __forceinline__ void attend_split(G8Smem<kBits, kRope>& sm, const G8Args<kBits>& a,
+template <int NB, bool kAppend, bool kWide, bool kPaged, int kBits, bool kRope, class Smem>
+__device__ __forceinline__ void attend_split(Smem& sm, const G8Args<kBits>& a,
                                              int gsize, int split, int g, int vg, int b,
                                              int bgv, int seq_w, bool build_lut) {
   constexpr int kRB = record_bytes<kBits>();
@@ -439,8 +453,8 @@ __device__ __forceinline__ void attend_split(G8Smem<kBits, kRope>& sm, const G8A
   uint32_t(*qop)[kHeads][kQRowWords] = sm.qop;
   int* qexp_s = sm.qexp;
   float(*wave_ml)[2][kHeads] = sm.wave_ml;
-  WaveStageB<kBits>* stage = sm.stage;
-  f32x4_t(*wave_o)[4][64] = sm.wave_o;
+  WaveStageB<kBits>* stage = sm.st.stage;
+  f32x4_t(*wave_o)[4][64] = sm.st.wave_o;
 
   // the thread index, opaque to the compiler: in a persistent workgroup's
   // loop over items, values derived from it are then recomputed per item
@@ -702,7 +716,8 @@ __device__ __forceinline__ void attend_split(G8Smem<kBits, kRope>& sm, const G8A
         m_run, l_run, vmax, o_acc, rp, rk0, qbr);
 
   // ---- merge the 8 waves in LDS ---------------------------------------------
-  lds_barrier();   // every wave is done with its staging area
+  // (a shared output area: once every wave is done with its staging area)
+  if constexpr (kWide) lds_barrier();
   // lane (u = col, grp) holds rows 4 grp + r = (head (4 grp + r) % 8, slot
   // grp / 2) of MFMA nb, i.e. dim 8 u + 2 nb + slot; stored as one 16-byte
   // vector per (r, lane) over nb (consecutive lanes: no bank conflicts)
@@ -819,7 +834,7 @@ void decode_g8_kernel(
                         quats,    partials, out,     capacity,   max_seq_len, n_kv_heads,
                         n_splits, split_len, qscale, cb,         k_new,       v_new,
                         new_f16,  status,   pages,   group,      batch};
-  __shared__ __attribute__((aligned(16))) G8Smem<kBits, kRope> sm;
+  __shared__ __attribute__((aligned(16))) G8Smem<kBits, kRope, !kWide> sm;
   const int gsize = kAnyGroup ? a.group : kHeads;
   const int vshift = kAnyGroup && gsize > kHeads ? 1 : 0;
   const int n_rows = a.n_kv_heads << vshift;
