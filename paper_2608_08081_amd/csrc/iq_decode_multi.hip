@@ -359,9 +359,14 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
   wave_lds_fence();
 
   // phase 1 (Table 2 A): every batch's keys decoded once, the scores of all
-  // kT tokens kept in registers; one max per token and head afterwards
+  // kT tokens kept in registers; one max per token and head afterwards.
+  // Lanes col and col ^ 8 hold the same four scores; the lane with col < 8
+  // keeps positions r = 0, 1 of its row group and its partner r = 2, 3
+  // (rs), so each weight is computed once (see phase 2).
+  const bool upper = col >= 8;
+  const int rs = upper ? 2 : 0;
   float m_run[kT], l_run[kT];
-  f32x4_t sc[kT][NB];
+  f32x2_t sc[kT][NB];
 #pragma unroll
   for (int t = 0; t < kT; ++t) m_run[t] = -INFINITY;
 #pragma unroll
@@ -381,15 +386,16 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[r] += xor_lane<8>(acc[r]);
-      f32x4_t x = acc * ks;
+      const f32x4_t x = acc * ks;
+      f32x2_t xs = upper ? f32x2_t{x[2], x[3]} : f32x2_t{x[0], x[1]};
 #pragma unroll
-      for (int r = 0; r < 4; ++r) x[r] = (16 * i + 4 * grp + r < nv[t]) ? x[r] : -INFINITY;
-      sc[t][i] = x;
-      m_run[t] = fmaxf(fmaxf(m_run[t], fmaxf(x[0], x[1])), fmaxf(x[2], x[3]));
+      for (int j = 0; j < 2; ++j) xs[j] = (16 * i + 4 * grp + rs + j < nv[t]) ? xs[j] : -INFINITY;
+      sc[t][i] = xs;
+      m_run[t] = fmaxf(fmaxf(m_run[t], xs[0]), xs[1]);
     }
   }
 #pragma unroll
-  for (int t = 0; t < kT; ++t) m_run[t] = wave_max(m_run[t]);
+  for (int t = 0; t < kT; ++t) m_run[t] = wave_max(fmaxf(m_run[t], xor_lane<8>(m_run[t])));
 
   // phase 2 (Table 2 B, C): value records of all batches to the stage behind
   // one fence, then per batch the decoded values feed every token's weights
@@ -412,26 +418,49 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) o_acc[t][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
-  const uint32_t slot_shift = (col >= 8) ? 16u : 0u;
+  // PV operand dwords from the packed (hi, lo) fp16 parts of this lane's
+  // weights and its partner's (one DPP move), as in the single-token kernel:
+  // v_perm_b32 puts the hi or lo part in half `upper` of the dword and zero
+  // (a copy of a weight part's sign bit, 0) in the other half; the sources
+  // (own, partner) for positions r < 2 and (partner, own) for r >= 2 share
+  // one selector per part.
+  const uint32_t sel_hi = upper ? 0x01000808u : 0x08080504u;
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
     if (16 * i >= nvalid) break;
     u32x4_t vb[4];
     value_pairs<kBits>(lut, st.rec[i], grp, vdw, vsh, vb);
-    const f32x4_t wv = st.vs[4 * i + grp];   // 0 past the last token's length
+    // this lane's two positions (0 past the last token's length)
+    const f32x2_t wv =
+        *reinterpret_cast<const f32x2_t*>(reinterpret_cast<const float*>(&st.vs[4 * i + grp]) + rs);
 #pragma unroll
     for (int t = 0; t < kT; ++t) {
-      u32x4_t pw_hi, pw_lo;
+      // p_hi: p with its low 13 mantissa bits cleared (exact in fp16),
+      // p_lo = p - p_hi, packed hi in bits 0..15
+      uint32_t pk[2];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][i][r], qdown[t], mq[t]));
+      for (int j = 0; j < 2; ++j) {
+        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][i][j], qdown[t], mq[t]));
         l_run[t] += e;
-        const float pf = e * wv[r];
-        const _Float16 ph = static_cast<_Float16>(pf);
-        const _Float16 pl = static_cast<_Float16>(pf - static_cast<float>(ph));
-        pw_hi[r] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, ph)) << slot_shift;
-        pw_lo[r] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, pl)) << slot_shift;
+        const float pf = e * wv[j];
+        const float ph = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, pf) & 0xFFFFE000u);
+        pk[j] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(ph, pf - ph));
       }
+      const uint32_t pp0 = static_cast<uint32_t>(
+          __builtin_amdgcn_mov_dpp(static_cast<int>(pk[0]), 0x128, 0xF, 0xF, true));
+      const uint32_t pp1 = static_cast<uint32_t>(
+          __builtin_amdgcn_mov_dpp(static_cast<int>(pk[1]), 0x128, 0xF, 0xF, true));
+      uint32_t sel_lo = sel_hi;
+      asm volatile("" : "+v"(sel_lo));
+      sel_lo |= 0x02020202u;
+      const u32x4_t pw_hi = u32x4_t{__builtin_amdgcn_perm(pk[0], pp0, sel_hi),
+                                    __builtin_amdgcn_perm(pk[1], pp1, sel_hi),
+                                    __builtin_amdgcn_perm(pp0, pk[0], sel_hi),
+                                    __builtin_amdgcn_perm(pp1, pk[1], sel_hi)};
+      const u32x4_t pw_lo = u32x4_t{__builtin_amdgcn_perm(pk[0], pp0, sel_lo),
+                                    __builtin_amdgcn_perm(pk[1], pp1, sel_lo),
+                                    __builtin_amdgcn_perm(pp0, pk[0], sel_lo),
+                                    __builtin_amdgcn_perm(pp1, pk[1], sel_lo)};
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) {
         o_acc[t][nb] = mfma(pw_hi, vb[nb], o_acc[t][nb]);
@@ -441,7 +470,7 @@ __global__ __launch_bounds__(kThreads) void decode_g8_multi_kernel(
   }
 #pragma unroll
   for (int t = 0; t < kT; ++t) {
-    l_run[t] = wave_sum(l_run[t]);
+    l_run[t] = wave_sum(l_run[t] + xor_lane<8>(l_run[t]));
     m_run[t] *= qdown[t];   // log2 units
   }
 
