@@ -550,28 +550,28 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     }
     M = Mn;
   }
-  // combine the 8 split groups
-  if (dq == 0) red_m[sg] = M;
+  // combine the 8 split groups: each stores its (M, L, O) as it is, and
+  // lanes 0..31 of wave 0 (block tid of the head) rescale them to the common
+  // maximum while summing, divide by the sum and apply the inverse rotation
+  // in registers
+  *reinterpret_cast<f32x4_t*>(&red_o[sg][4 * dq]) = O;
+  if (dq == 0) {
+    red_m[sg] = M;
+    red_l[sg] = L;
+  }
   lds_barrier();
-  float Mt = red_m[0];
-#pragma unroll
-  for (int j = 1; j < 8; ++j) Mt = fmaxf(Mt, red_m[j]);
-  const float c = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mt);
-  red_o[sg][4 * dq] = c * O[0];
-  red_o[sg][4 * dq + 1] = c * O[1];
-  red_o[sg][4 * dq + 2] = c * O[2];
-  red_o[sg][4 * dq + 3] = c * O[3];
-  if (dq == 0) red_l[sg] = c * L;
-  lds_barrier();
-  // lanes 0..31 of wave 0: block tid of the head, divided by the sum, then
-  // the inverse rotation in registers
   if (tid < 32) {
+    float Mt = red_m[0];
+#pragma unroll
+    for (int j = 1; j < 8; ++j) Mt = fmaxf(Mt, red_m[j]);
     f32x4_t o = f32x4_t{0.f, 0.f, 0.f, 0.f};
     float l = 0.f;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      o += *reinterpret_cast<const f32x4_t*>(&red_o[j][4 * tid]);
-      l += red_l[j];
+      const float mj = red_m[j];
+      const float c = (mj == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mj - Mt);
+      o += c * *reinterpret_cast<const f32x4_t*>(&red_o[j][4 * tid]);
+      l += c * red_l[j];
     }
     // an empty sequence (every split empty) gives a zero row
     const f32x4_t r = l > 0.f ? rotate_inverse(o * (1.0f / l), ql, qr, tid)
