@@ -927,8 +927,9 @@ void decode_g8_kernel(
 
 // Split plan of the group-8 path: splits per (sequence, KV head) and their
 // length (a multiple of 16).  A workgroup covers at most 8 waves x 5 batches
-// x 16 = 640 positions, capped at 560 so that long contexts keep more
-// splits; while the grid is small (<= 4 rounds of one workgroup per CU) the
+// x 16 = 640 positions (at 640 every wave has 5 batches and every SIMD the
+// same load; a cap of 560 left three SIMDs with one batch more than the
+// fourth for the same per-item time); while the grid is small (<= 4 rounds of one workgroup per CU) the
 // split count is raised so that the grid, with the fused step's append
 // workgroup per (sequence, KV head), fills whole rounds, but a split keeps at
 // least one batch per wave.  n_rows: the (KV head, head group) rows of the
@@ -936,7 +937,7 @@ void decode_g8_kernel(
 void g8_plan(int64_t batch, int64_t n_rows, int64_t max_seq_len, int* nb, int64_t* n_splits,
              int64_t* split_len) {
   constexpr int64_t kCus = 256;
-  constexpr int64_t kMaxLen = 560;
+  constexpr int64_t kMaxLen = 640;
   const int64_t t = max_seq_len > 0 ? max_seq_len : 1;
   const int64_t bg = batch * n_rows > 0 ? batch * n_rows : 1;
   int64_t s = (t + kMaxLen - 1) / kMaxLen;

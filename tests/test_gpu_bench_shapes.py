@@ -41,7 +41,7 @@ def g8_instance(batch, n_kv_heads, max_seq_len, append=True):
     """The library's group-8 split plan (same rule as its planner): batches
     of 16 positions per wave, splits per (sequence, KV head), and whether the
     grid takes more than one round of 256 workgroups."""
-    cus, max_len = 256, 560
+    cus, max_len = 256, 640
     t = max(max_seq_len, 1)
     bg = max(batch * n_kv_heads, 1)
     s = -(-t // max_len)
