@@ -206,16 +206,19 @@ iq_status iq_append_token(const void* k_new, const void* v_new, int32_t dtype,
 
 /*
  * iq_decode_workspace_bytes - size of the device workspace iq_decode_attention
- * needs for these shapes (the split-K partial results).  Returns 0 for
- * invalid shapes.
+ * and iq_decode_step need for these shapes (the split-K partial results and,
+ * for the fused step, each sequence's length at the step's start, which the
+ * merge of the partials reads while the step advances seq_lens).  Returns 0
+ * for invalid shapes.
  */
 size_t iq_decode_workspace_bytes(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
                                  int64_t max_seq_len, int64_t head_dim);
 
 /*
  * iq_decode_workspace_init - zero-fill a workspace (a fill kernel on `stream`,
- * safe under graph capture).  Optional: iq_decode_attention overwrites every
- * workspace byte it reads within the same call, so it needs no initialization.
+ * safe under graph capture).  Optional: iq_decode_attention and iq_decode_step
+ * write every workspace byte they read within the same call, so the workspace
+ * needs no initialization.
  */
 iq_status iq_decode_workspace_init(void* workspace, size_t workspace_bytes,
                                    hipStream_t stream);

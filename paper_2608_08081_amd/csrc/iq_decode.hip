@@ -282,8 +282,8 @@ bool plan_decode(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads, int64_t m
     p.g8_splits = splits;
     p.g8_split_len = len;
     // one partial per split, and one for the fused step's new token
-    p.g8_partial_bytes =
-        round256(static_cast<size_t>(batch) * rows * (splits + 1) * 8 * kPartialFloats * 4);
+    p.g8_partial_bytes = g8_partial_region_bytes(batch, rows, splits) +
+                         round256(static_cast<size_t>(batch) * 4);
     if (p.g8_partial_bytes > need) need = p.g8_partial_bytes;
   }
   size_t generic_bytes = p.ticket_bytes + need;

@@ -328,6 +328,7 @@ struct G8Args {
   int32_t* status;
   PageTable pages;
   int group, batch;
+  int32_t* lens0;   // fused steps on grids of several rounds: each sequence's length
 };
 
 // The fused step's new token for (sequence b, KV head g, head group vg):
@@ -336,7 +337,8 @@ struct G8Args {
 // partial of split index n_splits (m = -inf when the token is not attended:
 // at capacity, or at or past max_seq_len).  No attention work reads the
 // records being written, and seq_lens is advanced by the merge kernel after
-// every workgroup has read it.
+// every workgroup has read it.  lens0 (grids of several rounds): the
+// sequence's length as read here, for the merge.
 template <bool kPaged, int kBits, bool kRope, class Smem>
 __device__ __forceinline__ void append_token(Smem& sm, const G8Args<kBits>& a,
                                              int gsize, int g, int vg, int b, int bgv,
@@ -374,6 +376,8 @@ __device__ __forceinline__ void append_token(Smem& sm, const G8Args<kBits>& a,
   const bool attend_new = written && seq0 < a.max_seq_len;
   if (!written && a.status != nullptr && g == 0 && vg == 0 && tid == 0)
     atomicOr(a.status, static_cast<int32_t>(IQ_ERR_CAPACITY));
+  // the length the merge counts the live splits of (grids of several rounds)
+  if (a.lens0 != nullptr && g == 0 && vg == 0 && tid == 0) a.lens0[b] = seq0;
   // waves 4 and 5 compress the new key and value: lane l holds dims 2l,
   // 2l + 1 and the parameters of SO(4) block l / 2
   if (wave == 4 || wave == 5) {
@@ -823,7 +827,8 @@ void decode_g8_kernel(
     float* __restrict__ partials, float* __restrict__ out, int64_t capacity, int max_seq_len,
     int n_kv_heads, int n_splits, int split_len, float qscale, CodebookB<kBits> cb,
     const void* __restrict__ k_new, const void* __restrict__ v_new, int new_f16,
-    int32_t* __restrict__ status, PageTable pages, int group, int batch) {
+    int32_t* __restrict__ status, PageTable pages, int group, int batch,
+    int32_t* __restrict__ lens0) {
   static_assert(kBits == 3 || !kPaged, "paged pools hold 3-bit records");
   static_assert(!kRope || (!kAppend && !kPaged && kBits == 3 && kAnyGroup),
                 "the positional split runs on contiguous 3-bit caches, decode only");
@@ -833,7 +838,7 @@ void decode_g8_kernel(
   const G8Args<kBits> a{q,        k_codes,  k_norms, v_codes,    v_norms,     seq_lens,
                         quats,    partials, out,     capacity,   max_seq_len, n_kv_heads,
                         n_splits, split_len, qscale, cb,         k_new,       v_new,
-                        new_f16,  status,   pages,   group,      batch};
+                        new_f16,  status,   pages,   group,      batch,       lens0};
   __shared__ __attribute__((aligned(16))) G8Smem<kBits, kRope, !kWide> sm;
   const int gsize = kAnyGroup ? a.group : kHeads;
   const int vshift = kAnyGroup && gsize > kHeads ? 1 : 0;
@@ -1002,13 +1007,21 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   const void* v_side = rope ? static_cast<const void*>(rope->q_rope) : v_new;
   const int flag = rope ? rope->shared : new_f16;
   const bool any_group = group != kHeads;
+  // fused steps on grids of several rounds: each sequence's length at the
+  // step's start, after the partials (the merge's count of live splits)
+  int32_t* const lens0 =
+      wide && append && n_parts > 1
+          ? reinterpret_cast<int32_t*>(reinterpret_cast<char*>(partials) +
+                                       g8_partial_region_bytes(batch, n_rows, n_splits))
+          : nullptr;
 #define IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_, ANY_)                           \
   hipLaunchKernelGGL((decode_g8_kernel<NB_, APP_, WIDE_, PAGED_, BITS_, ROPE_, ANY_>), grid,     \
                      block, lds_pad, stream, q, k_codes, k_norms, v_codes, v_norms, seq_lens,   \
                      quats, partials, out, capacity, static_cast<int>(max_seq_len),             \
                      static_cast<int>(n_kv_heads), static_cast<int>(n_splits),                  \
                      static_cast<int>(split_len), qscale, codebook_for<BITS_>(cb), k_side,      \
-                     v_side, flag, status, pt, static_cast<int>(group), static_cast<int>(batch))
+                     v_side, flag, status, pt, static_cast<int>(group), static_cast<int>(batch), \
+                     lens0)
 #define IQ_LAUNCH_G8_WPB(NB_, APP_, WIDE_, PAGED_, BITS_)         \
   if (any_group) {                                                \
     IQ_LAUNCH_G8_K(NB_, APP_, WIDE_, PAGED_, BITS_, false, true);  \
@@ -1076,7 +1089,7 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   hipLaunchKernelGGL((merge_g8_kernel<APP_, 1, ANY_, LIVE_>), mgrid, dim3(kMergeThreads), 0,    \
                      stream, partials, quats, out, static_cast<int>(n_kv_heads),                \
                      static_cast<int>(n_parts), seq_lens, capacity, static_cast<int>(group),    \
-                     static_cast<int>(split_len), static_cast<int>(max_seq_len))
+                     static_cast<int>(split_len), static_cast<int>(max_seq_len), lens0)
 #define IQ_LAUNCH_MERGE(APP_, ANY_)        \
   if (wide) {                              \
     IQ_LAUNCH_MERGE_L(APP_, ANY_, true);   \

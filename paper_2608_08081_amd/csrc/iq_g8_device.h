@@ -460,12 +460,14 @@ __device__ __forceinline__ void value_pairs(const uint32_t* lut, const uint32_t*
 // kLive (grids of several rounds, whose decode workgroups skip the splits
 // past a sequence's length): only the splits holding positions before
 // min(seq_lens[b], max_seq_len) are read (ceil of that over split_len), and
-// the new-token partial; the others were never written.
+// the new-token partial; the others were never written.  With kAppend the
+// length is lens0[b], the one the decode kernel saw (seq_lens[b] may already
+// be advanced by this launch's workgroup of head 0).
 template <bool kAppend, int kTok = 1, bool kAnyGroup = false, bool kLive = false>
 __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     const float* __restrict__ partials, const float* __restrict__ quats, float* __restrict__ out,
     int n_kv_heads, int n_parts, int32_t* __restrict__ seq_lens, int64_t capacity, int group,
-    int split_len = 0, int max_seq_len = 0) {
+    int split_len = 0, int max_seq_len = 0, const int32_t* __restrict__ lens0 = nullptr) {
   static_assert(kTok == 1 || !kLive, "multi-token partials are read in full");
   constexpr int kUnroll = 8;   // 8 x 8 = 64 splits per pass, all loads in flight
   __shared__ __attribute__((aligned(16))) float red_o[8][kDim];
@@ -505,7 +507,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
   // step) the new token's at index n_parts - 1
   int n_iter = n_parts;
   if constexpr (kLive) {
-    int seq = seq_lens[b];
+    // the fused step: the length as the decode kernel read it (workgroup
+    // (b, head 0) of this launch advances seq_lens[b])
+    int seq = kAppend ? lens0[b] : seq_lens[b];
     seq = seq < 0 ? 0 : (seq > max_seq_len ? max_seq_len : seq);
     n_iter = (seq + split_len - 1) / split_len + (kAppend ? 1 : 0);
   }

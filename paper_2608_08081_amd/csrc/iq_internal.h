@@ -89,11 +89,22 @@ struct DecodePlan {
   int64_t g8_splits;        // splits per (sequence, KV head, head group)
   int64_t g8_split_len;     // positions per split
   size_t ticket_bytes;      // reserved (0)
-  size_t g8_partial_bytes;  // B * H_kv * head groups * (splits + 1) * 8 * 130 floats
+  size_t g8_partial_bytes;  // g8_partial_region_bytes + one int32 per sequence
   size_t total_bytes;       // max over both paths
 };
 bool plan_decode(int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
                  int64_t max_seq_len, DecodePlan* plan);
+
+// Workspace of the matrix-core path after the reserved bytes: the partials
+// of every (sequence, row, split or new token) in this many bytes (rows =
+// KV heads x head groups), then one int32 per sequence: in fused steps on
+// grids of several rounds, the length each sequence had when the step
+// began, recorded by its append workgroup for the merge (whose workgroup of
+// head 0 advances seq_lens while the others still need the old length).
+inline size_t g8_partial_region_bytes(int64_t batch, int64_t rows, int64_t n_splits) {
+  const size_t b = static_cast<size_t>(batch) * rows * (n_splits + 1) * 8 * (2 + kDim) * 4;
+  return (b + 255) / 256 * 256;
+}
 
 // Kernel launchers (return the launch's hipError_t).
 // bits: 3 (the cache format), or 2 / 4 (records of 16 * bits bytes).

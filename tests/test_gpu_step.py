@@ -102,6 +102,34 @@ def test_step_matches_oracle(hq, hkv, seq0, cap):
     _check_new_records(cache, ora, seq0, cap, "step")
 
 
+@pytest.mark.timeout(300)
+def test_step_many_sequences_stale_workspace():
+    """A grid of several rounds whose merge has far more workgroups than the
+    chip holds at once (384 sequences x 16 query heads = 6144), with lengths
+    at exact multiples of the split length (512 here: one position more would
+    add a live split) and empty sequences, on a workspace filled with stale
+    partials (scores far above any real one).  The merge must count each
+    sequence's live splits from the length the step began with, although its
+    workgroup of head 0 advances seq_lens[b] during the same launch; a stale
+    partial read would dominate the output."""
+    cap, n = 2048, 384
+    seq0 = [(0, 512, 1024, 1536)[i % 4] if i % 3 else (131 * i) % 2047 for i in range(n)]
+    w = synth.Workload(8, "step stale", n, 16, 2, cap, "f16", rotation_seed=12)
+    cache, quats, k_new, v_new, ora = _setup(w, 6, seq0, cap)
+    q = synth.queries(6, w)[0]
+    ws = api.alloc_workspace(n, 16, 2, cap, DEV)
+    ws.fill_(0x44)   # every partial m = l = o = 785.07 (0x44444444)
+    out = _step(cache, _dev(quats), _dev(q), _dev(k_new), _dev(v_new), cap, ws=ws)
+    torch.cuda.synchronize()
+    seq1 = [x + 1 for x in seq0]
+    assert cache["seq_lens"].cpu().numpy().tolist() == seq1
+    _check_new_records(cache, ora, seq0, cap, "stale ws")
+    # the decode on the device's own records (the new token's included)
+    dev_cache = [cache[nm].cpu().numpy() for nm in ("k_codes", "k_norms", "v_codes", "v_norms")]
+    ref = oatt.decode_fused(q, *dev_cache, seq1, quats, LEVELS)
+    check_attention(out.cpu().numpy(), ref, "stale ws")
+
+
 def test_step_f32_inputs_and_custom_scale():
     w = synth.Workload(0, "step32", 2, 16, 2, 777, "f32", rotation_seed=3)
     seq0, cap = [776, 100], 784
