@@ -69,7 +69,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--workload", choices=("step32k", "varlen", "compress", "append8k",
                                           "baseline32k", "rotation_fit", "paged", "bits32k",
-                                          "multi32k", "tiny1k"),
+                                          "multi32k", "tiny1k", "shard"),
                    default="step32k")
     p.add_argument("--steps", type=int, default=None,
                    help="timed steps (default: 4800; varlen 240; compress 20; append8k 1000)")
@@ -93,7 +93,7 @@ def parse():
     defaults = {"step32k": (4800, 48), "varlen": (240, 3), "compress": (20, 1),
                 "append8k": (1000, 48), "baseline32k": (960, 48),
                 "rotation_fit": (1, 1), "paged": (240, 3), "bits32k": (960, 48),
-                "multi32k": (960, 48), "tiny1k": (960, 48)}[a.workload]
+                "multi32k": (960, 48), "tiny1k": (960, 48), "shard": (4800, 0)}[a.workload]
     if a.steps is None:
         a.steps = defaults[0]
     if a.warmup is None:
@@ -522,6 +522,58 @@ def run_step32k(args, torch, api, synth, dev):
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.context, args.cpu_seconds)
     return result
+
+
+def run_shard(args, torch, api, synth, dev):
+    """The 32K step at one GPU's share of it: by KV heads (tensor parallel over
+    2 and 4 GPUs: 2 or 1 KV heads with their 8 query heads each) and by
+    positions (context parallel over 2, 4 and 8 GPUs: 16K, 8K and 4K of the
+    positions, all heads).  Each share cycles enough layer caches to span
+    twice the 256 MB cache on the memory side (so every step reads cold
+    data); value = the full step's share measured on this GPU."""
+    import dataclasses
+
+    w2 = synth.WORKLOADS[2]
+    shares = [("whole step", 4, 32768), ("TP=2", 2, 32768), ("TP=4", 1, 32768),
+              ("CP=2", 4, 16384), ("CP=4", 4, 8192), ("CP=8", 4, 4096)]
+    rows = []
+    for name, hkv, ctx in shares:
+        w = dataclasses.replace(w2, n_kv_heads=hkv, n_q_heads=8 * hkv)
+        layer_bytes = hkv * ctx * BYTES_PER_TOKEN_HEAD
+        nl = args.layers if args.layers else max(48, -(-(512 << 20) // layer_bytes))
+        capacity = cache_capacity(ctx, args.warmup, args.steps, nl)
+        print(f"# {name}: {nl} layer caches, {hkv} KV heads, {ctx} positions", file=sys.stderr,
+              flush=True)
+        quats, layers = make_layers(api, synth, w, nl, ctx, capacity, args.seed, dev)
+        ws = api.alloc_workspace(w.batch, w.n_q_heads, w.n_kv_heads, capacity, dev)
+        us, dec, wall = time_steps(api, layers, quats, ws, capacity, args)
+        r = step_result(METRIC, name, w, layers, nl, us, dec, wall, args, "")
+        rows.append({"share": name, "n_kv_heads": hkv, "n_q_heads": 8 * hkv, "context": ctx,
+                     "layers_cycled": nl, "us_per_step": r["us_per_step"],
+                     "decode_us": r["decode_us"], "GB/s": r["value"],
+                     "frac": r["roofline"]["frac"]})
+        del layers, ws
+        torch.cuda.empty_cache()
+    whole = rows[0]
+    return {
+        "metric": "32K decode step at one GPU's share (µs/step)",
+        "value": rows[2]["us_per_step"],
+        "unit": "µs/step (TP=4 share)",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "higher_is_better": False,
+        "scaling": "strong",
+        "vs_baseline": None,
+        "dtype": "u3 codes, f32 accumulate",
+        "data": "synthetic (seeded anisotropic fp16 K/V, compressed on device)",
+        "config": {"workload": "the 32K GQA fused step (batch 1, 32 query heads, 4 KV heads, "
+                               "32768 positions) at one GPU's share, one GPU",
+                   "shares": rows,
+                   "note": "a share's time plus the exchange of partials (context parallel) is "
+                           "the sharded step; the exchange is not measured here; "
+                           f"whole step {whole['us_per_step']} us"},
+    }
 
 
 def run_varlen(args, torch, api, synth, dev):
@@ -1159,6 +1211,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     run = {"step32k": run_step32k, "varlen": run_varlen, "compress": run_compress,
+           "shard": run_shard,
            "append8k": run_append8k, "baseline32k": run_baseline32k,
            "rotation_fit": run_rotation_fit, "paged": run_paged,
            "bits32k": run_bits32k, "multi32k": run_multi32k, "tiny1k": run_tiny1k}[args.workload]
