@@ -1084,17 +1084,29 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
   if (n_parts > 1) {
     const dim3 mgrid(static_cast<unsigned>(n_kv_heads * group), static_cast<unsigned>(batch));
     // grids of several rounds leave the splits past each length unwritten:
-    // their merge reads the live ones only
-#define IQ_LAUNCH_MERGE_L(APP_, ANY_, LIVE_)                                                   \
-  hipLaunchKernelGGL((merge_g8_kernel<APP_, 1, ANY_, LIVE_>), mgrid, dim3(kMergeThreads), 0,    \
+    // their merge reads the live ones only.  Rows of more than 64 partials
+    // (one sequence's long context over few KV heads) are read in passes of
+    // 128 or 256 partials by variants that hold them all in registers (fewer
+    // waves per SIMD: for merge grids of at most 256 workgroups)
+    const bool wide_pass = n_parts > 64 && n_kv_heads * group * batch <= kCus;
+#define IQ_LAUNCH_MERGE_U(APP_, ANY_, LIVE_, U_)                                               \
+  hipLaunchKernelGGL((merge_g8_kernel<APP_, 1, ANY_, LIVE_, U_>), mgrid, dim3(kMergeThreads), 0, \
                      stream, partials, quats, out, static_cast<int>(n_kv_heads),                \
                      static_cast<int>(n_parts), seq_lens, capacity, static_cast<int>(group),    \
                      static_cast<int>(split_len), static_cast<int>(max_seq_len), lens0)
+#define IQ_LAUNCH_MERGE_L(APP_, ANY_, LIVE_)        \
+  if (wide_pass && n_parts > 128) {                 \
+    IQ_LAUNCH_MERGE_U(APP_, ANY_, LIVE_, 32);       \
+  } else if (wide_pass) {                           \
+    IQ_LAUNCH_MERGE_U(APP_, ANY_, LIVE_, 16);       \
+  } else {                                          \
+    IQ_LAUNCH_MERGE_U(APP_, ANY_, LIVE_, 8);        \
+  }
 #define IQ_LAUNCH_MERGE(APP_, ANY_)        \
   if (wide) {                              \
-    IQ_LAUNCH_MERGE_L(APP_, ANY_, true);   \
+    IQ_LAUNCH_MERGE_L(APP_, ANY_, true)    \
   } else {                                 \
-    IQ_LAUNCH_MERGE_L(APP_, ANY_, false);  \
+    IQ_LAUNCH_MERGE_L(APP_, ANY_, false)   \
   }
     if (append && any_group) {
       IQ_LAUNCH_MERGE(true, true)
@@ -1107,6 +1119,7 @@ hipError_t launch_decode_g8(int nb, int64_t n_splits, int64_t split_len, const f
     }
 #undef IQ_LAUNCH_MERGE
 #undef IQ_LAUNCH_MERGE_L
+#undef IQ_LAUNCH_MERGE_U
     e = hipGetLastError();
   }
   return e;

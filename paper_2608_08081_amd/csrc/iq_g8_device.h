@@ -439,8 +439,8 @@ __device__ __forceinline__ void value_pairs(const uint32_t* lut, const uint32_t*
 
 // Merge of the split partials of one (sequence b, query head h): grid
 // (query head, sequence), one 256-thread workgroup each; thread (sg, dq)
-// takes partials sg, sg + 8, ... and dims 4 dq .. 4 dq + 3, with up to 8
-// partials' loads in flight per thread.  Then o = sum_s c_s O_s / sum_s c_s
+// takes partials sg, sg + 8, ... and dims 4 dq .. 4 dq + 3, with up to
+// kUnroll partials' loads in flight per thread.  Then o = sum_s c_s O_s / sum_s c_s
 // l_s with c_s = 2^(m_s - max m), and the single inverse rotation.  Splits
 // with nothing to attend carry m = -inf (their other entries are never read),
 // so the merge needs no sequence length.  kAppend: the last of the n_parts
@@ -463,13 +463,15 @@ __device__ __forceinline__ void value_pairs(const uint32_t* lut, const uint32_t*
 // the new-token partial; the others were never written.  With kAppend the
 // length is lens0[b], the one the decode kernel saw (seq_lens[b] may already
 // be advanced by this launch's workgroup of head 0).
-template <bool kAppend, int kTok = 1, bool kAnyGroup = false, bool kLive = false>
+template <bool kAppend, int kTok = 1, bool kAnyGroup = false, bool kLive = false,
+          int kUnroll = 8>
 __global__ __launch_bounds__(kMergeThreads) void merge_g8_kernel(
     const float* __restrict__ partials, const float* __restrict__ quats, float* __restrict__ out,
     int n_kv_heads, int n_parts, int32_t* __restrict__ seq_lens, int64_t capacity, int group,
     int split_len = 0, int max_seq_len = 0, const int32_t* __restrict__ lens0 = nullptr) {
   static_assert(kTok == 1 || !kLive, "multi-token partials are read in full");
-  constexpr int kUnroll = 8;   // 8 x 8 = 64 splits per pass, all loads in flight
+  // 8 x kUnroll splits per pass, all of a pass's loads in flight (rows of
+  // more than 64 partials take passes of 256)
   __shared__ __attribute__((aligned(16))) float red_o[8][kDim];
   __shared__ float red_m[8], red_l[8];
   const int tid = threadIdx.x;

@@ -63,6 +63,25 @@ def test_decode_parity_on_oracle_cache(hq, hkv, seq):
             assert np.all(got[b] == 0)
 
 
+@pytest.mark.parametrize("hkv,ctx", [(1, 32768), (2, 20000)])
+def test_many_splits_per_row(hkv, ctx):
+    """One sequence over one or two KV heads: the planner fills the chip with
+    short splits (229 of 144 positions at 32K over one KV head), so each row
+    has more than 64 partials, which the merge reads in one wide pass."""
+    from tests.test_gpu_bench_shapes import g8_instance
+
+    assert g8_instance(1, hkv, ctx, append=False)[1] > 64
+    w = synth.Workload(9, "many splits", 1, 8 * hkv, hkv, ctx, "f16", rotation_seed=91)
+    k, v, quats, kp, kn, vp, vn = _oracle_cache(w, 3, ctx, 1, ctx)
+    q = synth.queries(3, w)[0]
+    got = _gpu_decode(q, kp, kn, vp, vn, [ctx], quats, ctx)
+    ref = oatt.decode_fused(q, kp, kn, vp, vn, [ctx], quats, LEVELS)
+    check_attention(got, ref, f"many splits hkv{hkv} T{ctx}")
+    got2 = _gpu_decode(q, kp, kn, vp, vn, [ctx - 1000], quats, ctx)
+    ref2 = oatt.decode_fused(q, kp, kn, vp, vn, [ctx - 1000], quats, LEVELS)
+    check_attention(got2, ref2, f"many splits hkv{hkv} T{ctx - 1000}")
+
+
 def test_decode_custom_scale_and_determinism():
     w = synth.WORKLOADS[1]
     t = 2000

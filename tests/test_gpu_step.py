@@ -80,6 +80,7 @@ def _check_new_records(cache, ora, seq0, cap, label):
     (8, 1, [4095], 4096),
     (8, 1, [4096], 4112),
     (8, 1, [4096], 4100),       # capacity not a multiple of 16: generic path
+    (8, 1, [30000], 32768),     # one KV head: more than 64 partials per row
     # a grid of several rounds (64 sequences x 2 KV heads x 4 partials): the
     # instance that reads the length before its loads and skips empty splits
     (16, 2, [0, 1, 15, 16, 17, 31, 32, 33, 63, 64, 65, 127, 128, 129, 223, 224, 225, 447,
