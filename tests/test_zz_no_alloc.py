@@ -2,8 +2,9 @@
 static device scratch) against iq_decode_step with a caller workspace, on
 twin caches: identical outputs, records and lengths.  Two calls in a row on
 one GPU, the second on a smaller input (the scratch keeps the first call's
-contents), then a group size that takes the generic path, then a shape
-whose workspace exceeds the scratch (rejected on the host)."""
+contents), then a group size that takes the generic path, a grid of several
+rounds, and a shape whose workspace exceeds the scratch (rejected on the
+host)."""
 
 import numpy as np
 import pytest
@@ -57,6 +58,19 @@ def test_noalloc_step_equals_workspace_step_twice():
     # group 4 (generic path: append kernel, split kernel, combine kernel)
     w3 = synth.Workload(9, "noalloc_g4", 2, 16, 4, 700, "f16", rotation_seed=1009)
     _compare(w3, [699, 5], 704, 5, "group 4")
+
+
+def test_noalloc_grid_of_several_rounds():
+    """A fused step whose grid takes several rounds (24 sequences x 2 KV heads
+    x 10 partials), with lengths at multiples of the split length (352) and an
+    empty sequence: the merge counts each sequence's live splits from the
+    lengths the step records in the scratch after the partials."""
+    from tests.test_gpu_bench_shapes import g8_instance
+
+    w = synth.Workload(10, "noalloc_wide", 24, 16, 2, 3072, "f16", rotation_seed=1010)
+    assert g8_instance(w.batch, w.n_kv_heads, 3072)[2]
+    lens = [0, 352, 704, 3071] + [(131 * i) % 3000 for i in range(20)]
+    _compare(w, lens, 3072, 6, "grid of several rounds")
 
 
 def test_noalloc_rejects_shapes_beyond_the_scratch():
